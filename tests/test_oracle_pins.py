@@ -1,0 +1,485 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: a closed
+form, exact rational arithmetic, brute force, an independent per-event
+reading of Eq. 1-2, a library routine (torch on the CPU, float64), finite
+differences, or an invariant the paper states.
+"""
+
+import json
+import math
+import os
+import struct
+from dataclasses import replace
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import sequential, tgn
+from oracle.bf16 import round_bf16
+from synth import init_params, workload
+from tests._tiny import random_state, tiny_stream, tiny_workload
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+F32 = np.float32
+
+
+def _to_f32(fr: Fraction) -> float:
+    """Round an exact rational to the nearest binary32 (ties to even) by bisection on the bit pattern."""
+    x = float(fr)                       # nearest double (ties-to-even)
+    f = struct.unpack("<f", struct.pack("<f", x))[0]   # double -> single, nearest-even
+    # correct a possible double-rounding error by checking the neighbours exactly
+    best, best_err = f, abs(Fraction(f) - fr)
+    for cand in (np.nextafter(F32(f), F32(np.inf)), np.nextafter(F32(f), F32(-np.inf))):
+        err = abs(Fraction(float(cand)) - fr)
+        if err < best_err or (err == best_err and (struct.unpack("<I", struct.pack("<f", float(cand)))[0] & 1) == 0):
+            best, best_err = float(cand), err
+    return best
+
+
+# --------------------------------------------------------------------------- time encoding
+
+def test_time_encoding_special_cases():
+    p64 = tgn.Prec("f64")
+    w = np.array([1.0, 0.5, 0.0, 1e-3], F32)
+    b = np.array([0.0, 0.25, 0.0, -1.0], F32)
+    # dt = 0 -> cos(b); w = b = 0 -> 1
+    phi0 = tgn.time_encode(p64, np.zeros(1), w, b)[0]
+    assert np.allclose(phi0, np.cos(b.astype(np.float64)), rtol=0, atol=0)
+    assert phi0[2] == 1.0
+    # evenness for b = 0 and 2*pi/w periodicity
+    dt = np.array([0.3, 2.0, 7.5])
+    wz = np.array([1.0, 2.0], F32)
+    bz = np.zeros(2, F32)
+    assert np.allclose(tgn.time_encode(p64, dt, wz, bz), tgn.time_encode(p64, -dt, wz, bz), atol=1e-15)
+    per = 2 * math.pi / wz.astype(np.float64)
+    shifted = np.stack([tgn.time_encode(p64, dt + per[j], wz[j:j + 1], bz[j:j + 1])[:, 0] for j in range(2)], 1)
+    assert np.allclose(shifted, tgn.time_encode(p64, dt, wz, bz), atol=1e-12)
+    # a known value: w dt + b = pi -> -1
+    assert abs(tgn.time_encode(p64, np.array([math.pi]), np.array([1.0]), np.array([0.0]))[0, 0] + 1) < 1e-15
+
+
+def test_time_argument_rounding_is_two_fp32_roundings():
+    """The float32 cosine argument is round(round(w*dt) + b): two separate roundings, no fused multiply-add."""
+    rng = np.random.default_rng(3)
+    p32 = tgn.Prec("f32")
+    dts = np.concatenate([rng.random(200) * 1e5, rng.random(50) * 2.4e6, [0.0, 1e-3, 99999.99]]).astype(F32)
+    w = np.array([1.0, 0.7, 3.3e-5, 1e-9], F32)
+    b = np.array([0.0, 0.3, -1.7, 2.5], F32)
+    got = p32.time_arg(dts, w, b)
+    for i, d in enumerate(dts):
+        for j in range(w.size):
+            prod = _to_f32(Fraction(float(w[j])) * Fraction(float(d)))
+            ref = _to_f32(Fraction(prod) + Fraction(float(b[j])))
+            assert got[i, j] == F32(ref), (d, w[j], b[j])
+    # the fused form differs for some inputs: the rounding rule is observable
+    fused = np.array([[_to_f32(Fraction(float(w[1])) * Fraction(float(d)) + Fraction(float(b[1])))
+                       for d in dts]]).T
+    two = p32.time_arg(dts, w[1:2], b[1:2])
+    assert (fused.astype(F32) != two).any()
+    # cosine of the rounded argument, in float64
+    phi = tgn.time_encode(p32, dts[:5], w, b)
+    for i in range(5):
+        for j in range(w.size):
+            assert phi[i, j] == math.cos(float(got[i, j]))
+
+
+# --------------------------------------------------------------------------- selection (most recent message)
+
+def _select_bruteforce(src, dst, t, eid, flags):
+    best = {}
+    for i in range(len(src)):
+        if flags is not None and flags[i] & 2:
+            continue
+        for role, node in ((0, int(src[i])), (1, int(dst[i]))):
+            key = (F32(t[i]), int(eid[i]), role)
+            if node not in best or key > best[node][0]:
+                best[node] = (key, 2 * i + role)
+    nodes = sorted(best)
+    return np.array(nodes, np.int64), np.array([best[n][1] for n in nodes], np.int64)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_select_last_matches_bruteforce(seed):
+    w = tiny_workload(n_nodes=7, n_events=60)
+    s = tiny_stream(w, seed=seed, tie_every=3, flags_p=(0.3, 0.4) if seed % 2 else None)
+    eid = np.arange(len(s.src)) + 1000
+    u, win = tgn.select_last(s.src, s.dst, s.t, eid, s.flags)
+    u2, win2 = _select_bruteforce(s.src, s.dst, s.t, eid, s.flags)
+    assert np.array_equal(u, u2) and np.array_equal(win, win2)
+    # invariants: each non-pruned endpoint once; the winner carries the node's latest time
+    act = tgn.active_mask(s.flags, len(s.src))
+    ends = set(s.src[act].tolist()) | set(s.dst[act].tolist())
+    assert sorted(ends) == u.tolist()
+    for n, wv in zip(u, win):
+        i, role = wv // 2, wv % 2
+        assert (s.src[i] if role == 0 else s.dst[i]) == n
+        times = [s.t[j] for j in range(len(s.src)) if act[j] and n in (s.src[j], s.dst[j])]
+        assert s.t[i] == max(times)
+
+
+def test_select_last_self_loop_dst_role_wins():
+    u, win = tgn.select_last([3], [3], np.array([1.0], F32), [0])
+    assert u.tolist() == [3] and win.tolist() == [1]
+
+
+# --------------------------------------------------------------------------- GRU
+
+def test_gru_matches_hand_expansion_two_nodes():
+    rng = np.random.default_rng(5)
+    dm, D = 3, 7
+    W_ih = rng.normal(size=(3 * dm, D))
+    W_hh = rng.normal(size=(3 * dm, dm))
+    b_ih, b_hh = rng.normal(size=3 * dm), rng.normal(size=3 * dm)
+    x = rng.normal(size=(2, D))
+    h = rng.normal(size=(2, dm))
+    got, _ = tgn.gru_cell(x, h, W_ih, W_hh, b_ih, b_hh)
+    for r in range(2):
+        ref = sequential.gru_scalar(x[r], h[r], W_ih, W_hh, b_ih, b_hh)
+        assert np.allclose(got[r], ref, rtol=0, atol=1e-14)
+
+
+def test_gru_matches_torch_grucell_float64():
+    rng = np.random.default_rng(6)
+    dm, D, R = 5, 11, 9
+    cell = torch.nn.GRUCell(D, dm).double()
+    with torch.no_grad():
+        for prm in cell.parameters():
+            prm.copy_(torch.from_numpy(rng.normal(size=tuple(prm.shape))))
+    x = rng.normal(size=(R, D))
+    h = rng.normal(size=(R, dm))
+    got, _ = tgn.gru_cell(x, h, cell.weight_ih.detach().numpy(), cell.weight_hh.detach().numpy(),
+                          cell.bias_ih.detach().numpy(), cell.bias_hh.detach().numpy())
+    ref = cell(torch.from_numpy(x), torch.from_numpy(h)).detach().numpy()
+    assert np.allclose(got, ref, rtol=0, atol=1e-13)
+
+
+# --------------------------------------------------------------------------- memory phase semantics
+
+def _run_batches(prec, w, s, mem, lu, params, B):
+    for lo in range(0, len(s.src), B):
+        hi = min(len(s.src), lo + B)
+        mp = tgn.memory_phase(prec, w, tgn.batch_dict(s, lo, hi), mem, lu, s.x, params)
+        mem, lu = mp.mem, mp.lu
+    return mem, lu
+
+
+def test_batch_of_one_equals_sequential_events():
+    """Batch size 1 reproduces the per-event reading of Eq. 1-2 over 2,000 events of the tiny workload."""
+    w = replace(workload(1), n_events=2000)
+    s = tiny_stream(w, seed=11, t_scale=1e3, tie_every=7)
+    params = init_params(w, random_bias=True)
+    mem0, lu0 = random_state(w, seed=2)
+    p64 = tgn.Prec("f64")
+    mem_b, lu_b = _run_batches(p64, w, s, mem0.astype(np.float64), lu0.astype(np.float64), params, 1)
+    mem_s, lu_s = sequential.replay_events(s.src, s.dst, s.t, s.x, None, mem0, lu0, params)
+    assert np.array_equal(lu_b, lu_s)
+    assert np.max(np.abs(mem_b - mem_s)) < 1e-12
+
+
+def test_disjoint_batch_equals_sequential_events():
+    """When no two events of a batch share a node, the batch step equals the event-by-event step."""
+    w = tiny_workload(n_nodes=40, n_events=8, d_mem=6, d_time=5, d_edge=3)
+    rng = np.random.default_rng(9)
+    nodes = rng.permutation(40)[:16]
+    s = tiny_stream(w, seed=1)
+    s.src[:] = nodes[:8]
+    s.dst[:] = nodes[8:]
+    params = init_params(w, random_bias=True)
+    mem0, lu0 = random_state(w, seed=4)
+    p64 = tgn.Prec("f64")
+    mem_b, lu_b = _run_batches(p64, w, s, mem0.astype(np.float64), lu0.astype(np.float64), params, 8)
+    mem_s, lu_s = sequential.replay_events(s.src, s.dst, s.t, s.x, None, mem0, lu0, params)
+    assert np.array_equal(lu_b, lu_s)
+    assert np.max(np.abs(mem_b - mem_s)) < 1e-13
+
+
+def test_batch_uses_pre_batch_snapshot_and_last_message():
+    """Inside a batch every message reads the pre-batch state; a node keeps only its latest message."""
+    w = tiny_workload(n_nodes=5, n_events=3, d_edge=0)
+    s = tiny_stream(w, seed=2)
+    s.src[:] = [0, 0, 2]
+    s.dst[:] = [1, 2, 3]
+    s.t[:] = np.array([1.0, 2.0, 3.0], F32)
+    params = init_params(w, random_bias=True)
+    mem0, lu0 = random_state(w, seed=6)
+    p64 = tgn.Prec("f64")
+    mp = tgn.memory_phase(p64, w, tgn.batch_dict(s, 0, 3), mem0.astype(np.float64), lu0.astype(np.float64),
+                          None, params)
+    # node 0: last message is event 1 (role 0) with partner 2, both read before the batch
+    assert mp.uniq.tolist() == [0, 1, 2, 3]
+    assert mp.winner.tolist() == [2, 1, 4, 5]
+    one = sequential.replay_events(np.array([0]), np.array([2]), np.array([2.0]), None, None, mem0, lu0, params)
+    assert np.max(np.abs(mp.mem[0] - one[0][0])) < 1e-13
+
+
+def test_untouched_rows_bit_identical_and_last_update():
+    w = workload(1)
+    s = tiny_stream(replace(w, n_events=400), seed=3, t_scale=1e5)
+    params = init_params(w)
+    mem0, lu0 = random_state(w, seed=8)
+    p32 = tgn.Prec("f32")
+    mp = tgn.memory_phase(p32, w, tgn.batch_dict(s, 0, 200), mem0, lu0, s.x, params)
+    touched = np.zeros(w.n_nodes, bool)
+    touched[mp.uniq] = True
+    assert mp.mem.dtype == np.float32
+    assert np.array_equal(mp.mem[~touched].view(np.uint32), mem0[~touched].view(np.uint32))
+    assert np.array_equal(mp.lu[~touched].view(np.uint32), lu0[~touched].view(np.uint32))
+    # last_update of a touched node is its latest event time in the batch
+    for n in mp.uniq[:50]:
+        ev = [i for i in range(200) if n in (s.src[i], s.dst[i])]
+        assert mp.lu[n] == s.t[max(ev)]
+
+
+# --------------------------------------------------------------------------- sampling
+
+@pytest.mark.parametrize("seed", range(5))
+def test_sampling_matches_bruteforce(seed):
+    w = tiny_workload(n_nodes=6, n_events=70)
+    s = tiny_stream(w, seed=seed, tie_every=4)
+    adj = tgn.build_adjacency(s.src, s.dst, s.t, w.n_nodes)
+    rng = np.random.default_rng(seed)
+    q_node = rng.integers(0, w.n_nodes, 40)
+    q_t = np.concatenate([rng.random(30) * 11, s.t[rng.integers(0, 70, 10)]]).astype(F32)
+    for k in (1, 3, 8, 40):
+        got = tgn.sample_recent(adj, q_node, q_t, k)
+        ref = tgn.sample_recent_bruteforce(s.src, s.dst, s.t, q_node, q_t, k)
+        for a, b in zip(got, ref):
+            assert np.array_equal(a, b)
+        nbr, nt, neid = got
+        for qi in range(len(q_node)):
+            valid = nbr[qi] >= 0
+            m = int(valid.sum())
+            assert valid[:m].all() and not valid[m:].any()          # padding only at the tail
+            assert (nt[qi, :m] < q_t[qi]).all()                       # strictly earlier
+            assert (np.diff(nt[qi, :m]) <= 0).all()                   # newest first
+            n_elig = sum(int(s.t[e] < q_t[qi]) * (int(s.src[e] == q_node[qi]) + int(s.dst[e] == q_node[qi]))
+                         for e in range(len(s.src)))
+            assert m == min(k, n_elig)
+            assert (neid[qi, m:] == -1).all() and (nt[qi, m:] == 0).all()
+
+
+def test_adjacency_self_loop_twice_and_sorted():
+    w = tiny_workload(n_nodes=3, n_events=4)
+    s = tiny_stream(w, seed=0)
+    s.src[:] = [0, 1, 2, 2]
+    s.dst[:] = [1, 1, 0, 2]
+    adj = tgn.build_adjacency(s.src, s.dst, s.t, 3)
+    seg = slice(adj.off[1], adj.off[2])
+    assert adj.nbr[seg].tolist() == [0, 1, 1] and adj.eid[seg].tolist() == [0, 1, 1]
+    seg2 = slice(adj.off[2], adj.off[3])
+    assert adj.eid[seg2].tolist() == [2, 3, 3]
+
+
+# --------------------------------------------------------------------------- attention
+
+def _attn_inputs(seed=0, H=2, k=4, Q=5, dm=6, dt=3, de=2, da=8, n_valid=None):
+    w = tiny_workload(n_nodes=9, d_mem=dm, d_time=dt, d_edge=de, d_attn=da, n_heads=H, k=k, n_events=30)
+    s = tiny_stream(w, seed=seed)
+    params = init_params(w, random_bias=True)
+    rng = np.random.default_rng(seed)
+    mem = rng.uniform(-1, 1, (w.n_nodes, dm))
+    q_node = rng.integers(0, w.n_nodes, Q)
+    q_t = (rng.random(Q) * 10 + 10).astype(F32)
+    nbr = rng.integers(0, w.n_nodes, (Q, k))
+    nt = (rng.random((Q, k)) * 10).astype(F32)
+    neid = rng.integers(0, 30, (Q, k))
+    if n_valid is not None:
+        for qi in range(Q):
+            nbr[qi, n_valid[qi]:] = -1
+            nt[qi, n_valid[qi]:] = 0
+            neid[qi, n_valid[qi]:] = -1
+    return w, s, params, mem, q_node, q_t, nbr, nt, neid
+
+
+def test_attention_core_matches_torch_sdpa():
+    w, s, params, mem, q_node, q_t, nbr, nt, neid = _attn_inputs(n_valid=[4, 1, 2, 3, 4])
+    p64 = tgn.Prec("f64")
+    sv = tgn.attention_fwd(p64, w, mem, s.x, params, q_node, q_t, nbr, nt, neid)
+    Q, k, H, dh = 5, 4, w.n_heads, w.d_attn // w.n_heads
+    q = torch.from_numpy(sv.q.reshape(Q, 1, H, dh).transpose(0, 2, 1, 3).copy())
+    K = torch.from_numpy(sv.K.reshape(Q, k, H, dh).transpose(0, 2, 1, 3).copy())
+    V = torch.from_numpy(sv.V.reshape(Q, k, H, dh).transpose(0, 2, 1, 3).copy())
+    mask = torch.from_numpy(sv.valid[:, None, None, :])
+    ref = torch.nn.functional.scaled_dot_product_attention(q, K, V, attn_mask=mask)
+    ref = ref.transpose(1, 2).reshape(Q, -1).numpy()
+    assert np.allclose(sv.attn, ref, rtol=0, atol=1e-13)
+
+
+def test_attention_single_neighbour_and_empty():
+    w, s, params, mem, q_node, q_t, nbr, nt, neid = _attn_inputs(n_valid=[1, 0, 1, 0, 1])
+    sv = tgn.attention_fwd(tgn.Prec("f64"), w, mem, s.x, params, q_node, q_t, nbr, nt, neid)
+    for qi in (0, 2, 4):   # one valid slot: softmax weight 1, output = V of that slot
+        assert np.allclose(sv.attn[qi], sv.V[qi, 0], rtol=0, atol=1e-14)
+    for qi in (1, 3):      # no valid slot: attention output 0, o = b_o
+        assert np.all(sv.attn[qi] == 0)
+        assert np.allclose(sv.o[qi], params["b_o"], rtol=0, atol=0)
+
+
+def test_attention_permutation_invariant_over_slots():
+    w, s, params, mem, q_node, q_t, nbr, nt, neid = _attn_inputs(n_valid=[4, 2, 3, 4, 1])
+    p64 = tgn.Prec("f64")
+    a = tgn.attention_fwd(p64, w, mem, s.x, params, q_node, q_t, nbr, nt, neid)
+    perm = np.array([2, 0, 3, 1])
+    b = tgn.attention_fwd(p64, w, mem, s.x, params, q_node, q_t, nbr[:, perm], nt[:, perm], neid[:, perm])
+    assert np.allclose(a.z, b.z, rtol=0, atol=1e-13)
+
+
+# --------------------------------------------------------------------------- backward (finite differences)
+
+def _fd_setup(seed=0):
+    w = tiny_workload(n_nodes=6, n_events=24, batch=8, k=3, d_mem=4, d_time=3, d_edge=2, d_attn=4, n_heads=2)
+    s = tiny_stream(w, seed=seed, t_scale=6.0, tie_every=5)
+    params = {k: v.astype(np.float64) for k, v in init_params(w, random_bias=True).items()}
+    rng = np.random.default_rng(seed + 10)
+    params["time_w"] = rng.uniform(0.2, 1.5, w.d_time)
+    mem0 = rng.uniform(-1, 1, (w.n_nodes, w.d_mem))
+    lu0 = np.zeros(w.n_nodes)
+    adj = tgn.build_adjacency(s.src, s.dst, s.t, w.n_nodes)
+    prev = tgn.batch_dict(s, 8, 16)
+    cur = tgn.batch_dict(s, 16, 24)
+    noise = rng.standard_normal((24, w.d_attn))
+    return w, s, params, mem0, lu0, adj, prev, cur, noise
+
+
+def test_backward_matches_central_differences():
+    w, s, params, mem0, lu0, adj, prev, cur, noise = _fd_setup()
+    p64 = tgn.Prec("f64")
+    res = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, cur, noise)
+    assert len(res.mp.uniq) > 0 and np.abs(res.d_mem).max() > 0   # the GRU path is exercised
+
+    def loss(pp):
+        r = tgn.step(p64, w, mem0, lu0, pp, adj, s.x, prev, cur, noise)
+        return float(np.sum(r.dz * r.attn.z))
+
+    h = 1e-6
+    for name, g in res.grads.items():
+        base = params[name]
+        fd = np.zeros(base.size)
+        for i in range(base.size):
+            pp = dict(params)
+            for sgn in (1, -1):
+                arr = base.copy().reshape(-1)
+                arr[i] += sgn * h
+                pp[name] = arr.reshape(base.shape)
+                fd[i] += sgn * loss(pp)
+        fd /= 2 * h
+        scale = max(np.abs(fd).max(), 1e-3)      # FD noise is ~1e-10 here
+        err = np.abs(fd - np.asarray(g).reshape(-1)).max() / scale
+        assert err < 1e-6, (name, err)
+    # adding the same vector to every key shifts all scores of a head equally: d b_k = 0
+    assert np.abs(res.grads["b_k"]).max() < 1e-12
+
+
+def test_memory_grad_counts_query_and_neighbour_occurrences():
+    uniq = np.array([2, 5])
+    q_node = np.array([5, 1, 2, 5])
+    nbr = np.array([[2, -1], [5, 2], [0, 0], [-1, -1]])
+    dhq = np.arange(8, dtype=float).reshape(4, 2)
+    dhn = np.arange(16, dtype=float).reshape(4, 2, 2) * 10
+    out = tgn.memory_grad(uniq, q_node, nbr, dhq, dhn)
+    exp2 = dhq[2] + dhn[0, 0] + dhn[1, 1]
+    exp5 = dhq[0] + dhq[3] + dhn[1, 0]
+    assert np.array_equal(out, np.stack([exp2, exp5]))
+
+
+# --------------------------------------------------------------------------- masks (Def. 2, Eq. 10-13)
+
+def test_masks_replay_only_all_pruned_and_no_target():
+    w, s, params, mem0, lu0, adj, prev, cur, noise = _fd_setup(seed=3)
+    p64 = tgn.Prec("f64")
+    # replay-only embedding batch: no query, no loss, memory phase unchanged
+    cur_r = dict(cur, flags=np.ones(8, np.uint8))
+    r = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, cur_r, noise)
+    assert r.q_node.size == 0 and r.n_tar == 0
+    assert all(np.all(np.asarray(g) == 0) for g in r.grads.values())
+    # replay events still advance memory
+    prev_r = dict(prev, flags=np.ones(8, np.uint8))
+    r2 = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev_r, cur, noise)
+    assert len(r2.mp.uniq) > 0 and not np.array_equal(r2.mp.mem, mem0)
+    # all-pruned memory batch: state unchanged bit for bit
+    prev_p = dict(prev, flags=np.full(8, 3, np.uint8))
+    r3 = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev_p, cur, noise)
+    assert len(r3.mp.uniq) == 0
+    assert np.array_equal(r3.mp.mem, mem0) and np.array_equal(r3.mp.lu, lu0)
+    # the masked loss normalises by the number of target events
+    cur_m = dict(cur, flags=np.array([0, 1, 0, 1, 1, 0, 3, 0], np.uint8))
+    r4 = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, cur_m, noise)
+    assert r4.n_tar == 4 and r4.q_node.size == 12
+    assert np.allclose(r4.dz, noise[:12] / 4)
+
+
+# --------------------------------------------------------------------------- bf16
+
+def test_round_bf16_matches_torch_cast():
+    rng = np.random.default_rng(0)
+    vals = np.concatenate([
+        rng.standard_normal(10000).astype(F32) * 10.0 ** rng.integers(-30, 30, 10000),
+        np.array([0.0, -0.0, np.inf, -np.inf, 1e-40, -3e-39, 3.4e38, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8], F32),
+    ]).astype(F32)
+    # exact ties: mantissa pattern ...8000 with even/odd kept bit
+    ties = (np.arange(1000, dtype=np.uint32) << 16 | 0x8000).view(F32) + 0
+    vals = np.concatenate([vals, ties.astype(F32), -ties.astype(F32)])
+    ref = torch.from_numpy(vals).to(torch.bfloat16).to(torch.float32).numpy()
+    got = round_bf16(vals)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    assert np.isnan(round_bf16(np.array([np.nan], F32))[0])
+
+
+def test_bf16_mode_close_to_f32_mode():
+    w = replace(workload(5), n_nodes=300, n_events=3000, batch=500, k=5)
+    s = tiny_stream(w, seed=4, t_scale=1e3, flags_p=(0.25, 0.1))
+    params = init_params(w, random_bias=True)
+    mem0, lu0 = random_state(w, seed=3)
+    adj = tgn.build_adjacency(s.src, s.dst, s.t, w.n_nodes)
+    prev, cur = tgn.batch_dict(s, 1000, 1500), tgn.batch_dict(s, 1500, 2000)
+    noise = np.random.default_rng(1).standard_normal((1500, w.d_attn))
+    r32 = tgn.step(tgn.Prec("f32"), w, mem0, lu0, params, adj, s.x, prev, cur, noise)
+    r16 = tgn.step(tgn.Prec("bf16"), w, round_bf16(mem0), lu0, params, adj, s.x, prev, cur, noise)
+
+    def rel(a, b):
+        return np.abs(np.asarray(a, float) - b).max() / max(np.abs(b).max(), 1e-30)
+
+    assert rel(r16.attn.z, r32.attn.z) < 2e-2
+    assert rel(r16.mp.h_new, r32.mp.h_new) < 2e-2
+    # gradients move more (ReLU masks flip near zero); d b_k is identically zero in both
+    for name in r32.grads:
+        if name != "b_k":
+            assert rel(r16.grads[name], r32.grads[name]) < 0.1, name
+    assert np.abs(r16.grads["b_k"]).max() < 1e-9 * np.abs(r16.grads["W_k"]).max()
+
+
+# --------------------------------------------------------------------------- the paper's worked example
+
+def test_example_dependency_chain():
+    """Example 2 (Section III-C): the state of node 3 before e8 = (4, 3, t8) depends on e7, e6, e3 and e1."""
+    with open(os.path.join(GOLDEN, "example2_dependency.json")) as f:
+        ex = json.load(f)
+    ev = ex["events"]
+    src = np.array([e[0] for e in ev])
+    dst = np.array([e[1] for e in ev])
+    t = np.arange(1, len(ev) + 1, dtype=F32)
+    w = tiny_workload(n_nodes=16, n_events=len(ev), d_edge=2)
+    params = init_params(w, random_bias=True)
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((len(ev), 2)).astype(F32)
+    mem0 = np.zeros((16, w.d_mem), F32)
+    lu0 = np.zeros(16, F32)
+    target = ex["target_event"] - 1
+    node = ex["node"]
+
+    def state_before_target(xx):
+        m, _ = sequential.replay_events(src[:target], dst[:target], t[:target], xx[:target], None, mem0, lu0, params)
+        return m[node]
+
+    base = state_before_target(x)
+    deps = []
+    for e in range(target):
+        xx = x.copy()
+        xx[e] += 1.0
+        if np.abs(state_before_target(xx) - base).max() > 0:
+            deps.append(e + 1)
+    assert set(ex["must_depend_on"]) <= set(deps)
+    assert not set(ex["must_not_depend_on"]) & set(deps)
