@@ -1,0 +1,278 @@
+/*
+ * mtgnn -- the single-GPU batch step of memory-based temporal GNN training
+ * (TGN-style memory + temporal attention) for AMD Instinct MI355X (gfx950).
+ *
+ * The paper this implements (DepTGL, arXiv 2608.16305) describes distributed
+ * training of memory-based TGNNs.  Each worker executes mixed batches of target
+ * events and replayed auxiliary events (Definition 2, Eq. 5), with load-aware
+ * pruning of replay events (Eq. 10-11) and a loss masked to target events
+ * (Eq. 12-13).  Inside a batch the model follows the chronological node-state
+ * semantics of Section III-A (Eq. 1-2).  This library is that per-worker
+ * hot path on one GPU.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument named as device data points to device memory owned
+ *   by the caller.  The library never allocates, frees or synchronises, except
+ *   where an entry point says so.  Each call only enqueues kernels on `stream`
+ *   and returns; results are ready when the stream reaches them.
+ * - Scratch memory is passed as (ws, ws_bytes).  The required size comes from
+ *   mtgnn_workspace_bytes(); a smaller workspace returns MTGNN_EWORKSPACE.
+ *   Workspace contents need not be initialised and are garbage afterwards.
+ *   Calls that run at the same time need separate workspaces.
+ * - Arguments are validated on the host before any HIP call:
+ *   - null required pointers, non-positive sizes or an inconsistent
+ *     mtgnn_dims give MTGNN_EINVAL;
+ *   - an unknown dtype gives MTGNN_EUNSUPPORTED;
+ *   - a failed kernel launch gives MTGNN_EHIP (the HIP message is kept for
+ *     mtgnn_last_error()).
+ *   Device-resident preconditions are documented per call and are not checked.
+ *   These are index ranges, the event order and finite timestamps.
+ * - Device-side counts (`n_rows`, `n_q`, ...) are single int32 values in device
+ *   memory written by an earlier call.  The host passes the matching maximum
+ *   (`max_rows`, `max_q`), which sizes the buffers and grids.  A NULL count
+ *   means the maximum is exact.
+ * - Matrices are row-major.  Weights use the [out, in] layout of a linear
+ *   layer, y = x W^T + b.  Weights and the memory table are stored in the
+ *   dims' dtype: float32, or bfloat16 bit patterns rounded to nearest even.
+ *   Biases, timestamps, the time encoder and every gradient are float32.
+ * - Memory rows are dense: row n of the table starts at element n * d_mem.
+ */
+#ifndef MTGNN_H
+#define MTGNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MTGNN_OK = 0,
+  MTGNN_EINVAL = -1,
+  MTGNN_EUNSUPPORTED = -2,
+  MTGNN_EWORKSPACE = -3,
+  MTGNN_EHIP = -4
+} mtgnn_status;
+
+typedef enum { MTGNN_F32 = 0, MTGNN_BF16 = 1 } mtgnn_dtype;
+
+/* Model and table sizes.  d_msg = 2 d_mem + d_time + d_edge is the message width,
+ * d_kv = d_mem + d_edge + d_time the key/value input width, d_q = d_mem + d_time the
+ * query input width.  n_heads must divide d_attn.  d_edge may be 0. */
+typedef struct {
+  int64_t n_nodes;
+  int32_t d_mem, d_time, d_edge, d_attn, n_heads, k;
+  int32_t dtype; /* mtgnn_dtype */
+} mtgnn_dims;
+
+/* One mixed batch (Definition 2, Eq. 5), as device arrays of length n.
+ *   src, dst -- event endpoints u_k, v_k (Section III-A), node ids in [0, n_nodes);
+ *   t        -- timestamps, float32;
+ *   eid      -- event ids, which index the edge-feature rows;
+ *   flags    -- event-type mask, or NULL when every event is a target:
+ *               bit 0 = replayed auxiliary event (no query, no loss);
+ *               bit 1 = pruned by load-aware pruning (Eq. 10-11).
+ * Precondition: events are sorted by (t, eid) ascending and eids are unique. */
+typedef struct {
+  int64_t n;
+  const int32_t* src;
+  const int32_t* dst;
+  const int32_t* eid;
+  const float* t;
+  const uint8_t* flags;
+} mtgnn_batch;
+
+/* Attention parameters.  Weights are in the dims' dtype, biases are float32.
+ *   W_q [d_attn, d_q], W_k and W_v [d_attn, d_kv], W_o [d_attn, d_attn],
+ *   W_1 [d_attn, d_attn + d_mem], W_2 [d_attn, d_attn]. */
+typedef struct {
+  const void *W_q, *W_k, *W_v, *W_o, *W_1, *W_2;
+  const float *b_q, *b_k, *b_v, *b_o, *b_1, *b_2;
+} mtgnn_attn_params;
+
+/* Attention parameter gradients (float32, same shapes, overwritten). */
+typedef struct {
+  float *W_q, *W_k, *W_v, *W_o, *W_1, *W_2;
+  float *b_q, *b_k, *b_v, *b_o, *b_1, *b_2;
+} mtgnn_attn_grads;
+
+typedef enum {
+  MTGNN_OP_BUILD_QUERIES = 0,
+  MTGNN_OP_AGGREGATE_LAST = 1,
+  MTGNN_OP_BUILD_MESSAGES = 2,
+  MTGNN_OP_GRU_UPDATE = 3,
+  MTGNN_OP_SAMPLE_RECENT = 4,
+  MTGNN_OP_TEMPORAL_ATTN = 5,
+  MTGNN_OP_TEMPORAL_ATTN_BWD = 6,
+  MTGNN_OP_GRU_UPDATE_BWD = 7,
+  MTGNN_OP_BUILD_MESSAGES_BWD = 8,
+  MTGNN_OP_BUILD_CSR = 9
+} mtgnn_op;
+
+/* Workspace bytes for `op`.  max_rows is the batch size n for BUILD_QUERIES and
+ * AGGREGATE_LAST, the row maximum for the memory-phase ops, and the number of
+ * stream events for BUILD_CSR.  max_q is the query maximum for the attention
+ * ops.  Unused sizes are ignored.  Returns 0 for an invalid request. */
+size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* dims, int64_t max_rows, int64_t max_q);
+
+/* Bytes of the forward save buffer that the backward call of `op` reads.
+ * op = MTGNN_OP_GRU_UPDATE or MTGNN_OP_TEMPORAL_ATTN; 0 otherwise. */
+size_t mtgnn_save_bytes(int op, const mtgnn_dims* dims, int64_t max_rows, int64_t max_q);
+
+/* Row a1. Batch intake (Definition 2 and Eq. 12).  Builds the query list of
+ * the target events (flags & 3 == 0) in batch order as three blocks:
+ * sources, then destinations, then negatives, each at its event's time.
+ *   neg    -- [b->n] negative destination per event (device);
+ *   q_node -- [3 b->n] out; q_t -- [3 b->n] out;
+ *   n_q    -- device int32 out = 3 * (number of target events).
+ * Entries at or beyond n_q are left untouched. */
+mtgnn_status mtgnn_build_queries(const mtgnn_batch* b, const int32_t* neg, int32_t* q_node, float* q_t,
+                                 int32_t* n_q, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Row a2. Most-recent message aggregation (Eq. 2 applied once per batch).
+ * Every non-pruned event i sends message 2i to src[i] (role 0) and message
+ * 2i+1 to dst[i] (role 1).  For each node that receives a message, the winner
+ * is its message with the largest (t, eid, role).  Under the batch order
+ * precondition that is the largest message index; a self-loop's role 1 wins.
+ *   uniq   -- [2 b->n] out: receiving nodes, ascending;
+ *   winner -- [2 b->n] out: winner message index (2i + role) per uniq entry;
+ *   n_uniq -- device int32 out: number of entries written.
+ * Integer-exact.  No float atomics. */
+mtgnn_status mtgnn_aggregate_last(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
+                                  int32_t* n_uniq, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Row a3. Message construction (Eq. 1) for each aggregated row r < n_rows.
+ * Let i = winner[r] / 2 be the event, node = uniq[r] and partner its other
+ * endpoint.  Then
+ *     msg[r] = [ M[node] || M[partner] || cos(time_w * dt + time_b) || x[eid_i] ],
+ *     dt[r]  = t_i - last_update[node].
+ * dt is a float32 subtraction.  The cosine argument rounds the product and
+ * then the sum to float32, with no fused multiply-add.
+ *   memory      -- [n_nodes, d_mem] (dtype); last_update [n_nodes] float32;
+ *   edge_feat   -- [*, d_edge] float32 indexed by eid (NULL iff d_edge == 0);
+ *   time_w, time_b -- [d_time] float32;
+ *   msg         -- [max_rows, d_msg] out (dtype); dt -- [max_rows] float32 out.
+ * Reads only the pre-update table, so call it before mtgnn_gru_update. */
+mtgnn_status mtgnn_build_messages(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                                  const int32_t* n_rows, int64_t max_rows, const void* memory,
+                                  const float* last_update, const float* edge_feat, const float* time_w,
+                                  const float* time_b, const mtgnn_dims* dims, void* msg, float* dt,
+                                  hipStream_t stream);
+
+/* Row a4. GRU memory update (Eq. 2), gate order r, z, n:
+ *   r = sig(W_ir x + b_ir + W_hr h + b_hr),  z = sig(W_iz x + b_iz + W_hz h + b_hz),
+ *   n = tanh(W_in x + b_in + r * (W_hn h + b_hn)),  h' = (1 - z) n + z h,
+ * with x = msg[r] and h = memory[uniq[r]].  Writes memory[uniq[r]] = h'
+ * (rounded to the dtype) and last_update[uniq[r]] = t of the winning event.
+ * Rows not in uniq are never touched.
+ *   W_ih [3 d_mem, d_msg], W_hh [3 d_mem, d_mem] (dtype); b_ih, b_hh [3 d_mem] float32;
+ *   save -- mtgnn_save_bytes(MTGNN_OP_GRU_UPDATE) bytes for the backward, or NULL. */
+mtgnn_status mtgnn_gru_update(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                              const int32_t* n_rows, int64_t max_rows, const void* msg, const void* W_ih,
+                              const void* W_hh, const float* b_ih, const float* b_hh, const mtgnn_dims* dims,
+                              void* memory, float* last_update, void* save, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/* Row a5. Most-recent-k temporal neighbour sampling over the temporal
+ * adjacency.  The adjacency holds every stream event in both directions.
+ * For query (n, tau), take the entries of node n with t < tau (strictly),
+ * then the k largest by (t, eid, role), newest first.  Missing slots are
+ * padded with nbr = -1, t = 0, eid = -1.
+ *   csr_off [n_nodes+1] int64; csr_nbr, csr_eid int32 and csr_t float32 [2E],
+ *     each node's entries sorted by (t, eid, role) ascending
+ *     (as mtgnn_build_temporal_csr writes them);
+ *   q_node, q_t [max_q]; out_nbr, out_t, out_eid [max_q, k] out.
+ * Integer-exact. */
+mtgnn_status mtgnn_sample_recent(const int64_t* csr_off, const int32_t* csr_nbr, const float* csr_t,
+                                 const int32_t* csr_eid, int64_t n_nodes, const int32_t* q_node,
+                                 const float* q_t, const int32_t* n_q, int64_t max_q, int32_t k,
+                                 int32_t* out_nbr, float* out_t, int32_t* out_eid, hipStream_t stream);
+
+/* Row a6. One-layer multi-head temporal attention embedding for each query q.
+ *   q     = W_q [M[q_node] || phi(0)] + b_q
+ *   K_j   = W_k [M[nbr_j] || x[eid_j] || phi(q_t - t_j)] + b_k,  V_j likewise with W_v
+ *   per head h (d_attn / n_heads columns), over valid slots j (nbr_j >= 0):
+ *     p = softmax_j(q_h . K_jh / sqrt(d_attn / n_heads)),  a_h = sum_j p_j V_jh
+ *     (a = 0 when no slot is valid)
+ *   o     = W_o a + b_o
+ *   z     = W_2 relu(W_1 [o || M[q_node]] + b_1) + b_2
+ * phi(dt) = cos(time_w * dt + time_b) with the rounding of mtgnn_build_messages.
+ *   nbr, nt, neid -- [max_q, k] as written by mtgnn_sample_recent;
+ *   memory        -- the table after this step's mtgnn_gru_update;
+ *   z             -- [max_q, d_attn] float32 out;
+ *   save          -- mtgnn_save_bytes(MTGNN_OP_TEMPORAL_ATTN) bytes for the backward. */
+mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                 const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
+                                 const float* edge_feat, const float* time_w, const float* time_b,
+                                 const mtgnn_attn_params* params, const mtgnn_dims* dims, float* z, void* save,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Row a7. Backward of mtgnn_temporal_attn for the output gradient dz [max_q, d_attn].
+ * The caller computes dz from the masked loss (Eq. 13).
+ *   grads -- every attention parameter gradient (overwritten);
+ *   d_mem -- [max_rows, d_mem] float32 out, row r aligned with uniq[r]: the sum of
+ *            the gradients of every occurrence of node uniq[r], as a query or as a
+ *            valid neighbour.  Memory rows not in uniq get no gradient, because the
+ *            table is not differentiated across steps;
+ *   d_time_w, d_time_b -- [d_time] float32, OVERWRITTEN with the attention's share of the
+ *            time-encoder gradient (mtgnn_build_messages_bwd then adds the messages' share).
+ * q_node ... neid, memory, edge_feat and save are the forward call's.
+ * uniq/n_rows are the rows updated by this step's memory phase (mtgnn_aggregate_last). */
+mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                     const int32_t* nbr, const float* nt, const float* dz, const void* save,
+                                     const int32_t* uniq, const int32_t* n_rows, int64_t max_rows,
+                                     const float* time_w, const float* time_b, const mtgnn_attn_params* params,
+                                     const mtgnn_dims* dims, mtgnn_attn_grads* grads, float* d_mem,
+                                     float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes,
+                                     hipStream_t stream);
+
+/* Row a8. Backward of mtgnn_gru_update for d_mem = dL/dh' [max_rows, d_mem].
+ * The previous memory h is detached.
+ *   save, msg   -- the forward call's (save must not be NULL there);
+ *   dW_ih, dW_hh, db_ih, db_hh -- float32, overwritten;
+ *   dmsg_time   -- [max_rows, d_time] float32 out: dL/dphi for the message time slice,
+ *                  the only message slice the step back-propagates (memory and edge
+ *                  features are inputs, not parameters). */
+mtgnn_status mtgnn_gru_update_bwd(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,
+                                  int64_t max_rows, const void* W_ih, const void* W_hh, const mtgnn_dims* dims,
+                                  float* dW_ih, float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Row a9. Time-encoder gradient of the messages (Eq. 1), ACCUMULATED into d_time_w/d_time_b:
+ *   d_time_w[j] += sum_r dmsg_time[r, j] * (-sin(arg_rj)) * dt[r]
+ *   d_time_b[j] += sum_r dmsg_time[r, j] * (-sin(arg_rj))
+ * where arg_rj = time_w[j] * dt[r] + time_b[j], rounded as in mtgnn_build_messages.
+ * Reductions run in a fixed order (deterministic). */
+mtgnn_status mtgnn_build_messages_bwd(const float* dmsg_time, const float* dt, const int32_t* n_rows,
+                                      int64_t max_rows, const float* time_w, const float* time_b,
+                                      const mtgnn_dims* dims, float* d_time_w, float* d_time_b, void* ws,
+                                      size_t ws_bytes, hipStream_t stream);
+
+/* Temporal adjacency of a whole stream (built once, offline; outside the step).
+ * Event e = (src[e], dst[e], t[e]) with eid e gives two entries: (node src,
+ * nbr dst, role 0) and (node dst, nbr src, role 1).  Entries are grouped by
+ * node and sorted by (t, eid, role) within each node.
+ * Precondition: the stream is sorted by (t, eid) ascending.
+ *   csr_off [n_nodes+1] int64 out; csr_nbr, csr_eid int32 and csr_t float32 [2 n_events] out. */
+mtgnn_status mtgnn_build_temporal_csr(const int32_t* src, const int32_t* dst, const float* t, int64_t n_events,
+                                      int64_t n_nodes, int64_t* csr_off, int32_t* csr_nbr, float* csr_t,
+                                      int32_t* csr_eid, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* mtgnn_status_string(int status);
+
+/* The message of the last MTGNN_EHIP / validation failure on this host thread
+ * ("" if none). */
+const char* mtgnn_last_error(void);
+
+/* ABI version (major * 100 + minor). */
+int mtgnn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MTGNN_H */

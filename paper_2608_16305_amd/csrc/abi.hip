@@ -1,0 +1,316 @@
+// C ABI of the mtgnn library: argument validation (host only, before any HIP
+// call), workspace sizing, status strings, and dispatch to the step kernels.
+#include <string>
+
+#include "ops.h"
+
+namespace mtgnn {
+
+static thread_local std::string g_err;
+
+void set_hip_error(hipError_t e, const char* where) {
+  g_err = std::string(where) + ": " + hipGetErrorString(e);
+}
+
+static mtgnn_status fail(mtgnn_status s, const char* what) {
+  g_err = what;
+  return s;
+}
+
+// Limits of this implementation (beyond them: MTGNN_EUNSUPPORTED).
+constexpr int MAX_K = 64;          // one wave lane per neighbour slot
+constexpr int MAX_HEAD_DIM = 128;  // two columns per lane
+constexpr int MAX_SEG_WIDTH = 512; // d_mem + 2 d_attn, eight columns per lane
+
+static mtgnn_status check_dims(const mtgnn_dims* d) {
+  if (!d) return fail(MTGNN_EINVAL, "dims is NULL");
+  if (d->dtype != MTGNN_F32 && d->dtype != MTGNN_BF16) return fail(MTGNN_EUNSUPPORTED, "dtype");
+  if (d->n_nodes <= 0 || d->n_nodes >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "n_nodes");
+  if (d->d_mem <= 0 || d->d_time < 0 || d->d_edge < 0 || d->d_attn <= 0 || d->n_heads <= 0 || d->k <= 0)
+    return fail(MTGNN_EINVAL, "non-positive dimension");
+  if (d->d_attn % d->n_heads != 0) return fail(MTGNN_EINVAL, "n_heads does not divide d_attn");
+  if (d->k > MAX_K) return fail(MTGNN_EUNSUPPORTED, "k > 64");
+  if (d->d_attn / d->n_heads > MAX_HEAD_DIM) return fail(MTGNN_EUNSUPPORTED, "head width > 128");
+  if (d->d_mem + 2 * d->d_attn > MAX_SEG_WIDTH) return fail(MTGNN_EUNSUPPORTED, "d_mem + 2 d_attn > 512");
+  return MTGNN_OK;
+}
+
+static mtgnn_status check_batch(const mtgnn_batch* b) {
+  if (!b) return fail(MTGNN_EINVAL, "batch is NULL");
+  if (b->n < 0 || b->n >= (int64_t(1) << 30)) return fail(MTGNN_EINVAL, "batch size");
+  if (b->n > 0 && (!b->src || !b->dst || !b->t)) return fail(MTGNN_EINVAL, "batch src/dst/t NULL");
+  return MTGNN_OK;
+}
+
+static mtgnn_status check_rows(int64_t max_rows) {
+  if (max_rows < 0 || max_rows >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_rows");
+  return MTGNN_OK;
+}
+
+#define REQ(p, name) \
+  if (!(p)) return fail(MTGNN_EINVAL, name " is NULL")
+
+}  // namespace mtgnn
+
+using namespace mtgnn;
+
+extern "C" {
+
+int mtgnn_version(void) { return 100; }
+
+const char* mtgnn_status_string(int status) {
+  switch (status) {
+    case MTGNN_OK: return "ok";
+    case MTGNN_EINVAL: return "invalid argument";
+    case MTGNN_EUNSUPPORTED: return "unsupported configuration";
+    case MTGNN_EWORKSPACE: return "workspace too small";
+    case MTGNN_EHIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* mtgnn_last_error(void) { return g_err.c_str(); }
+
+size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int64_t max_q) {
+  if (max_rows < 0 || max_q < 0) return 0;
+  switch (op) {
+    case MTGNN_OP_BUILD_QUERIES: return build_queries_ws(max_rows);
+    case MTGNN_OP_AGGREGATE_LAST: return aggregate_last_ws(max_rows);
+    case MTGNN_OP_BUILD_MESSAGES: return 0;
+    case MTGNN_OP_SAMPLE_RECENT: return 0;
+    case MTGNN_OP_BUILD_CSR: return build_csr_ws(max_rows, d ? d->n_nodes : 0);
+    default: break;
+  }
+  if (check_dims(d) != MTGNN_OK) return 0;
+  switch (op) {
+    case MTGNN_OP_GRU_UPDATE: return gru_update_ws(d, max_rows);
+    case MTGNN_OP_TEMPORAL_ATTN: return attn_fwd_ws(d, max_q);
+    case MTGNN_OP_TEMPORAL_ATTN_BWD: return attn_bwd_ws(d, max_q, max_rows);
+    case MTGNN_OP_GRU_UPDATE_BWD: return gru_update_bwd_ws(d, max_rows);
+    case MTGNN_OP_BUILD_MESSAGES_BWD: return build_messages_bwd_ws(d, max_rows);
+    default: return 0;
+  }
+}
+
+size_t mtgnn_save_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int64_t max_q) {
+  if (check_dims(d) != MTGNN_OK || max_rows < 0 || max_q < 0) return 0;
+  if (op == MTGNN_OP_GRU_UPDATE) return gru_save_bytes(d, max_rows);
+  if (op == MTGNN_OP_TEMPORAL_ATTN) return attn_save_bytes(d, max_q);
+  return 0;
+}
+
+mtgnn_status mtgnn_build_queries(const mtgnn_batch* b, const int32_t* neg, int32_t* q_node, float* q_t, int32_t* n_q,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_batch(b));
+  REQ(neg || b->n == 0, "neg");
+  REQ(q_node, "q_node");
+  REQ(q_t, "q_t");
+  REQ(n_q, "n_q");
+  if (b->flags && b->n > 0 && ws_bytes < build_queries_ws(b->n)) return fail(MTGNN_EWORKSPACE, "build_queries ws");
+  if (b->flags && b->n > 0 && !ws) return fail(MTGNN_EINVAL, "ws is NULL");
+  return build_queries_impl(b, neg, q_node, q_t, n_q, ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_aggregate_last(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
+                                  int32_t* n_uniq, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_batch(b));
+  if (n_nodes <= 0 || n_nodes >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "n_nodes");
+  REQ(uniq, "uniq");
+  REQ(winner, "winner");
+  REQ(n_uniq, "n_uniq");
+  if (ws_bytes < aggregate_last_ws(b->n)) return fail(MTGNN_EWORKSPACE, "aggregate_last ws");
+  if (b->n > 0 && !ws) return fail(MTGNN_EINVAL, "ws is NULL");
+  return aggregate_last_impl(b, n_nodes, uniq, winner, n_uniq, ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_build_messages(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                                  const int32_t* n_rows, int64_t max_rows, const void* memory,
+                                  const float* last_update, const float* edge_feat, const float* time_w,
+                                  const float* time_b, const mtgnn_dims* d, void* msg, float* dt,
+                                  hipStream_t stream) {
+  MTGNN_TRY(check_batch(b));
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  REQ(uniq, "uniq");
+  REQ(winner, "winner");
+  REQ(memory, "memory");
+  REQ(last_update, "last_update");
+  REQ(msg, "msg");
+  REQ(dt, "dt");
+  if (d->d_time > 0 && (!time_w || !time_b)) return fail(MTGNN_EINVAL, "time encoder is NULL");
+  if ((d->d_edge > 0) != (edge_feat != nullptr)) return fail(MTGNN_EINVAL, "edge_feat must be given iff d_edge > 0");
+  if (d->d_edge > 0 && !b->eid && b->n > 0) return fail(MTGNN_EINVAL, "batch eid is NULL");
+  if (max_rows == 0) return MTGNN_OK;
+  return build_messages_impl(b, uniq, winner, n_rows, max_rows, memory, last_update, edge_feat, time_w, time_b, d, msg,
+                             dt, stream);
+}
+
+mtgnn_status mtgnn_gru_update(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                              const int32_t* n_rows, int64_t max_rows, const void* msg, const void* W_ih,
+                              const void* W_hh, const float* b_ih, const float* b_hh, const mtgnn_dims* d,
+                              void* memory, float* last_update, void* save, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  MTGNN_TRY(check_batch(b));
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  REQ(uniq, "uniq");
+  REQ(winner, "winner");
+  REQ(msg, "msg");
+  REQ(W_ih, "W_ih");
+  REQ(W_hh, "W_hh");
+  REQ(b_ih, "b_ih");
+  REQ(b_hh, "b_hh");
+  REQ(memory, "memory");
+  REQ(last_update, "last_update");
+  if (ws_bytes < gru_update_ws(d, max_rows)) return fail(MTGNN_EWORKSPACE, "gru_update ws");
+  if (max_rows == 0) return MTGNN_OK;
+  REQ(ws, "ws");
+  return gru_update_impl(b, uniq, winner, n_rows, max_rows, msg, W_ih, W_hh, b_ih, b_hh, d, memory, last_update, save,
+                         ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_sample_recent(const int64_t* csr_off, const int32_t* csr_nbr, const float* csr_t,
+                                 const int32_t* csr_eid, int64_t n_nodes, const int32_t* q_node, const float* q_t,
+                                 const int32_t* n_q, int64_t max_q, int32_t k, int32_t* out_nbr, float* out_t,
+                                 int32_t* out_eid, hipStream_t stream) {
+  REQ(csr_off, "csr_off");
+  REQ(csr_nbr, "csr_nbr");
+  REQ(csr_t, "csr_t");
+  REQ(csr_eid, "csr_eid");
+  if (n_nodes <= 0) return fail(MTGNN_EINVAL, "n_nodes");
+  if (max_q < 0 || max_q >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (k <= 0) return fail(MTGNN_EINVAL, "k");
+  if (k > MAX_K) return fail(MTGNN_EUNSUPPORTED, "k > 64");
+  if (max_q == 0) return MTGNN_OK;
+  REQ(q_node, "q_node");
+  REQ(q_t, "q_t");
+  REQ(out_nbr, "out_nbr");
+  REQ(out_t, "out_t");
+  REQ(out_eid, "out_eid");
+  return sample_recent_impl(csr_off, csr_nbr, csr_t, csr_eid, q_node, q_t, n_q, max_q, k, out_nbr, out_t, out_eid,
+                            stream);
+}
+
+static mtgnn_status check_attn_params(const mtgnn_attn_params* p) {
+  if (!p) return fail(MTGNN_EINVAL, "params is NULL");
+  if (!p->W_q || !p->W_k || !p->W_v || !p->W_o || !p->W_1 || !p->W_2) return fail(MTGNN_EINVAL, "weight is NULL");
+  if (!p->b_q || !p->b_k || !p->b_v || !p->b_o || !p->b_1 || !p->b_2) return fail(MTGNN_EINVAL, "bias is NULL");
+  return MTGNN_OK;
+}
+
+mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                 const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
+                                 const float* edge_feat, const float* time_w, const float* time_b,
+                                 const mtgnn_attn_params* params, const mtgnn_dims* d, float* z, void* save, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_attn_params(params));
+  if (max_q < 0 || max_q * (int64_t)d->k >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (max_q == 0) return MTGNN_OK;
+  REQ(q_node, "q_node");
+  REQ(q_t, "q_t");
+  REQ(nbr, "nbr");
+  REQ(nt, "nt");
+  REQ(neid, "neid");
+  REQ(memory, "memory");
+  REQ(z, "z");
+  REQ(save, "save");
+  if (d->d_time > 0 && (!time_w || !time_b)) return fail(MTGNN_EINVAL, "time encoder is NULL");
+  if ((d->d_edge > 0) != (edge_feat != nullptr)) return fail(MTGNN_EINVAL, "edge_feat must be given iff d_edge > 0");
+  if (ws_bytes < attn_fwd_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "temporal_attn ws");
+  return attn_fwd_impl(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b, params, d, z, save,
+                       ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                     const int32_t* nbr, const float* nt, const float* dz, const void* save,
+                                     const int32_t* uniq, const int32_t* n_rows, int64_t max_rows,
+                                     const float* time_w, const float* time_b, const mtgnn_attn_params* params,
+                                     const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem, float* d_time_w,
+                                     float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_attn_params(params));
+  MTGNN_TRY(check_rows(max_rows));
+  if (max_q < 0 || max_q * (int64_t)d->k >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (!g || !g->W_q || !g->W_k || !g->W_v || !g->W_o || !g->W_1 || !g->W_2 || !g->b_q || !g->b_k || !g->b_v ||
+      !g->b_o || !g->b_1 || !g->b_2)
+    return fail(MTGNN_EINVAL, "grads");
+  if (max_q == 0) return fail(MTGNN_EINVAL, "max_q == 0 (no query: every gradient is zero; skip the call)");
+  REQ(q_node, "q_node");
+  REQ(q_t, "q_t");
+  REQ(nbr, "nbr");
+  REQ(nt, "nt");
+  REQ(dz, "dz");
+  REQ(save, "save");
+  if (max_rows > 0) {
+    REQ(uniq, "uniq");
+    REQ(d_mem, "d_mem");
+  }
+  if (d->d_time > 0 && (!time_w || !time_b || !d_time_w || !d_time_b)) return fail(MTGNN_EINVAL, "time arrays");
+  if (ws_bytes < attn_bwd_ws(d, max_q, max_rows)) return fail(MTGNN_EWORKSPACE, "temporal_attn_bwd ws");
+  REQ(ws, "ws");
+  return attn_bwd_impl(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params, d,
+                       g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_gru_update_bwd(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,
+                                  int64_t max_rows, const void* W_ih, const void* W_hh, const mtgnn_dims* d,
+                                  float* dW_ih, float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  REQ(dW_ih, "dW_ih");
+  REQ(dW_hh, "dW_hh");
+  REQ(db_ih, "db_ih");
+  REQ(db_hh, "db_hh");
+  if (max_rows == 0) return fail(MTGNN_EINVAL, "max_rows == 0 (no updated row: every gradient is zero; skip the call)");
+  REQ(d_mem, "d_mem");
+  REQ(save, "save");
+  REQ(msg, "msg");
+  REQ(W_ih, "W_ih");
+  REQ(W_hh, "W_hh");
+  if (ws_bytes < gru_update_bwd_ws(d, max_rows)) return fail(MTGNN_EWORKSPACE, "gru_update_bwd ws");
+  REQ(ws, "ws");
+  return gru_update_bwd_impl(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d, dW_ih, dW_hh, db_ih, db_hh, dmsg_time,
+                             ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_build_messages_bwd(const float* dmsg_time, const float* dt, const int32_t* n_rows,
+                                      int64_t max_rows, const float* time_w, const float* time_b, const mtgnn_dims* d,
+                                      float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes,
+                                      hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  if (max_rows == 0 || d->d_time == 0) return MTGNN_OK;
+  REQ(dmsg_time, "dmsg_time");
+  REQ(dt, "dt");
+  REQ(time_w, "time_w");
+  REQ(time_b, "time_b");
+  REQ(d_time_w, "d_time_w");
+  REQ(d_time_b, "d_time_b");
+  if (ws_bytes < build_messages_bwd_ws(d, max_rows)) return fail(MTGNN_EWORKSPACE, "build_messages_bwd ws");
+  REQ(ws, "ws");
+  return build_messages_bwd_impl(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d, d_time_w, d_time_b, ws, ws_bytes,
+                                 stream);
+}
+
+mtgnn_status mtgnn_build_temporal_csr(const int32_t* src, const int32_t* dst, const float* t, int64_t n_events,
+                                      int64_t n_nodes, int64_t* csr_off, int32_t* csr_nbr, float* csr_t,
+                                      int32_t* csr_eid, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (n_events < 0 || n_events >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "n_events");
+  if (n_nodes <= 0 || n_nodes >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "n_nodes");
+  REQ(csr_off, "csr_off");
+  if (n_events > 0) {
+    REQ(src, "src");
+    REQ(dst, "dst");
+    REQ(t, "t");
+    REQ(csr_nbr, "csr_nbr");
+    REQ(csr_t, "csr_t");
+    REQ(csr_eid, "csr_eid");
+    REQ(ws, "ws");
+  }
+  if (ws_bytes < build_csr_ws(n_events, n_nodes)) return fail(MTGNN_EWORKSPACE, "build_csr ws");
+  return build_csr_impl(src, dst, t, n_events, n_nodes, csr_off, csr_nbr, csr_t, csr_eid, ws, ws_bytes, stream);
+}
+
+}  // extern "C"

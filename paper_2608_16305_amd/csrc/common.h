@@ -1,0 +1,108 @@
+// Shared device/host helpers for the mtgnn HIP library (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "mtgnn.h"
+
+namespace mtgnn {
+
+// ------------------------------------------------------------------ status plumbing
+
+// Records the HIP error string of the most recent failed launch (per thread).
+void set_hip_error(hipError_t e, const char* where);
+
+#define MTGNN_CHECK_LAUNCH(where)                                  \
+  do {                                                             \
+    hipError_t _e = hipGetLastError();                             \
+    if (_e != hipSuccess) {                                        \
+      ::mtgnn::set_hip_error(_e, where);                           \
+      return MTGNN_EHIP;                                           \
+    }                                                              \
+  } while (0)
+
+#define MTGNN_TRY(expr)                                            \
+  do {                                                             \
+    mtgnn_status _s = (expr);                                      \
+    if (_s != MTGNN_OK) return _s;                                 \
+  } while (0)
+
+// ------------------------------------------------------------------ small helpers
+
+constexpr int WAVE = 64;
+
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Effective count: the host-side maximum clamped by an optional device-side count.
+__device__ inline int64_t eff_count(int64_t host_max, const int32_t* dev_count) {
+  if (dev_count == nullptr) return host_max;
+  int64_t c = (int64_t)(*dev_count);
+  return c < host_max ? c : host_max;
+}
+
+// bf16 <-> fp32.  Storage conversion rounds to nearest even.
+__device__ __forceinline__ float bf16_to_f32(uint16_t v) {
+  return __uint_as_float(((uint32_t)v) << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);   // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  __device__ __forceinline__ static float load(const float* p, int64_t i) { return p[i]; }
+  __device__ __forceinline__ static void store(float* p, int64_t i, float v) { p[i] = v; }
+};
+template <> struct Elem<uint16_t> {   // bf16 bit patterns
+  __device__ __forceinline__ static float load(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+  __device__ __forceinline__ static void store(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+};
+
+// Cosine time encoding argument w*dt + b, rounded after the product and again
+// after the sum (no fused multiply-add), so every caller rounds it identically.
+__device__ __forceinline__ float time_arg(float w, float dt, float b) {
+#pragma clang fp contract(off)
+  float p = w * dt;
+  float a = p + b;
+  return a;
+}
+
+__device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
+
+// Wave-level reductions (wave64).
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// ------------------------------------------------------------------ library-internal primitives
+
+// Stable LSD radix sort of (key, value) pairs on the low `bits` bits of the key.
+// keys/vals are sorted in place (ping-pong through the workspace).
+size_t radix_sort_ws_bytes(int64_t n);
+mtgnn_status radix_sort_pairs(uint32_t* keys, uint32_t* vals, int64_t n, int bits, void* ws, size_t ws_bytes,
+                              hipStream_t s);
+
+// Exclusive prefix sum of int32 counts; optional device total.
+size_t scan_ws_bytes(int64_t n);
+mtgnn_status scan_exclusive(const int32_t* in, int32_t* out, int64_t n, int32_t* total, void* ws,
+                            size_t ws_bytes, hipStream_t s);
+
+// Deterministic column sums of a row-major [rows x cols] fp32 matrix (rows clamped by rows_dev).
+size_t colsum_ws_bytes(int64_t rows, int cols);
+mtgnn_status colsum(const float* X, int64_t ld, int64_t rows, const int32_t* rows_dev, int cols, float* out,
+                    bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
+
+int bits_for(int64_t max_value);   // bits needed to hold values 0..max_value
+
+}  // namespace mtgnn

@@ -1,0 +1,488 @@
+// Memory phase of the batch step: batch intake, most-recent aggregation,
+// message construction, GRU update with write-back, and their backward passes.
+#include "gemm.h"
+#include "ops.h"
+
+namespace mtgnn {
+
+namespace {
+
+size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// ---------------------------------------------------------------- batch intake
+
+__global__ void k_set_int(int32_t* p, int32_t v) { *p = v; }
+
+__global__ void k_queries_all(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                              const int32_t* __restrict__ neg, const float* __restrict__ t, int64_t n,
+                              int32_t* __restrict__ q_node, float* __restrict__ q_t, int32_t* __restrict__ n_q) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) *n_q = (int32_t)(3 * n);
+  if (i >= n) return;
+  const float ti = t[i];
+  q_node[i] = src[i];
+  q_node[n + i] = dst[i];
+  q_node[2 * n + i] = neg[i];
+  q_t[i] = ti;
+  q_t[n + i] = ti;
+  q_t[2 * n + i] = ti;
+}
+
+__global__ void k_target_flags(const uint8_t* __restrict__ flags, int64_t n, int32_t* __restrict__ tgt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) tgt[i] = (flags[i] & 3) == 0 ? 1 : 0;
+}
+
+__global__ void k_queries_masked(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                                 const int32_t* __restrict__ neg, const float* __restrict__ t,
+                                 const uint8_t* __restrict__ flags, int64_t n, const int32_t* __restrict__ pos,
+                                 const int32_t* __restrict__ n_tar, int32_t* __restrict__ q_node,
+                                 float* __restrict__ q_t, int32_t* __restrict__ n_q) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nt = *n_tar;
+  if (i == 0) *n_q = (int32_t)(3 * nt);
+  if (i >= n || (flags[i] & 3) != 0) return;
+  const int64_t p = pos[i];
+  const float ti = t[i];
+  q_node[p] = src[i];
+  q_node[nt + p] = dst[i];
+  q_node[2 * nt + p] = neg[i];
+  q_t[p] = ti;
+  q_t[nt + p] = ti;
+  q_t[2 * nt + p] = ti;
+}
+
+// ---------------------------------------------------------------- most-recent aggregation
+
+// Message m = 2i + role goes to src[i] (role 0) or dst[i] (role 1); pruned
+// events get the sentinel key n_nodes, which sorts after every node.
+__global__ void k_agg_keys(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                           const uint8_t* __restrict__ flags, int64_t n, uint32_t sentinel, uint32_t* __restrict__ keys,
+                           uint32_t* __restrict__ vals) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= 2 * n) return;
+  const int64_t i = m >> 1;
+  const bool pruned = flags != nullptr && (flags[i] & 2);
+  keys[m] = pruned ? sentinel : (uint32_t)((m & 1) ? dst[i] : src[i]);
+  vals[m] = (uint32_t)m;
+}
+
+// After a stable sort by node, the last message of each node's run is the
+// one with the largest message index.
+__global__ void k_agg_last_flags(const uint32_t* __restrict__ keys, int64_t nm, uint32_t sentinel,
+                                 int32_t* __restrict__ is_last) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= nm) return;
+  const uint32_t k = keys[p];
+  is_last[p] = (k != sentinel && (p == nm - 1 || keys[p + 1] != k)) ? 1 : 0;
+}
+
+__global__ void k_agg_write(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
+                            const int32_t* __restrict__ is_last, const int32_t* __restrict__ pos, int64_t nm,
+                            int32_t* __restrict__ uniq, int32_t* __restrict__ winner) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= nm || !is_last[p]) return;
+  uniq[pos[p]] = (int32_t)keys[p];
+  winner[pos[p]] = (int32_t)vals[p];
+}
+
+// ---------------------------------------------------------------- message construction
+
+// One wave per row; lanes stride over the message columns.
+template <typename T>
+__global__ __launch_bounds__(256) void k_build_messages(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                                                        const int32_t* __restrict__ eid, const float* __restrict__ t,
+                                                        const int32_t* __restrict__ uniq,
+                                                        const int32_t* __restrict__ winner,
+                                                        const int32_t* __restrict__ n_rows, int64_t max_rows,
+                                                        const T* __restrict__ mem, const float* __restrict__ lu,
+                                                        const float* __restrict__ x, const float* __restrict__ tw,
+                                                        const float* __restrict__ tb, int dm, int dt_dim, int de,
+                                                        T* __restrict__ msg, float* __restrict__ dt_out) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= eff_count(max_rows, n_rows)) return;
+  const int32_t w = winner[r];
+  const int64_t i = w >> 1;
+  const int64_t node = uniq[r];
+  const int64_t partner = (w & 1) ? src[i] : dst[i];
+  const float dt = t[i] - lu[node];
+  const int dmsg = 2 * dm + dt_dim + de;
+  T* out = msg + r * dmsg;
+  const T* mn = mem + node * dm;
+  const T* mp = mem + partner * dm;
+  for (int c = lane; c < dm; c += 64) {
+    out[c] = mn[c];
+    out[dm + c] = mp[c];
+  }
+  for (int j = lane; j < dt_dim; j += 64) Elem<T>::store(out, 2 * dm + j, cosf(time_arg(tw[j], dt, tb[j])));
+  if (de > 0) {
+    const float* xr = x + (int64_t)eid[i] * de;
+    for (int c = lane; c < de; c += 64) Elem<T>::store(out, 2 * dm + dt_dim + c, xr[c]);
+  }
+  if (lane == 0) dt_out[r] = dt;
+}
+
+// ---------------------------------------------------------------- GRU
+
+template <typename T>
+__global__ void k_gather_rows(const T* __restrict__ mem, const int32_t* __restrict__ uniq,
+                              const int32_t* __restrict__ n_rows, int64_t max_rows, int dm, float* __restrict__ out) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = e / dm;
+  if (r >= eff_count(max_rows, n_rows)) return;
+  const int c = (int)(e % dm);
+  out[e] = Elem<T>::load(mem, (int64_t)uniq[r] * dm + c);
+}
+
+// G = [gi | gh] (row stride 6 dm).  Writes the new memory row, last_update and the saved gates.
+template <typename T>
+__global__ void k_gru_gates(const float* __restrict__ G, const float* __restrict__ h_old,
+                            const int32_t* __restrict__ uniq, const int32_t* __restrict__ winner,
+                            const float* __restrict__ t, const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
+                            T* __restrict__ mem, float* __restrict__ lu, float* __restrict__ sr, float* __restrict__ sz,
+                            float* __restrict__ sn, float* __restrict__ sghn) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = e / dm;
+  if (r >= eff_count(max_rows, n_rows)) return;
+  const int j = (int)(e % dm);
+  const float* g = G + r * 6 * dm;
+  const float rr = sigmoidf_(g[j] + g[3 * dm + j]);
+  const float zz = sigmoidf_(g[dm + j] + g[4 * dm + j]);
+  const float ghn = g[5 * dm + j];
+  const float nn = tanhf(g[2 * dm + j] + rr * ghn);
+  const float h = h_old[e];
+  const float hn = (1.f - zz) * nn + zz * h;
+  const int64_t node = uniq[r];
+  Elem<T>::store(mem, node * dm + j, hn);
+  if (j == 0) lu[node] = t[winner[r] >> 1];
+  if (sr) {
+    sr[e] = rr;
+    sz[e] = zz;
+    sn[e] = nn;
+    sghn[e] = ghn;
+  }
+}
+
+__global__ void k_gru_bwd_gates(const float* __restrict__ dh, const float* __restrict__ h_old,
+                                const float* __restrict__ sr, const float* __restrict__ sz,
+                                const float* __restrict__ sn, const float* __restrict__ sghn,
+                                const int32_t* __restrict__ n_rows, int64_t max_rows, int dm, float* __restrict__ dgi,
+                                float* __restrict__ dgh) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = e / dm;
+  if (r >= eff_count(max_rows, n_rows)) return;
+  const int j = (int)(e % dm);
+  const float d = dh[e], rr = sr[e], zz = sz[e], nn = sn[e], ghn = sghn[e], h = h_old[e];
+  const float dn_pre = d * (1.f - zz) * (1.f - nn * nn);
+  const float dz_pre = d * (h - nn) * zz * (1.f - zz);
+  const float dr_pre = dn_pre * ghn * rr * (1.f - rr);
+  float* gi = dgi + r * 3 * dm;
+  float* gh = dgh + r * 3 * dm;
+  gi[j] = dr_pre;
+  gi[dm + j] = dz_pre;
+  gi[2 * dm + j] = dn_pre;
+  gh[j] = dr_pre;
+  gh[dm + j] = dz_pre;
+  gh[2 * dm + j] = dn_pre * rr;
+}
+
+// ---------------------------------------------------------------- time-encoder gradients
+
+constexpr int TG_ROWS = 512;
+
+struct MsgDelta {
+  const float* dt;
+  __device__ bool get(int64_t r, float& d) const {
+    d = dt[r];
+    return true;
+  }
+};
+
+template <typename D>
+__global__ __launch_bounds__(256) void k_timegrad_partial(const float* __restrict__ dphi, int64_t ld, int64_t rows,
+                                                          const int32_t* __restrict__ rows_dev, D delta,
+                                                          const float* __restrict__ tw, const float* __restrict__ tb,
+                                                          int dt_dim, float* __restrict__ part) {
+  __shared__ float red_w[4][64], red_b[4][64];
+  const int j = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int rg = threadIdx.x >> 6;
+  const int64_t nrows = eff_count(rows, rows_dev);
+  const int64_t r0 = (int64_t)blockIdx.y * TG_ROWS;
+  const int64_t r1 = min(nrows, r0 + TG_ROWS);
+  float sw = 0.f, sb = 0.f;
+  if (j < dt_dim) {
+    const float w = tw[j], b = tb[j];
+    for (int64_t r = r0 + rg; r < r1; r += 4) {
+      float d;
+      if (!delta.get(r, d)) continue;
+      const float g = dphi[r * ld + j] * -sinf(time_arg(w, d, b));
+      sb += g;
+      sw += g * d;
+    }
+  }
+  red_w[rg][threadIdx.x & 63] = sw;
+  red_b[rg][threadIdx.x & 63] = sb;
+  __syncthreads();
+  if (rg == 0 && j < dt_dim) {
+    const int c = threadIdx.x;
+    part[((int64_t)blockIdx.y * 2 + 0) * dt_dim + j] = ((red_w[0][c] + red_w[1][c]) + red_w[2][c]) + red_w[3][c];
+    part[((int64_t)blockIdx.y * 2 + 1) * dt_dim + j] = ((red_b[0][c] + red_b[1][c]) + red_b[2][c]) + red_b[3][c];
+  }
+}
+
+__global__ void k_timegrad_final(const float* __restrict__ part, int nch, int dt_dim, float* __restrict__ dw,
+                                 float* __restrict__ db, int accumulate) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= dt_dim) return;
+  float sw = 0.f, sb = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    sw += part[((int64_t)c * 2 + 0) * dt_dim + j];
+    sb += part[((int64_t)c * 2 + 1) * dt_dim + j];
+  }
+  dw[j] = accumulate ? dw[j] + sw : sw;
+  db[j] = accumulate ? db[j] + sb : sb;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- shared time-grad launcher
+
+size_t timegrad_ws_bytes(int64_t rows, int dt_dim) {
+  return a256(sizeof(float) * 2 * (size_t)cdiv(rows < 1 ? 1 : rows, TG_ROWS) * dt_dim);
+}
+
+template <typename D>
+mtgnn_status timegrad_launch(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, D delta,
+                             const float* tw, const float* tb, int dt_dim, float* dw, float* db, bool accumulate,
+                             void* ws, size_t ws_bytes, hipStream_t s) {
+  if (dt_dim <= 0) return MTGNN_OK;
+  if (rows <= 0) rows = 1;   // still writes (zero) sums when overwriting
+  if (ws_bytes < timegrad_ws_bytes(rows, dt_dim)) return MTGNN_EWORKSPACE;
+  const int nch = (int)cdiv(rows, TG_ROWS);
+  dim3 g((unsigned)cdiv(dt_dim, 64), (unsigned)nch);
+  k_timegrad_partial<D><<<g, 256, 0, s>>>(dphi, ld, rows, rows_dev, delta, tw, tb, dt_dim, (float*)ws);
+  MTGNN_CHECK_LAUNCH("timegrad_partial");
+  k_timegrad_final<<<(unsigned)cdiv(dt_dim, 256), 256, 0, s>>>((const float*)ws, nch, dt_dim, dw, db,
+                                                               accumulate ? 1 : 0);
+  MTGNN_CHECK_LAUNCH("timegrad_final");
+  return MTGNN_OK;
+}
+
+namespace {
+struct PairDelta {
+  const int32_t* nbr;
+  const float* q_t;
+  const float* nt;
+  const int32_t* n_q;
+  int k;
+  __device__ bool get(int64_t r, float& d) const {
+    const int64_t q = r / k;
+    if (n_q != nullptr && q >= *n_q) return false;
+    if (nbr[r] < 0) return false;
+    d = q_t[q] - nt[r];
+    return true;
+  }
+};
+struct ZeroDelta {
+  __device__ bool get(int64_t, float& d) const {
+    d = 0.f;
+    return true;
+  }
+};
+}  // namespace
+
+mtgnn_status timegrad_pairs(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev_q, int k,
+                            const int32_t* nbr, const float* q_t, const float* nt, const float* tw, const float* tb,
+                            int dt_dim, float* dw, float* db, bool accumulate, void* ws, size_t ws_bytes,
+                            hipStream_t s) {
+  return timegrad_launch(dphi, ld, rows, nullptr, PairDelta{nbr, q_t, nt, rows_dev_q, k}, tw, tb, dt_dim, dw, db,
+                         accumulate, ws, ws_bytes, s);
+}
+
+mtgnn_status timegrad_zero(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* tw,
+                           const float* tb, int dt_dim, float* dw, float* db, bool accumulate, void* ws,
+                           size_t ws_bytes, hipStream_t s) {
+  return timegrad_launch(dphi, ld, rows, rows_dev, ZeroDelta{}, tw, tb, dt_dim, dw, db, accumulate, ws, ws_bytes, s);
+}
+
+// ---------------------------------------------------------------- entry-point bodies
+
+size_t build_queries_ws(int64_t n) { return 2 * a256(sizeof(int32_t) * n) + a256(sizeof(int32_t)) + scan_ws_bytes(n); }
+
+mtgnn_status build_queries_impl(const mtgnn_batch* b, const int32_t* neg, int32_t* q_node, float* q_t, int32_t* n_q,
+                                void* ws, size_t ws_bytes, hipStream_t s) {
+  const int64_t n = b->n;
+  if (b->flags == nullptr || n == 0) {
+    k_queries_all<<<(unsigned)cdiv(n < 1 ? 1 : n, 256), 256, 0, s>>>(b->src, b->dst, neg, b->t, n, q_node, q_t, n_q);
+    MTGNN_CHECK_LAUNCH("queries_all");
+    return MTGNN_OK;
+  }
+  if (ws_bytes < build_queries_ws(n)) return MTGNN_EWORKSPACE;
+  char* w = (char*)ws;
+  int32_t* tgt = (int32_t*)w;
+  w += a256(sizeof(int32_t) * n);
+  int32_t* pos = (int32_t*)w;
+  w += a256(sizeof(int32_t) * n);
+  int32_t* ntar = (int32_t*)w;
+  w += a256(sizeof(int32_t));
+  const unsigned grid = (unsigned)cdiv(n, 256);
+  k_target_flags<<<grid, 256, 0, s>>>(b->flags, n, tgt);
+  MTGNN_CHECK_LAUNCH("target_flags");
+  MTGNN_TRY(scan_exclusive(tgt, pos, n, ntar, w, ws_bytes - (size_t)(w - (char*)ws), s));
+  k_queries_masked<<<grid, 256, 0, s>>>(b->src, b->dst, neg, b->t, b->flags, n, pos, ntar, q_node, q_t, n_q);
+  MTGNN_CHECK_LAUNCH("queries_masked");
+  return MTGNN_OK;
+}
+
+size_t aggregate_last_ws(int64_t n) {
+  const int64_t nm = 2 * n;
+  return 4 * a256(sizeof(int32_t) * nm) + radix_sort_ws_bytes(nm) + scan_ws_bytes(nm);
+}
+
+mtgnn_status aggregate_last_impl(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
+                                 int32_t* n_uniq, void* ws, size_t ws_bytes, hipStream_t s) {
+  const int64_t n = b->n, nm = 2 * n;
+  if (n == 0) {
+    k_set_int<<<1, 1, 0, s>>>(n_uniq, 0);
+    MTGNN_CHECK_LAUNCH("set_int");
+    return MTGNN_OK;
+  }
+  if (ws_bytes < aggregate_last_ws(n)) return MTGNN_EWORKSPACE;
+  char* w = (char*)ws;
+  uint32_t* keys = (uint32_t*)w;
+  w += a256(sizeof(int32_t) * nm);
+  uint32_t* vals = (uint32_t*)w;
+  w += a256(sizeof(int32_t) * nm);
+  int32_t* is_last = (int32_t*)w;
+  w += a256(sizeof(int32_t) * nm);
+  int32_t* pos = (int32_t*)w;
+  w += a256(sizeof(int32_t) * nm);
+  const size_t rest = ws_bytes - (size_t)(w - (char*)ws);
+  const uint32_t sentinel = (uint32_t)n_nodes;
+  const unsigned grid = (unsigned)cdiv(nm, 256);
+  k_agg_keys<<<grid, 256, 0, s>>>(b->src, b->dst, b->flags, n, sentinel, keys, vals);
+  MTGNN_CHECK_LAUNCH("agg_keys");
+  MTGNN_TRY(radix_sort_pairs(keys, vals, nm, bits_for(n_nodes), w, rest, s));
+  k_agg_last_flags<<<grid, 256, 0, s>>>(keys, nm, sentinel, is_last);
+  MTGNN_CHECK_LAUNCH("agg_last_flags");
+  MTGNN_TRY(scan_exclusive(is_last, pos, nm, n_uniq, w, rest, s));
+  k_agg_write<<<grid, 256, 0, s>>>(keys, vals, is_last, pos, nm, uniq, winner);
+  MTGNN_CHECK_LAUNCH("agg_write");
+  return MTGNN_OK;
+}
+
+mtgnn_status build_messages_impl(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                                 const int32_t* n_rows, int64_t max_rows, const void* memory, const float* lu,
+                                 const float* edge_feat, const float* tw, const float* tb, const mtgnn_dims* d,
+                                 void* msg, float* dt, hipStream_t s) {
+  const unsigned grid = (unsigned)cdiv(max_rows, 4);
+  if (d->dtype == MTGNN_F32)
+    k_build_messages<float><<<grid, 256, 0, s>>>(b->src, b->dst, b->eid, b->t, uniq, winner, n_rows, max_rows,
+                                                  (const float*)memory, lu, edge_feat, tw, tb, d->d_mem, d->d_time,
+                                                  d->d_edge, (float*)msg, dt);
+  else
+    k_build_messages<uint16_t><<<grid, 256, 0, s>>>(b->src, b->dst, b->eid, b->t, uniq, winner, n_rows, max_rows,
+                                                     (const uint16_t*)memory, lu, edge_feat, tw, tb, d->d_mem,
+                                                     d->d_time, d->d_edge, (uint16_t*)msg, dt);
+  MTGNN_CHECK_LAUNCH("build_messages");
+  return MTGNN_OK;
+}
+
+// GRU save layout: h_old, r, z, n, ghn, each [max_rows, d_mem] float32.
+size_t gru_save_bytes(const mtgnn_dims* d, int64_t max_rows) { return 5 * a256(sizeof(float) * max_rows * d->d_mem); }
+
+size_t gru_update_ws(const mtgnn_dims* d, int64_t max_rows) {
+  return a256(sizeof(float) * max_rows * 6 * d->d_mem) + a256(sizeof(float) * max_rows * d->d_mem);
+}
+
+mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner, const int32_t* n_rows,
+                             int64_t max_rows, const void* msg, const void* W_ih, const void* W_hh, const float* b_ih,
+                             const float* b_hh, const mtgnn_dims* d, void* memory, float* lu, void* save, void* ws,
+                             size_t ws_bytes, hipStream_t s) {
+  if (ws_bytes < gru_update_ws(d, max_rows)) return MTGNN_EWORKSPACE;
+  const int dm = d->d_mem, dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
+  const size_t plane = a256(sizeof(float) * max_rows * dm);
+  float* G = (float*)ws;
+  float* h_old = save ? (float*)save : (float*)((char*)ws + a256(sizeof(float) * max_rows * 6 * dm));
+  float *sr = nullptr, *sz = nullptr, *sn = nullptr, *sghn = nullptr;
+  if (save) {
+    sr = (float*)((char*)save + plane);
+    sz = (float*)((char*)save + 2 * plane);
+    sn = (float*)((char*)save + 3 * plane);
+    sghn = (float*)((char*)save + 4 * plane);
+  }
+  const unsigned gel = (unsigned)cdiv(max_rows * dm, 256);
+  if (d->dtype == MTGNN_F32)
+    k_gather_rows<float><<<gel, 256, 0, s>>>((const float*)memory, uniq, n_rows, max_rows, dm, h_old);
+  else
+    k_gather_rows<uint16_t><<<gel, 256, 0, s>>>((const uint16_t*)memory, uniq, n_rows, max_rows, dm, h_old);
+  MTGNN_CHECK_LAUNCH("gather_rows");
+  MTGNN_TRY(linear_fwd(msg, d->dtype, dmsg, W_ih, d->dtype, dmsg, b_ih, G, 6 * dm, max_rows, n_rows, 3 * dm, dmsg,
+                       false, s));
+  MTGNN_TRY(linear_fwd(h_old, MTGNN_F32, dm, W_hh, d->dtype, dm, b_hh, G + 3 * dm, 6 * dm, max_rows, n_rows, 3 * dm,
+                       dm, false, s));
+  if (d->dtype == MTGNN_F32)
+    k_gru_gates<float><<<gel, 256, 0, s>>>(G, h_old, uniq, winner, b->t, n_rows, max_rows, dm, (float*)memory, lu, sr,
+                                           sz, sn, sghn);
+  else
+    k_gru_gates<uint16_t><<<gel, 256, 0, s>>>(G, h_old, uniq, winner, b->t, n_rows, max_rows, dm, (uint16_t*)memory,
+                                              lu, sr, sz, sn, sghn);
+  MTGNN_CHECK_LAUNCH("gru_gates");
+  return MTGNN_OK;
+}
+
+size_t gru_update_bwd_ws(const mtgnn_dims* d, int64_t max_rows) {
+  const int dm = d->d_mem, dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
+  size_t dw = linear_dw_ws_bytes(max_rows, 3 * dm, dmsg);
+  size_t dw2 = linear_dw_ws_bytes(max_rows, 3 * dm, dm);
+  size_t cs = colsum_ws_bytes(max_rows, 3 * dm);
+  size_t m = dw > dw2 ? dw : dw2;
+  m = m > cs ? m : cs;
+  return 2 * a256(sizeof(float) * max_rows * 3 * dm) + a256(m);
+}
+
+mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,
+                                 int64_t max_rows, const void* W_ih, const void* W_hh, const mtgnn_dims* d, float* dW_ih,
+                                 float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time, void* ws, size_t ws_bytes,
+                                 hipStream_t s) {
+  if (ws_bytes < gru_update_bwd_ws(d, max_rows)) return MTGNN_EWORKSPACE;
+  const int dm = d->d_mem, dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
+  const size_t plane = a256(sizeof(float) * max_rows * dm);
+  const float* h_old = (const float*)save;
+  const float* sr = (const float*)((const char*)save + plane);
+  const float* sz = (const float*)((const char*)save + 2 * plane);
+  const float* sn = (const float*)((const char*)save + 3 * plane);
+  const float* sghn = (const float*)((const char*)save + 4 * plane);
+  char* w = (char*)ws;
+  float* dgi = (float*)w;
+  w += a256(sizeof(float) * max_rows * 3 * dm);
+  float* dgh = (float*)w;
+  w += a256(sizeof(float) * max_rows * 3 * dm);
+  const size_t rest = ws_bytes - (size_t)(w - (char*)ws);
+  k_gru_bwd_gates<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(d_mem, h_old, sr, sz, sn, sghn, n_rows, max_rows,
+                                                                        dm, dgi, dgh);
+  MTGNN_CHECK_LAUNCH("gru_bwd_gates");
+  MTGNN_TRY(linear_dw(dgi, 3 * dm, msg, d->dtype, dmsg, dW_ih, dmsg, max_rows, n_rows, 3 * dm, dmsg, w, rest, s));
+  MTGNN_TRY(linear_dw(dgh, 3 * dm, h_old, MTGNN_F32, dm, dW_hh, dm, max_rows, n_rows, 3 * dm, dm, w, rest, s));
+  MTGNN_TRY(colsum(dgi, 3 * dm, max_rows, n_rows, 3 * dm, db_ih, false, w, rest, s));
+  MTGNN_TRY(colsum(dgh, 3 * dm, max_rows, n_rows, 3 * dm, db_hh, false, w, rest, s));
+  if (dmsg_time && d->d_time > 0) {
+    const size_t esz = d->dtype == MTGNN_F32 ? 4 : 2;
+    const void* Wt = (const char*)W_ih + esz * (size_t)(2 * dm);   // columns [2 dm, 2 dm + d_time)
+    MTGNN_TRY(linear_dx(dgi, 3 * dm, Wt, d->dtype, dmsg, dmsg_time, d->d_time, max_rows, n_rows, 3 * dm, d->d_time,
+                        false, s));
+  }
+  return MTGNN_OK;
+}
+
+size_t build_messages_bwd_ws(const mtgnn_dims* d, int64_t max_rows) { return timegrad_ws_bytes(max_rows, d->d_time); }
+
+mtgnn_status build_messages_bwd_impl(const float* dmsg_time, const float* dt, const int32_t* n_rows, int64_t max_rows,
+                                     const float* tw, const float* tb, const mtgnn_dims* d, float* dw, float* db,
+                                     void* ws, size_t ws_bytes, hipStream_t s) {
+  return timegrad_launch(dmsg_time, d->d_time, max_rows, n_rows, MsgDelta{dt}, tw, tb, d->d_time, dw, db, true, ws,
+                         ws_bytes, s);
+}
+
+}  // namespace mtgnn

@@ -1,0 +1,70 @@
+// Internal entry points behind the C ABI (validation happens in abi.cpp).
+#pragma once
+
+#include "common.h"
+
+namespace mtgnn {
+
+// batch intake / memory phase
+size_t build_queries_ws(int64_t n);
+mtgnn_status build_queries_impl(const mtgnn_batch* b, const int32_t* neg, int32_t* q_node, float* q_t, int32_t* n_q,
+                                void* ws, size_t ws_bytes, hipStream_t s);
+size_t aggregate_last_ws(int64_t n);
+mtgnn_status aggregate_last_impl(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
+                                 int32_t* n_uniq, void* ws, size_t ws_bytes, hipStream_t s);
+mtgnn_status build_messages_impl(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                                 const int32_t* n_rows, int64_t max_rows, const void* memory, const float* lu,
+                                 const float* edge_feat, const float* tw, const float* tb, const mtgnn_dims* d,
+                                 void* msg, float* dt, hipStream_t s);
+size_t gru_save_bytes(const mtgnn_dims* d, int64_t max_rows);
+size_t gru_update_ws(const mtgnn_dims* d, int64_t max_rows);
+mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner, const int32_t* n_rows,
+                             int64_t max_rows, const void* msg, const void* W_ih, const void* W_hh, const float* b_ih,
+                             const float* b_hh, const mtgnn_dims* d, void* memory, float* lu, void* save, void* ws,
+                             size_t ws_bytes, hipStream_t s);
+size_t gru_update_bwd_ws(const mtgnn_dims* d, int64_t max_rows);
+mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,
+                                 int64_t max_rows, const void* W_ih, const void* W_hh, const mtgnn_dims* d,
+                                 float* dW_ih, float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time, void* ws,
+                                 size_t ws_bytes, hipStream_t s);
+size_t build_messages_bwd_ws(const mtgnn_dims* d, int64_t max_rows);
+mtgnn_status build_messages_bwd_impl(const float* dmsg_time, const float* dt, const int32_t* n_rows, int64_t max_rows,
+                                     const float* tw, const float* tb, const mtgnn_dims* d, float* dw, float* db,
+                                     void* ws, size_t ws_bytes, hipStream_t s);
+
+// time-encoder gradient reductions (fixed order)
+size_t timegrad_ws_bytes(int64_t rows, int dt_dim);
+// rows = query*k + slot; delta = q_t[row / k] - nt[row]; slots with nbr < 0 are skipped
+mtgnn_status timegrad_pairs(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev_q, int k,
+                            const int32_t* nbr, const float* q_t, const float* nt, const float* tw, const float* tb,
+                            int dt_dim, float* dw, float* db, bool accumulate, void* ws, size_t ws_bytes,
+                            hipStream_t s);
+// delta = 0 for every row (the query-side phi(0))
+mtgnn_status timegrad_zero(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* tw,
+                           const float* tb, int dt_dim, float* dw, float* db, bool accumulate, void* ws,
+                           size_t ws_bytes, hipStream_t s);
+
+// sampling / adjacency
+mtgnn_status sample_recent_impl(const int64_t* off, const int32_t* nbr, const float* t, const int32_t* eid,
+                                const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q, int k,
+                                int32_t* out_nbr, float* out_t, int32_t* out_eid, hipStream_t s);
+size_t build_csr_ws(int64_t n_events, int64_t n_nodes);
+mtgnn_status build_csr_impl(const int32_t* src, const int32_t* dst, const float* t, int64_t n_events, int64_t n_nodes,
+                            int64_t* off, int32_t* nbr, float* t_out, int32_t* eid_out, void* ws, size_t ws_bytes,
+                            hipStream_t s);
+
+// attention
+size_t attn_save_bytes(const mtgnn_dims* d, int64_t max_q);
+size_t attn_fwd_ws(const mtgnn_dims* d, int64_t max_q);
+mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                           const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
+                           const float* edge_feat, const float* tw, const float* tb, const mtgnn_attn_params* p,
+                           const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s);
+size_t attn_bwd_ws(const mtgnn_dims* d, int64_t max_q, int64_t max_rows);
+mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                           const int32_t* nbr, const float* nt, const float* dz, const void* save, const int32_t* uniq,
+                           const int32_t* n_rows, int64_t max_rows, const float* tw, const float* tb,
+                           const mtgnn_attn_params* p, const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem,
+                           float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes, hipStream_t s);
+
+}  // namespace mtgnn

@@ -1,0 +1,276 @@
+"""ctypes binding of libmtgnn.so.
+
+Argument marshalling only: every function checks that its tensors live on the
+GPU with the expected dtype and layout, passes their device pointers and the
+current HIP stream to the C entry point of the same name, and raises
+``MtgnnError`` on a non-zero status.  No computation happens here, and there
+is no fallback: if the library is missing, the first call raises.
+"""
+
+import ctypes as C
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmtgnn.so")
+
+F32, BF16 = 0, 1
+OP_BUILD_QUERIES, OP_AGGREGATE_LAST, OP_BUILD_MESSAGES, OP_GRU_UPDATE, OP_SAMPLE_RECENT = 0, 1, 2, 3, 4
+OP_TEMPORAL_ATTN, OP_TEMPORAL_ATTN_BWD, OP_GRU_UPDATE_BWD, OP_BUILD_MESSAGES_BWD, OP_BUILD_CSR = 5, 6, 7, 8, 9
+
+ENTRY_POINTS = (
+    "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
+    "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_bwd", "mtgnn_gru_update_bwd",
+    "mtgnn_build_messages_bwd", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
+    "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version",
+)
+
+
+class MtgnnError(RuntimeError):
+    pass
+
+
+class Dims(C.Structure):
+    _fields_ = [("n_nodes", C.c_int64), ("d_mem", C.c_int32), ("d_time", C.c_int32), ("d_edge", C.c_int32),
+                ("d_attn", C.c_int32), ("n_heads", C.c_int32), ("k", C.c_int32), ("dtype", C.c_int32)]
+
+
+class Batch(C.Structure):
+    _fields_ = [("n", C.c_int64), ("src", C.c_void_p), ("dst", C.c_void_p), ("eid", C.c_void_p),
+                ("t", C.c_void_p), ("flags", C.c_void_p)]
+
+
+_ATTN = ("W_q", "W_k", "W_v", "W_o", "W_1", "W_2", "b_q", "b_k", "b_v", "b_o", "b_1", "b_2")
+
+
+class AttnParams(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in _ATTN]
+
+
+class AttnGrads(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in _ATTN]
+
+
+_P = C.c_void_p
+_I64 = C.c_int64
+_I32 = C.c_int32
+_SZ = C.c_size_t
+_SIGS = {
+    "mtgnn_build_queries": [C.POINTER(Batch), _P, _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_aggregate_last": [C.POINTER(Batch), _I64, _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_build_messages": [C.POINTER(Batch), _P, _P, _P, _I64, _P, _P, _P, _P, _P, C.POINTER(Dims), _P, _P, _P],
+    "mtgnn_gru_update": [C.POINTER(Batch), _P, _P, _P, _I64, _P, _P, _P, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _SZ,
+                         _P],
+    "mtgnn_sample_recent": [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I32, _P, _P, _P, _P],
+    "mtgnn_temporal_attn": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams), C.POINTER(Dims), _P,
+                            _P, _P, _SZ, _P],
+    "mtgnn_temporal_attn_bwd": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, C.POINTER(AttnParams),
+                                C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_gru_update_bwd": [_P, _P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_build_messages_bwd": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _SZ, _P],
+    "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_workspace_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
+    "mtgnn_save_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
+    "mtgnn_status_string": [C.c_int],
+    "mtgnn_last_error": [],
+    "mtgnn_version": [],
+}
+_RES = {"mtgnn_workspace_bytes": _SZ, "mtgnn_save_bytes": _SZ, "mtgnn_status_string": C.c_char_p,
+        "mtgnn_last_error": C.c_char_p, "mtgnn_version": C.c_int}
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load the in-tree libmtgnn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise MtgnnError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = C.CDLL(LIB_PATH)
+        for name, args in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = _RES.get(name, C.c_int)
+        _lib = L
+    return _lib
+
+
+def _check(status: int, name: str):
+    if status != 0:
+        L = lib()
+        raise MtgnnError(f"{name}: {L.mtgnn_status_string(status).decode()} "
+                         f"({L.mtgnn_last_error().decode()})")
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+_DT = {F32: torch.float32, BF16: torch.bfloat16}
+
+
+def _ptr(t, dtype=None, name="tensor", optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise MtgnnError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise MtgnnError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise MtgnnError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise MtgnnError(f"{name} must be contiguous")
+    return C.c_void_p(t.data_ptr())
+
+
+def _ws(ws):
+    if ws is None:
+        return None, 0
+    return _ptr(ws, torch.uint8, "ws"), ws.numel()
+
+
+def dims(n_nodes, d_mem, d_time, d_edge, d_attn, n_heads, k, dtype=F32) -> Dims:
+    return Dims(int(n_nodes), int(d_mem), int(d_time), int(d_edge), int(d_attn), int(n_heads), int(k), int(dtype))
+
+
+def batch(src, dst, t, eid=None, flags=None) -> Batch:
+    n = int(src.numel())
+    return Batch(n, _ptr(src, torch.int32, "src"), _ptr(dst, torch.int32, "dst"),
+                 _ptr(eid, torch.int32, "eid", optional=True), _ptr(t, torch.float32, "t"),
+                 _ptr(flags, torch.uint8, "flags", optional=True))
+
+
+def workspace_bytes(op, d: Dims = None, max_rows=0, max_q=0) -> int:
+    return int(lib().mtgnn_workspace_bytes(op, C.byref(d) if d is not None else None, int(max_rows), int(max_q)))
+
+
+def save_bytes(op, d: Dims, max_rows=0, max_q=0) -> int:
+    return int(lib().mtgnn_save_bytes(op, C.byref(d), int(max_rows), int(max_q)))
+
+
+def alloc_bytes(n, device="cuda"):
+    return torch.empty(max(int(n), 1), dtype=torch.uint8, device=device)
+
+
+# ----------------------------------------------------------------------------- entry points
+
+def mtgnn_build_queries(b: Batch, neg, q_node, q_t, n_q, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_build_queries(C.byref(b), _ptr(neg, torch.int32, "neg"), _ptr(q_node, torch.int32, "q_node"),
+                                     _ptr(q_t, torch.float32, "q_t"), _ptr(n_q, torch.int32, "n_q"), wp, wb,
+                                     _stream(stream)), "mtgnn_build_queries")
+
+
+def mtgnn_aggregate_last(b: Batch, n_nodes, uniq, winner, n_uniq, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_aggregate_last(C.byref(b), int(n_nodes), _ptr(uniq, torch.int32, "uniq"),
+                                      _ptr(winner, torch.int32, "winner"), _ptr(n_uniq, torch.int32, "n_uniq"), wp, wb,
+                                      _stream(stream)), "mtgnn_aggregate_last")
+
+
+def mtgnn_build_messages(b: Batch, uniq, winner, n_rows, max_rows, memory, last_update, edge_feat, time_w, time_b,
+                         d: Dims, msg, dt, stream=None):
+    md = _DT[d.dtype]
+    _check(lib().mtgnn_build_messages(C.byref(b), _ptr(uniq, torch.int32, "uniq"), _ptr(winner, torch.int32, "winner"),
+                                      _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows),
+                                      _ptr(memory, md, "memory"), _ptr(last_update, torch.float32, "last_update"),
+                                      _ptr(edge_feat, torch.float32, "edge_feat", True),
+                                      _ptr(time_w, torch.float32, "time_w"), _ptr(time_b, torch.float32, "time_b"),
+                                      C.byref(d), _ptr(msg, md, "msg"), _ptr(dt, torch.float32, "dt"),
+                                      _stream(stream)), "mtgnn_build_messages")
+
+
+def mtgnn_gru_update(b: Batch, uniq, winner, n_rows, max_rows, msg, W_ih, W_hh, b_ih, b_hh, d: Dims, memory,
+                     last_update, save, ws, stream=None):
+    md = _DT[d.dtype]
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_gru_update(C.byref(b), _ptr(uniq, torch.int32, "uniq"), _ptr(winner, torch.int32, "winner"),
+                                  _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows), _ptr(msg, md, "msg"),
+                                  _ptr(W_ih, md, "W_ih"), _ptr(W_hh, md, "W_hh"), _ptr(b_ih, torch.float32, "b_ih"),
+                                  _ptr(b_hh, torch.float32, "b_hh"), C.byref(d), _ptr(memory, md, "memory"),
+                                  _ptr(last_update, torch.float32, "last_update"),
+                                  _ptr(save, torch.uint8, "save", True), wp, wb, _stream(stream)), "mtgnn_gru_update")
+
+
+def mtgnn_sample_recent(csr_off, csr_nbr, csr_t, csr_eid, n_nodes, q_node, q_t, n_q, max_q, k, out_nbr, out_t,
+                        out_eid, stream=None):
+    _check(lib().mtgnn_sample_recent(_ptr(csr_off, torch.int64, "csr_off"), _ptr(csr_nbr, torch.int32, "csr_nbr"),
+                                     _ptr(csr_t, torch.float32, "csr_t"), _ptr(csr_eid, torch.int32, "csr_eid"),
+                                     int(n_nodes), _ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"),
+                                     _ptr(n_q, torch.int32, "n_q", True), int(max_q), int(k),
+                                     _ptr(out_nbr, torch.int32, "out_nbr"), _ptr(out_t, torch.float32, "out_t"),
+                                     _ptr(out_eid, torch.int32, "out_eid"), _stream(stream)), "mtgnn_sample_recent")
+
+
+def attn_params(p: dict, d: Dims) -> AttnParams:
+    md = _DT[d.dtype]
+    return AttnParams(*[_ptr(p[n], md if n.startswith("W") else torch.float32, n) for n in _ATTN])
+
+
+def attn_grads(g: dict) -> AttnGrads:
+    return AttnGrads(*[_ptr(g[n], torch.float32, "d" + n) for n in _ATTN])
+
+
+def mtgnn_temporal_attn(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b,
+                        params: AttnParams, d: Dims, z, save, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_temporal_attn(_ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"),
+                                     _ptr(n_q, torch.int32, "n_q", True), int(max_q), _ptr(nbr, torch.int32, "nbr"),
+                                     _ptr(nt, torch.float32, "nt"), _ptr(neid, torch.int32, "neid"),
+                                     _ptr(memory, _DT[d.dtype], "memory"),
+                                     _ptr(edge_feat, torch.float32, "edge_feat", True),
+                                     _ptr(time_w, torch.float32, "time_w"), _ptr(time_b, torch.float32, "time_b"),
+                                     C.byref(params), C.byref(d), _ptr(z, torch.float32, "z"),
+                                     _ptr(save, torch.uint8, "save"), wp, wb, _stream(stream)), "mtgnn_temporal_attn")
+
+
+def mtgnn_temporal_attn_bwd(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b,
+                            params: AttnParams, d: Dims, grads: AttnGrads, d_mem, d_time_w, d_time_b, ws,
+                            stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_temporal_attn_bwd(_ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"),
+                                         _ptr(n_q, torch.int32, "n_q", True), int(max_q),
+                                         _ptr(nbr, torch.int32, "nbr"), _ptr(nt, torch.float32, "nt"),
+                                         _ptr(dz, torch.float32, "dz"), _ptr(save, torch.uint8, "save"),
+                                         _ptr(uniq, torch.int32, "uniq", True), _ptr(n_rows, torch.int32, "n_rows", True),
+                                         int(max_rows), _ptr(time_w, torch.float32, "time_w"),
+                                         _ptr(time_b, torch.float32, "time_b"), C.byref(params), C.byref(d),
+                                         C.byref(grads), _ptr(d_mem, torch.float32, "d_mem", True),
+                                         _ptr(d_time_w, torch.float32, "d_time_w"),
+                                         _ptr(d_time_b, torch.float32, "d_time_b"), wp, wb, _stream(stream)),
+           "mtgnn_temporal_attn_bwd")
+
+
+def mtgnn_gru_update_bwd(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d: Dims, dW_ih, dW_hh, db_ih, db_hh,
+                         dmsg_time, ws, stream=None):
+    md = _DT[d.dtype]
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_gru_update_bwd(_ptr(d_mem, torch.float32, "d_mem"), _ptr(save, torch.uint8, "save"),
+                                      _ptr(msg, md, "msg"), _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows),
+                                      _ptr(W_ih, md, "W_ih"), _ptr(W_hh, md, "W_hh"), C.byref(d),
+                                      _ptr(dW_ih, torch.float32, "dW_ih"), _ptr(dW_hh, torch.float32, "dW_hh"),
+                                      _ptr(db_ih, torch.float32, "db_ih"), _ptr(db_hh, torch.float32, "db_hh"),
+                                      _ptr(dmsg_time, torch.float32, "dmsg_time", True), wp, wb, _stream(stream)),
+           "mtgnn_gru_update_bwd")
+
+
+def mtgnn_build_messages_bwd(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d: Dims, d_time_w, d_time_b, ws,
+                             stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_build_messages_bwd(_ptr(dmsg_time, torch.float32, "dmsg_time"), _ptr(dt, torch.float32, "dt"),
+                                          _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows),
+                                          _ptr(time_w, torch.float32, "time_w"), _ptr(time_b, torch.float32, "time_b"),
+                                          C.byref(d), _ptr(d_time_w, torch.float32, "d_time_w"),
+                                          _ptr(d_time_b, torch.float32, "d_time_b"), wp, wb, _stream(stream)),
+           "mtgnn_build_messages_bwd")
+
+
+def mtgnn_build_temporal_csr(src, dst, t, n_nodes, csr_off, csr_nbr, csr_t, csr_eid, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_build_temporal_csr(_ptr(src, torch.int32, "src"), _ptr(dst, torch.int32, "dst"),
+                                          _ptr(t, torch.float32, "t"), int(src.numel()), int(n_nodes),
+                                          _ptr(csr_off, torch.int64, "csr_off"), _ptr(csr_nbr, torch.int32, "csr_nbr"),
+                                          _ptr(csr_t, torch.float32, "csr_t"), _ptr(csr_eid, torch.int32, "csr_eid"),
+                                          wp, wb, _stream(stream)), "mtgnn_build_temporal_csr")

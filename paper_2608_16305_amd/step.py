@@ -1,0 +1,145 @@
+"""Device-resident state and buffers for the batch step, driven through the C ABI.
+
+A step on batch b (default lag-1 order) runs
+  memory phase on batch b-1:  aggregate_last -> build_messages -> gru_update
+  embedding on batch b:       build_queries  -> sample_recent  -> temporal_attn
+  backward:                   temporal_attn_bwd -> gru_update_bwd -> build_messages_bwd
+all enqueued on one HIP stream with no host synchronisation: the only
+data-dependent sizes (updated rows, queries) stay in device memory.
+"""
+
+import numpy as np
+import torch
+
+from . import mtgnn as M
+
+ATTN_W = ("W_q", "W_k", "W_v", "W_o", "W_1", "W_2")
+ATTN_B = ("b_q", "b_k", "b_v", "b_o", "b_1", "b_2")
+
+
+class TGNStep:
+    def __init__(self, w, stream, params: dict, memory: np.ndarray, last_update: np.ndarray, device="cuda",
+                 lag: int = 1, torch_stream=None):
+        self.w = w
+        self.lag = lag
+        self.dev = torch.device(device)
+        self.ts = torch_stream
+        self.dtype_code = M.BF16 if w.dtype == "bf16" else M.F32
+        self.sdt = torch.bfloat16 if self.dtype_code == M.BF16 else torch.float32
+        self.d = M.dims(w.n_nodes, w.d_mem, w.d_time, w.d_edge, w.d_attn, w.n_heads, w.k, self.dtype_code)
+        dev = self.dev
+        E = stream.n_events
+        self.n_events = E
+        # stream (resident in HBM)
+        self.src = torch.from_numpy(stream.src).to(dev)
+        self.dst = torch.from_numpy(stream.dst).to(dev)
+        self.t = torch.from_numpy(stream.t).to(dev)
+        self.neg = torch.from_numpy(stream.neg).to(dev)
+        self.eid = torch.arange(E, dtype=torch.int32, device=dev)
+        self.x = torch.from_numpy(stream.x).to(dev) if w.d_edge > 0 else None
+        self.flags = torch.from_numpy(stream.flags).to(dev) if stream.flags is not None else None
+        # parameters: weights in the storage dtype, biases and time encoder in float32
+        self.params = {}
+        for k, v in params.items():
+            tv = torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+            self.params[k] = tv.to(self.sdt) if k.startswith("W") else tv.float()
+        self.memory = torch.from_numpy(np.ascontiguousarray(memory)).to(dev).to(self.sdt).contiguous()
+        self.last_update = torch.from_numpy(np.ascontiguousarray(last_update, np.float32)).to(dev)
+        # temporal adjacency, built once on the device
+        N = w.n_nodes
+        self.csr_off = torch.empty(N + 1, dtype=torch.int64, device=dev)
+        self.csr_nbr = torch.empty(max(2 * E, 1), dtype=torch.int32, device=dev)
+        self.csr_t = torch.empty(max(2 * E, 1), dtype=torch.float32, device=dev)
+        self.csr_eid = torch.empty(max(2 * E, 1), dtype=torch.int32, device=dev)
+        ws = M.alloc_bytes(M.workspace_bytes(M.OP_BUILD_CSR, self.d, E, 0), dev)
+        M.mtgnn_build_temporal_csr(self.src, self.dst, self.t, N, self.csr_off, self.csr_nbr, self.csr_t,
+                                   self.csr_eid, ws, stream=self.ts)
+        del ws
+        self._alloc(w.batch)
+
+    # ------------------------------------------------------------------ buffers
+    def _alloc(self, B):
+        dev, w, d = self.dev, self.w, self.d
+        self.B = B
+        self.max_rows = 2 * B
+        self.max_q = 3 * B
+        R, Q, k = self.max_rows, self.max_q, w.k
+        i32 = dict(dtype=torch.int32, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.uniq = torch.empty(R, **i32)
+        self.winner = torch.empty(R, **i32)
+        self.n_uniq = torch.zeros(1, **i32)
+        self.msg = torch.empty(R, w.d_msg, dtype=self.sdt, device=dev)
+        self.dt = torch.empty(R, **f32)
+        self.gru_save = M.alloc_bytes(M.save_bytes(M.OP_GRU_UPDATE, d, R, 0), dev)
+        self.q_node = torch.empty(Q, **i32)
+        self.q_t = torch.empty(Q, **f32)
+        self.n_q = torch.zeros(1, **i32)
+        self.nbr = torch.empty(Q, k, **i32)
+        self.nt = torch.empty(Q, k, **f32)
+        self.neid = torch.empty(Q, k, **i32)
+        self.z = torch.empty(Q, w.d_attn, **f32)
+        self.attn_save = M.alloc_bytes(M.save_bytes(M.OP_TEMPORAL_ATTN, d, 0, Q), dev)
+        self.d_mem = torch.empty(R, w.d_mem, **f32)
+        self.dmsg_time = torch.empty(R, max(w.d_time, 1), **f32)
+        self.grads = {n: torch.empty(tuple(self.params[n].shape), **f32)
+                      for n in list(ATTN_W) + list(ATTN_B) + ["W_ih", "W_hh", "b_ih", "b_hh", "time_w", "time_b"]}
+        ops = [(M.OP_BUILD_QUERIES, B, 0), (M.OP_AGGREGATE_LAST, B, 0), (M.OP_GRU_UPDATE, R, 0),
+               (M.OP_TEMPORAL_ATTN, 0, Q), (M.OP_TEMPORAL_ATTN_BWD, R, Q), (M.OP_GRU_UPDATE_BWD, R, 0),
+               (M.OP_BUILD_MESSAGES_BWD, R, 0)]
+        need = max(M.workspace_bytes(op, d, r, q) for op, r, q in ops)
+        self.ws = M.alloc_bytes(need, dev)   # the calls of one step run in stream order and share it
+        self.ap = M.attn_params(self.params, d)
+        self.ag = M.attn_grads(self.grads)
+
+    def _batch(self, lo, hi):
+        if hi <= lo:
+            return M.Batch(0, None, None, None, None, None)
+        f = self.flags[lo:hi] if self.flags is not None else None
+        return M.batch(self.src[lo:hi], self.dst[lo:hi], self.t[lo:hi], self.eid[lo:hi], f)
+
+    # ------------------------------------------------------------------ phases
+    def memory_phase(self, lo, hi, save=True):
+        b = self._batch(lo, hi)
+        p, s = self.params, self.ts
+        M.mtgnn_aggregate_last(b, self.w.n_nodes, self.uniq, self.winner, self.n_uniq, self.ws, stream=s)
+        M.mtgnn_build_messages(b, self.uniq, self.winner, self.n_uniq, self.max_rows, self.memory, self.last_update,
+                               self.x, p["time_w"], p["time_b"], self.d, self.msg, self.dt, stream=s)
+        M.mtgnn_gru_update(b, self.uniq, self.winner, self.n_uniq, self.max_rows, self.msg, p["W_ih"], p["W_hh"],
+                           p["b_ih"], p["b_hh"], self.d, self.memory, self.last_update,
+                           self.gru_save if save else None, self.ws, stream=s)
+
+    def embed(self, lo, hi):
+        b = self._batch(lo, hi)
+        p, s = self.params, self.ts
+        M.mtgnn_build_queries(b, self.neg[lo:hi], self.q_node, self.q_t, self.n_q, self.ws, stream=s)
+        M.mtgnn_sample_recent(self.csr_off, self.csr_nbr, self.csr_t, self.csr_eid, self.w.n_nodes, self.q_node,
+                              self.q_t, self.n_q, self.max_q, self.w.k, self.nbr, self.nt, self.neid, stream=s)
+        M.mtgnn_temporal_attn(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, self.neid, self.memory,
+                              self.x, p["time_w"], p["time_b"], self.ap, self.d, self.z, self.attn_save, self.ws,
+                              stream=s)
+
+    def backward(self, dz):
+        p, g, s = self.params, self.grads, self.ts
+        M.mtgnn_temporal_attn_bwd(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz, self.attn_save,
+                                  self.uniq, self.n_uniq, self.max_rows, p["time_w"], p["time_b"], self.ap, self.d,
+                                  self.ag, self.d_mem, g["time_w"], g["time_b"], self.ws, stream=s)
+        M.mtgnn_gru_update_bwd(self.d_mem, self.gru_save, self.msg, self.n_uniq, self.max_rows, p["W_ih"], p["W_hh"],
+                               self.d, g["W_ih"], g["W_hh"], g["b_ih"], g["b_hh"], self.dmsg_time, self.ws, stream=s)
+        M.mtgnn_build_messages_bwd(self.dmsg_time, self.dt, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],
+                                   self.d, g["time_w"], g["time_b"], self.ws, stream=s)
+
+    def batch_range(self, b):
+        lo = b * self.B
+        return lo, min(self.n_events, lo + self.B)
+
+    def step(self, b, dz):
+        """One training step on batch b: memory phase (lag order), embedding, backward."""
+        elo, ehi = self.batch_range(b)
+        if self.lag == 1:
+            mlo, mhi = self.batch_range(b - 1) if b > 0 else (0, 0)
+        else:
+            mlo, mhi = elo, ehi
+        self.memory_phase(mlo, mhi)
+        self.embed(elo, ehi)
+        self.backward(dz)

@@ -1,0 +1,135 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integer outputs (updated rows, winners, queries, sampled neighbours, event
+ids, copied times, last_update, untouched memory rows) must be bit-exact.
+Floating-point tensors must satisfy max|gpu - oracle| / max|oracle| <= 1e-4
+for float32 storage and <= 2e-2 for bfloat16 storage.  Each oracle step
+starts from the GPU's state before that step (teacher forcing).
+"""
+
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import tgn
+from synth import init_params, make_stream, window_state, workload
+from tests._gpu import compare_step, log, needs_gpu, to_np
+from tests._tiny import random_state, tiny_stream, tiny_workload
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def _runner(w, s, params, mem, lu, lag=1):
+    from paper_2608_16305_amd.step import TGNStep
+    return TGNStep(w, s, params, mem, lu, lag=lag)
+
+
+def _check_csr(runner, s, n_nodes):
+    adj = tgn.build_adjacency(s.src, s.dst, s.t, n_nodes)
+    assert np.array_equal(runner.csr_off.cpu().numpy(), adj.off)
+    ne = 2 * s.n_events
+    assert np.array_equal(runner.csr_nbr.cpu().numpy()[:ne], adj.nbr)
+    assert np.array_equal(runner.csr_eid.cpu().numpy()[:ne], adj.eid)
+    assert np.array_equal(runner.csr_t.cpu().numpy()[:ne].view(np.uint32), adj.t.view(np.uint32))
+    return adj
+
+
+@pytest.mark.parametrize("cid", [1, 2])
+def test_full_stream_steps(cid):
+    """Workloads 1-2 from an empty memory (M = 0, last_update = 0), steps 0..4, lag-1 order."""
+    w = workload(cid)
+    log(f"[parity] workload {cid} {w.name}")
+    s = make_stream(w)
+    params = init_params(w, random_bias=True)
+    r = _runner(w, s, params, np.zeros((w.n_nodes, w.d_mem), np.float32), np.zeros(w.n_nodes, np.float32))
+    adj = _check_csr(r, s, w.n_nodes)
+    for b in range(5):
+        compare_step(r, w, s, adj, b, TOL[w.dtype])
+
+
+def test_workload1_lag0_order():
+    w = workload(1)
+    s = make_stream(w)
+    params = init_params(w, random_bias=True)
+    mem, lu = random_state(w, seed=5)
+    r = _runner(w, s, params, mem, np.zeros(w.n_nodes, np.float32), lag=0)
+    adj = tgn.build_adjacency(s.src, s.dst, s.t, w.n_nodes)
+    for b in (0, 1, 7):
+        compare_step(r, w, s, adj, b, TOL[w.dtype], lag=0)
+
+
+def test_workload3_window():
+    """Skewed Zipf(1.2) stream, 1M nodes / 10M events, mid-stream window at batch 100 (hub lists of 1e5+ entries)."""
+    w = workload(3)
+    log("[parity] workload 3 window")
+    s = make_stream(w)
+    params = init_params(w, random_bias=True)
+    mem, lu = window_state(w, s, w.window_b0)
+    r = _runner(w, s, params, mem, lu)
+    adj = _check_csr(r, s, w.n_nodes)
+    for b in range(w.window_b0, w.window_b0 + 3):
+        compare_step(r, w, s, adj, b, TOL[w.dtype])
+
+
+# ----------------------------------------------------------------------------- edge cases
+
+def _tiny_run(w, s, mem, lu, steps, lag=1):
+    params = init_params(w, random_bias=True)
+    r = _runner(w, s, params, mem, lu, lag=lag)
+    adj = _check_csr(r, s, w.n_nodes)
+    out = []
+    for b in steps:
+        out.append(compare_step(r, w, s, adj, b, TOL[w.dtype], lag=lag))
+    return r, out
+
+
+def test_edge_ties_self_loops_k_beyond_degree():
+    """Timestamp ties, self-loops, and k larger than most neighbour lists (padding)."""
+    w = tiny_workload(n_nodes=9, n_events=90, batch=10, k=8, d_mem=6, d_time=5, d_edge=3, d_attn=8, n_heads=2)
+    s = tiny_stream(w, seed=3, tie_every=3)
+    assert (s.src == s.dst).any()
+    mem, lu = random_state(w, seed=1)
+    _tiny_run(w, s, mem, lu, range(0, 9))
+
+
+def test_edge_masks_replay_pruned():
+    """Replay events update memory but get no query; pruned events do nothing; zero-target batches."""
+    w = tiny_workload(n_nodes=12, n_events=120, batch=12, k=4, d_mem=8, d_time=4, d_edge=0, d_attn=8, n_heads=2)
+    s = tiny_stream(w, seed=4, flags_p=(0.4, 0.3))
+    s.flags[24:36] = 3          # batch 2: every event pruned -> memory phase of step 3 changes nothing
+    s.flags[48:60] = 1          # batch 4: replay only -> no query at step 4
+    mem, lu = random_state(w, seed=2)
+    r, out = _tiny_run(w, s, mem, lu, range(1, 10))
+    gpu3, ref3 = out[2]          # step 3 runs the memory phase on batch 2
+    assert gpu3["n_uniq"] == 0
+    gpu4, ref4 = out[3]          # step 4 embeds batch 4
+    assert gpu4["n_q"] == 0
+    assert all(np.abs(g).max() == 0 for k, g in gpu4["grads"].items())
+
+
+def test_edge_batch_of_one():
+    w = tiny_workload(n_nodes=5, n_events=30, batch=1, k=3, d_mem=4, d_time=3, d_edge=2, d_attn=4, n_heads=1)
+    s = tiny_stream(w, seed=6)
+    mem, lu = random_state(w, seed=3)
+    _tiny_run(w, s, mem, lu, range(0, 12))
+
+
+def test_edge_ragged_tiles():
+    """Sizes that are not multiples of any tile: 37 events per batch, d_mem 37, d_attn 30 with 3 heads."""
+    w = tiny_workload(n_nodes=61, n_events=600, batch=37, k=7, d_mem=37, d_time=11, d_edge=5, d_attn=30, n_heads=3)
+    s = tiny_stream(w, seed=8, t_scale=300.0, tie_every=5)
+    mem, lu = random_state(w, seed=4)
+    _tiny_run(w, s, mem, lu, range(0, 6))
+
+
+def test_bf16_small():
+    w = tiny_workload(n_nodes=50, n_events=800, batch=80, k=6, d_mem=16, d_time=8, d_edge=0, d_attn=16, n_heads=2)
+    w = replace(w, dtype="bf16")
+    s = tiny_stream(w, seed=9, t_scale=100.0, flags_p=(0.25, 0.1))
+    mem, lu = random_state(w, seed=5)
+    from oracle.bf16 import round_bf16
+    _tiny_run(w, s, round_bf16(mem), lu, range(1, 6))
