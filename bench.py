@@ -1,0 +1,207 @@
+"""Benchmark of the memory-based TGNN batch step on one MI355X.
+
+One step = the whole hot path over one batch: memory phase on the previous
+batch (most-recent aggregation, message construction, GRU update with
+write-back), embedding of the current batch's target events (queries,
+most-recent-k sampling, temporal attention), and the backward pass (attention,
+GRU, time encoder).  Inputs (event stream, temporal adjacency, memory table,
+parameters, loss gradients) are resident in HBM before the timed region.
+
+Default workload: the skewed stream (1M nodes, 10M events, Zipf(1.2) endpoints,
+batch 4,000, k = 10, memory/time/attention width 100, 2 heads, float32),
+mid-stream window starting at batch 100.
+
+Prints one JSON line.  `python bench.py --gpus N --steps K --warmup W`.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_PEAK_TFLOPS = 157.3       # MI355X dense fp32 matrix
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for the CPU baseline (0: skip)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the multi-GPU sharding is described, not built.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_16305_amd.step import TGNStep
+    from synth import init_params, loss_noise, make_stream, window_state, workload
+
+    w = workload(args.workload)
+    s = make_stream(w)
+    params = init_params(w)
+    b0 = w.window_b0
+    mem, lu = window_state(w, s, b0)
+    n_steps = args.warmup + args.steps
+    if b0 + n_steps > w.n_batches:
+        raise SystemExit(f"window [{b0}, {b0 + n_steps}) exceeds the {w.n_batches} batches of the stream")
+    runner = TGNStep(w, s, params, mem, lu)
+
+    # per-step loss gradients dZ = G / n_tar (masked loss), resident before timing
+    dzs, n_tar = [], []
+    for i in range(n_steps):
+        b = b0 + i
+        lo, hi = b * w.batch, min(w.n_events, (b + 1) * w.batch)
+        nt = (hi - lo) if s.flags is None else int(((s.flags[lo:hi] & 3) == 0).sum())
+        G = loss_noise(w, b, runner.max_q)
+        dzs.append(torch.from_numpy((G / max(nt, 1)).astype(np.float32)).cuda())
+        n_tar.append(nt)
+    torch.cuda.synchronize()
+
+    from paper_2608_16305_amd import mtgnn as M
+
+    # warmup; the matrix-product sites over the neighbour slots are timed one
+    # warmup step each to pick the dominant one
+    site_ms = {}
+    for i in range(args.warmup):
+        site = HOT_SITES[i % len(HOT_SITES)] if i >= 1 else None
+        if site:
+            M.timer_start(site, 16)
+        runner.step(b0 + i, dzs[i])
+        if site:
+            ms, n = M.timer_stop()
+            site_ms[site] = max(site_ms.get(site, 0.0), ms)
+    torch.cuda.synchronize()
+    dominant = max(site_ms, key=site_ms.get) if site_ms else HOT_SITES[0]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    M.timer_start(dominant, 16 * args.steps)
+    t0 = time.perf_counter()
+    ev0.record()
+    for i in range(args.warmup, n_steps):
+        runner.step(b0 + i, dzs[i])
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dom_ms, dom_launches = M.timer_stop()
+    gpu_ms = ev0.elapsed_time(ev1)
+    ms_per_step = gpu_ms / args.steps
+    events = w.batch * args.steps
+    value = events / (gpu_ms / 1e3)
+    target_events = sum(n_tar[args.warmup:])
+
+    out = {
+        "metric": "events/sec per batch step (fwd+bwd) on 1 MI355X",
+        "value": value,
+        "unit": "events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "target_events_per_s": target_events / (gpu_ms / 1e3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n_nodes": w.n_nodes, "n_events": w.n_events, "batch": w.batch, "k": w.k,
+                   "d_mem": w.d_mem, "d_time": w.d_time, "d_edge": w.d_edge, "d_attn": w.d_attn,
+                   "n_heads": w.n_heads, "first_batch": b0, "order": "lag-1"},
+    }
+
+    # algorithmic work of the dominant kernel: valid neighbour slots of the timed steps
+    valid_pairs = 0
+    for i in range(args.warmup, n_steps):
+        b = b0 + i
+        valid_pairs += valid_slots(runner, s, w, b)
+    launches_per_step = dom_launches / args.steps
+    # every launch of a hot site covers all valid slots of its step (K and V share one launch)
+    per_launch_pairs = valid_pairs / args.steps / max(launches_per_step, 1.0)
+    flops = 2.0 * per_launch_pairs * SITE_K(dominant, w) * SITE_N(dominant, w)
+    avg_s = dom_ms / 1e3 / max(dom_launches, 1)
+    peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
+    achieved = flops / avg_s / 1e12
+    out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                       "frac": achieved / peak, "traffic": None, "kernel": dominant,
+                       "launches_per_step": launches_per_step, "avg_launch_us": avg_s * 1e6,
+                       "flops_per_launch": flops}
+
+    if args.cpu_steps > 0:
+        out["cpu_baseline"] = cpu_baseline(w, s, params, mem, lu, b0, args.cpu_steps)
+    print(json.dumps(out), flush=True)
+
+
+# Matrix-product call sites over the neighbour slots (the largest products of the step).
+HOT_SITES = ("gemm_kv_proj", "gemm_kv_dw", "gemm_kv_dx")
+
+
+def SITE_K(site, w):
+    """Reduction length per neighbour slot of each hot site's product."""
+    return {"gemm_kv_proj": w.d_kv, "gemm_kv_dw": 2 * w.d_attn, "gemm_kv_dx": 2 * w.d_attn}[site]
+
+
+def SITE_N(site, w):
+    """Output width: K|V (2 d_attn), [dW_k; dW_v] (d_kv per row of 2 d_attn), dphi (d_time)."""
+    return {"gemm_kv_proj": 2 * w.d_attn, "gemm_kv_dw": w.d_kv, "gemm_kv_dx": w.d_time}[site]
+
+
+def valid_slots(runner, s, w, b):
+    """Non-padded neighbour slots of step b's queries (recomputed on the host from the
+    device-built adjacency, outside the timed region)."""
+    import torch
+    elo, ehi = runner.batch_range(b)
+    tar = np.ones(ehi - elo, bool) if s.flags is None else (s.flags[elo:ehi] & 3) == 0
+    q_node = np.concatenate([s.src[elo:ehi][tar], s.dst[elo:ehi][tar], s.neg[elo:ehi][tar]]).astype(np.int64)
+    q_t = np.tile(s.t[elo:ehi][tar], 3)
+    off = runner.csr_off.cpu().numpy() if not hasattr(runner, "_off_np") else runner._off_np
+    runner._off_np = off
+    if not hasattr(runner, "_csr_t_np"):
+        runner._csr_t_np = runner.csr_t.cpu().numpy()
+    ct = runner._csr_t_np
+    cnt = 0
+    for n, tau in zip(q_node, q_t):
+        lo, hi = off[n], off[n + 1]
+        cnt += min(w.k, int(np.searchsorted(ct[lo:hi], tau, side="left")))
+    return cnt
+
+
+def cpu_baseline(w, s, params, mem, lu, b0, n):
+    """The oracle (unchanged) on the host cores, over the first n steps of the same window."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import tgn
+    from synth import loss_noise
+    adj = tgn.build_adjacency(s.src, s.dst, s.t, w.n_nodes)
+    prec = tgn.Prec("bf16" if w.dtype == "bf16" else "f32")
+    m, l = mem.copy(), lu.copy()
+    t0 = time.perf_counter()
+    for i in range(n):
+        b = b0 + i
+        mb = tgn.batch_dict(s, (b - 1) * w.batch, b * w.batch)
+        eb = tgn.batch_dict(s, b * w.batch, (b + 1) * w.batch)
+        r = tgn.step(prec, w, m, l, params, adj, s.x, mb, eb, loss_noise(w, b, 3 * w.batch))
+        m, l = r.mp.mem, r.mp.lu
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": w.batch * n / dt, "unit": "events/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} consecutive steps from batch {b0} of the same workload ({w.batch * n} events), "
+                      f"float64 NumPy oracle, {os.cpu_count()} host CPUs visible"}
+
+
+if __name__ == "__main__":
+    main()

@@ -261,6 +261,18 @@ mtgnn_status mtgnn_build_temporal_csr(const int32_t* src, const int32_t* dst, co
                                       int64_t n_nodes, int64_t* csr_off, int32_t* csr_nbr, float* csr_t,
                                       int32_t* csr_eid, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Launch timer (instrumentation for benchmarks; not part of the step).
+ * mtgnn_timer_start arms it: each of the next `max_launches` launches whose
+ * timer name equals `kernel` is bracketed by HIP events recorded on the
+ * stream of that launch.  The names are the call-site names of the
+ * matrix-product kernels ("gemm_kv_proj", "gemm_kv_dw", "gemm_kv_dx", "gemm")
+ * and the function names of the other kernels (e.g. "k_attn_core").
+ * mtgnn_timer_stop waits for the recorded events (host-blocking), returns
+ * the summed duration in milliseconds and the number of timed launches, and
+ * disarms the timer.  Host-side state: use from one host thread. */
+mtgnn_status mtgnn_timer_start(const char* kernel, int max_launches);
+mtgnn_status mtgnn_timer_stop(double* total_ms, int* launches);
+
 /* Human-readable name of a status code (static storage). */
 const char* mtgnn_status_string(int status);
 

@@ -1,6 +1,7 @@
 // C ABI of the mtgnn library: argument validation (host only, before any HIP
 // call), workspace sizing, status strings, and dispatch to the step kernels.
 #include <string>
+#include <vector>
 
 #include "ops.h"
 
@@ -15,6 +16,23 @@ void set_hip_error(hipError_t e, const char* where) {
 static mtgnn_status fail(mtgnn_status s, const char* what) {
   g_err = what;
   return s;
+}
+
+// ------------------------------------------------------------------ launch timer state
+
+bool g_timer_armed = false;
+static std::string g_timer_name;
+static std::vector<hipEvent_t> g_timer_events;
+static int g_timer_used = 0;
+
+bool timer_begin(const char* name, hipStream_t s) {
+  if (g_timer_used * 2 + 1 >= (int)g_timer_events.size() || g_timer_name != name) return false;
+  return hipEventRecord(g_timer_events[2 * g_timer_used], s) == hipSuccess;
+}
+
+void timer_end(hipStream_t s) {
+  (void)hipEventRecord(g_timer_events[2 * g_timer_used + 1], s);
+  ++g_timer_used;
 }
 
 // Limits of this implementation (beyond them: MTGNN_EUNSUPPORTED).
@@ -70,6 +88,50 @@ const char* mtgnn_status_string(int status) {
 }
 
 const char* mtgnn_last_error(void) { return g_err.c_str(); }
+
+mtgnn_status mtgnn_timer_start(const char* kernel, int max_launches) {
+  if (!kernel || max_launches <= 0 || max_launches > (1 << 20)) return fail(MTGNN_EINVAL, "timer arguments");
+  if (g_timer_armed) return fail(MTGNN_EINVAL, "timer already running");
+  g_timer_events.assign(2 * (size_t)max_launches, nullptr);
+  for (auto& e : g_timer_events) {
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) {
+      set_hip_error(err, "hipEventCreate");
+      for (auto& x : g_timer_events)
+        if (x) (void)hipEventDestroy(x);
+      g_timer_events.clear();
+      return MTGNN_EHIP;
+    }
+  }
+  g_timer_name = kernel;
+  g_timer_used = 0;
+  g_timer_armed = true;
+  return MTGNN_OK;
+}
+
+mtgnn_status mtgnn_timer_stop(double* total_ms, int* launches) {
+  if (!g_timer_armed) return fail(MTGNN_EINVAL, "timer not running");
+  g_timer_armed = false;
+  double tot = 0.0;
+  mtgnn_status st = MTGNN_OK;
+  for (int i = 0; i < g_timer_used; ++i) {
+    float ms = 0.f;
+    hipError_t err = hipEventSynchronize(g_timer_events[2 * i + 1]);
+    if (err == hipSuccess) err = hipEventElapsedTime(&ms, g_timer_events[2 * i], g_timer_events[2 * i + 1]);
+    if (err != hipSuccess) {
+      set_hip_error(err, "timer events");
+      st = MTGNN_EHIP;
+      break;
+    }
+    tot += ms;
+  }
+  for (auto& e : g_timer_events) (void)hipEventDestroy(e);
+  g_timer_events.clear();
+  if (total_ms) *total_ms = tot;
+  if (launches) *launches = g_timer_used;
+  g_timer_used = 0;
+  return st;
+}
 
 size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int64_t max_q) {
   if (max_rows < 0 || max_q < 0) return 0;

@@ -30,6 +30,25 @@ void set_hip_error(hipError_t e, const char* where);
     if (_s != MTGNN_OK) return _s;                                 \
   } while (0)
 
+// ------------------------------------------------------------------ launch timer (instrumentation)
+
+// When armed through mtgnn_timer_start(name, n), the next n launches whose
+// timer name equals `name` are bracketed by HIP events on their stream.
+extern bool g_timer_armed;
+bool timer_begin(const char* name, hipStream_t s);
+void timer_end(hipStream_t s);
+
+struct TimedScope {
+  bool on = false;
+  hipStream_t s;
+  TimedScope(const char* name, hipStream_t st) : s(st) {
+    if (g_timer_armed) on = timer_begin(name, s);
+  }
+  ~TimedScope() {
+    if (on) timer_end(s);
+  }
+};
+
 // ------------------------------------------------------------------ small helpers
 
 constexpr int WAVE = 64;

@@ -1,22 +1,39 @@
-// Strided fp32-accumulating MFMA GEMM for gfx950:  C(i,j) = sum_k A(i,k) B(k,j).
+// Strided fp32-accumulating MFMA "strip" GEMM for gfx950:  C(i,j) = sum_k A(i,k) B(k,j).
 //
 // A(i,k) = A[i*a_si + k*a_sk], B(k,j) = B[k*b_sk + j*b_sj], C row-major.
 // One template covers the three products of a linear layer y = x W^T + b:
-//   forward   y  = x  W^T : A = x (k-contiguous),      B(k,j) = W[j][k] (k-contiguous)
-//   data grad dx = dy W   : A = dy (k-contiguous),     B(k,j) = W[k][j] (j-contiguous)
+//   forward   y  = x  W^T : A = x (k-contiguous),         B(k,j) = W[j][k] (k-contiguous)
+//   data grad dx = dy W   : A = dy (k-contiguous),        B(k,j) = W[k][j] (j-contiguous)
 //   weight    dW = dy^T x : A(i,k) = dy[k][i] (i-contig.), B(k,j) = x[k][j] (j-contiguous)
-// The contiguous dimension of each operand picks the global->LDS load mapping
-// (coalesced along it) and an LDS layout whose MFMA fragment reads are
-// bank-conflict free.  Inputs may be float32 or bfloat16 (converted on load);
-// the MFMA is v_mfma_f32_16x16x4_f32 (lane l supplies A[l%16][l/16] and
-// B[l/16][l%16]; accumulator register r of lane l is C[4*(l/16)+r][l%16]).
+//
+// Shape: the layer widths here are 32..500, while the row counts (events,
+// queries, neighbour slots) are 10^3..10^7.  A block therefore owns a strip of
+// 64 rows and up to 256 columns (the whole output width in one strip for
+// widths <= 256), so each A element is read from HBM once.  Each of the 4
+// waves computes 16 rows x BN columns with v_mfma_f32_16x16x4_f32 (lane l
+// supplies A[l%16][l/16] and B[l/16][l%16]; accumulator register r of lane l
+// is C[4*(l/16)+r][l%16]).  Operands move global -> registers -> LDS in
+// 32-deep k steps with 4-wide loads along each operand's contiguous
+// dimension; LDS keeps both operands k-contiguous and double-buffered (one
+// barrier per k step), so every MFMA operand comes from a 16-byte LDS read.
+// Inputs may be float32 or bfloat16 (converted on load).
 #pragma once
+
+#include <type_traits>
 
 #include "common.h"
 
 namespace mtgnn {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Call-site tags: the hot sites get their own kernel symbol (and timer name).
+namespace site {
+struct Generic { static constexpr const char* name = "gemm"; };
+struct KvProj { static constexpr const char* name = "gemm_kv_proj"; };    // K, V = kv_in W^T + b (neighbour slots)
+struct KvDw { static constexpr const char* name = "gemm_kv_dw"; };        // dW_k, dW_v (+ db) over neighbour slots
+struct KvDx { static constexpr const char* name = "gemm_kv_dx"; };        // dphi = dK W_k,t + dV W_v,t
+}  // namespace site
 
 struct GemmArgs {
   int64_t M, N, K;
@@ -38,41 +55,193 @@ struct GemmArgs {
   const float* gate;           // optional: result *= (gate(i,j) > 0)  (ReLU backward)
   int64_t ldgate;
   int round_bf16;              // round the stored result to bfloat16 (kept as float32)
+  int a_vec = 0, b_vec = 0;    // 4-wide loads along the contiguous dimension are aligned (set by the launcher)
+  int64_t ones_col = -1;       // B column treated as all ones (-1: none); its results go to col_out
+  float* col_out = nullptr;    // C(i, ones_col) is written to col_out[i] (weight-grad GEMMs: the bias grad)
 };
 
 // Epilogue rounding of a float32 value to the nearest bfloat16 (ties to even), widened back.
 __device__ __forceinline__ float round_to_bf16(float v) { return bf16_to_f32(f32_to_bf16(v)); }
 
-constexpr int G_BM = 64, G_BN = 64, G_BK = 16, G_THREADS = 256;
+constexpr int G_BK = 16, G_THREADS = 256;   // BK: k step of the library's launches (split-K chunks are multiples)
 
-template <bool KCONTIG, int BMN>
-struct TileLayout;
-// k-contiguous operand: [BMN][BK+1] (row = m or n)
-template <int BMN>
-struct TileLayout<true, BMN> {
-  static constexpr int SIZE = BMN * (G_BK + 1);
-  __device__ __forceinline__ static int idx(int mn, int k) { return mn * (G_BK + 1) + k; }
-  __device__ __forceinline__ static void coord(int e, int& mn, int& k) { k = e % G_BK; mn = e / G_BK; }
+// Four consecutive elements as float (fp32: one 16-byte load; bf16: one 8-byte load).
+template <typename T>
+struct Vec4;
+template <>
+struct Vec4<float> {
+  __device__ __forceinline__ static float4 load(const float* p) { return *reinterpret_cast<const float4*>(p); }
 };
-// m/n-contiguous operand: [BK][BMN+16]
-template <int BMN>
-struct TileLayout<false, BMN> {
-  static constexpr int SIZE = G_BK * (BMN + 16);
-  __device__ __forceinline__ static int idx(int mn, int k) { return k * (BMN + 16) + mn; }
-  __device__ __forceinline__ static void coord(int e, int& mn, int& k) { mn = e % BMN; k = e / BMN; }
+template <>
+struct Vec4<uint16_t> {
+  __device__ __forceinline__ static float4 load(const uint16_t* p) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return float4{bf16_to_f32((uint16_t)(u.x & 0xffffu)), bf16_to_f32((uint16_t)(u.x >> 16)),
+                  bf16_to_f32((uint16_t)(u.y & 0xffffu)), bf16_to_f32((uint16_t)(u.y >> 16))};
+  }
 };
 
-template <typename TA, typename TB, bool A_KCONTIG, bool B_KCONTIG>
-__global__ __launch_bounds__(G_THREADS) void k_gemm_f32(GemmArgs g) {
-  using LA = TileLayout<A_KCONTIG, G_BM>;
-  using LB = TileLayout<B_KCONTIG, G_BN>;
-  __shared__ float As[LA::SIZE];
-  __shared__ float Bs[LB::SIZE];
+// LDS layout of one operand tile (R rows of an output dimension x BK of the
+// reduction).  Operands contiguous along k are stored k-contiguous, [R][BK+4]:
+// a lane's four values of a 16-deep chunk come from one 16-byte read.  Operands
+// contiguous along their rows are stored as loaded, [BK][R+pad], with pad
+// chosen so consecutive k rows sit 16 banks apart; their fragment is four
+// 4-byte reads.  Either way, sub-step s of chunk kc gives lane l the value at
+// k = kc + 4 (l/16) + s.
+template <bool KC, int R, int BK>
+struct Lds {
+  static constexpr int LDK = BK + 4;                          // KC row stride
+  static constexpr int LDR = R + ((16 - (R % 32)) + 32) % 32;  // row-contiguous row stride (== 16 mod 32)
+  static constexpr int SIZE = KC ? R * LDK : BK * LDR;
+  __device__ __forceinline__ static float4 frag(const float* lds, int row, int kc, int lane) {
+    const int k = kc + 4 * (lane >> 4);
+    if (KC) return *reinterpret_cast<const float4*>(lds + row * LDK + k);
+    return float4{lds[(k + 0) * LDR + row], lds[(k + 1) * LDR + row], lds[(k + 2) * LDR + row],
+                  lds[(k + 3) * LDR + row]};
+  }
+  // group of 4: along k (KC) at (mn, k..k+3), or along rows at (mn..mn+3, k)
+  __device__ __forceinline__ static void put(float* lds, int mn, int k, float4 v) {
+    if (KC) *reinterpret_cast<float4*>(lds + mn * LDK + k) = v;
+    else *reinterpret_cast<float4*>(lds + k * LDR + mn) = v;
+  }
+  __device__ __forceinline__ static void coord(int g, int& mn, int& k) {
+    if (KC) { mn = g / (BK / 4); k = (g % (BK / 4)) * 4; }
+    else { mn = (g % (R / 4)) * 4; k = g / (R / 4); }
+  }
+};
+
+// One operand tile moving global -> registers -> LDS, for any shape: 4-wide
+// loads where a group is in range and aligned (vec), element loads otherwise.
+template <typename T, bool KC, int R, int BK>
+struct TileIO {
+  using L = Lds<KC, R, BK>;
+  static constexpr int GROUPS = R * BK / 4;
+  static constexpr int PER = (GROUPS + G_THREADS - 1) / G_THREADS;
+  float4 v[PER];
+
+  // e(mn, k) = base[mn * s_mn + k * s_k]; rows < rows_lim and k < k_lim are in range
+  __device__ __forceinline__ void load(const T* base, int64_t s_mn, int64_t s_k, int64_t mn0, int64_t k0,
+                                       int64_t rows_lim, int64_t k_lim, bool vec, int64_t ones_mn, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int g = tid + p * G_THREADS;
+      float e[4] = {0.f, 0.f, 0.f, 0.f};
+      if (g < GROUPS) {
+        int mn, k;
+        L::coord(g, mn, k);
+        const int64_t gm = mn0 + mn, gk = k0 + k;
+        const bool full = KC ? (gm < rows_lim && gk + 3 < k_lim) : (gm + 3 < rows_lim && gk < k_lim);
+        const bool has_ones = ones_mn >= gm && ones_mn <= (KC ? gm : gm + 3);   // virtual column: no memory
+        if (vec && full && !has_ones) {
+          const float4 f = Vec4<T>::load(base + gm * s_mn + gk * s_k);
+          e[0] = f.x; e[1] = f.y; e[2] = f.z; e[3] = f.w;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int64_t m = KC ? gm : gm + i, kk = KC ? gk + i : gk;
+            if (m < rows_lim && kk < k_lim) e[i] = m == ones_mn ? 1.f : Elem<T>::load(base, m * s_mn + kk * s_k);
+          }
+        }
+      }
+      v[p] = float4{e[0], e[1], e[2], e[3]};
+    }
+  }
+
+  __device__ __forceinline__ void store(float* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int g = tid + p * G_THREADS;
+      if (g >= GROUPS) continue;
+      int mn, k;
+      L::coord(g, mn, k);
+      L::put(lds, mn, k, v[p]);
+    }
+  }
+};
+
+// Branch-free variant of TileIO for aligned shapes (every row count of the
+// operand's contiguous dimension and every k extent are multiples of 4).  Each
+// thread keeps a pointer per 4-wide group and advances it by a constant per k
+// step; groups outside the matrix load from its first element (a valid
+// address) and are zeroed by selects, so the loop has no per-element branches.
+template <typename T, bool KC, int R, int BK>
+struct TileVec {
+  using L = Lds<KC, R, BK>;
+  static constexpr int GROUPS = R * BK / 4;
+  static constexpr int PER = (GROUPS + G_THREADS - 1) / G_THREADS;
+  const T* ptr[PER];
+  const T* safe;
+  int kq[PER];          // k offset of the group inside the tile
+  uint32_t row_ok;      // bit p: the group's rows exist
+  uint32_t ones;        // bit p: the group holds the virtual all-ones column (value 1 in its first row)
+  float4 v[PER];
+
+  __device__ __forceinline__ void init(const T* base, int64_t s_mn, int64_t s_k, int64_t mn0, int64_t k0,
+                                       int64_t rows_lim, int64_t ones_mn, int tid) {
+    safe = base;
+    row_ok = 0;
+    ones = 0;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int g = tid + p * G_THREADS;
+      int mn, k;
+      L::coord(g, mn, k);
+      const int64_t gm = mn0 + mn;
+      const bool is_ones = !KC && gm == ones_mn;
+      const bool ok = g < GROUPS && gm < rows_lim && !is_ones;
+      if (ok) row_ok |= 1u << p;
+      if (g < GROUPS && is_ones) ones |= 1u << p;
+      kq[p] = k;
+      ptr[p] = base + (ok ? gm : 0) * s_mn + (k0 + k) * s_k;
+    }
+  }
+  // k0: first k of the tile; k_lim: end of the reduction range
+  __device__ __forceinline__ void load(int64_t k0, int64_t k_lim) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const bool kin = k0 + kq[p] < k_lim;
+      const bool ok = ((row_ok >> p) & 1u) && kin;
+      const float4 f = Vec4<T>::load(ok ? ptr[p] : safe);
+      const bool one = ((ones >> p) & 1u) && kin;
+      v[p] = float4{ok ? f.x : (one ? 1.f : 0.f), ok ? f.y : 0.f, ok ? f.z : 0.f, ok ? f.w : 0.f};
+    }
+  }
+  __device__ __forceinline__ void advance(int64_t step) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) ptr[p] += step;
+  }
+  __device__ __forceinline__ void store(float* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int g = tid + p * G_THREADS;
+      if (g >= GROUPS) continue;
+      int mn, k;
+      L::coord(g, mn, k);
+      L::put(lds, mn, k, v[p]);
+    }
+  }
+};
+
+// Block: (64 WM) rows x BN columns; wave w computes WM 16-row tiles x BN.
+// Within each 16-deep k chunk, lane l feeds the MFMA k-slot l/16 with
+// k = 4 (l/16) + s at sub-step s (s = 0..3), for both operands (see Lds); the
+// sum over the chunk is unchanged.  NBUF = 2: double-buffered LDS, one barrier per k step; NBUF = 1:
+// one LDS buffer, the next tile waits in registers (two barriers per step).
+// VEC: aligned shapes use the branch-free TileVec loader.
+template <class Site, int BN, int WM, int BK, int NBUF, bool VEC, typename TA, typename TB, bool A_KCONTIG,
+          bool B_KCONTIG>
+__global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
+  constexpr int NT = BN / 16;
+  constexpr int BM = 64 * WM;
+  using LA = Lds<A_KCONTIG, BM, BK>;
+  using LB = Lds<B_KCONTIG, BN, BK>;
+  __shared__ float As[NBUF][LA::SIZE];
+  __shared__ float Bs[NBUF][LB::SIZE];
 
   const int64_t M = eff_count(g.M, g.M_dev);
   const int64_t Kall = eff_count(g.K, g.K_dev);
-  const int64_t row0 = (int64_t)blockIdx.x * G_BM;
-  const int64_t col0 = (int64_t)blockIdx.y * G_BN;
+  const int64_t row0 = (int64_t)blockIdx.x * BM;
+  const int64_t col0 = (int64_t)blockIdx.y * BN;
   if (row0 >= M) return;
   const int64_t kbeg = (int64_t)blockIdx.z * g.kchunk;
   const int64_t kend = min(Kall, kbeg + g.kchunk);
@@ -80,72 +249,95 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm_f32(GemmArgs g) {
   const TA* A = (const TA*)g.A;
   const TB* B = (const TB*)g.B;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
+  const int64_t a_smn = g.a_si, a_sk = g.a_sk, b_smn = g.b_sj, b_sk = g.b_sk;
 
-  f32x4 acc[2][2];
-  for (int i = 0; i < 2; ++i)
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  constexpr int PER_T = (G_BM * G_BK) / G_THREADS;   // 4 elements of A and of B per thread
-  float ra[PER_T], rb[PER_T];
-
-  auto load = [&](int64_t k0) {
+  f32x4 acc[WM][NT];
 #pragma unroll
-    for (int p = 0; p < PER_T; ++p) {
-      int e = tid + p * G_THREADS, mn, k;
-      LA::coord(e, mn, k);
-      int64_t gi = row0 + mn, gk = k0 + k;
-      ra[p] = (gi < M && gk < kend) ? Elem<TA>::load(A, gi * g.a_si + gk * g.a_sk) : 0.f;
-      LB::coord(e, mn, k);
-      int64_t gj = col0 + mn;
-      gk = k0 + k;
-      rb[p] = (gj < g.N && gk < kend) ? Elem<TB>::load(B, gk * g.b_sk + gj * g.b_sj) : 0.f;
-    }
-  };
-  auto stash = [&]() {
+  for (int i = 0; i < WM; ++i)
 #pragma unroll
-    for (int p = 0; p < PER_T; ++p) {
-      int e = tid + p * G_THREADS, mn, k;
-      LA::coord(e, mn, k);
-      As[LA::idx(mn, k)] = ra[p];
-      LB::coord(e, mn, k);
-      Bs[LB::idx(mn, k)] = rb[p];
+    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  using IOA = typename std::conditional<VEC, TileVec<TA, A_KCONTIG, BM, BK>, TileIO<TA, A_KCONTIG, BM, BK>>::type;
+  using IOB = typename std::conditional<VEC, TileVec<TB, B_KCONTIG, BN, BK>, TileIO<TB, B_KCONTIG, BN, BK>>::type;
+  IOA ta;
+  IOB tb;
+  auto load_tiles = [&](int64_t k0) {
+    if constexpr (VEC) {
+      ta.load(k0, kend);
+      tb.load(k0, kend);
+      ta.advance(BK * a_sk);
+      tb.advance(BK * b_sk);
+    } else {
+      ta.load(A, a_smn, a_sk, row0, k0, M, kend, g.a_vec != 0, -1, tid);
+      tb.load(B, b_smn, b_sk, col0, k0, g.N, kend, g.b_vec != 0, g.ones_col, tid);
     }
   };
 
   if (kbeg < kend) {
-    load(kbeg);
-    for (int64_t k0 = kbeg; k0 < kend; k0 += G_BK) {
-      __syncthreads();
-      stash();
-      __syncthreads();
-      if (k0 + G_BK < kend) load(k0 + G_BK);
+    if constexpr (VEC) {
+      ta.init(A, a_smn, a_sk, row0, kbeg, M, -1, tid);
+      tb.init(B, b_smn, b_sk, col0, kbeg, g.N, g.ones_col, tid);
+    }
+    load_tiles(kbeg);
+    ta.store(As[0], tid);
+    tb.store(Bs[0], tid);
+    __syncthreads();
+    int cur = 0;
+    for (int64_t k0 = kbeg; k0 < kend; k0 += BK) {
+      const bool more = k0 + BK < kend;
+      if (more) load_tiles(k0 + BK);
+      const float* as = As[cur];
+      const float* bs = Bs[cur];
 #pragma unroll
-      for (int ks = 0; ks < G_BK; ks += 4) {
-        float a[2], b[2];
+      for (int kc = 0; kc < BK; kc += 16) {
+        float4 a4[WM];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = As[LA::idx(wm * 32 + i * 16 + (lane & 15), ks + (lane >> 4))];
+        for (int i = 0; i < WM; ++i) a4[i] = LA::frag(as, (wid * WM + i) * 16 + (lane & 15), kc, lane);
+        float4 b4[NT];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) b[j] = Bs[LB::idx(wn * 32 + j * 16 + (lane & 15), ks + (lane >> 4))];
+        for (int j = 0; j < NT; ++j) b4[j] = LB::frag(bs, j * 16 + (lane & 15), kc, lane);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < WM; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].x, b4[j].x, acc[i][j], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].y, b4[j].y, acc[i][j], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].z, b4[j].z, acc[i][j], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].w, b4[j].w, acc[i][j], 0, 0, 0);
       }
+      if (more) {
+        const int nb = NBUF == 2 ? (cur ^ 1) : 0;
+        if (NBUF == 1) __syncthreads();   // every wave is done reading the only buffer
+        ta.store(As[nb], tid);
+        tb.store(Bs[nb], tid);
+      }
+      __syncthreads();
+      if (NBUF == 2) cur ^= 1;
     }
   }
 
+  // epilogue: bias, accumulate, ReLU gate / pre-activation, bf16 rounding, bias-grad column
   float* C = g.C + (int64_t)blockIdx.z * g.c_split_stride;
+  const bool split = g.c_split_stride != 0;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int j = 0; j < NT; ++j) {
+    const int64_t gj = col0 + j * 16 + (lane & 15);
+    if (gj >= g.N) continue;
+    const bool to_col = gj == g.ones_col && !split;
+    const float bj = g.bias ? g.bias[gj] : 0.f;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t gj = col0 + wn * 32 + j * 16 + (lane & 15);
-      if (gj >= g.N) continue;
-      const float bj = g.bias ? g.bias[gj] : 0.f;
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t gi = row0 + wm * 32 + i * 16 + 4 * (lane >> 4) + r;
+        const int64_t gi = row0 + (wid * WM + i) * 16 + 4 * (lane >> 4) + r;
         if (gi >= M) continue;
         float v = acc[i][j][r] + bj;
         if (g.accumulate) v += C[gi * g.ldc + gj];
@@ -155,34 +347,142 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm_f32(GemmArgs g) {
           v = fmaxf(v, 0.f);
         }
         if (g.round_bf16) v = round_to_bf16(v);
-        C[gi * g.ldc + gj] = v;
+        if (to_col) g.col_out[gi] = v;
+        else C[gi * g.ldc + gj] = v;
       }
-    }
+  }
 }
 
-// Sums split-K partials in a fixed order: out(i,j) (+)= sum_z part[z](i,j).
+// Tile shape used by the library's launches.
+constexpr int G_WM = 1, G_NBUF = 2;
+
+// Column `ones_col` (if >= 0) goes to col_out[i] instead of out.
 __global__ void k_splitk_reduce(const float* __restrict__ part, int64_t split_stride, int nsplit, int64_t rows,
-                                int64_t cols, float* __restrict__ out, int64_t ldo, int accumulate);
+                                int64_t cols, float* __restrict__ out, int64_t ldo, int64_t ones_col,
+                                float* __restrict__ col_out);
 
-// Host-side launcher.  a_kcontig / b_kcontig: the operand is contiguous along k.
-mtgnn_status gemm_launch(const GemmArgs& g, int dtype_a, int dtype_b, bool a_kcontig, bool b_kcontig, int ksplit,
-                         hipStream_t s);
+// Strip width for an output of N columns: one strip when N <= 256, else equal strips.
+int gemm_strip_width(int64_t N);
+void dw_split(int64_t R, int64_t N, int64_t K, int& ksplit, int64_t& kchunk);
 
-// Convenience wrappers for the three linear-layer products (row-major matrices).
-// y[M,N] (+)= x[M,K] W[N,K]^T + bias
+// A 4-wide load along the contiguous dimension is aligned when the base and the other stride are.
+inline bool vec_ok(const void* p, int64_t other_stride, size_t esz) {
+  return ((uintptr_t)p % (4 * esz)) == 0 && (other_stride % 4) == 0;
+}
+
+template <class Site, int BN, bool VEC, typename TA, typename TB, bool AK, bool BK>
+void gemm_kernel_launch(const GemmArgs& g, dim3 grid, hipStream_t s) {
+  k_gemm<Site, BN, G_WM, G_BK, G_NBUF, VEC, TA, TB, AK, BK><<<grid, G_THREADS, 0, s>>>(g);
+}
+
+template <class Site, bool VEC, typename TA, typename TB, bool AK, bool BK>
+void gemm_bn_launch(const GemmArgs& g, int bn, dim3 grid, hipStream_t s) {
+  switch (bn) {
+    case 64: gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK>(g, grid, s); break;
+    case 128: gemm_kernel_launch<Site, 128, VEC, TA, TB, AK, BK>(g, grid, s); break;
+    case 160: gemm_kernel_launch<Site, 160, VEC, TA, TB, AK, BK>(g, grid, s); break;
+    case 208: gemm_kernel_launch<Site, 208, VEC, TA, TB, AK, BK>(g, grid, s); break;
+    default: gemm_kernel_launch<Site, 256, VEC, TA, TB, AK, BK>(g, grid, s); break;
+  }
+}
+
+template <class Site, typename TA, typename TB, bool AK, bool BK>
+mtgnn_status gemm_launch_t(const GemmArgs& g0, int ksplit, hipStream_t s) {
+  GemmArgs g = g0;
+  g.a_vec = vec_ok(g.A, AK ? g.a_si : g.a_sk, sizeof(TA)) ? 1 : 0;   // general loader: 4-wide only when aligned
+  g.b_vec = vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) ? 1 : 0;
+  const int bn = gemm_strip_width(g.N);
+  dim3 grid((unsigned)cdiv(g.M, 64 * G_WM), (unsigned)cdiv(g.N, bn), (unsigned)(ksplit < 1 ? 1 : ksplit));
+  // The branch-free loader needs 4-aligned bases and strides, row counts of
+  // each operand's contiguous dimension that are multiples of 4, a virtual
+  // ones column (if any) at a multiple of 4, and k extents (host K and the
+  // split chunk) that are multiples of 4 for operands contiguous along k.
+  const bool vec = vec_ok(g.A, AK ? g.a_si : g.a_sk, sizeof(TA)) &&
+                   vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) &&
+                   (AK ? (g.K % 4 == 0 && g.kchunk % 4 == 0 && g.K_dev == nullptr) : (g.M % 4 == 0 && g.M_dev == nullptr)) &&
+                   (BK ? (g.K % 4 == 0 && g.kchunk % 4 == 0 && g.K_dev == nullptr) : g.N % 4 == 0 || g.ones_col == g.N - 1) &&
+                   (g.ones_col < 0 || g.ones_col % 4 == 0);
+  TimedScope ts(Site::name, s);
+  if (vec) gemm_bn_launch<Site, true, TA, TB, AK, BK>(g, bn, grid, s);
+  else gemm_bn_launch<Site, false, TA, TB, AK, BK>(g, bn, grid, s);
+  MTGNN_CHECK_LAUNCH(Site::name);
+  return MTGNN_OK;
+}
+
+// Instantiated once per (site, layout) in gemm_nt.hip / gemm_nn.hip / gemm_tn.hip.
+template <class Site, bool AK, bool BK>
+mtgnn_status gemm_launch(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s);
+
+template <class Site, bool AK, bool BK>
+mtgnn_status gemm_launch_impl(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return MTGNN_OK;
+  if (dtype_a == MTGNN_F32 && dtype_b == MTGNN_F32) return gemm_launch_t<Site, float, float, AK, BK>(g, ksplit, s);
+  if (dtype_a == MTGNN_F32) return gemm_launch_t<Site, float, uint16_t, AK, BK>(g, ksplit, s);
+  if (dtype_b == MTGNN_F32) return MTGNN_EUNSUPPORTED;   // bf16 activations always meet bf16 weights
+  return gemm_launch_t<Site, uint16_t, uint16_t, AK, BK>(g, ksplit, s);
+}
+
+// y[M,N] (+)= x[M,K] W[N,K]^T + bias.
 // pre_relu: store the pre-activation there and relu(y) in y.  round_bf16: round y to bfloat16.
+template <class Site = site::Generic>
 mtgnn_status linear_fwd(const void* x, int x_dtype, int64_t ldx, const void* W, int w_dtype, int64_t ldw,
                         const float* bias, float* y, int64_t ldy, int64_t M, const int32_t* M_dev, int64_t N,
                         int64_t K, bool accumulate, hipStream_t s, float* pre_relu = nullptr, int64_t ldpre = 0,
-                        bool round_bf16 = false);
+                        bool round_bf16 = false) {
+  GemmArgs g{};
+  g.M = M; g.N = N; g.K = K; g.M_dev = M_dev;
+  g.A = x; g.a_si = ldx; g.a_sk = 1;
+  g.B = W; g.b_sk = 1; g.b_sj = ldw;
+  g.C = y; g.ldc = ldy; g.bias = bias; g.accumulate = accumulate ? 1 : 0;
+  g.relu = pre_relu ? 1 : 0; g.C2 = pre_relu; g.ldc2 = ldpre;
+  g.kchunk = K; g.c_split_stride = 0; g.round_bf16 = round_bf16 ? 1 : 0;
+  return gemm_launch<Site, true, true>(g, x_dtype, w_dtype, 1, s);
+}
+
 // dx[M,K] (+)= dy[M,N] W[N,K]; gate: dx *= (gate > 0) elementwise (after accumulation)
+template <class Site = site::Generic>
 mtgnn_status linear_dx(const float* dy, int64_t lddy, const void* W, int w_dtype, int64_t ldw, float* dx,
                        int64_t lddx, int64_t M, const int32_t* M_dev, int64_t N, int64_t K, bool accumulate,
-                       hipStream_t s, const float* gate = nullptr, int64_t ldgate = 0);
+                       hipStream_t s, const float* gate = nullptr, int64_t ldgate = 0) {
+  GemmArgs g{};
+  g.M = M; g.N = K; g.K = N; g.M_dev = M_dev;
+  g.A = dy; g.a_si = lddy; g.a_sk = 1;
+  g.B = W; g.b_sk = ldw; g.b_sj = 1;
+  g.C = dx; g.ldc = lddx; g.accumulate = accumulate ? 1 : 0;
+  g.kchunk = N; g.c_split_stride = 0; g.gate = gate; g.ldgate = ldgate;
+  return gemm_launch<Site, true, false>(g, MTGNN_F32, w_dtype, 1, s);
+}
+
 // dW[N,K] = dy[R,N]^T x[R,K], reduction over R rows (clamped by R_dev), split-K through ws.
+// db (optional): db[N] = sum over rows of dy, computed as an extra all-ones column of x.
 size_t linear_dw_ws_bytes(int64_t R, int64_t N, int64_t K);
+
+template <class Site = site::Generic>
 mtgnn_status linear_dw(const float* dy, int64_t lddy, const void* x, int x_dtype, int64_t ldx, float* dW,
                        int64_t lddw, int64_t R, const int32_t* R_dev, int64_t N, int64_t K, void* ws,
-                       size_t ws_bytes, hipStream_t s);
+                       size_t ws_bytes, hipStream_t s, float* db = nullptr) {
+  int ksplit;
+  int64_t kchunk;
+  const int64_t Kc = db ? K + 1 : K;   // extra all-ones column of x gives the bias gradient
+  dw_split(R, N, Kc, ksplit, kchunk);
+  GemmArgs g{};
+  g.M = N; g.N = Kc; g.K = R; g.K_dev = R_dev;
+  if (db) { g.ones_col = K; g.col_out = db; }
+  g.A = dy; g.a_si = 1; g.a_sk = lddy;
+  g.B = x; g.b_sk = ldx; g.b_sj = 1;
+  g.kchunk = kchunk;
+  if (ksplit == 1) {
+    g.C = dW; g.ldc = lddw; g.c_split_stride = 0;
+    return gemm_launch<Site, false, false>(g, MTGNN_F32, x_dtype, 1, s);
+  }
+  if (ws_bytes < linear_dw_ws_bytes(R, N, K)) return MTGNN_EWORKSPACE;
+  g.C = (float*)ws; g.ldc = Kc; g.c_split_stride = N * Kc;
+  MTGNN_TRY((gemm_launch<Site, false, false>(g, MTGNN_F32, x_dtype, ksplit, s)));
+  const int64_t tot = N * Kc;
+  k_splitk_reduce<<<(unsigned)cdiv(tot, 64), 256, 0, s>>>((const float*)ws, N * Kc, ksplit, N, Kc, dW, lddw,
+                                                           db ? K : -1, db);
+  MTGNN_CHECK_LAUNCH("splitk_reduce");
+  return MTGNN_OK;
+}
 
 }  // namespace mtgnn

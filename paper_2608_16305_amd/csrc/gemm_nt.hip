@@ -1,0 +1,14 @@
+// Forward products y = x W^T (both operands contiguous along k).
+#include "gemm.h"
+
+namespace mtgnn {
+
+template <class Site, bool AK, bool BK>
+mtgnn_status gemm_launch(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s) {
+  return gemm_launch_impl<Site, AK, BK>(g, dtype_a, dtype_b, ksplit, s);
+}
+
+template mtgnn_status gemm_launch<site::Generic, true, true>(const GemmArgs&, int, int, int, hipStream_t);
+template mtgnn_status gemm_launch<site::KvProj, true, true>(const GemmArgs&, int, int, int, hipStream_t);
+
+}  // namespace mtgnn

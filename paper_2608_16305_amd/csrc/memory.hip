@@ -189,12 +189,13 @@ __global__ void k_gru_bwd_gates(const float* __restrict__ dh, const float* __res
 
 // ---------------------------------------------------------------- time-encoder gradients
 
-constexpr int TG_ROWS = 512;
+constexpr int TG_ROWS = 128;
 
-struct MsgDelta {
-  const float* dt;
+// Elapsed time of each row: delta[r] (delta == nullptr: 0, the query-side phi(0)).
+struct RowDelta {
+  const float* delta;
   __device__ bool get(int64_t r, float& d) const {
-    d = dt[r];
+    d = delta ? delta[r] : 0.f;
     return true;
   }
 };
@@ -203,7 +204,8 @@ template <typename D>
 __global__ __launch_bounds__(256) void k_timegrad_partial(const float* __restrict__ dphi, int64_t ld, int64_t rows,
                                                           const int32_t* __restrict__ rows_dev, D delta,
                                                           const float* __restrict__ tw, const float* __restrict__ tb,
-                                                          int dt_dim, float* __restrict__ part) {
+                                                          const float* __restrict__ sin_saved, int dt_dim,
+                                                          float* __restrict__ part) {
   __shared__ float red_w[4][64], red_b[4][64];
   const int j = blockIdx.x * 64 + (threadIdx.x & 63);
   const int rg = threadIdx.x >> 6;
@@ -216,7 +218,8 @@ __global__ __launch_bounds__(256) void k_timegrad_partial(const float* __restric
     for (int64_t r = r0 + rg; r < r1; r += 4) {
       float d;
       if (!delta.get(r, d)) continue;
-      const float g = dphi[r * ld + j] * -sinf(time_arg(w, d, b));
+      const float sn = sin_saved ? sin_saved[r * dt_dim + j] : sinf(time_arg(w, d, b));
+      const float g = dphi[r * ld + j] * -sn;
       sb += g;
       sw += g * d;
     }
@@ -231,15 +234,26 @@ __global__ __launch_bounds__(256) void k_timegrad_partial(const float* __restric
   }
 }
 
-__global__ void k_timegrad_final(const float* __restrict__ part, int nch, int dt_dim, float* __restrict__ dw,
-                                 float* __restrict__ db, int accumulate) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= dt_dim) return;
+// 64 columns per block; the 4 waves sum interleaved chunks, combined in a fixed order.
+__global__ __launch_bounds__(256) void k_timegrad_final(const float* __restrict__ part, int nch, int dt_dim,
+                                                        float* __restrict__ dw, float* __restrict__ db,
+                                                        int accumulate) {
+  __shared__ float rw[4][64], rb[4][64];
+  const int j = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int g = threadIdx.x >> 6;
   float sw = 0.f, sb = 0.f;
-  for (int c = 0; c < nch; ++c) {
-    sw += part[((int64_t)c * 2 + 0) * dt_dim + j];
-    sb += part[((int64_t)c * 2 + 1) * dt_dim + j];
-  }
+  if (j < dt_dim)
+    for (int c = g; c < nch; c += 4) {
+      sw += part[((int64_t)c * 2 + 0) * dt_dim + j];
+      sb += part[((int64_t)c * 2 + 1) * dt_dim + j];
+    }
+  rw[g][threadIdx.x & 63] = sw;
+  rb[g][threadIdx.x & 63] = sb;
+  __syncthreads();
+  if (g != 0 || j >= dt_dim) return;
+  const int l = threadIdx.x;
+  sw = ((rw[0][l] + rw[1][l]) + rw[2][l]) + rw[3][l];
+  sb = ((rb[0][l] + rb[1][l]) + rb[2][l]) + rb[3][l];
   dw[j] = accumulate ? dw[j] + sw : sw;
   db[j] = accumulate ? db[j] + sb : sb;
 }
@@ -254,56 +268,26 @@ size_t timegrad_ws_bytes(int64_t rows, int dt_dim) {
 
 template <typename D>
 mtgnn_status timegrad_launch(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, D delta,
-                             const float* tw, const float* tb, int dt_dim, float* dw, float* db, bool accumulate,
-                             void* ws, size_t ws_bytes, hipStream_t s) {
+                             const float* tw, const float* tb, const float* sin_saved, int dt_dim, float* dw, float* db,
+                             bool accumulate, void* ws, size_t ws_bytes, hipStream_t s) {
   if (dt_dim <= 0) return MTGNN_OK;
   if (rows <= 0) rows = 1;   // still writes (zero) sums when overwriting
   if (ws_bytes < timegrad_ws_bytes(rows, dt_dim)) return MTGNN_EWORKSPACE;
   const int nch = (int)cdiv(rows, TG_ROWS);
   dim3 g((unsigned)cdiv(dt_dim, 64), (unsigned)nch);
-  k_timegrad_partial<D><<<g, 256, 0, s>>>(dphi, ld, rows, rows_dev, delta, tw, tb, dt_dim, (float*)ws);
+  k_timegrad_partial<D><<<g, 256, 0, s>>>(dphi, ld, rows, rows_dev, delta, tw, tb, sin_saved, dt_dim, (float*)ws);
   MTGNN_CHECK_LAUNCH("timegrad_partial");
-  k_timegrad_final<<<(unsigned)cdiv(dt_dim, 256), 256, 0, s>>>((const float*)ws, nch, dt_dim, dw, db,
-                                                               accumulate ? 1 : 0);
+  k_timegrad_final<<<(unsigned)cdiv(dt_dim, 64), 256, 0, s>>>((const float*)ws, nch, dt_dim, dw, db,
+                                                              accumulate ? 1 : 0);
   MTGNN_CHECK_LAUNCH("timegrad_final");
   return MTGNN_OK;
 }
 
-namespace {
-struct PairDelta {
-  const int32_t* nbr;
-  const float* q_t;
-  const float* nt;
-  const int32_t* n_q;
-  int k;
-  __device__ bool get(int64_t r, float& d) const {
-    const int64_t q = r / k;
-    if (n_q != nullptr && q >= *n_q) return false;
-    if (nbr[r] < 0) return false;
-    d = q_t[q] - nt[r];
-    return true;
-  }
-};
-struct ZeroDelta {
-  __device__ bool get(int64_t, float& d) const {
-    d = 0.f;
-    return true;
-  }
-};
-}  // namespace
-
-mtgnn_status timegrad_pairs(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev_q, int k,
-                            const int32_t* nbr, const float* q_t, const float* nt, const float* tw, const float* tb,
-                            int dt_dim, float* dw, float* db, bool accumulate, void* ws, size_t ws_bytes,
-                            hipStream_t s) {
-  return timegrad_launch(dphi, ld, rows, nullptr, PairDelta{nbr, q_t, nt, rows_dev_q, k}, tw, tb, dt_dim, dw, db,
-                         accumulate, ws, ws_bytes, s);
-}
-
-mtgnn_status timegrad_zero(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* tw,
-                           const float* tb, int dt_dim, float* dw, float* db, bool accumulate, void* ws,
-                           size_t ws_bytes, hipStream_t s) {
-  return timegrad_launch(dphi, ld, rows, rows_dev, ZeroDelta{}, tw, tb, dt_dim, dw, db, accumulate, ws, ws_bytes, s);
+mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* delta,
+                           const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
+                           bool accumulate, void* ws, size_t ws_bytes, hipStream_t s) {
+  return timegrad_launch(dphi, ld, rows, rows_dev, RowDelta{delta}, tw, tb, sin_saved, dt_dim, dw, db, accumulate, ws,
+                         ws_bytes, s);
 }
 
 // ---------------------------------------------------------------- entry-point bodies
@@ -436,9 +420,7 @@ size_t gru_update_bwd_ws(const mtgnn_dims* d, int64_t max_rows) {
   const int dm = d->d_mem, dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
   size_t dw = linear_dw_ws_bytes(max_rows, 3 * dm, dmsg);
   size_t dw2 = linear_dw_ws_bytes(max_rows, 3 * dm, dm);
-  size_t cs = colsum_ws_bytes(max_rows, 3 * dm);
   size_t m = dw > dw2 ? dw : dw2;
-  m = m > cs ? m : cs;
   return 2 * a256(sizeof(float) * max_rows * 3 * dm) + a256(m);
 }
 
@@ -463,10 +445,8 @@ mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const voi
   k_gru_bwd_gates<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(d_mem, h_old, sr, sz, sn, sghn, n_rows, max_rows,
                                                                         dm, dgi, dgh);
   MTGNN_CHECK_LAUNCH("gru_bwd_gates");
-  MTGNN_TRY(linear_dw(dgi, 3 * dm, msg, d->dtype, dmsg, dW_ih, dmsg, max_rows, n_rows, 3 * dm, dmsg, w, rest, s));
-  MTGNN_TRY(linear_dw(dgh, 3 * dm, h_old, MTGNN_F32, dm, dW_hh, dm, max_rows, n_rows, 3 * dm, dm, w, rest, s));
-  MTGNN_TRY(colsum(dgi, 3 * dm, max_rows, n_rows, 3 * dm, db_ih, false, w, rest, s));
-  MTGNN_TRY(colsum(dgh, 3 * dm, max_rows, n_rows, 3 * dm, db_hh, false, w, rest, s));
+  MTGNN_TRY(linear_dw(dgi, 3 * dm, msg, d->dtype, dmsg, dW_ih, dmsg, max_rows, n_rows, 3 * dm, dmsg, w, rest, s, db_ih));
+  MTGNN_TRY(linear_dw(dgh, 3 * dm, h_old, MTGNN_F32, dm, dW_hh, dm, max_rows, n_rows, 3 * dm, dm, w, rest, s, db_hh));
   if (dmsg_time && d->d_time > 0) {
     const size_t esz = d->dtype == MTGNN_F32 ? 4 : 2;
     const void* Wt = (const char*)W_ih + esz * (size_t)(2 * dm);   // columns [2 dm, 2 dm + d_time)
@@ -481,8 +461,8 @@ size_t build_messages_bwd_ws(const mtgnn_dims* d, int64_t max_rows) { return tim
 mtgnn_status build_messages_bwd_impl(const float* dmsg_time, const float* dt, const int32_t* n_rows, int64_t max_rows,
                                      const float* tw, const float* tb, const mtgnn_dims* d, float* dw, float* db,
                                      void* ws, size_t ws_bytes, hipStream_t s) {
-  return timegrad_launch(dmsg_time, d->d_time, max_rows, n_rows, MsgDelta{dt}, tw, tb, d->d_time, dw, db, true, ws,
-                         ws_bytes, s);
+  return timegrad_rows(dmsg_time, d->d_time, max_rows, n_rows, dt, nullptr, tw, tb, d->d_time, dw, db, true, ws,
+                       ws_bytes, s);
 }
 
 }  // namespace mtgnn

@@ -34,15 +34,12 @@ mtgnn_status build_messages_bwd_impl(const float* dmsg_time, const float* dt, co
 
 // time-encoder gradient reductions (fixed order)
 size_t timegrad_ws_bytes(int64_t rows, int dt_dim);
-// rows = query*k + slot; delta = q_t[row / k] - nt[row]; slots with nbr < 0 are skipped
-mtgnn_status timegrad_pairs(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev_q, int k,
-                            const int32_t* nbr, const float* q_t, const float* nt, const float* tw, const float* tb,
-                            int dt_dim, float* dw, float* db, bool accumulate, void* ws, size_t ws_bytes,
-                            hipStream_t s);
-// delta = 0 for every row (the query-side phi(0))
-mtgnn_status timegrad_zero(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* tw,
-                           const float* tb, int dt_dim, float* dw, float* db, bool accumulate, void* ws,
-                           size_t ws_bytes, hipStream_t s);
+// d_time_w[j] (+)= sum_r dphi[r,j] (-sin(arg_rj)) delta_r,  d_time_b[j] (+)= sum_r dphi[r,j] (-sin(arg_rj)),
+// arg_rj = time_w[j] delta_r + time_b[j]; delta == nullptr means delta_r = 0; sin_saved (optional) holds
+// sin(arg) per [row, j]; rows are clamped by rows_dev.
+mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* delta,
+                           const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
+                           bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
 
 // sampling / adjacency
 mtgnn_status sample_recent_impl(const int64_t* off, const int32_t* nbr, const float* t, const int32_t* eid,

@@ -22,7 +22,7 @@ ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
     "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_bwd", "mtgnn_gru_update_bwd",
     "mtgnn_build_messages_bwd", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
-    "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version",
+    "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
 )
 
 
@@ -74,6 +74,8 @@ _SIGS = {
     "mtgnn_status_string": [C.c_int],
     "mtgnn_last_error": [],
     "mtgnn_version": [],
+    "mtgnn_timer_start": [C.c_char_p, C.c_int],
+    "mtgnn_timer_stop": [C.POINTER(C.c_double), C.POINTER(C.c_int)],
 }
 _RES = {"mtgnn_workspace_bytes": _SZ, "mtgnn_save_bytes": _SZ, "mtgnn_status_string": C.c_char_p,
         "mtgnn_last_error": C.c_char_p, "mtgnn_version": C.c_int}
@@ -274,3 +276,15 @@ def mtgnn_build_temporal_csr(src, dst, t, n_nodes, csr_off, csr_nbr, csr_t, csr_
                                           _ptr(csr_off, torch.int64, "csr_off"), _ptr(csr_nbr, torch.int32, "csr_nbr"),
                                           _ptr(csr_t, torch.float32, "csr_t"), _ptr(csr_eid, torch.int32, "csr_eid"),
                                           wp, wb, _stream(stream)), "mtgnn_build_temporal_csr")
+
+
+def timer_start(kernel: str, max_launches: int):
+    """Arm the library's launch timer for `kernel` (instrumentation)."""
+    _check(lib().mtgnn_timer_start(kernel.encode(), int(max_launches)), "mtgnn_timer_start")
+
+
+def timer_stop():
+    """Disarm the timer; returns (summed milliseconds, number of timed launches)."""
+    ms, n = C.c_double(0.0), C.c_int(0)
+    _check(lib().mtgnn_timer_stop(C.byref(ms), C.byref(n)), "mtgnn_timer_stop")
+    return ms.value, n.value
