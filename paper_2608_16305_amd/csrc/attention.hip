@@ -308,8 +308,12 @@ __global__ void k_occ_keys(const int32_t* __restrict__ q_node, const int32_t* __
                            const int32_t* __restrict__ n_q, int64_t max_q, const int32_t* __restrict__ n_valid,
                            int64_t max_p, const int32_t* __restrict__ uniq, const int32_t* __restrict__ n_rows,
                            int64_t max_rows, uint32_t sentinel, uint32_t* __restrict__ keys,
-                           uint32_t* __restrict__ vals) {
+                           uint32_t* __restrict__ vals, int32_t* __restrict__ seg_lo, int32_t* __restrict__ seg_hi) {
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (o < max_rows) {   // empty segments until k_seg_bounds records the real ones
+    seg_lo[o] = 0;
+    seg_hi[o] = 0;
+  }
   if (o >= max_q + max_p) return;
   int64_t node = -1;
   if (o < max_q) {
@@ -332,6 +336,17 @@ __global__ void k_occ_keys(const int32_t* __restrict__ q_node, const int32_t* __
   vals[o] = (uint32_t)o;
 }
 
+// seg_lo[row], seg_hi[row]: the sorted positions [lo, hi) holding row's occurrences.
+__global__ void k_seg_bounds(const uint32_t* __restrict__ keys, int64_t n, uint32_t sentinel,
+                             int32_t* __restrict__ seg_lo, int32_t* __restrict__ seg_hi) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n) return;
+  const uint32_t k = keys[p];
+  if (k == sentinel) return;
+  if (p == 0 || keys[p - 1] != k) seg_lo[k] = (int32_t)p;
+  if (p == n - 1 || keys[p + 1] != k) seg_hi[k] = (int32_t)(p + 1);
+}
+
 constexpr int SEG_TILE = 64;     // sorted occurrences per wave
 constexpr int SEG_MAXC = 8;      // columns per lane: width <= 512
 
@@ -348,6 +363,8 @@ struct SegCtx {
   float* S;           // [rows, W] complete sums
   float* head;        // [ntiles, W]
   float* tail;        // [ntiles, W]
+  const int32_t* seg_lo;   // [rows] first sorted position of the row
+  const int32_t* seg_hi;   // [rows] one past its last
 };
 
 __device__ __forceinline__ void seg_add(const SegCtx& c, uint32_t o, float* acc, int lane) {
@@ -365,6 +382,28 @@ __device__ __forceinline__ void seg_add(const SegCtx& c, uint32_t o, float* acc,
     for (int i = 0; i < SEG_MAXC; ++i) {
       const int col = lane + 64 * i;
       if (col >= c.dm && col < W) acc[i] += src[col - c.dm];
+    }
+  }
+}
+
+// The row of occurrence o spread over the lanes (zero outside its columns).
+__device__ __forceinline__ void seg_row(const SegCtx& c, uint32_t o, float* r, int lane) {
+  const int W = c.dm + c.w2;
+#pragma unroll
+  for (int i = 0; i < SEG_MAXC; ++i) r[i] = 0.f;
+  if ((int64_t)o < c.max_q) {
+    const float* src = c.dhq + (int64_t)o * c.ldq;
+#pragma unroll
+    for (int i = 0; i < SEG_MAXC; ++i) {
+      const int col = lane + 64 * i;
+      if (col < c.dm) r[i] = src[col];
+    }
+  } else {
+    const float* src = c.dkv + ((int64_t)o - c.max_q) * c.w2;
+#pragma unroll
+    for (int i = 0; i < SEG_MAXC; ++i) {
+      const int col = lane + 64 * i;
+      if (col >= c.dm && col < W) r[i] = src[col - c.dm];
     }
   }
 }
@@ -407,22 +446,24 @@ __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
     float acc[SEG_MAXC];
 #pragma unroll
     for (int i = 0; i < SEG_MAXC; ++i) acc[i] = 0.f;
-    for (int p = a; p < b; ++p) seg_add(c, __shfl(my_val, p, 64), acc, lane);
+    int p = a;
+    for (; p + 4 <= b; p += 4) {   // four rows in flight
+      const uint32_t o0 = __shfl(my_val, p, 64), o1 = __shfl(my_val, p + 1, 64);
+      const uint32_t o2 = __shfl(my_val, p + 2, 64), o3 = __shfl(my_val, p + 3, 64);
+      float r0[SEG_MAXC], r1[SEG_MAXC], r2[SEG_MAXC], r3[SEG_MAXC];
+      seg_row(c, o0, r0, lane);
+      seg_row(c, o1, r1, lane);
+      seg_row(c, o2, r2, lane);
+      seg_row(c, o3, r3, lane);
+#pragma unroll
+      for (int i = 0; i < SEG_MAXC; ++i) acc[i] += ((r0[i] + r1[i]) + r2[i]) + r3[i];
+    }
+    for (; p < b; ++p) seg_add(c, __shfl(my_val, p, 64), acc, lane);
     const bool before = a == 0 && key_before == key;
     const bool after = b == cnt && key_after == key;
     float* dst = before ? c.head + tile * W : (after ? c.tail + tile * W : c.S + (int64_t)key * W);
     seg_store(dst, acc, W, lane);
   }
-}
-
-__device__ __forceinline__ int64_t lower_bound_u32(const uint32_t* a, int64_t n, uint32_t v) {
-  int64_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int64_t mid = lo + ((hi - lo) >> 1);
-    if (a[mid] < v) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
 }
 
 // Block per row.  Rows inside one tile were written whole; a row spanning
@@ -435,8 +476,8 @@ __global__ __launch_bounds__(256) void k_segsum_fixup(SegCtx c, const int32_t* _
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   if (r >= eff_count(max_rows, n_rows)) return;
   const int W = c.dm + c.w2;
-  const int64_t a = lower_bound_u32(c.keys, c.n_occ, (uint32_t)r);
-  const int64_t b = lower_bound_u32(c.keys, c.n_occ, (uint32_t)r + 1);
+  const int64_t a = c.seg_lo[r];
+  const int64_t b = c.seg_hi[r];
   if (a == b) {   // no occurrence: zero gradient
     if (wid == 0) {
       float z[SEG_MAXC];
@@ -485,6 +526,7 @@ __global__ void k_copy_cols(const float* __restrict__ S, int64_t lds, const int3
 struct BwdWs {
   float *dm1, *dm_in, *dattn, *dqv, *dphi0, *dKV, *dphin, *S, *head, *tail, *dWkv, *dbkv;
   uint32_t *keys, *vals;
+  int32_t *seg_lo, *seg_hi;
   char* scratch;
   size_t scratch_bytes;
   size_t total;
@@ -512,6 +554,8 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   v.dbkv = (float*)take(sizeof(float) * 2 * s.da);
   v.keys = (uint32_t*)take(sizeof(uint32_t) * n_occ);
   v.vals = (uint32_t*)take(sizeof(uint32_t) * n_occ);
+  v.seg_lo = (int32_t*)take(sizeof(int32_t) * (max_rows > 0 ? max_rows : 1));
+  v.seg_hi = (int32_t*)take(sizeof(int32_t) * (max_rows > 0 ? max_rows : 1));
   size_t sc = radix_sort_ws_bytes(n_occ);
   auto mx = [&](size_t x) { if (x > sc) sc = x; };
   mx(linear_dw_ws_bytes(s.Q, s.da, s.da + s.dm));
@@ -647,12 +691,18 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   if (max_rows > 0) {
     const int64_t n_occ = Q + P;
     const uint32_t sentinel = (uint32_t)max_rows;
-    k_occ_keys<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(q_node, sv.pair_nbr, n_q, max_q, sv.n_valid, P, uniq,
-                                                           n_rows, max_rows, sentinel, b.keys, b.vals);
+    k_occ_keys<<<(unsigned)cdiv(n_occ > max_rows ? n_occ : max_rows, 256), 256, 0, s>>>(q_node, sv.pair_nbr, n_q, max_q, sv.n_valid, P, uniq,
+                                                           n_rows, max_rows, sentinel, b.keys, b.vals, b.seg_lo,
+                                                           b.seg_hi);
     MTGNN_CHECK_LAUNCH("occ_keys");
-    MTGNN_TRY(radix_sort_pairs(b.keys, b.vals, n_occ, bits_for(max_rows), sc, scb, s));
+    uint32_t* skeys = b.keys;
+    uint32_t* svals = b.vals;
+    MTGNN_TRY(radix_sort_pairs(&skeys, &svals, n_occ, bits_for(max_rows), sc, scb, s));
+    k_seg_bounds<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(skeys, n_occ, sentinel, b.seg_lo, b.seg_hi);
+    MTGNN_CHECK_LAUNCH("seg_bounds");
     SegCtx c;
-    c.keys = b.keys; c.vals = b.vals; c.n_occ = n_occ; c.sentinel = sentinel; c.max_q = max_q;
+    c.keys = skeys; c.vals = svals; c.n_occ = n_occ; c.sentinel = sentinel; c.max_q = max_q;
+    c.seg_lo = b.seg_lo; c.seg_hi = b.seg_hi;
     c.dhq = b.dm_in + da; c.ldq = ldm; c.dkv = b.dKV; c.dm = dm; c.w2 = 2 * da;
     c.S = b.S; c.head = b.head; c.tail = b.tail;
     const int64_t ntiles = cdiv(n_occ, SEG_TILE);

@@ -107,9 +107,12 @@ __device__ __forceinline__ float wave_max(float v) {
 // ------------------------------------------------------------------ library-internal primitives
 
 // Stable LSD radix sort of (key, value) pairs on the low `bits` bits of the key.
-// keys/vals are sorted in place (ping-pong through the workspace).
+// The passes ping-pong between the inputs and the first radix_sort_result_bytes(n)
+// of the workspace; *keys / *vals are updated to the buffers holding the result
+// (so that part of the workspace must stay untouched while the result is used).
 size_t radix_sort_ws_bytes(int64_t n);
-mtgnn_status radix_sort_pairs(uint32_t* keys, uint32_t* vals, int64_t n, int bits, void* ws, size_t ws_bytes,
+size_t radix_sort_result_bytes(int64_t n);
+mtgnn_status radix_sort_pairs(uint32_t** keys, uint32_t** vals, int64_t n, int bits, void* ws, size_t ws_bytes,
                               hipStream_t s);
 
 // Exclusive prefix sum of int32 counts; optional device total.

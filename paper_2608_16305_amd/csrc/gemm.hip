@@ -11,8 +11,15 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
   const int64_t e = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
   const int g = threadIdx.x >> 6;
   float s = 0.f;
-  if (e < rows * cols)
-    for (int z = g; z < nsplit; z += 4) s += part[(int64_t)z * split_stride + e];
+  if (e < rows * cols) {
+    int z = g;
+    for (; z + 12 < nsplit; z += 16) {   // four loads in flight
+      const float a0 = part[(int64_t)z * split_stride + e], a1 = part[(int64_t)(z + 4) * split_stride + e];
+      const float a2 = part[(int64_t)(z + 8) * split_stride + e], a3 = part[(int64_t)(z + 12) * split_stride + e];
+      s += ((a0 + a1) + a2) + a3;
+    }
+    for (; z < nsplit; z += 4) s += part[(int64_t)z * split_stride + e];
+  }
   red[g][threadIdx.x & 63] = s;
   __syncthreads();
   if (g != 0 || e >= rows * cols) return;

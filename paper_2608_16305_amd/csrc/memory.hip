@@ -242,11 +242,23 @@ __global__ __launch_bounds__(256) void k_timegrad_final(const float* __restrict_
   const int j = blockIdx.x * 64 + (threadIdx.x & 63);
   const int g = threadIdx.x >> 6;
   float sw = 0.f, sb = 0.f;
-  if (j < dt_dim)
-    for (int c = g; c < nch; c += 4) {
+  if (j < dt_dim) {
+    int c = g;
+    for (; c + 12 < nch; c += 16) {   // four chunks in flight
+      float w4[4], b4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        w4[u] = part[((int64_t)(c + 4 * u) * 2 + 0) * dt_dim + j];
+        b4[u] = part[((int64_t)(c + 4 * u) * 2 + 1) * dt_dim + j];
+      }
+      sw += ((w4[0] + w4[1]) + w4[2]) + w4[3];
+      sb += ((b4[0] + b4[1]) + b4[2]) + b4[3];
+    }
+    for (; c < nch; c += 4) {
       sw += part[((int64_t)c * 2 + 0) * dt_dim + j];
       sb += part[((int64_t)c * 2 + 1) * dt_dim + j];
     }
+  }
   rw[g][threadIdx.x & 63] = sw;
   rb[g][threadIdx.x & 63] = sb;
   __syncthreads();
@@ -321,7 +333,7 @@ mtgnn_status build_queries_impl(const mtgnn_batch* b, const int32_t* neg, int32_
 
 size_t aggregate_last_ws(int64_t n) {
   const int64_t nm = 2 * n;
-  return 4 * a256(sizeof(int32_t) * nm) + radix_sort_ws_bytes(nm) + scan_ws_bytes(nm);
+  return 4 * a256(sizeof(int32_t) * nm) + radix_sort_ws_bytes(nm) + radix_sort_result_bytes(nm) + scan_ws_bytes(nm);
 }
 
 mtgnn_status aggregate_last_impl(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
@@ -347,10 +359,11 @@ mtgnn_status aggregate_last_impl(const mtgnn_batch* b, int64_t n_nodes, int32_t*
   const unsigned grid = (unsigned)cdiv(nm, 256);
   k_agg_keys<<<grid, 256, 0, s>>>(b->src, b->dst, b->flags, n, sentinel, keys, vals);
   MTGNN_CHECK_LAUNCH("agg_keys");
-  MTGNN_TRY(radix_sort_pairs(keys, vals, nm, bits_for(n_nodes), w, rest, s));
+  MTGNN_TRY(radix_sort_pairs(&keys, &vals, nm, bits_for(n_nodes), w, rest, s));
   k_agg_last_flags<<<grid, 256, 0, s>>>(keys, nm, sentinel, is_last);
   MTGNN_CHECK_LAUNCH("agg_last_flags");
-  MTGNN_TRY(scan_exclusive(is_last, pos, nm, n_uniq, w, rest, s));
+  const size_t keep = radix_sort_result_bytes(nm);   // the sorted pairs may live there
+  MTGNN_TRY(scan_exclusive(is_last, pos, nm, n_uniq, w + keep, rest - keep, s));
   k_agg_write<<<grid, 256, 0, s>>>(keys, vals, is_last, pos, nm, uniq, winner);
   MTGNN_CHECK_LAUNCH("agg_write");
   return MTGNN_OK;

@@ -226,9 +226,13 @@ size_t radix_sort_ws_bytes(int64_t n) {
   return 2 * align256(sizeof(uint32_t) * n) + 2 * align256(sizeof(int32_t) * nc) + scan_ws_bytes(nc);
 }
 
-mtgnn_status radix_sort_pairs(uint32_t* keys, uint32_t* vals, int64_t n, int bits, void* ws, size_t ws_bytes,
+size_t radix_sort_result_bytes(int64_t n) { return 2 * align256(sizeof(uint32_t) * n); }
+
+mtgnn_status radix_sort_pairs(uint32_t** keys_io, uint32_t** vals_io, int64_t n, int bits, void* ws, size_t ws_bytes,
                               hipStream_t s) {
   if (n <= 1) return MTGNN_OK;
+  uint32_t* keys = *keys_io;
+  uint32_t* vals = *vals_io;
   if (ws_bytes < radix_sort_ws_bytes(n)) return MTGNN_EWORKSPACE;
   const int64_t nblk = cdiv(n, SORT_TILE);
   const int64_t nc = nblk * RADIX;
@@ -255,13 +259,9 @@ mtgnn_status radix_sort_pairs(uint32_t* keys, uint32_t* vals, int64_t n, int bit
     t = ki; ki = ko; ko = t;
     t = vi; vi = vo; vo = t;
   }
-  if (passes & 1) {
-    if (hipMemcpyAsync(keys, ki, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s) != hipSuccess ||
-        hipMemcpyAsync(vals, vi, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s) != hipSuccess) {
-      set_hip_error(hipGetLastError(), "radix_sort copy-back");
-      return MTGNN_EHIP;
-    }
-  }
+  (void)passes;
+  *keys_io = ki;   // the buffer holding the sorted pairs (the inputs or the first two workspace arrays)
+  *vals_io = vi;
   return MTGNN_OK;
 }
 

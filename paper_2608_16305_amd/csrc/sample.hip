@@ -108,7 +108,7 @@ mtgnn_status build_csr_impl(const int32_t* src, const int32_t* dst, const float*
   if (ne > 0) {
     k_csr_keys<<<(unsigned)cdiv(ne, 256), 256, 0, s>>>(src, dst, n_events, keys, vals);
     MTGNN_CHECK_LAUNCH("csr_keys");
-    MTGNN_TRY(radix_sort_pairs(keys, vals, ne, bits_for(n_nodes - 1), w, ws_bytes - (size_t)(w - (char*)ws), s));
+    MTGNN_TRY(radix_sort_pairs(&keys, &vals, ne, bits_for(n_nodes - 1), w, ws_bytes - (size_t)(w - (char*)ws), s));
   }
   k_csr_offsets<<<(unsigned)cdiv(n_nodes + 1, 256), 256, 0, s>>>(keys, ne, n_nodes, off);
   MTGNN_CHECK_LAUNCH("csr_offsets");
