@@ -38,11 +38,19 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for the CPU baseline (0: skip)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="before the warmup, copy a buffer of this many MiB twice (HBM counter calibration)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a run made with "
+                         "--copy-probe into the traffic record under profiles/, then exit")
     return ap.parse_args()
 
 
 def main():
     args = parse()
+    if args.traffic_from:
+        write_traffic(args)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the multi-GPU sharding is described, not built.", file=sys.stderr)
@@ -75,6 +83,16 @@ def main():
 
     from paper_2608_16305_amd import mtgnn as M
 
+    if args.copy_probe > 0:   # plain device copies of known size, just before the first step
+        n = args.copy_probe * (1 << 20) // 4
+        xa = torch.randn(n, device="cuda")
+        ya = torch.empty_like(xa)
+        torch.cuda.synchronize()
+        for _ in range(2):
+            ya.copy_(xa)
+        torch.cuda.synchronize()
+        del xa, ya
+
     # warmup; the matrix-product sites over the neighbour slots are timed one
     # warmup step each to pick the dominant one
     site_ms = {}
@@ -105,7 +123,7 @@ def main():
     target_events = sum(n_tar[args.warmup:])
 
     out = {
-        "metric": "events/sec per batch step (fwd+bwd) on 1 MI355X",
+        "metric": "events/sec per batch step (fwd+bwd) on 1 MI355X; % HBM / MFMA roofline",
         "value": value,
         "unit": "events/s",
         "n_gpus": 1,
@@ -137,7 +155,7 @@ def main():
     peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
     achieved = flops / avg_s / 1e12
     out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                       "frac": achieved / peak, "traffic": None, "kernel": dominant,
+                       "frac": achieved / peak, "traffic": read_traffic(dominant, w), "kernel": dominant,
                        "launches_per_step": launches_per_step, "avg_launch_us": avg_s * 1e6,
                        "flops_per_launch": flops}
 
@@ -178,6 +196,92 @@ def valid_slots(runner, s, w, b):
         lo, hi = off[n], off[n + 1]
         cnt += min(w.k, int(np.searchsorted(ct[lo:hi], tau, side="left")))
     return cnt
+
+
+# ------------------------------------------------------------------ HBM traffic from counter runs
+
+CSRC = os.path.join(ROOT, "paper_2608_16305_amd", "csrc")
+# sources that define the hot-site kernels and their launches
+TRAFFIC_SOURCES = ("common.h", "gemm.h", "gemm.hip", "gemm_nt.hip", "gemm_nn.hip", "gemm_tn.hip", "attention.hip")
+
+
+def kernel_fingerprint():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def traffic_path(w):
+    return os.path.join(ROOT, "profiles", f"hot-sites-{w.name}.traffic.json")
+
+
+def read_traffic(site, w):
+    """HBM bytes per launch of `site` from the committed counter record, or None when
+    there is none or the kernel sources changed since the counters were taken."""
+    p = traffic_path(w)
+    if not os.path.exists(p):
+        return None
+    with open(p) as fh:
+        rec = json.load(fh)
+    if rec.get("fingerprint") != kernel_fingerprint() or site not in rec.get("sites", {}):
+        return None
+    return rec["sites"][site]["bytes_per_launch"]
+
+
+def _site_of(name):
+    for site, tag in (("gemm_kv_proj", "KvProj"), ("gemm_kv_dw", "KvDw"), ("gemm_kv_dx", "KvDx")):
+        if f"site::{tag}," in name:
+            return site
+    return None
+
+
+def _counter_rows(path, counter):
+    import csv
+    with open(path) as fh:
+        rows = [r for r in csv.DictReader(fh) if r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def _calibrated(path, counter, probe_bytes):
+    """Per-site mean counter value (KiB per dispatch) scaled by the copy-probe factor."""
+    rows = _counter_rows(path, counter)
+    first_step = next(i for i, r in enumerate(rows) if "k_agg_keys" in r["Kernel_Name"])
+    probes = [r for r in rows[:first_step] if "copyBuffer" in r["Kernel_Name"]][-2:]
+    if len(probes) != 2:
+        raise SystemExit(f"{path}: the two probe copies before the first step were not found")
+    probe_kib = sum(float(r["Counter_Value"]) for r in probes) / 2
+    factor = probe_bytes / 1024.0 / probe_kib
+    per = {}
+    for r in rows[first_step:]:
+        site = _site_of(r["Kernel_Name"])
+        if site:
+            per.setdefault(site, []).append(float(r["Counter_Value"]))
+    return {k: (sum(v) / len(v)) * factor * 1024.0 for k, v in per.items()}, factor, probe_kib, \
+        {k: len(v) for k, v in per.items()}
+
+
+def write_traffic(args):
+    from synth import workload
+    w = workload(args.workload)
+    probe = args.copy_probe * (1 << 20)
+    if probe <= 0:
+        raise SystemExit("--traffic-from needs --copy-probe MIB (the probe size of the counter runs)")
+    fetch, ff, fkib, nf = _calibrated(args.traffic_from[0], "FETCH_SIZE", probe)
+    write, fw, wkib, nw = _calibrated(args.traffic_from[1], "WRITE_SIZE", probe)
+    sites = {s: {"fetch_bytes_per_launch": fetch[s], "write_bytes_per_launch": write[s],
+                 "bytes_per_launch": fetch[s] + write[s], "dispatches": nf[s]} for s in fetch if s in write}
+    rec = {"workload": w.name, "fingerprint": kernel_fingerprint(), "probe_bytes": probe,
+           "probe_fetch_kib": fkib, "probe_write_kib": wkib, "fetch_factor": ff, "write_factor": fw,
+           "sites": sites}
+    os.makedirs(os.path.dirname(traffic_path(w)), exist_ok=True)
+    with open(traffic_path(w), "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec))
 
 
 def cpu_baseline(w, s, params, mem, lu, b0, n):
