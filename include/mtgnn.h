@@ -137,10 +137,14 @@ mtgnn_status mtgnn_build_queries(const mtgnn_batch* b, const int32_t* neg, int32
  * 2i+1 to dst[i] (role 1).  For each node that receives a message, the winner
  * is its message with the largest (t, eid, role).  Under the batch order
  * precondition that is the largest message index; a self-loop's role 1 wins.
- *   uniq   -- [2 b->n] out: receiving nodes, ascending;
- *   winner -- [2 b->n] out: winner message index (2i + role) per uniq entry;
+ *   uniq   -- [2 b->n] out: receiving nodes, one row each, in increasing order
+ *             of their winning message (the order of each node's last message
+ *             in the batch);
+ *   winner -- [2 b->n] out: winner message index (2i + role) per uniq entry,
+ *             so winner[0 .. n_uniq) is strictly increasing;
  *   n_uniq -- device int32 out: number of entries written.
- * Integer-exact.  No float atomics. */
+ * The workspace holds an n_nodes-entry node table (no initialisation needed).
+ * Integer-exact and deterministic: integer max per node, fixed-order compaction. */
 mtgnn_status mtgnn_aggregate_last(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
                                   int32_t* n_uniq, void* ws, size_t ws_bytes, hipStream_t stream);
 

@@ -137,7 +137,7 @@ size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int6
   if (max_rows < 0 || max_q < 0) return 0;
   switch (op) {
     case MTGNN_OP_BUILD_QUERIES: return build_queries_ws(max_rows);
-    case MTGNN_OP_AGGREGATE_LAST: return aggregate_last_ws(max_rows);
+    case MTGNN_OP_AGGREGATE_LAST: return aggregate_last_ws(max_rows, d ? d->n_nodes : 0);
     case MTGNN_OP_BUILD_MESSAGES: return 0;
     case MTGNN_OP_SAMPLE_RECENT: return 0;
     case MTGNN_OP_BUILD_CSR: return build_csr_ws(max_rows, d ? d->n_nodes : 0);
@@ -180,7 +180,7 @@ mtgnn_status mtgnn_aggregate_last(const mtgnn_batch* b, int64_t n_nodes, int32_t
   REQ(uniq, "uniq");
   REQ(winner, "winner");
   REQ(n_uniq, "n_uniq");
-  if (ws_bytes < aggregate_last_ws(b->n)) return fail(MTGNN_EWORKSPACE, "aggregate_last ws");
+  if (ws_bytes < aggregate_last_ws(b->n, n_nodes)) return fail(MTGNN_EWORKSPACE, "aggregate_last ws");
   if (b->n > 0 && !ws) return fail(MTGNN_EINVAL, "ws is NULL");
   return aggregate_last_impl(b, n_nodes, uniq, winner, n_uniq, ws, ws_bytes, stream);
 }

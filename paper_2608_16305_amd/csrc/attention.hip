@@ -24,11 +24,11 @@ namespace {
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct AttnShape {
-  int64_t Q, P;
+  int64_t Q, P, N;
   int dm, dt, de, da, H, dh, k, Dq, Dkv;
   size_t esz;   // bytes per weight element
   explicit AttnShape(const mtgnn_dims* d, int64_t max_q) {
-    Q = max_q; k = d->k; P = max_q * k;
+    Q = max_q; k = d->k; P = max_q * k; N = d->n_nodes;
     dm = d->d_mem; dt = d->d_time; de = d->d_edge; da = d->d_attn; H = d->n_heads; dh = da / H;
     Dq = dm + dt; Dkv = dm + de + dt;
     esz = d->dtype == MTGNN_F32 ? 4 : 2;
@@ -301,19 +301,28 @@ __global__ void k_split_kv_grads(const float* __restrict__ dW, const float* __re
 
 // ---------------------------------------------------------------- d M' by node (deterministic)
 
-// Occurrence o < Q is query o; o >= Q is compact slot o - Q.  Its key is the
-// row of its node in `uniq` (ascending), or `sentinel` when the node was not
-// updated this step, or the query / slot is beyond the device counts.
+// Node -> row map for the rows updated this step, plus empty segment bounds.
+// The map lives in the workspace and is not cleared: a lookup is accepted only
+// if it names a row r < n_rows with uniq[r] equal to the node, so stale
+// entries are rejected.
+__global__ void k_row_map(const int32_t* __restrict__ uniq, const int32_t* __restrict__ n_rows, int64_t max_rows,
+                          int32_t* __restrict__ row_of, int32_t* __restrict__ seg_lo, int32_t* __restrict__ seg_hi) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= max_rows) return;
+  seg_lo[r] = 0;   // empty segments until k_seg_bounds records the real ones
+  seg_hi[r] = 0;
+  if (r < eff_count(max_rows, n_rows)) row_of[uniq[r]] = (int32_t)r;
+}
+
+// Occurrence o < max_q is query o; o = max_q + p is compact slot p.  Its key is
+// the row of its node among the rows updated this step, or `sentinel` when
+// the node was not updated, or the query / slot is beyond the device counts.
 __global__ void k_occ_keys(const int32_t* __restrict__ q_node, const int32_t* __restrict__ pair_nbr,
                            const int32_t* __restrict__ n_q, int64_t max_q, const int32_t* __restrict__ n_valid,
                            int64_t max_p, const int32_t* __restrict__ uniq, const int32_t* __restrict__ n_rows,
-                           int64_t max_rows, uint32_t sentinel, uint32_t* __restrict__ keys,
-                           uint32_t* __restrict__ vals, int32_t* __restrict__ seg_lo, int32_t* __restrict__ seg_hi) {
+                           int64_t max_rows, const int32_t* __restrict__ row_of, uint32_t sentinel,
+                           uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (o < max_rows) {   // empty segments until k_seg_bounds records the real ones
-    seg_lo[o] = 0;
-    seg_hi[o] = 0;
-  }
   if (o >= max_q + max_p) return;
   int64_t node = -1;
   if (o < max_q) {
@@ -323,14 +332,8 @@ __global__ void k_occ_keys(const int32_t* __restrict__ q_node, const int32_t* __
   }
   uint32_t key = sentinel;
   if (node >= 0) {
-    const int64_t nr = eff_count(max_rows, n_rows);
-    int64_t a = 0, b = nr;
-    while (a < b) {
-      const int64_t mid = a + ((b - a) >> 1);
-      if ((int64_t)uniq[mid] < node) a = mid + 1;
-      else b = mid;
-    }
-    if (a < nr && uniq[a] == node) key = (uint32_t)a;
+    const int32_t r = row_of[node];
+    if (r >= 0 && r < eff_count(max_rows, n_rows) && uniq[r] == node) key = (uint32_t)r;
   }
   keys[o] = key;
   vals[o] = (uint32_t)o;
@@ -466,52 +469,67 @@ __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   }
 }
 
-// Block per row.  Rows inside one tile were written whole; a row spanning
-// tiles t0..t1 is tail[t0] + head[t0+1] + ... + head[t1]: the 4 waves sum
-// interleaved heads, then the partial sums are added in wave order.
+// Block b: wave w first zeroes row 4b + w if that row has no occurrence.
+// Then, if the row at the end of tile b starts in tile b and continues past
+// it (rows inside one tile were written whole), the block sums that row:
+// tail[b] + head[b+1] + ... + head[t1].  The 4 waves take interleaved heads
+// with four loads in flight; their partial sums are added in wave order.
 __global__ __launch_bounds__(256) void k_segsum_fixup(SegCtx c, const int32_t* __restrict__ n_rows,
-                                                      int64_t max_rows) {
+                                                      int64_t max_rows, int64_t ntiles) {
   __shared__ float part[4][SEG_MAXC * 64];
-  const int64_t r = blockIdx.x;
+  const int64_t blk = blockIdx.x;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  if (r >= eff_count(max_rows, n_rows)) return;
   const int W = c.dm + c.w2;
-  const int64_t a = c.seg_lo[r];
-  const int64_t b = c.seg_hi[r];
-  if (a == b) {   // no occurrence: zero gradient
-    if (wid == 0) {
-      float z[SEG_MAXC];
+  const int64_t zr = blk * 4 + wid;
+  if (zr < eff_count(max_rows, n_rows) && c.seg_lo[zr] == c.seg_hi[zr]) {   // no occurrence: zero gradient
+    float z[SEG_MAXC];
 #pragma unroll
-      for (int i = 0; i < SEG_MAXC; ++i) z[i] = 0.f;
-      seg_store(c.S + r * W, z, W, lane);
-    }
-    return;
+    for (int i = 0; i < SEG_MAXC; ++i) z[i] = 0.f;
+    seg_store(c.S + zr * W, z, W, lane);
   }
-  const int64_t t0 = a / SEG_TILE, t1 = (b - 1) / SEG_TILE;
-  if (t0 == t1) return;   // written whole by its tile
+  // the rest depends on the block only (uniform branches around the barrier)
+  if (blk >= ntiles) return;
+  const int64_t p_last = min((blk + 1) * SEG_TILE, c.n_occ) - 1;
+  if (p_last + 1 >= c.n_occ) return;
+  const uint32_t key = c.keys[p_last];
+  if (key == c.sentinel || c.keys[p_last + 1] != key) return;
+  if (c.seg_lo[key] < blk * SEG_TILE) return;   // started in an earlier tile, whose block sums it
+  const int64_t t1 = (c.seg_hi[key] - 1) / SEG_TILE;
   float acc[SEG_MAXC];
 #pragma unroll
   for (int i = 0; i < SEG_MAXC; ++i) acc[i] = 0.f;
-  for (int64_t t = t0 + 1 + wid; t <= t1; t += 4) {
-    const float* src = c.head + t * W;
+  int64_t t = blk + 1 + wid;
+  for (; t + 12 <= t1; t += 16) {
+    const float* h0 = c.head + t * W;
+    const float* h1 = h0 + 4 * (int64_t)W;
+    const float* h2 = h0 + 8 * (int64_t)W;
+    const float* h3 = h0 + 12 * (int64_t)W;
 #pragma unroll
     for (int i = 0; i < SEG_MAXC; ++i) {
       const int col = lane + 64 * i;
-      if (col < W) acc[i] += src[col];
+      if (col < W) acc[i] += ((h0[col] + h1[col]) + h2[col]) + h3[col];
+    }
+  }
+  for (; t <= t1; t += 4) {
+    const float* h = c.head + t * W;
+#pragma unroll
+    for (int i = 0; i < SEG_MAXC; ++i) {
+      const int col = lane + 64 * i;
+      if (col < W) acc[i] += h[col];
     }
   }
 #pragma unroll
   for (int i = 0; i < SEG_MAXC; ++i) part[wid][i * 64 + lane] = acc[i];
   __syncthreads();
   if (wid != 0) return;
-  const float* tl = c.tail + t0 * W;
+  const float* tl = c.tail + blk * W;
 #pragma unroll
   for (int i = 0; i < SEG_MAXC; ++i) {
     const int col = lane + 64 * i;
     const int o = i * 64 + lane;
     if (col < W) acc[i] = tl[col] + (((part[0][o] + part[1][o]) + part[2][o]) + part[3][o]);
   }
-  seg_store(c.S + r * W, acc, W, lane);
+  seg_store(c.S + (int64_t)key * W, acc, W, lane);
 }
 
 __global__ void k_copy_cols(const float* __restrict__ S, int64_t lds, const int32_t* __restrict__ n_rows,
@@ -526,7 +544,7 @@ __global__ void k_copy_cols(const float* __restrict__ S, int64_t lds, const int3
 struct BwdWs {
   float *dm1, *dm_in, *dattn, *dqv, *dphi0, *dKV, *dphin, *S, *head, *tail, *dWkv, *dbkv;
   uint32_t *keys, *vals;
-  int32_t *seg_lo, *seg_hi;
+  int32_t *seg_lo, *seg_hi, *row_of;
   char* scratch;
   size_t scratch_bytes;
   size_t total;
@@ -556,6 +574,7 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   v.vals = (uint32_t*)take(sizeof(uint32_t) * n_occ);
   v.seg_lo = (int32_t*)take(sizeof(int32_t) * (max_rows > 0 ? max_rows : 1));
   v.seg_hi = (int32_t*)take(sizeof(int32_t) * (max_rows > 0 ? max_rows : 1));
+  v.row_of = (int32_t*)take(sizeof(int32_t) * s.N);
   size_t sc = radix_sort_ws_bytes(n_occ);
   auto mx = [&](size_t x) { if (x > sc) sc = x; };
   mx(linear_dw_ws_bytes(s.Q, s.da, s.da + s.dm));
@@ -691,9 +710,10 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   if (max_rows > 0) {
     const int64_t n_occ = Q + P;
     const uint32_t sentinel = (uint32_t)max_rows;
-    k_occ_keys<<<(unsigned)cdiv(n_occ > max_rows ? n_occ : max_rows, 256), 256, 0, s>>>(q_node, sv.pair_nbr, n_q, max_q, sv.n_valid, P, uniq,
-                                                           n_rows, max_rows, sentinel, b.keys, b.vals, b.seg_lo,
-                                                           b.seg_hi);
+    k_row_map<<<(unsigned)cdiv(max_rows, 256), 256, 0, s>>>(uniq, n_rows, max_rows, b.row_of, b.seg_lo, b.seg_hi);
+    MTGNN_CHECK_LAUNCH("row_map");
+    k_occ_keys<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(q_node, sv.pair_nbr, n_q, max_q, sv.n_valid, P, uniq,
+                                                           n_rows, max_rows, b.row_of, sentinel, b.keys, b.vals);
     MTGNN_CHECK_LAUNCH("occ_keys");
     uint32_t* skeys = b.keys;
     uint32_t* svals = b.vals;
@@ -708,7 +728,8 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     const int64_t ntiles = cdiv(n_occ, SEG_TILE);
     k_segsum_tiles<<<(unsigned)cdiv(ntiles, 4), 256, 0, s>>>(c);
     MTGNN_CHECK_LAUNCH("segsum_tiles");
-    k_segsum_fixup<<<(unsigned)max_rows, 256, 0, s>>>(c, n_rows, max_rows);
+    const int64_t nfix = ntiles > cdiv(max_rows, 4) ? ntiles : cdiv(max_rows, 4);
+    k_segsum_fixup<<<(unsigned)nfix, 256, 0, s>>>(c, n_rows, max_rows, ntiles);
     MTGNN_CHECK_LAUNCH("segsum_fixup");
     const int W = dm + 2 * da;
     k_copy_cols<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(b.S, W, n_rows, max_rows, dm, d_mem, dm);

@@ -58,7 +58,46 @@ struct GemmArgs {
   int a_vec = 0, b_vec = 0;    // 4-wide loads along the contiguous dimension are aligned (set by the launcher)
   int64_t ones_col = -1;       // B column treated as all ones (-1: none); its results go to col_out
   float* col_out = nullptr;    // C(i, ones_col) is written to col_out[i] (weight-grad GEMMs: the bias grad)
+  int xcd_group = 1;           // place blocks that share an operand chunk on one XCD (see gemm_tile)
+  int tile_bn = 0;             // host-side plan: output tile width (0: chosen by gemm_tile_width)
+  int tile_bk = 16;            // host-side plan: k step (64 only for weight-gradient 64-wide tiles)
 };
+
+// Tile coordinates of this block.  Workgroups are dispatched round-robin over
+// the 8 XCDs (block L runs on XCD L mod 8), and each XCD has its own L2.  The
+// blocks that read the same operand chunk form a group: with split-K, the
+// blocks of one k-chunk (they all read the same rows of the row-indexed
+// operand); otherwise the column strips of one row block (same A rows).
+// Group q is placed on XCD q mod 8, so a group's blocks share that XCD's L2,
+// and consecutive groups still spread over every XCD (a device-side row count
+// that leaves only the first groups active keeps all XCDs busy).  Groups past
+// the last multiple of 8 keep the plain order.
+struct TileCoord {
+  int64_t x, y, z;
+};
+__device__ __forceinline__ TileCoord gemm_tile(int xcd_group) {
+  const uint32_t gx = gridDim.x, gy = gridDim.y, gz = gridDim.z;
+  const uint32_t L = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  uint32_t V = L;
+  const uint32_t G = gz > 1 ? gx * gy : gy;       // blocks per group
+  const uint32_t ngroups = gz > 1 ? gz : gx;
+  const uint32_t full = G * (ngroups & ~7u);
+  if (xcd_group && G > 1 && L < full) {
+    const uint32_t xcd = L & 7u, slot = L >> 3;
+    V = (xcd + 8u * (slot / G)) * G + slot % G;
+  }
+  TileCoord t;
+  if (gz > 1) {   // V = (z * gx + x) * gy + y
+    t.y = V % gy;
+    t.x = (V / gy) % gx;
+    t.z = V / (gy * gx);
+  } else {        // V = x * gy + y
+    t.y = V % gy;
+    t.x = V / gy;
+    t.z = 0;
+  }
+  return t;
+}
 
 // Epilogue rounding of a float32 value to the nearest bfloat16 (ties to even), widened back.
 __device__ __forceinline__ float round_to_bf16(float v) { return bf16_to_f32(f32_to_bf16(v)); }
@@ -240,10 +279,11 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
 
   const int64_t M = eff_count(g.M, g.M_dev);
   const int64_t Kall = eff_count(g.K, g.K_dev);
-  const int64_t row0 = (int64_t)blockIdx.x * BM;
-  const int64_t col0 = (int64_t)blockIdx.y * BN;
+  const TileCoord tc = gemm_tile(g.xcd_group);
+  const int64_t row0 = tc.x * BM;
+  const int64_t col0 = tc.y * BN;
   if (row0 >= M) return;
-  const int64_t kbeg = (int64_t)blockIdx.z * g.kchunk;
+  const int64_t kbeg = tc.z * g.kchunk;
   const int64_t kend = min(Kall, kbeg + g.kchunk);
 
   const TA* A = (const TA*)g.A;
@@ -325,7 +365,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
   }
 
   // epilogue: bias, accumulate, ReLU gate / pre-activation, bf16 rounding, bias-grad column
-  float* C = g.C + (int64_t)blockIdx.z * g.c_split_stride;
+  float* C = g.C + tc.z * g.c_split_stride;
   const bool split = g.c_split_stride != 0;
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
@@ -363,22 +403,39 @@ __global__ void k_splitk_reduce(const float* __restrict__ part, int64_t split_st
 
 // Strip width for an output of N columns: one strip when N <= 256, else equal strips.
 int gemm_strip_width(int64_t N);
-void dw_split(int64_t R, int64_t N, int64_t K, int& ksplit, int64_t& kchunk);
+// Tile width for an M x N output: full strips, or 64-wide tiles when strips would
+// leave the launch with few blocks (small row counts are latency-bound).
+int gemm_tile_width(int64_t M, int64_t N, int ksplit);
+// Weight-gradient plan over R reduction rows for an N x K output.
+struct DwPlan {
+  int ksplit;
+  int64_t kchunk;
+  int bn, bk;
+};
+DwPlan dw_plan(int64_t R, int64_t N, int64_t K);
 
 // A 4-wide load along the contiguous dimension is aligned when the base and the other stride are.
 inline bool vec_ok(const void* p, int64_t other_stride, size_t esz) {
   return ((uintptr_t)p % (4 * esz)) == 0 && (other_stride % 4) == 0;
 }
 
-template <class Site, int BN, bool VEC, typename TA, typename TB, bool AK, bool BK>
+template <class Site, int BN, bool VEC, typename TA, typename TB, bool AK, bool BK, int KSTEP = G_BK>
 void gemm_kernel_launch(const GemmArgs& g, dim3 grid, hipStream_t s) {
-  k_gemm<Site, BN, G_WM, G_BK, G_NBUF, VEC, TA, TB, AK, BK><<<grid, G_THREADS, 0, s>>>(g);
+  k_gemm<Site, BN, G_WM, KSTEP, G_NBUF, VEC, TA, TB, AK, BK><<<grid, G_THREADS, 0, s>>>(g);
 }
 
 template <class Site, bool VEC, typename TA, typename TB, bool AK, bool BK>
 void gemm_bn_launch(const GemmArgs& g, int bn, dim3 grid, hipStream_t s) {
   switch (bn) {
-    case 64: gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK>(g, grid, s); break;
+    case 64:
+      if constexpr (!AK && !BK) {   // weight gradients: 64-deep k steps on 64 x 64 tiles
+        if (g.tile_bk == 64) {
+          gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK, 64>(g, grid, s);
+          break;
+        }
+      }
+      gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK>(g, grid, s);
+      break;
     case 128: gemm_kernel_launch<Site, 128, VEC, TA, TB, AK, BK>(g, grid, s); break;
     case 160: gemm_kernel_launch<Site, 160, VEC, TA, TB, AK, BK>(g, grid, s); break;
     case 208: gemm_kernel_launch<Site, 208, VEC, TA, TB, AK, BK>(g, grid, s); break;
@@ -391,7 +448,7 @@ mtgnn_status gemm_launch_t(const GemmArgs& g0, int ksplit, hipStream_t s) {
   GemmArgs g = g0;
   g.a_vec = vec_ok(g.A, AK ? g.a_si : g.a_sk, sizeof(TA)) ? 1 : 0;   // general loader: 4-wide only when aligned
   g.b_vec = vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) ? 1 : 0;
-  const int bn = gemm_strip_width(g.N);
+  const int bn = g.tile_bn > 0 ? g.tile_bn : gemm_tile_width(g.M, g.N, ksplit);
   dim3 grid((unsigned)cdiv(g.M, 64 * G_WM), (unsigned)cdiv(g.N, bn), (unsigned)(ksplit < 1 ? 1 : ksplit));
   // The branch-free loader needs 4-aligned bases and strides, row counts of
   // each operand's contiguous dimension that are multiples of 4, a virtual
@@ -461,11 +518,13 @@ template <class Site = site::Generic>
 mtgnn_status linear_dw(const float* dy, int64_t lddy, const void* x, int x_dtype, int64_t ldx, float* dW,
                        int64_t lddw, int64_t R, const int32_t* R_dev, int64_t N, int64_t K, void* ws,
                        size_t ws_bytes, hipStream_t s, float* db = nullptr) {
-  int ksplit;
-  int64_t kchunk;
   const int64_t Kc = db ? K + 1 : K;   // extra all-ones column of x gives the bias gradient
-  dw_split(R, N, Kc, ksplit, kchunk);
+  const DwPlan plan = dw_plan(R, N, Kc);
+  const int ksplit = plan.ksplit;
+  const int64_t kchunk = plan.kchunk;
   GemmArgs g{};
+  g.tile_bn = plan.bn;
+  g.tile_bk = plan.bk;
   g.M = N; g.N = Kc; g.K = R; g.K_dev = R_dev;
   if (db) { g.ones_col = K; g.col_out = db; }
   g.A = dy; g.a_si = 1; g.a_sk = lddy;

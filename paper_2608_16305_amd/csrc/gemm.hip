@@ -39,23 +39,41 @@ int gemm_strip_width(int64_t N) {
   return 256;
 }
 
-// Split the reduction over R rows so that the grid has roughly 512 blocks.
-void dw_split(int64_t R, int64_t N, int64_t K, int& ksplit, int64_t& kchunk) {
-  const int64_t tiles = cdiv(N, 64 * G_WM) * cdiv(K, gemm_strip_width(K));
-  int64_t want = cdiv(1024, tiles);
-  const int64_t maxs = cdiv(R < 1 ? 1 : R, 64);
-  if (want > maxs) want = maxs;
-  if (want < 1) want = 1;
-  if (want > 256) want = 256;
-  kchunk = cdiv(cdiv(R < 1 ? 1 : R, want), G_BK) * G_BK;
-  ksplit = (int)cdiv(R < 1 ? 1 : R, kchunk);
+int gemm_tile_width(int64_t M, int64_t N, int ksplit) {
+  const int full = gemm_strip_width(N);
+  const int64_t blocks = cdiv(M, 64 * G_WM) * cdiv(N, full) * (ksplit < 1 ? 1 : ksplit);
+  return blocks < 1024 ? 64 : full;
+}
+
+// Up to 16 K reduction rows, 64 x 64 tiles over 128-row chunks (each block one
+// short reduction; the grid is tiles x chunks).  Larger reductions keep full
+// strips and cut the rows into chunks of >= 256 so the grid has about 1536
+// blocks at the host row maximum (device-side counts often leave fewer active).
+DwPlan dw_plan(int64_t R, int64_t N, int64_t K) {
+  DwPlan p;
+  const int64_t r = R < 1 ? 1 : R;
+  if (r <= 16384) {
+    p.bn = 64;
+    p.bk = 64;
+    p.kchunk = 128;
+  } else {
+    p.bn = gemm_strip_width(K);
+    p.bk = G_BK;
+    const int64_t tiles = cdiv(N, 64 * G_WM) * cdiv(K, p.bn);
+    int64_t want = cdiv(1536, tiles);
+    if (want > 512) want = 512;
+    if (want < 1) want = 1;
+    p.kchunk = cdiv(cdiv(r, want), G_BK) * G_BK;
+    if (p.kchunk < 256) p.kchunk = 256;
+  }
+  p.ksplit = (int)cdiv(r, p.kchunk);
+  if (p.ksplit == 1) p.kchunk = r;
+  return p;
 }
 
 size_t linear_dw_ws_bytes(int64_t R, int64_t N, int64_t K) {
-  int ks;
-  int64_t kc;
-  dw_split(R, N, K + 1, ks, kc);
-  return ks > 1 ? sizeof(float) * (size_t)ks * N * (K + 1) : 0;
+  const DwPlan p = dw_plan(R, N, K + 1);
+  return p.ksplit > 1 ? sizeof(float) * (size_t)p.ksplit * N * (K + 1) : 0;
 }
 
 }  // namespace mtgnn

@@ -56,34 +56,107 @@ __global__ void k_queries_masked(const int32_t* __restrict__ src, const int32_t*
 
 // Message m = 2i + role goes to src[i] (role 0) or dst[i] (role 1); pruned
 // events get the sentinel key n_nodes, which sorts after every node.
-__global__ void k_agg_keys(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
-                           const uint8_t* __restrict__ flags, int64_t n, uint32_t sentinel, uint32_t* __restrict__ keys,
-                           uint32_t* __restrict__ vals) {
-  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= 2 * n) return;
+// Most-recent aggregation through a node-indexed table T in the workspace.
+// Message m = 2i + role of a non-pruned event i goes to node(m) (src for role
+// 0, dst for role 1).  Under the batch order precondition ((t, eid) ascending,
+// unique eids) the message with the largest (t, eid, role) is the one with
+// the largest index, so T[node] = max m over the node's messages.  The max is
+// taken with integer atomics (its value does not depend on their order); the
+// entries are first reset for exactly the nodes of this batch, so the table
+// needs no initialisation.  The winners (m == T[node(m)]) are then compacted in
+// increasing m.
+__device__ __forceinline__ int32_t msg_node(const int32_t* src, const int32_t* dst, const uint8_t* flags, int64_t m) {
   const int64_t i = m >> 1;
-  const bool pruned = flags != nullptr && (flags[i] & 2);
-  keys[m] = pruned ? sentinel : (uint32_t)((m & 1) ? dst[i] : src[i]);
-  vals[m] = (uint32_t)m;
+  if (flags != nullptr && (flags[i] & 2)) return -1;   // pruned: no message
+  return (m & 1) ? dst[i] : src[i];
 }
 
-// After a stable sort by node, the last message of each node's run is the
-// one with the largest message index.
-__global__ void k_agg_last_flags(const uint32_t* __restrict__ keys, int64_t nm, uint32_t sentinel,
-                                 int32_t* __restrict__ is_last) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= nm) return;
-  const uint32_t k = keys[p];
-  is_last[p] = (k != sentinel && (p == nm - 1 || keys[p + 1] != k)) ? 1 : 0;
+__global__ void k_agg_reset(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                            const uint8_t* __restrict__ flags, int64_t nm, int32_t* __restrict__ T) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= nm) return;
+  const int32_t node = msg_node(src, dst, flags, m);
+  if (node >= 0) T[node] = -1;
 }
 
-__global__ void k_agg_write(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
-                            const int32_t* __restrict__ is_last, const int32_t* __restrict__ pos, int64_t nm,
-                            int32_t* __restrict__ uniq, int32_t* __restrict__ winner) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= nm || !is_last[p]) return;
-  uniq[pos[p]] = (int32_t)keys[p];
-  winner[pos[p]] = (int32_t)vals[p];
+__global__ void k_agg_max(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                          const uint8_t* __restrict__ flags, int64_t nm, int32_t* __restrict__ T) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= nm) return;
+  const int32_t node = msg_node(src, dst, flags, m);
+  if (node >= 0) atomicMax(&T[node], (int32_t)m);
+}
+
+// One block compacts up to AGG_BLOCK_MAX messages.  Thread t first loads the
+// winner flags of messages 1024 j + t for every round j (all loads in
+// flight together); round j then ranks its winners with a wave ballot and the
+// 16 wave counts (double-buffered, one barrier per round).
+constexpr int AGG_BLOCK_THREADS = 1024;
+constexpr int AGG_ROUNDS = 16;
+constexpr int64_t AGG_BLOCK_MAX = AGG_BLOCK_THREADS * AGG_ROUNDS;
+
+__global__ __launch_bounds__(AGG_BLOCK_THREADS) void k_agg_compact_block(const int32_t* __restrict__ src,
+                                                                         const int32_t* __restrict__ dst,
+                                                                         const uint8_t* __restrict__ flags,
+                                                                         int64_t nm, const int32_t* __restrict__ T,
+                                                                         int32_t* __restrict__ uniq,
+                                                                         int32_t* __restrict__ winner,
+                                                                         int32_t* __restrict__ n_uniq) {
+  __shared__ int wcnt[2][AGG_BLOCK_THREADS / 64];
+  const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
+  const uint64_t lt_mask = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  int32_t node[AGG_ROUNDS];
+#pragma unroll
+  for (int j = 0; j < AGG_ROUNDS; ++j) {
+    const int64_t m = (int64_t)j * AGG_BLOCK_THREADS + t;
+    node[j] = m < nm ? msg_node(src, dst, flags, m) : -1;
+  }
+  uint32_t winbits = 0;
+#pragma unroll
+  for (int j = 0; j < AGG_ROUNDS; ++j) {
+    const int64_t m = (int64_t)j * AGG_BLOCK_THREADS + t;
+    if (node[j] >= 0 && T[node[j]] == (int32_t)m) winbits |= 1u << j;
+  }
+  int base = 0;
+#pragma unroll
+  for (int j = 0; j < AGG_ROUNDS; ++j) {
+    const bool win = (winbits >> j) & 1u;
+    const uint64_t bal = __ballot(win);
+    if (lane == 0) wcnt[j & 1][wid] = __popcll(bal);
+    __syncthreads();
+    int off = base, tot = 0;
+    for (int w = 0; w < AGG_BLOCK_THREADS / 64; ++w) {
+      const int c = wcnt[j & 1][w];
+      if (w < wid) off += c;
+      tot += c;
+    }
+    if (win) {
+      const int pos = off + __popcll(bal & lt_mask);
+      uniq[pos] = node[j];
+      winner[pos] = j * AGG_BLOCK_THREADS + t;
+    }
+    base += tot;
+  }
+  if (t == 0) *n_uniq = base;
+}
+
+__global__ void k_agg_flags(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                            const uint8_t* __restrict__ flags, int64_t nm, const int32_t* __restrict__ T,
+                            int32_t* __restrict__ win) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= nm) return;
+  const int32_t node = msg_node(src, dst, flags, m);
+  win[m] = (node >= 0 && T[node] == (int32_t)m) ? 1 : 0;
+}
+
+__global__ void k_agg_write(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                            const uint8_t* __restrict__ flags, int64_t nm, const int32_t* __restrict__ win,
+                            const int32_t* __restrict__ pos, int32_t* __restrict__ uniq,
+                            int32_t* __restrict__ winner) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= nm || !win[m]) return;
+  uniq[pos[m]] = msg_node(src, dst, flags, m);
+  winner[pos[m]] = (int32_t)m;
 }
 
 // ---------------------------------------------------------------- message construction
@@ -331,9 +404,11 @@ mtgnn_status build_queries_impl(const mtgnn_batch* b, const int32_t* neg, int32_
   return MTGNN_OK;
 }
 
-size_t aggregate_last_ws(int64_t n) {
+size_t aggregate_last_ws(int64_t n, int64_t n_nodes) {
   const int64_t nm = 2 * n;
-  return 4 * a256(sizeof(int32_t) * nm) + radix_sort_ws_bytes(nm) + radix_sort_result_bytes(nm) + scan_ws_bytes(nm);
+  size_t b = a256(sizeof(int32_t) * (n_nodes > 0 ? n_nodes : 1));
+  if (nm > AGG_BLOCK_MAX) b += 2 * a256(sizeof(int32_t) * nm) + scan_ws_bytes(nm);
+  return b;
 }
 
 mtgnn_status aggregate_last_impl(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
@@ -344,27 +419,29 @@ mtgnn_status aggregate_last_impl(const mtgnn_batch* b, int64_t n_nodes, int32_t*
     MTGNN_CHECK_LAUNCH("set_int");
     return MTGNN_OK;
   }
-  if (ws_bytes < aggregate_last_ws(n)) return MTGNN_EWORKSPACE;
+  if (ws_bytes < aggregate_last_ws(n, n_nodes)) return MTGNN_EWORKSPACE;
   char* w = (char*)ws;
-  uint32_t* keys = (uint32_t*)w;
-  w += a256(sizeof(int32_t) * nm);
-  uint32_t* vals = (uint32_t*)w;
-  w += a256(sizeof(int32_t) * nm);
-  int32_t* is_last = (int32_t*)w;
+  int32_t* T = (int32_t*)w;
+  w += a256(sizeof(int32_t) * n_nodes);
+  const unsigned grid = (unsigned)cdiv(nm, 256);
+  k_agg_reset<<<grid, 256, 0, s>>>(b->src, b->dst, b->flags, nm, T);
+  MTGNN_CHECK_LAUNCH("agg_reset");
+  k_agg_max<<<grid, 256, 0, s>>>(b->src, b->dst, b->flags, nm, T);
+  MTGNN_CHECK_LAUNCH("agg_max");
+  if (nm <= AGG_BLOCK_MAX) {
+    k_agg_compact_block<<<1, AGG_BLOCK_THREADS, 0, s>>>(b->src, b->dst, b->flags, nm, T, uniq, winner, n_uniq);
+    MTGNN_CHECK_LAUNCH("agg_compact_block");
+    return MTGNN_OK;
+  }
+  int32_t* win = (int32_t*)w;
   w += a256(sizeof(int32_t) * nm);
   int32_t* pos = (int32_t*)w;
   w += a256(sizeof(int32_t) * nm);
   const size_t rest = ws_bytes - (size_t)(w - (char*)ws);
-  const uint32_t sentinel = (uint32_t)n_nodes;
-  const unsigned grid = (unsigned)cdiv(nm, 256);
-  k_agg_keys<<<grid, 256, 0, s>>>(b->src, b->dst, b->flags, n, sentinel, keys, vals);
-  MTGNN_CHECK_LAUNCH("agg_keys");
-  MTGNN_TRY(radix_sort_pairs(&keys, &vals, nm, bits_for(n_nodes), w, rest, s));
-  k_agg_last_flags<<<grid, 256, 0, s>>>(keys, nm, sentinel, is_last);
-  MTGNN_CHECK_LAUNCH("agg_last_flags");
-  const size_t keep = radix_sort_result_bytes(nm);   // the sorted pairs may live there
-  MTGNN_TRY(scan_exclusive(is_last, pos, nm, n_uniq, w + keep, rest - keep, s));
-  k_agg_write<<<grid, 256, 0, s>>>(keys, vals, is_last, pos, nm, uniq, winner);
+  k_agg_flags<<<grid, 256, 0, s>>>(b->src, b->dst, b->flags, nm, T, win);
+  MTGNN_CHECK_LAUNCH("agg_flags");
+  MTGNN_TRY(scan_exclusive(win, pos, nm, n_uniq, w, rest, s));
+  k_agg_write<<<grid, 256, 0, s>>>(b->src, b->dst, b->flags, nm, win, pos, uniq, winner);
   MTGNN_CHECK_LAUNCH("agg_write");
   return MTGNN_OK;
 }

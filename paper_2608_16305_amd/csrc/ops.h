@@ -9,7 +9,7 @@ namespace mtgnn {
 size_t build_queries_ws(int64_t n);
 mtgnn_status build_queries_impl(const mtgnn_batch* b, const int32_t* neg, int32_t* q_node, float* q_t, int32_t* n_q,
                                 void* ws, size_t ws_bytes, hipStream_t s);
-size_t aggregate_last_ws(int64_t n);
+size_t aggregate_last_ws(int64_t n, int64_t n_nodes);
 mtgnn_status aggregate_last_impl(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
                                  int32_t* n_uniq, void* ws, size_t ws_bytes, hipStream_t s);
 mtgnn_status build_messages_impl(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,

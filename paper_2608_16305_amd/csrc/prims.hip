@@ -8,14 +8,17 @@ namespace mtgnn {
 namespace {
 
 constexpr int SORT_THREADS = 256;
-constexpr int SORT_ITEMS = 16;
-constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;   // 4096 keys per block
+constexpr int SORT_ITEMS = 4;
+constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;   // 1024 keys per block
 constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 
 constexpr int SCAN_THREADS = 256;
 constexpr int SCAN_ITEMS = 16;
 constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
+constexpr int SCAN1_THREADS = 1024;
+constexpr int SCAN1_ITEMS = 32;
+constexpr int64_t SCAN1_MAX = SCAN1_THREADS * SCAN1_ITEMS;   // one-block scan up to 32768 elements
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -83,6 +86,60 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile(const int32_t* __res
     *total = (block_off ? block_off[blockIdx.x] : 0) + tot;
 }
 
+// One block of 1024 threads scans up to SCAN1_MAX elements.  The input is
+// loaded coalesced (element i = j * 1024 + t goes to thread t) into LDS, then
+// thread t scans the contiguous chunk [32 t, 32 t + 32) from LDS; one padding
+// word per 32 keeps both access patterns free of bank conflicts.  The
+// offsets go back through LDS and out coalesced.
+__device__ __forceinline__ int scan1_pad(int i) { return i + (i >> 5); }
+
+__global__ __launch_bounds__(SCAN1_THREADS) void k_scan_one_block(const int32_t* __restrict__ in,
+                                                                  int32_t* __restrict__ out, int64_t n,
+                                                                  int32_t* __restrict__ total) {
+  __shared__ int buf[SCAN1_MAX + SCAN1_MAX / 32];
+  __shared__ int wsum[SCAN1_THREADS / 64];
+  const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
+#pragma unroll
+  for (int j = 0; j < SCAN1_ITEMS; ++j) {
+    const int i = j * SCAN1_THREADS + t;
+    buf[scan1_pad(i)] = i < n ? in[i] : 0;
+  }
+  __syncthreads();
+  int v[SCAN1_ITEMS];
+  int s = 0;
+#pragma unroll
+  for (int j = 0; j < SCAN1_ITEMS; ++j) {
+    v[j] = buf[scan1_pad(t * SCAN1_ITEMS + j)];
+    s += v[j];
+  }
+  int inc = s;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += u;
+  }
+  if (lane == 63) wsum[wid] = inc;
+  __syncthreads();
+  int run = 0, tot = 0;
+  for (int w = 0; w < SCAN1_THREADS / 64; ++w) {
+    const int x = wsum[w];
+    if (w < wid) run += x;
+    tot += x;
+  }
+  run += inc - s;
+#pragma unroll
+  for (int j = 0; j < SCAN1_ITEMS; ++j) {
+    buf[scan1_pad(t * SCAN1_ITEMS + j)] = run;
+    run += v[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < SCAN1_ITEMS; ++j) {
+    const int i = j * SCAN1_THREADS + t;
+    if (i < n) out[i] = buf[scan1_pad(i)];
+  }
+  if (total && t == 0) *total = tot;
+}
+
 // ---------------------------------------------------------------- radix sort kernels
 
 __global__ __launch_bounds__(SORT_THREADS) void k_radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
@@ -98,7 +155,7 @@ __global__ __launch_bounds__(SORT_THREADS) void k_radix_hist(const uint32_t* __r
     if (idx < n) atomicAdd(&hist[wid][(keys[idx] >> shift) & dmask], 1);
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS)
+  for (int d = threadIdx.x; d < (1 << digit_bits); d += SORT_THREADS)
     counts[(int64_t)d * nblk + blockIdx.x] = hist[0][d] + hist[1][d] + hist[2][d] + hist[3][d];
 }
 
@@ -114,16 +171,24 @@ __global__ __launch_bounds__(SORT_THREADS) void k_radix_scatter(const uint32_t* 
   __shared__ int run[RADIX];
   __shared__ int wcnt[4][RADIX];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS) run[d] = offsets[(int64_t)d * nblk + blockIdx.x];
+  for (int d = threadIdx.x; d < (1 << digit_bits); d += SORT_THREADS) run[d] = offsets[(int64_t)d * nblk + blockIdx.x];
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t base = (int64_t)blockIdx.x * SORT_TILE;
+  uint32_t kk[SORT_ITEMS], vv[SORT_ITEMS];   // the tile's items, loaded up front
+#pragma unroll
+  for (int i = 0; i < SORT_ITEMS; ++i) {
+    const int64_t idx = base + (int64_t)i * SORT_THREADS + threadIdx.x;
+    kk[i] = idx < n ? keys_in[idx] : 0u;
+    vv[i] = idx < n ? vals_in[idx] : 0u;
+  }
+#pragma unroll
   for (int i = 0; i < SORT_ITEMS; ++i) {
     for (int j = threadIdx.x; j < 4 * RADIX; j += SORT_THREADS) (&wcnt[0][0])[j] = 0;
     __syncthreads();
     const int64_t idx = base + (int64_t)i * SORT_THREADS + threadIdx.x;
     const bool valid = idx < n;
-    uint32_t key = valid ? keys_in[idx] : 0u;
-    uint32_t val = valid ? vals_in[idx] : 0u;
+    const uint32_t key = kk[i];
+    const uint32_t val = vv[i];
     const int d = (int)((key >> shift) & ((1u << digit_bits) - 1u));
     uint64_t peers = __ballot(valid);
     for (int b = 0; b < digit_bits; ++b) {
@@ -193,7 +258,7 @@ int bits_for(int64_t max_value) {
 }
 
 size_t scan_ws_bytes(int64_t n) {
-  if (n <= SCAN_TILE) return 0;
+  if (n <= SCAN1_MAX) return 0;
   int64_t nb = cdiv(n, SCAN_TILE);
   return align256(sizeof(int32_t) * nb) * 2 + scan_ws_bytes(nb);
 }
@@ -205,6 +270,11 @@ mtgnn_status scan_exclusive(const int32_t* in, int32_t* out, int64_t n, int32_t*
   if (n <= SCAN_TILE) {
     k_scan_tile<<<1, SCAN_THREADS, 0, s>>>(in, out, n, nullptr, total);
     MTGNN_CHECK_LAUNCH("scan_tile");
+    return MTGNN_OK;
+  }
+  if (n <= SCAN1_MAX) {
+    k_scan_one_block<<<1, SCAN1_THREADS, 0, s>>>(in, out, n, total);
+    MTGNN_CHECK_LAUNCH("scan_one_block");
     return MTGNN_OK;
   }
   const int64_t nb = cdiv(n, SCAN_TILE);
@@ -247,19 +317,20 @@ mtgnn_status radix_sort_pairs(uint32_t** keys_io, uint32_t** vals_io, int64_t n,
   w += align256(sizeof(int32_t) * nc);
   const size_t rest = ws_bytes - (size_t)(w - (char*)ws);
   uint32_t *ki = keys, *vi = vals, *ko = k2, *vo = v2;
-  int passes = 0;
-  for (int shift = 0; shift < bits; shift += RADIX_BITS, ++passes) {
-    const int dbits = (bits - shift) < RADIX_BITS ? (bits - shift) : RADIX_BITS;
+  // passes of equal width (at most 8 bits each), so each pass scans (2^width) x blocks counts
+  const int passes = (bits + RADIX_BITS - 1) / RADIX_BITS;
+  const int width = (bits + passes - 1) / passes;
+  for (int shift = 0; shift < bits; shift += width) {
+    const int dbits = (bits - shift) < width ? (bits - shift) : width;
     k_radix_hist<<<(unsigned)nblk, SORT_THREADS, 0, s>>>(ki, n, shift, dbits, (int)nblk, counts);
     MTGNN_CHECK_LAUNCH("radix_hist");
-    MTGNN_TRY(scan_exclusive(counts, offsets, nc, nullptr, w, rest, s));
+    MTGNN_TRY(scan_exclusive(counts, offsets, ((int64_t)1 << dbits) * nblk, nullptr, w, rest, s));
     k_radix_scatter<<<(unsigned)nblk, SORT_THREADS, 0, s>>>(ki, vi, ko, vo, n, shift, dbits, (int)nblk, offsets);
     MTGNN_CHECK_LAUNCH("radix_scatter");
     uint32_t* t;
     t = ki; ki = ko; ko = t;
     t = vi; vi = vo; vo = t;
   }
-  (void)passes;
   *keys_io = ki;   // the buffer holding the sorted pairs (the inputs or the first two workspace arrays)
   *vals_io = vi;
   return MTGNN_OK;

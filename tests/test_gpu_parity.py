@@ -133,3 +133,13 @@ def test_bf16_small():
     mem, lu = random_state(w, seed=5)
     from oracle.bf16 import round_bf16
     _tiny_run(w, s, round_bf16(mem), lu, range(1, 6))
+
+
+def test_edge_large_batch_multiblock_paths():
+    """A batch of 22,000 events: aggregation takes the multi-block sort path (44,000 messages),
+    the query-count scan the multi-level path (66,000 queries); replay/pruned masks included."""
+    w = tiny_workload(n_nodes=30000, n_events=66000, batch=22000, k=3, d_mem=8, d_time=4, d_edge=2, d_attn=8,
+                      n_heads=2)
+    s = tiny_stream(w, seed=11, t_scale=1000.0, tie_every=7, flags_p=(0.2, 0.3))
+    mem, lu = random_state(w, seed=6)
+    _tiny_run(w, s, mem, lu, range(1, 3))
