@@ -249,6 +249,28 @@ def build_adjacency(src, dst, t, n_nodes) -> Adjacency:
     return Adjacency(off, nbr[order], tt[order], ee[order])
 
 
+def build_adjacency_for(src, dst, t, n_nodes, nodes) -> Adjacency:
+    """The lists of ``nodes`` only, as ``build_adjacency`` orders them; every other list is empty.
+
+    Only events with an endpoint in ``nodes`` are read into the lists, so a
+    few queried nodes of a very long stream are cheap to serve.
+    """
+    want = np.zeros(n_nodes, bool)
+    want[np.asarray(nodes, np.int64)] = True
+    e_src = np.nonzero(want[src])[0]
+    e_dst = np.nonzero(want[dst])[0]
+    node = np.concatenate([np.asarray(src)[e_src], np.asarray(dst)[e_dst]]).astype(np.int64)
+    nbr = np.concatenate([np.asarray(dst)[e_src], np.asarray(src)[e_dst]]).astype(np.int64)
+    tt = np.concatenate([np.asarray(t, F32)[e_src], np.asarray(t, F32)[e_dst]])
+    ee = np.concatenate([e_src, e_dst]).astype(np.int64)
+    role = np.concatenate([np.zeros(e_src.size, np.int8), np.ones(e_dst.size, np.int8)])
+    order = np.lexsort((role, ee, tt, node))
+    counts = np.bincount(node, minlength=n_nodes)
+    off = np.zeros(n_nodes + 1, np.int64)
+    np.cumsum(counts, out=off[1:])
+    return Adjacency(off, nbr[order], tt[order], ee[order])
+
+
 def sample_recent(adj: Adjacency, q_node, q_t, k: int):
     """The k most recent neighbours strictly before each query time.
 

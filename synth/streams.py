@@ -50,9 +50,31 @@ def _zipf_cdf(n_ranks: int, s: float) -> np.ndarray:
     return cdf
 
 
-def _zipf_draw(rng: np.random.Generator, cdf: np.ndarray, n: int) -> np.ndarray:
+def _zipf_guide(cdf: np.ndarray) -> np.ndarray:
+    """Guide table of the inverse-CDF search: g[j] = first rank whose CDF exceeds j / M."""
+    M = cdf.shape[0]
+    return np.searchsorted(cdf, np.arange(M, dtype=np.float64) / M, side="right")
+
+
+def _zipf_draw(rng: np.random.Generator, cdf: np.ndarray, n: int, guide=None) -> np.ndarray:
+    """Ranks r = first index with cdf[r] > u for u ~ U[0, 1): the inverse CDF.
+
+    The guide table gives, for u in [j/M, (j+1)/M), a start that is never past
+    the answer; a short forward scan finishes it, so the result equals a
+    binary search (``searchsorted(cdf, u, side="right")``) exactly.
+    """
     u = rng.random(n)
-    r = np.searchsorted(cdf, u, side="right")
+    if guide is None:
+        r = np.searchsorted(cdf, u, side="right")
+    else:
+        M = cdf.shape[0]
+        r = guide[np.minimum((u * M).astype(np.int64), M - 1)]
+        np.minimum(r, M - 1, out=r)
+        act = np.nonzero(cdf[r] <= u)[0]
+        while act.size:
+            r[act] += 1
+            np.minimum(r, M - 1, out=r)
+            act = act[(cdf[r[act]] <= u[act]) & (r[act] < M - 1)]
     np.minimum(r, cdf.shape[0] - 1, out=r)
     return r
 
@@ -60,6 +82,19 @@ def _zipf_draw(rng: np.random.Generator, cdf: np.ndarray, n: int) -> np.ndarray:
 def _chunks(n: int):
     for c, lo in enumerate(range(0, n, CHUNK)):
         yield c, lo, min(n, lo + CHUNK)
+
+
+def _each_chunk(n: int, fn) -> None:
+    """fn(c, lo, hi) for every chunk; chunks have their own generators, so they run on threads."""
+    chunks = list(_chunks(n))
+    if len(chunks) == 1:
+        fn(*chunks[0])
+        return
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=min(len(chunks), os.cpu_count() or 1, 16)) as ex:
+        for f in [ex.submit(fn, *c) for c in chunks]:
+            f.result()
 
 
 def make_stream(w: Workload, base_seed: int = 0) -> Stream:
@@ -73,8 +108,9 @@ def make_stream(w: Workload, base_seed: int = 0) -> Stream:
     if w.src_rule.startswith("zipf") or w.dst_rule.startswith("zipf"):
         n_ranks = (N - w.n_src) if w.dst_rule == "zipf_dst" else N
         cdf = _zipf_cdf(n_ranks, w.zipf_s)
+        guide = _zipf_guide(cdf) if n_ranks > 2_000_000 else None   # same draws; faster for large rank counts
         perm = _rng(base_seed, cid, _PERM).permutation(n_ranks).astype(np.int64)
-    for c, lo, hi in _chunks(E):
+    def endpoints(c, lo, hi):
         n = hi - lo
         rs = _rng(base_seed, cid, _SRC, c)
         rd = _rng(base_seed, cid, _DST, c)
@@ -83,23 +119,27 @@ def make_stream(w: Workload, base_seed: int = 0) -> Stream:
         elif w.src_rule == "uniform_src":
             src[lo:hi] = rs.integers(0, w.n_src, n)
         else:  # zipf over all nodes through a seeded permutation
-            src[lo:hi] = perm[_zipf_draw(rs, cdf, n)]
+            src[lo:hi] = perm[_zipf_draw(rs, cdf, n, guide)]
         if w.dst_rule == "uniform":
             dst[lo:hi] = rd.integers(0, N, n)
         elif w.dst_rule == "zipf_dst":
-            dst[lo:hi] = w.n_src + perm[_zipf_draw(rd, cdf, n)]
+            dst[lo:hi] = w.n_src + perm[_zipf_draw(rd, cdf, n, guide)]
         else:
-            dst[lo:hi] = perm[_zipf_draw(rd, cdf, n)]
+            dst[lo:hi] = perm[_zipf_draw(rd, cdf, n, guide)]
         rn = _rng(base_seed, cid, _NEG, c)
         if w.neg_rule == "dst":
             neg[lo:hi] = rn.integers(w.n_src, N, n)
         else:
             neg[lo:hi] = rn.integers(0, N, n)
 
+    _each_chunk(E, endpoints)
+
     if w.t_rule == "uniform_sorted":
         t64 = np.empty(E, np.float64)
-        for c, lo, hi in _chunks(E):
+
+        def times(c, lo, hi):
             t64[lo:hi] = _rng(base_seed, cid, _T, c).random(hi - lo) * 1e5
+        _each_chunk(E, times)
         t64.sort()
     elif w.t_rule == "exp_gaps":
         gaps = np.empty(E, np.float64)
@@ -114,8 +154,10 @@ def make_stream(w: Workload, base_seed: int = 0) -> Stream:
     x = None
     if w.d_edge > 0:
         x = np.empty((E, w.d_edge), np.float32)
-        for c, lo, hi in _chunks(E):
-            x[lo:hi] = _rng(base_seed, cid, _X, c).standard_normal((hi - lo, w.d_edge), dtype=np.float32)
+
+        def feats(c, lo, hi):
+            _rng(base_seed, cid, _X, c).standard_normal((hi - lo, w.d_edge), dtype=np.float32, out=x[lo:hi])
+        _each_chunk(E, feats)
 
     flags = None
     if w.replay_p > 0:
@@ -182,15 +224,19 @@ def window_state(w: Workload, s: Stream, b0: int, base_seed: int = 0):
         hi = min(N, lo + step)
         mem[lo:hi] = _rng(base_seed, w.cid, _M0, c).uniform(-1.0, 1.0, (hi - lo, dm)).astype(np.float32)
     e0 = min(s.n_events, b0 * w.batch)
-    last = np.full(N, -1, np.int64)
-    if e0 > 0:
-        idx = np.arange(e0, dtype=np.int64)
-        np.maximum.at(last, s.src[:e0], idx)
-        np.maximum.at(last, s.dst[:e0], idx)
     lu = np.zeros(N, np.float32)
-    has = last >= 0
-    lu[has] = s.t[last[has]]
+    if e0 > 0:
+        lu[:] = last_event_time(s.src[:e0], s.dst[:e0], s.t[:e0], N)
     return mem, lu
+
+
+def last_event_time(src, dst, t, n_nodes: int) -> np.ndarray:
+    """t of each node's last event (as either endpoint) in a time-sorted stream, else 0 (times are >= 0)."""
+    lu = np.zeros(n_nodes, np.float32)
+    tt = np.asarray(t, np.float32)
+    np.maximum.at(lu, np.asarray(src, np.int64), tt)
+    np.maximum.at(lu, np.asarray(dst, np.int64), tt)
+    return lu
 
 
 def loss_noise(w: Workload, step: int, n_rows: int, base_seed: int = 0) -> np.ndarray:

@@ -126,3 +126,113 @@ def compare_step(runner, w, stream, adj, b, tol, lag=1, check=None):
     if check:
         check(gpu, ref)
     return gpu, ref
+
+
+def compare_step_sampled(runner, w, stream, b, tol, n_sample, seed=0):
+    """Full-size step b (lag-1) with the loss gradient restricted to the queries of a sample of target events.
+
+    The GPU runs the whole step at its real size, exactly as the benchmark
+    does; dZ is nonzero only on the src / dst / negative rows of `n_sample`
+    target events.  Because the backward is linear in dZ, every gradient and
+    d_mem then equals the oracle's step over those events alone, which the
+    oracle computes with the full memory phase of batch b-1 and an adjacency
+    restricted to the sampled query nodes.  Compared: the whole memory phase,
+    the sampled queries' neighbours and embeddings, d_mem and all gradients.
+    """
+    mem0, lu0 = mem_snapshot(runner)
+    elo, ehi = runner.batch_range(b)
+    mlo, mhi = runner.batch_range(b - 1)
+    flags = stream.flags[elo:ehi] if stream.flags is not None else None
+    tar = np.nonzero(tgn.target_mask(flags, ehi - elo))[0]
+    n_tar = tar.size
+    pick = np.sort(np.random.default_rng(seed).choice(n_tar, size=min(n_sample, n_tar), replace=False))
+    rows = np.concatenate([pick, n_tar + pick, 2 * n_tar + pick])
+    G = noise_for(w, b, runner.max_q)
+    dz = np.zeros_like(G)
+    dz[rows] = G[rows] / np.float32(n_tar)
+    runner.lag = 1
+    runner.step(b, torch.from_numpy(dz).to(runner.dev))
+    torch.cuda.synchronize()
+
+    ev = (elo + tar[pick]).astype(np.int64)
+    emb = {"src": stream.src[ev], "dst": stream.dst[ev], "t": stream.t[ev], "eid": ev, "neg": stream.neg[ev]}
+    noise_sub = G[rows].astype(np.float64) * (pick.size / n_tar)
+    q_nodes = np.unique(np.concatenate([emb["src"], emb["dst"], emb["neg"]]))
+    adj = tgn.build_adjacency_for(stream.src, stream.dst, stream.t, w.n_nodes, q_nodes)
+    params = {k: v.float().cpu().numpy() for k, v in runner.params.items()}
+    mb = tgn.batch_dict(stream, mlo, mhi)
+    ref = tgn.step(oracle_prec(w), w, mem0, lu0, params, adj, stream.x, mb, emb, noise_sub)
+    grad_tol = {}
+    if w.dtype == "bf16":
+        # bf16 gradients at this size are ill-conditioned: the oracle's own gradients move by a few
+        # percent when the values before each bf16 rounding carry fp32-level (1e-7 relative) errors,
+        # the size of an fp32 evaluation's.  Gradients are gated at max(tol, 2x that spread).
+        for seed in (1, 2):
+            alt = tgn.step(_PerturbedPrec("bf16", seed), w, mem0, lu0, params, adj, stream.x, mb, emb,
+                           noise_sub)
+            for name, g in ref.grads.items():
+                if name != "b_k":
+                    grad_tol[name] = max(grad_tol.get(name, tol), 2.0 * rel_err(alt.grads[name], g))
+            grad_tol["d_mem"] = max(grad_tol.get("d_mem", tol), 2.0 * rel_err(alt.d_mem, ref.d_mem))
+
+    U = int(runner.n_uniq.item())
+    Q = int(runner.n_q.item())
+    assert Q == 3 * n_tar
+    uniq = runner.uniq[:U].cpu().numpy()
+    winner = runner.winner[:U].cpu().numpy()
+    assert U == len(ref.mp.uniq)
+    assert np.all(np.diff(winner) > 0)
+    perm = np.argsort(uniq, kind="stable")
+    assert np.array_equal(uniq[perm], ref.mp.uniq)
+    assert np.array_equal(winner[perm], ref.mp.winner)
+    dt = runner.dt[:U].cpu().numpy()
+    assert np.array_equal(dt[perm].view(np.uint32), np.asarray(ref.mp.dt, np.float32).view(np.uint32))
+    mem1 = to_np(runner.memory)
+    lu1 = runner.last_update.cpu().numpy()
+    assert np.array_equal(lu1.view(np.uint32), ref.mp.lu.view(np.uint32))
+    h_new = mem1[ref.mp.uniq].copy()
+    mem1[ref.mp.uniq] = mem0[ref.mp.uniq]      # rows outside the update set must be untouched, bit for bit
+    assert np.array_equal(mem1.view(np.uint32), np.asarray(mem0).view(np.uint32))
+    del mem1
+    # the sampled queries
+    ti = torch.from_numpy(rows).to(runner.dev)
+    assert np.array_equal(runner.q_node[ti].cpu().numpy(), ref.q_node)
+    assert np.array_equal(runner.q_t[ti].cpu().numpy().view(np.uint32), ref.q_t.view(np.uint32))
+    assert np.array_equal(runner.nbr[ti].cpu().numpy(), ref.nbr)
+    assert np.array_equal(runner.neid[ti].cpu().numpy(), ref.neid)
+    assert np.array_equal(runner.nt[ti].cpu().numpy().view(np.uint32), ref.nt.view(np.uint32))
+    errs = {
+        "msg": rel_err(to_np(runner.msg[:U])[perm], ref.mp.msg),
+        "mem": rel_err(h_new, ref.mp.h_new),
+        "d_mem": rel_err(runner.d_mem[:U].cpu().numpy()[perm], ref.d_mem),
+        "z": rel_err(runner.z[ti].cpu().numpy(), ref.attn.z),
+    }
+    for name, g in ref.grads.items():
+        gg = runner.grads[name].cpu().numpy()
+        if name == "b_k":
+            errs[name] = float(np.abs(gg).max() / max(np.abs(ref.grads["W_k"]).max(), 1e-30))
+        else:
+            errs[name] = rel_err(gg, g)
+    worst = max(errs.items(), key=lambda kv: kv[1] / grad_tol.get(kv[0], tol))
+    log(f"  step {b}: U={U} Q={Q} sampled events={pick.size} worst {worst[0]}={worst[1]:.3e} "
+        f"(gate {grad_tol.get(worst[0], tol):.3e})")
+    if grad_tol:
+        log("  bf16 gradient gates: " + ", ".join(f"{k}={v:.1e}" for k, v in sorted(grad_tol.items())))
+    bad = {k: v for k, v in errs.items() if v > grad_tol.get(k, tol)}
+    assert not bad, bad
+
+
+class _PerturbedPrec(tgn.Prec):
+    """The oracle's bf16 mode with a relative 1e-7 perturbation of every computed value just before it
+    is rounded to bf16 (weights, which are rounded once from fixed parameters, are left alone)."""
+
+    def __init__(self, mode, seed):
+        super().__init__(mode)
+        self._rng = np.random.default_rng(seed)
+
+    def pack(self, x):
+        x = np.asarray(x, np.float64)
+        return super().pack(x * (1.0 + 1e-7 * self._rng.standard_normal(x.shape)))
+
+    def weight(self, x):
+        return tgn.Prec.pack(self, x)

@@ -15,7 +15,7 @@ import torch
 
 from oracle import tgn
 from synth import init_params, make_stream, window_state, workload
-from tests._gpu import compare_step, log, needs_gpu, to_np
+from tests._gpu import compare_step, compare_step_sampled, log, needs_gpu, to_np
 from tests._tiny import random_state, tiny_stream, tiny_workload
 
 pytestmark = [pytest.mark.gpu, needs_gpu]
@@ -73,6 +73,24 @@ def test_workload3_window():
     adj = _check_csr(r, s, w.n_nodes)
     for b in range(w.window_b0, w.window_b0 + 3):
         compare_step(r, w, s, adj, b, TOL[w.dtype])
+
+
+@pytest.mark.parametrize("cid", [4, 5])
+def test_full_size_sampled(cid):
+    """Workloads 4 (10M nodes, 100M events, batch 60,000, k 20, fp32) and 5 (replay / pruned
+    masks, bf16) at full size, mid-stream: the whole memory phase and every gradient, with the
+    loss gradient on the queries of 256 sampled target events per step."""
+    w = workload(cid)
+    log(f"[parity] workload {cid} {w.name}: generating the stream")
+    s = make_stream(w)
+    params = init_params(w, random_bias=True)
+    mem, lu = window_state(w, s, w.window_b0)
+    log("[parity] stream ready; uploading and building the adjacency on the GPU")
+    r = _runner(w, s, params, mem, lu)
+    del mem, lu
+    torch.cuda.synchronize()
+    for b in range(w.window_b0, w.window_b0 + 2):
+        compare_step_sampled(r, w, s, b, TOL[w.dtype], n_sample=256, seed=b)
 
 
 # ----------------------------------------------------------------------------- edge cases

@@ -483,3 +483,29 @@ def test_example_dependency_chain():
             deps.append(e + 1)
     assert set(ex["must_depend_on"]) <= set(deps)
     assert not set(ex["must_not_depend_on"]) & set(deps)
+
+
+def test_restricted_adjacency_equals_full_lists():
+    """The per-node lists built from the events touching a node subset equal the full build's lists."""
+    rng = np.random.default_rng(21)
+    E, N = 3000, 80
+    src = rng.integers(0, N, E).astype(np.int32)
+    dst = rng.integers(0, N, E).astype(np.int32)
+    t = np.sort(rng.random(E) * 50).astype(np.float32)
+    t[5::7] = t[4::7][: t[5::7].size]          # timestamp ties
+    full = tgn.build_adjacency(src, dst, t, N)
+    nodes = rng.choice(N, 17, replace=False)
+    part = tgn.build_adjacency_for(src, dst, t, N, nodes)
+    for n in range(N):
+        lo, hi = part.off[n], part.off[n + 1]
+        if n in nodes:
+            flo, fhi = full.off[n], full.off[n + 1]
+            assert np.array_equal(part.nbr[lo:hi], full.nbr[flo:fhi])
+            assert np.array_equal(part.t[lo:hi], full.t[flo:fhi])
+            assert np.array_equal(part.eid[lo:hi], full.eid[flo:fhi])
+        else:
+            assert hi == lo
+    q = rng.choice(nodes, 40)
+    qt = rng.random(40).astype(np.float32) * 50
+    for a, b in zip(tgn.sample_recent(part, q, qt, 6), tgn.sample_recent(full, q, qt, 6)):
+        assert np.array_equal(a, b)
