@@ -542,7 +542,7 @@ __global__ void k_copy_cols(const float* __restrict__ S, int64_t lds, const int3
 }
 
 struct BwdWs {
-  float *dm1, *dm_in, *dattn, *dqv, *dphi0, *dKV, *dphin, *S, *head, *tail, *dWkv, *dbkv;
+  float *dm1, *dm_in, *dattn, *dqv, *dKV, *tg_part, *S, *head, *tail, *dWkv, *dbkv;
   uint32_t *keys, *vals;
   int32_t *seg_lo, *seg_hi, *row_of;
   char* scratch;
@@ -562,9 +562,8 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   v.dm_in = (float*)take(sizeof(float) * s.Q * (s.da + s.dm));
   v.dattn = (float*)take(sizeof(float) * s.Q * s.da);
   v.dqv = (float*)take(sizeof(float) * s.Q * s.da);
-  v.dphi0 = (float*)take(sizeof(float) * s.Q * dtp);
   v.dKV = (float*)take(sizeof(float) * s.P * 2 * s.da);
-  v.dphin = (float*)take(sizeof(float) * s.P * dtp);
+  v.tg_part = (float*)take(sizeof(float) * 2 * dtp * gemm_tg_blocks(s.P > s.Q ? s.P : s.Q));
   v.S = (float*)take(sizeof(float) * (max_rows > 0 ? max_rows : 1) * W);
   v.head = (float*)take(sizeof(float) * ntiles * W);
   v.tail = (float*)take(sizeof(float) * ntiles * W);
@@ -580,8 +579,6 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   mx(linear_dw_ws_bytes(s.Q, s.da, s.da + s.dm));
   mx(linear_dw_ws_bytes(s.Q, s.da, s.Dq));
   mx(linear_dw_ws_bytes(s.P, 2 * s.da, s.Dkv));
-  mx(timegrad_ws_bytes(s.P, s.dt));
-  mx(timegrad_ws_bytes(s.Q, s.dt));
   v.scratch = take(sc);
   v.scratch_bytes = a256(sc);
   v.total = (size_t)(w - (char*)base);
@@ -690,9 +687,10 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   // query projection: dhq += dqv W_q[:, :dm];  dphi(0) = dqv W_q[:, dm:]
   MTGNN_TRY(linear_dw(b.dqv, da, sv.q_in, MTGNN_F32, sh.Dq, g->W_q, sh.Dq, Q, n_q, da, sh.Dq, sc, scb, s, g->b_q));
   MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
-  if (dt > 0) {
-    MTGNN_TRY(linear_dx(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, b.dphi0, dt, Q, n_q, da, dt, false, s));
-    MTGNN_TRY(timegrad_rows(b.dphi0, dt, Q, n_q, nullptr, nullptr, tw, tb, dt, d_time_w, d_time_b, false, sc, scb, s));
+  if (dt > 0) {   // phi(0) of the queries: delta = 0, so only the bias part is nonzero
+    MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,
+                                 b.tg_part, s));
+    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, Q, n_q, 64 * G_WM, dt, d_time_w, d_time_b, false, s));
   }
   // key/value projection over the compact slots (stacked [W_k; W_v])
   MTGNN_TRY(linear_dw<site::KvDw>(b.dKV, 2 * da, sv.kv_in, MTGNN_F32, sh.Dkv, b.dWkv, sh.Dkv, P, sv.n_valid, 2 * da,
@@ -700,11 +698,10 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   k_split_kv_grads<<<(unsigned)cdiv((int64_t)da * sh.Dkv, 256), 256, 0, s>>>(b.dWkv, b.dbkv, da, sh.Dkv, g->W_k,
                                                                               g->W_v, g->b_k, g->b_v);
   MTGNN_CHECK_LAUNCH("split_kv_grads");
-  if (dt > 0) {
-    MTGNN_TRY(linear_dx<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, b.dphin, dt, P, sv.n_valid,
-                                    2 * da, dt, false, s));
-    MTGNN_TRY(timegrad_rows(b.dphin, dt, P, sv.n_valid, sv.pair_delta, sv.sinv, tw, tb, dt, d_time_w, d_time_b, true,
-                            sc, scb, s));
+  if (dt > 0) {   // phi(tau - t_j) of the neighbour slots, with the saved sin(arg)
+    MTGNN_TRY(linear_dx_timegrad<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, P, sv.n_valid,
+                                             2 * da, dt, sv.sinv, sv.pair_delta, tw, tb, b.tg_part, s));
+    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, P, sv.n_valid, 64 * G_WM, dt, d_time_w, d_time_b, true, s));
   }
   // d M' for the updated rows: group every occurrence by row, sum in a fixed order
   if (max_rows > 0) {

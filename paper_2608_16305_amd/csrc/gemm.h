@@ -59,6 +59,14 @@ struct GemmArgs {
   int64_t ones_col = -1;       // B column treated as all ones (-1: none); its results go to col_out
   float* col_out = nullptr;    // C(i, ones_col) is written to col_out[i] (weight-grad GEMMs: the bias grad)
   int xcd_group = 1;           // place blocks that share an operand chunk on one XCD (see gemm_tile)
+  // Time-encoder gradient epilogue: instead of writing C, each block writes the
+  // column sums over its rows of  g = -C(i,j) sin(arg_ij)  and of  g * delta_i
+  // (arg_ij = w_j delta_i + b_j) to tg_part[row block][0 / 1][j].
+  float* tg_part = nullptr;
+  const float* tg_sin = nullptr;     // saved sin(arg) [M, N] (row stride N), or null: recomputed
+  const float* tg_delta = nullptr;   // per-row delta_i, or null: 0
+  const float* tg_w = nullptr;       // time encoder w, b (used when tg_sin is null)
+  const float* tg_b = nullptr;
   int tile_bn = 0;             // host-side plan: output tile width (0: chosen by gemm_tile_width)
   int tile_bk = 16;            // host-side plan: k step (64 only for weight-gradient 64-wide tiles)
 };
@@ -235,30 +243,32 @@ struct TileVec {
     }
   }
   // k0: first k of the tile; k_lim: end of the reduction range
-  __device__ __forceinline__ void load(int64_t k0, int64_t k_lim) {
+  __device__ __forceinline__ void load_into(int64_t k0, int64_t k_lim, float4* dst) const {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const bool kin = k0 + kq[p] < k_lim;
       const bool ok = ((row_ok >> p) & 1u) && kin;
       const float4 f = Vec4<T>::load(ok ? ptr[p] : safe);
       const bool one = ((ones >> p) & 1u) && kin;
-      v[p] = float4{ok ? f.x : (one ? 1.f : 0.f), ok ? f.y : 0.f, ok ? f.z : 0.f, ok ? f.w : 0.f};
+      dst[p] = float4{ok ? f.x : (one ? 1.f : 0.f), ok ? f.y : 0.f, ok ? f.z : 0.f, ok ? f.w : 0.f};
     }
   }
+  __device__ __forceinline__ void load(int64_t k0, int64_t k_lim) { load_into(k0, k_lim, v); }
   __device__ __forceinline__ void advance(int64_t step) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) ptr[p] += step;
   }
-  __device__ __forceinline__ void store(float* lds, int tid) const {
+  __device__ __forceinline__ void store_from(float* lds, int tid, const float4* src) const {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int g = tid + p * G_THREADS;
       if (g >= GROUPS) continue;
       int mn, k;
       L::coord(g, mn, k);
-      L::put(lds, mn, k, v[p]);
+      L::put(lds, mn, k, src[p]);
     }
   }
+  __device__ __forceinline__ void store(float* lds, int tid) const { store_from(lds, tid, v); }
 };
 
 // Block: (64 WM) rows x BN columns; wave w computes WM 16-row tiles x BN.
@@ -268,7 +278,7 @@ struct TileVec {
 // one LDS buffer, the next tile waits in registers (two barriers per step).
 // VEC: aligned shapes use the branch-free TileVec loader.
 template <class Site, int BN, int WM, int BK, int NBUF, bool VEC, typename TA, typename TB, bool A_KCONTIG,
-          bool B_KCONTIG>
+          bool B_KCONTIG, int PF = 1, bool TGE = false>
 __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
   constexpr int NT = BN / 16;
   constexpr int BM = 64 * WM;
@@ -313,7 +323,76 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
     }
   };
 
-  if (kbeg < kend) {
+  // MFMA work on one LDS tile pair
+  auto compute = [&](const float* as, const float* bs) {
+#pragma unroll
+    for (int kc = 0; kc < BK; kc += 16) {
+      float4 a4[WM];
+#pragma unroll
+      for (int i = 0; i < WM; ++i) a4[i] = LA::frag(as, (wid * WM + i) * 16 + (lane & 15), kc, lane);
+      float4 b4[NT];
+#pragma unroll
+      for (int j = 0; j < NT; ++j) b4[j] = LB::frag(bs, j * 16 + (lane & 15), kc, lane);
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].x, b4[j].x, acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].y, b4[j].y, acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].z, b4[j].z, acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].w, b4[j].w, acc[i][j], 0, 0, 0);
+    }
+  };
+
+  if constexpr (VEC && PF == 2 && NBUF == 2) {
+    // Prefetch distance 2: register sets 0 and 1 alternate (the loop is
+    // unrolled by two so each set stays in fixed registers).  While tile t is
+    // computed from LDS buffer t % 2, tile t + 2 is loading into the register
+    // set that held tile t, and tile t + 1 (loaded one iteration earlier) is
+    // then written to the other LDS buffer.
+    if (kbeg < kend) {
+      float4 ra0[IOA::PER], rb0[IOB::PER], ra1[IOA::PER], rb1[IOB::PER];
+      const int64_t ntile = cdiv(kend - kbeg, BK);
+      ta.init(A, a_smn, a_sk, row0, kbeg, M, -1, tid);
+      tb.init(B, b_smn, b_sk, col0, kbeg, g.N, g.ones_col, tid);
+      auto fetch = [&](int64_t t, float4* ra, float4* rb) {
+        ta.load_into(kbeg + t * BK, kend, ra);
+        tb.load_into(kbeg + t * BK, kend, rb);
+        ta.advance(BK * a_sk);
+        tb.advance(BK * b_sk);
+      };
+      fetch(0, ra0, rb0);
+      if (ntile > 1) fetch(1, ra1, rb1);
+      ta.store_from(As[0], tid, ra0);
+      tb.store_from(Bs[0], tid, rb0);
+      __syncthreads();
+      for (int64_t t = 0; t < ntile; t += 2) {
+        if (t + 2 < ntile) fetch(t + 2, ra0, rb0);
+        compute(As[0], Bs[0]);
+        if (t + 1 < ntile) {
+          ta.store_from(As[1], tid, ra1);
+          tb.store_from(Bs[1], tid, rb1);
+        }
+        __syncthreads();
+        if (t + 1 >= ntile) break;
+        if (t + 3 < ntile) fetch(t + 3, ra1, rb1);
+        compute(As[1], Bs[1]);
+        if (t + 2 < ntile) {
+          ta.store_from(As[0], tid, ra0);
+          tb.store_from(Bs[0], tid, rb0);
+        }
+        __syncthreads();
+      }
+    }
+  } else if (kbeg < kend) {
     if constexpr (VEC) {
       ta.init(A, a_smn, a_sk, row0, kbeg, M, -1, tid);
       tb.init(B, b_smn, b_sk, col0, kbeg, g.N, g.ones_col, tid);
@@ -326,33 +405,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
     for (int64_t k0 = kbeg; k0 < kend; k0 += BK) {
       const bool more = k0 + BK < kend;
       if (more) load_tiles(k0 + BK);
-      const float* as = As[cur];
-      const float* bs = Bs[cur];
-#pragma unroll
-      for (int kc = 0; kc < BK; kc += 16) {
-        float4 a4[WM];
-#pragma unroll
-        for (int i = 0; i < WM; ++i) a4[i] = LA::frag(as, (wid * WM + i) * 16 + (lane & 15), kc, lane);
-        float4 b4[NT];
-#pragma unroll
-        for (int j = 0; j < NT; ++j) b4[j] = LB::frag(bs, j * 16 + (lane & 15), kc, lane);
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].x, b4[j].x, acc[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].y, b4[j].y, acc[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].z, b4[j].z, acc[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[i].w, b4[j].w, acc[i][j], 0, 0, 0);
-      }
+      compute(As[cur], Bs[cur]);
       if (more) {
         const int nb = NBUF == 2 ? (cur ^ 1) : 0;
         if (NBUF == 1) __syncthreads();   // every wave is done reading the only buffer
@@ -361,6 +414,49 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
       }
       __syncthreads();
       if (NBUF == 2) cur ^= 1;
+    }
+  }
+
+  if constexpr (TGE) {   // time-gradient epilogue (tg_* arguments)
+    static_assert(8 * BN <= NBUF * LA::SIZE && WM == 1, "time-gradient epilogue scratch");
+    {
+      float* red_w = &As[0][0];   // the operand tiles are no longer read (last loop barrier)
+      float* red_b = red_w + 4 * BN;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int64_t gj = col0 + j * 16 + (lane & 15);
+        float cw = 0.f, cb = 0.f;
+        if (gj < g.N) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int64_t gi = row0 + wid * 16 + 4 * (lane >> 4) + r;
+            if (gi >= M) continue;
+            const float d = g.tg_delta ? g.tg_delta[gi] : 0.f;
+            const float sn = g.tg_sin ? g.tg_sin[gi * g.N + gj] : sinf(time_arg(g.tg_w[gj], d, g.tg_b[gj]));
+            const float gv = acc[0][j][r] * -sn;
+            cb += gv;
+            cw += gv * d;
+          }
+        }
+        cw += __shfl_xor(cw, 16, 64);
+        cb += __shfl_xor(cb, 16, 64);
+        cw += __shfl_xor(cw, 32, 64);
+        cb += __shfl_xor(cb, 32, 64);
+        if (lane < 16) {
+          red_w[wid * BN + j * 16 + lane] = cw;
+          red_b[wid * BN + j * 16 + lane] = cb;
+        }
+      }
+      __syncthreads();
+      for (int c = tid; c < BN; c += G_THREADS) {
+        const int64_t gj = col0 + c;
+        if (gj >= g.N) continue;
+        g.tg_part[(tc.x * 2 + 0) * g.N + gj] =
+            ((red_w[c] + red_w[BN + c]) + red_w[2 * BN + c]) + red_w[3 * BN + c];
+        g.tg_part[(tc.x * 2 + 1) * g.N + gj] =
+            ((red_b[c] + red_b[BN + c]) + red_b[2 * BN + c]) + red_b[3 * BN + c];
+      }
+      return;
     }
   }
 
@@ -419,13 +515,21 @@ inline bool vec_ok(const void* p, int64_t other_stride, size_t esz) {
   return ((uintptr_t)p % (4 * esz)) == 0 && (other_stride % 4) == 0;
 }
 
-template <class Site, int BN, bool VEC, typename TA, typename TB, bool AK, bool BK, int KSTEP = G_BK>
+template <class Site, int BN, bool VEC, typename TA, typename TB, bool AK, bool BK, int KSTEP = G_BK,
+          bool TGE = false>
 void gemm_kernel_launch(const GemmArgs& g, dim3 grid, hipStream_t s) {
-  k_gemm<Site, BN, G_WM, KSTEP, G_NBUF, VEC, TA, TB, AK, BK><<<grid, G_THREADS, 0, s>>>(g);
+  k_gemm<Site, BN, G_WM, KSTEP, G_NBUF, VEC, TA, TB, AK, BK, 1, TGE><<<grid, G_THREADS, 0, s>>>(g);
 }
 
 template <class Site, bool VEC, typename TA, typename TB, bool AK, bool BK>
 void gemm_bn_launch(const GemmArgs& g, int bn, dim3 grid, hipStream_t s) {
+  if constexpr (AK && !BK) {   // data gradients: the time-gradient epilogue on 64- or 128-wide tiles
+    if (g.tg_part != nullptr) {
+      if (bn == 128) gemm_kernel_launch<Site, 128, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s);
+      else gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s);
+      return;
+    }
+  }
   switch (bn) {
     case 64:
       if constexpr (!AK && !BK) {   // weight gradients: 64-deep k steps on 64 x 64 tiles
@@ -507,6 +611,25 @@ mtgnn_status linear_dx(const float* dy, int64_t lddy, const void* W, int w_dtype
   g.B = W; g.b_sk = ldw; g.b_sj = 1;
   g.C = dx; g.ldc = lddx; g.accumulate = accumulate ? 1 : 0;
   g.kchunk = N; g.c_split_stride = 0; g.gate = gate; g.ldgate = ldgate;
+  return gemm_launch<Site, true, false>(g, MTGNN_F32, w_dtype, 1, s);
+}
+
+// Time-gradient form of linear_dx: dphi = dy W is not stored; each 64-row block
+// writes its column sums of -dphi sin(arg) (and times delta) to part[block][2][K].
+// Rows come from M (clamped by M_dev); part needs gemm_tg_blocks(M) * 2 * K floats.
+inline int64_t gemm_tg_blocks(int64_t M) { return cdiv(M < 1 ? 1 : M, 64 * G_WM); }
+template <class Site = site::Generic>
+mtgnn_status linear_dx_timegrad(const float* dy, int64_t lddy, const void* W, int w_dtype, int64_t ldw, int64_t M,
+                                const int32_t* M_dev, int64_t N, int64_t K, const float* sin_saved,
+                                const float* delta, const float* tw, const float* tb, float* part, hipStream_t s) {
+  GemmArgs g{};
+  g.M = M; g.N = K; g.K = N; g.M_dev = M_dev;
+  g.A = dy; g.a_si = lddy; g.a_sk = 1;
+  g.B = W; g.b_sk = ldw; g.b_sj = 1;
+  g.C = nullptr; g.ldc = 0;
+  g.kchunk = N; g.c_split_stride = 0;
+  g.tg_part = part; g.tg_sin = sin_saved; g.tg_delta = delta; g.tg_w = tw; g.tg_b = tb;
+  g.tile_bn = (K > 128 || gemm_tile_width(M, K, 1) == 64) ? 64 : 128;   // the epilogue's two tile widths
   return gemm_launch<Site, true, false>(g, MTGNN_F32, w_dtype, 1, s);
 }
 

@@ -262,7 +262,7 @@ __global__ void k_gru_bwd_gates(const float* __restrict__ dh, const float* __res
 
 // ---------------------------------------------------------------- time-encoder gradients
 
-constexpr int TG_ROWS = 128;
+constexpr int TG_ROWS = 32;   // rows per partial (8 per wave)
 
 // Elapsed time of each row: delta[r] (delta == nullptr: 0, the query-side phi(0)).
 struct RowDelta {
@@ -307,40 +307,35 @@ __global__ __launch_bounds__(256) void k_timegrad_partial(const float* __restric
   }
 }
 
-// 64 columns per block; the 4 waves sum interleaved chunks, combined in a fixed order.
-__global__ __launch_bounds__(256) void k_timegrad_final(const float* __restrict__ part, int nch, int dt_dim,
-                                                        float* __restrict__ dw, float* __restrict__ db,
-                                                        int accumulate) {
-  __shared__ float rw[4][64], rb[4][64];
-  const int j = blockIdx.x * 64 + (threadIdx.x & 63);
-  const int g = threadIdx.x >> 6;
-  float sw = 0.f, sb = 0.f;
-  if (j < dt_dim) {
-    int c = g;
-    for (; c + 12 < nch; c += 16) {   // four chunks in flight
-      float w4[4], b4[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        w4[u] = part[((int64_t)(c + 4 * u) * 2 + 0) * dt_dim + j];
-        b4[u] = part[((int64_t)(c + 4 * u) * 2 + 1) * dt_dim + j];
-      }
-      sw += ((w4[0] + w4[1]) + w4[2]) + w4[3];
-      sb += ((b4[0] + b4[1]) + b4[2]) + b4[3];
-    }
-    for (; c < nch; c += 4) {
-      sw += part[((int64_t)c * 2 + 0) * dt_dim + j];
-      sb += part[((int64_t)c * 2 + 1) * dt_dim + j];
-    }
+// One block per column j: thread t sums chunks t, t + 256, ... of the partial
+// sums, then a fixed-order tree in LDS combines the 256 thread sums.  Chunks
+// beyond the device row count (ceil(rows / chunk_rows)) hold no partial.
+__global__ __launch_bounds__(256) void k_timegrad_reduce(const float* __restrict__ part, int64_t rows,
+                                                         const int32_t* __restrict__ rows_dev, int chunk_rows,
+                                                         int dt_dim, float* __restrict__ dw, float* __restrict__ db,
+                                                         int accumulate) {
+  __shared__ float sw[256], sb[256];
+  const int j = blockIdx.x, t = threadIdx.x;
+  const int64_t nch = cdiv(eff_count(rows, rows_dev), chunk_rows);
+  float aw = 0.f, ab = 0.f;
+  for (int64_t c = t; c < nch; c += 256) {
+    aw += part[(c * 2 + 0) * dt_dim + j];
+    ab += part[(c * 2 + 1) * dt_dim + j];
   }
-  rw[g][threadIdx.x & 63] = sw;
-  rb[g][threadIdx.x & 63] = sb;
+  sw[t] = aw;
+  sb[t] = ab;
   __syncthreads();
-  if (g != 0 || j >= dt_dim) return;
-  const int l = threadIdx.x;
-  sw = ((rw[0][l] + rw[1][l]) + rw[2][l]) + rw[3][l];
-  sb = ((rb[0][l] + rb[1][l]) + rb[2][l]) + rb[3][l];
-  dw[j] = accumulate ? dw[j] + sw : sw;
-  db[j] = accumulate ? db[j] + sb : sb;
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) {
+      sw[t] += sw[t + o];
+      sb[t] += sb[t + o];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    dw[j] = accumulate ? dw[j] + sw[0] : sw[0];
+    db[j] = accumulate ? db[j] + sb[0] : sb[0];
+  }
 }
 
 }  // namespace
@@ -362,9 +357,18 @@ mtgnn_status timegrad_launch(const float* dphi, int64_t ld, int64_t rows, const 
   dim3 g((unsigned)cdiv(dt_dim, 64), (unsigned)nch);
   k_timegrad_partial<D><<<g, 256, 0, s>>>(dphi, ld, rows, rows_dev, delta, tw, tb, sin_saved, dt_dim, (float*)ws);
   MTGNN_CHECK_LAUNCH("timegrad_partial");
-  k_timegrad_final<<<(unsigned)cdiv(dt_dim, 64), 256, 0, s>>>((const float*)ws, nch, dt_dim, dw, db,
-                                                              accumulate ? 1 : 0);
-  MTGNN_CHECK_LAUNCH("timegrad_final");
+k_timegrad_reduce<<<(unsigned)dt_dim, 256, 0, s>>>((const float*)ws, rows, rows_dev, TG_ROWS, dt_dim, dw, db,
+                                                     accumulate ? 1 : 0);
+  MTGNN_CHECK_LAUNCH("timegrad_reduce");
+  return MTGNN_OK;
+}
+
+mtgnn_status timegrad_reduce_blocks(const float* part, int64_t rows, const int32_t* rows_dev, int chunk_rows,
+                                    int dt_dim, float* dw, float* db, bool accumulate, hipStream_t s) {
+  if (dt_dim <= 0) return MTGNN_OK;
+  k_timegrad_reduce<<<(unsigned)dt_dim, 256, 0, s>>>(part, rows, rows_dev, chunk_rows, dt_dim, dw, db,
+                                                      accumulate ? 1 : 0);
+  MTGNN_CHECK_LAUNCH("timegrad_reduce");
   return MTGNN_OK;
 }
 

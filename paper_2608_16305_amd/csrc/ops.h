@@ -37,6 +37,10 @@ size_t timegrad_ws_bytes(int64_t rows, int dt_dim);
 // d_time_w[j] (+)= sum_r dphi[r,j] (-sin(arg_rj)) delta_r,  d_time_b[j] (+)= sum_r dphi[r,j] (-sin(arg_rj)),
 // arg_rj = time_w[j] delta_r + time_b[j]; delta == nullptr means delta_r = 0; sin_saved (optional) holds
 // sin(arg) per [row, j]; rows are clamped by rows_dev.
+// Sums the per-block partials [blocks][2][dt_dim] of a time-gradient GEMM epilogue
+// (blocks = ceil(rows / chunk_rows), rows clamped by rows_dev) into dw, db.
+mtgnn_status timegrad_reduce_blocks(const float* part, int64_t rows, const int32_t* rows_dev, int chunk_rows,
+                                    int dt_dim, float* dw, float* db, bool accumulate, hipStream_t s);
 mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* delta,
                            const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
                            bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
