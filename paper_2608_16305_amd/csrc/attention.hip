@@ -576,8 +576,10 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   v.row_of = (int32_t*)take(sizeof(int32_t) * s.N);
   size_t sc = radix_sort_ws_bytes(n_occ);
   auto mx = [&](size_t x) { if (x > sc) sc = x; };
-  mx(linear_dw_ws_bytes(s.Q, s.da, s.da + s.dm));
-  mx(linear_dw_ws_bytes(s.Q, s.da, s.Dq));
+  {
+    const int64_t Ns[4] = {s.da, s.da, s.da, s.da}, Ks[4] = {s.da, s.da + s.dm, s.da, s.Dq};
+    mx(linear_dw_batch_ws_bytes(s.Q, Ns, Ks, 4));
+  }
   mx(linear_dw_ws_bytes(s.P, 2 * s.da, s.Dkv));
   v.scratch = take(sc);
   v.scratch_bytes = a256(sc);
@@ -670,12 +672,10 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   auto wofs = [&](const void* W, int64_t col) { return (const void*)((const char*)W + sh.esz * (size_t)col); };
 
   // merge MLP: z = W_2 a1 + b_2, a1 = relu(m1), m1 = W_1 m_in + b_1
-  MTGNN_TRY(linear_dw(dz, da, sv.a1, MTGNN_F32, da, g->W_2, da, Q, n_q, da, da, sc, scb, s, g->b_2));
+  // (their weight gradients run as one batch after the score backward)
   MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
-  MTGNN_TRY(linear_dw(b.dm1, da, sv.m_in, MTGNN_F32, ldm, g->W_1, ldm, Q, n_q, da, ldm, sc, scb, s, g->b_1));
   MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
   // output projection: o = W_o attn + b_o   (do = dm_in[:, :da])
-  MTGNN_TRY(linear_dw(b.dm_in, ldm, sv.attn, MTGNN_F32, da, g->W_o, da, Q, n_q, da, da, sc, scb, s, g->b_o));
   MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
   // softmax-weighted sum and scores
   {
@@ -684,8 +684,15 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
                                                           sh.k, da, sh.H, b.dKV, b.dqv);
   }
   MTGNN_CHECK_LAUNCH("attn_core_bwd");
+  // weight gradients of the query, output and merge layers, one batch over the query rows
+  {
+    const DwProblem ps[4] = {{dz, da, sv.a1, da, g->W_2, da, da, da, g->b_2},
+                             {b.dm1, da, sv.m_in, ldm, g->W_1, ldm, da, ldm, g->b_1},
+                             {b.dm_in, ldm, sv.attn, da, g->W_o, da, da, da, g->b_o},
+                             {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, sh.Dq, g->b_q}};
+    MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
+  }
   // query projection: dhq += dqv W_q[:, :dm];  dphi(0) = dqv W_q[:, dm:]
-  MTGNN_TRY(linear_dw(b.dqv, da, sv.q_in, MTGNN_F32, sh.Dq, g->W_q, sh.Dq, Q, n_q, da, sh.Dq, sc, scb, s, g->b_q));
   MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
   if (dt > 0) {   // phi(0) of the queries: delta = 0, so only the bias part is nonzero
     MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,

@@ -19,6 +19,7 @@
 // Inputs may be float32 or bfloat16 (converted on load).
 #pragma once
 
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -279,7 +280,7 @@ struct TileVec {
 // VEC: aligned shapes use the branch-free TileVec loader.
 template <class Site, int BN, int WM, int BK, int NBUF, bool VEC, typename TA, typename TB, bool A_KCONTIG,
           bool B_KCONTIG, int PF = 1, bool TGE = false>
-__global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
+__device__ __forceinline__ void gemm_body(const GemmArgs& g, const TileCoord tc) {
   constexpr int NT = BN / 16;
   constexpr int BM = 64 * WM;
   using LA = Lds<A_KCONTIG, BM, BK>;
@@ -289,7 +290,6 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
 
   const int64_t M = eff_count(g.M, g.M_dev);
   const int64_t Kall = eff_count(g.K, g.K_dev);
-  const TileCoord tc = gemm_tile(g.xcd_group);
   const int64_t row0 = tc.x * BM;
   const int64_t col0 = tc.y * BN;
   if (row0 >= M) return;
@@ -489,6 +489,37 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
   }
 }
 
+// One output tile per block; tile coordinates from the XCD-grouped order.
+template <class Site, int BN, int WM, int BK, int NBUF, bool VEC, typename TA, typename TB, bool A_KCONTIG,
+          bool B_KCONTIG, int PF = 1, bool TGE = false>
+__global__ __launch_bounds__(G_THREADS) void k_gemm(GemmArgs g) {
+  gemm_body<Site, BN, WM, BK, NBUF, VEC, TA, TB, A_KCONTIG, B_KCONTIG, PF, TGE>(g, gemm_tile(g.xcd_group));
+}
+
+// Up to G_MAXBATCH independent products of one shape class in one launch:
+// blockIdx.z = problem * zper + split.  Blocks beyond a problem's own column
+// strips or splits return at once.
+constexpr int G_MAXBATCH = 4;
+struct GemmBatch {
+  GemmArgs a[G_MAXBATCH];
+  int n;
+  int zper;
+};
+
+template <class Site, int BN, int WM, int BK, int NBUF, bool VEC, typename TA, typename TB, bool A_KCONTIG,
+          bool B_KCONTIG>
+__global__ __launch_bounds__(G_THREADS) void k_gemm_batch(GemmBatch b) {
+  const int p = (int)(blockIdx.z / (uint32_t)b.zper);
+  if (p >= b.n) return;
+  const GemmArgs& g = b.a[p];
+  TileCoord tc;
+  tc.x = blockIdx.x;
+  tc.y = blockIdx.y;
+  tc.z = blockIdx.z % (uint32_t)b.zper;
+  if (tc.y * BN >= g.N || tc.z * g.kchunk >= g.K) return;
+  gemm_body<Site, BN, WM, BK, NBUF, VEC, TA, TB, A_KCONTIG, B_KCONTIG>(g, tc);
+}
+
 // Tile shape used by the library's launches.
 constexpr int G_WM = 1, G_NBUF = 2;
 
@@ -547,22 +578,30 @@ void gemm_bn_launch(const GemmArgs& g, int bn, dim3 grid, hipStream_t s) {
   }
 }
 
+// The branch-free loader needs 4-aligned bases and strides, row counts of
+// each operand's contiguous dimension that are multiples of 4, a virtual
+// ones column (if any) at a multiple of 4, and k extents (host K and the
+// split chunk) that are multiples of 4 for operands contiguous along k.
+template <typename TA, typename TB, bool AK, bool BK>
+bool gemm_vec_ok(const GemmArgs& g) {
+  return vec_ok(g.A, AK ? g.a_si : g.a_sk, sizeof(TA)) && vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) &&
+         (AK ? (g.K % 4 == 0 && g.kchunk % 4 == 0 && g.K_dev == nullptr) : (g.M % 4 == 0 && g.M_dev == nullptr)) &&
+         (BK ? (g.K % 4 == 0 && g.kchunk % 4 == 0 && g.K_dev == nullptr) : g.N % 4 == 0 || g.ones_col == g.N - 1) &&
+         (g.ones_col < 0 || g.ones_col % 4 == 0);
+}
+template <typename TA, typename TB, bool AK, bool BK>
+void gemm_set_vec_flags(GemmArgs& g) {   // general loader: 4-wide only when aligned
+  g.a_vec = vec_ok(g.A, AK ? g.a_si : g.a_sk, sizeof(TA)) ? 1 : 0;
+  g.b_vec = vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) ? 1 : 0;
+}
+
 template <class Site, typename TA, typename TB, bool AK, bool BK>
 mtgnn_status gemm_launch_t(const GemmArgs& g0, int ksplit, hipStream_t s) {
   GemmArgs g = g0;
-  g.a_vec = vec_ok(g.A, AK ? g.a_si : g.a_sk, sizeof(TA)) ? 1 : 0;   // general loader: 4-wide only when aligned
-  g.b_vec = vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) ? 1 : 0;
+  gemm_set_vec_flags<TA, TB, AK, BK>(g);
   const int bn = g.tile_bn > 0 ? g.tile_bn : gemm_tile_width(g.M, g.N, ksplit);
   dim3 grid((unsigned)cdiv(g.M, 64 * G_WM), (unsigned)cdiv(g.N, bn), (unsigned)(ksplit < 1 ? 1 : ksplit));
-  // The branch-free loader needs 4-aligned bases and strides, row counts of
-  // each operand's contiguous dimension that are multiples of 4, a virtual
-  // ones column (if any) at a multiple of 4, and k extents (host K and the
-  // split chunk) that are multiples of 4 for operands contiguous along k.
-  const bool vec = vec_ok(g.A, AK ? g.a_si : g.a_sk, sizeof(TA)) &&
-                   vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) &&
-                   (AK ? (g.K % 4 == 0 && g.kchunk % 4 == 0 && g.K_dev == nullptr) : (g.M % 4 == 0 && g.M_dev == nullptr)) &&
-                   (BK ? (g.K % 4 == 0 && g.kchunk % 4 == 0 && g.K_dev == nullptr) : g.N % 4 == 0 || g.ones_col == g.N - 1) &&
-                   (g.ones_col < 0 || g.ones_col % 4 == 0);
+  const bool vec = gemm_vec_ok<TA, TB, AK, BK>(g);
   TimedScope ts(Site::name, s);
   if (vec) gemm_bn_launch<Site, true, TA, TB, AK, BK>(g, bn, grid, s);
   else gemm_bn_launch<Site, false, TA, TB, AK, BK>(g, bn, grid, s);
@@ -570,9 +609,70 @@ mtgnn_status gemm_launch_t(const GemmArgs& g0, int ksplit, hipStream_t s) {
   return MTGNN_OK;
 }
 
+template <class Site, int BN, bool VEC, typename TA, typename TB, bool AK, bool BK>
+void gemm_batch_kernel(const GemmBatch& b, dim3 grid, hipStream_t s) {
+  if constexpr (!AK && !BK && BN == 64) {   // weight gradients on 64-wide tiles may take 64-deep steps
+    if (b.a[0].tile_bk == 64) {
+      k_gemm_batch<Site, BN, G_WM, 64, G_NBUF, VEC, TA, TB, AK, BK><<<grid, G_THREADS, 0, s>>>(b);
+      return;
+    }
+  }
+  k_gemm_batch<Site, BN, G_WM, G_BK, G_NBUF, VEC, TA, TB, AK, BK><<<grid, G_THREADS, 0, s>>>(b);
+}
+
+// Batched launch: every problem shares the tile width of the first (its tile_bn, or the width rule
+// at its shape) and the launch uses the branch-free loader only if every problem allows it.
+template <class Site, typename TA, typename TB, bool AK, bool BK>
+mtgnn_status gemm_batch_launch_t(const GemmArgs* gs, int n, int zper, hipStream_t s) {
+  if (n < 1 || n > G_MAXBATCH || zper < 1) return MTGNN_EINVAL;
+  GemmBatch b{};
+  b.n = n;
+  b.zper = zper;
+  const int bn = gs[0].tile_bn > 0 ? gs[0].tile_bn : gemm_tile_width(gs[0].M, gs[0].N, zper);
+  bool vec = true;
+  int64_t gx = 1, gy = 1;
+  for (int i = 0; i < n; ++i) {
+    b.a[i] = gs[i];
+    gemm_set_vec_flags<TA, TB, AK, BK>(b.a[i]);
+    vec = vec && gemm_vec_ok<TA, TB, AK, BK>(b.a[i]);
+    gx = std::max<int64_t>(gx, cdiv(gs[i].M, 64 * G_WM));
+    gy = std::max<int64_t>(gy, cdiv(gs[i].N, bn));
+  }
+  dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)(n * zper));
+  TimedScope ts(Site::name, s);
+#define MTGNN_BATCH_BN(W)                                                    \
+  case W:                                                                    \
+    if (vec) gemm_batch_kernel<Site, W, true, TA, TB, AK, BK>(b, grid, s);   \
+    else gemm_batch_kernel<Site, W, false, TA, TB, AK, BK>(b, grid, s);      \
+    break;
+  switch (bn) {
+    MTGNN_BATCH_BN(64)
+    MTGNN_BATCH_BN(128)
+    MTGNN_BATCH_BN(160)
+    MTGNN_BATCH_BN(208)
+    default:
+      if (vec) gemm_batch_kernel<Site, 256, true, TA, TB, AK, BK>(b, grid, s);
+      else gemm_batch_kernel<Site, 256, false, TA, TB, AK, BK>(b, grid, s);
+      break;
+  }
+#undef MTGNN_BATCH_BN
+  MTGNN_CHECK_LAUNCH(Site::name);
+  return MTGNN_OK;
+}
+
 // Instantiated once per (site, layout) in gemm_nt.hip / gemm_nn.hip / gemm_tn.hip.
 template <class Site, bool AK, bool BK>
 mtgnn_status gemm_launch(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s);
+template <class Site, bool AK, bool BK>
+mtgnn_status gemm_batch_launch(const GemmArgs* gs, int n, int zper, int dtype_a, int dtype_b, hipStream_t s);
+
+template <class Site, bool AK, bool BK>
+mtgnn_status gemm_batch_launch_impl(const GemmArgs* gs, int n, int zper, int dtype_a, int dtype_b, hipStream_t s) {
+  if (dtype_a == MTGNN_F32 && dtype_b == MTGNN_F32) return gemm_batch_launch_t<Site, float, float, AK, BK>(gs, n, zper, s);
+  if (dtype_a == MTGNN_F32) return gemm_batch_launch_t<Site, float, uint16_t, AK, BK>(gs, n, zper, s);
+  if (dtype_b == MTGNN_F32) return MTGNN_EUNSUPPORTED;
+  return gemm_batch_launch_t<Site, uint16_t, uint16_t, AK, BK>(gs, n, zper, s);
+}
 
 template <class Site, bool AK, bool BK>
 mtgnn_status gemm_launch_impl(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s) {
@@ -666,5 +766,39 @@ mtgnn_status linear_dw(const float* dy, int64_t lddy, const void* x, int x_dtype
   MTGNN_CHECK_LAUNCH("splitk_reduce");
   return MTGNN_OK;
 }
+
+// ---------------------------------------------------------------- batched products
+
+// Independent forward products over the same rows M (clamped by M_dev):
+// y_i[M, N_i] = x_i[M, K_i] W_i[N_i, K_i]^T + b_i, in one launch.
+struct FwdProblem {
+  const void* x;
+  int64_t ldx;
+  const void* W;
+  int64_t ldw;
+  const float* bias;
+  float* y;
+  int64_t ldy;
+  int64_t N, K;
+};
+mtgnn_status linear_fwd_batch(const FwdProblem* ps, int n, int64_t M, const int32_t* M_dev, int x_dtype,
+                              int w_dtype, hipStream_t s);
+
+// Independent weight gradients over the same reduction rows R (clamped by R_dev):
+// dW_i[N_i, K_i] = dy_i[R, N_i]^T x_i[R, K_i], and db_i = column sums of dy_i when db_i is set.
+// One product launch and one split-K reduce launch for the whole batch.
+struct DwProblem {
+  const float* dy;
+  int64_t lddy;
+  const void* x;
+  int64_t ldx;
+  float* dW;
+  int64_t lddw;
+  int64_t N, K;
+  float* db;
+};
+size_t linear_dw_batch_ws_bytes(int64_t R, const int64_t* N, const int64_t* K, int n);   // sizes only
+mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_t* R_dev, int x_dtype, void* ws,
+                             size_t ws_bytes, hipStream_t s);
 
 }  // namespace mtgnn

@@ -3,10 +3,12 @@
 
 namespace mtgnn {
 
+namespace {
+
 // 64 outputs per block; the 4 waves sum interleaved split slices, combined in a fixed order.
-__global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ part, int64_t split_stride,
-                                                       int nsplit, int64_t rows, int64_t cols, float* __restrict__ out,
-                                                       int64_t ldo, int64_t ones_col, float* __restrict__ col_out) {
+__device__ __forceinline__ void splitk_reduce_body(const float* __restrict__ part, int64_t split_stride, int nsplit,
+                                                   int64_t rows, int64_t cols, float* __restrict__ out, int64_t ldo,
+                                                   int64_t ones_col, float* __restrict__ col_out) {
   __shared__ float red[4][64];
   const int64_t e = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
   const int g = threadIdx.x >> 6;
@@ -28,6 +30,37 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
   const int64_t i = e / cols, j = e % cols;
   if (j == ones_col) col_out[i] = s;
   else out[i * ldo + j] = s;
+}
+
+struct ReduceProblem {
+  const float* part;
+  int64_t split_stride;
+  int nsplit;
+  int64_t rows, cols;
+  float* out;
+  int64_t ldo;
+  int64_t ones_col;
+  float* col_out;
+};
+struct ReduceBatch {
+  ReduceProblem p[G_MAXBATCH];
+  int n;
+};
+
+// blockIdx.y selects the problem; blocks past its outputs return before the barrier.
+__global__ __launch_bounds__(256) void k_splitk_reduce_batch(ReduceBatch b) {
+  if ((int)blockIdx.y >= b.n) return;
+  const ReduceProblem& q = b.p[blockIdx.y];
+  if ((int64_t)blockIdx.x * 64 >= q.rows * q.cols) return;
+  splitk_reduce_body(q.part, q.split_stride, q.nsplit, q.rows, q.cols, q.out, q.ldo, q.ones_col, q.col_out);
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ part, int64_t split_stride,
+                                                       int nsplit, int64_t rows, int64_t cols, float* __restrict__ out,
+                                                       int64_t ldo, int64_t ones_col, float* __restrict__ col_out) {
+  splitk_reduce_body(part, split_stride, nsplit, rows, cols, out, ldo, ones_col, col_out);
 }
 
 int gemm_strip_width(int64_t N) {
@@ -69,6 +102,91 @@ DwPlan dw_plan(int64_t R, int64_t N, int64_t K) {
   p.ksplit = (int)cdiv(r, p.kchunk);
   if (p.ksplit == 1) p.kchunk = r;
   return p;
+}
+
+// ---------------------------------------------------------------- batched products
+
+mtgnn_status linear_fwd_batch(const FwdProblem* ps, int n, int64_t M, const int32_t* M_dev, int x_dtype,
+                              int w_dtype, hipStream_t s) {
+  if (n < 1 || n > G_MAXBATCH) return MTGNN_EINVAL;
+  if (M <= 0) return MTGNN_OK;
+  int64_t nmax = 1;
+  for (int i = 0; i < n; ++i) nmax = ps[i].N > nmax ? ps[i].N : nmax;
+  const int bn = gemm_tile_width(M, nmax, 1);
+  GemmArgs gs[G_MAXBATCH];
+  for (int i = 0; i < n; ++i) {
+    GemmArgs g{};
+    g.M = M; g.N = ps[i].N; g.K = ps[i].K; g.M_dev = M_dev;
+    g.A = ps[i].x; g.a_si = ps[i].ldx; g.a_sk = 1;
+    g.B = ps[i].W; g.b_sk = 1; g.b_sj = ps[i].ldw;
+    g.C = ps[i].y; g.ldc = ps[i].ldy; g.bias = ps[i].bias;
+    g.kchunk = ps[i].K; g.c_split_stride = 0;
+    g.tile_bn = bn;
+    gs[i] = g;
+  }
+  return gemm_batch_launch<site::Generic, true, true>(gs, n, 1, x_dtype, w_dtype, s);
+}
+
+namespace {
+// One plan for the batch, from its largest output (with room for a bias column).
+DwPlan dw_batch_plan(int64_t R, const int64_t* N, const int64_t* K, int n) {
+  int best = 0;
+  for (int i = 1; i < n; ++i)
+    if (N[i] * (K[i] + 1) > N[best] * (K[best] + 1)) best = i;
+  return dw_plan(R, N[best], K[best] + 1);
+}
+}  // namespace
+
+size_t linear_dw_batch_ws_bytes(int64_t R, const int64_t* N, const int64_t* K, int n) {
+  const DwPlan p = dw_batch_plan(R, N, K, n);
+  if (p.ksplit <= 1) return 0;
+  size_t b = 0;
+  for (int i = 0; i < n; ++i) b += (sizeof(float) * (size_t)p.ksplit * N[i] * (K[i] + 1) + 255) & ~size_t(255);
+  return b;
+}
+
+mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_t* R_dev, int x_dtype, void* ws,
+                             size_t ws_bytes, hipStream_t s) {
+  if (n < 1 || n > G_MAXBATCH) return MTGNN_EINVAL;
+  int64_t Ns[G_MAXBATCH], Ks[G_MAXBATCH];
+  for (int i = 0; i < n; ++i) {
+    Ns[i] = ps[i].N;
+    Ks[i] = ps[i].K;
+  }
+  const DwPlan plan = dw_batch_plan(R, Ns, Ks, n);
+  if (ws_bytes < linear_dw_batch_ws_bytes(R, Ns, Ks, n)) return MTGNN_EWORKSPACE;
+  GemmArgs gs[G_MAXBATCH];
+  ReduceBatch rb{};
+  rb.n = n;
+  char* w = (char*)ws;
+  int64_t max_out = 1;
+  for (int i = 0; i < n; ++i) {
+    const DwProblem& q = ps[i];
+    const int64_t Kc = q.db ? q.K + 1 : q.K;
+    GemmArgs g{};
+    g.M = q.N; g.N = Kc; g.K = R < 1 ? 1 : R; g.K_dev = R_dev;
+    if (q.db) { g.ones_col = q.K; g.col_out = q.db; }
+    g.A = q.dy; g.a_si = 1; g.a_sk = q.lddy;
+    g.B = q.x; g.b_sk = q.ldx; g.b_sj = 1;
+    g.kchunk = plan.kchunk;
+    g.tile_bn = plan.bn;
+    g.tile_bk = plan.bk;
+    if (plan.ksplit == 1) {
+      g.C = q.dW; g.ldc = q.lddw; g.c_split_stride = 0;
+    } else {
+      g.C = (float*)w; g.ldc = Kc; g.c_split_stride = q.N * Kc;
+      rb.p[i] = ReduceProblem{(const float*)w, q.N * Kc, plan.ksplit, q.N, Kc, q.dW, q.lddw, q.db ? q.K : -1, q.db};
+      w += (sizeof(float) * (size_t)plan.ksplit * q.N * Kc + 255) & ~size_t(255);
+      max_out = q.N * Kc > max_out ? q.N * Kc : max_out;
+    }
+    gs[i] = g;
+  }
+  MTGNN_TRY((gemm_batch_launch<site::Generic, false, false>(gs, n, plan.ksplit, MTGNN_F32, x_dtype, s)));
+  if (plan.ksplit > 1) {
+    k_splitk_reduce_batch<<<dim3((unsigned)cdiv(max_out, 64), (unsigned)n), 256, 0, s>>>(rb);
+    MTGNN_CHECK_LAUNCH("splitk_reduce_batch");
+  }
+  return MTGNN_OK;
 }
 
 size_t linear_dw_ws_bytes(int64_t R, int64_t N, int64_t K) {

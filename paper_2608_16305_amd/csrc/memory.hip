@@ -496,10 +496,16 @@ mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const in
   else
     k_gather_rows<uint16_t><<<gel, 256, 0, s>>>((const uint16_t*)memory, uniq, n_rows, max_rows, dm, h_old);
   MTGNN_CHECK_LAUNCH("gather_rows");
-  MTGNN_TRY(linear_fwd(msg, d->dtype, dmsg, W_ih, d->dtype, dmsg, b_ih, G, 6 * dm, max_rows, n_rows, 3 * dm, dmsg,
-                       false, s));
-  MTGNN_TRY(linear_fwd(h_old, MTGNN_F32, dm, W_hh, d->dtype, dm, b_hh, G + 3 * dm, 6 * dm, max_rows, n_rows, 3 * dm,
-                       dm, false, s));
+  if (d->dtype == MTGNN_F32) {   // both products in one launch (their inputs share a type)
+    const FwdProblem ps[2] = {{msg, dmsg, W_ih, dmsg, b_ih, G, 6 * dm, 3 * dm, dmsg},
+                              {h_old, dm, W_hh, dm, b_hh, G + 3 * dm, 6 * dm, 3 * dm, dm}};
+    MTGNN_TRY(linear_fwd_batch(ps, 2, max_rows, n_rows, MTGNN_F32, MTGNN_F32, s));
+  } else {
+    MTGNN_TRY(linear_fwd(msg, d->dtype, dmsg, W_ih, d->dtype, dmsg, b_ih, G, 6 * dm, max_rows, n_rows, 3 * dm, dmsg,
+                         false, s));
+    MTGNN_TRY(linear_fwd(h_old, MTGNN_F32, dm, W_hh, d->dtype, dm, b_hh, G + 3 * dm, 6 * dm, max_rows, n_rows, 3 * dm,
+                         dm, false, s));
+  }
   if (d->dtype == MTGNN_F32)
     k_gru_gates<float><<<gel, 256, 0, s>>>(G, h_old, uniq, winner, b->t, n_rows, max_rows, dm, (float*)memory, lu, sr,
                                            sz, sn, sghn);
@@ -514,7 +520,10 @@ size_t gru_update_bwd_ws(const mtgnn_dims* d, int64_t max_rows) {
   const int dm = d->d_mem, dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
   size_t dw = linear_dw_ws_bytes(max_rows, 3 * dm, dmsg);
   size_t dw2 = linear_dw_ws_bytes(max_rows, 3 * dm, dm);
+  const int64_t Ns[2] = {3 * dm, 3 * dm}, Ks[2] = {dmsg, dm};
+  size_t dwb = linear_dw_batch_ws_bytes(max_rows, Ns, Ks, 2);
   size_t m = dw > dw2 ? dw : dw2;
+  m = m > dwb ? m : dwb;
   return 2 * a256(sizeof(float) * max_rows * 3 * dm) + a256(m);
 }
 
@@ -539,8 +548,16 @@ mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const voi
   k_gru_bwd_gates<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(d_mem, h_old, sr, sz, sn, sghn, n_rows, max_rows,
                                                                         dm, dgi, dgh);
   MTGNN_CHECK_LAUNCH("gru_bwd_gates");
-  MTGNN_TRY(linear_dw(dgi, 3 * dm, msg, d->dtype, dmsg, dW_ih, dmsg, max_rows, n_rows, 3 * dm, dmsg, w, rest, s, db_ih));
-  MTGNN_TRY(linear_dw(dgh, 3 * dm, h_old, MTGNN_F32, dm, dW_hh, dm, max_rows, n_rows, 3 * dm, dm, w, rest, s, db_hh));
+  if (d->dtype == MTGNN_F32) {   // both weight gradients in one launch
+    const DwProblem ps[2] = {{dgi, 3 * dm, msg, dmsg, dW_ih, dmsg, 3 * dm, dmsg, db_ih},
+                             {dgh, 3 * dm, h_old, dm, dW_hh, dm, 3 * dm, dm, db_hh}};
+    MTGNN_TRY(linear_dw_batch(ps, 2, max_rows, n_rows, MTGNN_F32, w, rest, s));
+  } else {
+    MTGNN_TRY(linear_dw(dgi, 3 * dm, msg, d->dtype, dmsg, dW_ih, dmsg, max_rows, n_rows, 3 * dm, dmsg, w, rest, s,
+                        db_ih));
+    MTGNN_TRY(linear_dw(dgh, 3 * dm, h_old, MTGNN_F32, dm, dW_hh, dm, max_rows, n_rows, 3 * dm, dm, w, rest, s,
+                        db_hh));
+  }
   if (dmsg_time && d->d_time > 0) {
     const size_t esz = d->dtype == MTGNN_F32 ? 4 : 2;
     const void* Wt = (const char*)W_ih + esz * (size_t)(2 * dm);   // columns [2 dm, 2 dm + d_time)
