@@ -121,6 +121,9 @@ __global__ __launch_bounds__(256) void k_attn_gather_q(const int32_t* __restrict
 
 // Wave per query: the rows of its valid slots, [M[n_j] || x[e_j] || cos(w (tau - t_j) + b)],
 // plus sin of the same arguments (for the time-encoder gradient), the slot's node and its tau - t_j.
+// Slots go GATHER_CHUNK at a time: the chunk's memory-row loads are all issued before any is stored.
+constexpr int GATHER_CHUNK = 8;
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_gather_kv(const int32_t* __restrict__ nbr, const float* __restrict__ nt,
                                                         const int32_t* __restrict__ neid,
@@ -138,33 +141,64 @@ __global__ __launch_bounds__(256) void k_attn_gather_kv(const int32_t* __restric
   const int c = cnt[q];
   const int64_t off = pair_off[q];
   const float tau = q_t[q];
-  for (int j = 0; j < c; ++j) {
-    const int64_t r = q * k + j, row = off + j;
-    const int64_t nb = nbr[r];
-    float* out = kv_in + row * Dkv;
-    for (int cc = lane; cc < dm; cc += 64) out[cc] = Elem<T>::load(mem, nb * dm + cc);
+  // lane j < c holds slot j's node, edge and time difference
+  const int32_t my_nb = lane < c ? nbr[q * k + lane] : 0;
+  const int32_t my_e = lane < c ? neid[q * k + lane] : 0;
+  const float my_delta = lane < c ? tau - nt[q * k + lane] : 0.f;
+  if (lane < c) {
+    pair_nbr[off + lane] = my_nb;
+    pair_delta[off + lane] = my_delta;
+  }
+  for (int j0 = 0; j0 < c; j0 += GATHER_CHUNK) {
+    int64_t nb[GATHER_CHUNK];
+#pragma unroll
+    for (int u = 0; u < GATHER_CHUNK; ++u) nb[u] = __shfl(my_nb, j0 + u, 64);
+    for (int c0 = 0; c0 < dm; c0 += 64) {
+      const int cc = c0 + lane;
+      float v[GATHER_CHUNK];
+#pragma unroll
+      for (int u = 0; u < GATHER_CHUNK; ++u) v[u] = (j0 + u < c && cc < dm) ? Elem<T>::load(mem, nb[u] * dm + cc) : 0.f;
+#pragma unroll
+      for (int u = 0; u < GATHER_CHUNK; ++u)
+        if (j0 + u < c && cc < dm) kv_in[(off + j0 + u) * Dkv + cc] = v[u];
+    }
     if (de > 0) {
-      const float* xr = x + (int64_t)neid[r] * de;
-      for (int cc = lane; cc < de; cc += 64) out[dm + cc] = pack_val(xr[cc], bf16);
+      for (int c0 = 0; c0 < de; c0 += 64) {
+        const int cc = c0 + lane;
+        float v[GATHER_CHUNK];
+#pragma unroll
+        for (int u = 0; u < GATHER_CHUNK; ++u) {
+          const int64_t e = __shfl(my_e, j0 + u, 64);
+          v[u] = (j0 + u < c && cc < de) ? x[e * de + cc] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < GATHER_CHUNK; ++u)
+          if (j0 + u < c && cc < de) kv_in[(off + j0 + u) * Dkv + dm + cc] = pack_val(v[u], bf16);
+      }
     }
-    const float delta = tau - nt[r];
-    for (int jj = lane; jj < dt; jj += 64) {
-      float sn, cs;
-      sincosf(time_arg(tw[jj], delta, tb[jj]), &sn, &cs);
-      out[dm + de + jj] = pack_val(cs, bf16);
-      sinv[row * dt + jj] = sn;
-    }
-    if (lane == 0) {
-      pair_nbr[row] = (int32_t)nb;
-      pair_delta[row] = delta;
+    for (int u = 0; u < GATHER_CHUNK; ++u) {
+      if (j0 + u >= c) break;
+      const float delta = __shfl(my_delta, j0 + u, 64);
+      const int64_t row = off + j0 + u;
+      for (int jj = lane; jj < dt; jj += 64) {
+        float sn, cs;
+        sincosf(time_arg(tw[jj], delta, tb[jj]), &sn, &cs);
+        kv_in[row * Dkv + dm + de + jj] = pack_val(cs, bf16);
+        sinv[row * dt + jj] = sn;
+      }
     }
   }
 }
 
 constexpr int MAX_DH_CHUNKS = 2;   // head width <= 128
 
+constexpr int SLOT_CHUNK = 8;   // slots whose rows are loaded together (their loads in flight at once)
+
 // Wave per query: softmax over the valid slots of each head, then the
 // probability-weighted sum of the values.  Lane j < cnt holds slot j's score.
+// Slot rows are read SLOT_CHUNK at a time, all loads issued before use; the
+// per-slot sums keep their order.  (The backward below keeps one slot at a
+// time: grouping its loads measured slower.)
 __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv, const float* __restrict__ KV,
                                                    const int32_t* __restrict__ cnt,
                                                    const int32_t* __restrict__ pair_off,
@@ -185,16 +219,26 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
       qd[cc] = d < dh ? qv[q * da + h * dh + d] : 0.f;
     }
     float my_s = -INFINITY;
-    for (int j = 0; j < c; ++j) {
-      const float* Kr = KV + (off + j) * 2 * da + h * dh;
-      float part = 0.f;
+    for (int j0 = 0; j0 < c; j0 += SLOT_CHUNK) {
+      float kv[SLOT_CHUNK][MAX_DH_CHUNKS];
 #pragma unroll
-      for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
-        const int d = lane + 64 * cc;
-        if (d < dh) part += qd[cc] * Kr[d];
+      for (int u = 0; u < SLOT_CHUNK; ++u) {
+        const float* Kr = KV + (off + j0 + u) * 2 * da + h * dh;
+#pragma unroll
+        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+          const int d = lane + 64 * cc;
+          kv[u][cc] = (j0 + u < c && d < dh) ? Kr[d] : 0.f;
+        }
       }
-      const float sc = wave_sum(part) * scale;
-      if (lane == j) my_s = sc;
+#pragma unroll
+      for (int u = 0; u < SLOT_CHUNK; ++u) {
+        if (j0 + u >= c) break;
+        float part = 0.f;
+#pragma unroll
+        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) part += qd[cc] * kv[u][cc];
+        const float sc = wave_sum(part) * scale;
+        if (lane == j0 + u) my_s = sc;
+      }
     }
     const float m = wave_max(my_s);
     const float e = lane < c ? expf(my_s - m) : 0.f;
@@ -202,13 +246,23 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
     const float pj = den > 0.f ? e / den : 0.f;
     if (lane < k) P[(q * H + h) * k + lane] = pj;
     float acc[MAX_DH_CHUNKS] = {0.f, 0.f};
-    for (int j = 0; j < c; ++j) {
-      const float pb = __shfl(pj, j, 64);
-      const float* Vr = KV + (off + j) * 2 * da + da + h * dh;
+    for (int j0 = 0; j0 < c; j0 += SLOT_CHUNK) {
+      float vv[SLOT_CHUNK][MAX_DH_CHUNKS];
 #pragma unroll
-      for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
-        const int d = lane + 64 * cc;
-        if (d < dh) acc[cc] += pb * Vr[d];
+      for (int u = 0; u < SLOT_CHUNK; ++u) {
+        const float* Vr = KV + (off + j0 + u) * 2 * da + da + h * dh;
+#pragma unroll
+        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+          const int d = lane + 64 * cc;
+          vv[u][cc] = (j0 + u < c && d < dh) ? Vr[d] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < SLOT_CHUNK; ++u) {
+        if (j0 + u >= c) break;
+        const float pb = __shfl(pj, j0 + u, 64);
+#pragma unroll
+        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) acc[cc] += pb * vv[u][cc];
       }
     }
 #pragma unroll

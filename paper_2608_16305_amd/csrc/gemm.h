@@ -530,8 +530,9 @@ __global__ void k_splitk_reduce(const float* __restrict__ part, int64_t split_st
 
 // Strip width for an output of N columns: one strip when N <= 256, else equal strips.
 int gemm_strip_width(int64_t N);
-// Tile width for an M x N output: full strips, or 64-wide tiles when strips would
-// leave the launch with few blocks (small row counts are latency-bound).
+// Tile width for an M x N output: full strips, or 32-wide tiles when strips would
+// leave the launch with few blocks (small row counts are latency-bound; more,
+// narrower blocks put more waves on each SIMD).
 int gemm_tile_width(int64_t M, int64_t N, int ksplit);
 // Weight-gradient plan over R reduction rows for an N x K output.
 struct DwPlan {
@@ -557,11 +558,12 @@ void gemm_bn_launch(const GemmArgs& g, int bn, dim3 grid, hipStream_t s) {
   if constexpr (AK && !BK) {   // data gradients: the time-gradient epilogue on 64- or 128-wide tiles
     if (g.tg_part != nullptr) {
       if (bn == 128) gemm_kernel_launch<Site, 128, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s);
-      else gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s);
+      else gemm_kernel_launch<Site, 32, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s);
       return;
     }
   }
   switch (bn) {
+    case 32: gemm_kernel_launch<Site, 32, VEC, TA, TB, AK, BK>(g, grid, s); break;
     case 64:
       if constexpr (!AK && !BK) {   // weight gradients: 64-deep k steps on 64 x 64 tiles
         if (g.tile_bk == 64) {
@@ -646,6 +648,7 @@ mtgnn_status gemm_batch_launch_t(const GemmArgs* gs, int n, int zper, hipStream_
     else gemm_batch_kernel<Site, W, false, TA, TB, AK, BK>(b, grid, s);      \
     break;
   switch (bn) {
+    MTGNN_BATCH_BN(32)
     MTGNN_BATCH_BN(64)
     MTGNN_BATCH_BN(128)
     MTGNN_BATCH_BN(160)
@@ -729,7 +732,7 @@ mtgnn_status linear_dx_timegrad(const float* dy, int64_t lddy, const void* W, in
   g.C = nullptr; g.ldc = 0;
   g.kchunk = N; g.c_split_stride = 0;
   g.tg_part = part; g.tg_sin = sin_saved; g.tg_delta = delta; g.tg_w = tw; g.tg_b = tb;
-  g.tile_bn = (K > 128 || gemm_tile_width(M, K, 1) == 64) ? 64 : 128;   // the epilogue's two tile widths
+  g.tile_bn = (K > 128 || gemm_tile_width(M, K, 1) < 128) ? 32 : 128;   // the epilogue's two tile widths
   return gemm_launch<Site, true, false>(g, MTGNN_F32, w_dtype, 1, s);
 }
 

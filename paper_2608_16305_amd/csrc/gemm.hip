@@ -75,10 +75,10 @@ int gemm_strip_width(int64_t N) {
 int gemm_tile_width(int64_t M, int64_t N, int ksplit) {
   const int full = gemm_strip_width(N);
   const int64_t blocks = cdiv(M, 64 * G_WM) * cdiv(N, full) * (ksplit < 1 ? 1 : ksplit);
-  return blocks < 1024 ? 64 : full;
+  return blocks < 1024 ? 32 : full;
 }
 
-// Up to 16 K reduction rows, 64 x 64 tiles over 128-row chunks (each block one
+// Up to 16 K reduction rows: 64 x 32 tiles over 256-row chunks (each block one
 // short reduction; the grid is tiles x chunks).  Larger reductions keep full
 // strips and cut the rows into chunks of >= 256 so the grid has about 1536
 // blocks at the host row maximum (device-side counts often leave fewer active).
@@ -86,9 +86,9 @@ DwPlan dw_plan(int64_t R, int64_t N, int64_t K) {
   DwPlan p;
   const int64_t r = R < 1 ? 1 : R;
   if (r <= 16384) {
-    p.bn = 64;
-    p.bk = 64;
-    p.kchunk = 128;
+    p.bn = 32;
+    p.bk = G_BK;
+    p.kchunk = 256;
   } else {
     p.bn = gemm_strip_width(K);
     p.bk = G_BK;
