@@ -528,8 +528,12 @@ __global__ void k_splitk_reduce(const float* __restrict__ part, int64_t split_st
                                 int64_t cols, float* __restrict__ out, int64_t ldo, int64_t ones_col,
                                 float* __restrict__ col_out);
 
-// Strip width for an output of N columns: one strip when N <= 256, else equal strips.
+// Strip width for an output of N columns: equal strips of at most 128 columns
+// (32, 64, 112 or 128 wide).  Narrower strips need less LDS, so more blocks
+// share a CU; that measured faster than reading the A rows once.
 int gemm_strip_width(int64_t N);
+// Weight gradients over many rows: one strip up to 256 columns (64 .. 256 wide).
+int gemm_wide_strip_width(int64_t N);
 // Tile width for an M x N output: full strips, or 32-wide tiles when strips would
 // leave the launch with few blocks (small row counts are latency-bound; more,
 // narrower blocks put more waves on each SIMD).
@@ -555,15 +559,29 @@ void gemm_kernel_launch(const GemmArgs& g, dim3 grid, hipStream_t s) {
 
 template <class Site, bool VEC, typename TA, typename TB, bool AK, bool BK>
 void gemm_bn_launch(const GemmArgs& g, int bn, dim3 grid, hipStream_t s) {
-  if constexpr (AK && !BK) {   // data gradients: the time-gradient epilogue on 64- or 128-wide tiles
+  if constexpr (AK && !BK) {   // data gradients: the time-gradient epilogue
     if (g.tg_part != nullptr) {
-      if (bn == 128) gemm_kernel_launch<Site, 128, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s);
-      else gemm_kernel_launch<Site, 32, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s);
+      switch (bn) {
+        case 32: gemm_kernel_launch<Site, 32, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s); break;
+        case 64: gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s); break;
+        case 112: gemm_kernel_launch<Site, 112, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s); break;
+        default: gemm_kernel_launch<Site, 128, VEC, TA, TB, AK, BK, G_BK, true>(g, grid, s); break;
+      }
       return;
     }
   }
+  if constexpr (AK || BK) {   // forward and data-gradient products: strips of at most 128 columns
+    switch (bn) {
+      case 32: gemm_kernel_launch<Site, 32, VEC, TA, TB, AK, BK>(g, grid, s); break;
+      case 64: gemm_kernel_launch<Site, 64, VEC, TA, TB, AK, BK>(g, grid, s); break;
+      case 112: gemm_kernel_launch<Site, 112, VEC, TA, TB, AK, BK>(g, grid, s); break;
+      default: gemm_kernel_launch<Site, 128, VEC, TA, TB, AK, BK>(g, grid, s); break;
+    }
+    return;
+  }
   switch (bn) {
     case 32: gemm_kernel_launch<Site, 32, VEC, TA, TB, AK, BK>(g, grid, s); break;
+    case 112: gemm_kernel_launch<Site, 112, VEC, TA, TB, AK, BK>(g, grid, s); break;
     case 64:
       if constexpr (!AK && !BK) {   // weight gradients: 64-deep k steps on 64 x 64 tiles
         if (g.tile_bk == 64) {
@@ -647,16 +665,29 @@ mtgnn_status gemm_batch_launch_t(const GemmArgs* gs, int n, int zper, hipStream_
     if (vec) gemm_batch_kernel<Site, W, true, TA, TB, AK, BK>(b, grid, s);   \
     else gemm_batch_kernel<Site, W, false, TA, TB, AK, BK>(b, grid, s);      \
     break;
-  switch (bn) {
-    MTGNN_BATCH_BN(32)
-    MTGNN_BATCH_BN(64)
-    MTGNN_BATCH_BN(128)
-    MTGNN_BATCH_BN(160)
-    MTGNN_BATCH_BN(208)
-    default:
-      if (vec) gemm_batch_kernel<Site, 256, true, TA, TB, AK, BK>(b, grid, s);
-      else gemm_batch_kernel<Site, 256, false, TA, TB, AK, BK>(b, grid, s);
-      break;
+  if constexpr (AK || BK) {
+    switch (bn) {
+      MTGNN_BATCH_BN(32)
+      MTGNN_BATCH_BN(64)
+      MTGNN_BATCH_BN(112)
+      default:
+        if (vec) gemm_batch_kernel<Site, 128, true, TA, TB, AK, BK>(b, grid, s);
+        else gemm_batch_kernel<Site, 128, false, TA, TB, AK, BK>(b, grid, s);
+        break;
+    }
+  } else {
+    switch (bn) {
+      MTGNN_BATCH_BN(32)
+      MTGNN_BATCH_BN(64)
+      MTGNN_BATCH_BN(112)
+      MTGNN_BATCH_BN(128)
+      MTGNN_BATCH_BN(160)
+      MTGNN_BATCH_BN(208)
+      default:
+        if (vec) gemm_batch_kernel<Site, 256, true, TA, TB, AK, BK>(b, grid, s);
+        else gemm_batch_kernel<Site, 256, false, TA, TB, AK, BK>(b, grid, s);
+        break;
+    }
   }
 #undef MTGNN_BATCH_BN
   MTGNN_CHECK_LAUNCH(Site::name);
@@ -732,7 +763,7 @@ mtgnn_status linear_dx_timegrad(const float* dy, int64_t lddy, const void* W, in
   g.C = nullptr; g.ldc = 0;
   g.kchunk = N; g.c_split_stride = 0;
   g.tg_part = part; g.tg_sin = sin_saved; g.tg_delta = delta; g.tg_w = tw; g.tg_b = tb;
-  g.tile_bn = (K > 128 || gemm_tile_width(M, K, 1) < 128) ? 32 : 128;   // the epilogue's two tile widths
+  g.tile_bn = gemm_tile_width(M, K, 1);
   return gemm_launch<Site, true, false>(g, MTGNN_F32, w_dtype, 1, s);
 }
 

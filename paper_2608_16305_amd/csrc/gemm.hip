@@ -64,6 +64,11 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
 }
 
 int gemm_strip_width(int64_t N) {
+  const int64_t per = cdiv(N, cdiv(N, 128));   // equal strips of at most 128 columns
+  return per <= 32 ? 32 : per <= 64 ? 64 : per <= 112 ? 112 : 128;
+}
+
+int gemm_wide_strip_width(int64_t N) {
   static const int widths[] = {64, 128, 160, 208, 256};
   const int64_t strips = cdiv(N, 256);
   const int64_t per = cdiv(N, strips);
@@ -90,7 +95,7 @@ DwPlan dw_plan(int64_t R, int64_t N, int64_t K) {
     p.bk = G_BK;
     p.kchunk = 256;
   } else {
-    p.bn = gemm_strip_width(K);
+    p.bn = gemm_wide_strip_width(K);
     p.bk = G_BK;
     const int64_t tiles = cdiv(N, 64 * G_WM) * cdiv(K, p.bn);
     int64_t want = cdiv(1536, tiles);
