@@ -424,47 +424,6 @@ struct SegCtx {
   const int32_t* seg_hi;   // [rows] one past its last
 };
 
-__device__ __forceinline__ void seg_add(const SegCtx& c, uint32_t o, float* acc, int lane) {
-  const int W = c.dm + c.w2;
-  if ((int64_t)o < c.max_q) {
-    const float* src = c.dhq + (int64_t)o * c.ldq;
-#pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) {
-      const int col = lane + 64 * i;
-      if (col < c.dm) acc[i] += src[col];
-    }
-  } else {
-    const float* src = c.dkv + ((int64_t)o - c.max_q) * c.w2;
-#pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) {
-      const int col = lane + 64 * i;
-      if (col >= c.dm && col < W) acc[i] += src[col - c.dm];
-    }
-  }
-}
-
-// The row of occurrence o spread over the lanes (zero outside its columns).
-__device__ __forceinline__ void seg_row(const SegCtx& c, uint32_t o, float* r, int lane) {
-  const int W = c.dm + c.w2;
-#pragma unroll
-  for (int i = 0; i < SEG_MAXC; ++i) r[i] = 0.f;
-  if ((int64_t)o < c.max_q) {
-    const float* src = c.dhq + (int64_t)o * c.ldq;
-#pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) {
-      const int col = lane + 64 * i;
-      if (col < c.dm) r[i] = src[col];
-    }
-  } else {
-    const float* src = c.dkv + ((int64_t)o - c.max_q) * c.w2;
-#pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) {
-      const int col = lane + 64 * i;
-      if (col >= c.dm && col < W) r[i] = src[col - c.dm];
-    }
-  }
-}
-
 __device__ __forceinline__ void seg_store(float* dst, const float* acc, int W, int lane) {
 #pragma unroll
   for (int i = 0; i < SEG_MAXC; ++i) {
@@ -473,11 +432,38 @@ __device__ __forceinline__ void seg_store(float* dst, const float* acc, int W, i
   }
 }
 
+// The row of occurrence o over the lanes, NC column chunks (zero outside its columns).
+template <int NC>
+__device__ __forceinline__ void seg_row_nc(const SegCtx& c, uint32_t o, float* r, int lane) {
+  const int W = c.dm + c.w2;
+  if ((int64_t)o < c.max_q) {
+    const float* src = c.dhq + (int64_t)o * c.ldq;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int col = lane + 64 * i;
+      r[i] = col < c.dm ? src[col] : 0.f;
+    }
+  } else {
+    const float* src = c.dkv + ((int64_t)o - c.max_q) * c.w2;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int col = lane + 64 * i;
+      r[i] = (col >= c.dm && col < W) ? src[col - c.dm] : 0.f;
+    }
+  }
+}
+
 // Wave per tile of SEG_TILE (= 64) sorted positions; lane i holds position
-// p0 + i.  A segment (one row) entirely inside the tile is written to S; the
-// piece of a segment that began before the tile goes to head[tile]; the piece
-// of one that continues past it goes to tail[tile].  The fixup pass adds the
-// pieces in tile order.
+// p0 + i.  The wave walks the positions in order with one running sum,
+// loading the rows of SEG_PREFETCH positions at a time (whatever segments
+// they belong to); when the key changes, the finished segment is stored.  A
+// segment entirely inside the tile goes to S; the piece of one that began
+// before the tile goes to head[tile]; the piece of one that continues past it
+// goes to tail[tile].  The fixup pass adds the pieces in tile order.  Each
+// segment's sum runs over its positions in order.
+constexpr int SEG_PREFETCH = 8;
+
+template <int NC>
 __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -487,40 +473,56 @@ __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   const int W = c.dm + c.w2;
   const uint32_t my_key = lane < cnt ? c.keys[p0 + lane] : c.sentinel;
   const uint32_t my_val = lane < cnt ? c.vals[p0 + lane] : 0u;
-  const uint32_t prev_key = __shfl_up(my_key, 1, 64);
-  const bool is_start = lane < cnt && my_key != c.sentinel && (lane == 0 || prev_key != my_key);
-  uint64_t starts = __ballot(is_start);
   const uint32_t key_before = p0 > 0 ? c.keys[p0 - 1] : c.sentinel;
   const uint32_t key_after = p0 + cnt < c.n_occ ? c.keys[p0 + cnt] : c.sentinel;
-  while (starts) {
-    const int a = __ffsll((unsigned long long)starts) - 1;
-    starts &= starts - 1;
-    const uint32_t key = __shfl(my_key, a, 64);
-    // segment end: next start, or the first sentinel, or the tile end
-    int b = starts ? __ffsll((unsigned long long)starts) - 1 : cnt;
-    const uint64_t sent = __ballot(lane < cnt && my_key == c.sentinel) & ~((2ull << a) - 1ull);
-    if (sent) b = min(b, __ffsll((unsigned long long)sent) - 1);
-    float acc[SEG_MAXC];
+  uint32_t cur = __shfl(my_key, 0, 64);
+  if (cur == c.sentinel) return;   // sentinels sort last: nothing in this tile
+  int start = 0;
+  float acc[NC];
 #pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) acc[i] = 0.f;
-    int p = a;
-    for (; p + 4 <= b; p += 4) {   // four rows in flight
-      const uint32_t o0 = __shfl(my_val, p, 64), o1 = __shfl(my_val, p + 1, 64);
-      const uint32_t o2 = __shfl(my_val, p + 2, 64), o3 = __shfl(my_val, p + 3, 64);
-      float r0[SEG_MAXC], r1[SEG_MAXC], r2[SEG_MAXC], r3[SEG_MAXC];
-      seg_row(c, o0, r0, lane);
-      seg_row(c, o1, r1, lane);
-      seg_row(c, o2, r2, lane);
-      seg_row(c, o3, r3, lane);
+  for (int i = 0; i < NC; ++i) acc[i] = 0.f;
+  auto flush = [&](int end) {
+    const bool before = start == 0 && key_before == cur;
+    const bool after = end == cnt && key_after == cur;
+    float* dst = before ? c.head + tile * W : (after ? c.tail + tile * W : c.S + (int64_t)cur * W);
 #pragma unroll
-      for (int i = 0; i < SEG_MAXC; ++i) acc[i] += ((r0[i] + r1[i]) + r2[i]) + r3[i];
+    for (int i = 0; i < NC; ++i) {
+      const int col = lane + 64 * i;
+      if (col < W) dst[col] = acc[i];
     }
-    for (; p < b; ++p) seg_add(c, __shfl(my_val, p, 64), acc, lane);
-    const bool before = a == 0 && key_before == key;
-    const bool after = b == cnt && key_after == key;
-    float* dst = before ? c.head + tile * W : (after ? c.tail + tile * W : c.S + (int64_t)key * W);
-    seg_store(dst, acc, W, lane);
+  };
+  for (int q0 = 0; q0 < cnt; q0 += SEG_PREFETCH) {
+    float r[SEG_PREFETCH][NC];
+#pragma unroll
+    for (int u = 0; u < SEG_PREFETCH; ++u) {
+      const int p = q0 + u;
+      const uint32_t k = __shfl(my_key, p, 64);
+      const uint32_t o = __shfl(my_val, p, 64);
+      if (p < cnt && k != c.sentinel) {
+        seg_row_nc<NC>(c, o, r[u], lane);
+      } else {
+#pragma unroll
+        for (int i = 0; i < NC; ++i) r[u][i] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SEG_PREFETCH; ++u) {
+      const int p = q0 + u;
+      if (p >= cnt) break;
+      const uint32_t k = __shfl(my_key, p, 64);
+      if (k != cur) {
+        flush(p);
+        if (k == c.sentinel) return;
+        cur = k;
+        start = p;
+#pragma unroll
+        for (int i = 0; i < NC; ++i) acc[i] = 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < NC; ++i) acc[i] += r[u][i];
+    }
   }
+  flush(cnt);
 }
 
 // Block b: wave w first zeroes row 4b + w if that row has no occurrence.
@@ -784,7 +786,19 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     c.dhq = b.dm_in + da; c.ldq = ldm; c.dkv = b.dKV; c.dm = dm; c.w2 = 2 * da;
     c.S = b.S; c.head = b.head; c.tail = b.tail;
     const int64_t ntiles = cdiv(n_occ, SEG_TILE);
-    k_segsum_tiles<<<(unsigned)cdiv(ntiles, 4), 256, 0, s>>>(c);
+    {
+      const unsigned gt = (unsigned)cdiv(ntiles, 4);
+      switch (cdiv(dm + 2 * da, 64)) {   // column chunks per lane (validation keeps the width <= 512)
+        case 1: k_segsum_tiles<1><<<gt, 256, 0, s>>>(c); break;
+        case 2: k_segsum_tiles<2><<<gt, 256, 0, s>>>(c); break;
+        case 3: k_segsum_tiles<3><<<gt, 256, 0, s>>>(c); break;
+        case 4: k_segsum_tiles<4><<<gt, 256, 0, s>>>(c); break;
+        case 5: k_segsum_tiles<5><<<gt, 256, 0, s>>>(c); break;
+        case 6: k_segsum_tiles<6><<<gt, 256, 0, s>>>(c); break;
+        case 7: k_segsum_tiles<7><<<gt, 256, 0, s>>>(c); break;
+        default: k_segsum_tiles<8><<<gt, 256, 0, s>>>(c); break;
+      }
+    }
     MTGNN_CHECK_LAUNCH("segsum_tiles");
     const int64_t nfix = ntiles > cdiv(max_rows, 4) ? ntiles : cdiv(max_rows, 4);
     k_segsum_fixup<<<(unsigned)nfix, 256, 0, s>>>(c, n_rows, max_rows, ntiles);
