@@ -197,8 +197,8 @@ constexpr int SLOT_CHUNK = 8;   // slots whose rows are loaded together (their l
 // Wave per query: softmax over the valid slots of each head, then the
 // probability-weighted sum of the values.  Lane j < cnt holds slot j's score.
 // Slot rows are read SLOT_CHUNK at a time, all loads issued before use; the
-// per-slot sums keep their order.  (The backward below keeps one slot at a
-// time: grouping its loads measured slower.)
+// per-slot sums keep their order.  (The backward below groups the value-row
+// loads of its first phase only: grouping the second phase measured slower.)
 __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv, const float* __restrict__ KV,
                                                    const int32_t* __restrict__ cnt,
                                                    const int32_t* __restrict__ pair_off,
@@ -299,16 +299,26 @@ __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__
     }
     const float pl = lane < c ? P[(q * H + h) * k + lane] : 0.f;
     float my_dp = 0.f;
-    for (int j = 0; j < c; ++j) {
-      const float* Vr = KV + (off + j) * 2 * da + da + h * dh;
-      float part = 0.f;
+    for (int j0 = 0; j0 < c; j0 += SLOT_CHUNK) {   // value rows of SLOT_CHUNK slots loaded together
+      float vv[SLOT_CHUNK][MAX_DH_CHUNKS];
 #pragma unroll
-      for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
-        const int d = lane + 64 * cc;
-        if (d < dh) part += gd[cc] * Vr[d];
+      for (int u = 0; u < SLOT_CHUNK; ++u) {
+        const float* Vr = KV + (off + j0 + u) * 2 * da + da + h * dh;
+#pragma unroll
+        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+          const int d = lane + 64 * cc;
+          vv[u][cc] = (j0 + u < c && d < dh) ? Vr[d] : 0.f;
+        }
       }
-      const float dp = wave_sum(part);
-      if (lane == j) my_dp = dp;
+#pragma unroll
+      for (int u = 0; u < SLOT_CHUNK; ++u) {
+        if (j0 + u >= c) break;
+        float part = 0.f;
+#pragma unroll
+        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) part += gd[cc] * vv[u][cc];
+        const float dp = wave_sum(part);
+        if (lane == j0 + u) my_dp = dp;
+      }
     }
     const float sdp = wave_sum(pl * my_dp);
     const float dsl = pl * (my_dp - sdp);
@@ -525,18 +535,21 @@ __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   flush(cnt);
 }
 
-// Block b: wave w first zeroes row 4b + w if that row has no occurrence.
-// Then, if the row at the end of tile b starts in tile b and continues past
-// it (rows inside one tile were written whole), the block sums that row:
-// tail[b] + head[b+1] + ... + head[t1].  The 4 waves take interleaved heads
-// with four loads in flight; their partial sums are added in wave order.
-__global__ __launch_bounds__(256) void k_segsum_fixup(SegCtx c, const int32_t* __restrict__ n_rows,
-                                                      int64_t max_rows, int64_t ntiles) {
-  __shared__ float part[4][SEG_MAXC * 64];
+// Block b (FIX_WAVES waves): wave w first zeroes row FIX_WAVES b + w if that
+// row has no occurrence.  Then, if the row at the end of tile b starts in
+// tile b and continues past it (rows inside one tile were written whole), the
+// block sums that row: tail[b] + head[b+1] + ... + head[t1].  The waves take
+// interleaved heads with four loads in flight; their partial sums are added
+// in wave order.
+constexpr int FIX_WAVES = 16;
+
+__global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const int32_t* __restrict__ n_rows,
+                                                                 int64_t max_rows, int64_t ntiles) {
+  __shared__ float part[FIX_WAVES][SEG_MAXC * 64];
   const int64_t blk = blockIdx.x;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int W = c.dm + c.w2;
-  const int64_t zr = blk * 4 + wid;
+  const int64_t zr = blk * FIX_WAVES + wid;
   if (zr < eff_count(max_rows, n_rows) && c.seg_lo[zr] == c.seg_hi[zr]) {   // no occurrence: zero gradient
     float z[SEG_MAXC];
 #pragma unroll
@@ -555,18 +568,19 @@ __global__ __launch_bounds__(256) void k_segsum_fixup(SegCtx c, const int32_t* _
 #pragma unroll
   for (int i = 0; i < SEG_MAXC; ++i) acc[i] = 0.f;
   int64_t t = blk + 1 + wid;
-  for (; t + 12 <= t1; t += 16) {
+  constexpr int64_t S4 = 4 * FIX_WAVES;
+  for (; t + 3 * FIX_WAVES <= t1; t += S4) {
     const float* h0 = c.head + t * W;
-    const float* h1 = h0 + 4 * (int64_t)W;
-    const float* h2 = h0 + 8 * (int64_t)W;
-    const float* h3 = h0 + 12 * (int64_t)W;
+    const float* h1 = h0 + FIX_WAVES * (int64_t)W;
+    const float* h2 = h0 + 2 * FIX_WAVES * (int64_t)W;
+    const float* h3 = h0 + 3 * FIX_WAVES * (int64_t)W;
 #pragma unroll
     for (int i = 0; i < SEG_MAXC; ++i) {
       const int col = lane + 64 * i;
       if (col < W) acc[i] += ((h0[col] + h1[col]) + h2[col]) + h3[col];
     }
   }
-  for (; t <= t1; t += 4) {
+  for (; t <= t1; t += FIX_WAVES) {
     const float* h = c.head + t * W;
 #pragma unroll
     for (int i = 0; i < SEG_MAXC; ++i) {
@@ -583,7 +597,11 @@ __global__ __launch_bounds__(256) void k_segsum_fixup(SegCtx c, const int32_t* _
   for (int i = 0; i < SEG_MAXC; ++i) {
     const int col = lane + 64 * i;
     const int o = i * 64 + lane;
-    if (col < W) acc[i] = tl[col] + (((part[0][o] + part[1][o]) + part[2][o]) + part[3][o]);
+    if (col < W) {
+      float sum = 0.f;
+      for (int w = 0; w < FIX_WAVES; ++w) sum += part[w][o];
+      acc[i] = tl[col] + sum;
+    }
   }
   seg_store(c.S + (int64_t)key * W, acc, W, lane);
 }
@@ -800,8 +818,8 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
       }
     }
     MTGNN_CHECK_LAUNCH("segsum_tiles");
-    const int64_t nfix = ntiles > cdiv(max_rows, 4) ? ntiles : cdiv(max_rows, 4);
-    k_segsum_fixup<<<(unsigned)nfix, 256, 0, s>>>(c, n_rows, max_rows, ntiles);
+    const int64_t nfix = ntiles > cdiv(max_rows, FIX_WAVES) ? ntiles : cdiv(max_rows, FIX_WAVES);
+    k_segsum_fixup<<<(unsigned)nfix, 64 * FIX_WAVES, 0, s>>>(c, n_rows, max_rows, ntiles);
     MTGNN_CHECK_LAUNCH("segsum_fixup");
     const int W = dm + 2 * da;
     k_copy_cols<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(b.S, W, n_rows, max_rows, dm, d_mem, dm);
