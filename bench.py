@@ -249,7 +249,7 @@ def _counter_rows(path, counter):
 def _calibrated(path, counter, probe_bytes):
     """Per-site mean counter value (KiB per dispatch) scaled by the copy-probe factor."""
     rows = _counter_rows(path, counter)
-    first_step = next(i for i, r in enumerate(rows) if "k_agg_keys" in r["Kernel_Name"])
+    first_step = next(i for i, r in enumerate(rows) if "mtgnn::(anonymous namespace)::k_agg_" in r["Kernel_Name"] or "mtgnn::k_agg_" in r["Kernel_Name"])
     probes = [r for r in rows[:first_step] if "copyBuffer" in r["Kernel_Name"]][-2:]
     if len(probes) != 2:
         raise SystemExit(f"{path}: the two probe copies before the first step were not found")
