@@ -6,6 +6,7 @@ Usage:  python -m paper_2608_16305_amd.build   (or __graft_entry__.build())
 import concurrent.futures
 import glob
 import os
+import re
 import subprocess
 import sys
 
@@ -24,12 +25,35 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-u
          "-I", INCLUDE, "-I", SRC]
 
 
+# Kernels that read LDS filled by direct global-to-LDS loads through inline
+# assembly must not spill: a spill could copy a register before its LDS data
+# has arrived.  The build fails if one of them does.
+NO_SPILL = ("k_gemm_rs",)
+
+
+def _spilling_kernels(remarks: str) -> list:
+    """Names of NO_SPILL kernels whose resource-usage remarks report a VGPR or SGPR spill."""
+    bad, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"[VS]GPRs Spill: (\d+)", line)
+        if m and name and int(m.group(1)) > 0 and any(k in name for k in NO_SPILL):
+            bad.append(name)
+    return bad
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+    cmd = [HIPCC] + FLAGS + ["-Rpass-analysis=kernel-resource-usage", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
+    bad = _spilling_kernels(r.stderr)
+    if bad:
+        raise RuntimeError(f"{src}: kernels that must not spill do: {sorted(set(bad))}")
     return obj
 
 

@@ -272,6 +272,89 @@ struct TileVec {
   __device__ __forceinline__ void store(float* lds, int tid) const { store_from(lds, tid, v); }
 };
 
+// Time-gradient epilogue of a 64-row block (4 waves x 16 rows): instead of C,
+// write the column sums over the block's rows of  g = -C(i,j) sin(arg_ij)  and of
+// g * delta_i to tg_part[row block][0 / 1][j].  red: 8 BN floats of LDS that no
+// wave reads any more.
+template <int BN>
+__device__ __forceinline__ void gemm_store_timegrad(const GemmArgs& g, const TileCoord tc, int64_t M,
+                                                    const f32x4 (&acc)[BN / 16], float* red) {
+  constexpr int NT = BN / 16;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t row0 = tc.x * 64, col0 = tc.y * BN;
+  float* red_w = red;
+  float* red_b = red + 4 * BN;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int64_t gj = col0 + j * 16 + (lane & 15);
+    float cw = 0.f, cb = 0.f;
+    if (gj < g.N) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t gi = row0 + wid * 16 + 4 * (lane >> 4) + r;
+        if (gi >= M) continue;
+        const float d = g.tg_delta ? g.tg_delta[gi] : 0.f;
+        const float sn = g.tg_sin ? g.tg_sin[gi * g.N + gj] : sinf(time_arg(g.tg_w[gj], d, g.tg_b[gj]));
+        const float gv = acc[j][r] * -sn;
+        cb += gv;
+        cw += gv * d;
+      }
+    }
+    cw += __shfl_xor(cw, 16, 64);
+    cb += __shfl_xor(cb, 16, 64);
+    cw += __shfl_xor(cw, 32, 64);
+    cb += __shfl_xor(cb, 32, 64);
+    if (lane < 16) {
+      red_w[wid * BN + j * 16 + lane] = cw;
+      red_b[wid * BN + j * 16 + lane] = cb;
+    }
+  }
+  __syncthreads();
+  for (int c = tid; c < BN; c += G_THREADS) {
+    const int64_t gj = col0 + c;
+    if (gj >= g.N) continue;
+    g.tg_part[(tc.x * 2 + 0) * g.N + gj] = ((red_w[c] + red_w[BN + c]) + red_w[2 * BN + c]) + red_w[3 * BN + c];
+    g.tg_part[(tc.x * 2 + 1) * g.N + gj] = ((red_b[c] + red_b[BN + c]) + red_b[2 * BN + c]) + red_b[3 * BN + c];
+  }
+}
+
+// Epilogue of a (64 WM) x BN block: bias, accumulate, ReLU gate / pre-activation,
+// bf16 rounding, bias-grad column, split-K partial placement.
+template <int BN, int WM>
+__device__ __forceinline__ void gemm_store(const GemmArgs& g, const TileCoord tc, int64_t M,
+                                           const f32x4 (&acc)[WM][BN / 16]) {
+  constexpr int NT = BN / 16;
+  constexpr int BM = 64 * WM;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int64_t row0 = tc.x * BM, col0 = tc.y * BN;
+  float* C = g.C + tc.z * g.c_split_stride;
+  const bool split = g.c_split_stride != 0;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int64_t gj = col0 + j * 16 + (lane & 15);
+    if (gj >= g.N) continue;
+    const bool to_col = gj == g.ones_col && !split;
+    const float bj = g.bias ? g.bias[gj] : 0.f;
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t gi = row0 + (wid * WM + i) * 16 + 4 * (lane >> 4) + r;
+        if (gi >= M) continue;
+        float v = acc[i][j][r] + bj;
+        if (g.accumulate) v += C[gi * g.ldc + gj];
+        if (g.gate && !(g.gate[gi * g.ldgate + gj] > 0.f)) v = 0.f;
+        if (g.relu) {
+          g.C2[gi * g.ldc2 + gj] = v;
+          v = fmaxf(v, 0.f);
+        }
+        if (g.round_bf16) v = round_to_bf16(v);
+        if (to_col) g.col_out[gi] = v;
+        else C[gi * g.ldc + gj] = v;
+      }
+  }
+}
+
 // Block: (64 WM) rows x BN columns; wave w computes WM 16-row tiles x BN.
 // Within each 16-deep k chunk, lane l feeds the MFMA k-slot l/16 with
 // k = 4 (l/16) + s at sub-step s (s = 0..3), for both operands (see Lds); the
@@ -419,74 +502,10 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, const TileCoord tc)
 
   if constexpr (TGE) {   // time-gradient epilogue (tg_* arguments)
     static_assert(8 * BN <= NBUF * LA::SIZE && WM == 1, "time-gradient epilogue scratch");
-    {
-      float* red_w = &As[0][0];   // the operand tiles are no longer read (last loop barrier)
-      float* red_b = red_w + 4 * BN;
-#pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        const int64_t gj = col0 + j * 16 + (lane & 15);
-        float cw = 0.f, cb = 0.f;
-        if (gj < g.N) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int64_t gi = row0 + wid * 16 + 4 * (lane >> 4) + r;
-            if (gi >= M) continue;
-            const float d = g.tg_delta ? g.tg_delta[gi] : 0.f;
-            const float sn = g.tg_sin ? g.tg_sin[gi * g.N + gj] : sinf(time_arg(g.tg_w[gj], d, g.tg_b[gj]));
-            const float gv = acc[0][j][r] * -sn;
-            cb += gv;
-            cw += gv * d;
-          }
-        }
-        cw += __shfl_xor(cw, 16, 64);
-        cb += __shfl_xor(cb, 16, 64);
-        cw += __shfl_xor(cw, 32, 64);
-        cb += __shfl_xor(cb, 32, 64);
-        if (lane < 16) {
-          red_w[wid * BN + j * 16 + lane] = cw;
-          red_b[wid * BN + j * 16 + lane] = cb;
-        }
-      }
-      __syncthreads();
-      for (int c = tid; c < BN; c += G_THREADS) {
-        const int64_t gj = col0 + c;
-        if (gj >= g.N) continue;
-        g.tg_part[(tc.x * 2 + 0) * g.N + gj] =
-            ((red_w[c] + red_w[BN + c]) + red_w[2 * BN + c]) + red_w[3 * BN + c];
-        g.tg_part[(tc.x * 2 + 1) * g.N + gj] =
-            ((red_b[c] + red_b[BN + c]) + red_b[2 * BN + c]) + red_b[3 * BN + c];
-      }
-      return;
-    }
+    gemm_store_timegrad<BN>(g, tc, M, acc[0], &As[0][0]);   // the operand tiles are no longer read
+    return;
   }
-
-  // epilogue: bias, accumulate, ReLU gate / pre-activation, bf16 rounding, bias-grad column
-  float* C = g.C + tc.z * g.c_split_stride;
-  const bool split = g.c_split_stride != 0;
-#pragma unroll
-  for (int j = 0; j < NT; ++j) {
-    const int64_t gj = col0 + j * 16 + (lane & 15);
-    if (gj >= g.N) continue;
-    const bool to_col = gj == g.ones_col && !split;
-    const float bj = g.bias ? g.bias[gj] : 0.f;
-#pragma unroll
-    for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t gi = row0 + (wid * WM + i) * 16 + 4 * (lane >> 4) + r;
-        if (gi >= M) continue;
-        float v = acc[i][j][r] + bj;
-        if (g.accumulate) v += C[gi * g.ldc + gj];
-        if (g.gate && !(g.gate[gi * g.ldgate + gj] > 0.f)) v = 0.f;
-        if (g.relu) {
-          g.C2[gi * g.ldc2 + gj] = v;
-          v = fmaxf(v, 0.f);
-        }
-        if (g.round_bf16) v = round_to_bf16(v);
-        if (to_col) g.col_out[gi] = v;
-        else C[gi * g.ldc + gj] = v;
-      }
-  }
+  gemm_store<BN, WM>(g, tc, M, acc);
 }
 
 // One output tile per block; tile coordinates from the XCD-grouped order.
@@ -615,8 +634,19 @@ void gemm_set_vec_flags(GemmArgs& g) {   // general loader: 4-wide only when ali
   g.b_vec = vec_ok(g.B, BK ? g.b_sj : g.b_sk, sizeof(TB)) ? 1 : 0;
 }
 
+bool gemm_rs_applicable(const GemmArgs& g);
+mtgnn_status gemm_rs_launch(const GemmArgs& g, hipStream_t s);
+
 template <class Site, typename TA, typename TB, bool AK, bool BK>
 mtgnn_status gemm_launch_t(const GemmArgs& g0, int ksplit, hipStream_t s) {
+  if constexpr (std::is_same<Site, site::KvProj>::value && std::is_same<TA, float>::value &&
+                std::is_same<TB, float>::value && AK && BK) {
+    // key/value projection over the neighbour slots: weight-stationary kernel (gemm_rs.h)
+    if (ksplit <= 1 && gemm_rs_applicable(g0)) {
+      TimedScope ts(Site::name, s);
+      return gemm_rs_launch(g0, s);
+    }
+  }
   GemmArgs g = g0;
   gemm_set_vec_flags<TA, TB, AK, BK>(g);
   const int bn = g.tile_bn > 0 ? g.tile_bn : gemm_tile_width(g.M, g.N, ksplit);
