@@ -157,7 +157,8 @@ def main():
     out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                        "frac": achieved / peak, "traffic": read_traffic(dominant, w), "kernel": dominant,
                        "launches_per_step": launches_per_step, "avg_launch_us": avg_s * 1e6,
-                       "flops_per_launch": flops}
+                       "flops_per_launch": flops,
+                       "warmup_site_us": {k: v * 1e3 for k, v in site_ms.items()}}
 
     if args.cpu_steps > 0:
         out["cpu_baseline"] = cpu_baseline(w, s, params, mem, lu, b0, args.cpu_steps)
@@ -202,7 +203,8 @@ def valid_slots(runner, s, w, b):
 
 CSRC = os.path.join(ROOT, "paper_2608_16305_amd", "csrc")
 # sources that define the hot-site kernels and their launches
-TRAFFIC_SOURCES = ("common.h", "gemm.h", "gemm.hip", "gemm_nt.hip", "gemm_nn.hip", "gemm_tn.hip", "attention.hip")
+TRAFFIC_SOURCES = ("common.h", "gemm.h", "gemm.hip", "gemm_nt.hip", "gemm_nn.hip", "gemm_tn.hip", "gemm_rs.h",
+                   "gemm_rs.hip", "lds_dma.h", "attention.hip")
 
 
 def kernel_fingerprint():

@@ -801,10 +801,20 @@ mtgnn_status linear_dx_timegrad(const float* dy, int64_t lddy, const void* W, in
 // db (optional): db[N] = sum over rows of dy, computed as an extra all-ones column of x.
 size_t linear_dw_ws_bytes(int64_t R, int64_t N, int64_t K);
 
+bool dw_rs_applicable(const float* X, int64_t ldx, int nx, const void* Y, int y_dtype, int64_t ldy, int ny);
+mtgnn_status dw_rs_launch(const float* X, int64_t ldx, int nx, const float* Y, int64_t ldy, int ny, int64_t R,
+                          const int32_t* R_dev, float* dW, int64_t lddw, float* db, void* ws, size_t ws_bytes,
+                          hipStream_t s);
+
 template <class Site = site::Generic>
 mtgnn_status linear_dw(const float* dy, int64_t lddy, const void* x, int x_dtype, int64_t ldx, float* dW,
                        int64_t lddw, int64_t R, const int32_t* R_dev, int64_t N, int64_t K, void* ws,
                        size_t ws_bytes, hipStream_t s, float* db = nullptr) {
+  if constexpr (std::is_same<Site, site::KvDw>::value) {
+    // key/value weight gradient over the neighbour slots: output-stationary kernel (gemm_rs.h)
+    if (db && dw_rs_applicable(dy, lddy, (int)N, x, x_dtype, ldx, (int)K))
+      return dw_rs_launch(dy, lddy, (int)N, (const float*)x, ldx, (int)K, R, R_dev, dW, lddw, db, ws, ws_bytes, s);
+  }
   const int64_t Kc = db ? K + 1 : K;   // extra all-ones column of x gives the bias gradient
   const DwPlan plan = dw_plan(R, N, Kc);
   const int ksplit = plan.ksplit;

@@ -194,9 +194,17 @@ mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_
   return MTGNN_OK;
 }
 
+size_t dw_rs_ws_bytes(int nx, int ny);
+
 size_t linear_dw_ws_bytes(int64_t R, int64_t N, int64_t K) {
   const DwPlan p = dw_plan(R, N, K + 1);
-  return p.ksplit > 1 ? sizeof(float) * (size_t)p.ksplit * N * (K + 1) : 0;
+  size_t b = p.ksplit > 1 ? sizeof(float) * (size_t)p.ksplit * N * (K + 1) : 0;
+  const int64_t nj = cdiv(K + 1, 16);
+  if (N > 192 && N <= 208 && (nj == 13 || nj == 14)) {   // shapes the output-stationary kernel may take
+    const size_t r = dw_rs_ws_bytes((int)N, (int)K);
+    b = r > b ? r : b;
+  }
+  return b;
 }
 
 }  // namespace mtgnn

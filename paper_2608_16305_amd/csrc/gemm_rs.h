@@ -262,3 +262,172 @@ bool gemm_rs_applicable(const GemmArgs& g);
 mtgnn_status gemm_rs_launch(const GemmArgs& g, hipStream_t s);
 
 }  // namespace mtgnn
+
+namespace mtgnn {
+
+namespace rs {
+constexpr int dw_stride(int nt) {   // smallest stride >= 16 nt floats that is 16 mod 32
+  return (16 * nt) % 32 == 16 ? 16 * nt : 16 * nt + 16;
+}
+}  // namespace rs
+
+// Output-stationary weight gradient over many rows:
+//   part[block][i][j] = sum over the block's rows p of X[p][i] Y[p][j],   i < NI 16, j < NJ 16,
+// with X = the output gradient (dy, row stride ldx, nx = N_out valid columns) and
+// Y = the layer input (row stride ldy, ny valid columns) followed by an
+// all-ones column at j = ny (the bias gradient).  Rows come in 16-row chunks;
+// block b takes chunks b, b + gridDim.x, ...; a fixed-order reduction over the
+// blocks' partials (k_splitk_reduce) gives dW and db.
+//
+// Each of the 4 waves accumulates a fixed set of 16 x 16 output tiles for the
+// whole launch: tile rows I = 3 wid .. 3 wid + 2 (all NJ tile columns) and, in
+// the last tile row I = 12, the tile columns J = wid, wid + 4, ...  (NI = 13).
+// Per chunk both operands go to LDS by direct global-to-LDS loads one chunk
+// ahead; MFMA sub-step s of a chunk takes rows 4 s + l/16 (lane l), reading one
+// float per operand fragment.  Rows past the row count are zero-filled.
+template <class Site, int NJ>
+__global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict__ X, int64_t ldx, int nx,
+                                                     const float* __restrict__ Y, int64_t ldy, int ny, int64_t R,
+                                                     const int32_t* R_dev, float* __restrict__ part) {
+  constexpr int NI = 13, RW = 3;                 // tile rows: 3 per wave + the shared last one
+  constexpr int EX = (NJ + 3) / 4;               // tiles of the last tile row per wave, at most
+  constexpr int SX = rs::dw_stride(NI), SY = rs::dw_stride(NJ);
+  constexpr int SLOT = 16 * (SX + SY);           // floats per chunk slot
+  __shared__ __attribute__((aligned(16))) float lds[2 * SLOT];
+
+  const int64_t rows = eff_count(R, R_dev);
+  const int64_t nchunks = cdiv(rows, 16);
+  const int64_t b0 = blockIdx.x, G = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int fr = lane & 15, fg = lane >> 4;
+  const uint32_t base = (uint32_t)(uintptr_t)(lds_void_ptr)lds;
+
+  // constant columns of both slots: X columns nx .. 16 NI and Y columns ny .. 16 NJ are
+  // zero, except Y column ny (the all-ones column)
+  for (int e = tid; e < 2 * 16 * (SX + SY); e += G_THREADS) {
+    const int slot = e / (16 * (SX + SY)), rem = e % (16 * (SX + SY));
+    const bool isx = rem < 16 * SX;
+    const int col = isx ? rem % SX : (rem - 16 * SX) % SY;
+    const int lim = isx ? nx : ny;
+    if (col >= lim) {
+      const float v = (!isx && col == ny) ? 1.f : 0.f;
+      asm volatile("ds_write_b32 %0, %1" ::"v"(base + (uint32_t)(slot * SLOT + rem) * 4u), "v"(v) : "memory");
+    }
+  }
+
+  // DMA of one chunk: this wave's rows 4 wid .. 4 wid + 3 of X and of Y; rows past
+  // the row count are zero-filled instead
+  auto issue = [&](int64_t chunk, int slot) {
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int r = 4 * wid + rr;
+      const int64_t gr = chunk * 16 + r;
+      const uint32_t dx = base + (uint32_t)(slot * SLOT + r * SX) * 4u;
+      const uint32_t dy = base + (uint32_t)(slot * SLOT + 16 * SX + r * SY) * 4u;
+      if (gr < rows) {
+        if (4 * lane < nx) dma::load16(X + gr * ldx + 4 * lane, dx);
+        if (4 * lane < ny) dma::load16(Y + gr * ldy + 4 * lane, dy);
+      } else {
+        if (4 * lane < nx) dma::ds_zero4(dx + 16u * lane);
+        if (4 * lane < ny) dma::ds_zero4(dy + 16u * lane);
+      }
+    }
+  };
+
+  f32x4 acc[RW][NJ], acx[EX];
+#pragma unroll
+  for (int i = 0; i < RW; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int e = 0; e < EX; ++e) acx[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int64_t nmine = b0 < nchunks ? cdiv(nchunks - b0, G) : 0;
+  if (nmine > 0) issue(b0, 0);
+  // fragment addresses within a slot: X column 16 I + fr, Y column 16 J + fr, row 4 s + fg
+  const uint32_t xa = (uint32_t)(fg * SX + 16 * RW * wid + fr) * 4u;
+  const uint32_t xl = (uint32_t)(fg * SX + 16 * (NI - 1) + fr) * 4u;
+  const uint32_t ya = (uint32_t)(16 * SX + fg * SY + fr) * 4u;
+  auto read1 = [&](uint32_t addr) {
+    float v;
+    asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+  };
+  for (int64_t it = 0; it < nmine; ++it) {
+    const int slot = (int)(it & 1);
+    dma::wait_vm<0>();
+    dma::wait_lgkm0();
+    dma::barrier();   // chunk `it` is in LDS; every wave is done with chunk it - 1's slot
+    if (it + 1 < nmine) issue(b0 + (it + 1) * G, slot ^ 1);
+    const uint32_t sb = base + (uint32_t)(slot * SLOT) * 4u;
+    // fragments of sub-step s (rows 4 s + fg of the chunk); those of s + 1 are read while
+    // the MFMAs of s run (they pass through asm statements after the next reads)
+    float fx[4][RW + 1], fy[4][NJ], fe[4][EX];
+    auto read_frags = [&](int s) {
+      const uint32_t rx = sb + (uint32_t)(4 * s * SX) * 4u, ry = sb + (uint32_t)(4 * s * SY) * 4u;
+#pragma unroll
+      for (int i = 0; i < RW; ++i) fx[s][i] = read1(rx + xa + 64u * i);
+      fx[s][RW] = read1(rx + xl);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) fy[s][j] = read1(ry + ya + 64u * j);
+#pragma unroll
+      for (int e = 0; e < EX; ++e) {   // branch-free: a tile past the last column reads the last one (never stored)
+        const int J = wid + 4 * e < NJ ? wid + 4 * e : NJ - 1;
+        fe[s][e] = read1(ry + ya + 64u * (uint32_t)J);
+      }
+    };
+    read_frags(0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      dma::wait_lgkm0();
+      if (s + 1 < 4) read_frags(s + 1);
+#pragma unroll
+      for (int i = 0; i <= RW; ++i) asm volatile("" : "+v"(fx[s][i]));
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) asm volatile("" : "+v"(fy[s][j]));
+#pragma unroll
+      for (int e = 0; e < EX; ++e) asm volatile("" : "+v"(fe[s][e]));
+#pragma unroll
+      for (int i = 0; i < RW; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fx[s][i], fy[s][j], acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int e = 0; e < EX; ++e)
+        acx[e] = __builtin_amdgcn_mfma_f32_16x16x4f32(fx[s][RW], fe[s][e], acx[e], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);   // the sub-step's MFMAs stay above the next wait
+    }
+  }
+
+  // this block's partial: [NI 16 (rows < nx)][ny + 1 columns]
+  const int64_t ldp = ny + 1;
+  float* out = part + b0 * (int64_t)nx * ldp;
+  auto store = [&](int I, int J, const f32x4& v) {
+    const int col = 16 * J + fr;
+    if (col > ny) return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 16 * I + 4 * fg + r;
+      if (row < nx) out[(int64_t)row * ldp + col] = v[r];
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < RW; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) store(RW * wid + i, j, acc[i][j]);
+#pragma unroll
+  for (int e = 0; e < EX; ++e)
+    if (wid + 4 * e < NJ) store(NI - 1, wid + 4 * e, acx[e]);
+}
+
+// Host side (gemm_rs.hip): dW[nx, ny] = X^T Y and db[nx] = column sums of X over R rows
+// (clamped by R_dev), for nx in (192, 208] and ny + 1 <= 16 NJ with NJ in {13, 14}.
+// part: workspace of dw_rs_ws_bytes(nx, ny).
+bool dw_rs_applicable(const float* X, int64_t ldx, int nx, const void* Y, int y_dtype, int64_t ldy, int ny);
+size_t dw_rs_ws_bytes(int nx, int ny);
+mtgnn_status dw_rs_launch(const float* X, int64_t ldx, int nx, const float* Y, int64_t ldy, int ny, int64_t R,
+                          const int32_t* R_dev, float* dW, int64_t lddw, float* db, void* ws, size_t ws_bytes,
+                          hipStream_t s);
+
+}  // namespace mtgnn

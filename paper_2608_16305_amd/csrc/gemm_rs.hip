@@ -38,3 +38,41 @@ mtgnn_status gemm_rs_launch(const GemmArgs& g0, hipStream_t s) {
 }
 
 }  // namespace mtgnn
+
+namespace mtgnn {
+
+namespace {
+constexpr int DW_RS_MAX_BLOCKS = 256;   // partials the workspace is sized for (one per CU of an MI355X)
+}
+
+bool dw_rs_applicable(const float* X, int64_t ldx, int nx, const void* Y, int y_dtype, int64_t ldy, int ny) {
+  const int nj = (int)cdiv(ny + 1, 16);
+  return y_dtype == MTGNN_F32 && nx > 192 && nx <= 208 && nx % 4 == 0 && ny % 4 == 0 && (nj == 13 || nj == 14) &&
+         ((uintptr_t)X % 16) == 0 && ((uintptr_t)Y % 16) == 0 && ldx % 4 == 0 && ldy % 4 == 0 && cu_count() > 0;
+}
+
+size_t dw_rs_ws_bytes(int nx, int ny) { return sizeof(float) * (size_t)DW_RS_MAX_BLOCKS * nx * (ny + 1); }
+
+mtgnn_status dw_rs_launch(const float* X, int64_t ldx, int nx, const float* Y, int64_t ldy, int ny, int64_t R,
+                          const int32_t* R_dev, float* dW, int64_t lddw, float* db, void* ws, size_t ws_bytes,
+                          hipStream_t s) {
+  const size_t per = sizeof(float) * (size_t)nx * (ny + 1);
+  int64_t grid = cu_count();
+  if ((int64_t)(ws_bytes / per) < grid) grid = (int64_t)(ws_bytes / per);
+  if (grid < 1) return MTGNN_EWORKSPACE;
+  float* part = (float*)ws;
+  {
+    TimedScope ts(site::KvDw::name, s);
+    if (cdiv(ny + 1, 16) == 13)
+      k_dw_rs<site::KvDw, 13><<<(unsigned)grid, G_THREADS, 0, s>>>(X, ldx, nx, Y, ldy, ny, R, R_dev, part);
+    else
+      k_dw_rs<site::KvDw, 14><<<(unsigned)grid, G_THREADS, 0, s>>>(X, ldx, nx, Y, ldy, ny, R, R_dev, part);
+  }
+  MTGNN_CHECK_LAUNCH("dw_rs");
+  const int64_t outs = (int64_t)nx * (ny + 1);
+  k_splitk_reduce<<<(unsigned)cdiv(outs, 64), 256, 0, s>>>(part, outs, (int)grid, nx, ny + 1, dW, lddw, ny, db);
+  MTGNN_CHECK_LAUNCH("splitk_reduce");
+  return MTGNN_OK;
+}
+
+}  // namespace mtgnn
