@@ -79,21 +79,32 @@ __global__ void k_agg_reset(const int32_t* __restrict__ src, const int32_t* __re
   if (node >= 0) T[node] = -1;
 }
 
+// Messages of one wave are consecutive, so among the wave's messages to one node
+// the largest index is the highest such lane: only that lane issues the atomic
+// (hub nodes receive hundreds of messages per batch; this bounds their atomics
+// by the number of waves).
 __global__ void k_agg_max(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
                           const uint8_t* __restrict__ flags, int64_t nm, int32_t* __restrict__ T) {
   const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= nm) return;
-  const int32_t node = msg_node(src, dst, flags, m);
-  if (node >= 0) atomicMax(&T[node], (int32_t)m);
+  const int lane = threadIdx.x & 63;
+  const int32_t node = m < nm ? msg_node(src, dst, flags, m) : -1;
+  uint64_t pending = __ballot(node >= 0);
+  while (pending) {   // one pass per distinct node of the wave
+    const int leader = __ffsll((unsigned long long)pending) - 1;
+    const int32_t v = __builtin_amdgcn_readlane(node, leader);
+    const uint64_t same = __ballot(node == v);
+    if (lane == 63 - __clzll(same)) atomicMax(&T[v], (int32_t)m);
+    pending &= ~same;
+  }
 }
 
-// One block compacts up to AGG_BLOCK_MAX messages.  Thread t first loads the
-// winner flags of messages 1024 j + t for every round j (all loads in
-// flight together); round j then ranks its winners with a wave ballot and the
-// 16 wave counts (double-buffered, one barrier per round).
+// One block compacts up to AGG_BLOCK_MAX messages: thread t owns messages
+// 16 t .. 16 t + 15 (so the output order, increasing m, is thread order), flags
+// its winners (m == T[node(m)]), and one block-wide exclusive scan of the
+// per-thread winner counts gives every winner its position.
 constexpr int AGG_BLOCK_THREADS = 1024;
-constexpr int AGG_ROUNDS = 16;
-constexpr int64_t AGG_BLOCK_MAX = AGG_BLOCK_THREADS * AGG_ROUNDS;
+constexpr int AGG_PER_THREAD = 16;
+constexpr int64_t AGG_BLOCK_MAX = AGG_BLOCK_THREADS * AGG_PER_THREAD;
 
 __global__ __launch_bounds__(AGG_BLOCK_THREADS) void k_agg_compact_block(const int32_t* __restrict__ src,
                                                                          const int32_t* __restrict__ dst,
@@ -102,42 +113,42 @@ __global__ __launch_bounds__(AGG_BLOCK_THREADS) void k_agg_compact_block(const i
                                                                          int32_t* __restrict__ uniq,
                                                                          int32_t* __restrict__ winner,
                                                                          int32_t* __restrict__ n_uniq) {
-  __shared__ int wcnt[2][AGG_BLOCK_THREADS / 64];
+  __shared__ int wsum[AGG_BLOCK_THREADS / 64];
   const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
-  const uint64_t lt_mask = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-  int32_t node[AGG_ROUNDS];
+  const int64_t m0 = (int64_t)t * AGG_PER_THREAD;
+  int32_t node[AGG_PER_THREAD];
 #pragma unroll
-  for (int j = 0; j < AGG_ROUNDS; ++j) {
-    const int64_t m = (int64_t)j * AGG_BLOCK_THREADS + t;
-    node[j] = m < nm ? msg_node(src, dst, flags, m) : -1;
-  }
+  for (int j = 0; j < AGG_PER_THREAD; ++j) node[j] = m0 + j < nm ? msg_node(src, dst, flags, m0 + j) : -1;
   uint32_t winbits = 0;
 #pragma unroll
-  for (int j = 0; j < AGG_ROUNDS; ++j) {
-    const int64_t m = (int64_t)j * AGG_BLOCK_THREADS + t;
-    if (node[j] >= 0 && T[node[j]] == (int32_t)m) winbits |= 1u << j;
-  }
-  int base = 0;
+  for (int j = 0; j < AGG_PER_THREAD; ++j)
+    if (node[j] >= 0 && T[node[j]] == (int32_t)(m0 + j)) winbits |= 1u << j;
+  const int cnt = __popc(winbits);
+  int incl = cnt;   // inclusive scan over the wave
 #pragma unroll
-  for (int j = 0; j < AGG_ROUNDS; ++j) {
-    const bool win = (winbits >> j) & 1u;
-    const uint64_t bal = __ballot(win);
-    if (lane == 0) wcnt[j & 1][wid] = __popcll(bal);
-    __syncthreads();
-    int off = base, tot = 0;
-    for (int w = 0; w < AGG_BLOCK_THREADS / 64; ++w) {
-      const int c = wcnt[j & 1][w];
-      if (w < wid) off += c;
-      tot += c;
-    }
-    if (win) {
-      const int pos = off + __popcll(bal & lt_mask);
-      uniq[pos] = node[j];
-      winner[pos] = j * AGG_BLOCK_THREADS + t;
-    }
-    base += tot;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
   }
-  if (t == 0) *n_uniq = base;
+  if (lane == 63) wsum[wid] = incl;
+  __syncthreads();
+  int base = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < AGG_BLOCK_THREADS / 64; ++w) {
+    const int c = wsum[w];
+    base += w < wid ? c : 0;
+    total += c;
+  }
+  int pos = base + incl - cnt;
+#pragma unroll
+  for (int j = 0; j < AGG_PER_THREAD; ++j) {
+    if ((winbits >> j) & 1u) {
+      uniq[pos] = node[j];
+      winner[pos] = (int32_t)(m0 + j);
+      ++pos;
+    }
+  }
+  if (t == 0) *n_uniq = total;
 }
 
 __global__ void k_agg_flags(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,

@@ -7,28 +7,37 @@ namespace {
 
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// One thread per query: lower_bound of the query time in the node's
-// time-sorted list, then the k entries just before it, newest first.
+// One wave per query: lower_bound of the query time in the node's time-sorted
+// list by a 64-way search (each round the 64 lanes probe evenly spaced entries
+// and the range shrinks 64-fold: a list of 4 M entries takes 4 dependent
+// rounds), then the k entries just before it, newest first, one lane each.
 __global__ __launch_bounds__(256) void k_sample_recent(const int64_t* __restrict__ off, const int32_t* __restrict__ nbr,
                                                        const float* __restrict__ t, const int32_t* __restrict__ eid,
                                                        const int32_t* __restrict__ q_node,
                                                        const float* __restrict__ q_t, const int32_t* __restrict__ n_q,
                                                        int64_t max_q, int k, int32_t* __restrict__ out_nbr,
                                                        float* __restrict__ out_t, int32_t* __restrict__ out_eid) {
-  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= eff_count(max_q, n_q)) return;
+  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (q >= eff_count(max_q, n_q)) return;   // wave-uniform
   const int64_t n = q_node[q];
   const float tau = q_t[q];
   const int64_t lo = off[n];
+  // invariant: the first entry with t >= tau lies in [a, b] (b: none)
   int64_t a = lo, b = off[n + 1];
-  while (a < b) {
-    const int64_t mid = a + ((b - a) >> 1);
-    if (t[mid] < tau) a = mid + 1;
-    else b = mid;
+  while (b - a > 64) {
+    const int64_t step = (b - a + 63) >> 6;
+    const int64_t p = a + (int64_t)(lane + 1) * step - 1;
+    const bool lt = p < b && t[p] < tau;                       // true for a prefix of the lanes
+    const int c = __popcll(__ballot(lt));
+    const int64_t pc = a + (int64_t)(c + 1) * step - 1;        // probe of lane c: t >= tau there
+    a += (int64_t)c * step;
+    if (c < 64 && pc < b) b = pc;
   }
-  const int64_t end = a;
+  const int64_t p = a + lane;
+  const int64_t end = a + __popcll(__ballot(p < b && t[p] < tau));
   const int64_t o = q * k;
-  for (int s = 0; s < k; ++s) {
+  for (int s = lane; s < k; s += 64) {
     const int64_t idx = end - 1 - s;
     if (idx >= lo) {
       out_nbr[o + s] = nbr[idx];
@@ -84,8 +93,8 @@ mtgnn_status sample_recent_impl(const int64_t* off, const int32_t* nbr, const fl
                                 const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q, int k,
                                 int32_t* out_nbr, float* out_t, int32_t* out_eid, hipStream_t s) {
   if (max_q <= 0) return MTGNN_OK;
-  k_sample_recent<<<(unsigned)cdiv(max_q, 256), 256, 0, s>>>(off, nbr, t, eid, q_node, q_t, n_q, max_q, k, out_nbr,
-                                                              out_t, out_eid);
+  k_sample_recent<<<(unsigned)cdiv(max_q, 4), 256, 0, s>>>(off, nbr, t, eid, q_node, q_t, n_q, max_q, k, out_nbr,
+                                                            out_t, out_eid);
   MTGNN_CHECK_LAUNCH("sample_recent");
   return MTGNN_OK;
 }
