@@ -32,7 +32,9 @@ NO_SPILL = ("k_gemm_rs", "k_dw_rs")
 
 
 def _spilling_kernels(remarks: str) -> list:
-    """Names of NO_SPILL kernels whose resource-usage remarks report a VGPR or SGPR spill."""
+    """Names of kernels whose resource-usage remarks report a spill (NO_SPILL kernels) or any use of
+    scratch memory (every kernel: private arrays that are indexed at run time land there, and
+    each access is then a memory round trip)."""
     bad, name = [], None
     for line in remarks.splitlines():
         m = re.search(r"Function Name: (\S+)", line)
@@ -41,6 +43,9 @@ def _spilling_kernels(remarks: str) -> list:
             continue
         m = re.search(r"[VS]GPRs Spill: (\d+)", line)
         if m and name and int(m.group(1)) > 0 and any(k in name for k in NO_SPILL):
+            bad.append(name)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name and int(m.group(1)) > 0:
             bad.append(name)
     return bad
 
@@ -53,7 +58,7 @@ def _compile(src: str) -> str:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
     bad = _spilling_kernels(r.stderr)
     if bad:
-        raise RuntimeError(f"{src}: kernels that must not spill do: {sorted(set(bad))}")
+        raise RuntimeError(f"{src}: kernels spill or use scratch memory: {sorted(set(bad))}")
     return obj
 
 
