@@ -233,6 +233,29 @@ mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, co
                                      float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes,
                                      hipStream_t stream);
 
+/* Row a7 with two streams: the same computation, arguments and results as
+ * mtgnn_temporal_attn_bwd, with the d_mem part (grouping every occurrence of
+ * an updated node and summing it) enqueued on a second stream so that it runs
+ * concurrently with the parameter gradients, which stay on `stream`.
+ *   dmem_stream -- a second stream of the caller, at the default priority;
+ *   fork, join  -- two events of the caller (timing may be disabled).
+ * The call records `fork` on `stream` once the inputs of the d_mem part are
+ * ready, makes dmem_stream wait for it, enqueues the d_mem part there, records
+ * `join` on dmem_stream and makes `stream` wait for `join`: work enqueued on
+ * `stream` afterwards is ordered after both parts, as with
+ * mtgnn_temporal_attn_bwd.  Results are bitwise identical to it.  The two
+ * parts use disjoint regions of ws (the same size as for
+ * mtgnn_temporal_attn_bwd).  Errors: as mtgnn_temporal_attn_bwd; EINVAL if
+ * dmem_stream, fork or join is NULL while max_rows > 0. */
+mtgnn_status mtgnn_temporal_attn_bwd_overlap(const int32_t* q_node, const float* q_t, const int32_t* n_q,
+                                             int64_t max_q, const int32_t* nbr, const float* nt, const float* dz,
+                                             const void* save, const int32_t* uniq, const int32_t* n_rows,
+                                             int64_t max_rows, const float* time_w, const float* time_b,
+                                             const mtgnn_attn_params* params, const mtgnn_dims* dims,
+                                             mtgnn_attn_grads* grads, float* d_mem, float* d_time_w,
+                                             float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
+                                             hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join);
+
 /* Row a8. Backward of mtgnn_gru_update for d_mem = dL/dh' [max_rows, d_mem].
  * The previous memory h is detached.
  *   save, msg   -- the forward call's (save must not be NULL there);

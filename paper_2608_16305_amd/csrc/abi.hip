@@ -284,12 +284,13 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
                        ws, ws_bytes, stream);
 }
 
-mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+static mtgnn_status attn_bwd_checked(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
                                      const int32_t* nbr, const float* nt, const float* dz, const void* save,
                                      const int32_t* uniq, const int32_t* n_rows, int64_t max_rows,
                                      const float* time_w, const float* time_b, const mtgnn_attn_params* params,
                                      const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem, float* d_time_w,
-                                     float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream) {
+                                     float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
+                                     hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join) {
   MTGNN_TRY(check_dims(d));
   MTGNN_TRY(check_attn_params(params));
   MTGNN_TRY(check_rows(max_rows));
@@ -312,7 +313,31 @@ mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, co
   if (ws_bytes < attn_bwd_ws(d, max_q, max_rows)) return fail(MTGNN_EWORKSPACE, "temporal_attn_bwd ws");
   REQ(ws, "ws");
   return attn_bwd_impl(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params, d,
-                       g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream);
+                       g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, dmem_stream, fork, join);
+}
+
+mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                     const int32_t* nbr, const float* nt, const float* dz, const void* save,
+                                     const int32_t* uniq, const int32_t* n_rows, int64_t max_rows,
+                                     const float* time_w, const float* time_b, const mtgnn_attn_params* params,
+                                     const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem, float* d_time_w,
+                                     float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return attn_bwd_checked(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params,
+                          d, g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, nullptr, nullptr, nullptr);
+}
+
+mtgnn_status mtgnn_temporal_attn_bwd_overlap(const int32_t* q_node, const float* q_t, const int32_t* n_q,
+                                             int64_t max_q, const int32_t* nbr, const float* nt, const float* dz,
+                                             const void* save, const int32_t* uniq, const int32_t* n_rows,
+                                             int64_t max_rows, const float* time_w, const float* time_b,
+                                             const mtgnn_attn_params* params, const mtgnn_dims* d,
+                                             mtgnn_attn_grads* g, float* d_mem, float* d_time_w, float* d_time_b,
+                                             void* ws, size_t ws_bytes, hipStream_t stream, hipStream_t dmem_stream,
+                                             hipEvent_t fork, hipEvent_t join) {
+  if (max_rows > 0 && (!dmem_stream || !fork || !join))
+    return fail(MTGNN_EINVAL, "temporal_attn_bwd_overlap: dmem_stream, fork and join are required");
+  return attn_bwd_checked(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params,
+                          d, g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, dmem_stream, fork, join);
 }
 
 mtgnn_status mtgnn_gru_update_bwd(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,

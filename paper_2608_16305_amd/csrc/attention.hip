@@ -619,8 +619,10 @@ struct BwdWs {
   float *dm1, *dm_in, *dattn, *dqv, *dKV, *tg_part, *S, *head, *tail, *dWkv, *dbkv;
   uint32_t *keys, *vals;
   int32_t *seg_lo, *seg_hi, *row_of;
-  char* scratch;
+  char* scratch;          // split-K partials of the parameter-gradient products
   size_t scratch_bytes;
+  char* sort_scratch;     // radix sort of the dM' grouping (disjoint: the two parts may run concurrently)
+  size_t sort_scratch_bytes;
   size_t total;
 };
 
@@ -648,15 +650,17 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   v.seg_lo = (int32_t*)take(sizeof(int32_t) * (max_rows > 0 ? max_rows : 1));
   v.seg_hi = (int32_t*)take(sizeof(int32_t) * (max_rows > 0 ? max_rows : 1));
   v.row_of = (int32_t*)take(sizeof(int32_t) * s.N);
-  size_t sc = radix_sort_ws_bytes(n_occ);
+  size_t sc = 0;
   auto mx = [&](size_t x) { if (x > sc) sc = x; };
   {
     const int64_t Ns[4] = {s.da, s.da, s.da, s.da}, Ks[4] = {s.da, s.da + s.dm, s.da, s.Dq};
     mx(linear_dw_batch_ws_bytes(s.Q, Ns, Ks, 4));
   }
   mx(linear_dw_ws_bytes(s.P, 2 * s.da, s.Dkv));
-  v.scratch = take(sc);
-  v.scratch_bytes = a256(sc);
+  v.scratch = take(sc > 0 ? sc : 1);
+  v.scratch_bytes = a256(sc > 0 ? sc : 1);
+  v.sort_scratch_bytes = a256(radix_sort_ws_bytes(n_occ));
+  v.sort_scratch = take(v.sort_scratch_bytes);
   v.total = (size_t)(w - (char*)base);
   return v;
 }
@@ -726,65 +730,19 @@ size_t attn_bwd_ws(const mtgnn_dims* d, int64_t max_q, int64_t max_rows) {
   return carve_bwd(nullptr, AttnShape(d, max_q), max_rows).total;
 }
 
-mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
-                           const int32_t* nbr, const float* nt, const float* dz, const void* save, const int32_t* uniq,
-                           const int32_t* n_rows, int64_t max_rows, const float* tw, const float* tb,
-                           const mtgnn_attn_params* p, const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem,
-                           float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes, hipStream_t s) {
-  (void)q_t;
-  (void)nbr;
-  (void)nt;
-  const AttnShape sh(d, max_q);
-  const AttnSave sv = carve_save((void*)save, sh);
-  const BwdWs b = carve_bwd(ws, sh, max_rows);
-  if (ws_bytes < b.total) return MTGNN_EWORKSPACE;
-  const int wt = d->dtype;
-  const int64_t Q = sh.Q, P = sh.P, ldm = sh.da + sh.dm;
-  const int da = sh.da, dm = sh.dm, dt = sh.dt;
-  char* sc = b.scratch;
-  const size_t scb = b.scratch_bytes;
-  auto wofs = [&](const void* W, int64_t col) { return (const void*)((const char*)W + sh.esz * (size_t)col); };
+namespace {
 
-  // merge MLP: z = W_2 a1 + b_2, a1 = relu(m1), m1 = W_1 m_in + b_1
-  // (their weight gradients run as one batch after the score backward)
-  MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
-  MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
-  // output projection: o = W_o attn + b_o   (do = dm_in[:, :da])
-  MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
-  // softmax-weighted sum and scores
-  {
-    TimedScope ts("k_attn_core_bwd", s);
-    k_attn_core_bwd<<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q, max_q,
-                                                          sh.k, da, sh.H, b.dKV, b.dqv);
-  }
-  MTGNN_CHECK_LAUNCH("attn_core_bwd");
-  // weight gradients of the query, output and merge layers, one batch over the query rows
-  {
-    const DwProblem ps[4] = {{dz, da, sv.a1, da, g->W_2, da, da, da, g->b_2},
-                             {b.dm1, da, sv.m_in, ldm, g->W_1, ldm, da, ldm, g->b_1},
-                             {b.dm_in, ldm, sv.attn, da, g->W_o, da, da, da, g->b_o},
-                             {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, sh.Dq, g->b_q}};
-    MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
-  }
-  // query projection: dhq += dqv W_q[:, :dm];  dphi(0) = dqv W_q[:, dm:]
-  MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
-  if (dt > 0) {   // phi(0) of the queries: delta = 0, so only the bias part is nonzero
-    MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,
-                                 b.tg_part, s));
-    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, Q, n_q, 64 * G_WM, dt, d_time_w, d_time_b, false, s));
-  }
-  // key/value projection over the compact slots (stacked [W_k; W_v])
-  MTGNN_TRY(linear_dw<site::KvDw>(b.dKV, 2 * da, sv.kv_in, MTGNN_F32, sh.Dkv, b.dWkv, sh.Dkv, P, sv.n_valid, 2 * da,
-                                  sh.Dkv, sc, scb, s, b.dbkv));
-  k_split_kv_grads<<<(unsigned)cdiv((int64_t)da * sh.Dkv, 256), 256, 0, s>>>(b.dWkv, b.dbkv, da, sh.Dkv, g->W_k,
-                                                                              g->W_v, g->b_k, g->b_v);
-  MTGNN_CHECK_LAUNCH("split_kv_grads");
-  if (dt > 0) {   // phi(tau - t_j) of the neighbour slots, with the saved sin(arg)
-    MTGNN_TRY(linear_dx_timegrad<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, P, sv.n_valid,
-                                             2 * da, dt, sv.sinv, sv.pair_delta, tw, tb, b.tg_part, s));
-    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, P, sv.n_valid, 64 * G_WM, dt, d_time_w, d_time_b, true, s));
-  }
-  // d M' for the updated rows: group every occurrence by row, sum in a fixed order
+// d M' for the updated rows (reads dh_q in dm_in[:, da:], dK|dV, the slot nodes and
+// [W_k; W_v]; writes d_mem).  Its workspace regions (keys, vals, segment bounds, row
+// map, S, tile partials, sort scratch) are disjoint from the parameter part's.
+mtgnn_status attn_bwd_dmem(const int32_t* q_node, const int32_t* n_q, int64_t max_q, const AttnShape& sh,
+                           const AttnSave& sv, const BwdWs& b, const int32_t* uniq, const int32_t* n_rows,
+                           int64_t max_rows, int wt, float* d_mem, hipStream_t s) {
+  const int64_t Q = sh.Q, P = sh.P, ldm = sh.da + sh.dm;
+  const int da = sh.da, dm = sh.dm;
+  char* sc = b.sort_scratch;
+  const size_t scb = b.sort_scratch_bytes;
+  // group every occurrence by row, sum in a fixed order
   if (max_rows > 0) {
     const int64_t n_occ = Q + P;
     const uint32_t sentinel = (uint32_t)max_rows;
@@ -827,6 +785,108 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     MTGNN_TRY(linear_dx(b.S + dm, W, sv.W_kv, wt, sh.Dkv, d_mem, dm, max_rows, n_rows, 2 * da, dm, true, s));
   }
   return MTGNN_OK;
+}
+
+// The parameter gradients that follow the fork point (weight gradients of the
+// query/output/merge layers and of [W_k; W_v], the time-encoder gradients).
+mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const AttnSave& sv, const BwdWs& b,
+                             const float* dz, const float* tw, const float* tb, const mtgnn_attn_params* p,
+                             int wt, mtgnn_attn_grads* g, float* d_time_w, float* d_time_b, hipStream_t s) {
+  const int64_t Q = sh.Q, P = sh.P, ldm = sh.da + sh.dm;
+  const int da = sh.da, dm = sh.dm, dt = sh.dt;
+  char* sc = b.scratch;
+  const size_t scb = b.scratch_bytes;
+  auto wofs = [&](const void* W, int64_t col) { return (const void*)((const char*)W + sh.esz * (size_t)col); };
+  // Order: the time-encoder gradients and the data-gradient product first, the
+  // weight gradients last, so that the d M' part (on its own stream when
+  // overlapped) shares the GPU with the smaller products rather than with the
+  // key/value weight gradient.
+  if (dt > 0) {   // phi(0) of the queries: delta = 0, so only the bias part is nonzero
+    MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,
+                                 b.tg_part, s));
+    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, Q, n_q, 64 * G_WM, dt, d_time_w, d_time_b, false, s));
+  }
+  if (dt > 0) {   // phi(tau - t_j) of the neighbour slots, with the saved sin(arg)
+    MTGNN_TRY(linear_dx_timegrad<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, P, sv.n_valid,
+                                             2 * da, dt, sv.sinv, sv.pair_delta, tw, tb, b.tg_part, s));
+    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, P, sv.n_valid, 64 * G_WM, dt, d_time_w, d_time_b, true, s));
+  }
+  // weight gradients of the query, output and merge layers, one batch over the query rows
+  {
+    const DwProblem ps[4] = {{dz, da, sv.a1, da, g->W_2, da, da, da, g->b_2},
+                             {b.dm1, da, sv.m_in, ldm, g->W_1, ldm, da, ldm, g->b_1},
+                             {b.dm_in, ldm, sv.attn, da, g->W_o, da, da, da, g->b_o},
+                             {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, sh.Dq, g->b_q}};
+    MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
+  }
+  // key/value projection over the compact slots (stacked [W_k; W_v])
+  MTGNN_TRY(linear_dw<site::KvDw>(b.dKV, 2 * da, sv.kv_in, MTGNN_F32, sh.Dkv, b.dWkv, sh.Dkv, P, sv.n_valid, 2 * da,
+                                  sh.Dkv, sc, scb, s, b.dbkv));
+  k_split_kv_grads<<<(unsigned)cdiv((int64_t)da * sh.Dkv, 256), 256, 0, s>>>(b.dWkv, b.dbkv, da, sh.Dkv, g->W_k,
+                                                                              g->W_v, g->b_k, g->b_v);
+  MTGNN_CHECK_LAUNCH("split_kv_grads");
+  return MTGNN_OK;
+}
+
+}  // namespace
+
+mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                           const int32_t* nbr, const float* nt, const float* dz, const void* save, const int32_t* uniq,
+                           const int32_t* n_rows, int64_t max_rows, const float* tw, const float* tb,
+                           const mtgnn_attn_params* p, const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem,
+                           float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes, hipStream_t s,
+                           hipStream_t s_dmem, hipEvent_t fork, hipEvent_t join) {
+  (void)q_t;
+  (void)nbr;
+  (void)nt;
+  const AttnShape sh(d, max_q);
+  const AttnSave sv = carve_save((void*)save, sh);
+  const BwdWs b = carve_bwd(ws, sh, max_rows);
+  if (ws_bytes < b.total) return MTGNN_EWORKSPACE;
+  const int wt = d->dtype;
+  const int64_t Q = sh.Q, ldm = sh.da + sh.dm;
+  const int da = sh.da, dm = sh.dm;
+
+  // merge MLP: z = W_2 a1 + b_2, a1 = relu(m1), m1 = W_1 m_in + b_1
+  // (their weight gradients run as one batch after the score backward)
+  MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
+  MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
+  // output projection: o = W_o attn + b_o   (do = dm_in[:, :da])
+  MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
+  // softmax-weighted sum and scores
+  {
+    TimedScope ts("k_attn_core_bwd", s);
+    k_attn_core_bwd<<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q, max_q,
+                                                          sh.k, da, sh.H, b.dKV, b.dqv);
+  }
+  MTGNN_CHECK_LAUNCH("attn_core_bwd");
+  // query projection, data gradient: dhq += dqv W_q[:, :dm] (the last input of the d M' grouping)
+  MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
+  if (s_dmem == nullptr || max_rows <= 0) {
+    MTGNN_TRY(attn_bwd_params(n_q, sh, sv, b, dz, tw, tb, p, wt, g, d_time_w, d_time_b, s));
+    if (max_rows > 0) MTGNN_TRY(attn_bwd_dmem(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, wt, d_mem, s));
+    return MTGNN_OK;
+  }
+  // fork: d M' on the second stream, the parameter gradients here; join before returning
+  hipError_t e = hipEventRecord(fork, s);
+  if (e == hipSuccess) e = hipStreamWaitEvent(s_dmem, fork, 0);
+  if (e != hipSuccess) {
+    set_hip_error(e, "attn_bwd fork");
+    return MTGNN_EHIP;
+  }
+  MTGNN_TRY(attn_bwd_dmem(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, wt, d_mem, s_dmem));
+  e = hipEventRecord(join, s_dmem);
+  if (e != hipSuccess) {
+    set_hip_error(e, "attn_bwd join");
+    return MTGNN_EHIP;
+  }
+  const mtgnn_status st = attn_bwd_params(n_q, sh, sv, b, dz, tw, tb, p, wt, g, d_time_w, d_time_b, s);
+  e = hipStreamWaitEvent(s, join, 0);   // even after a failure, leave `stream` ordered after the second stream
+  if (e != hipSuccess) {
+    set_hip_error(e, "attn_bwd join wait");
+    return MTGNN_EHIP;
+  }
+  return st;
 }
 
 }  // namespace mtgnn

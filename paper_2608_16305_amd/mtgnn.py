@@ -20,7 +20,8 @@ OP_TEMPORAL_ATTN, OP_TEMPORAL_ATTN_BWD, OP_GRU_UPDATE_BWD, OP_BUILD_MESSAGES_BWD
 
 ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
-    "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_bwd", "mtgnn_gru_update_bwd",
+    "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap",
+    "mtgnn_gru_update_bwd",
     "mtgnn_build_messages_bwd", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
 )
@@ -66,6 +67,9 @@ _SIGS = {
                             _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_bwd": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, C.POINTER(AttnParams),
                                 C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_temporal_attn_bwd_overlap": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P,
+                                        C.POINTER(AttnParams), C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P,
+                                        _SZ, _P, _P, _P, _P],
     "mtgnn_gru_update_bwd": [_P, _P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_build_messages_bwd": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _SZ, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
@@ -243,6 +247,28 @@ def mtgnn_temporal_attn_bwd(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_
                                          _ptr(d_time_w, torch.float32, "d_time_w"),
                                          _ptr(d_time_b, torch.float32, "d_time_b"), wp, wb, _stream(stream)),
            "mtgnn_temporal_attn_bwd")
+
+
+def _event(e, name):
+    h = e.cuda_event if isinstance(e, torch.cuda.Event) else 0
+    if not h:
+        raise MtgnnError(f"{name}: a torch.cuda.Event that has been recorded once (so that it exists) is required")
+    return C.c_void_p(h)
+
+
+def mtgnn_temporal_attn_bwd_overlap(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w,
+                                    time_b, params: AttnParams, d: Dims, grads: AttnGrads, d_mem, d_time_w, d_time_b,
+                                    ws, dmem_stream, fork, join, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_temporal_attn_bwd_overlap(
+        _ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"), _ptr(n_q, torch.int32, "n_q", True),
+        int(max_q), _ptr(nbr, torch.int32, "nbr"), _ptr(nt, torch.float32, "nt"), _ptr(dz, torch.float32, "dz"),
+        _ptr(save, torch.uint8, "save"), _ptr(uniq, torch.int32, "uniq", True),
+        _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows), _ptr(time_w, torch.float32, "time_w"),
+        _ptr(time_b, torch.float32, "time_b"), C.byref(params), C.byref(d), C.byref(grads),
+        _ptr(d_mem, torch.float32, "d_mem", True), _ptr(d_time_w, torch.float32, "d_time_w"),
+        _ptr(d_time_b, torch.float32, "d_time_b"), wp, wb, _stream(stream), _stream(dmem_stream),
+        _event(fork, "fork"), _event(join, "join")), "mtgnn_temporal_attn_bwd_overlap")
 
 
 def mtgnn_gru_update_bwd(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d: Dims, dW_ih, dW_hh, db_ih, db_hh,

@@ -4,8 +4,10 @@ A step on batch b (default lag-1 order) runs
   memory phase on batch b-1:  aggregate_last -> build_messages -> gru_update
   embedding on batch b:       build_queries  -> sample_recent  -> temporal_attn
   backward:                   temporal_attn_bwd -> gru_update_bwd -> build_messages_bwd
-all enqueued on one HIP stream with no host synchronisation: the only
-data-dependent sizes (updated rows, queries) stay in device memory.
+all enqueued on one HIP stream with no host synchronisation (the only
+data-dependent sizes, updated rows and queries, stay in device memory), except
+that the attention backward's d_mem part runs on a second stream, forked and
+joined with events inside the call (overlap=True; bitwise the same results).
 """
 
 import numpy as np
@@ -19,9 +21,10 @@ ATTN_B = ("b_q", "b_k", "b_v", "b_o", "b_1", "b_2")
 
 class TGNStep:
     def __init__(self, w, stream, params: dict, memory: np.ndarray, last_update: np.ndarray, device="cuda",
-                 lag: int = 1, torch_stream=None):
+                 lag: int = 1, torch_stream=None, overlap: bool = True):
         self.w = w
         self.lag = lag
+        self.overlap = overlap
         self.dev = torch.device(device)
         self.ts = torch_stream
         self.dtype_code = M.BF16 if w.dtype == "bf16" else M.F32
@@ -91,6 +94,13 @@ class TGNStep:
         self.ws = M.alloc_bytes(need, dev)   # the calls of one step run in stream order and share it
         self.ap = M.attn_params(self.params, d)
         self.ag = M.attn_grads(self.grads)
+        # second stream (default priority) and fork/join events for the attention
+        # backward's d_mem part; recording the events once makes them exist
+        self.dmem_stream = torch.cuda.Stream(device=dev)
+        self.fork, self.join = torch.cuda.Event(), torch.cuda.Event()
+        s0 = self.ts if self.ts is not None else torch.cuda.current_stream(dev)
+        self.fork.record(s0)
+        self.join.record(s0)
 
     def _batch(self, lo, hi):
         if hi <= lo:
@@ -121,9 +131,16 @@ class TGNStep:
 
     def backward(self, dz):
         p, g, s = self.params, self.grads, self.ts
-        M.mtgnn_temporal_attn_bwd(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz, self.attn_save,
-                                  self.uniq, self.n_uniq, self.max_rows, p["time_w"], p["time_b"], self.ap, self.d,
-                                  self.ag, self.d_mem, g["time_w"], g["time_b"], self.ws, stream=s)
+        if self.overlap:   # the d_mem part runs on the second stream, joined before the GRU backward
+            M.mtgnn_temporal_attn_bwd_overlap(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
+                                              self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"],
+                                              p["time_b"], self.ap, self.d, self.ag, self.d_mem, g["time_w"],
+                                              g["time_b"], self.ws, self.dmem_stream, self.fork, self.join, stream=s)
+        else:
+            M.mtgnn_temporal_attn_bwd(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
+                                      self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],
+                                      self.ap, self.d, self.ag, self.d_mem, g["time_w"], g["time_b"], self.ws,
+                                      stream=s)
         M.mtgnn_gru_update_bwd(self.d_mem, self.gru_save, self.msg, self.n_uniq, self.max_rows, p["W_ih"], p["W_hh"],
                                self.d, g["W_ih"], g["W_hh"], g["b_ih"], g["b_hh"], self.dmsg_time, self.ws, stream=s)
         M.mtgnn_build_messages_bwd(self.dmsg_time, self.dt, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],

@@ -161,3 +161,34 @@ def test_edge_large_batch_multiblock_paths():
     s = tiny_stream(w, seed=11, t_scale=1000.0, tie_every=7, flags_p=(0.2, 0.3))
     mem, lu = random_state(w, seed=6)
     _tiny_run(w, s, mem, lu, range(1, 3))
+
+
+def test_backward_overlap_bitwise():
+    """The two-stream attention backward (d_mem part on a second stream) gives bitwise the
+    results of the single-stream call, from the same state (bipartite stream, 3 steps)."""
+    from paper_2608_16305_amd.step import TGNStep
+    from tests._gpu import dz_tensor, n_targets
+    w = workload(2)
+    log("[parity] overlap vs single stream, workload 2")
+    s = make_stream(w)
+    params = init_params(w, random_bias=True)
+    mem, lu = random_state(w, seed=11)
+    outs = []
+    for overlap in (False, True):
+        r = TGNStep(w, s, params, mem, lu, overlap=overlap)
+        res = {}
+        for b in range(1, 4):
+            dz, _ = dz_tensor(r, w, b, n_targets(s, *r.batch_range(b)))
+            r.step(b, dz)
+            torch.cuda.synchronize()
+            n = int(r.n_uniq.item())
+            res[f"d_mem{b}"] = to_np(r.d_mem)[:n].copy()
+            res.update({f"{k}{b}": to_np(v).copy() for k, v in r.grads.items()})
+        res["memory"] = to_np(r.memory).copy()
+        outs.append(res)
+        del r
+        torch.cuda.empty_cache()
+    assert outs[0].keys() == outs[1].keys()
+    for k in outs[0]:
+        a, b = outs[0][k], outs[1][k]
+        assert a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
