@@ -6,8 +6,10 @@ A step on batch b (default lag-1 order) runs
   backward:                   temporal_attn_bwd -> gru_update_bwd -> build_messages_bwd
 all enqueued on one HIP stream with no host synchronisation (the only
 data-dependent sizes, updated rows and queries, stay in device memory), except
-that the attention backward's d_mem part runs on a second stream, forked and
-joined with events inside the call (overlap=True; bitwise the same results).
+that with overlap=True (the default) two pieces run on a second stream, forked
+and joined with events: the queries and their sampling, during the memory
+phase, and the attention backward's d_mem part.  Results are bitwise those of
+overlap=False.
 """
 
 import numpy as np
@@ -92,15 +94,18 @@ class TGNStep:
                (M.OP_BUILD_MESSAGES_BWD, R, 0)]
         need = max(M.workspace_bytes(op, d, r, q) for op, r, q in ops)
         self.ws = M.alloc_bytes(need, dev)   # the calls of one step run in stream order and share it
+        # query building runs on the second stream, concurrently with the memory phase: its own workspace
+        self.ws_q = M.alloc_bytes(max(M.workspace_bytes(M.OP_BUILD_QUERIES, d, B, 0), 256), dev)
         self.ap = M.attn_params(self.params, d)
         self.ag = M.attn_grads(self.grads)
-        # second stream (default priority) and fork/join events for the attention
-        # backward's d_mem part; recording the events once makes them exist
-        self.dmem_stream = torch.cuda.Stream(device=dev)
+        # second stream (default priority) and fork/join events for the work that
+        # overlaps the main stream; recording the events once makes them exist
+        self.side_stream = torch.cuda.Stream(device=dev)
         self.fork, self.join = torch.cuda.Event(), torch.cuda.Event()
+        self.q_fork, self.q_join = torch.cuda.Event(), torch.cuda.Event()
         s0 = self.ts if self.ts is not None else torch.cuda.current_stream(dev)
-        self.fork.record(s0)
-        self.join.record(s0)
+        for e in (self.fork, self.join, self.q_fork, self.q_join):
+            e.record(s0)
 
     def _batch(self, lo, hi):
         if hi <= lo:
@@ -119,12 +124,17 @@ class TGNStep:
                            p["b_ih"], p["b_hh"], self.d, self.memory, self.last_update,
                            self.gru_save if save else None, self.ws, stream=s)
 
-    def embed(self, lo, hi):
+    def queries(self, lo, hi, stream):
+        """Queries of the batch's target events and their most-recent-k neighbours (no memory read)."""
         b = self._batch(lo, hi)
-        p, s = self.params, self.ts
-        M.mtgnn_build_queries(b, self.neg[lo:hi], self.q_node, self.q_t, self.n_q, self.ws, stream=s)
+        M.mtgnn_build_queries(b, self.neg[lo:hi], self.q_node, self.q_t, self.n_q, self.ws_q, stream=stream)
         M.mtgnn_sample_recent(self.csr_off, self.csr_nbr, self.csr_t, self.csr_eid, self.w.n_nodes, self.q_node,
-                              self.q_t, self.n_q, self.max_q, self.w.k, self.nbr, self.nt, self.neid, stream=s)
+                              self.q_t, self.n_q, self.max_q, self.w.k, self.nbr, self.nt, self.neid, stream=stream)
+
+    def embed(self, lo, hi, queries_done=False):
+        p, s = self.params, self.ts
+        if not queries_done:
+            self.queries(lo, hi, s)
         M.mtgnn_temporal_attn(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, self.neid, self.memory,
                               self.x, p["time_w"], p["time_b"], self.ap, self.d, self.z, self.attn_save, self.ws,
                               stream=s)
@@ -135,7 +145,7 @@ class TGNStep:
             M.mtgnn_temporal_attn_bwd_overlap(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
                                               self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"],
                                               p["time_b"], self.ap, self.d, self.ag, self.d_mem, g["time_w"],
-                                              g["time_b"], self.ws, self.dmem_stream, self.fork, self.join, stream=s)
+                                              g["time_b"], self.ws, self.side_stream, self.fork, self.join, stream=s)
         else:
             M.mtgnn_temporal_attn_bwd(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
                                       self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],
@@ -157,6 +167,18 @@ class TGNStep:
             mlo, mhi = self.batch_range(b - 1) if b > 0 else (0, 0)
         else:
             mlo, mhi = elo, ehi
-        self.memory_phase(mlo, mhi)
-        self.embed(elo, ehi)
+        if self.overlap:
+            # queries and sampling on the second stream while the memory phase runs here (they
+            # read only the batch and the adjacency); joined before the attention reads memory
+            main = self.ts if self.ts is not None else torch.cuda.current_stream(self.dev)
+            self.q_fork.record(main)
+            self.side_stream.wait_event(self.q_fork)
+            self.queries(elo, ehi, self.side_stream)
+            self.q_join.record(self.side_stream)
+            self.memory_phase(mlo, mhi)
+            main.wait_event(self.q_join)
+            self.embed(elo, ehi, queries_done=True)
+        else:
+            self.memory_phase(mlo, mhi)
+            self.embed(elo, ehi)
         self.backward(dz)
