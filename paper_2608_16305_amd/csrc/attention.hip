@@ -42,6 +42,7 @@ struct AttnSave {
   int32_t *cnt, *pair_off, *n_valid, *pair_nbr;
   float *pair_delta;     // per compact slot: tau - t_j
   float *q_in, *kv_in, *sinv, *qv, *KV, *p, *attn, *m_in, *m1, *a1;
+  float* merge_w;        // zero-padded merge weights and their transposes for the fused chains (float32 only)
   size_t total;
 };
 
@@ -67,6 +68,7 @@ AttnSave carve_save(void* base, const AttnShape& s) {
   v.m_in = (float*)take(sizeof(float) * s.Q * (s.da + s.dm));
   v.m1 = (float*)take(sizeof(float) * s.Q * s.da);
   v.a1 = (float*)take(sizeof(float) * s.Q * s.da);
+  v.merge_w = (float*)take(sizeof(float) * (s.esz == 4 ? merge_weights_floats(s.da, s.dm) : 1));
   v.total = (size_t)(w - (char*)base);
   return v;
 }
@@ -717,6 +719,12 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
   }
   MTGNN_CHECK_LAUNCH("attn_core");
   const int64_t ldm = sh.da + sh.dm;
+  if (merge_fused_ok(d->dtype, sh.da, sh.dm)) {
+    MTGNN_TRY(merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm,
+                            sv.merge_w, s));
+    return merge_fwd_fused(sv.attn, sv.m_in, sv.merge_w, p->b_o, p->b_1, p->b_2, sv.m1, sv.a1, z, n_q, max_q, sh.da,
+                           sh.dm, s);
+  }
   MTGNN_TRY(linear_fwd(sv.attn, MTGNN_F32, sh.da, p->W_o, wt, sh.da, p->b_o, sv.m_in, ldm, sh.Q, n_q, sh.da, sh.da,
                        false, s, nullptr, 0, bf != 0));
   MTGNN_TRY(linear_fwd(sv.m_in, MTGNN_F32, ldm, p->W_1, wt, ldm, p->b_1, sv.a1, sh.da, sh.Q, n_q, sh.da, ldm, false, s,
@@ -849,10 +857,14 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
 
   // merge MLP: z = W_2 a1 + b_2, a1 = relu(m1), m1 = W_1 m_in + b_1
   // (their weight gradients run as one batch after the score backward)
-  MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
-  MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
   // output projection: o = W_o attn + b_o   (do = dm_in[:, :da])
-  MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
+  if (merge_fused_ok(wt, da, dm)) {
+    MTGNN_TRY(merge_bwd_fused(dz, sv.merge_w, sv.m1, b.dm1, b.dm_in, b.dattn, n_q, max_q, da, dm, s));
+  } else {
+    MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
+    MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
+    MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
+  }
   // softmax-weighted sum and scores
   {
     TimedScope ts("k_attn_core_bwd", s);

@@ -1,0 +1,312 @@
+// Fused merge-layer chains of the attention embedding (float32).
+//
+// Forward, per query row (a = attention output, h = M[q], o stored in m_in[:, :da]):
+//   o  = W_o a + b_o;   m1 = W_1 [o || h] + b_1;   a1 = relu(m1);   z = W_2 a1 + b_2
+// Backward, from dz:
+//   dm1 = (W_2^T dz) * [m1 > 0];   dm_in = W_1^T dm1;   dattn = W_o^T dm_in[:, :da]
+//
+// Each chain runs as one kernel instead of three products, every output the
+// backward needs still written to memory.  A block of four waves owns a 16-row
+// tile: the activations sit in LDS, shared by the waves, and each wave computes
+// every fourth 16-column output tile of a layer, with a block barrier between
+// layers.  A layer Y = X B^T (B row-major [N, K]: W for the forward, the
+// transposed copies W^T for the backward) runs as 16-deep k chunks of
+// v_mfma_f32_16x16x4_f32: lane l reads X[l%16][16 c + 4 (l/16) ..] from LDS and
+// B[16 t + l%16][16 c + 4 (l/16) ..] from memory (the weights stay in L2),
+// several chunks of weight fragments in flight ahead of the MFMAs.
+#include <algorithm>
+#include <type_traits>
+
+#include "gemm.h"
+#include "ops.h"
+
+namespace mtgnn {
+
+namespace {
+
+constexpr int XS = 212;   // LDS row stride (floats) of an activation tile: >= 208, XS / 4 odd (conflict-free rows)
+constexpr int MW = 4;     // waves per block; wave w computes the output column tiles w, w + 4, ...
+constexpr int PD = 3;     // weight chunks in flight ahead of the one being multiplied
+
+template <int NCT> struct Tiles { static constexpr int per_wave = (NCT + MW - 1) / MW; };
+
+// acc[u] (16 x 16 output tile t = wave + 4 u) += X[16 rows, 16 KC] B[16 t.., 16 KC]^T.  X: the block's LDS
+// tile (row stride XS, zero beyond the true width).  B: a zero-padded weight copy, 16 MW NU rows by 16 KC
+// columns, so every fragment load is in bounds and unconditional.
+template <int NCT, int KC>
+__device__ __forceinline__ void layer(const float* X, const float* __restrict__ B, f32x4 (&acc)[Tiles<NCT>::per_wave]) {
+  constexpr int NU = Tiles<NCT>::per_wave;
+  constexpr int LDB = 16 * KC;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, fr = lane & 15, fg = lane >> 4;
+#pragma unroll
+  for (int u = 0; u < NU; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const float* Bl = B + (16 * wid + fr) * LDB + 4 * fg;
+  float4 bf[KC][NU];
+  auto load_b = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < NU; ++u) bf[c][u] = *reinterpret_cast<const float4*>(Bl + 16 * MW * u * LDB + 16 * c);
+  };
+#pragma unroll
+  for (int c = 0; c < PD && c < KC; ++c) load_b(c);
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    if (c + PD < KC) load_b(c + PD);   // in flight while this chunk's MFMAs run
+    const float4 a = *reinterpret_cast<const float4*>(X + fr * XS + 16 * c + 4 * fg);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, bf[c][u].x, acc[u], 0, 0, 0);
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, bf[c][u].y, acc[u], 0, 0, 0);
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, bf[c][u].z, acc[u], 0, 0, 0);
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, bf[c][u].w, acc[u], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);   // keeps the prefetch distance as written
+  }
+}
+
+// rows r0 .. r0 + 15 (those < M) of a row-major [M, n] matrix into an LDS tile at column offset col0
+__device__ __forceinline__ void load_rows(float* X, int col0, const float* __restrict__ src, int64_t ld, int n,
+                                          int64_t r0, int64_t M) {
+  const int nq = n / 4;
+  for (int e = threadIdx.x; e < 16 * nq; e += 64 * MW) {
+    const int r = e / nq, q = e % nq;
+    const float4 v = r0 + r < M ? *reinterpret_cast<const float4*>(src + (r0 + r) * ld + 4 * q)
+                                : float4{0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<float4*>(X + r * XS + col0 + 4 * q) = v;
+  }
+}
+
+__device__ __forceinline__ void zero_cols(float* X, int c0, int c1) {
+  for (int e = threadIdx.x; e < 16 * (c1 - c0); e += 64 * MW) X[(e / (c1 - c0)) * XS + c0 + e % (c1 - c0)] = 0.f;
+}
+
+// Epilogue of a layer: f(i, j, row valid, value) for this wave's tiles, row 4 (l/16) + r, column 16 t + l%16
+// (j < N only).  A full 16-row tile takes a path with the row test folded away.
+template <int NCT, class F>
+__device__ __forceinline__ void each_out(const f32x4 (&acc)[Tiles<NCT>::per_wave], int N, int64_t r0, int64_t M,
+                                         F f) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, fr = lane & 15, fg = lane >> 4;
+  auto run = [&](auto full) {
+#pragma unroll
+    for (int u = 0; u < Tiles<NCT>::per_wave; ++u) {
+      const int j = 16 * (wid + MW * u) + fr;
+      if (j >= N) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 4 * fg + r;
+        f(i, j, decltype(full)::value || r0 + i < M, acc[u][r]);
+      }
+    }
+  };
+  if (r0 + 16 <= M)
+    run(std::true_type{});
+  else
+    run(std::false_type{});
+}
+
+// NA = ceil(da / 16), NS = ceil((da + dm) / 16)
+template <int NA, int NS>
+__global__ __launch_bounds__(64 * MW) void k_merge_fwd(const float* __restrict__ attn, float* __restrict__ m_in,
+                                                       const float* __restrict__ Wo, const float* __restrict__ bo,
+                                                       const float* __restrict__ W1, const float* __restrict__ b1,
+                                                       const float* __restrict__ W2, const float* __restrict__ b2,
+                                                       float* __restrict__ m1, float* __restrict__ a1,
+                                                       float* __restrict__ z, const int32_t* __restrict__ n_q,
+                                                       int64_t max_q, int da, int dm) {
+  __shared__ __attribute__((aligned(16))) float X0[16 * XS], X1[16 * XS];
+  const int64_t M = eff_count(max_q, n_q);
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= M) return;   // block-uniform
+  const int ldm = da + dm;
+  zero_cols(X0, da, 16 * NS);
+  zero_cols(X1, ldm, 16 * NS);
+  load_rows(X0, 0, attn, da, da, r0, M);
+  load_rows(X1, da, m_in + da, ldm, dm, r0, M);   // h = M[q], written by the query gather
+  __syncthreads();
+  f32x4 acc[Tiles<NA>::per_wave];
+  // o = W_o a + b_o  -> m_in[:, :da] and X1[:, :da]
+  layer<NA, NA>(X0, Wo, acc);
+  each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+    v += bo[j];
+    if (ok) m_in[(r0 + i) * ldm + j] = v;
+    X1[i * XS + j] = v;
+  });
+  __syncthreads();
+  // m1 = W_1 [o || h] + b_1;  a1 = relu(m1)  -> m1, a1 and X0[:, :da]  (X0 is no longer read)
+  layer<NA, NS>(X1, W1, acc);
+  each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+    v += b1[j];
+    const float r = fmaxf(v, 0.f);
+    if (ok) {
+      m1[(r0 + i) * da + j] = v;
+      a1[(r0 + i) * da + j] = r;
+    }
+    X0[i * XS + j] = r;
+  });
+  __syncthreads();
+  // z = W_2 a1 + b_2
+  layer<NA, NA>(X0, W2, acc);
+  each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+    if (ok) z[(r0 + i) * da + j] = v + b2[j];
+  });
+}
+
+// W2t = W_2^T [da, da], W1t = W_1^T [da + dm, da], Wot = W_o^T [da, da]
+template <int NA, int NS>
+__global__ __launch_bounds__(64 * MW) void k_merge_bwd(const float* __restrict__ dz, const float* __restrict__ W2t,
+                                                       const float* __restrict__ W1t, const float* __restrict__ Wot,
+                                                       const float* __restrict__ m1, float* __restrict__ dm1,
+                                                       float* __restrict__ dm_in, float* __restrict__ dattn,
+                                                       const int32_t* __restrict__ n_q, int64_t max_q, int da,
+                                                       int dm) {
+  __shared__ __attribute__((aligned(16))) float X0[16 * XS], X1[16 * XS];
+  const int64_t M = eff_count(max_q, n_q);
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= M) return;   // block-uniform
+  const int ldm = da + dm;
+  zero_cols(X0, da, 16 * NS);
+  zero_cols(X1, da, 16 * NS);
+  load_rows(X0, 0, dz, da, da, r0, M);
+  __syncthreads();
+  // dm1 = (W_2^T dz) * [m1 > 0]  -> dm1 and X1[:, :da]
+  {
+    f32x4 acc[Tiles<NA>::per_wave];
+    layer<NA, NA>(X0, W2t, acc);
+    each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+      if (ok) {
+        v = m1[(r0 + i) * da + j] > 0.f ? v : 0.f;
+        dm1[(r0 + i) * da + j] = v;
+      } else {
+        v = 0.f;
+      }
+      X1[i * XS + j] = v;
+    });
+  }
+  __syncthreads();
+  // dm_in = W_1^T dm1  -> dm_in [.., da + dm] and X0[:, :da]  (X0 is no longer read)
+  {
+    f32x4 acc[Tiles<NS>::per_wave];
+    layer<NS, NA>(X1, W1t, acc);
+    each_out<NS>(acc, ldm, r0, M, [&](int i, int j, bool ok, float v) {
+      if (ok) dm_in[(r0 + i) * ldm + j] = v;
+      if (j < da) X0[i * XS + j] = v;
+    });
+  }
+  __syncthreads();
+  // dattn = W_o^T dm_in[:, :da]
+  {
+    f32x4 acc[Tiles<NA>::per_wave];
+    layer<NA, NA>(X0, Wot, acc);
+    each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+      if (ok) dattn[(r0 + i) * da + j] = v;
+    });
+  }
+}
+
+// Zero-padded copies of the merge weights: dst[r][c] = W[r][c] (or W[c][r] for a transposed copy) for r < n,
+// c < k, else 0.  blockIdx.y selects the copy.
+struct PrepArgs {
+  const float* src[6];
+  float* dst[6];
+  int rows[6], cols[6], n[6], k[6], ld[6], tr[6];
+};
+
+__global__ void k_merge_prepare(PrepArgs a) {
+  const int m = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)a.rows[m] * a.cols[m]) return;
+  const int r = (int)(e / a.cols[m]), c = (int)(e % a.cols[m]);
+  float v = 0.f;
+  if (r < a.n[m] && c < a.k[m]) v = a.tr[m] ? a.src[m][(int64_t)c * a.ld[m] + r] : a.src[m][(int64_t)r * a.ld[m] + c];
+  a.dst[m][e] = v;
+}
+
+// Layout of the padded copies in one buffer: forward W_o, W_1, W_2, then backward W_2^T, W_1^T, W_o^T.
+struct PackLayout {
+  int rows[6], cols[6];
+  size_t off[7];
+  PackLayout(int da, int dm) {
+    const int na = (int)cdiv(da, 16), ns = (int)cdiv(da + dm, 16);
+    auto R = [](int nct) { return 16 * MW * (int)cdiv(nct, MW); };
+    const int r[6] = {R(na), R(na), R(na), R(na), R(ns), R(na)};
+    const int c[6] = {16 * na, 16 * ns, 16 * na, 16 * na, 16 * na, 16 * na};
+    off[0] = 0;
+    for (int m = 0; m < 6; ++m) {
+      rows[m] = r[m];
+      cols[m] = c[m];
+      off[m + 1] = off[m] + (size_t)r[m] * c[m];
+    }
+  }
+};
+
+bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
+
+}  // namespace
+
+bool merge_fused_ok(int dtype, int da, int dm) {
+  const int na = (int)cdiv(da, 16), ns = (int)cdiv(da + dm, 16);
+  return dtype == MTGNN_F32 && da % 4 == 0 && dm % 4 == 0 && ((na == 7 && ns == 13) || (na == 2 && ns == 4));
+}
+
+size_t merge_weights_floats(int da, int dm) { return PackLayout(da, dm).off[6]; }
+
+mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
+                           hipStream_t s) {
+  const PackLayout L(da, dm);
+  const int ldm = da + dm;
+  PrepArgs a;
+  const float* src[6] = {Wo, W1, W2, W2, W1, Wo};
+  const int n[6] = {da, da, da, da, ldm, da}, k[6] = {da, ldm, da, da, da, da};
+  const int ld[6] = {da, ldm, da, da, ldm, da}, tr[6] = {0, 0, 0, 1, 1, 1};
+  int64_t most = 0;
+  for (int m = 0; m < 6; ++m) {
+    a.src[m] = src[m];
+    a.dst[m] = Wp + L.off[m];
+    a.rows[m] = L.rows[m];
+    a.cols[m] = L.cols[m];
+    a.n[m] = n[m];
+    a.k[m] = k[m];
+    a.ld[m] = ld[m];
+    a.tr[m] = tr[m];
+    most = std::max<int64_t>(most, (int64_t)L.rows[m] * L.cols[m]);
+  }
+  k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), 6), 256, 0, s>>>(a);
+  MTGNN_CHECK_LAUNCH("merge_prepare");
+  return MTGNN_OK;
+}
+
+mtgnn_status merge_fwd_fused(const float* attn, float* m_in, const float* Wp, const float* bo, const float* b1,
+                             const float* b2, float* m1, float* a1, float* z, const int32_t* n_q, int64_t max_q,
+                             int da, int dm, hipStream_t s) {
+  if (max_q <= 0) return MTGNN_OK;
+  if (!aligned16(attn) || !aligned16(m_in) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
+  const PackLayout L(da, dm);
+  const unsigned grid = (unsigned)cdiv(max_q, 16);
+  TimedScope ts("merge_fwd", s);
+  if (cdiv(da, 16) == 7)
+    k_merge_fwd<7, 13><<<grid, 64 * MW, 0, s>>>(attn, m_in, Wp + L.off[0], bo, Wp + L.off[1], b1, Wp + L.off[2], b2,
+                                                m1, a1, z, n_q, max_q, da, dm);
+  else
+    k_merge_fwd<2, 4><<<grid, 64 * MW, 0, s>>>(attn, m_in, Wp + L.off[0], bo, Wp + L.off[1], b1, Wp + L.off[2], b2,
+                                               m1, a1, z, n_q, max_q, da, dm);
+  MTGNN_CHECK_LAUNCH("merge_fwd");
+  return MTGNN_OK;
+}
+
+mtgnn_status merge_bwd_fused(const float* dz, const float* Wp, const float* m1, float* dm1, float* dm_in,
+                             float* dattn, const int32_t* n_q, int64_t max_q, int da, int dm, hipStream_t s) {
+  if (max_q <= 0) return MTGNN_OK;
+  if (!aligned16(dz) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
+  const PackLayout L(da, dm);
+  const unsigned grid = (unsigned)cdiv(max_q, 16);
+  TimedScope ts("merge_bwd", s);
+  if (cdiv(da, 16) == 7)
+    k_merge_bwd<7, 13><<<grid, 64 * MW, 0, s>>>(dz, Wp + L.off[3], Wp + L.off[4], Wp + L.off[5], m1, dm1, dm_in,
+                                                dattn, n_q, max_q, da, dm);
+  else
+    k_merge_bwd<2, 4><<<grid, 64 * MW, 0, s>>>(dz, Wp + L.off[3], Wp + L.off[4], Wp + L.off[5], m1, dm1, dm_in,
+                                               dattn, n_q, max_q, da, dm);
+  MTGNN_CHECK_LAUNCH("merge_bwd");
+  return MTGNN_OK;
+}
+
+}  // namespace mtgnn

@@ -55,6 +55,17 @@ mtgnn_status build_csr_impl(const int32_t* src, const int32_t* dst, const float*
                             hipStream_t s);
 
 // attention
+// Fused merge-layer chains (merge.hip): float32 and the attention / memory widths they are built for.
+bool merge_fused_ok(int dtype, int da, int dm);
+size_t merge_weights_floats(int da, int dm);
+mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
+                           hipStream_t s);
+mtgnn_status merge_fwd_fused(const float* attn, float* m_in, const float* Wp, const float* bo, const float* b1,
+                             const float* b2, float* m1, float* a1, float* z, const int32_t* n_q, int64_t max_q,
+                             int da, int dm, hipStream_t s);
+mtgnn_status merge_bwd_fused(const float* dz, const float* Wp, const float* m1, float* dm1, float* dm_in,
+                             float* dattn, const int32_t* n_q, int64_t max_q, int da, int dm, hipStream_t s);
+
 size_t attn_save_bytes(const mtgnn_dims* d, int64_t max_q);
 size_t attn_fwd_ws(const mtgnn_dims* d, int64_t max_q);
 mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
