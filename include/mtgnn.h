@@ -239,10 +239,12 @@ mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, co
  * concurrently with the parameter gradients, which stay on `stream`.
  *   dmem_stream -- a second stream of the caller, at the default priority;
  *   fork, join  -- two events of the caller (timing may be disabled).
- * The call records `fork` on `stream` once the inputs of the d_mem part are
- * ready, makes dmem_stream wait for it, enqueues the d_mem part there, records
- * `join` on dmem_stream and makes `stream` wait for `join`: work enqueued on
- * `stream` afterwards is ordered after both parts, as with
+ * The call records `fork` on `stream` at entry and makes dmem_stream wait for
+ * it (the grouping's key sort, which reads only forward outputs, starts there
+ * while the data gradients run on `stream`), records `fork` again once the
+ * gradients the sums need are ready and makes dmem_stream wait for it (the
+ * sums), records `join` on dmem_stream and makes `stream` wait for `join`:
+ * work enqueued on `stream` afterwards is ordered after both parts, as with
  * mtgnn_temporal_attn_bwd.  Results are bitwise identical to it.  The two
  * parts use disjoint regions of ws (the same size as for
  * mtgnn_temporal_attn_bwd).  Errors: as mtgnn_temporal_attn_bwd; EINVAL if

@@ -28,7 +28,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-u
 # Kernels that read LDS filled by direct global-to-LDS loads through inline
 # assembly must not spill: a spill could copy a register before its LDS data
 # has arrived.  The build fails if one of them does.
-NO_SPILL = ("k_gemm_rs", "k_dw_rs")
+NO_SPILL = ("k_gemm_rs", "k_dw_rs", "k_dw_os")
 
 
 def _spilling_kernels(remarks: str) -> list:

@@ -743,29 +743,40 @@ namespace {
 // d M' for the updated rows (reads dh_q in dm_in[:, da:], dK|dV, the slot nodes and
 // [W_k; W_v]; writes d_mem).  Its workspace regions (keys, vals, segment bounds, row
 // map, S, tile partials, sort scratch) are disjoint from the parameter part's.
-mtgnn_status attn_bwd_dmem(const int32_t* q_node, const int32_t* n_q, int64_t max_q, const AttnShape& sh,
-                           const AttnSave& sv, const BwdWs& b, const int32_t* uniq, const int32_t* n_rows,
-                           int64_t max_rows, int wt, float* d_mem, hipStream_t s) {
+// d M' grouping, first half: every occurrence (query rows, then compact neighbour slots) keyed by
+// the updated row of its node (or the sentinel max_rows), sorted stably by key, and each row's
+// segment bounds.  Reads only forward outputs and the updated-row list, so it may run before
+// any gradient exists.  *skeys / *svals: the buffers holding the sorted pairs.
+mtgnn_status attn_bwd_dmem_group(const int32_t* q_node, const int32_t* n_q, int64_t max_q, const AttnShape& sh,
+                                 const AttnSave& sv, const BwdWs& b, const int32_t* uniq, const int32_t* n_rows,
+                                 int64_t max_rows, uint32_t** skeys, uint32_t** svals, hipStream_t s) {
+  const int64_t n_occ = sh.Q + sh.P;
+  const uint32_t sentinel = (uint32_t)max_rows;
+  k_row_map<<<(unsigned)cdiv(max_rows, 256), 256, 0, s>>>(uniq, n_rows, max_rows, b.row_of, b.seg_lo, b.seg_hi);
+  MTGNN_CHECK_LAUNCH("row_map");
+  k_occ_keys<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(q_node, sv.pair_nbr, n_q, max_q, sv.n_valid, sh.P, uniq,
+                                                         n_rows, max_rows, b.row_of, sentinel, b.keys, b.vals);
+  MTGNN_CHECK_LAUNCH("occ_keys");
+  *skeys = b.keys;
+  *svals = b.vals;
+  MTGNN_TRY(radix_sort_pairs(skeys, svals, n_occ, bits_for(max_rows), b.sort_scratch, b.sort_scratch_bytes, s));
+  k_seg_bounds<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(*skeys, n_occ, sentinel, b.seg_lo, b.seg_hi);
+  MTGNN_CHECK_LAUNCH("seg_bounds");
+  return MTGNN_OK;
+}
+
+// d M' grouping, second half: per-row sums of [dh_q | dK | dV] over the sorted occurrences, in a
+// fixed order, then d M' = (sum of dh_q) + (sum of dK|dV) W_kv[:, :dm].
+mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSave& sv, const BwdWs& b,
+                               const uint32_t* skeys, const uint32_t* svals, const int32_t* n_rows, int64_t max_rows,
+                               int wt, float* d_mem, hipStream_t s) {
   const int64_t Q = sh.Q, P = sh.P, ldm = sh.da + sh.dm;
   const int da = sh.da, dm = sh.dm;
-  char* sc = b.sort_scratch;
-  const size_t scb = b.sort_scratch_bytes;
-  // group every occurrence by row, sum in a fixed order
-  if (max_rows > 0) {
+  {
     const int64_t n_occ = Q + P;
     const uint32_t sentinel = (uint32_t)max_rows;
-    k_row_map<<<(unsigned)cdiv(max_rows, 256), 256, 0, s>>>(uniq, n_rows, max_rows, b.row_of, b.seg_lo, b.seg_hi);
-    MTGNN_CHECK_LAUNCH("row_map");
-    k_occ_keys<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(q_node, sv.pair_nbr, n_q, max_q, sv.n_valid, P, uniq,
-                                                           n_rows, max_rows, b.row_of, sentinel, b.keys, b.vals);
-    MTGNN_CHECK_LAUNCH("occ_keys");
-    uint32_t* skeys = b.keys;
-    uint32_t* svals = b.vals;
-    MTGNN_TRY(radix_sort_pairs(&skeys, &svals, n_occ, bits_for(max_rows), sc, scb, s));
-    k_seg_bounds<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(skeys, n_occ, sentinel, b.seg_lo, b.seg_hi);
-    MTGNN_CHECK_LAUNCH("seg_bounds");
     SegCtx c;
-    c.keys = skeys; c.vals = svals; c.n_occ = n_occ; c.sentinel = sentinel; c.max_q = max_q;
+    c.keys = (uint32_t*)skeys; c.vals = (uint32_t*)svals; c.n_occ = n_occ; c.sentinel = sentinel; c.max_q = max_q;
     c.seg_lo = b.seg_lo; c.seg_hi = b.seg_hi;
     c.dhq = b.dm_in + da; c.ldq = ldm; c.dkv = b.dKV; c.dm = dm; c.w2 = 2 * da;
     c.S = b.S; c.head = b.head; c.tail = b.tail;
@@ -855,38 +866,67 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   const int64_t Q = sh.Q, ldm = sh.da + sh.dm;
   const int da = sh.da, dm = sh.dm;
 
-  // merge MLP: z = W_2 a1 + b_2, a1 = relu(m1), m1 = W_1 m_in + b_1
-  // (their weight gradients run as one batch after the score backward)
-  // output projection: o = W_o attn + b_o   (do = dm_in[:, :da])
-  if (merge_fused_ok(wt, da, dm)) {
-    MTGNN_TRY(merge_bwd_fused(dz, sv.merge_w, sv.m1, b.dm1, b.dm_in, b.dattn, n_q, max_q, da, dm, s));
-  } else {
-    MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
-    MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
-    MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
+  // With a second stream, the d M' grouping's key sort starts there at once (it reads only forward
+  // outputs): first fork.  The same event marks the second fork below.
+  const bool overlap = s_dmem != nullptr && max_rows > 0;
+  uint32_t *skeys = nullptr, *svals = nullptr;
+  if (overlap) {
+    hipError_t e0 = hipEventRecord(fork, s);
+    if (e0 == hipSuccess) e0 = hipStreamWaitEvent(s_dmem, fork, 0);
+    if (e0 != hipSuccess) {
+      set_hip_error(e0, "attn_bwd fork");
+      return MTGNN_EHIP;
+    }
+    const mtgnn_status st0 =
+        attn_bwd_dmem_group(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, &skeys, &svals, s_dmem);
+    if (st0 != MTGNN_OK) {   // leave `stream` ordered after the second stream
+      if (hipEventRecord(join, s_dmem) == hipSuccess) (void)hipStreamWaitEvent(s, join, 0);
+      return st0;
+    }
   }
-  // softmax-weighted sum and scores
-  {
-    TimedScope ts("k_attn_core_bwd", s);
-    k_attn_core_bwd<<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q, max_q,
-                                                          sh.k, da, sh.H, b.dKV, b.dqv);
+  // data gradients down to dK|dV and dh_q, on `stream`
+  auto chain = [&]() -> mtgnn_status {
+    // merge MLP: z = W_2 a1 + b_2, a1 = relu(m1), m1 = W_1 m_in + b_1
+    // (their weight gradients run as one batch after the score backward)
+    // output projection: o = W_o attn + b_o   (do = dm_in[:, :da])
+    if (merge_fused_ok(wt, da, dm)) {
+      MTGNN_TRY(merge_bwd_fused(dz, sv.merge_w, sv.m1, b.dm1, b.dm_in, b.dattn, n_q, max_q, da, dm, s));
+    } else {
+      MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
+      MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
+      MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
+    }
+    // softmax-weighted sum and scores
+    {
+      TimedScope ts("k_attn_core_bwd", s);
+      k_attn_core_bwd<<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q,
+                                                            max_q, sh.k, da, sh.H, b.dKV, b.dqv);
+    }
+    MTGNN_CHECK_LAUNCH("attn_core_bwd");
+    // query projection, data gradient: dhq += dqv W_q[:, :dm] (the last input of the d M' grouping)
+    MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
+    return MTGNN_OK;
+  };
+  if (const mtgnn_status st1 = chain(); st1 != MTGNN_OK) {
+    if (overlap && hipEventRecord(join, s_dmem) == hipSuccess) (void)hipStreamWaitEvent(s, join, 0);
+    return st1;
   }
-  MTGNN_CHECK_LAUNCH("attn_core_bwd");
-  // query projection, data gradient: dhq += dqv W_q[:, :dm] (the last input of the d M' grouping)
-  MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
-  if (s_dmem == nullptr || max_rows <= 0) {
+  if (!overlap) {
     MTGNN_TRY(attn_bwd_params(n_q, sh, sv, b, dz, tw, tb, p, wt, g, d_time_w, d_time_b, s));
-    if (max_rows > 0) MTGNN_TRY(attn_bwd_dmem(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, wt, d_mem, s));
+    if (max_rows > 0) {
+      MTGNN_TRY(attn_bwd_dmem_group(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, &skeys, &svals, s));
+      MTGNN_TRY(attn_bwd_dmem_sum(max_q, sh, sv, b, skeys, svals, n_rows, max_rows, wt, d_mem, s));
+    }
     return MTGNN_OK;
   }
-  // fork: d M' on the second stream, the parameter gradients here; join before returning
+  // second fork: the sums of d M' on the second stream, the parameter gradients here; join before returning
   hipError_t e = hipEventRecord(fork, s);
   if (e == hipSuccess) e = hipStreamWaitEvent(s_dmem, fork, 0);
   if (e != hipSuccess) {
     set_hip_error(e, "attn_bwd fork");
     return MTGNN_EHIP;
   }
-  MTGNN_TRY(attn_bwd_dmem(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, wt, d_mem, s_dmem));
+  MTGNN_TRY(attn_bwd_dmem_sum(max_q, sh, sv, b, skeys, svals, n_rows, max_rows, wt, d_mem, s_dmem));
   e = hipEventRecord(join, s_dmem);
   if (e != hipSuccess) {
     set_hip_error(e, "attn_bwd join");

@@ -872,6 +872,27 @@ struct DwProblem {
   float* db;
 };
 size_t linear_dw_batch_ws_bytes(int64_t R, const int64_t* N, const int64_t* K, int n);   // sizes only
+
+// Batched output-stationary weight gradients (gemm_rs.h), for float32 outputs of at
+// most 7 x 13 16 x 16 tiles: part_p[block][nx_p][ny_p + 1] = X_p^T [Y_p | 1] over the
+// blocks' 16-row chunks.  Problem p owns blocks b_begin .. b_begin + nblk - 1.
+struct DwOsProblem {
+  const float* X;
+  int64_t ldx;
+  const float* Y;
+  int64_t ldy;
+  float* part;
+  int nx, ny, b_begin, nblk;
+};
+struct DwOsBatch {
+  DwOsProblem p[G_MAXBATCH];
+  int n;
+  int64_t R;
+  const int32_t* R_dev;
+};
+constexpr int DW_OS_MAX_BLOCKS = 256;
+mtgnn_status dw_os_launch(const DwOsBatch& b, int grid, hipStream_t s);
+int dw_os_cu_count();
 mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_t* R_dev, int x_dtype, void* ws,
                              size_t ws_bytes, hipStream_t s);
 

@@ -142,11 +142,46 @@ DwPlan dw_batch_plan(int64_t R, const int64_t* N, const int64_t* K, int n) {
 }
 }  // namespace
 
+namespace {
+
+// Output-stationary batch (k_dw_os): every output at most 112 x 208 with its bias column, both
+// operands at least 4 wide (every DMA instruction of a chunk has an active lane: the waits count them).
+bool dw_os_shapes_ok(const int64_t* N, const int64_t* K, int n) {
+  for (int i = 0; i < n; ++i)
+    if (N[i] < 4 || N[i] > 112 || N[i] % 4 != 0 || K[i] < 4 || K[i] % 4 != 0 || K[i] + 1 > 208) return false;
+  return true;
+}
+
+// Blocks per problem out of `total`, in proportion to the MFMAs per chunk (7 x 2 or 7 x 4 tiles a wave).
+void dw_os_split(const int64_t* K, int n, int total, int* nblk) {
+  int w[G_MAXBATCH], sum = 0;
+  for (int i = 0; i < n; ++i) sum += (w[i] = cdiv(K[i] + 1, 16) <= 7 ? 2 : 4);
+  int used = 0;
+  for (int i = 0; i < n; ++i) {
+    nblk[i] = (int)((int64_t)total * w[i] / sum);
+    if (nblk[i] < 1) nblk[i] = 1;
+    used += nblk[i];
+  }
+  for (int i = 0; used > total && i < n; ++i)   // only when rounding up single blocks overshot
+    while (nblk[i] > 1 && used > total) --nblk[i], --used;
+}
+
+size_t dw_os_ws(const int64_t* N, const int64_t* K, int n, int total) {
+  int nblk[G_MAXBATCH];
+  dw_os_split(K, n, total, nblk);
+  size_t b = 0;
+  for (int i = 0; i < n; ++i) b += (sizeof(float) * (size_t)nblk[i] * N[i] * (K[i] + 1) + 255) & ~size_t(255);
+  return b;
+}
+
+}  // namespace
+
 size_t linear_dw_batch_ws_bytes(int64_t R, const int64_t* N, const int64_t* K, int n) {
   const DwPlan p = dw_batch_plan(R, N, K, n);
-  if (p.ksplit <= 1) return 0;
   size_t b = 0;
-  for (int i = 0; i < n; ++i) b += (sizeof(float) * (size_t)p.ksplit * N[i] * (K[i] + 1) + 255) & ~size_t(255);
+  if (p.ksplit > 1)
+    for (int i = 0; i < n; ++i) b += (sizeof(float) * (size_t)p.ksplit * N[i] * (K[i] + 1) + 255) & ~size_t(255);
+  if (dw_os_shapes_ok(N, K, n)) b = std::max(b, dw_os_ws(N, K, n, DW_OS_MAX_BLOCKS));
   return b;
 }
 
@@ -158,8 +193,38 @@ mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_
     Ns[i] = ps[i].N;
     Ks[i] = ps[i].K;
   }
-  const DwPlan plan = dw_batch_plan(R, Ns, Ks, n);
   if (ws_bytes < linear_dw_batch_ws_bytes(R, Ns, Ks, n)) return MTGNN_EWORKSPACE;
+  bool os = x_dtype == MTGNN_F32 && dw_os_shapes_ok(Ns, Ks, n) && dw_os_cu_count() > 0;
+  for (int i = 0; i < n && os; ++i)
+    os = ps[i].db != nullptr && vec_ok(ps[i].dy, ps[i].lddy, sizeof(float)) &&
+         vec_ok(ps[i].x, ps[i].ldx, sizeof(float));
+  if (os) {   // one block per CU, blocks split over the problems; fixed-order reduce of the partials
+    const int total = std::min(dw_os_cu_count(), DW_OS_MAX_BLOCKS);
+    int nblk[G_MAXBATCH];
+    dw_os_split(Ks, n, total, nblk);
+    DwOsBatch b{};
+    ReduceBatch rb{};
+    b.n = rb.n = n;
+    b.R = R < 0 ? 0 : R;
+    b.R_dev = R_dev;
+    char* w = (char*)ws;
+    int64_t max_out = 1, begin = 0;
+    for (int i = 0; i < n; ++i) {
+      const DwProblem& q = ps[i];
+      const int64_t per = q.N * (q.K + 1);
+      b.p[i] = DwOsProblem{q.dy, q.lddy, (const float*)q.x, q.ldx, (float*)w, (int)q.N, (int)q.K, (int)begin,
+                           nblk[i]};
+      rb.p[i] = ReduceProblem{(const float*)w, per, nblk[i], q.N, q.K + 1, q.dW, q.lddw, q.K, q.db};
+      w += (sizeof(float) * (size_t)nblk[i] * per + 255) & ~size_t(255);
+      begin += nblk[i];
+      max_out = std::max(max_out, per);
+    }
+    MTGNN_TRY(dw_os_launch(b, (int)begin, s));
+    k_splitk_reduce_batch<<<dim3((unsigned)cdiv(max_out, 64), (unsigned)n), 256, 0, s>>>(rb);
+    MTGNN_CHECK_LAUNCH("splitk_reduce_batch");
+    return MTGNN_OK;
+  }
+  const DwPlan plan = dw_batch_plan(R, Ns, Ks, n);
   GemmArgs gs[G_MAXBATCH];
   ReduceBatch rb{};
   rb.n = n;

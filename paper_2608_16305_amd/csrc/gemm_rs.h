@@ -303,19 +303,6 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict_
   const int fr = lane & 15, fg = lane >> 4;
   const uint32_t base = (uint32_t)(uintptr_t)(lds_void_ptr)lds;
 
-  // constant columns of both slots: X columns nx .. 16 NI and Y columns ny .. 16 NJ are
-  // zero, except Y column ny (the all-ones column)
-  for (int e = tid; e < 2 * 16 * (SX + SY); e += G_THREADS) {
-    const int slot = e / (16 * (SX + SY)), rem = e % (16 * (SX + SY));
-    const bool isx = rem < 16 * SX;
-    const int col = isx ? rem % SX : (rem - 16 * SX) % SY;
-    const int lim = isx ? nx : ny;
-    if (col >= lim) {
-      const float v = (!isx && col == ny) ? 1.f : 0.f;
-      asm volatile("ds_write_b32 %0, %1" ::"v"(base + (uint32_t)(slot * SLOT + rem) * 4u), "v"(v) : "memory");
-    }
-  }
-
   // DMA of one chunk: this wave's rows 4 wid .. 4 wid + 3 of X and of Y; rows past
   // the row count are zero-filled instead
   auto issue = [&](int64_t chunk, int slot) {
@@ -345,6 +332,18 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict_
 
   const int64_t nmine = b0 < nchunks ? cdiv(nchunks - b0, G) : 0;
   if (nmine > 0) issue(b0, 0);
+  // padding columns of both slots, while the first chunk loads (the loads fill columns < nx, < ny):
+  // X columns nx .. 16 NI and Y columns ny .. 16 NJ are zero except Y column ny, the all-ones column
+  {
+    const int cx = 16 * NI - nx, cw = cx + 16 * NJ - ny;
+    for (int e = tid; e < 2 * 16 * cw; e += G_THREADS) {
+      const int slot = e / (16 * cw), rem = e % (16 * cw), r = rem / cw, c = rem % cw;
+      const uint32_t off = c < cx ? (uint32_t)(slot * SLOT + r * SX + nx + c)
+                                  : (uint32_t)(slot * SLOT + 16 * SX + r * SY + ny + (c - cx));
+      const float v = c == cx ? 1.f : 0.f;
+      asm volatile("ds_write_b32 %0, %1" ::"v"(base + off * 4u), "v"(v) : "memory");
+    }
+  }
   // fragment addresses within a slot: X column 16 I + fr, Y column 16 J + fr, row 4 s + fg
   const uint32_t xa = (uint32_t)(fg * SX + 16 * RW * wid + fr) * 4u;
   const uint32_t xl = (uint32_t)(fg * SX + 16 * (NI - 1) + fr) * 4u;
@@ -419,6 +418,159 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict_
 #pragma unroll
   for (int e = 0; e < EX; ++e)
     if (wid + 4 * e < NJ) store(NI - 1, wid + 4 * e, acx[e]);
+}
+
+// Batched output-stationary weight gradients for small outputs (nx <= 16 NI, ny + 1 <= 16 NJ),
+// the chunk layout of k_dw_rs: each wave owns the tile columns J = wid, wid + 4, ... over all NI
+// tile rows (a column past the last one is computed on a clamped copy and not stored).
+// DW_OS_SLOTS LDS slots keep DW_OS_SLOTS - 1 chunks in flight.  Every full chunk is 8 DMA
+// instructions per wave (4 rows of X and of Y), so the wait for the oldest one is vmcnt(8 n)
+// with n full chunks issued after it; a partial chunk (the stream's last) is waited for with
+// the chunks before it.
+constexpr int DW_OS_SLOTS = 2;
+
+template <int N>
+__device__ __forceinline__ void wait_vm_chunks(int n) {   // vmcnt(8 n'), n' = min(n, N) (wave-uniform n)
+  if constexpr (N > 0) {
+    if (n >= N) {
+      dma::wait_vm<8 * N>();
+      return;
+    }
+    wait_vm_chunks<N - 1>(n);
+  } else {
+    dma::wait_vm<0>();
+  }
+}
+
+template <int NI, int NJ>
+__device__ __forceinline__ void dw_os_body(const DwOsProblem& q, int64_t rows, int64_t bi, float* lds) {
+  constexpr int EJ = (NJ + 3) / 4;
+  constexpr int SX = rs::dw_stride(NI), SY = rs::dw_stride(NJ);
+  constexpr int SLOT = 16 * (SX + SY);
+  const int nx = q.nx, ny = q.ny;
+  const int64_t nchunks = cdiv(rows, 16), G = q.nblk;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int fr = lane & 15, fg = lane >> 4;
+  const uint32_t base = (uint32_t)(uintptr_t)(lds_void_ptr)lds;
+  const float* X = q.X;
+  const float* Y = q.Y;
+
+  auto issue = [&](int64_t chunk, int slot) {
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int r = 4 * wid + rr;
+      const int64_t gr = chunk * 16 + r;
+      const uint32_t dx = base + (uint32_t)(slot * SLOT + r * SX) * 4u;
+      const uint32_t dy = base + (uint32_t)(slot * SLOT + 16 * SX + r * SY) * 4u;
+      if (gr < rows) {
+        if (4 * lane < nx) dma::load16(X + gr * q.ldx + 4 * lane, dx);
+        if (4 * lane < ny) dma::load16(Y + gr * q.ldy + 4 * lane, dy);
+      } else {
+        if (4 * lane < nx) dma::ds_zero4(dx + 16u * lane);
+        if (4 * lane < ny) dma::ds_zero4(dy + 16u * lane);
+      }
+    }
+  };
+
+  f32x4 acc[NI][EJ];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int e = 0; e < EJ; ++e) acc[i][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int64_t nmine = bi < nchunks ? cdiv(nchunks - bi, G) : 0;
+  for (int c = 0; c < DW_OS_SLOTS - 1 && c < nmine; ++c) issue(bi + c * G, c);
+  // padding columns of every slot, while the first chunks load (the loads fill columns < nx, < ny):
+  // X columns nx .. 16 NI and Y columns ny .. 16 NJ are zero except Y column ny, the all-ones column
+  {
+    const int cx = 16 * NI - nx, cw = cx + 16 * NJ - ny;
+    for (int e = tid; e < DW_OS_SLOTS * 16 * cw; e += G_THREADS) {
+      const int slot = e / (16 * cw), rem = e % (16 * cw), r = rem / cw, c = rem % cw;
+      const uint32_t off = c < cx ? (uint32_t)(slot * SLOT + r * SX + nx + c)
+                                  : (uint32_t)(slot * SLOT + 16 * SX + r * SY + ny + (c - cx));
+      const float v = c == cx ? 1.f : 0.f;
+      asm volatile("ds_write_b32 %0, %1" ::"v"(base + off * 4u), "v"(v) : "memory");
+    }
+  }
+  const uint32_t xa = (uint32_t)(fg * SX + fr) * 4u;
+  const uint32_t ya = (uint32_t)(16 * SX + fg * SY + fr) * 4u;
+  uint32_t yoff[EJ];
+#pragma unroll
+  for (int e = 0; e < EJ; ++e) {   // branch-free: a tile past the last column reads the last one
+    const int J = wid + 4 * e < NJ ? wid + 4 * e : NJ - 1;
+    yoff[e] = ya + 64u * (uint32_t)J;
+  }
+  auto read1 = [&](uint32_t addr) {
+    float v;
+    asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+  };
+  for (int64_t it = 0; it < nmine; ++it) {
+    const int slot = (int)(it % DW_OS_SLOTS);
+    // chunks issued after `it`: it + 1 .. last; the stream's partial last chunk counts as not full
+    const int64_t last = it + DW_OS_SLOTS - 2 < nmine - 1 ? it + DW_OS_SLOTS - 2 : nmine - 1;
+    const int after = (int)(last - it) - ((bi + last * G + 1) * 16 > rows && last > it ? 1 : 0);
+    wait_vm_chunks<DW_OS_SLOTS - 2>(after);
+    dma::wait_lgkm0();
+    dma::barrier();   // chunk `it` is in LDS; every wave is done with chunk it - 1's slot
+    if (it + DW_OS_SLOTS - 1 < nmine)
+      issue(bi + (it + DW_OS_SLOTS - 1) * G, (int)((it + DW_OS_SLOTS - 1) % DW_OS_SLOTS));
+    const uint32_t sb = base + (uint32_t)(slot * SLOT) * 4u;
+    float fx[4][NI], fy[4][EJ];
+    auto read_frags = [&](int s) {
+      const uint32_t rx = sb + (uint32_t)(4 * s * SX) * 4u, ry = sb + (uint32_t)(4 * s * SY) * 4u;
+#pragma unroll
+      for (int i = 0; i < NI; ++i) fx[s][i] = read1(rx + xa + 64u * i);
+#pragma unroll
+      for (int e = 0; e < EJ; ++e) fy[s][e] = read1(ry + yoff[e]);
+    };
+    read_frags(0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      dma::wait_lgkm0();
+      if (s + 1 < 4) read_frags(s + 1);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) asm volatile("" : "+v"(fx[s][i]));
+#pragma unroll
+      for (int e = 0; e < EJ; ++e) asm volatile("" : "+v"(fy[s][e]));
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int e = 0; e < EJ; ++e)
+          acc[i][e] = __builtin_amdgcn_mfma_f32_16x16x4f32(fx[s][i], fy[s][e], acc[i][e], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  const int64_t ldp = ny + 1;
+  float* out = q.part + bi * (int64_t)nx * ldp;
+#pragma unroll
+  for (int e = 0; e < EJ; ++e) {
+    const int col = 16 * (wid + 4 * e) + fr;
+    if (wid + 4 * e >= NJ || col > ny) continue;
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * i + 4 * fg + r;
+        if (row < nx) out[(int64_t)row * ldp + col] = acc[i][e][r];
+      }
+  }
+}
+
+// One launch for the whole batch: block b works for the problem whose block range holds b.
+__global__ __launch_bounds__(G_THREADS, 1) void k_dw_os(DwOsBatch b) {
+  constexpr int SLOT_MAX = 16 * (rs::dw_stride(7) + rs::dw_stride(13));
+  __shared__ __attribute__((aligned(16))) float lds[DW_OS_SLOTS * SLOT_MAX];
+  const int bx = blockIdx.x;
+  const DwOsProblem q = (b.n > 3 && bx >= b.p[3].b_begin)   ? b.p[3]
+                        : (b.n > 2 && bx >= b.p[2].b_begin) ? b.p[2]
+                        : (b.n > 1 && bx >= b.p[1].b_begin) ? b.p[1]
+                                                            : b.p[0];
+  const int64_t rows = eff_count(b.R, b.R_dev);
+  if (q.ny + 1 <= 16 * 7) dw_os_body<7, 7>(q, rows, bx - q.b_begin, lds);
+  else dw_os_body<7, 13>(q, rows, bx - q.b_begin, lds);
 }
 
 // Host side (gemm_rs.hip): dW[nx, ny] = X^T Y and db[nx] = column sums of X over R rows

@@ -75,4 +75,15 @@ mtgnn_status dw_rs_launch(const float* X, int64_t ldx, int nx, const float* Y, i
   return MTGNN_OK;
 }
 
+int dw_os_cu_count() { return cu_count(); }
+
+mtgnn_status dw_os_launch(const DwOsBatch& b, int grid, hipStream_t s) {
+  {
+    TimedScope ts("dw_os", s);
+    k_dw_os<<<(unsigned)grid, G_THREADS, 0, s>>>(b);
+  }
+  MTGNN_CHECK_LAUNCH("dw_os");
+  return MTGNN_OK;
+}
+
 }  // namespace mtgnn
