@@ -8,7 +8,8 @@ all enqueued on one HIP stream with no host synchronisation (the only
 data-dependent sizes, updated rows and queries, stay in device memory), except
 that with overlap=True (the default) two pieces run on a second stream, forked
 and joined with events: the queries and their sampling, during the memory
-phase, and the attention backward's d_mem part.  Results are bitwise those of
+phase, and the attention backward's d_mem part followed by the GRU backward,
+during the attention parameter gradients.  Results are bitwise those of
 overlap=False.
 """
 
@@ -94,8 +95,10 @@ class TGNStep:
                (M.OP_BUILD_MESSAGES_BWD, R, 0)]
         need = max(M.workspace_bytes(op, d, r, q) for op, r, q in ops)
         self.ws = M.alloc_bytes(need, dev)   # the calls of one step run in stream order and share it
-        # query building runs on the second stream, concurrently with the memory phase: its own workspace
-        self.ws_q = M.alloc_bytes(max(M.workspace_bytes(M.OP_BUILD_QUERIES, d, B, 0), 256), dev)
+        # work on the second stream (query building during the memory phase, the GRU backward during the
+        # attention backward's parameter gradients) has its own workspace
+        self.ws_q = M.alloc_bytes(max(M.workspace_bytes(M.OP_BUILD_QUERIES, d, B, 0),
+                                      M.workspace_bytes(M.OP_GRU_UPDATE_BWD, d, R, 0), 256), dev)
         self.ap = M.attn_params(self.params, d)
         self.ag = M.attn_grads(self.grads)
         # second stream (default priority) and fork/join events for the work that
@@ -103,8 +106,9 @@ class TGNStep:
         self.side_stream = torch.cuda.Stream(device=dev)
         self.fork, self.join = torch.cuda.Event(), torch.cuda.Event()
         self.q_fork, self.q_join = torch.cuda.Event(), torch.cuda.Event()
+        self.g_join = torch.cuda.Event()
         s0 = self.ts if self.ts is not None else torch.cuda.current_stream(dev)
-        for e in (self.fork, self.join, self.q_fork, self.q_join):
+        for e in (self.fork, self.join, self.q_fork, self.q_join, self.g_join):
             e.record(s0)
 
     def _batch(self, lo, hi):
@@ -141,18 +145,28 @@ class TGNStep:
 
     def backward(self, dz):
         p, g, s = self.params, self.grads, self.ts
-        if self.overlap:   # the d_mem part runs on the second stream, joined before the GRU backward
+        if self.overlap:
+            # d_mem, then the GRU backward, on the second stream while the attention parameter gradients
+            # run here; the time-encoder gradient of the messages accumulates here after the join, in the
+            # same order as without overlap
             M.mtgnn_temporal_attn_bwd_overlap(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
                                               self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"],
                                               p["time_b"], self.ap, self.d, self.ag, self.d_mem, g["time_w"],
                                               g["time_b"], self.ws, self.side_stream, self.fork, self.join, stream=s)
+            M.mtgnn_gru_update_bwd(self.d_mem, self.gru_save, self.msg, self.n_uniq, self.max_rows, p["W_ih"],
+                                   p["W_hh"], self.d, g["W_ih"], g["W_hh"], g["b_ih"], g["b_hh"], self.dmsg_time,
+                                   self.ws_q, stream=self.side_stream)
+            self.g_join.record(self.side_stream)
+            main = s if s is not None else torch.cuda.current_stream(self.dev)
+            main.wait_event(self.g_join)
         else:
             M.mtgnn_temporal_attn_bwd(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
                                       self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],
                                       self.ap, self.d, self.ag, self.d_mem, g["time_w"], g["time_b"], self.ws,
                                       stream=s)
-        M.mtgnn_gru_update_bwd(self.d_mem, self.gru_save, self.msg, self.n_uniq, self.max_rows, p["W_ih"], p["W_hh"],
-                               self.d, g["W_ih"], g["W_hh"], g["b_ih"], g["b_hh"], self.dmsg_time, self.ws, stream=s)
+            M.mtgnn_gru_update_bwd(self.d_mem, self.gru_save, self.msg, self.n_uniq, self.max_rows, p["W_ih"],
+                                   p["W_hh"], self.d, g["W_ih"], g["W_hh"], g["b_ih"], g["b_hh"], self.dmsg_time,
+                                   self.ws, stream=s)
         M.mtgnn_build_messages_bwd(self.dmsg_time, self.dt, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],
                                    self.d, g["time_w"], g["time_b"], self.ws, stream=s)
 
