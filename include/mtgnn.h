@@ -214,6 +214,29 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
                                  const mtgnn_attn_params* params, const mtgnn_dims* dims, float* z, void* save,
                                  void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Row a6 in two calls, for callers that run the first on another stream while
+ * the memory table is still being updated (it reads neither the memory nor
+ * the queries).  mtgnn_temporal_attn is exactly
+ * mtgnn_temporal_attn_prepare followed by mtgnn_temporal_attn_prepared on
+ * one stream, and the results are bitwise the same.
+ *   _prepare  -- from nbr (valid slots lead each row) and the weights, writes
+ *                into save the stacked [W_k; W_v] and [b_k; b_v], the padded
+ *                merge-layer weights (float32) and the per-query valid-slot
+ *                counts, their exclusive prefix sums and the valid total;
+ *                ws as for mtgnn_temporal_attn.
+ *   _prepared -- the rest of the forward, reading what _prepare wrote into
+ *                the same save (same nbr, n_q, max_q, weights and dims); the
+ *                caller orders it after _prepare (same stream, or an event).
+ * Arguments, layouts and errors as for mtgnn_temporal_attn. */
+mtgnn_status mtgnn_temporal_attn_prepare(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
+                                         const mtgnn_attn_params* params, const mtgnn_dims* d, void* save, void* ws,
+                                         size_t ws_bytes, hipStream_t stream);
+mtgnn_status mtgnn_temporal_attn_prepared(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                          const int32_t* nbr, const float* nt, const int32_t* neid,
+                                          const void* memory, const float* edge_feat, const float* time_w,
+                                          const float* time_b, const mtgnn_attn_params* params, const mtgnn_dims* d,
+                                          float* z, void* save, hipStream_t stream);
+
 /* Row a7. Backward of mtgnn_temporal_attn for the output gradient dz [max_q, d_attn].
  * The caller computes dz from the masked loss (Eq. 13).
  *   grads -- every attention parameter gradient (overwritten);

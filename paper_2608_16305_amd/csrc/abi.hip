@@ -260,11 +260,10 @@ static mtgnn_status check_attn_params(const mtgnn_attn_params* p) {
   return MTGNN_OK;
 }
 
-mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
-                                 const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
-                                 const float* edge_feat, const float* time_w, const float* time_b,
-                                 const mtgnn_attn_params* params, const mtgnn_dims* d, float* z, void* save, void* ws,
-                                 size_t ws_bytes, hipStream_t stream) {
+static mtgnn_status attn_fwd_checked(const int32_t* q_node, const float* q_t, int64_t max_q, const int32_t* nbr,
+                                     const float* nt, const int32_t* neid, const void* memory, const float* edge_feat,
+                                     const float* time_w, const float* time_b, const mtgnn_attn_params* params,
+                                     const mtgnn_dims* d, const float* z, const void* save) {
   MTGNN_TRY(check_dims(d));
   MTGNN_TRY(check_attn_params(params));
   if (max_q < 0 || max_q * (int64_t)d->k >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
@@ -279,9 +278,45 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
   REQ(save, "save");
   if (d->d_time > 0 && (!time_w || !time_b)) return fail(MTGNN_EINVAL, "time encoder is NULL");
   if ((d->d_edge > 0) != (edge_feat != nullptr)) return fail(MTGNN_EINVAL, "edge_feat must be given iff d_edge > 0");
+  return MTGNN_OK;
+}
+
+mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                 const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
+                                 const float* edge_feat, const float* time_w, const float* time_b,
+                                 const mtgnn_attn_params* params, const mtgnn_dims* d, float* z, void* save, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(attn_fwd_checked(q_node, q_t, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b, params, d, z,
+                             save));
+  if (max_q == 0) return MTGNN_OK;
   if (ws_bytes < attn_fwd_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "temporal_attn ws");
   return attn_fwd_impl(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b, params, d, z, save,
                        ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_temporal_attn_prepare(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
+                                         const mtgnn_attn_params* params, const mtgnn_dims* d, void* save, void* ws,
+                                         size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_attn_params(params));
+  if (max_q < 0 || max_q * (int64_t)d->k >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (max_q == 0) return MTGNN_OK;
+  REQ(nbr, "nbr");
+  REQ(save, "save");
+  if (ws_bytes < attn_fwd_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "temporal_attn_prepare ws");
+  return attn_prepare_impl(nbr, n_q, max_q, params, d, save, ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_temporal_attn_prepared(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                          const int32_t* nbr, const float* nt, const int32_t* neid,
+                                          const void* memory, const float* edge_feat, const float* time_w,
+                                          const float* time_b, const mtgnn_attn_params* params, const mtgnn_dims* d,
+                                          float* z, void* save, hipStream_t stream) {
+  MTGNN_TRY(attn_fwd_checked(q_node, q_t, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b, params, d, z,
+                             save));
+  if (max_q == 0) return MTGNN_OK;
+  return attn_fwd_prepared_impl(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b, params, d,
+                                z, save, stream);
 }
 
 static mtgnn_status attn_bwd_checked(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,

@@ -673,14 +673,11 @@ size_t attn_save_bytes(const mtgnn_dims* d, int64_t max_q) { return carve_save(n
 
 size_t attn_fwd_ws(const mtgnn_dims*, int64_t max_q) { return scan_ws_bytes(max_q); }
 
-mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
-                           const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
-                           const float* edge_feat, const float* tw, const float* tb, const mtgnn_attn_params* p,
-                           const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s) {
+mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,
+                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes, hipStream_t s) {
   const AttnShape sh(d, max_q);
   const AttnSave sv = carve_save(save, sh);
   const int bf = d->dtype == MTGNN_BF16 ? 1 : 0;
-  const int wt = d->dtype;
   const int64_t wkv = (int64_t)sh.da * sh.Dkv;
   if (!bf)
     k_stack_kv<float><<<(unsigned)cdiv(wkv, 256), 256, 0, s>>>((const float*)p->W_k, (const float*)p->W_v, p->b_k,
@@ -690,9 +687,31 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
                                                                   p->b_k, p->b_v, sh.da, sh.Dkv,
                                                                   (uint16_t*)sv.W_kv, sv.b_kv);
   MTGNN_CHECK_LAUNCH("stack_kv");
+  if (merge_fused_ok(d->dtype, sh.da, sh.dm))
+    MTGNN_TRY(merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm,
+                            sv.merge_w, s));
   k_pair_counts<<<(unsigned)cdiv(max_q, 256), 256, 0, s>>>(nbr, n_q, max_q, sh.k, sv.cnt);
   MTGNN_CHECK_LAUNCH("pair_counts");
-  MTGNN_TRY(scan_exclusive(sv.cnt, sv.pair_off, max_q, sv.n_valid, ws, ws_bytes, s));
+  return scan_exclusive(sv.cnt, sv.pair_off, max_q, sv.n_valid, ws, ws_bytes, s);
+}
+
+mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                           const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
+                           const float* edge_feat, const float* tw, const float* tb, const mtgnn_attn_params* p,
+                           const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s) {
+  MTGNN_TRY(attn_prepare_impl(nbr, n_q, max_q, p, d, save, ws, ws_bytes, s));
+  return attn_fwd_prepared_impl(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, tw, tb, p, d, z, save, s);
+}
+
+mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                    const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
+                                    const float* edge_feat, const float* tw, const float* tb,
+                                    const mtgnn_attn_params* p, const mtgnn_dims* d, float* z, void* save,
+                                    hipStream_t s) {
+  const AttnShape sh(d, max_q);
+  const AttnSave sv = carve_save(save, sh);
+  const int bf = d->dtype == MTGNN_BF16 ? 1 : 0;
+  const int wt = d->dtype;
   const unsigned gq = (unsigned)cdiv(sh.Q, 4);
   if (!bf) {
     k_attn_gather_q<float><<<gq, 256, 0, s>>>(q_node, n_q, max_q, (const float*)memory, tw, tb, sh.dm, sh.dt, sh.da, 0,
@@ -720,8 +739,6 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
   MTGNN_CHECK_LAUNCH("attn_core");
   const int64_t ldm = sh.da + sh.dm;
   if (merge_fused_ok(d->dtype, sh.da, sh.dm)) {
-    MTGNN_TRY(merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm,
-                            sv.merge_w, s));
     return merge_fwd_fused(sv.attn, sv.m_in, sv.merge_w, p->b_o, p->b_1, p->b_2, sv.m1, sv.a1, z, n_q, max_q, sh.da,
                            sh.dm, s);
   }

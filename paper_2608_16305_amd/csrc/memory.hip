@@ -98,14 +98,15 @@ __global__ void k_agg_max(const int32_t* __restrict__ src, const int32_t* __rest
   }
 }
 
-// One block compacts up to AGG_BLOCK_MAX messages: thread t owns messages
-// 16 t .. 16 t + 15 (so the output order, increasing m, is thread order), flags
-// its winners (m == T[node(m)]), and one block-wide exclusive scan of the
-// per-thread winner counts gives every winner its position.
 constexpr int AGG_BLOCK_THREADS = 1024;
 constexpr int AGG_PER_THREAD = 16;
 constexpr int64_t AGG_BLOCK_MAX = AGG_BLOCK_THREADS * AGG_PER_THREAD;
 
+// One block compacts up to AGG_BLOCK_MAX messages: thread t owns messages 16 t .. 16 t + 15 (so
+// the output order, increasing m, is thread order), flags its winners (m == T[node(m)]), and
+// one block-wide exclusive scan of the per-thread winner counts gives every winner its
+// position.  Each thread's loads are issued together (clamped indices, no branches), so the
+// block waits for two rounds of memory latency rather than one per message.
 __global__ __launch_bounds__(AGG_BLOCK_THREADS) void k_agg_compact_block(const int32_t* __restrict__ src,
                                                                          const int32_t* __restrict__ dst,
                                                                          const uint8_t* __restrict__ flags,
@@ -117,12 +118,28 @@ __global__ __launch_bounds__(AGG_BLOCK_THREADS) void k_agg_compact_block(const i
   const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
   const int64_t m0 = (int64_t)t * AGG_PER_THREAD;
   int32_t node[AGG_PER_THREAD];
+  {   // messages 2 i, 2 i + 1 of events i = m0 / 2 ..
+    const int64_t ne = nm >> 1, e0 = m0 >> 1;
+    // without flags, bytes of src stand in for them (in bounds: src holds 4 ne bytes) under a zero mask
+    const uint8_t* fl = flags != nullptr ? flags : (const uint8_t*)src;
+    const uint8_t pruned = flags != nullptr ? 2 : 0;
 #pragma unroll
-  for (int j = 0; j < AGG_PER_THREAD; ++j) node[j] = m0 + j < nm ? msg_node(src, dst, flags, m0 + j) : -1;
+    for (int k = 0; k < AGG_PER_THREAD / 2; ++k) {
+      const int64_t i = e0 + k < ne ? e0 + k : ne - 1;
+      const int32_t a = src[i], b = dst[i];
+      const uint8_t f = fl[i];
+      const bool ok = (e0 + k < ne) & ((f & pruned) == 0);
+      node[2 * k] = ok ? a : -1;
+      node[2 * k + 1] = ok ? b : -1;
+    }
+  }
+  int32_t tv[AGG_PER_THREAD];   // entry 0 stands in for a missing message
+#pragma unroll
+  for (int j = 0; j < AGG_PER_THREAD; ++j) tv[j] = T[node[j] >= 0 ? node[j] : 0];
   uint32_t winbits = 0;
 #pragma unroll
   for (int j = 0; j < AGG_PER_THREAD; ++j)
-    if (node[j] >= 0 && T[node[j]] == (int32_t)(m0 + j)) winbits |= 1u << j;
+    winbits |= (node[j] >= 0 && tv[j] == (int32_t)(m0 + j)) ? 1u << j : 0u;
   const int cnt = __popc(winbits);
   int incl = cnt;   // inclusive scan over the wave
 #pragma unroll

@@ -72,6 +72,15 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
                            const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
                            const float* edge_feat, const float* tw, const float* tb, const mtgnn_attn_params* p,
                            const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s);
+// The forward's inputs that need only the sampled neighbours and the weights (stacked key/value
+// weights, padded merge weights, per-query valid-slot counts and offsets), then the rest.
+mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,
+                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes, hipStream_t s);
+mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                    const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
+                                    const float* edge_feat, const float* tw, const float* tb,
+                                    const mtgnn_attn_params* p, const mtgnn_dims* d, float* z, void* save,
+                                    hipStream_t s);
 size_t attn_bwd_ws(const mtgnn_dims* d, int64_t max_q, int64_t max_rows);
 mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
                            const int32_t* nbr, const float* nt, const float* dz, const void* save, const int32_t* uniq,

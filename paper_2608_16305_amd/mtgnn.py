@@ -20,7 +20,8 @@ OP_TEMPORAL_ATTN, OP_TEMPORAL_ATTN_BWD, OP_GRU_UPDATE_BWD, OP_BUILD_MESSAGES_BWD
 
 ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
-    "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap",
+    "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_prepare", "mtgnn_temporal_attn_prepared",
+    "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap",
     "mtgnn_gru_update_bwd",
     "mtgnn_build_messages_bwd", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
@@ -65,6 +66,9 @@ _SIGS = {
     "mtgnn_sample_recent": [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I32, _P, _P, _P, _P],
     "mtgnn_temporal_attn": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams), C.POINTER(Dims), _P,
                             _P, _P, _SZ, _P],
+    "mtgnn_temporal_attn_prepare": [_P, _P, _I64, C.POINTER(AttnParams), C.POINTER(Dims), _P, _P, _SZ, _P],
+    "mtgnn_temporal_attn_prepared": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams),
+                                     C.POINTER(Dims), _P, _P, _P],
     "mtgnn_temporal_attn_bwd": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, C.POINTER(AttnParams),
                                 C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_bwd_overlap": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P,
@@ -230,6 +234,27 @@ def mtgnn_temporal_attn(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_fea
                                      _ptr(time_w, torch.float32, "time_w"), _ptr(time_b, torch.float32, "time_b"),
                                      C.byref(params), C.byref(d), _ptr(z, torch.float32, "z"),
                                      _ptr(save, torch.uint8, "save"), wp, wb, _stream(stream)), "mtgnn_temporal_attn")
+
+
+def mtgnn_temporal_attn_prepare(nbr, n_q, max_q, params: AttnParams, d: Dims, save, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_temporal_attn_prepare(_ptr(nbr, torch.int32, "nbr"), _ptr(n_q, torch.int32, "n_q", True),
+                                             int(max_q), C.byref(params), C.byref(d),
+                                             _ptr(save, torch.uint8, "save"), wp, wb, _stream(stream)),
+           "mtgnn_temporal_attn_prepare")
+
+
+def mtgnn_temporal_attn_prepared(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b,
+                                 params: AttnParams, d: Dims, z, save, stream=None):
+    _check(lib().mtgnn_temporal_attn_prepared(_ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"),
+                                              _ptr(n_q, torch.int32, "n_q", True), int(max_q),
+                                              _ptr(nbr, torch.int32, "nbr"), _ptr(nt, torch.float32, "nt"),
+                                              _ptr(neid, torch.int32, "neid"), _ptr(memory, _DT[d.dtype], "memory"),
+                                              _ptr(edge_feat, torch.float32, "edge_feat", True),
+                                              _ptr(time_w, torch.float32, "time_w"),
+                                              _ptr(time_b, torch.float32, "time_b"), C.byref(params), C.byref(d),
+                                              _ptr(z, torch.float32, "z"), _ptr(save, torch.uint8, "save"),
+                                              _stream(stream)), "mtgnn_temporal_attn_prepared")
 
 
 def mtgnn_temporal_attn_bwd(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b,

@@ -2,13 +2,14 @@
 
 A step on batch b (default lag-1 order) runs
   memory phase on batch b-1:  aggregate_last -> build_messages -> gru_update
-  embedding on batch b:       build_queries  -> sample_recent  -> temporal_attn
+  embedding on batch b:       build_queries  -> sample_recent  -> temporal_attn (prepare, prepared)
   backward:                   temporal_attn_bwd -> gru_update_bwd -> build_messages_bwd
 all enqueued on one HIP stream with no host synchronisation (the only
 data-dependent sizes, updated rows and queries, stay in device memory), except
 that with overlap=True (the default) two pieces run on a second stream, forked
-and joined with events: the queries and their sampling, during the memory
-phase, and the attention backward's d_mem part followed by the GRU backward,
+and joined with events: the queries, their sampling and the attention's
+preparation, during the memory phase, and the attention backward's d_mem part
+(its key sort from the backward's start) followed by the GRU backward,
 during the attention parameter gradients.  Results are bitwise those of
 overlap=False.
 """
@@ -95,9 +96,10 @@ class TGNStep:
                (M.OP_BUILD_MESSAGES_BWD, R, 0)]
         need = max(M.workspace_bytes(op, d, r, q) for op, r, q in ops)
         self.ws = M.alloc_bytes(need, dev)   # the calls of one step run in stream order and share it
-        # work on the second stream (query building during the memory phase, the GRU backward during the
-        # attention backward's parameter gradients) has its own workspace
+        # work on the second stream (queries, sampling and the attention's preparation during the memory
+        # phase, the GRU backward during the attention backward's parameter gradients) has its own workspace
         self.ws_q = M.alloc_bytes(max(M.workspace_bytes(M.OP_BUILD_QUERIES, d, B, 0),
+                                      M.workspace_bytes(M.OP_TEMPORAL_ATTN, d, 0, Q),
                                       M.workspace_bytes(M.OP_GRU_UPDATE_BWD, d, R, 0), 256), dev)
         self.ap = M.attn_params(self.params, d)
         self.ag = M.attn_grads(self.grads)
@@ -129,19 +131,22 @@ class TGNStep:
                            self.gru_save if save else None, self.ws, stream=s)
 
     def queries(self, lo, hi, stream):
-        """Queries of the batch's target events and their most-recent-k neighbours (no memory read)."""
+        """Queries of the batch's target events, their most-recent-k neighbours and the attention's
+        preparation (slot counts and offsets, stacked and padded weights): no memory read."""
         b = self._batch(lo, hi)
         M.mtgnn_build_queries(b, self.neg[lo:hi], self.q_node, self.q_t, self.n_q, self.ws_q, stream=stream)
         M.mtgnn_sample_recent(self.csr_off, self.csr_nbr, self.csr_t, self.csr_eid, self.w.n_nodes, self.q_node,
                               self.q_t, self.n_q, self.max_q, self.w.k, self.nbr, self.nt, self.neid, stream=stream)
+        M.mtgnn_temporal_attn_prepare(self.nbr, self.n_q, self.max_q, self.ap, self.d, self.attn_save, self.ws_q,
+                                      stream=stream)
 
     def embed(self, lo, hi, queries_done=False):
         p, s = self.params, self.ts
         if not queries_done:
             self.queries(lo, hi, s)
-        M.mtgnn_temporal_attn(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, self.neid, self.memory,
-                              self.x, p["time_w"], p["time_b"], self.ap, self.d, self.z, self.attn_save, self.ws,
-                              stream=s)
+        M.mtgnn_temporal_attn_prepared(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, self.neid,
+                                       self.memory, self.x, p["time_w"], p["time_b"], self.ap, self.d, self.z,
+                                       self.attn_save, stream=s)
 
     def backward(self, dz):
         p, g, s = self.params, self.grads, self.ts
@@ -182,8 +187,8 @@ class TGNStep:
         else:
             mlo, mhi = elo, ehi
         if self.overlap:
-            # queries and sampling on the second stream while the memory phase runs here (they
-            # read only the batch and the adjacency); joined before the attention reads memory
+            # queries, sampling and preparation on the second stream while the memory phase runs here (they
+            # read only the batch, the adjacency and the weights); joined before the attention reads memory
             main = self.ts if self.ts is not None else torch.cuda.current_stream(self.dev)
             self.q_fork.record(main)
             self.side_stream.wait_event(self.q_fork)

@@ -192,3 +192,35 @@ def test_backward_overlap_bitwise():
     for k in outs[0]:
         a, b = outs[0][k], outs[1][k]
         assert a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
+
+
+def test_forward_single_call_matches_prepare_prepared():
+    """mtgnn_temporal_attn in one call gives bitwise the z and the save buffer of
+    mtgnn_temporal_attn_prepare followed by mtgnn_temporal_attn_prepared (bipartite stream)."""
+    from paper_2608_16305_amd import mtgnn as M
+    from paper_2608_16305_amd.step import TGNStep
+    w = workload(2)
+    log("[parity] single-call forward vs prepare + prepared, workload 2")
+    s = make_stream(w)
+    params = init_params(w, random_bias=True)
+    mem, lu = random_state(w, seed=5)
+    r = TGNStep(w, s, params, mem, lu, overlap=False)
+    b = 2
+    r.memory_phase(*r.batch_range(b - 1))
+    r.queries(*r.batch_range(b), None)
+    p = r.params
+    outs = []
+    for split in (False, True):
+        save = torch.zeros_like(r.attn_save)
+        z = torch.zeros_like(r.z)
+        args = (r.q_node, r.q_t, r.n_q, r.max_q, r.nbr, r.nt, r.neid, r.memory, r.x, p["time_w"], p["time_b"],
+                r.ap, r.d, z, save)
+        if split:
+            M.mtgnn_temporal_attn_prepare(r.nbr, r.n_q, r.max_q, r.ap, r.d, save, r.ws)
+            M.mtgnn_temporal_attn_prepared(*args)
+        else:
+            M.mtgnn_temporal_attn(*args, r.ws)
+        torch.cuda.synchronize()
+        outs.append((to_np(z).copy(), to_np(save).copy()))
+    assert np.array_equal(outs[0][0].view(np.uint32), outs[1][0].view(np.uint32))
+    assert np.array_equal(outs[0][1], outs[1][1])
