@@ -8,8 +8,11 @@ all enqueued on one HIP stream with no host synchronisation (the only
 data-dependent sizes, updated rows and queries, stay in device memory), except
 that with overlap=True (the default) two pieces run on a second stream, forked
 and joined with events: the queries, their sampling and the attention's
-preparation, during the memory phase, and the attention backward's d_mem part
-(its key sort from the backward's start) followed by the GRU backward,
+preparation, during the memory phase; the next step's aggregation and
+messages (lag-1 order: its memory batch is this step's batch, read from the
+memory this step's update leaves), during the embedding; and the attention
+backward's d_mem part (its key sort from the backward's start) followed by the
+GRU backward,
 during the attention parameter gradients.  Results are bitwise those of
 overlap=False.
 """
@@ -73,11 +76,13 @@ class TGNStep:
         R, Q, k = self.max_rows, self.max_q, w.k
         i32 = dict(dtype=torch.int32, device=dev)
         f32 = dict(dtype=torch.float32, device=dev)
-        self.uniq = torch.empty(R, **i32)
-        self.winner = torch.empty(R, **i32)
-        self.n_uniq = torch.zeros(1, **i32)
-        self.msg = torch.empty(R, w.d_msg, dtype=self.sdt, device=dev)
-        self.dt = torch.empty(R, **f32)
+        # two sets of the memory phase's aggregation and message buffers: with overlap, the next
+        # step's set is filled on the second stream while this step's is still read by its backward
+        self._sets = [dict(uniq=torch.empty(R, **i32), winner=torch.empty(R, **i32), n_uniq=torch.zeros(1, **i32),
+                           msg=torch.empty(R, w.d_msg, dtype=self.sdt, device=dev), dt=torch.empty(R, **f32))
+                      for _ in range(2)]
+        self._bind(0)
+        self._pre = None   # (lo, hi) of the batch whose aggregation and messages fill the other set
         self.gru_save = M.alloc_bytes(M.save_bytes(M.OP_GRU_UPDATE, d, R, 0), dev)
         self.q_node = torch.empty(Q, **i32)
         self.q_t = torch.empty(Q, **f32)
@@ -99,6 +104,7 @@ class TGNStep:
         # work on the second stream (queries, sampling and the attention's preparation during the memory
         # phase, the GRU backward during the attention backward's parameter gradients) has its own workspace
         self.ws_q = M.alloc_bytes(max(M.workspace_bytes(M.OP_BUILD_QUERIES, d, B, 0),
+                                      M.workspace_bytes(M.OP_AGGREGATE_LAST, d, B, 0),
                                       M.workspace_bytes(M.OP_TEMPORAL_ATTN, d, 0, Q),
                                       M.workspace_bytes(M.OP_GRU_UPDATE_BWD, d, R, 0), 256), dev)
         self.ap = M.attn_params(self.params, d)
@@ -109,8 +115,9 @@ class TGNStep:
         self.fork, self.join = torch.cuda.Event(), torch.cuda.Event()
         self.q_fork, self.q_join = torch.cuda.Event(), torch.cuda.Event()
         self.g_join = torch.cuda.Event()
+        self.m_done, self.pre_join = torch.cuda.Event(), torch.cuda.Event()
         s0 = self.ts if self.ts is not None else torch.cuda.current_stream(dev)
-        for e in (self.fork, self.join, self.q_fork, self.q_join, self.g_join):
+        for e in (self.fork, self.join, self.q_fork, self.q_join, self.g_join, self.m_done, self.pre_join):
             e.record(s0)
 
     def _batch(self, lo, hi):
@@ -119,16 +126,32 @@ class TGNStep:
         f = self.flags[lo:hi] if self.flags is not None else None
         return M.batch(self.src[lo:hi], self.dst[lo:hi], self.t[lo:hi], self.eid[lo:hi], f)
 
+    def _bind(self, i):
+        """Make buffer set i the current one (self.uniq, winner, n_uniq, msg, dt)."""
+        self._cur = i
+        for k, v in self._sets[i].items():
+            setattr(self, k, v)
+
     # ------------------------------------------------------------------ phases
-    def memory_phase(self, lo, hi, save=True):
+    def _messages(self, lo, hi, bufs, ws, stream):
+        """Most-recent aggregation and message construction of events lo..hi into the buffer set bufs."""
         b = self._batch(lo, hi)
-        p, s = self.params, self.ts
-        M.mtgnn_aggregate_last(b, self.w.n_nodes, self.uniq, self.winner, self.n_uniq, self.ws, stream=s)
-        M.mtgnn_build_messages(b, self.uniq, self.winner, self.n_uniq, self.max_rows, self.memory, self.last_update,
-                               self.x, p["time_w"], p["time_b"], self.d, self.msg, self.dt, stream=s)
-        M.mtgnn_gru_update(b, self.uniq, self.winner, self.n_uniq, self.max_rows, self.msg, p["W_ih"], p["W_hh"],
-                           p["b_ih"], p["b_hh"], self.d, self.memory, self.last_update,
-                           self.gru_save if save else None, self.ws, stream=s)
+        p = self.params
+        M.mtgnn_aggregate_last(b, self.w.n_nodes, bufs["uniq"], bufs["winner"], bufs["n_uniq"], ws, stream=stream)
+        M.mtgnn_build_messages(b, bufs["uniq"], bufs["winner"], bufs["n_uniq"], self.max_rows, self.memory,
+                               self.last_update, self.x, p["time_w"], p["time_b"], self.d, bufs["msg"], bufs["dt"],
+                               stream=stream)
+
+    def _gru(self, lo, hi, save=True):
+        p = self.params
+        M.mtgnn_gru_update(self._batch(lo, hi), self.uniq, self.winner, self.n_uniq, self.max_rows, self.msg,
+                           p["W_ih"], p["W_hh"], p["b_ih"], p["b_hh"], self.d, self.memory, self.last_update,
+                           self.gru_save if save else None, self.ws, stream=self.ts)
+
+    def memory_phase(self, lo, hi, save=True):
+        self._pre = None   # the memory changes: nothing prepared from the old state stays valid
+        self._messages(lo, hi, self._sets[self._cur], self.ws, self.ts)
+        self._gru(lo, hi, save)
 
     def queries(self, lo, hi, stream):
         """Queries of the batch's target events, their most-recent-k neighbours and the attention's
@@ -190,11 +213,29 @@ class TGNStep:
             # queries, sampling and preparation on the second stream while the memory phase runs here (they
             # read only the batch, the adjacency and the weights); joined before the attention reads memory
             main = self.ts if self.ts is not None else torch.cuda.current_stream(self.dev)
+            side = self.side_stream
             self.q_fork.record(main)
-            self.side_stream.wait_event(self.q_fork)
-            self.queries(elo, ehi, self.side_stream)
-            self.q_join.record(self.side_stream)
-            self.memory_phase(mlo, mhi)
+            side.wait_event(self.q_fork)
+            self.queries(elo, ehi, side)
+            self.q_join.record(side)
+            if self.lag == 1 and self._pre == (mlo, mhi):
+                # this memory batch's aggregation and messages were built during the previous step's
+                # embedding, from the memory as it is now: only the GRU update is left
+                self._bind(1 - self._cur)
+                main.wait_event(self.pre_join)
+                self._pre = None
+                self._gru(mlo, mhi)
+            else:
+                self.memory_phase(mlo, mhi)
+            if self.lag == 1:
+                # the next step's memory batch is this step's batch: its aggregation and messages read the
+                # memory as this update leaves it, which nothing changes before the next step's GRU update;
+                # built on the second stream into the other buffer set while the embedding runs here
+                self.m_done.record(main)
+                side.wait_event(self.m_done)
+                self._messages(elo, ehi, self._sets[1 - self._cur], self.ws_q, side)
+                self.pre_join.record(side)
+                self._pre = (elo, ehi)
             main.wait_event(self.q_join)
             self.embed(elo, ehi, queries_done=True)
         else:
