@@ -223,7 +223,11 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
  *                into save the stacked [W_k; W_v] and [b_k; b_v], the padded
  *                merge-layer weights (float32) and the per-query valid-slot
  *                counts, their exclusive prefix sums and the valid total;
- *                ws as for mtgnn_temporal_attn.
+ *                ws as for mtgnn_temporal_attn.  It is exactly
+ *                _prepare_weights (the weight copies: they read only the
+ *                weights, and their place in save does not depend on max_q)
+ *                followed by _prepare_slots (the counts, offsets and total);
+ *                the two may run on different streams, in either order.
  *   _prepared -- the rest of the forward, reading what _prepare wrote into
  *                the same save (same nbr, n_q, max_q, weights and dims); the
  *                caller orders it after _prepare (same stream, or an event).
@@ -231,6 +235,11 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
 mtgnn_status mtgnn_temporal_attn_prepare(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
                                          const mtgnn_attn_params* params, const mtgnn_dims* d, void* save, void* ws,
                                          size_t ws_bytes, hipStream_t stream);
+mtgnn_status mtgnn_temporal_attn_prepare_weights(const mtgnn_attn_params* params, const mtgnn_dims* d, void* save,
+                                                 hipStream_t stream);
+mtgnn_status mtgnn_temporal_attn_prepare_slots(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
+                                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes,
+                                               hipStream_t stream);
 mtgnn_status mtgnn_temporal_attn_prepared(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
                                           const int32_t* nbr, const float* nt, const int32_t* neid,
                                           const void* memory, const float* edge_feat, const float* time_w,

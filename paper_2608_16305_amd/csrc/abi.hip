@@ -307,6 +307,26 @@ mtgnn_status mtgnn_temporal_attn_prepare(const int32_t* nbr, const int32_t* n_q,
   return attn_prepare_impl(nbr, n_q, max_q, params, d, save, ws, ws_bytes, stream);
 }
 
+mtgnn_status mtgnn_temporal_attn_prepare_weights(const mtgnn_attn_params* params, const mtgnn_dims* d, void* save,
+                                                 hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_attn_params(params));
+  REQ(save, "save");
+  return attn_prepare_weights_impl(params, d, save, stream);
+}
+
+mtgnn_status mtgnn_temporal_attn_prepare_slots(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
+                                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes,
+                                               hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  if (max_q < 0 || max_q * (int64_t)d->k >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (max_q == 0) return MTGNN_OK;
+  REQ(nbr, "nbr");
+  REQ(save, "save");
+  if (ws_bytes < attn_fwd_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "temporal_attn_prepare_slots ws");
+  return attn_prepare_slots_impl(nbr, n_q, max_q, d, save, ws, ws_bytes, stream);
+}
+
 mtgnn_status mtgnn_temporal_attn_prepared(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
                                           const int32_t* nbr, const float* nt, const int32_t* neid,
                                           const void* memory, const float* edge_feat, const float* time_w,

@@ -51,8 +51,11 @@ AttnSave carve_save(void* base, const AttnShape& s) {
   AttnSave v;
   auto take = [&](size_t bytes) { char* r = w; w += a256(bytes); return r; };
   const int64_t dtp = s.dt > 0 ? s.dt : 1;
+  // the weight copies first: their offsets do not depend on the query count (the weights-only
+  // preparation carves with none)
   v.W_kv = take(s.esz * 2 * s.da * s.Dkv);
   v.b_kv = (float*)take(sizeof(float) * 2 * s.da);
+  v.merge_w = (float*)take(sizeof(float) * (s.esz == 4 ? merge_weights_floats(s.da, s.dm) : 1));
   v.cnt = (int32_t*)take(sizeof(int32_t) * s.Q);
   v.pair_off = (int32_t*)take(sizeof(int32_t) * s.Q);
   v.n_valid = (int32_t*)take(sizeof(int32_t));
@@ -68,7 +71,6 @@ AttnSave carve_save(void* base, const AttnShape& s) {
   v.m_in = (float*)take(sizeof(float) * s.Q * (s.da + s.dm));
   v.m1 = (float*)take(sizeof(float) * s.Q * s.da);
   v.a1 = (float*)take(sizeof(float) * s.Q * s.da);
-  v.merge_w = (float*)take(sizeof(float) * (s.esz == 4 ? merge_weights_floats(s.da, s.dm) : 1));
   v.total = (size_t)(w - (char*)base);
   return v;
 }
@@ -201,6 +203,7 @@ constexpr int SLOT_CHUNK = 8;   // slots whose rows are loaded together (their l
 // Slot rows are read SLOT_CHUNK at a time, all loads issued before use; the
 // per-slot sums keep their order.  (The backward below groups the value-row
 // loads of its first phase only: grouping the second phase measured slower.)
+template <int DHC>   // 64-wide chunks of a head (DHC 64 >= dh)
 __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv, const float* __restrict__ KV,
                                                    const int32_t* __restrict__ cnt,
                                                    const int32_t* __restrict__ pair_off,
@@ -214,20 +217,20 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
   const int c = cnt[q];
   const int64_t off = pair_off[q];
   for (int h = 0; h < H; ++h) {
-    float qd[MAX_DH_CHUNKS];
+    float qd[DHC];
 #pragma unroll
-    for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+    for (int cc = 0; cc < DHC; ++cc) {
       const int d = lane + 64 * cc;
       qd[cc] = d < dh ? qv[q * da + h * dh + d] : 0.f;
     }
     float my_s = -INFINITY;
     for (int j0 = 0; j0 < c; j0 += SLOT_CHUNK) {
-      float kv[SLOT_CHUNK][MAX_DH_CHUNKS];
+      float kv[SLOT_CHUNK][DHC];
 #pragma unroll
       for (int u = 0; u < SLOT_CHUNK; ++u) {
         const float* Kr = KV + (off + j0 + u) * 2 * da + h * dh;
 #pragma unroll
-        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+        for (int cc = 0; cc < DHC; ++cc) {
           const int d = lane + 64 * cc;
           kv[u][cc] = (j0 + u < c && d < dh) ? Kr[d] : 0.f;
         }
@@ -237,7 +240,7 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
         if (j0 + u >= c) break;
         float part = 0.f;
 #pragma unroll
-        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) part += qd[cc] * kv[u][cc];
+        for (int cc = 0; cc < DHC; ++cc) part += qd[cc] * kv[u][cc];
         const float sc = wave_sum(part) * scale;
         if (lane == j0 + u) my_s = sc;
       }
@@ -247,14 +250,14 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
     const float den = wave_sum(e);
     const float pj = den > 0.f ? e / den : 0.f;
     if (lane < k) P[(q * H + h) * k + lane] = pj;
-    float acc[MAX_DH_CHUNKS] = {0.f, 0.f};
+    float acc[DHC] = {};
     for (int j0 = 0; j0 < c; j0 += SLOT_CHUNK) {
-      float vv[SLOT_CHUNK][MAX_DH_CHUNKS];
+      float vv[SLOT_CHUNK][DHC];
 #pragma unroll
       for (int u = 0; u < SLOT_CHUNK; ++u) {
         const float* Vr = KV + (off + j0 + u) * 2 * da + da + h * dh;
 #pragma unroll
-        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+        for (int cc = 0; cc < DHC; ++cc) {
           const int d = lane + 64 * cc;
           vv[u][cc] = (j0 + u < c && d < dh) ? Vr[d] : 0.f;
         }
@@ -264,11 +267,11 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
         if (j0 + u >= c) break;
         const float pb = __shfl(pj, j0 + u, 64);
 #pragma unroll
-        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) acc[cc] += pb * vv[u][cc];
+        for (int cc = 0; cc < DHC; ++cc) acc[cc] += pb * vv[u][cc];
       }
     }
 #pragma unroll
-    for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+    for (int cc = 0; cc < DHC; ++cc) {
       const int d = lane + 64 * cc;
       if (d < dh) attn[q * da + h * dh + d] = pack_val(acc[cc], bf16);
     }
@@ -278,6 +281,7 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
 // Wave per query: gradients of the softmax-weighted sum and of the scores.
 //   dV_j = p_j da_h;  dp_j = da_h . V_j;  ds_j = p_j (dp_j - sum_i p_i dp_i)
 //   dq_h = sum_j ds_j K_jh / sqrt(dh);  dK_j = ds_j q_h / sqrt(dh)
+template <int DHC>   // 64-wide chunks of a head (DHC 64 >= dh)
 __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__ qv, const float* __restrict__ KV,
                                                        const float* __restrict__ P, const float* __restrict__ dattn,
                                                        const int32_t* __restrict__ cnt,
@@ -292,9 +296,9 @@ __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__
   const int c = cnt[q];
   const int64_t off = pair_off[q];
   for (int h = 0; h < H; ++h) {
-    float qd[MAX_DH_CHUNKS], gd[MAX_DH_CHUNKS];
+    float qd[DHC], gd[DHC];
 #pragma unroll
-    for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+    for (int cc = 0; cc < DHC; ++cc) {
       const int d = lane + 64 * cc;
       qd[cc] = d < dh ? qv[q * da + h * dh + d] : 0.f;
       gd[cc] = d < dh ? dattn[q * da + h * dh + d] : 0.f;
@@ -302,12 +306,12 @@ __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__
     const float pl = lane < c ? P[(q * H + h) * k + lane] : 0.f;
     float my_dp = 0.f;
     for (int j0 = 0; j0 < c; j0 += SLOT_CHUNK) {   // value rows of SLOT_CHUNK slots loaded together
-      float vv[SLOT_CHUNK][MAX_DH_CHUNKS];
+      float vv[SLOT_CHUNK][DHC];
 #pragma unroll
       for (int u = 0; u < SLOT_CHUNK; ++u) {
         const float* Vr = KV + (off + j0 + u) * 2 * da + da + h * dh;
 #pragma unroll
-        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+        for (int cc = 0; cc < DHC; ++cc) {
           const int d = lane + 64 * cc;
           vv[u][cc] = (j0 + u < c && d < dh) ? Vr[d] : 0.f;
         }
@@ -317,14 +321,14 @@ __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__
         if (j0 + u >= c) break;
         float part = 0.f;
 #pragma unroll
-        for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) part += gd[cc] * vv[u][cc];
+        for (int cc = 0; cc < DHC; ++cc) part += gd[cc] * vv[u][cc];
         const float dp = wave_sum(part);
         if (lane == j0 + u) my_dp = dp;
       }
     }
     const float sdp = wave_sum(pl * my_dp);
     const float dsl = pl * (my_dp - sdp);
-    float dq[MAX_DH_CHUNKS] = {0.f, 0.f};
+    float dq[DHC] = {};
     for (int j = 0; j < c; ++j) {
       const float dsj = __shfl(dsl, j, 64);
       const float pj = __shfl(pl, j, 64);
@@ -332,7 +336,7 @@ __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__
       const float* Kr = KV + row * 2 * da + h * dh;
       float* dK = dKV + row * 2 * da + h * dh;
 #pragma unroll
-      for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+      for (int cc = 0; cc < DHC; ++cc) {
         const int d = lane + 64 * cc;
         if (d < dh) {
           dq[cc] += dsj * Kr[d];
@@ -342,7 +346,7 @@ __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__
       }
     }
 #pragma unroll
-    for (int cc = 0; cc < MAX_DH_CHUNKS; ++cc) {
+    for (int cc = 0; cc < DHC; ++cc) {
       const int d = lane + 64 * cc;
       if (d < dh) dqv[q * da + h * dh + d] = dq[cc] * scale;
     }
@@ -673,13 +677,20 @@ size_t attn_save_bytes(const mtgnn_dims* d, int64_t max_q) { return carve_save(n
 
 size_t attn_fwd_ws(const mtgnn_dims*, int64_t max_q) { return scan_ws_bytes(max_q); }
 
-mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,
-                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes, hipStream_t s) {
-  const AttnShape sh(d, max_q);
+mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const mtgnn_dims* d, void* save,
+                                       hipStream_t s) {
+  const AttnShape sh(d, 0);
   const AttnSave sv = carve_save(save, sh);
-  const int bf = d->dtype == MTGNN_BF16 ? 1 : 0;
+  if (merge_fused_ok(d->dtype, sh.da, sh.dm)) {   // float32: one launch for every copy
+    const PlainCopy kv[4] = {{(const float*)p->W_k, (float*)sv.W_kv, sh.da, (int)sh.Dkv},
+                             {(const float*)p->W_v, (float*)sv.W_kv + (size_t)sh.da * sh.Dkv, sh.da, (int)sh.Dkv},
+                             {p->b_k, sv.b_kv, 1, sh.da},
+                             {p->b_v, sv.b_kv + sh.da, 1, sh.da}};
+    return merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm, sv.merge_w,
+                         s, kv, 4);
+  }
   const int64_t wkv = (int64_t)sh.da * sh.Dkv;
-  if (!bf)
+  if (d->dtype == MTGNN_F32)
     k_stack_kv<float><<<(unsigned)cdiv(wkv, 256), 256, 0, s>>>((const float*)p->W_k, (const float*)p->W_v, p->b_k,
                                                                p->b_v, sh.da, sh.Dkv, (float*)sv.W_kv, sv.b_kv);
   else
@@ -687,12 +698,22 @@ mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t m
                                                                   p->b_k, p->b_v, sh.da, sh.Dkv,
                                                                   (uint16_t*)sv.W_kv, sv.b_kv);
   MTGNN_CHECK_LAUNCH("stack_kv");
-  if (merge_fused_ok(d->dtype, sh.da, sh.dm))
-    MTGNN_TRY(merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm,
-                            sv.merge_w, s));
+  return MTGNN_OK;
+}
+
+mtgnn_status attn_prepare_slots_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_dims* d,
+                                     void* save, void* ws, size_t ws_bytes, hipStream_t s) {
+  const AttnShape sh(d, max_q);
+  const AttnSave sv = carve_save(save, sh);
   k_pair_counts<<<(unsigned)cdiv(max_q, 256), 256, 0, s>>>(nbr, n_q, max_q, sh.k, sv.cnt);
   MTGNN_CHECK_LAUNCH("pair_counts");
   return scan_exclusive(sv.cnt, sv.pair_off, max_q, sv.n_valid, ws, ws_bytes, s);
+}
+
+mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,
+                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes, hipStream_t s) {
+  MTGNN_TRY(attn_prepare_weights_impl(p, d, save, s));
+  return attn_prepare_slots_impl(nbr, n_q, max_q, d, save, ws, ws_bytes, s);
 }
 
 mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
@@ -733,8 +754,12 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
                                      sh.P, sv.n_valid, 2 * sh.da, sh.Dkv, false, s));
   {
     TimedScope ts("k_attn_core", s);
-    k_attn_core<<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, sh.H, bf, sv.p,
-                                   sv.attn);
+    if (sh.dh <= 64)
+      k_attn_core<1><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, sh.H, bf, sv.p,
+                                        sv.attn);
+    else
+      k_attn_core<MAX_DH_CHUNKS><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, sh.H,
+                                                    bf, sv.p, sv.attn);
   }
   MTGNN_CHECK_LAUNCH("attn_core");
   const int64_t ldm = sh.da + sh.dm;
@@ -916,8 +941,13 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     // softmax-weighted sum and scores
     {
       TimedScope ts("k_attn_core_bwd", s);
-      k_attn_core_bwd<<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q,
-                                                            max_q, sh.k, da, sh.H, b.dKV, b.dqv);
+      if (sh.dh <= 64)
+        k_attn_core_bwd<1><<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off,
+                                                                 n_q, max_q, sh.k, da, sh.H, b.dKV, b.dqv);
+      else
+        k_attn_core_bwd<MAX_DH_CHUNKS><<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt,
+                                                                             sv.pair_off, n_q, max_q, sh.k, da, sh.H,
+                                                                             b.dKV, b.dqv);
     }
     MTGNN_CHECK_LAUNCH("attn_core_bwd");
     // query projection, data gradient: dhq += dqv W_q[:, :dm] (the last input of the d M' grouping)

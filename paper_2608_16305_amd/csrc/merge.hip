@@ -203,11 +203,12 @@ __global__ __launch_bounds__(64 * MW) void k_merge_bwd(const float* __restrict__
 }
 
 // Zero-padded copies of the merge weights: dst[r][c] = W[r][c] (or W[c][r] for a transposed copy) for r < n,
-// c < k, else 0.  blockIdx.y selects the copy.
+// c < k, else 0.  blockIdx.y selects the copy (the extra ones are plain: rows = n, cols = k).
+constexpr int PREP_MAX = 10;   // the six merge copies and up to four extra plain copies
 struct PrepArgs {
-  const float* src[6];
-  float* dst[6];
-  int rows[6], cols[6], n[6], k[6], ld[6], tr[6];
+  const float* src[PREP_MAX];
+  float* dst[PREP_MAX];
+  int rows[PREP_MAX], cols[PREP_MAX], n[PREP_MAX], k[PREP_MAX], ld[PREP_MAX], tr[PREP_MAX];
 };
 
 __global__ void k_merge_prepare(PrepArgs a) {
@@ -250,7 +251,8 @@ bool merge_fused_ok(int dtype, int da, int dm) {
 size_t merge_weights_floats(int da, int dm) { return PackLayout(da, dm).off[6]; }
 
 mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
-                           hipStream_t s) {
+                           hipStream_t s, const PlainCopy* extra, int n_extra) {
+  if (n_extra < 0 || n_extra > PREP_MAX - 6) return MTGNN_EINVAL;
   const PackLayout L(da, dm);
   const int ldm = da + dm;
   PrepArgs a;
@@ -269,7 +271,16 @@ mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, in
     a.tr[m] = tr[m];
     most = std::max<int64_t>(most, (int64_t)L.rows[m] * L.cols[m]);
   }
-  k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), 6), 256, 0, s>>>(a);
+  for (int x = 0; x < n_extra; ++x) {
+    const int m = 6 + x;
+    a.src[m] = extra[x].src;
+    a.dst[m] = extra[x].dst;
+    a.rows[m] = a.n[m] = extra[x].rows;
+    a.cols[m] = a.k[m] = a.ld[m] = extra[x].cols;
+    a.tr[m] = 0;
+    most = std::max<int64_t>(most, (int64_t)extra[x].rows * extra[x].cols);
+  }
+  k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), (unsigned)(6 + n_extra)), 256, 0, s>>>(a);
   MTGNN_CHECK_LAUNCH("merge_prepare");
   return MTGNN_OK;
 }

@@ -58,8 +58,14 @@ mtgnn_status build_csr_impl(const int32_t* src, const int32_t* dst, const float*
 // Fused merge-layer chains (merge.hip): float32 and the attention / memory widths they are built for.
 bool merge_fused_ok(int dtype, int da, int dm);
 size_t merge_weights_floats(int da, int dm);
+struct PlainCopy {   // dst[rows x cols] = src[rows x cols], both contiguous
+  const float* src;
+  float* dst;
+  int rows, cols;
+};
+// One launch: the padded merge copies, then the extra plain copies (at most four).
 mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
-                           hipStream_t s);
+                           hipStream_t s, const PlainCopy* extra = nullptr, int n_extra = 0);
 mtgnn_status merge_fwd_fused(const float* attn, float* m_in, const float* Wp, const float* bo, const float* b1,
                              const float* b2, float* m1, float* a1, float* z, const int32_t* n_q, int64_t max_q,
                              int da, int dm, hipStream_t s);
@@ -74,6 +80,10 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
                            const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s);
 // The forward's inputs that need only the sampled neighbours and the weights (stacked key/value
 // weights, padded merge weights, per-query valid-slot counts and offsets), then the rest.
+mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const mtgnn_dims* d, void* save,
+                                       hipStream_t s);
+mtgnn_status attn_prepare_slots_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_dims* d,
+                                     void* save, void* ws, size_t ws_bytes, hipStream_t s);
 mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,
                                const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes, hipStream_t s);
 mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,

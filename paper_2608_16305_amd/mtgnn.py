@@ -20,7 +20,8 @@ OP_TEMPORAL_ATTN, OP_TEMPORAL_ATTN_BWD, OP_GRU_UPDATE_BWD, OP_BUILD_MESSAGES_BWD
 
 ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
-    "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_prepare", "mtgnn_temporal_attn_prepared",
+    "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_prepare", "mtgnn_temporal_attn_prepare_weights",
+    "mtgnn_temporal_attn_prepare_slots", "mtgnn_temporal_attn_prepared",
     "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap",
     "mtgnn_gru_update_bwd",
     "mtgnn_build_messages_bwd", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
@@ -67,6 +68,8 @@ _SIGS = {
     "mtgnn_temporal_attn": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams), C.POINTER(Dims), _P,
                             _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_prepare": [_P, _P, _I64, C.POINTER(AttnParams), C.POINTER(Dims), _P, _P, _SZ, _P],
+    "mtgnn_temporal_attn_prepare_weights": [C.POINTER(AttnParams), C.POINTER(Dims), _P, _P],
+    "mtgnn_temporal_attn_prepare_slots": [_P, _P, _I64, C.POINTER(Dims), _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_prepared": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams),
                                      C.POINTER(Dims), _P, _P, _P],
     "mtgnn_temporal_attn_bwd": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, C.POINTER(AttnParams),
@@ -242,6 +245,18 @@ def mtgnn_temporal_attn_prepare(nbr, n_q, max_q, params: AttnParams, d: Dims, sa
                                              int(max_q), C.byref(params), C.byref(d),
                                              _ptr(save, torch.uint8, "save"), wp, wb, _stream(stream)),
            "mtgnn_temporal_attn_prepare")
+
+
+def mtgnn_temporal_attn_prepare_weights(params: AttnParams, d: Dims, save, stream=None):
+    _check(lib().mtgnn_temporal_attn_prepare_weights(C.byref(params), C.byref(d), _ptr(save, torch.uint8, "save"),
+                                                     _stream(stream)), "mtgnn_temporal_attn_prepare_weights")
+
+
+def mtgnn_temporal_attn_prepare_slots(nbr, n_q, max_q, d: Dims, save, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_temporal_attn_prepare_slots(_ptr(nbr, torch.int32, "nbr"), _ptr(n_q, torch.int32, "n_q", True),
+                                                   int(max_q), C.byref(d), _ptr(save, torch.uint8, "save"), wp, wb,
+                                                   _stream(stream)), "mtgnn_temporal_attn_prepare_slots")
 
 
 def mtgnn_temporal_attn_prepared(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, time_w, time_b,

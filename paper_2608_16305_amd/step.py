@@ -155,17 +155,22 @@ class TGNStep:
 
     def queries(self, lo, hi, stream):
         """Queries of the batch's target events, their most-recent-k neighbours and the attention's
-        preparation (slot counts and offsets, stacked and padded weights): no memory read."""
+        per-query valid-slot counts and offsets: no memory read."""
         b = self._batch(lo, hi)
         M.mtgnn_build_queries(b, self.neg[lo:hi], self.q_node, self.q_t, self.n_q, self.ws_q, stream=stream)
         M.mtgnn_sample_recent(self.csr_off, self.csr_nbr, self.csr_t, self.csr_eid, self.w.n_nodes, self.q_node,
                               self.q_t, self.n_q, self.max_q, self.w.k, self.nbr, self.nt, self.neid, stream=stream)
-        M.mtgnn_temporal_attn_prepare(self.nbr, self.n_q, self.max_q, self.ap, self.d, self.attn_save, self.ws_q,
-                                      stream=stream)
+        M.mtgnn_temporal_attn_prepare_slots(self.nbr, self.n_q, self.max_q, self.d, self.attn_save, self.ws_q,
+                                            stream=stream)
+
+    def prepare_weights(self, stream):
+        """The attention's weight copies (stacked K|V, padded merge layers): they read only the weights."""
+        M.mtgnn_temporal_attn_prepare_weights(self.ap, self.d, self.attn_save, stream=stream)
 
     def embed(self, lo, hi, queries_done=False):
         p, s = self.params, self.ts
         if not queries_done:
+            self.prepare_weights(s)
             self.queries(lo, hi, s)
         M.mtgnn_temporal_attn_prepared(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, self.neid,
                                        self.memory, self.x, p["time_w"], p["time_b"], self.ap, self.d, self.z,
@@ -218,6 +223,7 @@ class TGNStep:
             side.wait_event(self.q_fork)
             self.queries(elo, ehi, side)
             self.q_join.record(side)
+            self.prepare_weights(main)   # one launch here, so the second stream's chain is shorter
             if self.lag == 1 and self._pre == (mlo, mhi):
                 # this memory batch's aggregation and messages were built during the previous step's
                 # embedding, from the memory as it is now: only the GRU update is left

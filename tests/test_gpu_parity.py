@@ -196,7 +196,8 @@ def test_backward_overlap_bitwise():
 
 def test_forward_single_call_matches_prepare_prepared():
     """mtgnn_temporal_attn in one call gives bitwise the z and the save buffer of
-    mtgnn_temporal_attn_prepare followed by mtgnn_temporal_attn_prepared (bipartite stream)."""
+    mtgnn_temporal_attn_prepare followed by mtgnn_temporal_attn_prepared, and of the preparation's
+    two halves (slots, then weights) followed by _prepared (bipartite stream)."""
     from paper_2608_16305_amd import mtgnn as M
     from paper_2608_16305_amd.step import TGNStep
     w = workload(2)
@@ -210,17 +211,22 @@ def test_forward_single_call_matches_prepare_prepared():
     r.queries(*r.batch_range(b), None)
     p = r.params
     outs = []
-    for split in (False, True):
+    for split in (0, 1, 2):
         save = torch.zeros_like(r.attn_save)
         z = torch.zeros_like(r.z)
         args = (r.q_node, r.q_t, r.n_q, r.max_q, r.nbr, r.nt, r.neid, r.memory, r.x, p["time_w"], p["time_b"],
                 r.ap, r.d, z, save)
-        if split:
+        if split == 1:
             M.mtgnn_temporal_attn_prepare(r.nbr, r.n_q, r.max_q, r.ap, r.d, save, r.ws)
+            M.mtgnn_temporal_attn_prepared(*args)
+        elif split == 2:   # the two halves of the preparation, slots first
+            M.mtgnn_temporal_attn_prepare_slots(r.nbr, r.n_q, r.max_q, r.d, save, r.ws)
+            M.mtgnn_temporal_attn_prepare_weights(r.ap, r.d, save)
             M.mtgnn_temporal_attn_prepared(*args)
         else:
             M.mtgnn_temporal_attn(*args, r.ws)
         torch.cuda.synchronize()
         outs.append((to_np(z).copy(), to_np(save).copy()))
-    assert np.array_equal(outs[0][0].view(np.uint32), outs[1][0].view(np.uint32))
-    assert np.array_equal(outs[0][1], outs[1][1])
+    for o in outs[1:]:
+        assert np.array_equal(outs[0][0].view(np.uint32), o[0].view(np.uint32))
+        assert np.array_equal(outs[0][1], o[1])
