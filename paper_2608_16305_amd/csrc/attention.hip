@@ -622,7 +622,7 @@ __global__ void k_copy_cols(const float* __restrict__ S, int64_t lds, const int3
 }
 
 struct BwdWs {
-  float *dm1, *dm_in, *dattn, *dqv, *dKV, *tg_part, *S, *head, *tail, *dWkv, *dbkv;
+  float *dm1, *dm_in, *dattn, *dqv, *dKV, *tg_part, *tg_part2, *S, *head, *tail, *dWkv, *dbkv;
   uint32_t *keys, *vals;
   int32_t *seg_lo, *seg_hi, *row_of;
   char* scratch;          // split-K partials of the parameter-gradient products
@@ -645,7 +645,8 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   v.dattn = (float*)take(sizeof(float) * s.Q * s.da);
   v.dqv = (float*)take(sizeof(float) * s.Q * s.da);
   v.dKV = (float*)take(sizeof(float) * s.P * 2 * s.da);
-  v.tg_part = (float*)take(sizeof(float) * 2 * dtp * gemm_tg_blocks(s.P > s.Q ? s.P : s.Q));
+  v.tg_part = (float*)take(sizeof(float) * 2 * dtp * gemm_tg_blocks(s.Q));    // query rows
+  v.tg_part2 = (float*)take(sizeof(float) * 2 * dtp * gemm_tg_blocks(s.P));   // neighbour slots
   v.S = (float*)take(sizeof(float) * (max_rows > 0 ? max_rows : 1) * W);
   v.head = (float*)take(sizeof(float) * ntiles * W);
   v.tail = (float*)take(sizeof(float) * ntiles * W);
@@ -862,15 +863,15 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
   // weight gradients last, so that the d M' part (on its own stream when
   // overlapped) shares the GPU with the smaller products rather than with the
   // key/value weight gradient.
-  if (dt > 0) {   // phi(0) of the queries: delta = 0, so only the bias part is nonzero
+  if (dt > 0) {
+    // phi(0) of the queries (delta = 0, so only the bias part is nonzero), then phi(tau - t_j) of the
+    // neighbour slots with the saved sin(arg); one reduce of both partial sets (queries' sum first)
     MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,
                                  b.tg_part, s));
-    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, Q, n_q, 64 * G_WM, dt, d_time_w, d_time_b, false, s));
-  }
-  if (dt > 0) {   // phi(tau - t_j) of the neighbour slots, with the saved sin(arg)
     MTGNN_TRY(linear_dx_timegrad<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, P, sv.n_valid,
-                                             2 * da, dt, sv.sinv, sv.pair_delta, tw, tb, b.tg_part, s));
-    MTGNN_TRY(timegrad_reduce_blocks(b.tg_part, P, sv.n_valid, 64 * G_WM, dt, d_time_w, d_time_b, true, s));
+                                             2 * da, dt, sv.sinv, sv.pair_delta, tw, tb, b.tg_part2, s));
+    MTGNN_TRY(timegrad_reduce_blocks2(b.tg_part, Q, n_q, b.tg_part2, P, sv.n_valid, 64 * G_WM, dt, d_time_w,
+                                      d_time_b, s));
   }
   // weight gradients of the query, output and merge layers, one batch over the query rows
   {
@@ -880,7 +881,11 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
                              {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, sh.Dq, g->b_q}};
     MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
   }
-  // key/value projection over the compact slots (stacked [W_k; W_v])
+  // key/value projection over the compact slots (stacked [W_k; W_v]); the output-stationary kernel's
+  // reduce writes the W_k and W_v halves (rows < d_a, rows >= d_a) straight to their gradients
+  if (dw_rs_applicable(b.dKV, 2 * da, 2 * da, sv.kv_in, MTGNN_F32, sh.Dkv, (int)sh.Dkv))
+    return dw_rs_launch_rows2(b.dKV, 2 * da, 2 * da, sv.kv_in, sh.Dkv, (int)sh.Dkv, P, sv.n_valid, g->W_k, g->W_v,
+                              sh.Dkv, g->b_k, g->b_v, da, sc, scb, s);
   MTGNN_TRY(linear_dw<site::KvDw>(b.dKV, 2 * da, sv.kv_in, MTGNN_F32, sh.Dkv, b.dWkv, sh.Dkv, P, sv.n_valid, 2 * da,
                                   sh.Dkv, sc, scb, s, b.dbkv));
   k_split_kv_grads<<<(unsigned)cdiv((int64_t)da * sh.Dkv, 256), 256, 0, s>>>(b.dWkv, b.dbkv, da, sh.Dkv, g->W_k,

@@ -546,6 +546,11 @@ constexpr int G_WM = 1, G_NBUF = 2;
 __global__ void k_splitk_reduce(const float* __restrict__ part, int64_t split_stride, int nsplit, int64_t rows,
                                 int64_t cols, float* __restrict__ out, int64_t ldo, int64_t ones_col,
                                 float* __restrict__ col_out);
+// The same, with rows from row_split on written to out_hi / col_out_hi (row index minus row_split).
+__global__ void k_splitk_reduce_rows2(const float* __restrict__ part, int64_t split_stride, int nsplit, int64_t rows,
+                                      int64_t cols, float* __restrict__ out, float* __restrict__ out_hi, int64_t ldo,
+                                      int64_t ones_col, float* __restrict__ col_out, float* __restrict__ col_out_hi,
+                                      int64_t row_split);
 
 // Strip width for an output of N columns: equal strips of at most 128 columns
 // (32, 64, 112 or 128 wide).  Narrower strips need less LDS, so more blocks
@@ -805,6 +810,10 @@ bool dw_rs_applicable(const float* X, int64_t ldx, int nx, const void* Y, int y_
 mtgnn_status dw_rs_launch(const float* X, int64_t ldx, int nx, const float* Y, int64_t ldy, int ny, int64_t R,
                           const int32_t* R_dev, float* dW, int64_t lddw, float* db, void* ws, size_t ws_bytes,
                           hipStream_t s);
+// The same, with output rows from row_split on written to dW_hi / db_hi.
+mtgnn_status dw_rs_launch_rows2(const float* X, int64_t ldx, int nx, const float* Y, int64_t ldy, int ny, int64_t R,
+                                const int32_t* R_dev, float* dW, float* dW_hi, int64_t lddw, float* db, float* db_hi,
+                                int row_split, void* ws, size_t ws_bytes, hipStream_t s);
 
 template <class Site = site::Generic>
 mtgnn_status linear_dw(const float* dy, int64_t lddy, const void* x, int x_dtype, int64_t ldx, float* dW,

@@ -8,7 +8,9 @@ namespace {
 // 64 outputs per block; the 4 waves sum interleaved split slices, combined in a fixed order.
 __device__ __forceinline__ void splitk_reduce_body(const float* __restrict__ part, int64_t split_stride, int nsplit,
                                                    int64_t rows, int64_t cols, float* __restrict__ out, int64_t ldo,
-                                                   int64_t ones_col, float* __restrict__ col_out) {
+                                                   int64_t ones_col, float* __restrict__ col_out,
+                                                   float* __restrict__ out_hi = nullptr,
+                                                   float* __restrict__ col_out_hi = nullptr, int64_t row_split = 0) {
   __shared__ float red[4][64];
   const int64_t e = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
   const int g = threadIdx.x >> 6;
@@ -27,7 +29,13 @@ __device__ __forceinline__ void splitk_reduce_body(const float* __restrict__ par
   if (g != 0 || e >= rows * cols) return;
   const int l = threadIdx.x;
   s = ((red[0][l] + red[1][l]) + red[2][l]) + red[3][l];
-  const int64_t i = e / cols, j = e % cols;
+  int64_t i = e / cols;
+  const int64_t j = e % cols;
+  if (out_hi && i >= row_split) {   // rows from row_split on go to the second output pair
+    i -= row_split;
+    out = out_hi;
+    col_out = col_out_hi;
+  }
   if (j == ones_col) col_out[i] = s;
   else out[i * ldo + j] = s;
 }
@@ -61,6 +69,15 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
                                                        int nsplit, int64_t rows, int64_t cols, float* __restrict__ out,
                                                        int64_t ldo, int64_t ones_col, float* __restrict__ col_out) {
   splitk_reduce_body(part, split_stride, nsplit, rows, cols, out, ldo, ones_col, col_out);
+}
+
+__global__ __launch_bounds__(256) void k_splitk_reduce_rows2(const float* __restrict__ part, int64_t split_stride,
+                                                             int nsplit, int64_t rows, int64_t cols,
+                                                             float* __restrict__ out, float* __restrict__ out_hi,
+                                                             int64_t ldo, int64_t ones_col, float* __restrict__ col_out,
+                                                             float* __restrict__ col_out_hi, int64_t row_split) {
+  splitk_reduce_body(part, split_stride, nsplit, rows, cols, out, ldo, ones_col, col_out, out_hi, col_out_hi,
+                     row_split);
 }
 
 int gemm_strip_width(int64_t N) {

@@ -56,6 +56,12 @@ size_t dw_rs_ws_bytes(int nx, int ny) { return sizeof(float) * (size_t)DW_RS_MAX
 mtgnn_status dw_rs_launch(const float* X, int64_t ldx, int nx, const float* Y, int64_t ldy, int ny, int64_t R,
                           const int32_t* R_dev, float* dW, int64_t lddw, float* db, void* ws, size_t ws_bytes,
                           hipStream_t s) {
+  return dw_rs_launch_rows2(X, ldx, nx, Y, ldy, ny, R, R_dev, dW, nullptr, lddw, db, nullptr, nx, ws, ws_bytes, s);
+}
+
+mtgnn_status dw_rs_launch_rows2(const float* X, int64_t ldx, int nx, const float* Y, int64_t ldy, int ny, int64_t R,
+                                const int32_t* R_dev, float* dW, float* dW_hi, int64_t lddw, float* db, float* db_hi,
+                                int row_split, void* ws, size_t ws_bytes, hipStream_t s) {
   const size_t per = sizeof(float) * (size_t)nx * (ny + 1);
   int64_t grid = cu_count();
   if ((int64_t)(ws_bytes / per) < grid) grid = (int64_t)(ws_bytes / per);
@@ -70,7 +76,11 @@ mtgnn_status dw_rs_launch(const float* X, int64_t ldx, int nx, const float* Y, i
   }
   MTGNN_CHECK_LAUNCH("dw_rs");
   const int64_t outs = (int64_t)nx * (ny + 1);
-  k_splitk_reduce<<<(unsigned)cdiv(outs, 64), 256, 0, s>>>(part, outs, (int)grid, nx, ny + 1, dW, lddw, ny, db);
+  if (dW_hi)
+    k_splitk_reduce_rows2<<<(unsigned)cdiv(outs, 64), 256, 0, s>>>(part, outs, (int)grid, nx, ny + 1, dW, dW_hi, lddw,
+                                                                  ny, db, db_hi, row_split);
+  else
+    k_splitk_reduce<<<(unsigned)cdiv(outs, 64), 256, 0, s>>>(part, outs, (int)grid, nx, ny + 1, dW, lddw, ny, db);
   MTGNN_CHECK_LAUNCH("splitk_reduce");
   return MTGNN_OK;
 }

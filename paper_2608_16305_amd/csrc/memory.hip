@@ -338,11 +338,10 @@ __global__ __launch_bounds__(256) void k_timegrad_partial(const float* __restric
 // One block per column j: thread t sums chunks t, t + 256, ... of the partial
 // sums, then a fixed-order tree in LDS combines the 256 thread sums.  Chunks
 // beyond the device row count (ceil(rows / chunk_rows)) hold no partial.
-__global__ __launch_bounds__(256) void k_timegrad_reduce(const float* __restrict__ part, int64_t rows,
-                                                         const int32_t* __restrict__ rows_dev, int chunk_rows,
-                                                         int dt_dim, float* __restrict__ dw, float* __restrict__ db,
-                                                         int accumulate) {
-  __shared__ float sw[256], sb[256];
+// Column j's sums over the row chunks' partials (fixed tree order), by a block of 256 threads.
+__device__ __forceinline__ void timegrad_sum(const float* __restrict__ part, int64_t rows,
+                                             const int32_t* __restrict__ rows_dev, int chunk_rows, int dt_dim,
+                                             float* sw, float* sb, float& w, float& b) {
   const int j = blockIdx.x, t = threadIdx.x;
   const int64_t nch = cdiv(eff_count(rows, rows_dev), chunk_rows);
   float aw = 0.f, ab = 0.f;
@@ -360,9 +359,40 @@ __global__ __launch_bounds__(256) void k_timegrad_reduce(const float* __restrict
     }
     __syncthreads();
   }
-  if (t == 0) {
-    dw[j] = accumulate ? dw[j] + sw[0] : sw[0];
-    db[j] = accumulate ? db[j] + sb[0] : sb[0];
+  w = sw[0];
+  b = sb[0];
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void k_timegrad_reduce(const float* __restrict__ part, int64_t rows,
+                                                         const int32_t* __restrict__ rows_dev, int chunk_rows,
+                                                         int dt_dim, float* __restrict__ dw, float* __restrict__ db,
+                                                         int accumulate) {
+  __shared__ float sw[256], sb[256];
+  float w, b;
+  timegrad_sum(part, rows, rows_dev, chunk_rows, dt_dim, sw, sb, w, b);
+  const int j = blockIdx.x;
+  if (threadIdx.x == 0) {
+    dw[j] = accumulate ? dw[j] + w : w;
+    db[j] = accumulate ? db[j] + b : b;
+  }
+}
+
+// Two partial sets in one launch: d = (sum of the first) + (sum of the second), as two reduces
+// (the first overwriting, the second accumulating) would give.
+__global__ __launch_bounds__(256) void k_timegrad_reduce2(const float* __restrict__ p1, int64_t rows1,
+                                                          const int32_t* __restrict__ rows_dev1,
+                                                          const float* __restrict__ p2, int64_t rows2,
+                                                          const int32_t* __restrict__ rows_dev2, int chunk_rows,
+                                                          int dt_dim, float* __restrict__ dw, float* __restrict__ db) {
+  __shared__ float sw[256], sb[256];
+  float w1, b1, w2, b2;
+  timegrad_sum(p1, rows1, rows_dev1, chunk_rows, dt_dim, sw, sb, w1, b1);
+  timegrad_sum(p2, rows2, rows_dev2, chunk_rows, dt_dim, sw, sb, w2, b2);
+  const int j = blockIdx.x;
+  if (threadIdx.x == 0) {
+    dw[j] = w1 + w2;
+    db[j] = b1 + b2;
   }
 }
 
@@ -397,6 +427,16 @@ mtgnn_status timegrad_reduce_blocks(const float* part, int64_t rows, const int32
   k_timegrad_reduce<<<(unsigned)dt_dim, 256, 0, s>>>(part, rows, rows_dev, chunk_rows, dt_dim, dw, db,
                                                       accumulate ? 1 : 0);
   MTGNN_CHECK_LAUNCH("timegrad_reduce");
+  return MTGNN_OK;
+}
+
+mtgnn_status timegrad_reduce_blocks2(const float* p1, int64_t rows1, const int32_t* rows_dev1, const float* p2,
+                                     int64_t rows2, const int32_t* rows_dev2, int chunk_rows, int dt_dim, float* dw,
+                                     float* db, hipStream_t s) {
+  if (dt_dim <= 0) return MTGNN_OK;
+  k_timegrad_reduce2<<<(unsigned)dt_dim, 256, 0, s>>>(p1, rows1, rows_dev1, p2, rows2, rows_dev2, chunk_rows, dt_dim,
+                                                       dw, db);
+  MTGNN_CHECK_LAUNCH("timegrad_reduce2");
   return MTGNN_OK;
 }
 

@@ -41,6 +41,11 @@ size_t timegrad_ws_bytes(int64_t rows, int dt_dim);
 // (blocks = ceil(rows / chunk_rows), rows clamped by rows_dev) into dw, db.
 mtgnn_status timegrad_reduce_blocks(const float* part, int64_t rows, const int32_t* rows_dev, int chunk_rows,
                                     int dt_dim, float* dw, float* db, bool accumulate, hipStream_t s);
+// dw = (sum over p1's row chunks) + (sum over p2's), in one launch (the same bits as two reduces,
+// the first overwriting, the second accumulating).
+mtgnn_status timegrad_reduce_blocks2(const float* p1, int64_t rows1, const int32_t* rows_dev1, const float* p2,
+                                     int64_t rows2, const int32_t* rows_dev2, int chunk_rows, int dt_dim, float* dw,
+                                     float* db, hipStream_t s);
 mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* delta,
                            const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
                            bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
