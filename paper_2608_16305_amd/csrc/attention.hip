@@ -105,14 +105,10 @@ __global__ void k_pair_counts(const int32_t* __restrict__ nbr, const int32_t* __
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_attn_gather_q(const int32_t* __restrict__ q_node,
-                                                       const int32_t* __restrict__ n_q, int64_t max_q,
-                                                       const T* __restrict__ mem, const float* __restrict__ tw,
-                                                       const float* __restrict__ tb, int dm, int dt, int da, int bf16,
-                                                       float* __restrict__ q_in, float* __restrict__ m_in) {
-  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (q >= eff_count(max_q, n_q)) return;
+__device__ __forceinline__ void gather_q_body(int64_t q, int lane, const int32_t* __restrict__ q_node,
+                                              const T* __restrict__ mem, const float* __restrict__ tw,
+                                              const float* __restrict__ tb, int dm, int dt, int da, int bf16,
+                                              float* __restrict__ q_in, float* __restrict__ m_in) {
   const int64_t node = q_node[q];
   const int Dq = dm + dt;
   for (int c = lane; c < dm; c += 64) {
@@ -129,18 +125,14 @@ __global__ __launch_bounds__(256) void k_attn_gather_q(const int32_t* __restrict
 constexpr int GATHER_CHUNK = 8;
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_attn_gather_kv(const int32_t* __restrict__ nbr, const float* __restrict__ nt,
-                                                        const int32_t* __restrict__ neid,
-                                                        const float* __restrict__ q_t, const int32_t* __restrict__ n_q,
-                                                        int64_t max_q, int k, const int32_t* __restrict__ cnt,
-                                                        const int32_t* __restrict__ pair_off, const T* __restrict__ mem,
-                                                        const float* __restrict__ x, const float* __restrict__ tw,
-                                                        const float* __restrict__ tb, int dm, int de, int dt, int bf16,
-                                                        float* __restrict__ kv_in, float* __restrict__ sinv,
-                                                        int32_t* __restrict__ pair_nbr, float* __restrict__ pair_delta) {
-  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (q >= eff_count(max_q, n_q)) return;
+__device__ __forceinline__ void gather_kv_body(int64_t q, int lane, const int32_t* __restrict__ nbr,
+                                               const float* __restrict__ nt, const int32_t* __restrict__ neid,
+                                               const float* __restrict__ q_t, int k, const int32_t* __restrict__ cnt,
+                                               const int32_t* __restrict__ pair_off, const T* __restrict__ mem,
+                                               const float* __restrict__ x, const float* __restrict__ tw,
+                                               const float* __restrict__ tb, int dm, int de, int dt, int bf16,
+                                               float* __restrict__ kv_in, float* __restrict__ sinv,
+                                               int32_t* __restrict__ pair_nbr, float* __restrict__ pair_delta) {
   const int Dkv = dm + de + dt;
   const int c = cnt[q];
   const int64_t off = pair_off[q];
@@ -192,6 +184,26 @@ __global__ __launch_bounds__(256) void k_attn_gather_kv(const int32_t* __restric
       }
     }
   }
+}
+
+// Wave per query: its query-side input and its valid slots' rows, in one launch.
+struct GatherArgs {
+  const int32_t *q_node, *nbr, *neid, *n_q, *cnt, *pair_off;
+  const float *nt, *q_t, *x, *tw, *tb;
+  int64_t max_q;
+  int k, dm, de, dt, da, bf16;
+  float *q_in, *m_in, *kv_in, *sinv, *pair_delta;
+  int32_t* pair_nbr;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_attn_gather(GatherArgs a, const T* __restrict__ mem) {
+  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (q >= eff_count(a.max_q, a.n_q)) return;
+  gather_q_body<T>(q, lane, a.q_node, mem, a.tw, a.tb, a.dm, a.dt, a.da, a.bf16, a.q_in, a.m_in);
+  gather_kv_body<T>(q, lane, a.nbr, a.nt, a.neid, a.q_t, a.k, a.cnt, a.pair_off, mem, a.x, a.tw, a.tb, a.dm, a.de,
+                    a.dt, a.bf16, a.kv_in, a.sinv, a.pair_nbr, a.pair_delta);
 }
 
 constexpr int MAX_DH_CHUNKS = 2;   // head width <= 128
@@ -735,19 +747,12 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
   const int bf = d->dtype == MTGNN_BF16 ? 1 : 0;
   const int wt = d->dtype;
   const unsigned gq = (unsigned)cdiv(sh.Q, 4);
-  if (!bf) {
-    k_attn_gather_q<float><<<gq, 256, 0, s>>>(q_node, n_q, max_q, (const float*)memory, tw, tb, sh.dm, sh.dt, sh.da, 0,
-                                              sv.q_in, sv.m_in);
-    k_attn_gather_kv<float><<<gq, 256, 0, s>>>(nbr, nt, neid, q_t, n_q, max_q, sh.k, sv.cnt, sv.pair_off,
-                                               (const float*)memory, edge_feat, tw, tb, sh.dm, sh.de, sh.dt, 0,
-                                               sv.kv_in, sv.sinv, sv.pair_nbr, sv.pair_delta);
-  } else {
-    k_attn_gather_q<uint16_t><<<gq, 256, 0, s>>>(q_node, n_q, max_q, (const uint16_t*)memory, tw, tb, sh.dm, sh.dt,
-                                                 sh.da, 1, sv.q_in, sv.m_in);
-    k_attn_gather_kv<uint16_t><<<gq, 256, 0, s>>>(nbr, nt, neid, q_t, n_q, max_q, sh.k, sv.cnt, sv.pair_off,
-                                                  (const uint16_t*)memory, edge_feat, tw, tb, sh.dm, sh.de, sh.dt, 1,
-                                                  sv.kv_in, sv.sinv, sv.pair_nbr, sv.pair_delta);
-  }
+  const GatherArgs ga{q_node, nbr, neid, n_q, sv.cnt, sv.pair_off, nt, q_t, edge_feat, tw, tb, max_q, sh.k, sh.dm,
+                      sh.de, sh.dt, sh.da, bf, sv.q_in, sv.m_in, sv.kv_in, sv.sinv, sv.pair_delta, sv.pair_nbr};
+  if (!bf)
+    k_attn_gather<float><<<gq, 256, 0, s>>>(ga, (const float*)memory);
+  else
+    k_attn_gather<uint16_t><<<gq, 256, 0, s>>>(ga, (const uint16_t*)memory);
   MTGNN_CHECK_LAUNCH("attn_gather");
   MTGNN_TRY(linear_fwd(sv.q_in, MTGNN_F32, sh.Dq, p->W_q, wt, sh.Dq, p->b_q, sv.qv, sh.da, sh.Q, n_q, sh.da, sh.Dq,
                        false, s));

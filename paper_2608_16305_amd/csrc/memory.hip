@@ -238,7 +238,7 @@ __global__ void k_gather_rows(const T* __restrict__ mem, const int32_t* __restri
 
 // G = [gi | gh] (row stride 6 dm).  Writes the new memory row, last_update and the saved gates.
 template <typename T>
-__global__ void k_gru_gates(const float* __restrict__ G, const float* __restrict__ h_old,
+__global__ void k_gru_gates(const float* __restrict__ G, const float* __restrict__ h_old, int64_t ldh,
                             const int32_t* __restrict__ uniq, const int32_t* __restrict__ winner,
                             const float* __restrict__ t, const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
                             T* __restrict__ mem, float* __restrict__ lu, float* __restrict__ sr, float* __restrict__ sz,
@@ -252,7 +252,7 @@ __global__ void k_gru_gates(const float* __restrict__ G, const float* __restrict
   const float zz = sigmoidf_(g[dm + j] + g[4 * dm + j]);
   const float ghn = g[5 * dm + j];
   const float nn = tanhf(g[2 * dm + j] + rr * ghn);
-  const float h = h_old[e];
+  const float h = h_old[r * ldh + j];
   const float hn = (1.f - zz) * nn + zz * h;
   const int64_t node = uniq[r];
   Elem<T>::store(mem, node * dm + j, hn);
@@ -265,7 +265,7 @@ __global__ void k_gru_gates(const float* __restrict__ G, const float* __restrict
   }
 }
 
-__global__ void k_gru_bwd_gates(const float* __restrict__ dh, const float* __restrict__ h_old,
+__global__ void k_gru_bwd_gates(const float* __restrict__ dh, const float* __restrict__ h_old, int64_t ldh,
                                 const float* __restrict__ sr, const float* __restrict__ sz,
                                 const float* __restrict__ sn, const float* __restrict__ sghn,
                                 const int32_t* __restrict__ n_rows, int64_t max_rows, int dm, float* __restrict__ dgi,
@@ -274,7 +274,7 @@ __global__ void k_gru_bwd_gates(const float* __restrict__ dh, const float* __res
   const int64_t r = e / dm;
   if (r >= eff_count(max_rows, n_rows)) return;
   const int j = (int)(e % dm);
-  const float d = dh[e], rr = sr[e], zz = sz[e], nn = sn[e], ghn = sghn[e], h = h_old[e];
+  const float d = dh[e], rr = sr[e], zz = sz[e], nn = sn[e], ghn = sghn[e], h = h_old[r * ldh + j];
   const float dn_pre = d * (1.f - zz) * (1.f - nn * nn);
   const float dz_pre = d * (h - nn) * zz * (1.f - zz);
   const float dr_pre = dn_pre * ghn * rr * (1.f - rr);
@@ -535,7 +535,9 @@ mtgnn_status build_messages_impl(const mtgnn_batch* b, const int32_t* uniq, cons
   return MTGNN_OK;
 }
 
-// GRU save layout: h_old, r, z, n, ghn, each [max_rows, d_mem] float32.
+// GRU save layout: h_old, r, z, n, ghn, each [max_rows, d_mem] float32.  In float32 the h_old plane
+// stays unused: the message rows start with M[uniq[r]] (the same values), so both passes read h
+// from msg with its row stride instead of gathering it.
 size_t gru_save_bytes(const mtgnn_dims* d, int64_t max_rows) { return 5 * a256(sizeof(float) * max_rows * d->d_mem); }
 
 size_t gru_update_ws(const mtgnn_dims* d, int64_t max_rows) {
@@ -559,27 +561,27 @@ mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const in
     sghn = (float*)((char*)save + 4 * plane);
   }
   const unsigned gel = (unsigned)cdiv(max_rows * dm, 256);
-  if (d->dtype == MTGNN_F32)
-    k_gather_rows<float><<<gel, 256, 0, s>>>((const float*)memory, uniq, n_rows, max_rows, dm, h_old);
-  else
-    k_gather_rows<uint16_t><<<gel, 256, 0, s>>>((const uint16_t*)memory, uniq, n_rows, max_rows, dm, h_old);
-  MTGNN_CHECK_LAUNCH("gather_rows");
-  if (d->dtype == MTGNN_F32) {   // both products in one launch (their inputs share a type)
+  int64_t ldh = dm;
+  if (d->dtype == MTGNN_F32) {   // h = msg[:, :dm]; both products in one launch (their inputs share a type)
+    h_old = (float*)msg;
+    ldh = dmsg;
     const FwdProblem ps[2] = {{msg, dmsg, W_ih, dmsg, b_ih, G, 6 * dm, 3 * dm, dmsg},
-                              {h_old, dm, W_hh, dm, b_hh, G + 3 * dm, 6 * dm, 3 * dm, dm}};
+                              {msg, dmsg, W_hh, dm, b_hh, G + 3 * dm, 6 * dm, 3 * dm, dm}};
     MTGNN_TRY(linear_fwd_batch(ps, 2, max_rows, n_rows, MTGNN_F32, MTGNN_F32, s));
   } else {
+    k_gather_rows<uint16_t><<<gel, 256, 0, s>>>((const uint16_t*)memory, uniq, n_rows, max_rows, dm, h_old);
+    MTGNN_CHECK_LAUNCH("gather_rows");
     MTGNN_TRY(linear_fwd(msg, d->dtype, dmsg, W_ih, d->dtype, dmsg, b_ih, G, 6 * dm, max_rows, n_rows, 3 * dm, dmsg,
                          false, s));
     MTGNN_TRY(linear_fwd(h_old, MTGNN_F32, dm, W_hh, d->dtype, dm, b_hh, G + 3 * dm, 6 * dm, max_rows, n_rows, 3 * dm,
                          dm, false, s));
   }
   if (d->dtype == MTGNN_F32)
-    k_gru_gates<float><<<gel, 256, 0, s>>>(G, h_old, uniq, winner, b->t, n_rows, max_rows, dm, (float*)memory, lu, sr,
-                                           sz, sn, sghn);
+    k_gru_gates<float><<<gel, 256, 0, s>>>(G, h_old, ldh, uniq, winner, b->t, n_rows, max_rows, dm, (float*)memory,
+                                           lu, sr, sz, sn, sghn);
   else
-    k_gru_gates<uint16_t><<<gel, 256, 0, s>>>(G, h_old, uniq, winner, b->t, n_rows, max_rows, dm, (uint16_t*)memory,
-                                              lu, sr, sz, sn, sghn);
+    k_gru_gates<uint16_t><<<gel, 256, 0, s>>>(G, h_old, ldh, uniq, winner, b->t, n_rows, max_rows, dm,
+                                              (uint16_t*)memory, lu, sr, sz, sn, sghn);
   MTGNN_CHECK_LAUNCH("gru_gates");
   return MTGNN_OK;
 }
@@ -602,7 +604,9 @@ mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const voi
   if (ws_bytes < gru_update_bwd_ws(d, max_rows)) return MTGNN_EWORKSPACE;
   const int dm = d->d_mem, dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
   const size_t plane = a256(sizeof(float) * max_rows * dm);
-  const float* h_old = (const float*)save;
+  const bool f32 = d->dtype == MTGNN_F32;
+  const float* h_old = f32 ? (const float*)msg : (const float*)save;   // float32: h = msg[:, :dm]
+  const int64_t ldh = f32 ? dmsg : dm;
   const float* sr = (const float*)((const char*)save + plane);
   const float* sz = (const float*)((const char*)save + 2 * plane);
   const float* sn = (const float*)((const char*)save + 3 * plane);
@@ -613,12 +617,12 @@ mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const voi
   float* dgh = (float*)w;
   w += a256(sizeof(float) * max_rows * 3 * dm);
   const size_t rest = ws_bytes - (size_t)(w - (char*)ws);
-  k_gru_bwd_gates<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(d_mem, h_old, sr, sz, sn, sghn, n_rows, max_rows,
-                                                                        dm, dgi, dgh);
+  k_gru_bwd_gates<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(d_mem, h_old, ldh, sr, sz, sn, sghn, n_rows,
+                                                                        max_rows, dm, dgi, dgh);
   MTGNN_CHECK_LAUNCH("gru_bwd_gates");
   if (d->dtype == MTGNN_F32) {   // both weight gradients in one launch
     const DwProblem ps[2] = {{dgi, 3 * dm, msg, dmsg, dW_ih, dmsg, 3 * dm, dmsg, db_ih},
-                             {dgh, 3 * dm, h_old, dm, dW_hh, dm, 3 * dm, dm, db_hh}};
+                             {dgh, 3 * dm, h_old, ldh, dW_hh, dm, 3 * dm, dm, db_hh}};
     MTGNN_TRY(linear_dw_batch(ps, 2, max_rows, n_rows, MTGNN_F32, w, rest, s));
   } else {
     MTGNN_TRY(linear_dw(dgi, 3 * dm, msg, d->dtype, dmsg, dW_ih, dmsg, max_rows, n_rows, 3 * dm, dmsg, w, rest, s,
