@@ -445,18 +445,23 @@ struct SegCtx {
   int64_t ldq;
   const float* dkv;   // [P, 2 da] compact-slot gradient of (K, V)
   int dm, w2;         // w2 = 2 da ; row width W = dm + w2
-  float* S;           // [rows, W] complete sums
+  float* S;           // [rows, W] complete sums (columns [0, dm) go to D instead)
+  float* D;           // [rows, dm] d M' itself: the dh_q sums land there, the dK|dV product adds to them
   float* head;        // [ntiles, W]
   float* tail;        // [ntiles, W]
   const int32_t* seg_lo;   // [rows] first sorted position of the row
   const int32_t* seg_hi;   // [rows] one past its last
 };
 
-__device__ __forceinline__ void seg_store(float* dst, const float* acc, int W, int lane) {
+// A complete row of sums: columns < dm to D, the rest to S.
+template <int NC>
+__device__ __forceinline__ void seg_store_row(const SegCtx& c, int64_t row, const float* acc, int lane) {
+  const int W = c.dm + c.w2;
 #pragma unroll
-  for (int i = 0; i < SEG_MAXC; ++i) {
+  for (int i = 0; i < NC; ++i) {
     const int col = lane + 64 * i;
-    if (col < W) dst[col] = acc[i];
+    if (col < c.dm) c.D[row * c.dm + col] = acc[i];
+    else if (col < W) c.S[row * W + col] = acc[i];
   }
 }
 
@@ -512,7 +517,11 @@ __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   auto flush = [&](int end) {
     const bool before = start == 0 && key_before == cur;
     const bool after = end == cnt && key_after == cur;
-    float* dst = before ? c.head + tile * W : (after ? c.tail + tile * W : c.S + (int64_t)cur * W);
+    if (!before && !after) {   // the whole segment is in this tile
+      seg_store_row<NC>(c, (int64_t)cur, acc, lane);
+      return;
+    }
+    float* dst = before ? c.head + tile * W : c.tail + tile * W;
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
       const int col = lane + 64 * i;
@@ -572,7 +581,7 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
     float z[SEG_MAXC];
 #pragma unroll
     for (int i = 0; i < SEG_MAXC; ++i) z[i] = 0.f;
-    seg_store(c.S + zr * W, z, W, lane);
+    seg_store_row<SEG_MAXC>(c, zr, z, lane);
   }
   // the rest depends on the block only (uniform branches around the barrier)
   if (blk >= ntiles) return;
@@ -621,16 +630,7 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
       acc[i] = tl[col] + sum;
     }
   }
-  seg_store(c.S + (int64_t)key * W, acc, W, lane);
-}
-
-__global__ void k_copy_cols(const float* __restrict__ S, int64_t lds, const int32_t* __restrict__ n_rows,
-                            int64_t max_rows, int cols, float* __restrict__ out, int64_t ldo) {
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t r = e / cols;
-  if (r >= eff_count(max_rows, n_rows)) return;
-  const int c = (int)(e % cols);
-  out[r * ldo + c] = S[r * lds + c];
+  seg_store_row<SEG_MAXC>(c, (int64_t)key, acc, lane);
 }
 
 struct BwdWs {
@@ -827,7 +827,7 @@ mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSav
     c.keys = (uint32_t*)skeys; c.vals = (uint32_t*)svals; c.n_occ = n_occ; c.sentinel = sentinel; c.max_q = max_q;
     c.seg_lo = b.seg_lo; c.seg_hi = b.seg_hi;
     c.dhq = b.dm_in + da; c.ldq = ldm; c.dkv = b.dKV; c.dm = dm; c.w2 = 2 * da;
-    c.S = b.S; c.head = b.head; c.tail = b.tail;
+    c.S = b.S; c.D = d_mem; c.head = b.head; c.tail = b.tail;
     const int64_t ntiles = cdiv(n_occ, SEG_TILE);
     {
       const unsigned gt = (unsigned)cdiv(ntiles, 4);
@@ -847,8 +847,6 @@ mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSav
     k_segsum_fixup<<<(unsigned)nfix, 64 * FIX_WAVES, 0, s>>>(c, n_rows, max_rows, ntiles);
     MTGNN_CHECK_LAUNCH("segsum_fixup");
     const int W = dm + 2 * da;
-    k_copy_cols<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(b.S, W, n_rows, max_rows, dm, d_mem, dm);
-    MTGNN_CHECK_LAUNCH("copy_cols");
     MTGNN_TRY(linear_dx(b.S + dm, W, sv.W_kv, wt, sh.Dkv, d_mem, dm, max_rows, n_rows, 2 * da, dm, true, s));
   }
   return MTGNN_OK;
