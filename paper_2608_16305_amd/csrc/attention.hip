@@ -55,7 +55,7 @@ AttnSave carve_save(void* base, const AttnShape& s) {
   // preparation carves with none)
   v.W_kv = take(s.esz * 2 * s.da * s.Dkv);
   v.b_kv = (float*)take(sizeof(float) * 2 * s.da);
-  v.merge_w = (float*)take(sizeof(float) * (s.esz == 4 ? merge_weights_floats(s.da, s.dm) : 1));
+  v.merge_w = (float*)take(sizeof(float) * (s.esz == 4 ? merge_weights_floats(s.da, s.dm, s.dt) : 1));
   v.cnt = (int32_t*)take(sizeof(int32_t) * s.Q);
   v.pair_off = (int32_t*)take(sizeof(int32_t) * s.Q);
   v.n_valid = (int32_t*)take(sizeof(int32_t));
@@ -695,12 +695,16 @@ mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const mtgnn_d
   const AttnShape sh(d, 0);
   const AttnSave sv = carve_save(save, sh);
   if (merge_fused_ok(d->dtype, sh.da, sh.dm)) {   // float32: one launch for every copy
-    const PlainCopy kv[4] = {{(const float*)p->W_k, (float*)sv.W_kv, sh.da, (int)sh.Dkv},
-                             {(const float*)p->W_v, (float*)sv.W_kv + (size_t)sh.da * sh.Dkv, sh.da, (int)sh.Dkv},
-                             {p->b_k, sv.b_kv, 1, sh.da},
-                             {p->b_v, sv.b_kv + sh.da, 1, sh.da}};
+    PadCopy ex[6] = {plain_copy((const float*)p->W_k, (float*)sv.W_kv, sh.da, (int)sh.Dkv),
+                     plain_copy((const float*)p->W_v, (float*)sv.W_kv + (size_t)sh.da * sh.Dkv, sh.da, (int)sh.Dkv),
+                     plain_copy(p->b_k, sv.b_kv, 1, sh.da), plain_copy(p->b_v, sv.b_kv + sh.da, 1, sh.da)};
+    int n_ex = 4;
+    if (qproj_fused_ok(d->dtype, sh.da, sh.dm, sh.dt)) {
+      ex[n_ex++] = qproj_copy((const float*)p->W_q, sh.da, sh.dm, sh.dt, sv.merge_w, 0);
+      ex[n_ex++] = qproj_copy((const float*)p->W_q, sh.da, sh.dm, sh.dt, sv.merge_w, 1);
+    }
     return merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm, sv.merge_w,
-                         s, kv, 4);
+                         s, ex, n_ex);
   }
   const int64_t wkv = (int64_t)sh.da * sh.Dkv;
   if (d->dtype == MTGNN_F32)
@@ -754,8 +758,11 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
   else
     k_attn_gather<uint16_t><<<gq, 256, 0, s>>>(ga, (const uint16_t*)memory);
   MTGNN_CHECK_LAUNCH("attn_gather");
-  MTGNN_TRY(linear_fwd(sv.q_in, MTGNN_F32, sh.Dq, p->W_q, wt, sh.Dq, p->b_q, sv.qv, sh.da, sh.Q, n_q, sh.da, sh.Dq,
-                       false, s));
+  if (qproj_fused_ok(d->dtype, sh.da, sh.dm, sh.dt))
+    MTGNN_TRY(qproj_fwd_fused(sv.q_in, sv.merge_w, p->b_q, sv.qv, n_q, max_q, sh.da, sh.dm, sh.dt, s));
+  else
+    MTGNN_TRY(linear_fwd(sv.q_in, MTGNN_F32, sh.Dq, p->W_q, wt, sh.Dq, p->b_q, sv.qv, sh.da, sh.Q, n_q, sh.da, sh.Dq,
+                         false, s));
   MTGNN_TRY(linear_fwd<site::KvProj>(sv.kv_in, MTGNN_F32, sh.Dkv, sv.W_kv, wt, sh.Dkv, sv.b_kv, sv.KV, 2 * sh.da,
                                      sh.P, sv.n_valid, 2 * sh.da, sh.Dkv, false, s));
   {
@@ -959,7 +966,10 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     }
     MTGNN_CHECK_LAUNCH("attn_core_bwd");
     // query projection, data gradient: dhq += dqv W_q[:, :dm] (the last input of the d M' grouping)
-    MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
+    if (qproj_fused_ok(wt, da, dm, sh.dt))
+      MTGNN_TRY(qproj_dx_fused(b.dqv, sv.merge_w, b.dm_in, ldm, n_q, max_q, da, dm, sh.dt, s));
+    else
+      MTGNN_TRY(linear_dx(b.dqv, da, p->W_q, wt, sh.Dq, b.dm_in + da, ldm, Q, n_q, da, dm, true, s));
     return MTGNN_OK;
   };
   if (const mtgnn_status st1 = chain(); st1 != MTGNN_OK) {

@@ -203,8 +203,8 @@ __global__ __launch_bounds__(64 * MW) void k_merge_bwd(const float* __restrict__
 }
 
 // Zero-padded copies of the merge weights: dst[r][c] = W[r][c] (or W[c][r] for a transposed copy) for r < n,
-// c < k, else 0.  blockIdx.y selects the copy (the extra ones are plain: rows = n, cols = k).
-constexpr int PREP_MAX = 10;   // the six merge copies and up to four extra plain copies
+// c < k, else 0.  blockIdx.y selects the copy.
+constexpr int PREP_MAX = 12;   // the six merge copies and up to six extra copies
 struct PrepArgs {
   const float* src[PREP_MAX];
   float* dst[PREP_MAX];
@@ -239,19 +239,120 @@ struct PackLayout {
   }
 };
 
+// The query projection's padded copies, after the merge copies: W_q (d_a rows, D_q = d_m + d_t columns)
+// and W_q[:, :d_m]^T (d_m rows, d_a columns).
+struct QLayout {
+  int na, kq, nm;
+  int rows[2], cols[2];
+  size_t off[3];
+  QLayout(int da, int dm, int dt) {
+    na = (int)cdiv(da, 16);
+    kq = (int)cdiv(dm + dt, 16);
+    nm = (int)cdiv(dm, 16);
+    auto R = [](int nct) { return 16 * MW * (int)cdiv(nct, MW); };
+    rows[0] = R(na);
+    cols[0] = 16 * kq;
+    rows[1] = R(nm);
+    cols[1] = 16 * na;
+    off[0] = PackLayout(da, dm).off[6];
+    off[1] = off[0] + (size_t)rows[0] * cols[0];
+    off[2] = off[1] + (size_t)rows[1] * cols[1];
+  }
+};
+
+// qv = W_q x + b_q over 16-row tiles of the query inputs x = [M[q] || phi(0)] (row stride D_q).
+template <int NA, int KQ>
+__global__ __launch_bounds__(64 * MW) void k_qproj_fwd(const float* __restrict__ q_in, const float* __restrict__ Wq,
+                                                       const float* __restrict__ bq, float* __restrict__ qv,
+                                                       const int32_t* __restrict__ n_q, int64_t max_q, int da, int Dq) {
+  __shared__ __attribute__((aligned(16))) float X0[16 * XS];
+  const int64_t M = eff_count(max_q, n_q);
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= M) return;   // block-uniform
+  zero_cols(X0, Dq, 16 * KQ);
+  load_rows(X0, 0, q_in, Dq, Dq, r0, M);
+  __syncthreads();
+  f32x4 acc[Tiles<NA>::per_wave];
+  layer<NA, KQ>(X0, Wq, acc);
+  each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+    if (ok) qv[(r0 + i) * da + j] = v + bq[j];
+  });
+}
+
+// dm_in[:, da:] += dqv W_q[:, :dm] (the memory part of the query input), WqT = W_q[:, :dm]^T padded.
+template <int NM, int NA>
+__global__ __launch_bounds__(64 * MW) void k_qproj_dx(const float* __restrict__ dqv, const float* __restrict__ WqT,
+                                                      float* __restrict__ dm_in, int64_t ldm,
+                                                      const int32_t* __restrict__ n_q, int64_t max_q, int da, int dm) {
+  __shared__ __attribute__((aligned(16))) float X0[16 * XS];
+  const int64_t M = eff_count(max_q, n_q);
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= M) return;   // block-uniform
+  zero_cols(X0, da, 16 * NA);
+  load_rows(X0, 0, dqv, da, da, r0, M);
+  __syncthreads();
+  f32x4 acc[Tiles<NM>::per_wave];
+  layer<NM, NA>(X0, WqT, acc);
+  each_out<NM>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
+    if (ok) dm_in[(r0 + i) * ldm + da + j] += v;
+  });
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
 
 }  // namespace
+
+bool qproj_fused_ok(int dtype, int da, int dm, int dt) {
+  if (!merge_fused_ok(dtype, da, dm) || dt % 4 != 0) return false;
+  const QLayout L(da, dm, dt);
+  return (L.na == 7 && L.kq == 13 && L.nm == 7) || (L.na == 2 && L.kq == 4 && L.nm == 2);
+}
 
 bool merge_fused_ok(int dtype, int da, int dm) {
   const int na = (int)cdiv(da, 16), ns = (int)cdiv(da + dm, 16);
   return dtype == MTGNN_F32 && da % 4 == 0 && dm % 4 == 0 && ((na == 7 && ns == 13) || (na == 2 && ns == 4));
 }
 
-size_t merge_weights_floats(int da, int dm) { return PackLayout(da, dm).off[6]; }
+size_t merge_weights_floats(int da, int dm, int dt) {
+  return qproj_fused_ok(MTGNN_F32, da, dm, dt) ? QLayout(da, dm, dt).off[2] : PackLayout(da, dm).off[6];
+}
+
+PadCopy qproj_copy(const float* Wq, int da, int dm, int dt, float* Wp, int which) {
+  const QLayout L(da, dm, dt);
+  if (which == 0) return PadCopy{Wq, Wp + L.off[0], L.rows[0], L.cols[0], da, dm + dt, dm + dt, 0};
+  return PadCopy{Wq, Wp + L.off[1], L.rows[1], L.cols[1], dm, da, dm + dt, 1};
+}
+
+mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* bq, float* qv, const int32_t* n_q,
+                             int64_t max_q, int da, int dm, int dt, hipStream_t s) {
+  if (max_q <= 0) return MTGNN_OK;
+  if (!aligned16(q_in) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
+  const QLayout L(da, dm, dt);
+  const unsigned grid = (unsigned)cdiv(max_q, 16);
+  if (L.na == 7)
+    k_qproj_fwd<7, 13><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], bq, qv, n_q, max_q, da, dm + dt);
+  else
+    k_qproj_fwd<2, 4><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], bq, qv, n_q, max_q, da, dm + dt);
+  MTGNN_CHECK_LAUNCH("qproj_fwd");
+  return MTGNN_OK;
+}
+
+mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int64_t ldm, const int32_t* n_q,
+                            int64_t max_q, int da, int dm, int dt, hipStream_t s) {
+  if (max_q <= 0) return MTGNN_OK;
+  if (!aligned16(dqv) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
+  const QLayout L(da, dm, dt);
+  const unsigned grid = (unsigned)cdiv(max_q, 16);
+  if (L.na == 7)
+    k_qproj_dx<7, 7><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
+  else
+    k_qproj_dx<2, 2><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
+  MTGNN_CHECK_LAUNCH("qproj_dx");
+  return MTGNN_OK;
+}
 
 mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
-                           hipStream_t s, const PlainCopy* extra, int n_extra) {
+                           hipStream_t s, const PadCopy* extra, int n_extra) {
   if (n_extra < 0 || n_extra > PREP_MAX - 6) return MTGNN_EINVAL;
   const PackLayout L(da, dm);
   const int ldm = da + dm;
@@ -275,9 +376,12 @@ mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, in
     const int m = 6 + x;
     a.src[m] = extra[x].src;
     a.dst[m] = extra[x].dst;
-    a.rows[m] = a.n[m] = extra[x].rows;
-    a.cols[m] = a.k[m] = a.ld[m] = extra[x].cols;
-    a.tr[m] = 0;
+    a.rows[m] = extra[x].rows;
+    a.cols[m] = extra[x].cols;
+    a.n[m] = extra[x].n;
+    a.k[m] = extra[x].k;
+    a.ld[m] = extra[x].ld;
+    a.tr[m] = extra[x].tr;
     most = std::max<int64_t>(most, (int64_t)extra[x].rows * extra[x].cols);
   }
   k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), (unsigned)(6 + n_extra)), 256, 0, s>>>(a);

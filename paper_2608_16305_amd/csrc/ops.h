@@ -62,15 +62,27 @@ mtgnn_status build_csr_impl(const int32_t* src, const int32_t* dst, const float*
 // attention
 // Fused merge-layer chains (merge.hip): float32 and the attention / memory widths they are built for.
 bool merge_fused_ok(int dtype, int da, int dm);
-size_t merge_weights_floats(int da, int dm);
-struct PlainCopy {   // dst[rows x cols] = src[rows x cols], both contiguous
+size_t merge_weights_floats(int da, int dm, int dt);
+// dst[rows x cols] (contiguous): dst[r][c] = src[r * ld + c] (tr: src[c * ld + r]) for r < n, c < k, else 0.
+struct PadCopy {
   const float* src;
   float* dst;
-  int rows, cols;
+  int rows, cols, n, k, ld, tr;
 };
-// One launch: the padded merge copies, then the extra plain copies (at most four).
+inline PadCopy plain_copy(const float* src, float* dst, int rows, int cols) {
+  return PadCopy{src, dst, rows, cols, rows, cols, cols, 0};
+}
+// One launch: the padded merge copies, then the extra copies (at most six).
 mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
-                           hipStream_t s, const PlainCopy* extra = nullptr, int n_extra = 0);
+                           hipStream_t s, const PadCopy* extra = nullptr, int n_extra = 0);
+// The query projection on the same machinery (float32, the widths qproj_fused_ok accepts); its padded
+// copies (qproj_copy 0: W_q, 1: W_q[:, :dm]^T) follow the merge copies in the same buffer.
+bool qproj_fused_ok(int dtype, int da, int dm, int dt);
+PadCopy qproj_copy(const float* Wq, int da, int dm, int dt, float* Wp, int which);
+mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* bq, float* qv, const int32_t* n_q,
+                             int64_t max_q, int da, int dm, int dt, hipStream_t s);
+mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int64_t ldm, const int32_t* n_q,
+                            int64_t max_q, int da, int dm, int dt, hipStream_t s);
 mtgnn_status merge_fwd_fused(const float* attn, float* m_in, const float* Wp, const float* bo, const float* b1,
                              const float* b2, float* m1, float* a1, float* z, const int32_t* n_q, int64_t max_q,
                              int da, int dm, hipStream_t s);
