@@ -873,15 +873,20 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
   // weight gradients last, so that the d M' part (on its own stream when
   // overlapped) shares the GPU with the smaller products rather than with the
   // key/value weight gradient.
+  // Time-encoder gradient: phi(tau - t_j) of the neighbour slots (with the saved sin(arg)), and phi(0)
+  // of the queries.  In float32 the queries' share is closed-form from the query projection's bias
+  // gradient (their delta is 0), added in the reduce after the weight-gradient batch; otherwise it
+  // is a product of its own (its w part is zero, its b part is not).
+  const bool q_closed = wt == MTGNN_F32;
   if (dt > 0) {
-    // phi(0) of the queries (delta = 0, so only the bias part is nonzero), then phi(tau - t_j) of the
-    // neighbour slots with the saved sin(arg); one reduce of both partial sets (queries' sum first)
-    MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,
-                                 b.tg_part, s));
+    if (!q_closed)
+      MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,
+                                   b.tg_part, s));
     MTGNN_TRY(linear_dx_timegrad<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, P, sv.n_valid,
                                              2 * da, dt, sv.sinv, sv.pair_delta, tw, tb, b.tg_part2, s));
-    MTGNN_TRY(timegrad_reduce_blocks2(b.tg_part, Q, n_q, b.tg_part2, P, sv.n_valid, 64 * G_WM, dt, d_time_w,
-                                      d_time_b, s));
+    if (!q_closed)
+      MTGNN_TRY(timegrad_reduce_blocks2(b.tg_part, Q, n_q, b.tg_part2, P, sv.n_valid, 64 * G_WM, dt, d_time_w,
+                                        d_time_b, s));
   }
   // weight gradients of the query, output and merge layers, one batch over the query rows
   {
@@ -891,6 +896,9 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
                              {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, sh.Dq, g->b_q}};
     MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
   }
+  if (dt > 0 && q_closed)
+    MTGNN_TRY(timegrad_reduce_slots_q(b.tg_part2, P, sv.n_valid, 64 * G_WM, dt, g->b_q, (const float*)p->W_q, sh.Dq,
+                                      dm, da, tw, tb, d_time_w, d_time_b, s));
   // key/value projection over the compact slots (stacked [W_k; W_v]); the output-stationary kernel's
   // reduce writes the W_k and W_v halves (rows < d_a, rows >= d_a) straight to their gradients
   if (dw_rs_applicable(b.dKV, 2 * da, 2 * da, sv.kv_in, MTGNN_F32, sh.Dkv, (int)sh.Dkv))

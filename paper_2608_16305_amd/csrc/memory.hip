@@ -378,6 +378,34 @@ __global__ __launch_bounds__(256) void k_timegrad_reduce(const float* __restrict
   }
 }
 
+// The neighbour slots' partial sums plus the queries' share, which is closed-form: a query's time
+// input is phi(0) (delta = 0), so its w-gradient is zero and its b-gradient in column j is
+// -sin(b_j) sum_i dphi_ij = -sin(b_j) sum_a (sum_i dqv_ia) Wq[a][col0 + j], with sum_i dqv_ia the
+// query projection's bias gradient dbq.
+__global__ __launch_bounds__(256) void k_timegrad_reduce_q(const float* __restrict__ part, int64_t rows,
+                                                           const int32_t* __restrict__ rows_dev, int chunk_rows,
+                                                           int dt_dim, const float* __restrict__ dbq,
+                                                           const float* __restrict__ Wq, int64_t ldw, int col0, int da,
+                                                           const float* __restrict__ tw, const float* __restrict__ tb,
+                                                           float* __restrict__ dw, float* __restrict__ db) {
+  __shared__ float sw[256], sb[256];
+  float w, b;
+  timegrad_sum(part, rows, rows_dev, chunk_rows, dt_dim, sw, sb, w, b);
+  const int j = blockIdx.x, t = threadIdx.x;
+  float m = 0.f;
+  for (int a = t; a < da; a += 256) m += dbq[a] * Wq[(int64_t)a * ldw + col0 + j];
+  sw[t] = m;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) sw[t] += sw[t + o];
+    __syncthreads();
+  }
+  if (t == 0) {
+    dw[j] = w;
+    db[j] = -sinf(time_arg(tw[j], 0.f, tb[j])) * sw[0] + b;
+  }
+}
+
 // Two partial sets in one launch: d = (sum of the first) + (sum of the second), as two reduces
 // (the first overwriting, the second accumulating) would give.
 __global__ __launch_bounds__(256) void k_timegrad_reduce2(const float* __restrict__ p1, int64_t rows1,
@@ -427,6 +455,16 @@ mtgnn_status timegrad_reduce_blocks(const float* part, int64_t rows, const int32
   k_timegrad_reduce<<<(unsigned)dt_dim, 256, 0, s>>>(part, rows, rows_dev, chunk_rows, dt_dim, dw, db,
                                                       accumulate ? 1 : 0);
   MTGNN_CHECK_LAUNCH("timegrad_reduce");
+  return MTGNN_OK;
+}
+
+mtgnn_status timegrad_reduce_slots_q(const float* part, int64_t rows, const int32_t* rows_dev, int chunk_rows,
+                                     int dt_dim, const float* dbq, const float* Wq, int64_t ldw, int col0, int da,
+                                     const float* tw, const float* tb, float* dw, float* db, hipStream_t s) {
+  if (dt_dim <= 0) return MTGNN_OK;
+  k_timegrad_reduce_q<<<(unsigned)dt_dim, 256, 0, s>>>(part, rows, rows_dev, chunk_rows, dt_dim, dbq, Wq, ldw, col0,
+                                                        da, tw, tb, dw, db);
+  MTGNN_CHECK_LAUNCH("timegrad_reduce_q");
   return MTGNN_OK;
 }
 

@@ -46,6 +46,11 @@ mtgnn_status timegrad_reduce_blocks(const float* part, int64_t rows, const int32
 mtgnn_status timegrad_reduce_blocks2(const float* p1, int64_t rows1, const int32_t* rows_dev1, const float* p2,
                                      int64_t rows2, const int32_t* rows_dev2, int chunk_rows, int dt_dim, float* dw,
                                      float* db, hipStream_t s);
+// dw = the slots' sum; db = the slots' sum + the queries' closed-form share (their time input is
+// phi(0)): -sin(b_j) sum_a dbq[a] Wq[a * ldw + col0 + j] (float32 weights).
+mtgnn_status timegrad_reduce_slots_q(const float* part, int64_t rows, const int32_t* rows_dev, int chunk_rows,
+                                     int dt_dim, const float* dbq, const float* Wq, int64_t ldw, int col0, int da,
+                                     const float* tw, const float* tb, float* dw, float* db, hipStream_t s);
 mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* delta,
                            const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
                            bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
