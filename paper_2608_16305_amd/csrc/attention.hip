@@ -695,13 +695,16 @@ mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const mtgnn_d
   const AttnShape sh(d, 0);
   const AttnSave sv = carve_save(save, sh);
   if (merge_fused_ok(d->dtype, sh.da, sh.dm)) {   // float32: one launch for every copy
-    PadCopy ex[6] = {plain_copy((const float*)p->W_k, (float*)sv.W_kv, sh.da, (int)sh.Dkv),
+    PadCopy ex[8] = {plain_copy((const float*)p->W_k, (float*)sv.W_kv, sh.da, (int)sh.Dkv),
                      plain_copy((const float*)p->W_v, (float*)sv.W_kv + (size_t)sh.da * sh.Dkv, sh.da, (int)sh.Dkv),
                      plain_copy(p->b_k, sv.b_kv, 1, sh.da), plain_copy(p->b_v, sv.b_kv + sh.da, 1, sh.da)};
     int n_ex = 4;
     if (qproj_fused_ok(d->dtype, sh.da, sh.dm, sh.dt)) {
       ex[n_ex++] = qproj_copy((const float*)p->W_q, sh.da, sh.dm, sh.dt, sv.merge_w, 0);
       ex[n_ex++] = qproj_copy((const float*)p->W_q, sh.da, sh.dm, sh.dt, sv.merge_w, 1);
+      for (int which = 0; which < 2; ++which)
+        ex[n_ex++] = dmem_copy((const float*)p->W_k, (const float*)p->W_v, sh.da, sh.dm, sh.dt, (int)sh.Dkv,
+                               sv.merge_w, which);
     }
     return merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm, sv.merge_w,
                          s, ex, n_ex);
@@ -854,7 +857,10 @@ mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSav
     k_segsum_fixup<<<(unsigned)nfix, 64 * FIX_WAVES, 0, s>>>(c, n_rows, max_rows, ntiles);
     MTGNN_CHECK_LAUNCH("segsum_fixup");
     const int W = dm + 2 * da;
-    MTGNN_TRY(linear_dx(b.S + dm, W, sv.W_kv, wt, sh.Dkv, d_mem, dm, max_rows, n_rows, 2 * da, dm, true, s));
+    if (qproj_fused_ok(wt, da, dm, sh.dt))
+      MTGNN_TRY(dmem_dx_fused(b.S, W, sv.merge_w, d_mem, n_rows, max_rows, da, dm, sh.dt, s));
+    else
+      MTGNN_TRY(linear_dx(b.S + dm, W, sv.W_kv, wt, sh.Dkv, d_mem, dm, max_rows, n_rows, 2 * da, dm, true, s));
   }
   return MTGNN_OK;
 }

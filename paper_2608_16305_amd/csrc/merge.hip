@@ -204,11 +204,11 @@ __global__ __launch_bounds__(64 * MW) void k_merge_bwd(const float* __restrict__
 
 // Zero-padded copies of the merge weights: dst[r][c] = W[r][c] (or W[c][r] for a transposed copy) for r < n,
 // c < k, else 0.  blockIdx.y selects the copy.
-constexpr int PREP_MAX = 12;   // the six merge copies and up to six extra copies
+constexpr int PREP_MAX = 14;   // the six merge copies and up to eight extra copies
 struct PrepArgs {
   const float* src[PREP_MAX];
   float* dst[PREP_MAX];
-  int rows[PREP_MAX], cols[PREP_MAX], n[PREP_MAX], k[PREP_MAX], ld[PREP_MAX], tr[PREP_MAX];
+  int rows[PREP_MAX], cols[PREP_MAX], n[PREP_MAX], k[PREP_MAX], ld[PREP_MAX], tr[PREP_MAX], ldd[PREP_MAX];
 };
 
 __global__ void k_merge_prepare(PrepArgs a) {
@@ -218,7 +218,7 @@ __global__ void k_merge_prepare(PrepArgs a) {
   const int r = (int)(e / a.cols[m]), c = (int)(e % a.cols[m]);
   float v = 0.f;
   if (r < a.n[m] && c < a.k[m]) v = a.tr[m] ? a.src[m][(int64_t)c * a.ld[m] + r] : a.src[m][(int64_t)r * a.ld[m] + c];
-  a.dst[m][e] = v;
+  a.dst[m][(int64_t)r * a.ldd[m] + c] = v;
 }
 
 // Layout of the padded copies in one buffer: forward W_o, W_1, W_2, then backward W_2^T, W_1^T, W_o^T.
@@ -240,23 +240,26 @@ struct PackLayout {
 };
 
 // The query projection's padded copies, after the merge copies: W_q (d_a rows, D_q = d_m + d_t columns)
-// and W_q[:, :d_m]^T (d_m rows, d_a columns).
+// and W_q[:, :d_m]^T (d_m rows, d_a columns);
+// and W_kv[:, :d_m]^T (d_m rows, 2 d_a columns: the d M' product over the summed dK|dV).
 struct QLayout {
-  int na, kq, nm;
-  int rows[2], cols[2];
-  size_t off[3];
+  int na, kq, nm, kk;
+  int rows[3], cols[3];
+  size_t off[4];
   QLayout(int da, int dm, int dt) {
     na = (int)cdiv(da, 16);
     kq = (int)cdiv(dm + dt, 16);
     nm = (int)cdiv(dm, 16);
+    kk = (int)cdiv(2 * da, 16);
     auto R = [](int nct) { return 16 * MW * (int)cdiv(nct, MW); };
     rows[0] = R(na);
     cols[0] = 16 * kq;
     rows[1] = R(nm);
     cols[1] = 16 * na;
+    rows[2] = R(nm);
+    cols[2] = 16 * kk;
     off[0] = PackLayout(da, dm).off[6];
-    off[1] = off[0] + (size_t)rows[0] * cols[0];
-    off[2] = off[1] + (size_t)rows[1] * cols[1];
+    for (int m = 0; m < 3; ++m) off[m + 1] = off[m] + (size_t)rows[m] * cols[m];
   }
 };
 
@@ -298,6 +301,27 @@ __global__ __launch_bounds__(64 * MW) void k_qproj_dx(const float* __restrict__ 
   });
 }
 
+// d_mem[:, :dm] += S[:, dm : dm + 2 da] W_kv[:, :dm] over 16-row tiles (S: the per-row sums of
+// [dh_q | dK | dV], row stride ldS; WkT = W_kv[:, :dm]^T padded).
+template <int NM, int KK>
+__global__ __launch_bounds__(64 * MW) void k_dmem_dx(const float* __restrict__ S, int64_t ldS,
+                                                     const float* __restrict__ WkT, float* __restrict__ d_mem,
+                                                     const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
+                                                     int w2) {
+  __shared__ __attribute__((aligned(16))) float X0[16 * XS];
+  const int64_t M = eff_count(max_rows, n_rows);
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= M) return;   // block-uniform
+  zero_cols(X0, w2, 16 * KK);
+  load_rows(X0, 0, S + dm, ldS, w2, r0, M);
+  __syncthreads();
+  f32x4 acc[Tiles<NM>::per_wave];
+  layer<NM, KK>(X0, WkT, acc);
+  each_out<NM>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
+    if (ok) d_mem[(r0 + i) * dm + j] += v;
+  });
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
 
 }  // namespace
@@ -305,7 +329,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
 bool qproj_fused_ok(int dtype, int da, int dm, int dt) {
   if (!merge_fused_ok(dtype, da, dm) || dt % 4 != 0) return false;
   const QLayout L(da, dm, dt);
-  return (L.na == 7 && L.kq == 13 && L.nm == 7) || (L.na == 2 && L.kq == 4 && L.nm == 2);
+  return (L.na == 7 && L.kq == 13 && L.nm == 7 && L.kk == 13) || (L.na == 2 && L.kq == 4 && L.nm == 2 && L.kk == 4);
 }
 
 bool merge_fused_ok(int dtype, int da, int dm) {
@@ -314,13 +338,35 @@ bool merge_fused_ok(int dtype, int da, int dm) {
 }
 
 size_t merge_weights_floats(int da, int dm, int dt) {
-  return qproj_fused_ok(MTGNN_F32, da, dm, dt) ? QLayout(da, dm, dt).off[2] : PackLayout(da, dm).off[6];
+  return qproj_fused_ok(MTGNN_F32, da, dm, dt) ? QLayout(da, dm, dt).off[3] : PackLayout(da, dm).off[6];
 }
 
 PadCopy qproj_copy(const float* Wq, int da, int dm, int dt, float* Wp, int which) {
   const QLayout L(da, dm, dt);
-  if (which == 0) return PadCopy{Wq, Wp + L.off[0], L.rows[0], L.cols[0], da, dm + dt, dm + dt, 0};
-  return PadCopy{Wq, Wp + L.off[1], L.rows[1], L.cols[1], dm, da, dm + dt, 1};
+  if (which == 0) return PadCopy{Wq, Wp + L.off[0], L.rows[0], L.cols[0], da, dm + dt, dm + dt, 0, 0};
+  return PadCopy{Wq, Wp + L.off[1], L.rows[1], L.cols[1], dm, da, dm + dt, 1, 0};
+}
+
+PadCopy dmem_copy(const float* Wk, const float* Wv, int da, int dm, int dt, int Dkv, float* Wp, int which) {
+  // the d M' product's W_kv[:, :dm]^T: its first d_a columns from W_k, the rest from W_v (and zeros)
+  const QLayout L(da, dm, dt);
+  float* base = Wp + L.off[2];
+  if (which == 0) return PadCopy{Wk, base, L.rows[2], da, dm, da, Dkv, 1, L.cols[2]};
+  return PadCopy{Wv, base + da, L.rows[2], L.cols[2] - da, dm, da, Dkv, 1, L.cols[2]};
+}
+
+mtgnn_status dmem_dx_fused(const float* S, int64_t ldS, const float* Wp, float* d_mem, const int32_t* n_rows,
+                           int64_t max_rows, int da, int dm, int dt, hipStream_t s) {
+  if (max_rows <= 0) return MTGNN_OK;
+  if (!aligned16(S) || !aligned16(Wp) || (dm * sizeof(float)) % 16 != 0 || ldS % 4 != 0) return MTGNN_EUNSUPPORTED;
+  const QLayout L(da, dm, dt);
+  const unsigned grid = (unsigned)cdiv(max_rows, 16);
+  if (L.nm == 7)
+    k_dmem_dx<7, 13><<<grid, 64 * MW, 0, s>>>(S, ldS, Wp + L.off[2], d_mem, n_rows, max_rows, dm, 2 * da);
+  else
+    k_dmem_dx<2, 4><<<grid, 64 * MW, 0, s>>>(S, ldS, Wp + L.off[2], d_mem, n_rows, max_rows, dm, 2 * da);
+  MTGNN_CHECK_LAUNCH("dmem_dx");
+  return MTGNN_OK;
 }
 
 mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* bq, float* qv, const int32_t* n_q,
@@ -370,6 +416,7 @@ mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, in
     a.k[m] = k[m];
     a.ld[m] = ld[m];
     a.tr[m] = tr[m];
+    a.ldd[m] = L.cols[m];
     most = std::max<int64_t>(most, (int64_t)L.rows[m] * L.cols[m]);
   }
   for (int x = 0; x < n_extra; ++x) {
@@ -382,6 +429,7 @@ mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, in
     a.k[m] = extra[x].k;
     a.ld[m] = extra[x].ld;
     a.tr[m] = extra[x].tr;
+    a.ldd[m] = extra[x].ldd > 0 ? extra[x].ldd : extra[x].cols;
     most = std::max<int64_t>(most, (int64_t)extra[x].rows * extra[x].cols);
   }
   k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), (unsigned)(6 + n_extra)), 256, 0, s>>>(a);

@@ -69,15 +69,16 @@ mtgnn_status build_csr_impl(const int32_t* src, const int32_t* dst, const float*
 bool merge_fused_ok(int dtype, int da, int dm);
 size_t merge_weights_floats(int da, int dm, int dt);
 // dst[rows x cols] (contiguous): dst[r][c] = src[r * ld + c] (tr: src[c * ld + r]) for r < n, c < k, else 0.
+// ldd: the destination's row stride (0: cols).
 struct PadCopy {
   const float* src;
   float* dst;
-  int rows, cols, n, k, ld, tr;
+  int rows, cols, n, k, ld, tr, ldd;
 };
 inline PadCopy plain_copy(const float* src, float* dst, int rows, int cols) {
-  return PadCopy{src, dst, rows, cols, rows, cols, cols, 0};
+  return PadCopy{src, dst, rows, cols, rows, cols, cols, 0, 0};
 }
-// One launch: the padded merge copies, then the extra copies (at most six).
+// One launch: the padded merge copies, then the extra copies (at most eight).
 mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
                            hipStream_t s, const PadCopy* extra = nullptr, int n_extra = 0);
 // The query projection on the same machinery (float32, the widths qproj_fused_ok accepts); its padded
@@ -88,6 +89,11 @@ mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* bq
                              int64_t max_q, int da, int dm, int dt, hipStream_t s);
 mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int64_t ldm, const int32_t* n_q,
                             int64_t max_q, int da, int dm, int dt, hipStream_t s);
+// The d M' product (d_mem += S[:, dm:] W_kv[:, :dm]) on the same machinery, for the shapes qproj_fused_ok
+// accepts; dmem_copy 0 / 1 are its padded weight's two halves (from W_k, from W_v).
+PadCopy dmem_copy(const float* Wk, const float* Wv, int da, int dm, int dt, int Dkv, float* Wp, int which);
+mtgnn_status dmem_dx_fused(const float* S, int64_t ldS, const float* Wp, float* d_mem, const int32_t* n_rows,
+                           int64_t max_rows, int da, int dm, int dt, hipStream_t s);
 mtgnn_status merge_fwd_fused(const float* attn, float* m_in, const float* Wp, const float* bo, const float* b1,
                              const float* b2, float* m1, float* a1, float* z, const int32_t* n_q, int64_t max_q,
                              int da, int dm, hipStream_t s);
