@@ -237,13 +237,26 @@ __global__ void k_gather_rows(const T* __restrict__ mem, const int32_t* __restri
 }
 
 // G = [gi | gh] (row stride 6 dm).  Writes the new memory row, last_update and the saved gates.
+// Optional side job (wt.dst set): the zero-padded W_ih[:, col0 : col0 + dt]^T for the backward's fused
+// time-feature gradient, written by every thread before the row test (grid-stride).
+struct GruWT {
+  const float* W_ih;
+  float* dst;
+  int rows, cols, dt, K, ld, col0;
+};
+
 template <typename T>
 __global__ void k_gru_gates(const float* __restrict__ G, const float* __restrict__ h_old, int64_t ldh,
                             const int32_t* __restrict__ uniq, const int32_t* __restrict__ winner,
                             const float* __restrict__ t, const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
                             T* __restrict__ mem, float* __restrict__ lu, float* __restrict__ sr, float* __restrict__ sz,
-                            float* __restrict__ sn, float* __restrict__ sghn) {
+                            float* __restrict__ sn, float* __restrict__ sghn, GruWT wt) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (wt.dst)
+    for (int64_t x = e; x < (int64_t)wt.rows * wt.cols; x += (int64_t)gridDim.x * blockDim.x) {
+      const int rr = (int)(x / wt.cols), cc = (int)(x % wt.cols);
+      wt.dst[x] = (rr < wt.dt && cc < wt.K) ? wt.W_ih[(int64_t)cc * wt.ld + wt.col0 + rr] : 0.f;
+    }
   const int64_t r = e / dm;
   if (r >= eff_count(max_rows, n_rows)) return;
   const int j = (int)(e % dm);
@@ -573,10 +586,14 @@ mtgnn_status build_messages_impl(const mtgnn_batch* b, const int32_t* uniq, cons
   return MTGNN_OK;
 }
 
-// GRU save layout: h_old, r, z, n, ghn, each [max_rows, d_mem] float32.  In float32 the h_old plane
+// GRU save layout: h_old, r, z, n, ghn, each [max_rows, d_mem] float32, then (float32) the padded
+// W_ih[:, 2 dm : 2 dm + dt]^T of the backward's fused time-feature gradient.  In float32 the h_old plane
 // stays unused: the message rows start with M[uniq[r]] (the same values), so both passes read h
 // from msg with its row stride instead of gathering it.
-size_t gru_save_bytes(const mtgnn_dims* d, int64_t max_rows) { return 5 * a256(sizeof(float) * max_rows * d->d_mem); }
+size_t gru_save_bytes(const mtgnn_dims* d, int64_t max_rows) {
+  const size_t wt = gru_dx_fused_ok(d->dtype, d->d_mem, d->d_time) ? gru_dx_weight_floats(d->d_mem, d->d_time) : 1;
+  return 5 * a256(sizeof(float) * max_rows * d->d_mem) + a256(sizeof(float) * wt);
+}
 
 size_t gru_update_ws(const mtgnn_dims* d, int64_t max_rows) {
   return a256(sizeof(float) * max_rows * 6 * d->d_mem) + a256(sizeof(float) * max_rows * d->d_mem);
@@ -614,12 +631,18 @@ mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const in
     MTGNN_TRY(linear_fwd(h_old, MTGNN_F32, dm, W_hh, d->dtype, dm, b_hh, G + 3 * dm, 6 * dm, max_rows, n_rows, 3 * dm,
                          dm, false, s));
   }
+  GruWT wt{};
+  if (save && gru_dx_fused_ok(d->dtype, dm, d->d_time)) {
+    const int kc = (int)cdiv(3 * dm, 16);
+    wt = GruWT{(const float*)W_ih, (float*)((char*)save + 5 * plane),
+               (int)(gru_dx_weight_floats(dm, d->d_time) / (16 * kc)), 16 * kc, d->d_time, 3 * dm, dmsg, 2 * dm};
+  }
   if (d->dtype == MTGNN_F32)
     k_gru_gates<float><<<gel, 256, 0, s>>>(G, h_old, ldh, uniq, winner, b->t, n_rows, max_rows, dm, (float*)memory,
-                                           lu, sr, sz, sn, sghn);
+                                           lu, sr, sz, sn, sghn, wt);
   else
     k_gru_gates<uint16_t><<<gel, 256, 0, s>>>(G, h_old, ldh, uniq, winner, b->t, n_rows, max_rows, dm,
-                                              (uint16_t*)memory, lu, sr, sz, sn, sghn);
+                                              (uint16_t*)memory, lu, sr, sz, sn, sghn, wt);
   MTGNN_CHECK_LAUNCH("gru_gates");
   return MTGNN_OK;
 }
@@ -668,6 +691,9 @@ mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const voi
     MTGNN_TRY(linear_dw(dgh, 3 * dm, h_old, MTGNN_F32, dm, dW_hh, dm, max_rows, n_rows, 3 * dm, dm, w, rest, s,
                         db_hh));
   }
+  if (dmsg_time && d->d_time > 0 && gru_dx_fused_ok(d->dtype, dm, d->d_time))
+    return gru_dx_fused(dgi, (const float*)((const char*)save + 5 * plane), dmsg_time, n_rows, max_rows, dm,
+                        d->d_time, s);
   if (dmsg_time && d->d_time > 0) {
     const size_t esz = d->dtype == MTGNN_F32 ? 4 : 2;
     const void* Wt = (const char*)W_ih + esz * (size_t)(2 * dm);   // columns [2 dm, 2 dm + d_time)

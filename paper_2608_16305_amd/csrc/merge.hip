@@ -33,7 +33,7 @@ template <int NCT> struct Tiles { static constexpr int per_wave = (NCT + MW - 1)
 // acc[u] (16 x 16 output tile t = wave + 4 u) += X[16 rows, 16 KC] B[16 t.., 16 KC]^T.  X: the block's LDS
 // tile (row stride XS, zero beyond the true width).  B: a zero-padded weight copy, 16 MW NU rows by 16 KC
 // columns, so every fragment load is in bounds and unconditional.
-template <int NCT, int KC>
+template <int NCT, int KC, int XSS = XS>
 __device__ __forceinline__ void layer(const float* X, const float* __restrict__ B, f32x4 (&acc)[Tiles<NCT>::per_wave]) {
   constexpr int NU = Tiles<NCT>::per_wave;
   constexpr int LDB = 16 * KC;
@@ -51,7 +51,7 @@ __device__ __forceinline__ void layer(const float* X, const float* __restrict__ 
 #pragma unroll
   for (int c = 0; c < KC; ++c) {
     if (c + PD < KC) load_b(c + PD);   // in flight while this chunk's MFMAs run
-    const float4 a = *reinterpret_cast<const float4*>(X + fr * XS + 16 * c + 4 * fg);
+    const float4 a = *reinterpret_cast<const float4*>(X + fr * XSS + 16 * c + 4 * fg);
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
       acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, bf[c][u].x, acc[u], 0, 0, 0);
@@ -64,6 +64,7 @@ __device__ __forceinline__ void layer(const float* X, const float* __restrict__ 
 }
 
 // rows r0 .. r0 + 15 (those < M) of a row-major [M, n] matrix into an LDS tile at column offset col0
+template <int XSS = XS>
 __device__ __forceinline__ void load_rows(float* X, int col0, const float* __restrict__ src, int64_t ld, int n,
                                           int64_t r0, int64_t M) {
   const int nq = n / 4;
@@ -71,12 +72,13 @@ __device__ __forceinline__ void load_rows(float* X, int col0, const float* __res
     const int r = e / nq, q = e % nq;
     const float4 v = r0 + r < M ? *reinterpret_cast<const float4*>(src + (r0 + r) * ld + 4 * q)
                                 : float4{0.f, 0.f, 0.f, 0.f};
-    *reinterpret_cast<float4*>(X + r * XS + col0 + 4 * q) = v;
+    *reinterpret_cast<float4*>(X + r * XSS + col0 + 4 * q) = v;
   }
 }
 
+template <int XSS = XS>
 __device__ __forceinline__ void zero_cols(float* X, int c0, int c1) {
-  for (int e = threadIdx.x; e < 16 * (c1 - c0); e += 64 * MW) X[(e / (c1 - c0)) * XS + c0 + e % (c1 - c0)] = 0.f;
+  for (int e = threadIdx.x; e < 16 * (c1 - c0); e += 64 * MW) X[(e / (c1 - c0)) * XSS + c0 + e % (c1 - c0)] = 0.f;
 }
 
 // Epilogue of a layer: f(i, j, row valid, value) for this wave's tiles, row 4 (l/16) + r, column 16 t + l%16
@@ -322,9 +324,54 @@ __global__ __launch_bounds__(64 * MW) void k_dmem_dx(const float* __restrict__ S
   });
 }
 
+// The GRU backward's time-feature gradient: dmsg_time = dgi W_ih[:, c0 : c0 + dt] over 16-row tiles of dgi
+// (3 dm wide); WT = W_ih[:, c0 : c0 + dt]^T zero-padded (gru_dx_weight_copy).
+constexpr int XS_GRU = 308;   // >= 304 (19 chunks of 16), XS_GRU / 4 odd
+
+template <int NT, int KC>
+__global__ __launch_bounds__(64 * MW) void k_gru_dx(const float* __restrict__ dgi, int64_t ldg,
+                                                    const float* __restrict__ WT, float* __restrict__ out, int dt,
+                                                    const int32_t* __restrict__ n_rows, int64_t max_rows, int K) {
+  __shared__ __attribute__((aligned(16))) float X0[16 * XS_GRU];
+  const int64_t M = eff_count(max_rows, n_rows);
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= M) return;   // block-uniform
+  zero_cols<XS_GRU>(X0, K, 16 * KC);
+  load_rows<XS_GRU>(X0, 0, dgi, ldg, K, r0, M);
+  __syncthreads();
+  f32x4 acc[Tiles<NT>::per_wave];
+  layer<NT, KC, XS_GRU>(X0, WT, acc);
+  each_out<NT>(acc, dt, r0, M, [&](int i, int j, bool ok, float v) {
+    if (ok) out[(r0 + i) * dt + j] = v;
+  });
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
 
 }  // namespace
+
+// Shapes of the fused GRU time-feature gradient: 3 dm in (288, 304] or (80, 96], dt tiles 7 or 2.
+bool gru_dx_fused_ok(int dtype, int dm, int dt) {
+  const int kc = (int)cdiv(3 * dm, 16), nt = (int)cdiv(dt, 16);
+  return dtype == MTGNN_F32 && dm % 4 == 0 && dt % 4 == 0 && ((kc == 19 && nt == 7) || (kc == 6 && nt == 2));
+}
+
+size_t gru_dx_weight_floats(int dm, int dt) {
+  return (size_t)16 * MW * cdiv(cdiv(dt, 16), MW) * 16 * cdiv(3 * dm, 16);
+}
+
+mtgnn_status gru_dx_fused(const float* dgi, const float* WT, float* dmsg_time, const int32_t* n_rows,
+                          int64_t max_rows, int dm, int dt, hipStream_t s) {
+  if (max_rows <= 0) return MTGNN_OK;
+  if (!aligned16(dgi) || !aligned16(WT)) return MTGNN_EUNSUPPORTED;
+  const unsigned grid = (unsigned)cdiv(max_rows, 16);
+  if (cdiv(3 * dm, 16) == 19)
+    k_gru_dx<7, 19><<<grid, 64 * MW, 0, s>>>(dgi, 3 * dm, WT, dmsg_time, dt, n_rows, max_rows, 3 * dm);
+  else
+    k_gru_dx<2, 6><<<grid, 64 * MW, 0, s>>>(dgi, 3 * dm, WT, dmsg_time, dt, n_rows, max_rows, 3 * dm);
+  MTGNN_CHECK_LAUNCH("gru_dx");
+  return MTGNN_OK;
+}
 
 bool qproj_fused_ok(int dtype, int da, int dm, int dt) {
   if (!merge_fused_ok(dtype, da, dm) || dt % 4 != 0) return false;

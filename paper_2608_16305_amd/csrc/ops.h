@@ -92,6 +92,12 @@ mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int
 // The d M' product (d_mem += S[:, dm:] W_kv[:, :dm]) on the same machinery, for the shapes qproj_fused_ok
 // accepts; dmem_copy 0 / 1 are its padded weight's two halves (from W_k, from W_v).
 PadCopy dmem_copy(const float* Wk, const float* Wv, int da, int dm, int dt, int Dkv, float* Wp, int which);
+// The GRU backward's time-feature gradient on the same machinery (float32; gru_dx_fused_ok shapes), from
+// W_ih[:, 2 dm : 2 dm + dt]^T zero-padded to gru_dx_weight_floats floats (written by the GRU update).
+bool gru_dx_fused_ok(int dtype, int dm, int dt);
+size_t gru_dx_weight_floats(int dm, int dt);
+mtgnn_status gru_dx_fused(const float* dgi, const float* WT, float* dmsg_time, const int32_t* n_rows,
+                          int64_t max_rows, int dm, int dt, hipStream_t s);
 mtgnn_status dmem_dx_fused(const float* S, int64_t ldS, const float* Wp, float* d_mem, const int32_t* n_rows,
                            int64_t max_rows, int da, int dm, int dt, hipStream_t s);
 mtgnn_status merge_fwd_fused(const float* attn, float* m_in, const float* Wp, const float* bo, const float* b1,
