@@ -93,23 +93,27 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile(const int32_t* __res
 // offsets go back through LDS and out coalesced.
 __device__ __forceinline__ int scan1_pad(int i) { return i + (i >> 5); }
 
+// ITEMS per thread (8, 16 or 32): the launcher takes the smallest that covers n, so a short scan does
+// not pay for the padding's LDS traffic.
+template <int ITEMS>
 __global__ __launch_bounds__(SCAN1_THREADS) void k_scan_one_block(const int32_t* __restrict__ in,
                                                                   int32_t* __restrict__ out, int64_t n,
                                                                   int32_t* __restrict__ total) {
-  __shared__ int buf[SCAN1_MAX + SCAN1_MAX / 32];
+  constexpr int CAP = SCAN1_THREADS * ITEMS;
+  __shared__ int buf[CAP + CAP / 32];
   __shared__ int wsum[SCAN1_THREADS / 64];
   const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
 #pragma unroll
-  for (int j = 0; j < SCAN1_ITEMS; ++j) {
+  for (int j = 0; j < ITEMS; ++j) {
     const int i = j * SCAN1_THREADS + t;
     buf[scan1_pad(i)] = i < n ? in[i] : 0;
   }
   __syncthreads();
-  int v[SCAN1_ITEMS];
+  int v[ITEMS];
   int s = 0;
 #pragma unroll
-  for (int j = 0; j < SCAN1_ITEMS; ++j) {
-    v[j] = buf[scan1_pad(t * SCAN1_ITEMS + j)];
+  for (int j = 0; j < ITEMS; ++j) {
+    v[j] = buf[scan1_pad(t * ITEMS + j)];
     s += v[j];
   }
   int inc = s;
@@ -127,13 +131,13 @@ __global__ __launch_bounds__(SCAN1_THREADS) void k_scan_one_block(const int32_t*
   }
   run += inc - s;
 #pragma unroll
-  for (int j = 0; j < SCAN1_ITEMS; ++j) {
-    buf[scan1_pad(t * SCAN1_ITEMS + j)] = run;
+  for (int j = 0; j < ITEMS; ++j) {
+    buf[scan1_pad(t * ITEMS + j)] = run;
     run += v[j];
   }
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < SCAN1_ITEMS; ++j) {
+  for (int j = 0; j < ITEMS; ++j) {
     const int i = j * SCAN1_THREADS + t;
     if (i < n) out[i] = buf[scan1_pad(i)];
   }
@@ -273,7 +277,12 @@ mtgnn_status scan_exclusive(const int32_t* in, int32_t* out, int64_t n, int32_t*
     return MTGNN_OK;
   }
   if (n <= SCAN1_MAX) {
-    k_scan_one_block<<<1, SCAN1_THREADS, 0, s>>>(in, out, n, total);
+    if (n <= SCAN1_THREADS * 8)
+      k_scan_one_block<8><<<1, SCAN1_THREADS, 0, s>>>(in, out, n, total);
+    else if (n <= SCAN1_THREADS * 16)
+      k_scan_one_block<16><<<1, SCAN1_THREADS, 0, s>>>(in, out, n, total);
+    else
+      k_scan_one_block<SCAN1_ITEMS><<<1, SCAN1_THREADS, 0, s>>>(in, out, n, total);
     MTGNN_CHECK_LAUNCH("scan_one_block");
     return MTGNN_OK;
   }
