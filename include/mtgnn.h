@@ -290,6 +290,36 @@ mtgnn_status mtgnn_temporal_attn_bwd_overlap(const int32_t* q_node, const float*
                                              float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
                                              hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join);
 
+/* Row a7, the d_mem grouping ahead of the gradients: every occurrence of an updated node among the
+ * queries and the valid neighbour slots, keyed by its updated row, sorted stably by key, and each
+ * row's segment bounds, written into ws (the backward's workspace, mtgnn_workspace_bytes for
+ * MTGNN_OP_TEMPORAL_ATTN_BWD).  It reads only q_node / n_q, the sampled neighbours nbr
+ * [max_q, k], the slot counts and offsets that the attention's preparation left in save, and the
+ * updated rows uniq / n_rows, so it may run before the forward's gather and long before any
+ * gradient exists; the caller runs it on the stream it will pass as dmem_stream to
+ * mtgnn_temporal_attn_bwd_grouped, which consumes it.  Between the two calls nothing may write
+ * ws, save's slot counts, uniq or n_rows.  max_rows == 0: nothing to do.  Errors: EINVAL (a NULL
+ * pointer, max_q out of range), EWORKSPACE. */
+mtgnn_status mtgnn_temporal_attn_bwd_group(const int32_t* q_node, const int32_t* n_q, int64_t max_q,
+                                           const int32_t* nbr, const void* save, const int32_t* uniq,
+                                           const int32_t* n_rows, int64_t max_rows, const mtgnn_dims* dims,
+                                           void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Row a7 with two streams, the grouping done ahead: as mtgnn_temporal_attn_bwd_overlap, except that
+ * the d_mem grouping is the one mtgnn_temporal_attn_bwd_group left in ws, so there is no fork at
+ * entry.  dmem_stream must be ordered after that call (it was enqueued on dmem_stream, or
+ * dmem_stream waits for it).  The call records `fork` on `stream` once the gradients the sums need
+ * are ready, makes dmem_stream wait for it (the sums), records `join` on dmem_stream and makes
+ * `stream` wait for `join`.  Results are bitwise identical to mtgnn_temporal_attn_bwd. */
+mtgnn_status mtgnn_temporal_attn_bwd_grouped(const int32_t* q_node, const float* q_t, const int32_t* n_q,
+                                             int64_t max_q, const int32_t* nbr, const float* nt, const float* dz,
+                                             const void* save, const int32_t* uniq, const int32_t* n_rows,
+                                             int64_t max_rows, const float* time_w, const float* time_b,
+                                             const mtgnn_attn_params* params, const mtgnn_dims* dims,
+                                             mtgnn_attn_grads* grads, float* d_mem, float* d_time_w,
+                                             float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
+                                             hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join);
+
 /* Row a8. Backward of mtgnn_gru_update for d_mem = dL/dh' [max_rows, d_mem].
  * The previous memory h is detached.
  *   save, msg   -- the forward call's (save must not be NULL there);

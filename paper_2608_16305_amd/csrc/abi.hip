@@ -345,7 +345,8 @@ static mtgnn_status attn_bwd_checked(const int32_t* q_node, const float* q_t, co
                                      const float* time_w, const float* time_b, const mtgnn_attn_params* params,
                                      const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem, float* d_time_w,
                                      float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
-                                     hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join) {
+                                     hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join,
+                                     bool grouped = false) {
   MTGNN_TRY(check_dims(d));
   MTGNN_TRY(check_attn_params(params));
   MTGNN_TRY(check_rows(max_rows));
@@ -368,7 +369,7 @@ static mtgnn_status attn_bwd_checked(const int32_t* q_node, const float* q_t, co
   if (ws_bytes < attn_bwd_ws(d, max_q, max_rows)) return fail(MTGNN_EWORKSPACE, "temporal_attn_bwd ws");
   REQ(ws, "ws");
   return attn_bwd_impl(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params, d,
-                       g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, dmem_stream, fork, join);
+                       g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, dmem_stream, fork, join, grouped);
 }
 
 mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
@@ -393,6 +394,36 @@ mtgnn_status mtgnn_temporal_attn_bwd_overlap(const int32_t* q_node, const float*
     return fail(MTGNN_EINVAL, "temporal_attn_bwd_overlap: dmem_stream, fork and join are required");
   return attn_bwd_checked(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params,
                           d, g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, dmem_stream, fork, join);
+}
+
+mtgnn_status mtgnn_temporal_attn_bwd_group(const int32_t* q_node, const int32_t* n_q, int64_t max_q,
+                                           const int32_t* nbr, const void* save, const int32_t* uniq,
+                                           const int32_t* n_rows, int64_t max_rows, const mtgnn_dims* d, void* ws,
+                                           size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  if (max_q <= 0 || max_q * (int64_t)d->k >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  REQ(q_node, "q_node");
+  REQ(nbr, "nbr");
+  REQ(save, "save");
+  if (max_rows > 0) REQ(uniq, "uniq");
+  if (ws_bytes < attn_bwd_ws(d, max_q, max_rows)) return fail(MTGNN_EWORKSPACE, "temporal_attn_bwd_group ws");
+  REQ(ws, "ws");
+  return attn_bwd_group_impl(q_node, n_q, max_q, nbr, save, uniq, n_rows, max_rows, d, ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_temporal_attn_bwd_grouped(const int32_t* q_node, const float* q_t, const int32_t* n_q,
+                                             int64_t max_q, const int32_t* nbr, const float* nt, const float* dz,
+                                             const void* save, const int32_t* uniq, const int32_t* n_rows,
+                                             int64_t max_rows, const float* time_w, const float* time_b,
+                                             const mtgnn_attn_params* params, const mtgnn_dims* d,
+                                             mtgnn_attn_grads* g, float* d_mem, float* d_time_w, float* d_time_b,
+                                             void* ws, size_t ws_bytes, hipStream_t stream, hipStream_t dmem_stream,
+                                             hipEvent_t fork, hipEvent_t join) {
+  if (max_rows > 0 && (!dmem_stream || !fork || !join))
+    return fail(MTGNN_EINVAL, "temporal_attn_bwd_grouped: dmem_stream, fork and join are required");
+  return attn_bwd_checked(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params,
+                          d, g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, dmem_stream, fork, join, true);
 }
 
 mtgnn_status mtgnn_gru_update_bwd(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,

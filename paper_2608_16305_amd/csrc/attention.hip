@@ -399,26 +399,43 @@ __global__ void k_row_map(const int32_t* __restrict__ uniq, const int32_t* __res
 // Occurrence o < max_q is query o; o = max_q + p is compact slot p.  Its key is
 // the row of its node among the rows updated this step, or `sentinel` when
 // the node was not updated, or the query / slot is beyond the device counts.
-__global__ void k_occ_keys(const int32_t* __restrict__ q_node, const int32_t* __restrict__ pair_nbr,
-                           const int32_t* __restrict__ n_q, int64_t max_q, const int32_t* __restrict__ n_valid,
-                           int64_t max_p, const int32_t* __restrict__ uniq, const int32_t* __restrict__ n_rows,
-                           int64_t max_rows, const int32_t* __restrict__ row_of, uint32_t sentinel,
-                           uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+// Threads o >= max_q walk the sampled grid (query q, slot j): the valid slots of a query are the
+// prefix of its list, so slot j < cnt[q] is compact slot pair_off[q] + j, and the thread for grid
+// index i also fills compact position i when i is past the valid count.  Every position is written
+// once, from the sampler's output and the slot counts alone (no forward gather needed).
+__device__ __forceinline__ uint32_t occ_key(int64_t node, const int32_t* __restrict__ uniq, int32_t rows,
+                                            const int32_t* __restrict__ row_of, uint32_t sentinel) {
+  if (node < 0) return sentinel;
+  const int32_t r = row_of[node];
+  return (r >= 0 && r < rows && uniq[r] == node) ? (uint32_t)r : sentinel;
+}
+
+__global__ void k_occ_keys(const int32_t* __restrict__ q_node, const int32_t* __restrict__ nbr,
+                           const int32_t* __restrict__ cnt, const int32_t* __restrict__ pair_off,
+                           const int32_t* __restrict__ n_q, int64_t max_q, int k,
+                           const int32_t* __restrict__ n_valid, int64_t max_p, const int32_t* __restrict__ uniq,
+                           const int32_t* __restrict__ n_rows, int64_t max_rows, const int32_t* __restrict__ row_of,
+                           uint32_t sentinel, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (o >= max_q + max_p) return;
-  int64_t node = -1;
+  const int32_t rows = (int32_t)eff_count(max_rows, n_rows);
   if (o < max_q) {
-    if (o < eff_count(max_q, n_q)) node = q_node[o];
-  } else if (o - max_q < eff_count(max_p, n_valid)) {
-    node = pair_nbr[o - max_q];
+    keys[o] = occ_key(o < eff_count(max_q, n_q) ? q_node[o] : -1, uniq, rows, row_of, sentinel);
+    vals[o] = (uint32_t)o;
+    return;
   }
-  uint32_t key = sentinel;
-  if (node >= 0) {
-    const int32_t r = row_of[node];
-    if (r >= 0 && r < eff_count(max_rows, n_rows) && uniq[r] == node) key = (uint32_t)r;
+  const int64_t i = o - max_q;
+  const int64_t q = i / k;
+  const int j = (int)(i - q * k);
+  if (j < cnt[q]) {
+    const int64_t p = max_q + pair_off[q] + j;
+    keys[p] = occ_key(nbr[i], uniq, rows, row_of, sentinel);
+    vals[p] = (uint32_t)p;
   }
-  keys[o] = key;
-  vals[o] = (uint32_t)o;
+  if (i >= eff_count(max_p, n_valid)) {
+    keys[o] = sentinel;
+    vals[o] = (uint32_t)o;
+  }
 }
 
 // seg_lo[row], seg_hi[row]: the sorted positions [lo, hi) holding row's occurrences.
@@ -805,15 +822,17 @@ namespace {
 // the updated row of its node (or the sentinel max_rows), sorted stably by key, and each row's
 // segment bounds.  Reads only forward outputs and the updated-row list, so it may run before
 // any gradient exists.  *skeys / *svals: the buffers holding the sorted pairs.
-mtgnn_status attn_bwd_dmem_group(const int32_t* q_node, const int32_t* n_q, int64_t max_q, const AttnShape& sh,
-                                 const AttnSave& sv, const BwdWs& b, const int32_t* uniq, const int32_t* n_rows,
-                                 int64_t max_rows, uint32_t** skeys, uint32_t** svals, hipStream_t s) {
+mtgnn_status attn_bwd_dmem_group(const int32_t* q_node, const int32_t* n_q, int64_t max_q, const int32_t* nbr,
+                                 const AttnShape& sh, const AttnSave& sv, const BwdWs& b, const int32_t* uniq,
+                                 const int32_t* n_rows, int64_t max_rows, uint32_t** skeys, uint32_t** svals,
+                                 hipStream_t s) {
   const int64_t n_occ = sh.Q + sh.P;
   const uint32_t sentinel = (uint32_t)max_rows;
   k_row_map<<<(unsigned)cdiv(max_rows, 256), 256, 0, s>>>(uniq, n_rows, max_rows, b.row_of, b.seg_lo, b.seg_hi);
   MTGNN_CHECK_LAUNCH("row_map");
-  k_occ_keys<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(q_node, sv.pair_nbr, n_q, max_q, sv.n_valid, sh.P, uniq,
-                                                         n_rows, max_rows, b.row_of, sentinel, b.keys, b.vals);
+  k_occ_keys<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(q_node, nbr, sv.cnt, sv.pair_off, n_q, max_q, sh.k,
+                                                         sv.n_valid, sh.P, uniq, n_rows, max_rows, b.row_of, sentinel,
+                                                         b.keys, b.vals);
   MTGNN_CHECK_LAUNCH("occ_keys");
   *skeys = b.keys;
   *svals = b.vals;
@@ -920,14 +939,25 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
 
 }  // namespace
 
+mtgnn_status attn_bwd_group_impl(const int32_t* q_node, const int32_t* n_q, int64_t max_q, const int32_t* nbr,
+                                 const void* save, const int32_t* uniq, const int32_t* n_rows, int64_t max_rows,
+                                 const mtgnn_dims* d, void* ws, size_t ws_bytes, hipStream_t s) {
+  const AttnShape sh(d, max_q);
+  const AttnSave sv = carve_save((void*)save, sh);
+  const BwdWs b = carve_bwd(ws, sh, max_rows);
+  if (ws_bytes < b.total) return MTGNN_EWORKSPACE;
+  if (max_rows == 0) return MTGNN_OK;
+  uint32_t *skeys = nullptr, *svals = nullptr;
+  return attn_bwd_dmem_group(q_node, n_q, max_q, nbr, sh, sv, b, uniq, n_rows, max_rows, &skeys, &svals, s);
+}
+
 mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
                            const int32_t* nbr, const float* nt, const float* dz, const void* save, const int32_t* uniq,
                            const int32_t* n_rows, int64_t max_rows, const float* tw, const float* tb,
                            const mtgnn_attn_params* p, const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem,
                            float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes, hipStream_t s,
-                           hipStream_t s_dmem, hipEvent_t fork, hipEvent_t join) {
+                           hipStream_t s_dmem, hipEvent_t fork, hipEvent_t join, bool grouped) {
   (void)q_t;
-  (void)nbr;
   (void)nt;
   const AttnShape sh(d, max_q);
   const AttnSave sv = carve_save((void*)save, sh);
@@ -938,10 +968,15 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   const int da = sh.da, dm = sh.dm;
 
   // With a second stream, the d M' grouping's key sort starts there at once (it reads only forward
-  // outputs): first fork.  The same event marks the second fork below.
+  // outputs): first fork.  The same event marks the second fork below.  `grouped`: the grouping is
+  // already in ws (attn_bwd_group_impl, ordered before the second stream's next work).
   const bool overlap = s_dmem != nullptr && max_rows > 0;
   uint32_t *skeys = nullptr, *svals = nullptr;
-  if (overlap) {
+  if (overlap && grouped) {
+    skeys = b.keys;
+    svals = b.vals;
+    radix_sort_output(&skeys, &svals, sh.Q + sh.P, bits_for(max_rows), b.sort_scratch);
+  } else if (overlap) {
     hipError_t e0 = hipEventRecord(fork, s);
     if (e0 == hipSuccess) e0 = hipStreamWaitEvent(s_dmem, fork, 0);
     if (e0 != hipSuccess) {
@@ -949,7 +984,7 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
       return MTGNN_EHIP;
     }
     const mtgnn_status st0 =
-        attn_bwd_dmem_group(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, &skeys, &svals, s_dmem);
+        attn_bwd_dmem_group(q_node, n_q, max_q, nbr, sh, sv, b, uniq, n_rows, max_rows, &skeys, &svals, s_dmem);
     if (st0 != MTGNN_OK) {   // leave `stream` ordered after the second stream
       if (hipEventRecord(join, s_dmem) == hipSuccess) (void)hipStreamWaitEvent(s, join, 0);
       return st0;
@@ -993,7 +1028,7 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
   if (!overlap) {
     MTGNN_TRY(attn_bwd_params(n_q, sh, sv, b, dz, tw, tb, p, wt, g, d_time_w, d_time_b, s));
     if (max_rows > 0) {
-      MTGNN_TRY(attn_bwd_dmem_group(q_node, n_q, max_q, sh, sv, b, uniq, n_rows, max_rows, &skeys, &svals, s));
+      MTGNN_TRY(attn_bwd_dmem_group(q_node, n_q, max_q, nbr, sh, sv, b, uniq, n_rows, max_rows, &skeys, &svals, s));
       MTGNN_TRY(attn_bwd_dmem_sum(max_q, sh, sv, b, skeys, svals, n_rows, max_rows, wt, d_mem, s));
     }
     return MTGNN_OK;

@@ -114,6 +114,9 @@ size_t radix_sort_ws_bytes(int64_t n);
 size_t radix_sort_result_bytes(int64_t n);
 mtgnn_status radix_sort_pairs(uint32_t** keys, uint32_t** vals, int64_t n, int bits, void* ws, size_t ws_bytes,
                               hipStream_t s);
+int radix_passes(int bits);
+// Where radix_sort_pairs(keys, vals, n, bits, ws, ...) leaves the sorted pairs, without sorting.
+void radix_sort_output(uint32_t** keys, uint32_t** vals, int64_t n, int bits, void* ws);
 
 // Exclusive prefix sum of int32 counts; optional device total.
 size_t scan_ws_bytes(int64_t n);

@@ -348,46 +348,59 @@ __global__ __launch_bounds__(256) void k_timegrad_partial(const float* __restric
   }
 }
 
-// One block per column j: thread t sums chunks t, t + 256, ... of the partial
-// sums, then a fixed-order tree in LDS combines the 256 thread sums.  Chunks
-// beyond the device row count (ceil(rows / chunk_rows)) hold no partial.
-// Column j's sums over the row chunks' partials (fixed tree order), by a block of 256 threads.
-__device__ __forceinline__ void timegrad_sum(const float* __restrict__ part, int64_t rows,
-                                             const int32_t* __restrict__ rows_dev, int chunk_rows, int dt_dim,
-                                             float* sw, float* sb, float& w, float& b) {
+// One block of 256 threads per column j.  Thread t adds the partials of row chunks t, t + 256, ... in
+// that order (loads issued eight at a time, chunks past the count read a valid chunk and add zero);
+// chunks beyond the device row count (ceil(rows / chunk_rows)) hold no partial.
+__device__ __forceinline__ void timegrad_part(const float* __restrict__ part, int64_t rows,
+                                              const int32_t* __restrict__ rows_dev, int chunk_rows, int dt_dim,
+                                              float& aw, float& ab) {
   const int j = blockIdx.x, t = threadIdx.x;
   const int64_t nch = cdiv(eff_count(rows, rows_dev), chunk_rows);
-  float aw = 0.f, ab = 0.f;
-  for (int64_t c = t; c < nch; c += 256) {
-    aw += part[(c * 2 + 0) * dt_dim + j];
-    ab += part[(c * 2 + 1) * dt_dim + j];
-  }
-  sw[t] = aw;
-  sb[t] = ab;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (t < o) {
-      sw[t] += sw[t + o];
-      sb[t] += sb[t + o];
+  for (int64_t c0 = t; c0 < nch; c0 += 256 * 8) {
+    float vw[8], vb[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t c = c0 + 256 * u < nch ? c0 + 256 * u : c0;
+      vw[u] = part[(c * 2 + 0) * dt_dim + j];
+      vb[u] = part[(c * 2 + 1) * dt_dim + j];
     }
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const bool ok = c0 + 256 * u < nch;
+      aw += ok ? vw[u] : 0.f;
+      ab += ok ? vb[u] : 0.f;
+    }
   }
-  w = sw[0];
-  b = sb[0];
+}
+
+// Block sums of NV values over 256 threads, in a fixed order: a butterfly in each wave (lane 0's
+// result), then the four wave sums as (w0 + w1) + (w2 + w3).  s holds 4 NV floats.
+template <int NV>
+__device__ __forceinline__ void block_sums256(float (&v)[NV], float* s) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = wave_sum(v[i]);
+  if ((t & 63) == 0) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) s[i * 4 + (t >> 6)] = v[i];
+  }
   __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = (s[i * 4] + s[i * 4 + 1]) + (s[i * 4 + 2] + s[i * 4 + 3]);
 }
 
 __global__ __launch_bounds__(256) void k_timegrad_reduce(const float* __restrict__ part, int64_t rows,
                                                          const int32_t* __restrict__ rows_dev, int chunk_rows,
                                                          int dt_dim, float* __restrict__ dw, float* __restrict__ db,
                                                          int accumulate) {
-  __shared__ float sw[256], sb[256];
-  float w, b;
-  timegrad_sum(part, rows, rows_dev, chunk_rows, dt_dim, sw, sb, w, b);
+  __shared__ float s[8];
+  float v[2] = {0.f, 0.f};
+  timegrad_part(part, rows, rows_dev, chunk_rows, dt_dim, v[0], v[1]);
+  block_sums256<2>(v, s);
   const int j = blockIdx.x;
   if (threadIdx.x == 0) {
-    dw[j] = accumulate ? dw[j] + w : w;
-    db[j] = accumulate ? db[j] + b : b;
+    dw[j] = accumulate ? dw[j] + v[0] : v[0];
+    db[j] = accumulate ? db[j] + v[1] : v[1];
   }
 }
 
@@ -401,21 +414,15 @@ __global__ __launch_bounds__(256) void k_timegrad_reduce_q(const float* __restri
                                                            const float* __restrict__ Wq, int64_t ldw, int col0, int da,
                                                            const float* __restrict__ tw, const float* __restrict__ tb,
                                                            float* __restrict__ dw, float* __restrict__ db) {
-  __shared__ float sw[256], sb[256];
-  float w, b;
-  timegrad_sum(part, rows, rows_dev, chunk_rows, dt_dim, sw, sb, w, b);
+  __shared__ float s[12];
   const int j = blockIdx.x, t = threadIdx.x;
-  float m = 0.f;
-  for (int a = t; a < da; a += 256) m += dbq[a] * Wq[(int64_t)a * ldw + col0 + j];
-  sw[t] = m;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (t < o) sw[t] += sw[t + o];
-    __syncthreads();
-  }
+  float v[3] = {0.f, 0.f, 0.f};
+  for (int a = t; a < da; a += 256) v[2] += dbq[a] * Wq[(int64_t)a * ldw + col0 + j];
+  timegrad_part(part, rows, rows_dev, chunk_rows, dt_dim, v[0], v[1]);
+  block_sums256<3>(v, s);
   if (t == 0) {
-    dw[j] = w;
-    db[j] = -sinf(time_arg(tw[j], 0.f, tb[j])) * sw[0] + b;
+    dw[j] = v[0];
+    db[j] = -sinf(time_arg(tw[j], 0.f, tb[j])) * v[2] + v[1];
   }
 }
 
@@ -426,14 +433,15 @@ __global__ __launch_bounds__(256) void k_timegrad_reduce2(const float* __restric
                                                           const float* __restrict__ p2, int64_t rows2,
                                                           const int32_t* __restrict__ rows_dev2, int chunk_rows,
                                                           int dt_dim, float* __restrict__ dw, float* __restrict__ db) {
-  __shared__ float sw[256], sb[256];
-  float w1, b1, w2, b2;
-  timegrad_sum(p1, rows1, rows_dev1, chunk_rows, dt_dim, sw, sb, w1, b1);
-  timegrad_sum(p2, rows2, rows_dev2, chunk_rows, dt_dim, sw, sb, w2, b2);
+  __shared__ float s[16];
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  timegrad_part(p1, rows1, rows_dev1, chunk_rows, dt_dim, v[0], v[1]);
+  timegrad_part(p2, rows2, rows_dev2, chunk_rows, dt_dim, v[2], v[3]);
+  block_sums256<4>(v, s);
   const int j = blockIdx.x;
   if (threadIdx.x == 0) {
-    dw[j] = w1 + w2;
-    db[j] = b1 + b2;
+    dw[j] = v[0] + v[2];
+    db[j] = v[1] + v[3];
   }
 }
 

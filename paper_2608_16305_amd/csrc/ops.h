@@ -131,6 +131,12 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
                            const int32_t* n_rows, int64_t max_rows, const float* tw, const float* tb,
                            const mtgnn_attn_params* p, const mtgnn_dims* d, mtgnn_attn_grads* g, float* d_mem,
                            float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes, hipStream_t s,
-                           hipStream_t s_dmem = nullptr, hipEvent_t fork = nullptr, hipEvent_t join = nullptr);
+                           hipStream_t s_dmem = nullptr, hipEvent_t fork = nullptr, hipEvent_t join = nullptr,
+                           bool grouped = false);
+// The backward's d M' grouping alone (row map, occurrence keys, stable sort, segment bounds) into ws,
+// from the queries, the sampled neighbours, the slot counts in save and the updated rows.
+mtgnn_status attn_bwd_group_impl(const int32_t* q_node, const int32_t* n_q, int64_t max_q, const int32_t* nbr,
+                                 const void* save, const int32_t* uniq, const int32_t* n_rows, int64_t max_rows,
+                                 const mtgnn_dims* d, void* ws, size_t ws_bytes, hipStream_t s);
 
 }  // namespace mtgnn

@@ -307,6 +307,15 @@ size_t radix_sort_ws_bytes(int64_t n) {
 
 size_t radix_sort_result_bytes(int64_t n) { return 2 * align256(sizeof(uint32_t) * n); }
 
+int radix_passes(int bits) { return (bits + RADIX_BITS - 1) / RADIX_BITS; }
+
+void radix_sort_output(uint32_t** keys_io, uint32_t** vals_io, int64_t n, int bits, void* ws) {
+  // an odd number of passes leaves the pairs in the first two workspace arrays
+  if (n <= 1 || radix_passes(bits) % 2 == 0) return;
+  *keys_io = (uint32_t*)ws;
+  *vals_io = (uint32_t*)((char*)ws + align256(sizeof(uint32_t) * n));
+}
+
 mtgnn_status radix_sort_pairs(uint32_t** keys_io, uint32_t** vals_io, int64_t n, int bits, void* ws, size_t ws_bytes,
                               hipStream_t s) {
   if (n <= 1) return MTGNN_OK;
@@ -327,7 +336,7 @@ mtgnn_status radix_sort_pairs(uint32_t** keys_io, uint32_t** vals_io, int64_t n,
   const size_t rest = ws_bytes - (size_t)(w - (char*)ws);
   uint32_t *ki = keys, *vi = vals, *ko = k2, *vo = v2;
   // passes of equal width (at most 8 bits each), so each pass scans (2^width) x blocks counts
-  const int passes = (bits + RADIX_BITS - 1) / RADIX_BITS;
+  const int passes = radix_passes(bits);
   const int width = (bits + passes - 1) / passes;
   for (int shift = 0; shift < bits; shift += width) {
     const int dbits = (bits - shift) < width ? (bits - shift) : width;

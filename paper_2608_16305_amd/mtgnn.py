@@ -22,7 +22,8 @@ ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
     "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_prepare", "mtgnn_temporal_attn_prepare_weights",
     "mtgnn_temporal_attn_prepare_slots", "mtgnn_temporal_attn_prepared",
-    "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap",
+    "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap", "mtgnn_temporal_attn_bwd_group",
+    "mtgnn_temporal_attn_bwd_grouped",
     "mtgnn_gru_update_bwd",
     "mtgnn_build_messages_bwd", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
@@ -75,6 +76,10 @@ _SIGS = {
     "mtgnn_temporal_attn_bwd": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, C.POINTER(AttnParams),
                                 C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_bwd_overlap": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P,
+                                        C.POINTER(AttnParams), C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P,
+                                        _SZ, _P, _P, _P, _P],
+    "mtgnn_temporal_attn_bwd_group": [_P, _P, _I64, _P, _P, _P, _P, _I64, C.POINTER(Dims), _P, _SZ, _P],
+    "mtgnn_temporal_attn_bwd_grouped": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P,
                                         C.POINTER(AttnParams), C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P,
                                         _SZ, _P, _P, _P, _P],
     "mtgnn_gru_update_bwd": [_P, _P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _P, _P, _SZ, _P],
@@ -289,18 +294,78 @@ def mtgnn_temporal_attn_bwd(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_
            "mtgnn_temporal_attn_bwd")
 
 
+_hip = None
+
+
+def _hip_rt():
+    # the HIP runtime already loaded in this process (torch's, which the library resolves to as well)
+    global _hip
+    if _hip is None:
+        _hip = C.CDLL("libamdhip64.so.7", mode=C.RTLD_GLOBAL)
+        for f in ("hipEventCreateWithFlags", "hipEventRecord", "hipStreamWaitEvent", "hipEventDestroy"):
+            getattr(_hip, f).restype = C.c_int
+    return _hip
+
+
+def _hip_check(rc, what):
+    if rc != 0:
+        raise MtgnnError(f"{what} failed with HIP error {rc}")
+
+
+class DeviceEvent:
+    """An event that orders work between two streams of the current device.
+
+    No timing, and a device-scope release when it is recorded (hipEventDisableSystemFence): both streams
+    run on one GPU, so the system-scope fence of a default event, a cache write-back and invalidate that
+    costs several microseconds per record, is not needed.  Methods follow torch.cuda.Event's:
+    record(stream) and wait(stream) (the stream waits for the event)."""
+
+    _FLAGS = 0x2 | 0x20000000   # hipEventDisableTiming | hipEventDisableSystemFence
+
+    def __init__(self):
+        self._rt = _hip_rt()
+        h = C.c_void_p()
+        _hip_check(self._rt.hipEventCreateWithFlags(C.byref(h), C.c_uint(self._FLAGS)), "hipEventCreateWithFlags")
+        self.handle = h
+
+    def record(self, stream=None):
+        _hip_check(self._rt.hipEventRecord(self.handle, _stream(stream)), "hipEventRecord")
+
+    def wait(self, stream=None):
+        _hip_check(self._rt.hipStreamWaitEvent(_stream(stream), self.handle, C.c_uint(0)), "hipStreamWaitEvent")
+
+    def __del__(self):
+        if getattr(self, "handle", None) and self.handle.value:
+            self._rt.hipEventDestroy(self.handle)
+            self.handle = C.c_void_p()
+
+
 def _event(e, name):
+    if isinstance(e, DeviceEvent):
+        return e.handle
     h = e.cuda_event if isinstance(e, torch.cuda.Event) else 0
     if not h:
         raise MtgnnError(f"{name}: a torch.cuda.Event that has been recorded once (so that it exists) is required")
     return C.c_void_p(h)
 
 
+def mtgnn_temporal_attn_bwd_group(q_node, n_q, max_q, nbr, save, uniq, n_rows, max_rows, d: Dims, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_temporal_attn_bwd_group(
+        _ptr(q_node, torch.int32, "q_node"), _ptr(n_q, torch.int32, "n_q", True), int(max_q),
+        _ptr(nbr, torch.int32, "nbr"), _ptr(save, torch.uint8, "save"), _ptr(uniq, torch.int32, "uniq", True),
+        _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows), C.byref(d), wp, wb, _stream(stream)),
+        "mtgnn_temporal_attn_bwd_group")
+
+
 def mtgnn_temporal_attn_bwd_overlap(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w,
                                     time_b, params: AttnParams, d: Dims, grads: AttnGrads, d_mem, d_time_w, d_time_b,
-                                    ws, dmem_stream, fork, join, stream=None):
+                                    ws, dmem_stream, fork, join, stream=None, grouped=False):
+    """grouped=True calls mtgnn_temporal_attn_bwd_grouped (the grouping left in ws by
+    mtgnn_temporal_attn_bwd_group on dmem_stream)."""
     wp, wb = _ws(ws)
-    _check(lib().mtgnn_temporal_attn_bwd_overlap(
+    name = "mtgnn_temporal_attn_bwd_grouped" if grouped else "mtgnn_temporal_attn_bwd_overlap"
+    _check(getattr(lib(), name)(
         _ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"), _ptr(n_q, torch.int32, "n_q", True),
         int(max_q), _ptr(nbr, torch.int32, "nbr"), _ptr(nt, torch.float32, "nt"), _ptr(dz, torch.float32, "dz"),
         _ptr(save, torch.uint8, "save"), _ptr(uniq, torch.int32, "uniq", True),
@@ -308,7 +373,7 @@ def mtgnn_temporal_attn_bwd_overlap(q_node, q_t, n_q, max_q, nbr, nt, dz, save, 
         _ptr(time_b, torch.float32, "time_b"), C.byref(params), C.byref(d), C.byref(grads),
         _ptr(d_mem, torch.float32, "d_mem", True), _ptr(d_time_w, torch.float32, "d_time_w"),
         _ptr(d_time_b, torch.float32, "d_time_b"), wp, wb, _stream(stream), _stream(dmem_stream),
-        _event(fork, "fork"), _event(join, "join")), "mtgnn_temporal_attn_bwd_overlap")
+        _event(fork, "fork"), _event(join, "join")), name)
 
 
 def mtgnn_gru_update_bwd(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d: Dims, dW_ih, dW_hh, db_ih, db_hh,

@@ -10,11 +10,10 @@ that with overlap=True (the default) two pieces run on a second stream, forked
 and joined with events: the queries, their sampling and the attention's
 preparation, during the memory phase; the next step's aggregation and
 messages (lag-1 order: its memory batch is this step's batch, read from the
-memory this step's update leaves), during the embedding; and the attention
-backward's d_mem part (its key sort from the backward's start) followed by the
-GRU backward,
-during the attention parameter gradients.  Results are bitwise those of
-overlap=False.
+memory this step's update leaves), and the attention backward's d_mem
+grouping (a key sort), during the embedding; and the backward's d_mem sums
+followed by the GRU backward, during the attention parameter gradients.
+Results are bitwise those of overlap=False.
 """
 
 import numpy as np
@@ -109,16 +108,15 @@ class TGNStep:
                                       M.workspace_bytes(M.OP_GRU_UPDATE_BWD, d, R, 0), 256), dev)
         self.ap = M.attn_params(self.params, d)
         self.ag = M.attn_grads(self.grads)
-        # second stream (default priority) and fork/join events for the work that
-        # overlaps the main stream; recording the events once makes them exist
+        # second stream (default priority) and fork/join events for the work that overlaps the main stream
+        # (device-scope events: no system-scope fence per record)
         self.side_stream = torch.cuda.Stream(device=dev)
-        self.fork, self.join = torch.cuda.Event(), torch.cuda.Event()
-        self.q_fork, self.q_join = torch.cuda.Event(), torch.cuda.Event()
-        self.g_join = torch.cuda.Event()
-        self.m_done, self.pre_join = torch.cuda.Event(), torch.cuda.Event()
-        s0 = self.ts if self.ts is not None else torch.cuda.current_stream(dev)
-        for e in (self.fork, self.join, self.q_fork, self.q_join, self.g_join, self.m_done, self.pre_join):
-            e.record(s0)
+        self.fork, self.join = M.DeviceEvent(), M.DeviceEvent()
+        self.q_fork, self.q_join = M.DeviceEvent(), M.DeviceEvent()
+        self.g_join = M.DeviceEvent()
+        self.m_done, self.pre_join = M.DeviceEvent(), M.DeviceEvent()
+        self.group_ahead = True   # step(): the backward's d_mem grouping during the embedding (second stream)
+        self._grouped = False     # ... and it has been enqueued
 
     def _batch(self, lo, hi):
         if hi <= lo:
@@ -185,13 +183,15 @@ class TGNStep:
             M.mtgnn_temporal_attn_bwd_overlap(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
                                               self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"],
                                               p["time_b"], self.ap, self.d, self.ag, self.d_mem, g["time_w"],
-                                              g["time_b"], self.ws, self.side_stream, self.fork, self.join, stream=s)
+                                              g["time_b"], self.ws, self.side_stream, self.fork, self.join, stream=s,
+                                              grouped=self._grouped)
+            self._grouped = False
             M.mtgnn_gru_update_bwd(self.d_mem, self.gru_save, self.msg, self.n_uniq, self.max_rows, p["W_ih"],
                                    p["W_hh"], self.d, g["W_ih"], g["W_hh"], g["b_ih"], g["b_hh"], self.dmsg_time,
                                    self.ws_q, stream=self.side_stream)
             self.g_join.record(self.side_stream)
             main = s if s is not None else torch.cuda.current_stream(self.dev)
-            main.wait_event(self.g_join)
+            self.g_join.wait(main)
         else:
             M.mtgnn_temporal_attn_bwd(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
                                       self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],
@@ -220,7 +220,7 @@ class TGNStep:
             main = self.ts if self.ts is not None else torch.cuda.current_stream(self.dev)
             side = self.side_stream
             self.q_fork.record(main)
-            side.wait_event(self.q_fork)
+            self.q_fork.wait(side)
             self.queries(elo, ehi, side)
             self.q_join.record(side)
             self.prepare_weights(main)   # one launch here, so the second stream's chain is shorter
@@ -228,21 +228,28 @@ class TGNStep:
                 # this memory batch's aggregation and messages were built during the previous step's
                 # embedding, from the memory as it is now: only the GRU update is left
                 self._bind(1 - self._cur)
-                main.wait_event(self.pre_join)
+                self.pre_join.wait(main)
                 self._pre = None
                 self._gru(mlo, mhi)
             else:
                 self.memory_phase(mlo, mhi)
+            self.m_done.record(main)
+            self.m_done.wait(side)
             if self.lag == 1:
                 # the next step's memory batch is this step's batch: its aggregation and messages read the
                 # memory as this update leaves it, which nothing changes before the next step's GRU update;
                 # built on the second stream into the other buffer set while the embedding runs here
-                self.m_done.record(main)
-                side.wait_event(self.m_done)
                 self._messages(elo, ehi, self._sets[1 - self._cur], self.ws_q, side)
                 self.pre_join.record(side)
                 self._pre = (elo, ehi)
-            main.wait_event(self.q_join)
+            # the backward's d_mem grouping (a key sort) needs only this step's updated rows and sampled
+            # slots: on the second stream during the embedding, into the backward's workspace, which
+            # nothing here touches until the backward
+            if self.group_ahead:
+                M.mtgnn_temporal_attn_bwd_group(self.q_node, self.n_q, self.max_q, self.nbr, self.attn_save,
+                                                self.uniq, self.n_uniq, self.max_rows, self.d, self.ws, stream=side)
+                self._grouped = True
+            self.q_join.wait(main)
             self.embed(elo, ehi, queries_done=True)
         else:
             self.memory_phase(mlo, mhi)

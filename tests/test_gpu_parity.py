@@ -165,7 +165,9 @@ def test_edge_large_batch_multiblock_paths():
 
 def test_backward_overlap_bitwise():
     """The two-stream attention backward (d_mem part on a second stream) gives bitwise the
-    results of the single-stream call, from the same state (bipartite stream, 3 steps)."""
+    results of the single-stream call, from the same state (bipartite stream, 3 steps), both with
+    the d_mem grouping at the backward's entry (mtgnn_temporal_attn_bwd_overlap) and with it done
+    during the embedding (mtgnn_temporal_attn_bwd_group, then _grouped)."""
     from paper_2608_16305_amd.step import TGNStep
     from tests._gpu import dz_tensor, n_targets
     w = workload(2)
@@ -174,8 +176,9 @@ def test_backward_overlap_bitwise():
     params = init_params(w, random_bias=True)
     mem, lu = random_state(w, seed=11)
     outs = []
-    for overlap in (False, True):
+    for overlap, ahead in ((False, False), (True, False), (True, True)):
         r = TGNStep(w, s, params, mem, lu, overlap=overlap)
+        r.group_ahead = ahead
         res = {}
         for b in range(1, 4):
             dz, _ = dz_tensor(r, w, b, n_targets(s, *r.batch_range(b)))
@@ -188,10 +191,11 @@ def test_backward_overlap_bitwise():
         outs.append(res)
         del r
         torch.cuda.empty_cache()
-    assert outs[0].keys() == outs[1].keys()
-    for k in outs[0]:
-        a, b = outs[0][k], outs[1][k]
-        assert a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
+    for o in outs[1:]:
+        assert outs[0].keys() == o.keys()
+        for k in outs[0]:
+            a, b = outs[0][k], o[k]
+            assert a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
 
 
 def test_forward_single_call_matches_prepare_prepared():
