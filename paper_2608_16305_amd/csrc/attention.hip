@@ -41,7 +41,7 @@ struct AttnSave {
   float* b_kv;           // [2 da]
   int32_t *cnt, *pair_off, *n_valid, *pair_nbr;
   float *pair_delta;     // per compact slot: tau - t_j
-  float *q_in, *kv_in, *sinv, *qv, *KV, *p, *attn, *m_in, *m1, *a1;
+  float *q_in, *kv_in, *qv, *KV, *p, *attn, *m_in, *m1, *a1;
   float* merge_w;        // zero-padded merge weights and their transposes for the fused chains (float32 only)
   size_t total;
 };
@@ -50,7 +50,6 @@ AttnSave carve_save(void* base, const AttnShape& s) {
   char* w = (char*)base;
   AttnSave v;
   auto take = [&](size_t bytes) { char* r = w; w += a256(bytes); return r; };
-  const int64_t dtp = s.dt > 0 ? s.dt : 1;
   // the weight copies first: their offsets do not depend on the query count (the weights-only
   // preparation carves with none)
   v.W_kv = take(s.esz * 2 * s.da * s.Dkv);
@@ -63,7 +62,6 @@ AttnSave carve_save(void* base, const AttnShape& s) {
   v.pair_delta = (float*)take(sizeof(float) * s.P);
   v.q_in = (float*)take(sizeof(float) * s.Q * s.Dq);
   v.kv_in = (float*)take(sizeof(float) * s.P * s.Dkv);
-  v.sinv = (float*)take(sizeof(float) * s.P * dtp);
   v.qv = (float*)take(sizeof(float) * s.Q * s.da);
   v.KV = (float*)take(sizeof(float) * s.P * 2 * s.da);
   v.p = (float*)take(sizeof(float) * s.Q * s.H * s.k);
@@ -131,8 +129,8 @@ __device__ __forceinline__ void gather_kv_body(int64_t q, int lane, const int32_
                                                const int32_t* __restrict__ pair_off, const T* __restrict__ mem,
                                                const float* __restrict__ x, const float* __restrict__ tw,
                                                const float* __restrict__ tb, int dm, int de, int dt, int bf16,
-                                               float* __restrict__ kv_in, float* __restrict__ sinv,
-                                               int32_t* __restrict__ pair_nbr, float* __restrict__ pair_delta) {
+                                               float* __restrict__ kv_in, int32_t* __restrict__ pair_nbr,
+                                               float* __restrict__ pair_delta) {
   const int Dkv = dm + de + dt;
   const int c = cnt[q];
   const int64_t off = pair_off[q];
@@ -176,12 +174,8 @@ __device__ __forceinline__ void gather_kv_body(int64_t q, int lane, const int32_
       if (j0 + u >= c) break;
       const float delta = __shfl(my_delta, j0 + u, 64);
       const int64_t row = off + j0 + u;
-      for (int jj = lane; jj < dt; jj += 64) {
-        float sn, cs;
-        sincosf(time_arg(tw[jj], delta, tb[jj]), &sn, &cs);
-        kv_in[row * Dkv + dm + de + jj] = pack_val(cs, bf16);
-        sinv[row * dt + jj] = sn;
-      }
+      for (int jj = lane; jj < dt; jj += 64)
+        kv_in[row * Dkv + dm + de + jj] = pack_val(cosf(time_arg(tw[jj], delta, tb[jj])), bf16);
     }
   }
 }
@@ -192,7 +186,7 @@ struct GatherArgs {
   const float *nt, *q_t, *x, *tw, *tb;
   int64_t max_q;
   int k, dm, de, dt, da, bf16;
-  float *q_in, *m_in, *kv_in, *sinv, *pair_delta;
+  float *q_in, *m_in, *kv_in, *pair_delta;
   int32_t* pair_nbr;
 };
 
@@ -203,7 +197,7 @@ __global__ __launch_bounds__(256) void k_attn_gather(GatherArgs a, const T* __re
   if (q >= eff_count(a.max_q, a.n_q)) return;
   gather_q_body<T>(q, lane, a.q_node, mem, a.tw, a.tb, a.dm, a.dt, a.da, a.bf16, a.q_in, a.m_in);
   gather_kv_body<T>(q, lane, a.nbr, a.nt, a.neid, a.q_t, a.k, a.cnt, a.pair_off, mem, a.x, a.tw, a.tb, a.dm, a.de,
-                    a.dt, a.bf16, a.kv_in, a.sinv, a.pair_nbr, a.pair_delta);
+                    a.dt, a.bf16, a.kv_in, a.pair_nbr, a.pair_delta);
 }
 
 constexpr int MAX_DH_CHUNKS = 2;   // head width <= 128
@@ -772,7 +766,7 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
   const int wt = d->dtype;
   const unsigned gq = (unsigned)cdiv(sh.Q, 4);
   const GatherArgs ga{q_node, nbr, neid, n_q, sv.cnt, sv.pair_off, nt, q_t, edge_feat, tw, tb, max_q, sh.k, sh.dm,
-                      sh.de, sh.dt, sh.da, bf, sv.q_in, sv.m_in, sv.kv_in, sv.sinv, sv.pair_delta, sv.pair_nbr};
+                      sh.de, sh.dt, sh.da, bf, sv.q_in, sv.m_in, sv.kv_in, sv.pair_delta, sv.pair_nbr};
   if (!bf)
     k_attn_gather<float><<<gq, 256, 0, s>>>(ga, (const float*)memory);
   else
@@ -898,8 +892,8 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
   // weight gradients last, so that the d M' part (on its own stream when
   // overlapped) shares the GPU with the smaller products rather than with the
   // key/value weight gradient.
-  // Time-encoder gradient: phi(tau - t_j) of the neighbour slots (with the saved sin(arg)), and phi(0)
-  // of the queries.  In float32 the queries' share is closed-form from the query projection's bias
+  // Time-encoder gradient: phi(tau - t_j) of the neighbour slots (sin(arg) recomputed in the
+  // product's epilogue from the saved tau - t_j), and phi(0) of the queries.  In float32 the queries' share is closed-form from the query projection's bias
   // gradient (their delta is 0), added in the reduce after the weight-gradient batch; otherwise it
   // is a product of its own (its w part is zero, its b part is not).
   const bool q_closed = wt == MTGNN_F32;
@@ -908,7 +902,7 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
       MTGNN_TRY(linear_dx_timegrad(b.dqv, da, wofs(p->W_q, dm), wt, sh.Dq, Q, n_q, da, dt, nullptr, nullptr, tw, tb,
                                    b.tg_part, s));
     MTGNN_TRY(linear_dx_timegrad<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, P, sv.n_valid,
-                                             2 * da, dt, sv.sinv, sv.pair_delta, tw, tb, b.tg_part2, s));
+                                             2 * da, dt, nullptr, sv.pair_delta, tw, tb, b.tg_part2, s));
     if (!q_closed)
       MTGNN_TRY(timegrad_reduce_blocks2(b.tg_part, Q, n_q, b.tg_part2, P, sv.n_valid, 64 * G_WM, dt, d_time_w,
                                         d_time_b, s));
