@@ -118,7 +118,7 @@ __device__ __forceinline__ void gather_q_body(int64_t q, int lane, const int32_t
 }
 
 // Wave per query: the rows of its valid slots, [M[n_j] || x[e_j] || cos(w (tau - t_j) + b)],
-// plus sin of the same arguments (for the time-encoder gradient), the slot's node and its tau - t_j.
+// the slot's node and its tau - t_j.
 // Slots go GATHER_CHUNK at a time: the chunk's memory-row loads are all issued before any is stored.
 constexpr int GATHER_CHUNK = 8;
 
@@ -198,6 +198,81 @@ __global__ __launch_bounds__(256) void k_attn_gather(GatherArgs a, const T* __re
   gather_q_body<T>(q, lane, a.q_node, mem, a.tw, a.tb, a.dm, a.dt, a.da, a.bf16, a.q_in, a.m_in);
   gather_kv_body<T>(q, lane, a.nbr, a.nt, a.neid, a.q_t, a.k, a.cnt, a.pair_off, mem, a.x, a.tw, a.tb, a.dm, a.de,
                     a.dt, a.bf16, a.kv_in, a.pair_nbr, a.pair_delta);
+}
+
+// Float32 fast path (no edge features, widths divisible by 4): the values of k_attn_gather<float>,
+// computed the same way, with a query's rows cut into 4-float groups laid out flat across the
+// wave, so that each lane moves 16 bytes per load or store: the query row in one pass, then the
+// memory groups of all its valid slots (loads issued GV_UNROLL passes at a time before any store),
+// then the time-encoding groups (four cosines per lane).
+constexpr int GV_UNROLL = 4;
+
+__global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const float* __restrict__ mem) {
+  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (q >= eff_count(a.max_q, a.n_q)) return;
+  const int dm = a.dm, dt = a.dt, da = a.da, gm = dm >> 2, gt = dt >> 2;
+  const int D = dm + dt;   // row width of both q_in and kv_in
+  {
+    const int64_t node = a.q_node[q];
+    for (int g = lane; g < gm + gt; g += 64) {
+      if (g < gm) {
+        const float4 v = *(const float4*)(mem + node * dm + 4 * g);
+        *(float4*)(a.q_in + q * D + 4 * g) = v;
+        *(float4*)(a.m_in + q * (da + dm) + da + 4 * g) = v;
+      } else {
+        const int j = 4 * (g - gm);
+        float4 o;
+        o.x = cosf(time_arg(a.tw[j], 0.f, a.tb[j]));
+        o.y = cosf(time_arg(a.tw[j + 1], 0.f, a.tb[j + 1]));
+        o.z = cosf(time_arg(a.tw[j + 2], 0.f, a.tb[j + 2]));
+        o.w = cosf(time_arg(a.tw[j + 3], 0.f, a.tb[j + 3]));
+        *(float4*)(a.q_in + q * D + dm + j) = o;
+      }
+    }
+  }
+  const int c = a.cnt[q];
+  const int64_t off = a.pair_off[q];
+  const float tau = a.q_t[q];
+  const int32_t my_nb = lane < c ? a.nbr[q * a.k + lane] : 0;
+  const float my_delta = lane < c ? tau - a.nt[q * a.k + lane] : 0.f;
+  if (lane < c) {
+    a.pair_nbr[off + lane] = my_nb;
+    a.pair_delta[off + lane] = my_delta;
+  }
+  const int nm = c * gm;
+  for (int e0 = 0; e0 < nm; e0 += 64 * GV_UNROLL) {
+    float4 v[GV_UNROLL];
+    int64_t dst[GV_UNROLL];
+#pragma unroll
+    for (int u = 0; u < GV_UNROLL; ++u) {
+      const int e = e0 + 64 * u + lane;
+      const int ec = e < nm ? e : nm - 1;   // a valid group, stored only when e < nm
+      const int sl = ec / gm, g = ec - sl * gm;
+      const int64_t nb = __shfl(my_nb, sl, 64);
+      v[u] = *(const float4*)(mem + nb * dm + 4 * g);
+      dst[u] = (off + sl) * D + 4 * g;
+    }
+#pragma unroll
+    for (int u = 0; u < GV_UNROLL; ++u)
+      if (e0 + 64 * u + lane < nm) *(float4*)(a.kv_in + dst[u]) = v[u];
+  }
+  const int ntg = c * gt;
+  for (int e0 = 0; e0 < ntg; e0 += 64) {
+    const int e = e0 + lane;
+    const int ec = e < ntg ? e : ntg - 1;
+    const int sl = ec / gt, g = ec - sl * gt;
+    const float delta = __shfl(my_delta, sl, 64);
+    if (e < ntg) {
+      const int j = 4 * g;
+      float4 o;
+      o.x = cosf(time_arg(a.tw[j], delta, a.tb[j]));
+      o.y = cosf(time_arg(a.tw[j + 1], delta, a.tb[j + 1]));
+      o.z = cosf(time_arg(a.tw[j + 2], delta, a.tb[j + 2]));
+      o.w = cosf(time_arg(a.tw[j + 3], delta, a.tb[j + 3]));
+      *(float4*)(a.kv_in + (off + sl) * D + dm + j) = o;
+    }
+  }
 }
 
 constexpr int MAX_DH_CHUNKS = 2;   // head width <= 128
@@ -767,7 +842,11 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
   const unsigned gq = (unsigned)cdiv(sh.Q, 4);
   const GatherArgs ga{q_node, nbr, neid, n_q, sv.cnt, sv.pair_off, nt, q_t, edge_feat, tw, tb, max_q, sh.k, sh.dm,
                       sh.de, sh.dt, sh.da, bf, sv.q_in, sv.m_in, sv.kv_in, sv.pair_delta, sv.pair_nbr};
-  if (!bf)
+  const bool v4 = !bf && sh.de == 0 && sh.dm % 4 == 0 && sh.dt % 4 == 0 && sh.da % 4 == 0 &&
+                  ((uintptr_t)memory & 15) == 0;
+  if (v4)
+    k_attn_gather_v4<<<gq, 256, 0, s>>>(ga, (const float*)memory);
+  else if (!bf)
     k_attn_gather<float><<<gq, 256, 0, s>>>(ga, (const float*)memory);
   else
     k_attn_gather<uint16_t><<<gq, 256, 0, s>>>(ga, (const uint16_t*)memory);
