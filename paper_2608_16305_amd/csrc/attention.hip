@@ -213,8 +213,17 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
   if (q >= eff_count(a.max_q, a.n_q)) return;
   const int dm = a.dm, dt = a.dt, da = a.da, gm = dm >> 2, gt = dt >> 2;
   const int D = dm + dt;   // row width of both q_in and kv_in
+  // every per-query scalar first, so that their loads overlap the query row's
+  const int64_t node = a.q_node[q];
+  const int c = a.cnt[q];
+  const int64_t off = a.pair_off[q];
+  const float tau = a.q_t[q];
+  // loaded on lane < k (in bounds of the [max_q, k] arrays), so they need not wait for c
+  const int32_t nb_raw = lane < a.k ? a.nbr[q * a.k + lane] : 0;
+  const float t_raw = lane < a.k ? a.nt[q * a.k + lane] : 0.f;
+  const int32_t my_nb = lane < c ? nb_raw : 0;
+  const float my_t = lane < c ? t_raw : 0.f;
   {
-    const int64_t node = a.q_node[q];
     for (int g = lane; g < gm + gt; g += 64) {
       if (g < gm) {
         const float4 v = *(const float4*)(mem + node * dm + 4 * g);
@@ -231,11 +240,7 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
       }
     }
   }
-  const int c = a.cnt[q];
-  const int64_t off = a.pair_off[q];
-  const float tau = a.q_t[q];
-  const int32_t my_nb = lane < c ? a.nbr[q * a.k + lane] : 0;
-  const float my_delta = lane < c ? tau - a.nt[q * a.k + lane] : 0.f;
+  const float my_delta = lane < c ? tau - my_t : 0.f;
   if (lane < c) {
     a.pair_nbr[off + lane] = my_nb;
     a.pair_delta[off + lane] = my_delta;
