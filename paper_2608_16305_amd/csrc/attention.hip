@@ -364,6 +364,101 @@ __global__ __launch_bounds__(256) void k_attn_core(const float* __restrict__ qv,
   }
 }
 
+// Wave per query, for one or two heads, d_attn <= 128 and divisible by 4, and at most 2 NP slots.
+// A query's K|V rows are contiguous, so each pass takes two slots (slot 2 p + half), 32 lanes per
+// slot: lane g of a half holds the row's 4-float group g of K and of V (16-byte loads, all issued
+// first; a slot past the count reads row 0, and its products are dropped).  A head's score is the half's 32-lane
+// sum of the groups' partial dot products; the softmax runs over each lane's slots and then the two
+// halves; the probability-weighted sum of the values stays in the lane of its group, the halves
+// added at the end.
+template <int NP, int H>
+__global__ __launch_bounds__(256) void k_attn_core_v4(const float* __restrict__ qv, const float* __restrict__ KV,
+                                                      const int32_t* __restrict__ cnt,
+                                                      const int32_t* __restrict__ pair_off,
+                                                      const int32_t* __restrict__ n_q, int64_t max_q, int k, int da,
+                                                      int bf16, float* __restrict__ P, float* __restrict__ attn) {
+  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (q >= eff_count(max_q, n_q)) return;
+  const int half = lane >> 5, g = lane & 31;
+  const bool gon = 4 * g < da;
+  const int gc = gon ? g : 0;
+  const int dh = da / H;
+  const float scale = 1.0f / sqrtf((float)dh);
+  const int c = cnt[q];
+  const int64_t off = pair_off[q];
+  const float4 q4 = *(const float4*)(qv + q * da + 4 * gc);
+  float4 kr[NP], vr[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int j = 2 * p + half;
+    const int64_t row = j < c ? off + j : 0;
+    kr[p] = *(const float4*)(KV + row * 2 * da + 4 * gc);
+    vr[p] = *(const float4*)(KV + row * 2 * da + da + 4 * gc);
+  }
+  // head of each element of the group (a group may straddle the head boundary)
+  int hd[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) hd[e] = H == 1 ? 0 : (4 * g + e >= dh ? 1 : 0);
+  const float qe[4] = {q4.x, q4.y, q4.z, q4.w};
+  float pj[NP][H];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const float ke[4] = {kr[p].x, kr[p].y, kr[p].z, kr[p].w};
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      float v = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v += (gon && hd[e] == h) ? qe[e] * ke[e] : 0.f;
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
+      pj[p][h] = v * scale;
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+      if (2 * p + half < c) m = fmaxf(m, pj[p][h]);
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    float den = 0.f;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      pj[p][h] = 2 * p + half < c ? expf(pj[p][h] - m) : 0.f;
+      den += pj[p][h];
+    }
+    den += __shfl_xor(den, 32, 64);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      pj[p][h] = den > 0.f ? pj[p][h] / den : 0.f;
+      const int j = 2 * p + half;
+      if (g == 0 && j < k) P[(q * H + h) * k + j] = pj[p][h];
+    }
+  }
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const float ve[4] = {vr[p].x, vr[p].y, vr[p].z, vr[p].w};
+    const bool on = 2 * p + half < c;   // a slot past the count read row 0, whatever it holds
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float t = ((H == 1 || hd[e] == 0) ? pj[p][0] : pj[p][H - 1]) * ve[e];
+      acc[e] += on ? t : 0.f;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) acc[e] += __shfl_xor(acc[e], 32, 64);
+  if (half == 0 && gon) {
+    float4 o;
+    o.x = pack_val(acc[0], bf16);
+    o.y = pack_val(acc[1], bf16);
+    o.z = pack_val(acc[2], bf16);
+    o.w = pack_val(acc[3], bf16);
+    *(float4*)(attn + q * da + 4 * g) = o;
+  }
+}
+
 // Wave per query: gradients of the softmax-weighted sum and of the scores.
 //   dV_j = p_j da_h;  dp_j = da_h . V_j;  ds_j = p_j (dp_j - sum_i p_i dp_i)
 //   dq_h = sum_j ds_j K_jh / sqrt(dh);  dK_j = ds_j q_h / sqrt(dh)
@@ -865,7 +960,20 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
                                      sh.P, sv.n_valid, 2 * sh.da, sh.Dkv, false, s));
   {
     TimedScope ts("k_attn_core", s);
-    if (sh.dh <= 64)
+    const bool v4 = sh.da % 4 == 0 && sh.da <= 128 && sh.H <= 2 && sh.k <= 20;
+    if (v4 && sh.k <= 10 && sh.H == 2)
+      k_attn_core_v4<5, 2><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, bf, sv.p,
+                                              sv.attn);
+    else if (v4 && sh.H == 2)
+      k_attn_core_v4<10, 2><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, bf, sv.p,
+                                               sv.attn);
+    else if (v4 && sh.k <= 10)
+      k_attn_core_v4<5, 1><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, bf, sv.p,
+                                              sv.attn);
+    else if (v4)
+      k_attn_core_v4<10, 1><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, bf, sv.p,
+                                               sv.attn);
+    else if (sh.dh <= 64)
       k_attn_core<1><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.cnt, sv.pair_off, n_q, max_q, sh.k, sh.da, sh.H, bf, sv.p,
                                         sv.attn);
     else
