@@ -534,6 +534,105 @@ __global__ __launch_bounds__(256) void k_attn_core_bwd(const float* __restrict__
   }
 }
 
+// The backward of k_attn_core_v4 in its layout (two slots per pass, lane g of a half holding
+// 4-float group g of K, V, q and dattn): dp per slot and head as a 32-lane sum, the softmax
+// backward over each lane's slots and the two halves, dK and dV of a slot stored by the lanes of
+// its half as 16-byte groups, dq summed over each lane's slots and then the halves.  A slot past
+// the count reads row 0, and every value it could contribute is dropped by a select.
+template <int NP, int H>
+__global__ __launch_bounds__(256) void k_attn_core_bwd_v4(const float* __restrict__ qv, const float* __restrict__ KV,
+                                                          const float* __restrict__ P,
+                                                          const float* __restrict__ dattn,
+                                                          const int32_t* __restrict__ cnt,
+                                                          const int32_t* __restrict__ pair_off,
+                                                          const int32_t* __restrict__ n_q, int64_t max_q, int k,
+                                                          int da, float* __restrict__ dKV, float* __restrict__ dqv) {
+  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (q >= eff_count(max_q, n_q)) return;
+  const int half = lane >> 5, g = lane & 31;
+  const bool gon = 4 * g < da;
+  const int gc = gon ? g : 0;
+  const int dh = da / H;
+  const float scale = 1.0f / sqrtf((float)dh);
+  const int c = cnt[q];
+  const int64_t off = pair_off[q];
+  const float4 q4 = *(const float4*)(qv + q * da + 4 * gc);
+  const float4 g4 = *(const float4*)(dattn + q * da + 4 * gc);
+  float4 kr[NP], vr[NP];
+  float pp[NP][H];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int j = 2 * p + half;
+    const bool on = j < c;
+    const int64_t row = on ? off + j : 0;
+    kr[p] = *(const float4*)(KV + row * 2 * da + 4 * gc);
+    vr[p] = *(const float4*)(KV + row * 2 * da + da + 4 * gc);
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const float v = P[(q * H + h) * k + (on ? j : 0)];
+      pp[p][h] = on ? v : 0.f;
+    }
+  }
+  int hd[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) hd[e] = H == 1 ? 0 : (4 * g + e >= dh ? 1 : 0);
+  const float qe[4] = {q4.x, q4.y, q4.z, q4.w};
+  const float ge[4] = {g4.x, g4.y, g4.z, g4.w};
+  // dp_j = dattn_h . V_j (32-lane sums), then sdp_h = sum_j p_j dp_j over both halves
+  float ds[NP][H];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const float ve[4] = {vr[p].x, vr[p].y, vr[p].z, vr[p].w};
+    const bool on = 2 * p + half < c;
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      float v = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v += (gon && hd[e] == h) ? ge[e] * ve[e] : 0.f;
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
+      ds[p][h] = on ? v : 0.f;
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    float sdp = 0.f;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) sdp += pp[p][h] * ds[p][h];
+    sdp += __shfl_xor(sdp, 32, 64);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) ds[p][h] = pp[p][h] * (ds[p][h] - sdp);
+  }
+  float dq[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int j = 2 * p + half;
+    const bool on = j < c;
+    const float ke[4] = {kr[p].x, kr[p].y, kr[p].z, kr[p].w};
+    float dk[4], dv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float dsh = (H == 1 || hd[e] == 0) ? ds[p][0] : ds[p][H - 1];
+      const float ph = (H == 1 || hd[e] == 0) ? pp[p][0] : pp[p][H - 1];
+      const float t = dsh * ke[e];
+      dq[e] += on ? t : 0.f;
+      dk[e] = dsh * qe[e] * scale;
+      dv[e] = ph * ge[e];
+    }
+    if (on && gon) {
+      float* dst = dKV + (off + j) * 2 * da + 4 * g;
+      *(float4*)dst = make_float4(dk[0], dk[1], dk[2], dk[3]);
+      *(float4*)(dst + da) = make_float4(dv[0], dv[1], dv[2], dv[3]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) dq[e] += __shfl_xor(dq[e], 32, 64);
+  if (half == 0 && gon)
+    *(float4*)(dqv + q * da + 4 * g) =
+        make_float4(dq[0] * scale, dq[1] * scale, dq[2] * scale, dq[3] * scale);
+}
+
 // [dW_k; dW_v] and [db_k; db_v] from the stacked weight gradient.
 __global__ void k_split_kv_grads(const float* __restrict__ dW, const float* __restrict__ db, int da, int Dkv,
                                  float* __restrict__ dWk, float* __restrict__ dWv, float* __restrict__ dbk,
@@ -1191,7 +1290,21 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     // softmax-weighted sum and scores
     {
       TimedScope ts("k_attn_core_bwd", s);
-      if (sh.dh <= 64)
+      const bool v4 = sh.da % 4 == 0 && sh.da <= 128 && sh.H <= 2 && sh.k <= 20;
+      const unsigned gq = (unsigned)cdiv(Q, 4);
+      if (v4 && sh.k <= 10 && sh.H == 2)
+        k_attn_core_bwd_v4<5, 2><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q, max_q,
+                                                    sh.k, da, b.dKV, b.dqv);
+      else if (v4 && sh.H == 2)
+        k_attn_core_bwd_v4<10, 2><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q, max_q,
+                                                     sh.k, da, b.dKV, b.dqv);
+      else if (v4 && sh.k <= 10)
+        k_attn_core_bwd_v4<5, 1><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q, max_q,
+                                                    sh.k, da, b.dKV, b.dqv);
+      else if (v4)
+        k_attn_core_bwd_v4<10, 1><<<gq, 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off, n_q, max_q,
+                                                     sh.k, da, b.dKV, b.dqv);
+      else if (sh.dh <= 64)
         k_attn_core_bwd<1><<<(unsigned)cdiv(Q, 4), 256, 0, s>>>(sv.qv, sv.KV, sv.p, b.dattn, sv.cnt, sv.pair_off,
                                                                  n_q, max_q, sh.k, da, sh.H, b.dKV, b.dqv);
       else
