@@ -1195,7 +1195,7 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
     MTGNN_TRY(linear_dx_timegrad<site::KvDx>(b.dKV, 2 * da, wofs(sv.W_kv, dm + sh.de), wt, sh.Dkv, P, sv.n_valid,
                                              2 * da, dt, nullptr, sv.pair_delta, tw, tb, b.tg_part2, s));
     if (!q_closed)
-      MTGNN_TRY(timegrad_reduce_blocks2(b.tg_part, Q, n_q, b.tg_part2, P, sv.n_valid, 64 * G_WM, dt, d_time_w,
+      MTGNN_TRY(timegrad_reduce_blocks2(b.tg_part, Q, n_q, b.tg_part2, P, sv.n_valid, G_TG_ROWS, dt, d_time_w,
                                         d_time_b, s));
   }
   // weight gradients of the query, output and merge layers, one batch over the query rows
@@ -1207,7 +1207,7 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
     MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
   }
   if (dt > 0 && q_closed)
-    MTGNN_TRY(timegrad_reduce_slots_q(b.tg_part2, P, sv.n_valid, 64 * G_WM, dt, g->b_q, (const float*)p->W_q, sh.Dq,
+    MTGNN_TRY(timegrad_reduce_slots_q(b.tg_part2, P, sv.n_valid, G_TG_ROWS, dt, g->b_q, (const float*)p->W_q, sh.Dq,
                                       dm, da, tw, tb, d_time_w, d_time_b, s));
   // key/value projection over the compact slots (stacked [W_k; W_v]); the output-stationary kernel's
   // reduce writes the W_k and W_v halves (rows < d_a, rows >= d_a) straight to their gradients

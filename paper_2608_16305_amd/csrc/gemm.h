@@ -272,16 +272,16 @@ struct TileVec {
   __device__ __forceinline__ void store(float* lds, int tid) const { store_from(lds, tid, v); }
 };
 
-// Time-gradient epilogue of a 64-row block (4 waves x 16 rows): instead of C,
+// Time-gradient epilogue of a (64 WM)-row block (4 waves x WM 16-row tiles): instead of C,
 // write the column sums over the block's rows of  g = -C(i,j) sin(arg_ij)  and of
 // g * delta_i to tg_part[row block][0 / 1][j].  red: 8 BN floats of LDS that no
 // wave reads any more.
-template <int BN>
+template <int BN, int WM>
 __device__ __forceinline__ void gemm_store_timegrad(const GemmArgs& g, const TileCoord tc, int64_t M,
-                                                    const f32x4 (&acc)[BN / 16], float* red) {
+                                                    const f32x4 (&acc)[WM][BN / 16], float* red) {
   constexpr int NT = BN / 16;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int64_t row0 = tc.x * 64, col0 = tc.y * BN;
+  const int64_t row0 = tc.x * 64 * WM, col0 = tc.y * BN;
   float* red_w = red;
   float* red_b = red + 4 * BN;
 #pragma unroll
@@ -290,12 +290,14 @@ __device__ __forceinline__ void gemm_store_timegrad(const GemmArgs& g, const Til
     float cw = 0.f, cb = 0.f;
     if (gj < g.N) {
 #pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t gi = row0 + wid * 16 + 4 * (lane >> 4) + r;
+        const int64_t gi = row0 + (wid * WM + i) * 16 + 4 * (lane >> 4) + r;
         if (gi >= M) continue;
         const float d = g.tg_delta ? g.tg_delta[gi] : 0.f;
         const float sn = g.tg_sin ? g.tg_sin[gi * g.N + gj] : sinf(time_arg(g.tg_w[gj], d, g.tg_b[gj]));
-        const float gv = acc[j][r] * -sn;
+        const float gv = acc[i][j][r] * -sn;
         cb += gv;
         cw += gv * d;
       }
@@ -501,8 +503,8 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, const TileCoord tc)
   }
 
   if constexpr (TGE) {   // time-gradient epilogue (tg_* arguments)
-    static_assert(8 * BN <= NBUF * LA::SIZE && WM == 1, "time-gradient epilogue scratch");
-    gemm_store_timegrad<BN>(g, tc, M, acc[0], &As[0][0]);   // the operand tiles are no longer read
+    static_assert(8 * BN <= NBUF * LA::SIZE, "time-gradient epilogue scratch");
+    gemm_store_timegrad<BN, WM>(g, tc, M, acc, &As[0][0]);   // the operand tiles are no longer read
     return;
   }
   gemm_store<BN, WM>(g, tc, M, acc);
@@ -541,6 +543,10 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm_batch(GemmBatch b) {
 
 // Tile shape used by the library's launches.
 constexpr int G_WM = 1, G_NBUF = 2;
+// Row tiles per wave of the time-gradient products (64-row blocks; 128-row blocks, with half the
+// weight-strip reads and partial sums, measured slower on the neighbour-slot product: 60 vs 52 us).
+constexpr int G_WM_TG = 1;
+constexpr int G_TG_ROWS = 64 * G_WM_TG;   // rows per partial of a time-gradient product
 
 // Column `ones_col` (if >= 0) goes to col_out[i] instead of out.
 __global__ void k_splitk_reduce(const float* __restrict__ part, int64_t split_stride, int nsplit, int64_t rows,
@@ -578,7 +584,7 @@ inline bool vec_ok(const void* p, int64_t other_stride, size_t esz) {
 template <class Site, int BN, bool VEC, typename TA, typename TB, bool AK, bool BK, int KSTEP = G_BK,
           bool TGE = false>
 void gemm_kernel_launch(const GemmArgs& g, dim3 grid, hipStream_t s) {
-  k_gemm<Site, BN, G_WM, KSTEP, G_NBUF, VEC, TA, TB, AK, BK, 1, TGE><<<grid, G_THREADS, 0, s>>>(g);
+  k_gemm<Site, BN, TGE ? G_WM_TG : G_WM, KSTEP, G_NBUF, VEC, TA, TB, AK, BK, 1, TGE><<<grid, G_THREADS, 0, s>>>(g);
 }
 
 template <class Site, bool VEC, typename TA, typename TB, bool AK, bool BK>
@@ -655,7 +661,8 @@ mtgnn_status gemm_launch_t(const GemmArgs& g0, int ksplit, hipStream_t s) {
   GemmArgs g = g0;
   gemm_set_vec_flags<TA, TB, AK, BK>(g);
   const int bn = g.tile_bn > 0 ? g.tile_bn : gemm_tile_width(g.M, g.N, ksplit);
-  dim3 grid((unsigned)cdiv(g.M, 64 * G_WM), (unsigned)cdiv(g.N, bn), (unsigned)(ksplit < 1 ? 1 : ksplit));
+  const int64_t bm = (AK && !BK && g.tg_part != nullptr) ? G_TG_ROWS : 64 * G_WM;   // time-gradient form: taller
+  dim3 grid((unsigned)cdiv(g.M, bm), (unsigned)cdiv(g.N, bn), (unsigned)(ksplit < 1 ? 1 : ksplit));
   const bool vec = gemm_vec_ok<TA, TB, AK, BK>(g);
   TimedScope ts(Site::name, s);
   if (vec) gemm_bn_launch<Site, true, TA, TB, AK, BK>(g, bn, grid, s);
@@ -783,10 +790,10 @@ mtgnn_status linear_dx(const float* dy, int64_t lddy, const void* W, int w_dtype
   return gemm_launch<Site, true, false>(g, MTGNN_F32, w_dtype, 1, s);
 }
 
-// Time-gradient form of linear_dx: dphi = dy W is not stored; each 64-row block
+// Time-gradient form of linear_dx: dphi = dy W is not stored; each G_TG_ROWS-row block
 // writes its column sums of -dphi sin(arg) (and times delta) to part[block][2][K].
 // Rows come from M (clamped by M_dev); part needs gemm_tg_blocks(M) * 2 * K floats.
-inline int64_t gemm_tg_blocks(int64_t M) { return cdiv(M < 1 ? 1 : M, 64 * G_WM); }
+inline int64_t gemm_tg_blocks(int64_t M) { return cdiv(M < 1 ? 1 : M, G_TG_ROWS); }
 template <class Site = site::Generic>
 mtgnn_status linear_dx_timegrad(const float* dy, int64_t lddy, const void* W, int w_dtype, int64_t ldw, int64_t M,
                                 const int32_t* M_dev, int64_t N, int64_t K, const float* sin_saved,
