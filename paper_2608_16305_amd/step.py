@@ -83,14 +83,16 @@ class TGNStep:
         self._bind(0)
         self._pre = None   # (lo, hi) of the batch whose aggregation and messages fill the other set
         self.gru_save = M.alloc_bytes(M.save_bytes(M.OP_GRU_UPDATE, d, R, 0), dev)
-        self.q_node = torch.empty(Q, **i32)
-        self.q_t = torch.empty(Q, **f32)
-        self.n_q = torch.zeros(1, **i32)
-        self.nbr = torch.empty(Q, k, **i32)
-        self.nt = torch.empty(Q, k, **f32)
-        self.neid = torch.empty(Q, k, **i32)
+        # two sets of the query-side buffers (queries, their samples, the attention's save): with overlap,
+        # a step's queries fill the set the step before last used (see step())
+        self._qsets = [dict(q_node=torch.empty(Q, **i32), q_t=torch.empty(Q, **f32), n_q=torch.zeros(1, **i32),
+                            nbr=torch.empty(Q, k, **i32), nt=torch.empty(Q, k, **f32), neid=torch.empty(Q, k, **i32),
+                            attn_save=M.alloc_bytes(M.save_bytes(M.OP_TEMPORAL_ATTN, d, 0, Q), dev))
+                       for _ in range(2)]
+        self._qbind(0)
+        self._q_chain = 0   # overlapped step() calls in a row (nothing else in between)
+        self._in_step = False
         self.z = torch.empty(Q, w.d_attn, **f32)
-        self.attn_save = M.alloc_bytes(M.save_bytes(M.OP_TEMPORAL_ATTN, d, 0, Q), dev)
         self.d_mem = torch.empty(R, w.d_mem, **f32)
         self.dmsg_time = torch.empty(R, max(w.d_time, 1), **f32)
         self.grads = {n: torch.empty(tuple(self.params[n].shape), **f32)
@@ -124,6 +126,12 @@ class TGNStep:
         f = self.flags[lo:hi] if self.flags is not None else None
         return M.batch(self.src[lo:hi], self.dst[lo:hi], self.t[lo:hi], self.eid[lo:hi], f)
 
+    def _qbind(self, i):
+        """Make query set i the current one (self.q_node, q_t, n_q, nbr, nt, neid, attn_save)."""
+        self._qcur = i
+        for k, v in self._qsets[i].items():
+            setattr(self, k, v)
+
     def _bind(self, i):
         """Make buffer set i the current one (self.uniq, winner, n_uniq, msg, dt)."""
         self._cur = i
@@ -147,6 +155,7 @@ class TGNStep:
                            self.gru_save if save else None, self.ws, stream=self.ts)
 
     def memory_phase(self, lo, hi, save=True):
+        self._q_chain = self._q_chain if self._in_step else 0
         self._pre = None   # the memory changes: nothing prepared from the old state stays valid
         self._messages(lo, hi, self._sets[self._cur], self.ws, self.ts)
         self._gru(lo, hi, save)
@@ -154,6 +163,7 @@ class TGNStep:
     def queries(self, lo, hi, stream):
         """Queries of the batch's target events, their most-recent-k neighbours and the attention's
         per-query valid-slot counts and offsets: no memory read."""
+        self._q_chain = self._q_chain if self._in_step else 0
         b = self._batch(lo, hi)
         M.mtgnn_build_queries(b, self.neg[lo:hi], self.q_node, self.q_t, self.n_q, self.ws_q, stream=stream)
         M.mtgnn_sample_recent(self.csr_off, self.csr_nbr, self.csr_t, self.csr_eid, self.w.n_nodes, self.q_node,
@@ -163,9 +173,11 @@ class TGNStep:
 
     def prepare_weights(self, stream):
         """The attention's weight copies (stacked K|V, padded merge layers): they read only the weights."""
+        self._q_chain = self._q_chain if self._in_step else 0
         M.mtgnn_temporal_attn_prepare_weights(self.ap, self.d, self.attn_save, stream=stream)
 
     def embed(self, lo, hi, queries_done=False):
+        self._q_chain = self._q_chain if self._in_step else 0
         p, s = self.params, self.ts
         if not queries_done:
             self.prepare_weights(s)
@@ -175,6 +187,7 @@ class TGNStep:
                                        self.attn_save, stream=s)
 
     def backward(self, dz):
+        self._q_chain = self._q_chain if self._in_step else 0
         p, g, s = self.params, self.grads, self.ts
         if self.overlap:
             # d_mem, then the GRU backward, on the second stream while the attention parameter gradients
@@ -210,6 +223,7 @@ class TGNStep:
     def step(self, b, dz):
         """One training step on batch b: memory phase (lag order), embedding, backward."""
         elo, ehi = self.batch_range(b)
+        self._in_step = True
         if self.lag == 1:
             mlo, mhi = self.batch_range(b - 1) if b > 0 else (0, 0)
         else:
@@ -219,8 +233,13 @@ class TGNStep:
             # read only the batch, the adjacency and the weights); joined before the attention reads memory
             main = self.ts if self.ts is not None else torch.cuda.current_stream(self.dev)
             side = self.side_stream
-            self.q_fork.record(main)
-            self.q_fork.wait(side)
+            # the queries fill the other query set, last used by the step before the previous one: after
+            # an overlapped step, all its uses here precede that step's m_done, which the second stream
+            # waited for, so no fork is needed (the first step, or after other calls, forks)
+            self._qbind(1 - self._qcur)
+            if self._q_chain == 0:
+                self.q_fork.record(main)
+                self.q_fork.wait(side)
             self.queries(elo, ehi, side)
             self.q_join.record(side)
             self.prepare_weights(main)   # one launch here, so the second stream's chain is shorter
@@ -228,7 +247,8 @@ class TGNStep:
                 # this memory batch's aggregation and messages were built during the previous step's
                 # embedding, from the memory as it is now: only the GRU update is left
                 self._bind(1 - self._cur)
-                self.pre_join.wait(main)
+                if self._q_chain == 0:   # else implied: the previous step's backward waited for g_join,
+                    self.pre_join.wait(main)   # recorded on the second stream after these messages
                 self._pre = None
                 self._gru(mlo, mhi)
             else:
@@ -255,3 +275,5 @@ class TGNStep:
             self.memory_phase(mlo, mhi)
             self.embed(elo, ehi)
         self.backward(dz)
+        self._in_step = False
+        self._q_chain = self._q_chain + 1 if self.overlap else 0
