@@ -847,6 +847,95 @@ __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   flush(cnt);
 }
 
+// k_segsum_tiles with 16-byte groups (d_mem and d_attn divisible by 4, W <= 512): lane l holds
+// the row's 4-column groups l and l + 64, so a neighbour slot's row is two loads per lane and a
+// query's one.  Every column's sum runs over the positions in the same order as k_segsum_tiles,
+// so the results are bitwise the same.
+__device__ __forceinline__ float4 f4add(float4 a, float4 b) {
+  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+// A finished segment's sums (groups qa and qb of this lane): a whole segment to D / S, a piece that
+// began before the tile to head[tile], one that continues past it to tail[tile].
+__device__ __forceinline__ void seg_flush_v4(const SegCtx& c, int64_t tile, uint32_t cur, bool before, bool after,
+                                             int qa, int qb, float4 acc_a, float4 acc_b) {
+  const int W = c.dm + c.w2, W4 = W >> 2, dm4 = c.dm >> 2;
+  if (!before && !after) {
+    float* row_d = c.D + (int64_t)cur * c.dm;
+    float* row_s = c.S + (int64_t)cur * W;
+    if (qa < dm4) *(float4*)(row_d + 4 * qa) = acc_a;
+    else if (qa < W4) *(float4*)(row_s + 4 * qa) = acc_a;
+    if (qb < dm4) *(float4*)(row_d + 4 * qb) = acc_b;
+    else if (qb < W4) *(float4*)(row_s + 4 * qb) = acc_b;
+    return;
+  }
+  float* dst = before ? c.head + tile * W : c.tail + tile * W;
+  if (qa < W4) *(float4*)(dst + 4 * qa) = acc_a;
+  if (qb < W4) *(float4*)(dst + 4 * qb) = acc_b;
+}
+
+__global__ __launch_bounds__(256) void k_segsum_tiles_v4(SegCtx c) {
+  const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int64_t p0 = tile * SEG_TILE;
+  if (p0 >= c.n_occ) return;
+  const int cnt = (int)min((int64_t)SEG_TILE, c.n_occ - p0);
+  const int W = c.dm + c.w2, W4 = W >> 2, dm4 = c.dm >> 2;
+  const int qa = lane, qb = lane + 64;   // this lane's column groups
+  const uint32_t my_key = lane < cnt ? c.keys[p0 + lane] : c.sentinel;
+  const uint32_t my_val = lane < cnt ? c.vals[p0 + lane] : 0u;
+  const uint32_t key_before = p0 > 0 ? c.keys[p0 - 1] : c.sentinel;
+  const uint32_t key_after = p0 + cnt < c.n_occ ? c.keys[p0 + cnt] : c.sentinel;
+  uint32_t cur = __shfl(my_key, 0, 64);
+  if (cur == c.sentinel) return;   // sentinels sort last: nothing in this tile
+  const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  // groups this lane loads from a query row (columns < dm) and from a slot row (columns >= dm)
+  const bool qa_q = qa < dm4, qb_q = qb < dm4;
+  const bool qa_s = qa >= dm4 && qa < W4, qb_s = qb >= dm4 && qb < W4;
+  int start = 0;
+  float4 acc_a = z4, acc_b = z4;
+  for (int q0 = 0; q0 < cnt; q0 += SEG_PREFETCH) {
+    float4 ra[SEG_PREFETCH], rb[SEG_PREFETCH];
+#pragma unroll
+    for (int u = 0; u < SEG_PREFETCH; ++u) {
+      const int p = q0 + u;
+      const uint32_t k = __shfl(my_key, p, 64);
+      const uint32_t o = __shfl(my_val, p, 64);
+      ra[u] = z4;
+      rb[u] = z4;
+      if (p < cnt && k != c.sentinel) {
+        if ((int64_t)o < c.max_q) {
+          const float* src = c.dhq + (int64_t)o * c.ldq;
+          if (qa_q) ra[u] = *(const float4*)(src + 4 * qa);
+          if (qb_q) rb[u] = *(const float4*)(src + 4 * qb);
+        } else {
+          const float* src = c.dkv + ((int64_t)o - c.max_q) * c.w2 - c.dm;   // column col at src[col]
+          if (qa_s) ra[u] = *(const float4*)(src + 4 * qa);
+          if (qb_s) rb[u] = *(const float4*)(src + 4 * qb);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SEG_PREFETCH; ++u) {
+      const int p = q0 + u;
+      if (p < cnt) {
+        const uint32_t k = __shfl(my_key, p, 64);
+        if (k != cur) {
+          seg_flush_v4(c, tile, cur, start == 0 && key_before == cur, false, qa, qb, acc_a, acc_b);
+          if (k == c.sentinel) return;
+          cur = k;
+          start = p;
+          acc_a = z4;
+          acc_b = z4;
+        }
+        acc_a = f4add(acc_a, ra[u]);
+        acc_b = f4add(acc_b, rb[u]);
+      }
+    }
+  }
+  seg_flush_v4(c, tile, cur, start == 0 && key_before == cur, key_after == cur, qa, qb, acc_a, acc_b);
+}
+
 // Block b (FIX_WAVES waves): wave w first zeroes row FIX_WAVES b + w if that
 // row has no occurrence.  Then, if the row at the end of tile b starts in
 // tile b and continues past it (rows inside one tile were written whole), the
@@ -1143,8 +1232,10 @@ mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSav
     c.dhq = b.dm_in + da; c.ldq = ldm; c.dkv = b.dKV; c.dm = dm; c.w2 = 2 * da;
     c.S = b.S; c.D = d_mem; c.head = b.head; c.tail = b.tail;
     const int64_t ntiles = cdiv(n_occ, SEG_TILE);
-    {
-      const unsigned gt = (unsigned)cdiv(ntiles, 4);
+    const unsigned gt = (unsigned)cdiv(ntiles, 4);
+    if (dm % 4 == 0 && da % 4 == 0 && dm + 2 * da <= 512) {   // 16-byte aligned rows and groups
+      k_segsum_tiles_v4<<<gt, 256, 0, s>>>(c);
+    } else {
       switch (cdiv(dm + 2 * da, 64)) {   // column chunks per lane (validation keeps the width <= 512)
         case 1: k_segsum_tiles<1><<<gt, 256, 0, s>>>(c); break;
         case 2: k_segsum_tiles<2><<<gt, 256, 0, s>>>(c); break;
