@@ -221,11 +221,15 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
  * one stream, and the results are bitwise the same.
  *   _prepare  -- from nbr (valid slots lead each row) and the weights, writes
  *                into save the stacked [W_k; W_v] and [b_k; b_v], the padded
- *                merge-layer weights (float32) and the per-query valid-slot
- *                counts, their exclusive prefix sums and the valid total;
- *                ws as for mtgnn_temporal_attn.  It is exactly
- *                _prepare_weights (the weight copies: they read only the
- *                weights, and their place in save does not depend on max_q)
+ *merge-layer weights (float32), the query projection's constant
+ *                term b_q + W_q[:, d_mem:] cos(time_b) (every query's time
+ *                input is the encoding of 0, so its share is one vector; it
+ *                needs time_w and time_b, the forward's) and the per-query
+ *                valid-slot counts, their exclusive prefix sums and the
+ *                valid total; ws as for mtgnn_temporal_attn.  It is exactly
+ *                _prepare_weights (the weight copies and that constant: they
+ *                read only the parameters, and their place in save does not
+ *                depend on max_q)
  *                followed by _prepare_slots (the counts, offsets and total);
  *                the two may run on different streams, in either order.
  *   _prepared -- the rest of the forward, reading what _prepare wrote into
@@ -233,9 +237,11 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
  *                caller orders it after _prepare (same stream, or an event).
  * Arguments, layouts and errors as for mtgnn_temporal_attn. */
 mtgnn_status mtgnn_temporal_attn_prepare(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
-                                         const mtgnn_attn_params* params, const mtgnn_dims* d, void* save, void* ws,
-                                         size_t ws_bytes, hipStream_t stream);
-mtgnn_status mtgnn_temporal_attn_prepare_weights(const mtgnn_attn_params* params, const mtgnn_dims* d, void* save,
+                                         const mtgnn_attn_params* params, const float* time_w, const float* time_b,
+                                         const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes,
+                                         hipStream_t stream);
+mtgnn_status mtgnn_temporal_attn_prepare_weights(const mtgnn_attn_params* params, const float* time_w,
+                                                 const float* time_b, const mtgnn_dims* d, void* save,
                                                  hipStream_t stream);
 mtgnn_status mtgnn_temporal_attn_prepare_slots(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
                                                const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes,

@@ -295,24 +295,28 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
 }
 
 mtgnn_status mtgnn_temporal_attn_prepare(const int32_t* nbr, const int32_t* n_q, int64_t max_q,
-                                         const mtgnn_attn_params* params, const mtgnn_dims* d, void* save, void* ws,
-                                         size_t ws_bytes, hipStream_t stream) {
+                                         const mtgnn_attn_params* params, const float* time_w, const float* time_b,
+                                         const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes,
+                                         hipStream_t stream) {
   MTGNN_TRY(check_dims(d));
   MTGNN_TRY(check_attn_params(params));
   if (max_q < 0 || max_q * (int64_t)d->k >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
   if (max_q == 0) return MTGNN_OK;
   REQ(nbr, "nbr");
   REQ(save, "save");
+  if (d->d_time > 0 && (!time_w || !time_b)) return fail(MTGNN_EINVAL, "time arrays");
   if (ws_bytes < attn_fwd_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "temporal_attn_prepare ws");
-  return attn_prepare_impl(nbr, n_q, max_q, params, d, save, ws, ws_bytes, stream);
+  return attn_prepare_impl(nbr, n_q, max_q, params, time_w, time_b, d, save, ws, ws_bytes, stream);
 }
 
-mtgnn_status mtgnn_temporal_attn_prepare_weights(const mtgnn_attn_params* params, const mtgnn_dims* d, void* save,
+mtgnn_status mtgnn_temporal_attn_prepare_weights(const mtgnn_attn_params* params, const float* time_w,
+                                                 const float* time_b, const mtgnn_dims* d, void* save,
                                                  hipStream_t stream) {
   MTGNN_TRY(check_dims(d));
   MTGNN_TRY(check_attn_params(params));
   REQ(save, "save");
-  return attn_prepare_weights_impl(params, d, save, stream);
+  if (d->d_time > 0 && (!time_w || !time_b)) return fail(MTGNN_EINVAL, "time arrays");
+  return attn_prepare_weights_impl(params, time_w, time_b, d, save, stream);
 }
 
 mtgnn_status mtgnn_temporal_attn_prepare_slots(const int32_t* nbr, const int32_t* n_q, int64_t max_q,

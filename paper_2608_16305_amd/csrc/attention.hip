@@ -43,6 +43,7 @@ struct AttnSave {
   float *pair_delta;     // per compact slot: tau - t_j
   float *q_in, *kv_in, *qv, *KV, *p, *attn, *m_in, *m1, *a1;
   float* merge_w;        // zero-padded merge weights and their transposes for the fused chains (float32 only)
+  float* qc;             // the query projection's constant b_q + W_q[:, dm:] phi(0) (fused float32 path)
   size_t total;
 };
 
@@ -55,6 +56,7 @@ AttnSave carve_save(void* base, const AttnShape& s) {
   v.W_kv = take(s.esz * 2 * s.da * s.Dkv);
   v.b_kv = (float*)take(sizeof(float) * 2 * s.da);
   v.merge_w = (float*)take(sizeof(float) * (s.esz == 4 ? merge_weights_floats(s.da, s.dm, s.dt) : 1));
+  v.qc = (float*)take(sizeof(float) * s.da);
   v.cnt = (int32_t*)take(sizeof(int32_t) * s.Q);
   v.pair_off = (int32_t*)take(sizeof(int32_t) * s.Q);
   v.n_valid = (int32_t*)take(sizeof(int32_t));
@@ -1046,8 +1048,11 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   size_t sc = 0;
   auto mx = [&](size_t x) { if (x > sc) sc = x; };
   {
+    // the query weight's problem spans d_m columns when its time columns are closed-form, else D_q
     const int64_t Ns[4] = {s.da, s.da, s.da, s.da}, Ks[4] = {s.da, s.da + s.dm, s.da, s.Dq};
+    const int64_t Ks2[4] = {s.da, s.da + s.dm, s.da, s.dm};
     mx(linear_dw_batch_ws_bytes(s.Q, Ns, Ks, 4));
+    mx(linear_dw_batch_ws_bytes(s.Q, Ns, Ks2, 4));
   }
   mx(linear_dw_ws_bytes(s.P, 2 * s.da, s.Dkv));
   v.scratch = take(sc > 0 ? sc : 1);
@@ -1064,8 +1069,8 @@ size_t attn_save_bytes(const mtgnn_dims* d, int64_t max_q) { return carve_save(n
 
 size_t attn_fwd_ws(const mtgnn_dims*, int64_t max_q) { return scan_ws_bytes(max_q); }
 
-mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const mtgnn_dims* d, void* save,
-                                       hipStream_t s) {
+mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const float* tw, const float* tb,
+                                       const mtgnn_dims* d, void* save, hipStream_t s) {
   const AttnShape sh(d, 0);
   const AttnSave sv = carve_save(save, sh);
   if (merge_fused_ok(d->dtype, sh.da, sh.dm)) {   // float32: one launch for every copy
@@ -1073,15 +1078,17 @@ mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const mtgnn_d
                      plain_copy((const float*)p->W_v, (float*)sv.W_kv + (size_t)sh.da * sh.Dkv, sh.da, (int)sh.Dkv),
                      plain_copy(p->b_k, sv.b_kv, 1, sh.da), plain_copy(p->b_v, sv.b_kv + sh.da, 1, sh.da)};
     int n_ex = 4;
-    if (qproj_fused_ok(d->dtype, sh.da, sh.dm, sh.dt)) {
+    const bool qf = qproj_fused_ok(d->dtype, sh.da, sh.dm, sh.dt);
+    if (qf) {
       ex[n_ex++] = qproj_copy((const float*)p->W_q, sh.da, sh.dm, sh.dt, sv.merge_w, 0);
       ex[n_ex++] = qproj_copy((const float*)p->W_q, sh.da, sh.dm, sh.dt, sv.merge_w, 1);
       for (int which = 0; which < 2; ++which)
         ex[n_ex++] = dmem_copy((const float*)p->W_k, (const float*)p->W_v, sh.da, sh.dm, sh.dt, (int)sh.Dkv,
                                sv.merge_w, which);
     }
+    const QConst qc{(const float*)p->W_q, p->b_q, tw, tb, sv.qc, sh.da, sh.dm, sh.dt};
     return merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm, sv.merge_w,
-                         s, ex, n_ex);
+                         s, ex, n_ex, qf ? &qc : nullptr);
   }
   const int64_t wkv = (int64_t)sh.da * sh.Dkv;
   if (d->dtype == MTGNN_F32)
@@ -1105,8 +1112,9 @@ mtgnn_status attn_prepare_slots_impl(const int32_t* nbr, const int32_t* n_q, int
 }
 
 mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,
-                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes, hipStream_t s) {
-  MTGNN_TRY(attn_prepare_weights_impl(p, d, save, s));
+                               const float* tw, const float* tb, const mtgnn_dims* d, void* save, void* ws,
+                               size_t ws_bytes, hipStream_t s) {
+  MTGNN_TRY(attn_prepare_weights_impl(p, tw, tb, d, save, s));
   return attn_prepare_slots_impl(nbr, n_q, max_q, d, save, ws, ws_bytes, s);
 }
 
@@ -1114,7 +1122,7 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
                            const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
                            const float* edge_feat, const float* tw, const float* tb, const mtgnn_attn_params* p,
                            const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s) {
-  MTGNN_TRY(attn_prepare_impl(nbr, n_q, max_q, p, d, save, ws, ws_bytes, s));
+  MTGNN_TRY(attn_prepare_impl(nbr, n_q, max_q, p, tw, tb, d, save, ws, ws_bytes, s));
   return attn_fwd_prepared_impl(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_feat, tw, tb, p, d, z, save, s);
 }
 
@@ -1140,7 +1148,7 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
     k_attn_gather<uint16_t><<<gq, 256, 0, s>>>(ga, (const uint16_t*)memory);
   MTGNN_CHECK_LAUNCH("attn_gather");
   if (qproj_fused_ok(d->dtype, sh.da, sh.dm, sh.dt))
-    MTGNN_TRY(qproj_fwd_fused(sv.q_in, sv.merge_w, p->b_q, sv.qv, n_q, max_q, sh.da, sh.dm, sh.dt, s));
+    MTGNN_TRY(qproj_fwd_fused(sv.q_in, sv.merge_w, sv.qc, sv.qv, n_q, max_q, sh.da, sh.dm, sh.dt, s));
   else
     MTGNN_TRY(linear_fwd(sv.q_in, MTGNN_F32, sh.Dq, p->W_q, wt, sh.Dq, p->b_q, sv.qv, sh.da, sh.Q, n_q, sh.da, sh.Dq,
                          false, s));
@@ -1294,12 +1302,12 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
     const DwProblem ps[4] = {{dz, da, sv.a1, da, g->W_2, da, da, da, g->b_2},
                              {b.dm1, da, sv.m_in, ldm, g->W_1, ldm, da, ldm, g->b_1},
                              {b.dm_in, ldm, sv.attn, da, g->W_o, da, da, da, g->b_o},
-                             {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, sh.Dq, g->b_q}};
+                             {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, q_closed && dt > 0 ? dm : sh.Dq, g->b_q}};
     MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
   }
   if (dt > 0 && q_closed)
     MTGNN_TRY(timegrad_reduce_slots_q(b.tg_part2, P, sv.n_valid, G_TG_ROWS, dt, g->b_q, (const float*)p->W_q, sh.Dq,
-                                      dm, da, tw, tb, d_time_w, d_time_b, s));
+                                      dm, da, tw, tb, d_time_w, d_time_b, g->W_q, s));
   // key/value projection over the compact slots (stacked [W_k; W_v]); the output-stationary kernel's
   // reduce writes the W_k and W_v halves (rows < d_a, rows >= d_a) straight to their gradients
   if (dw_rs_applicable(b.dKV, 2 * da, 2 * da, sv.kv_in, MTGNN_F32, sh.Dkv, (int)sh.Dkv))

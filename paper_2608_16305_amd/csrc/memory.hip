@@ -407,17 +407,23 @@ __global__ __launch_bounds__(256) void k_timegrad_reduce(const float* __restrict
 // The neighbour slots' partial sums plus the queries' share, which is closed-form: a query's time
 // input is phi(0) (delta = 0), so its w-gradient is zero and its b-gradient in column j is
 // -sin(b_j) sum_i dphi_ij = -sin(b_j) sum_a (sum_i dqv_ia) Wq[a][col0 + j], with sum_i dqv_ia the
-// query projection's bias gradient dbq.
+// query projection's bias gradient dbq.  The same constant input makes the query weight's time
+// columns an outer product, written here too: dWq[a][col0 + j] = dbq[a] phi(0)_j.
 __global__ __launch_bounds__(256) void k_timegrad_reduce_q(const float* __restrict__ part, int64_t rows,
                                                            const int32_t* __restrict__ rows_dev, int chunk_rows,
                                                            int dt_dim, const float* __restrict__ dbq,
                                                            const float* __restrict__ Wq, int64_t ldw, int col0, int da,
                                                            const float* __restrict__ tw, const float* __restrict__ tb,
-                                                           float* __restrict__ dw, float* __restrict__ db) {
+                                                           float* __restrict__ dw, float* __restrict__ db,
+                                                           float* __restrict__ dWq) {
   __shared__ float s[12];
   const int j = blockIdx.x, t = threadIdx.x;
   float v[3] = {0.f, 0.f, 0.f};
-  for (int a = t; a < da; a += 256) v[2] += dbq[a] * Wq[(int64_t)a * ldw + col0 + j];
+  const float phi0 = cosf(time_arg(tw[j], 0.f, tb[j]));
+  for (int a = t; a < da; a += 256) {
+    v[2] += dbq[a] * Wq[(int64_t)a * ldw + col0 + j];
+    dWq[(int64_t)a * ldw + col0 + j] = dbq[a] * phi0;
+  }
   timegrad_part(part, rows, rows_dev, chunk_rows, dt_dim, v[0], v[1]);
   block_sums256<3>(v, s);
   if (t == 0) {
@@ -481,10 +487,11 @@ mtgnn_status timegrad_reduce_blocks(const float* part, int64_t rows, const int32
 
 mtgnn_status timegrad_reduce_slots_q(const float* part, int64_t rows, const int32_t* rows_dev, int chunk_rows,
                                      int dt_dim, const float* dbq, const float* Wq, int64_t ldw, int col0, int da,
-                                     const float* tw, const float* tb, float* dw, float* db, hipStream_t s) {
+                                     const float* tw, const float* tb, float* dw, float* db, float* dWq,
+                                     hipStream_t s) {
   if (dt_dim <= 0) return MTGNN_OK;
   k_timegrad_reduce_q<<<(unsigned)dt_dim, 256, 0, s>>>(part, rows, rows_dev, chunk_rows, dt_dim, dbq, Wq, ldw, col0,
-                                                        da, tw, tb, dw, db);
+                                                        da, tw, tb, dw, db, dWq);
   MTGNN_CHECK_LAUNCH("timegrad_reduce_q");
   return MTGNN_OK;
 }

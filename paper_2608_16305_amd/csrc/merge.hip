@@ -211,10 +211,24 @@ struct PrepArgs {
   const float* src[PREP_MAX];
   float* dst[PREP_MAX];
   int rows[PREP_MAX], cols[PREP_MAX], n[PREP_MAX], k[PREP_MAX], ld[PREP_MAX], tr[PREP_MAX], ldd[PREP_MAX];
+  int ncopy;   // copies; grid slice ncopy (if present) forms the query constant
+  QConst qc;
 };
 
 __global__ void k_merge_prepare(PrepArgs a) {
   const int m = blockIdx.y;
+  if (m == a.ncopy) {   // the query constant c_j = b_q[j] + sum_t W_q[j][dm + t] phi(0)_t, a wave per j
+    const QConst& q = a.qc;
+    const int lane = threadIdx.x & 63;
+    const int Dq = q.dm + q.dt;
+    for (int j = blockIdx.x * 4 + (threadIdx.x >> 6); j < q.da; j += gridDim.x * 4) {
+      float v = 0.f;
+      for (int t = lane; t < q.dt; t += 64) v += q.Wq[(int64_t)j * Dq + q.dm + t] * cosf(time_arg(q.tw[t], 0.f, q.tb[t]));
+      v = wave_sum(v);
+      if (lane == 0) q.out[j] = q.bq[j] + v;
+    }
+    return;
+  }
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= (int64_t)a.rows[m] * a.cols[m]) return;
   const int r = (int)(e / a.cols[m]), c = (int)(e % a.cols[m]);
@@ -241,21 +255,21 @@ struct PackLayout {
   }
 };
 
-// The query projection's padded copies, after the merge copies: W_q (d_a rows, D_q = d_m + d_t columns)
-// and W_q[:, :d_m]^T (d_m rows, d_a columns);
+// The query projection's padded copies, after the merge copies: W_q[:, :d_m] (d_a rows, d_m columns:
+// a query's time input is the constant phi(0), whose share is added as a bias) and W_q[:, :d_m]^T
+// (d_m rows, d_a columns);
 // and W_kv[:, :d_m]^T (d_m rows, 2 d_a columns: the d M' product over the summed dK|dV).
 struct QLayout {
-  int na, kq, nm, kk;
+  int na, nm, kk;
   int rows[3], cols[3];
   size_t off[4];
   QLayout(int da, int dm, int dt) {
     na = (int)cdiv(da, 16);
-    kq = (int)cdiv(dm + dt, 16);
     nm = (int)cdiv(dm, 16);
     kk = (int)cdiv(2 * da, 16);
     auto R = [](int nct) { return 16 * MW * (int)cdiv(nct, MW); };
     rows[0] = R(na);
-    cols[0] = 16 * kq;
+    cols[0] = 16 * nm;
     rows[1] = R(nm);
     cols[1] = 16 * na;
     rows[2] = R(nm);
@@ -265,22 +279,26 @@ struct QLayout {
   }
 };
 
-// qv = W_q x + b_q over 16-row tiles of the query inputs x = [M[q] || phi(0)] (row stride D_q).
-template <int NA, int KQ>
-__global__ __launch_bounds__(64 * MW) void k_qproj_fwd(const float* __restrict__ q_in, const float* __restrict__ Wq,
-                                                       const float* __restrict__ bq, float* __restrict__ qv,
-                                                       const int32_t* __restrict__ n_q, int64_t max_q, int da, int Dq) {
+// qv = W_q [M[q] || phi(0)] + b_q over 16-row tiles of the queries.  The time input phi(0) = cos(b) is
+// the same for every query, so qv = W_q[:, :dm] M[q] + c with c = b_q + W_q[:, dm:] phi(0) (formed
+// once by the weight preparation): the product runs over the dm memory columns of q_in (row stride
+// D_q).  Wp: W_q[:, :dm] padded.
+template <int NA, int KM>
+__global__ __launch_bounds__(64 * MW) void k_qproj_fwd(const float* __restrict__ q_in, const float* __restrict__ Wp,
+                                                       const float* __restrict__ cq, float* __restrict__ qv,
+                                                       const int32_t* __restrict__ n_q, int64_t max_q, int da, int dm,
+                                                       int Dq) {
   __shared__ __attribute__((aligned(16))) float X0[16 * XS];
   const int64_t M = eff_count(max_q, n_q);
   const int64_t r0 = (int64_t)blockIdx.x * 16;
   if (r0 >= M) return;   // block-uniform
-  zero_cols(X0, Dq, 16 * KQ);
-  load_rows(X0, 0, q_in, Dq, Dq, r0, M);
+  zero_cols(X0, dm, 16 * KM);
+  load_rows(X0, 0, q_in, Dq, dm, r0, M);
   __syncthreads();
   f32x4 acc[Tiles<NA>::per_wave];
-  layer<NA, KQ>(X0, Wq, acc);
+  layer<NA, KM>(X0, Wp, acc);
   each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
-    if (ok) qv[(r0 + i) * da + j] = v + bq[j];
+    if (ok) qv[(r0 + i) * da + j] = v + cq[j];
   });
 }
 
@@ -376,7 +394,7 @@ mtgnn_status gru_dx_fused(const float* dgi, const float* WT, float* dmsg_time, c
 bool qproj_fused_ok(int dtype, int da, int dm, int dt) {
   if (!merge_fused_ok(dtype, da, dm) || dt % 4 != 0) return false;
   const QLayout L(da, dm, dt);
-  return (L.na == 7 && L.kq == 13 && L.nm == 7 && L.kk == 13) || (L.na == 2 && L.kq == 4 && L.nm == 2 && L.kk == 4);
+  return (L.na == 7 && L.nm == 7 && L.kk == 13) || (L.na == 2 && L.nm == 2 && L.kk == 4);
 }
 
 bool merge_fused_ok(int dtype, int da, int dm) {
@@ -390,7 +408,7 @@ size_t merge_weights_floats(int da, int dm, int dt) {
 
 PadCopy qproj_copy(const float* Wq, int da, int dm, int dt, float* Wp, int which) {
   const QLayout L(da, dm, dt);
-  if (which == 0) return PadCopy{Wq, Wp + L.off[0], L.rows[0], L.cols[0], da, dm + dt, dm + dt, 0, 0};
+  if (which == 0) return PadCopy{Wq, Wp + L.off[0], L.rows[0], L.cols[0], da, dm, dm + dt, 0, 0};
   return PadCopy{Wq, Wp + L.off[1], L.rows[1], L.cols[1], dm, da, dm + dt, 1, 0};
 }
 
@@ -416,16 +434,16 @@ mtgnn_status dmem_dx_fused(const float* S, int64_t ldS, const float* Wp, float* 
   return MTGNN_OK;
 }
 
-mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* bq, float* qv, const int32_t* n_q,
+mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* cq, float* qv, const int32_t* n_q,
                              int64_t max_q, int da, int dm, int dt, hipStream_t s) {
   if (max_q <= 0) return MTGNN_OK;
-  if (!aligned16(q_in) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
+  if (!aligned16(q_in) || !aligned16(Wp) || (dm + dt) % 4 != 0) return MTGNN_EUNSUPPORTED;
   const QLayout L(da, dm, dt);
   const unsigned grid = (unsigned)cdiv(max_q, 16);
   if (L.na == 7)
-    k_qproj_fwd<7, 13><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], bq, qv, n_q, max_q, da, dm + dt);
+    k_qproj_fwd<7, 7><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], cq, qv, n_q, max_q, da, dm, dm + dt);
   else
-    k_qproj_fwd<2, 4><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], bq, qv, n_q, max_q, da, dm + dt);
+    k_qproj_fwd<2, 2><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], cq, qv, n_q, max_q, da, dm, dm + dt);
   MTGNN_CHECK_LAUNCH("qproj_fwd");
   return MTGNN_OK;
 }
@@ -445,7 +463,7 @@ mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int
 }
 
 mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
-                           hipStream_t s, const PadCopy* extra, int n_extra) {
+                           hipStream_t s, const PadCopy* extra, int n_extra, const QConst* qc) {
   if (n_extra < 0 || n_extra > PREP_MAX - 6) return MTGNN_EINVAL;
   const PackLayout L(da, dm);
   const int ldm = da + dm;
@@ -479,7 +497,9 @@ mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, in
     a.ldd[m] = extra[x].ldd > 0 ? extra[x].ldd : extra[x].cols;
     most = std::max<int64_t>(most, (int64_t)extra[x].rows * extra[x].cols);
   }
-  k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), (unsigned)(6 + n_extra)), 256, 0, s>>>(a);
+  a.ncopy = 6 + n_extra;
+  if (qc) a.qc = *qc;
+  k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), (unsigned)(6 + n_extra + (qc ? 1 : 0))), 256, 0, s>>>(a);
   MTGNN_CHECK_LAUNCH("merge_prepare");
   return MTGNN_OK;
 }

@@ -47,10 +47,12 @@ mtgnn_status timegrad_reduce_blocks2(const float* p1, int64_t rows1, const int32
                                      int64_t rows2, const int32_t* rows_dev2, int chunk_rows, int dt_dim, float* dw,
                                      float* db, hipStream_t s);
 // dw = the slots' sum; db = the slots' sum + the queries' closed-form share (their time input is
-// phi(0)): -sin(b_j) sum_a dbq[a] Wq[a * ldw + col0 + j] (float32 weights).
+// phi(0)): -sin(b_j) sum_a dbq[a] Wq[a * ldw + col0 + j] (float32 weights); and the query weight's
+// time columns dWq[a * ldw + col0 + j] = dbq[a] phi(0)_j.
 mtgnn_status timegrad_reduce_slots_q(const float* part, int64_t rows, const int32_t* rows_dev, int chunk_rows,
                                      int dt_dim, const float* dbq, const float* Wq, int64_t ldw, int col0, int da,
-                                     const float* tw, const float* tb, float* dw, float* db, hipStream_t s);
+                                     const float* tw, const float* tb, float* dw, float* db, float* dWq,
+                                     hipStream_t s);
 mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const int32_t* rows_dev, const float* delta,
                            const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
                            bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
@@ -78,14 +80,25 @@ struct PadCopy {
 inline PadCopy plain_copy(const float* src, float* dst, int rows, int cols) {
   return PadCopy{src, dst, rows, cols, rows, cols, cols, 0, 0};
 }
-// One launch: the padded merge copies, then the extra copies (at most eight).
+// The query projection's constant: out[j] = bq[j] + sum_t Wq[j][dm + t] cos(w_t 0 + b_t) (a query's
+// time input is phi(0)); Wq row stride dm + dt.
+struct QConst {
+  const float *Wq, *bq, *tw, *tb;
+  float* out;
+  int da, dm, dt;
+};
+// One launch: the padded merge copies, then the extra copies (at most eight), and the query constant
+// when qc is given.
 mtgnn_status merge_prepare(const float* Wo, const float* W1, const float* W2, int da, int dm, float* Wp,
-                           hipStream_t s, const PadCopy* extra = nullptr, int n_extra = 0);
+                           hipStream_t s, const PadCopy* extra = nullptr, int n_extra = 0,
+                           const QConst* qc = nullptr);
 // The query projection on the same machinery (float32, the widths qproj_fused_ok accepts); its padded
-// copies (qproj_copy 0: W_q, 1: W_q[:, :dm]^T) follow the merge copies in the same buffer.
+// copies (qproj_copy 0: W_q[:, :dm], 1: W_q[:, :dm]^T) follow the merge copies in the same buffer.
 bool qproj_fused_ok(int dtype, int da, int dm, int dt);
 PadCopy qproj_copy(const float* Wq, int da, int dm, int dt, float* Wp, int which);
-mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* bq, float* qv, const int32_t* n_q,
+// qv = W_q[:, :dm] q_in[:, :dm] + cq, cq = b_q + W_q[:, dm:] phi(0) (QConst): a query's time input is
+// the constant phi(0).
+mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* cq, float* qv, const int32_t* n_q,
                              int64_t max_q, int da, int dm, int dt, hipStream_t s);
 mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int64_t ldm, const int32_t* n_q,
                             int64_t max_q, int da, int dm, int dt, hipStream_t s);
@@ -114,12 +127,13 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
                            const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s);
 // The forward's inputs that need only the sampled neighbours and the weights (stacked key/value
 // weights, padded merge weights, per-query valid-slot counts and offsets), then the rest.
-mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const mtgnn_dims* d, void* save,
-                                       hipStream_t s);
+mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const float* tw, const float* tb,
+                                       const mtgnn_dims* d, void* save, hipStream_t s);
 mtgnn_status attn_prepare_slots_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_dims* d,
                                      void* save, void* ws, size_t ws_bytes, hipStream_t s);
 mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,
-                               const mtgnn_dims* d, void* save, void* ws, size_t ws_bytes, hipStream_t s);
+                               const float* tw, const float* tb, const mtgnn_dims* d, void* save, void* ws,
+                               size_t ws_bytes, hipStream_t s);
 mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
                                     const int32_t* nbr, const float* nt, const int32_t* neid, const void* memory,
                                     const float* edge_feat, const float* tw, const float* tb,

@@ -68,8 +68,8 @@ _SIGS = {
     "mtgnn_sample_recent": [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I32, _P, _P, _P, _P],
     "mtgnn_temporal_attn": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams), C.POINTER(Dims), _P,
                             _P, _P, _SZ, _P],
-    "mtgnn_temporal_attn_prepare": [_P, _P, _I64, C.POINTER(AttnParams), C.POINTER(Dims), _P, _P, _SZ, _P],
-    "mtgnn_temporal_attn_prepare_weights": [C.POINTER(AttnParams), C.POINTER(Dims), _P, _P],
+    "mtgnn_temporal_attn_prepare": [_P, _P, _I64, C.POINTER(AttnParams), _P, _P, C.POINTER(Dims), _P, _P, _SZ, _P],
+    "mtgnn_temporal_attn_prepare_weights": [C.POINTER(AttnParams), _P, _P, C.POINTER(Dims), _P, _P],
     "mtgnn_temporal_attn_prepare_slots": [_P, _P, _I64, C.POINTER(Dims), _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_prepared": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams),
                                      C.POINTER(Dims), _P, _P, _P],
@@ -244,17 +244,21 @@ def mtgnn_temporal_attn(q_node, q_t, n_q, max_q, nbr, nt, neid, memory, edge_fea
                                      _ptr(save, torch.uint8, "save"), wp, wb, _stream(stream)), "mtgnn_temporal_attn")
 
 
-def mtgnn_temporal_attn_prepare(nbr, n_q, max_q, params: AttnParams, d: Dims, save, ws=None, stream=None):
+def mtgnn_temporal_attn_prepare(nbr, n_q, max_q, params: AttnParams, time_w, time_b, d: Dims, save, ws=None,
+                                stream=None):
     wp, wb = _ws(ws)
     _check(lib().mtgnn_temporal_attn_prepare(_ptr(nbr, torch.int32, "nbr"), _ptr(n_q, torch.int32, "n_q", True),
-                                             int(max_q), C.byref(params), C.byref(d),
+                                             int(max_q), C.byref(params), _ptr(time_w, torch.float32, "time_w"),
+                                             _ptr(time_b, torch.float32, "time_b"), C.byref(d),
                                              _ptr(save, torch.uint8, "save"), wp, wb, _stream(stream)),
            "mtgnn_temporal_attn_prepare")
 
 
-def mtgnn_temporal_attn_prepare_weights(params: AttnParams, d: Dims, save, stream=None):
-    _check(lib().mtgnn_temporal_attn_prepare_weights(C.byref(params), C.byref(d), _ptr(save, torch.uint8, "save"),
-                                                     _stream(stream)), "mtgnn_temporal_attn_prepare_weights")
+def mtgnn_temporal_attn_prepare_weights(params: AttnParams, time_w, time_b, d: Dims, save, stream=None):
+    _check(lib().mtgnn_temporal_attn_prepare_weights(C.byref(params), _ptr(time_w, torch.float32, "time_w"),
+                                                     _ptr(time_b, torch.float32, "time_b"), C.byref(d),
+                                                     _ptr(save, torch.uint8, "save"), _stream(stream)),
+           "mtgnn_temporal_attn_prepare_weights")
 
 
 def mtgnn_temporal_attn_prepare_slots(nbr, n_q, max_q, d: Dims, save, ws=None, stream=None):

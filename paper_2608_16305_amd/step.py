@@ -174,7 +174,8 @@ class TGNStep:
     def prepare_weights(self, stream):
         """The attention's weight copies (stacked K|V, padded merge layers): they read only the weights."""
         self._q_chain = self._q_chain if self._in_step else 0
-        M.mtgnn_temporal_attn_prepare_weights(self.ap, self.d, self.attn_save, stream=stream)
+        p = self.params
+        M.mtgnn_temporal_attn_prepare_weights(self.ap, p["time_w"], p["time_b"], self.d, self.attn_save, stream=stream)
 
     def embed(self, lo, hi, queries_done=False):
         self._q_chain = self._q_chain if self._in_step else 0

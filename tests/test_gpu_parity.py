@@ -221,11 +221,11 @@ def test_forward_single_call_matches_prepare_prepared():
         args = (r.q_node, r.q_t, r.n_q, r.max_q, r.nbr, r.nt, r.neid, r.memory, r.x, p["time_w"], p["time_b"],
                 r.ap, r.d, z, save)
         if split == 1:
-            M.mtgnn_temporal_attn_prepare(r.nbr, r.n_q, r.max_q, r.ap, r.d, save, r.ws)
+            M.mtgnn_temporal_attn_prepare(r.nbr, r.n_q, r.max_q, r.ap, p["time_w"], p["time_b"], r.d, save, r.ws)
             M.mtgnn_temporal_attn_prepared(*args)
         elif split == 2:   # the two halves of the preparation, slots first
             M.mtgnn_temporal_attn_prepare_slots(r.nbr, r.n_q, r.max_q, r.d, save, r.ws)
-            M.mtgnn_temporal_attn_prepare_weights(r.ap, r.d, save)
+            M.mtgnn_temporal_attn_prepare_weights(r.ap, p["time_w"], p["time_b"], r.d, save)
             M.mtgnn_temporal_attn_prepared(*args)
         else:
             M.mtgnn_temporal_attn(*args, r.ws)
