@@ -316,7 +316,11 @@ mtgnn_status mtgnn_temporal_attn_bwd_group(const int32_t* q_node, const int32_t*
  * entry.  dmem_stream must be ordered after that call (it was enqueued on dmem_stream, or
  * dmem_stream waits for it).  The call records `fork` on `stream` once the gradients the sums need
  * are ready, makes dmem_stream wait for it (the sums), records `join` on dmem_stream and makes
- * `stream` wait for `join`.  Results are bitwise identical to mtgnn_temporal_attn_bwd. */
+ * `stream` wait for `join`.  join may be NULL: then the call records and waits for nothing at the
+ * end, and the caller must order later work on `stream` after dmem_stream itself (an event recorded
+ * on dmem_stream after its own later work there serves).  Results are bitwise identical to
+ * mtgnn_temporal_attn_bwd.  Errors: as mtgnn_temporal_attn_bwd_overlap; EINVAL if dmem_stream or
+ * fork is NULL while max_rows > 0. */
 mtgnn_status mtgnn_temporal_attn_bwd_grouped(const int32_t* q_node, const float* q_t, const int32_t* n_q,
                                              int64_t max_q, const int32_t* nbr, const float* nt, const float* dz,
                                              const void* save, const int32_t* uniq, const int32_t* n_rows,

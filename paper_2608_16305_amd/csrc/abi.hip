@@ -424,8 +424,8 @@ mtgnn_status mtgnn_temporal_attn_bwd_grouped(const int32_t* q_node, const float*
                                              mtgnn_attn_grads* g, float* d_mem, float* d_time_w, float* d_time_b,
                                              void* ws, size_t ws_bytes, hipStream_t stream, hipStream_t dmem_stream,
                                              hipEvent_t fork, hipEvent_t join) {
-  if (max_rows > 0 && (!dmem_stream || !fork || !join))
-    return fail(MTGNN_EINVAL, "temporal_attn_bwd_grouped: dmem_stream, fork and join are required");
+  if (max_rows > 0 && (!dmem_stream || !fork))
+    return fail(MTGNN_EINVAL, "temporal_attn_bwd_grouped: dmem_stream and fork are required");
   return attn_bwd_checked(q_node, q_t, n_q, max_q, nbr, nt, dz, save, uniq, n_rows, max_rows, time_w, time_b, params,
                           d, g, d_mem, d_time_w, d_time_b, ws, ws_bytes, stream, dmem_stream, fork, join, true);
 }

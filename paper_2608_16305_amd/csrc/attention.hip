@@ -1420,7 +1420,7 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     return MTGNN_OK;
   };
   if (const mtgnn_status st1 = chain(); st1 != MTGNN_OK) {
-    if (overlap && hipEventRecord(join, s_dmem) == hipSuccess) (void)hipStreamWaitEvent(s, join, 0);
+    if (overlap && join && hipEventRecord(join, s_dmem) == hipSuccess) (void)hipStreamWaitEvent(s, join, 0);
     return st1;
   }
   if (!overlap) {
@@ -1432,6 +1432,7 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     return MTGNN_OK;
   }
   // second fork: the sums of d M' on the second stream, the parameter gradients here; join before returning
+  // (join == NULL, grouped form only: the caller orders `stream` after the second stream itself)
   hipError_t e = hipEventRecord(fork, s);
   if (e == hipSuccess) e = hipStreamWaitEvent(s_dmem, fork, 0);
   if (e != hipSuccess) {
@@ -1439,6 +1440,7 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
     return MTGNN_EHIP;
   }
   MTGNN_TRY(attn_bwd_dmem_sum(max_q, sh, sv, b, skeys, svals, n_rows, max_rows, wt, d_mem, s_dmem));
+  if (!join) return attn_bwd_params(n_q, sh, sv, b, dz, tw, tb, p, wt, g, d_time_w, d_time_b, s);
   e = hipEventRecord(join, s_dmem);
   if (e != hipSuccess) {
     set_hip_error(e, "attn_bwd join");

@@ -366,7 +366,7 @@ def mtgnn_temporal_attn_bwd_overlap(q_node, q_t, n_q, max_q, nbr, nt, dz, save, 
                                     time_b, params: AttnParams, d: Dims, grads: AttnGrads, d_mem, d_time_w, d_time_b,
                                     ws, dmem_stream, fork, join, stream=None, grouped=False):
     """grouped=True calls mtgnn_temporal_attn_bwd_grouped (the grouping left in ws by
-    mtgnn_temporal_attn_bwd_group on dmem_stream)."""
+    mtgnn_temporal_attn_bwd_group on dmem_stream); there join may be None (the caller joins)."""
     wp, wb = _ws(ws)
     name = "mtgnn_temporal_attn_bwd_grouped" if grouped else "mtgnn_temporal_attn_bwd_overlap"
     _check(getattr(lib(), name)(
@@ -377,7 +377,7 @@ def mtgnn_temporal_attn_bwd_overlap(q_node, q_t, n_q, max_q, nbr, nt, dz, save, 
         _ptr(time_b, torch.float32, "time_b"), C.byref(params), C.byref(d), C.byref(grads),
         _ptr(d_mem, torch.float32, "d_mem", True), _ptr(d_time_w, torch.float32, "d_time_w"),
         _ptr(d_time_b, torch.float32, "d_time_b"), wp, wb, _stream(stream), _stream(dmem_stream),
-        _event(fork, "fork"), _event(join, "join")), name)
+        _event(fork, "fork"), None if (grouped and join is None) else _event(join, "join")), name)
 
 
 def mtgnn_gru_update_bwd(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d: Dims, dW_ih, dW_hh, db_ih, db_hh,

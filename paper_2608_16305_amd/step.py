@@ -197,7 +197,8 @@ class TGNStep:
             M.mtgnn_temporal_attn_bwd_overlap(self.q_node, self.q_t, self.n_q, self.max_q, self.nbr, self.nt, dz,
                                               self.attn_save, self.uniq, self.n_uniq, self.max_rows, p["time_w"],
                                               p["time_b"], self.ap, self.d, self.ag, self.d_mem, g["time_w"],
-                                              g["time_b"], self.ws, self.side_stream, self.fork, self.join, stream=s,
+                                              g["time_b"], self.ws, self.side_stream, self.fork,
+                                              None if self._grouped else self.join, stream=s,
                                               grouped=self._grouped)
             self._grouped = False
             M.mtgnn_gru_update_bwd(self.d_mem, self.gru_save, self.msg, self.n_uniq, self.max_rows, p["W_ih"],
