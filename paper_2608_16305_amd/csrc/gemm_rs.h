@@ -282,9 +282,11 @@ constexpr int dw_stride(int nt) {   // smallest stride >= 16 nt floats that is 1
 // Each of the 4 waves accumulates a fixed set of 16 x 16 output tiles for the
 // whole launch: tile rows I = 3 wid .. 3 wid + 2 (all NJ tile columns) and, in
 // the last tile row I = 12, the tile columns J = wid, wid + 4, ...  (NI = 13).
-// Per chunk both operands go to LDS by direct global-to-LDS loads one chunk
-// ahead; MFMA sub-step s of a chunk takes rows 4 s + l/16 (lane l), reading one
+// Per chunk both operands go to LDS by direct global-to-LDS loads DW_RS_SLOTS - 1
+// chunks ahead; MFMA sub-step s of a chunk takes rows 4 s + l/16 (lane l), reading one
 // float per operand fragment.  Rows past the row count are zero-filled.
+constexpr int DW_RS_SLOTS = 2;   // 2 or 3 (3, two chunks in flight, measured slower: 88 vs 85 us)
+
 template <class Site, int NJ>
 __global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict__ X, int64_t ldx, int nx,
                                                      const float* __restrict__ Y, int64_t ldy, int ny, int64_t R,
@@ -293,7 +295,8 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict_
   constexpr int EX = (NJ + 3) / 4;               // tiles of the last tile row per wave, at most
   constexpr int SX = rs::dw_stride(NI), SY = rs::dw_stride(NJ);
   constexpr int SLOT = 16 * (SX + SY);           // floats per chunk slot
-  __shared__ __attribute__((aligned(16))) float lds[2 * SLOT];
+  constexpr int NSL = DW_RS_SLOTS;               // chunk slots: NSL - 1 chunks in flight
+  __shared__ __attribute__((aligned(16))) float lds[NSL * SLOT];
 
   const int64_t rows = eff_count(R, R_dev);
   const int64_t nchunks = cdiv(rows, 16);
@@ -331,12 +334,14 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict_
   for (int e = 0; e < EX; ++e) acx[e] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int64_t nmine = b0 < nchunks ? cdiv(nchunks - b0, G) : 0;
-  if (nmine > 0) issue(b0, 0);
-  // padding columns of both slots, while the first chunk loads (the loads fill columns < nx, < ny):
+#pragma unroll
+  for (int c = 0; c < NSL - 1; ++c)
+    if (c < nmine) issue(b0 + c * G, c);
+  // padding columns of every slot, while the first chunks load (the loads fill columns < nx, < ny):
   // X columns nx .. 16 NI and Y columns ny .. 16 NJ are zero except Y column ny, the all-ones column
   {
     const int cx = 16 * NI - nx, cw = cx + 16 * NJ - ny;
-    for (int e = tid; e < 2 * 16 * cw; e += G_THREADS) {
+    for (int e = tid; e < NSL * 16 * cw; e += G_THREADS) {
       const int slot = e / (16 * cw), rem = e % (16 * cw), r = rem / cw, c = rem % cw;
       const uint32_t off = c < cx ? (uint32_t)(slot * SLOT + r * SX + nx + c)
                                   : (uint32_t)(slot * SLOT + 16 * SX + r * SY + ny + (c - cx));
@@ -354,11 +359,16 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_rs(const float* __restrict_
     return v;
   };
   for (int64_t it = 0; it < nmine; ++it) {
-    const int slot = (int)(it & 1);
-    dma::wait_vm<0>();
+    const int slot = (int)(it % NSL);
+    // chunk `it` has landed once at most the later chunks' loads are outstanding: a full chunk is 8
+    // loads per wave (4 rows of X and of Y); a partial one (only the last can be) is waited out too
+    if (NSL == 3 && it + 1 < nmine && (b0 + (it + 1) * G + 1) * 16 <= rows)
+      dma::wait_vm<8>();
+    else
+      dma::wait_vm<0>();
     dma::wait_lgkm0();
     dma::barrier();   // chunk `it` is in LDS; every wave is done with chunk it - 1's slot
-    if (it + 1 < nmine) issue(b0 + (it + 1) * G, slot ^ 1);
+    if (it + NSL - 1 < nmine) issue(b0 + (it + NSL - 1) * G, (int)((it + NSL - 1) % NSL));
     const uint32_t sb = base + (uint32_t)(slot * SLOT) * 4u;
     // fragments of sub-step s (rows 4 s + fg of the chunk); those of s + 1 are read while
     // the MFMAs of s run (they pass through asm statements after the next reads)

@@ -28,18 +28,23 @@ constexpr int XS = 212;   // LDS row stride (floats) of an activation tile: >= 2
 constexpr int MW = 4;     // waves per block; wave w computes the output column tiles w, w + 4, ...
 constexpr int PD = 3;     // weight chunks in flight ahead of the one being multiplied
 
+constexpr int RT1 = 1;   // row tiles per block of the single-layer kernels (query projection, d M', GRU dx);
+                          // 2 (half the weight-fragment loads per row) measured slower: half the blocks
+
 template <int NCT> struct Tiles { static constexpr int per_wave = (NCT + MW - 1) / MW; };
 
-// acc[u] (16 x 16 output tile t = wave + 4 u) += X[16 rows, 16 KC] B[16 t.., 16 KC]^T.  X: the block's LDS
-// tile (row stride XS, zero beyond the true width).  B: a zero-padded weight copy, 16 MW NU rows by 16 KC
-// columns, so every fragment load is in bounds and unconditional.
-template <int NCT, int KC, int XSS = XS>
-__device__ __forceinline__ void layer(const float* X, const float* __restrict__ B, f32x4 (&acc)[Tiles<NCT>::per_wave]) {
+// acc[r NU + u] (16 x 16 output tile t = wave + 4 u of row tile r) += X[16 rows of tile r, 16 KC]
+// B[16 t.., 16 KC]^T.  X: the block's LDS tile of 16 RT rows (row stride XSS, zero beyond the true width).
+// B: a zero-padded weight copy, 16 MW NU rows by 16 KC columns, so every fragment load is in bounds and
+// unconditional; each fragment serves the RT row tiles.
+template <int NCT, int KC, int XSS = XS, int RT = 1>
+__device__ __forceinline__ void layer(const float* X, const float* __restrict__ B,
+                                      f32x4 (&acc)[RT * Tiles<NCT>::per_wave]) {
   constexpr int NU = Tiles<NCT>::per_wave;
   constexpr int LDB = 16 * KC;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, fr = lane & 15, fg = lane >> 4;
 #pragma unroll
-  for (int u = 0; u < NU; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int u = 0; u < RT * NU; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
   const float* Bl = B + (16 * wid + fr) * LDB + 4 * fg;
   float4 bf[KC][NU];
   auto load_b = [&](int c) {
@@ -51,24 +56,28 @@ __device__ __forceinline__ void layer(const float* X, const float* __restrict__ 
 #pragma unroll
   for (int c = 0; c < KC; ++c) {
     if (c + PD < KC) load_b(c + PD);   // in flight while this chunk's MFMAs run
-    const float4 a = *reinterpret_cast<const float4*>(X + fr * XSS + 16 * c + 4 * fg);
 #pragma unroll
-    for (int u = 0; u < NU; ++u) {
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, bf[c][u].x, acc[u], 0, 0, 0);
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, bf[c][u].y, acc[u], 0, 0, 0);
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, bf[c][u].z, acc[u], 0, 0, 0);
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, bf[c][u].w, acc[u], 0, 0, 0);
+    for (int r = 0; r < RT; ++r) {
+      const float4 a = *reinterpret_cast<const float4*>(X + (16 * r + fr) * XSS + 16 * c + 4 * fg);
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        f32x4& d = acc[r * NU + u];
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, bf[c][u].x, d, 0, 0, 0);
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, bf[c][u].y, d, 0, 0, 0);
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, bf[c][u].z, d, 0, 0, 0);
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, bf[c][u].w, d, 0, 0, 0);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);   // keeps the prefetch distance as written
   }
 }
 
-// rows r0 .. r0 + 15 (those < M) of a row-major [M, n] matrix into an LDS tile at column offset col0
-template <int XSS = XS>
+// rows r0 .. r0 + 16 RT - 1 (those < M) of a row-major [M, n] matrix into an LDS tile at column offset col0
+template <int XSS = XS, int RT = 1>
 __device__ __forceinline__ void load_rows(float* X, int col0, const float* __restrict__ src, int64_t ld, int n,
                                           int64_t r0, int64_t M) {
   const int nq = n / 4;
-  for (int e = threadIdx.x; e < 16 * nq; e += 64 * MW) {
+  for (int e = threadIdx.x; e < 16 * RT * nq; e += 64 * MW) {
     const int r = e / nq, q = e % nq;
     const float4 v = r0 + r < M ? *reinterpret_cast<const float4*>(src + (r0 + r) * ld + 4 * q)
                                 : float4{0.f, 0.f, 0.f, 0.f};
@@ -76,30 +85,34 @@ __device__ __forceinline__ void load_rows(float* X, int col0, const float* __res
   }
 }
 
-template <int XSS = XS>
+template <int XSS = XS, int RT = 1>
 __device__ __forceinline__ void zero_cols(float* X, int c0, int c1) {
-  for (int e = threadIdx.x; e < 16 * (c1 - c0); e += 64 * MW) X[(e / (c1 - c0)) * XSS + c0 + e % (c1 - c0)] = 0.f;
+  for (int e = threadIdx.x; e < 16 * RT * (c1 - c0); e += 64 * MW)
+    X[(e / (c1 - c0)) * XSS + c0 + e % (c1 - c0)] = 0.f;
 }
 
-// Epilogue of a layer: f(i, j, row valid, value) for this wave's tiles, row 4 (l/16) + r, column 16 t + l%16
-// (j < N only).  A full 16-row tile takes a path with the row test folded away.
-template <int NCT, class F>
-__device__ __forceinline__ void each_out(const f32x4 (&acc)[Tiles<NCT>::per_wave], int N, int64_t r0, int64_t M,
-                                         F f) {
+// Epilogue of a layer: f(i, j, row valid, value) for this wave's tiles, row 16 t + 4 (l/16) + r of row tile
+// t, column 16 u' + l%16 (j < N only).  A full block of rows takes a path with the row test folded away.
+template <int NCT, int RT = 1, class F>
+__device__ __forceinline__ void each_out(const f32x4 (&acc)[RT * Tiles<NCT>::per_wave], int N, int64_t r0,
+                                         int64_t M, F f) {
+  constexpr int NU = Tiles<NCT>::per_wave;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, fr = lane & 15, fg = lane >> 4;
   auto run = [&](auto full) {
 #pragma unroll
-    for (int u = 0; u < Tiles<NCT>::per_wave; ++u) {
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
       const int j = 16 * (wid + MW * u) + fr;
       if (j >= N) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int i = 4 * fg + r;
-        f(i, j, decltype(full)::value || r0 + i < M, acc[u][r]);
+        const int i = 16 * t + 4 * fg + r;
+        f(i, j, decltype(full)::value || r0 + i < M, acc[t * NU + u][r]);
       }
     }
   };
-  if (r0 + 16 <= M)
+  if (r0 + 16 * RT <= M)
     run(std::true_type{});
   else
     run(std::false_type{});
@@ -288,16 +301,16 @@ __global__ __launch_bounds__(64 * MW) void k_qproj_fwd(const float* __restrict__
                                                        const float* __restrict__ cq, float* __restrict__ qv,
                                                        const int32_t* __restrict__ n_q, int64_t max_q, int da, int dm,
                                                        int Dq) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * XS];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS];
   const int64_t M = eff_count(max_q, n_q);
-  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
   if (r0 >= M) return;   // block-uniform
-  zero_cols(X0, dm, 16 * KM);
-  load_rows(X0, 0, q_in, Dq, dm, r0, M);
+  zero_cols<XS, RT1>(X0, dm, 16 * KM);
+  load_rows<XS, RT1>(X0, 0, q_in, Dq, dm, r0, M);
   __syncthreads();
-  f32x4 acc[Tiles<NA>::per_wave];
-  layer<NA, KM>(X0, Wp, acc);
-  each_out<NA>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT1 * Tiles<NA>::per_wave];
+  layer<NA, KM, XS, RT1>(X0, Wp, acc);
+  each_out<NA, RT1>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) qv[(r0 + i) * da + j] = v + cq[j];
   });
 }
@@ -307,16 +320,16 @@ template <int NM, int NA>
 __global__ __launch_bounds__(64 * MW) void k_qproj_dx(const float* __restrict__ dqv, const float* __restrict__ WqT,
                                                       float* __restrict__ dm_in, int64_t ldm,
                                                       const int32_t* __restrict__ n_q, int64_t max_q, int da, int dm) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * XS];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS];
   const int64_t M = eff_count(max_q, n_q);
-  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
   if (r0 >= M) return;   // block-uniform
-  zero_cols(X0, da, 16 * NA);
-  load_rows(X0, 0, dqv, da, da, r0, M);
+  zero_cols<XS, RT1>(X0, da, 16 * NA);
+  load_rows<XS, RT1>(X0, 0, dqv, da, da, r0, M);
   __syncthreads();
-  f32x4 acc[Tiles<NM>::per_wave];
-  layer<NM, NA>(X0, WqT, acc);
-  each_out<NM>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT1 * Tiles<NM>::per_wave];
+  layer<NM, NA, XS, RT1>(X0, WqT, acc);
+  each_out<NM, RT1>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) dm_in[(r0 + i) * ldm + da + j] += v;
   });
 }
@@ -328,16 +341,16 @@ __global__ __launch_bounds__(64 * MW) void k_dmem_dx(const float* __restrict__ S
                                                      const float* __restrict__ WkT, float* __restrict__ d_mem,
                                                      const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
                                                      int w2) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * XS];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS];
   const int64_t M = eff_count(max_rows, n_rows);
-  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
   if (r0 >= M) return;   // block-uniform
-  zero_cols(X0, w2, 16 * KK);
-  load_rows(X0, 0, S + dm, ldS, w2, r0, M);
+  zero_cols<XS, RT1>(X0, w2, 16 * KK);
+  load_rows<XS, RT1>(X0, 0, S + dm, ldS, w2, r0, M);
   __syncthreads();
-  f32x4 acc[Tiles<NM>::per_wave];
-  layer<NM, KK>(X0, WkT, acc);
-  each_out<NM>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT1 * Tiles<NM>::per_wave];
+  layer<NM, KK, XS, RT1>(X0, WkT, acc);
+  each_out<NM, RT1>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) d_mem[(r0 + i) * dm + j] += v;
   });
 }
@@ -350,16 +363,16 @@ template <int NT, int KC>
 __global__ __launch_bounds__(64 * MW) void k_gru_dx(const float* __restrict__ dgi, int64_t ldg,
                                                     const float* __restrict__ WT, float* __restrict__ out, int dt,
                                                     const int32_t* __restrict__ n_rows, int64_t max_rows, int K) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * XS_GRU];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS_GRU];
   const int64_t M = eff_count(max_rows, n_rows);
-  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
   if (r0 >= M) return;   // block-uniform
-  zero_cols<XS_GRU>(X0, K, 16 * KC);
-  load_rows<XS_GRU>(X0, 0, dgi, ldg, K, r0, M);
+  zero_cols<XS_GRU, RT1>(X0, K, 16 * KC);
+  load_rows<XS_GRU, RT1>(X0, 0, dgi, ldg, K, r0, M);
   __syncthreads();
-  f32x4 acc[Tiles<NT>::per_wave];
-  layer<NT, KC, XS_GRU>(X0, WT, acc);
-  each_out<NT>(acc, dt, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT1 * Tiles<NT>::per_wave];
+  layer<NT, KC, XS_GRU, RT1>(X0, WT, acc);
+  each_out<NT, RT1>(acc, dt, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) out[(r0 + i) * dt + j] = v;
   });
 }
@@ -382,7 +395,7 @@ mtgnn_status gru_dx_fused(const float* dgi, const float* WT, float* dmsg_time, c
                           int64_t max_rows, int dm, int dt, hipStream_t s) {
   if (max_rows <= 0) return MTGNN_OK;
   if (!aligned16(dgi) || !aligned16(WT)) return MTGNN_EUNSUPPORTED;
-  const unsigned grid = (unsigned)cdiv(max_rows, 16);
+  const unsigned grid = (unsigned)cdiv(max_rows, 16 * RT1);
   if (cdiv(3 * dm, 16) == 19)
     k_gru_dx<7, 19><<<grid, 64 * MW, 0, s>>>(dgi, 3 * dm, WT, dmsg_time, dt, n_rows, max_rows, 3 * dm);
   else
@@ -425,7 +438,7 @@ mtgnn_status dmem_dx_fused(const float* S, int64_t ldS, const float* Wp, float* 
   if (max_rows <= 0) return MTGNN_OK;
   if (!aligned16(S) || !aligned16(Wp) || (dm * sizeof(float)) % 16 != 0 || ldS % 4 != 0) return MTGNN_EUNSUPPORTED;
   const QLayout L(da, dm, dt);
-  const unsigned grid = (unsigned)cdiv(max_rows, 16);
+  const unsigned grid = (unsigned)cdiv(max_rows, 16 * RT1);
   if (L.nm == 7)
     k_dmem_dx<7, 13><<<grid, 64 * MW, 0, s>>>(S, ldS, Wp + L.off[2], d_mem, n_rows, max_rows, dm, 2 * da);
   else
@@ -439,7 +452,7 @@ mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* cq
   if (max_q <= 0) return MTGNN_OK;
   if (!aligned16(q_in) || !aligned16(Wp) || (dm + dt) % 4 != 0) return MTGNN_EUNSUPPORTED;
   const QLayout L(da, dm, dt);
-  const unsigned grid = (unsigned)cdiv(max_q, 16);
+  const unsigned grid = (unsigned)cdiv(max_q, 16 * RT1);
   if (L.na == 7)
     k_qproj_fwd<7, 7><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], cq, qv, n_q, max_q, da, dm, dm + dt);
   else
@@ -453,7 +466,7 @@ mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int
   if (max_q <= 0) return MTGNN_OK;
   if (!aligned16(dqv) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
   const QLayout L(da, dm, dt);
-  const unsigned grid = (unsigned)cdiv(max_q, 16);
+  const unsigned grid = (unsigned)cdiv(max_q, 16 * RT1);
   if (L.na == 7)
     k_qproj_dx<7, 7><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
   else
