@@ -139,7 +139,10 @@ struct Vec4<uint16_t> {
 template <bool KC, int R, int BK>
 struct Lds {
   static constexpr int LDK = BK + 4;                          // KC row stride
-  static constexpr int LDR = R + ((16 - (R % 32)) + 32) % 32;  // row-contiguous row stride (== 16 mod 32)
+  // Row-contiguous row stride, == 4 mod 32: a fragment read takes k = kc + 4 (l/16) + i, so the two lane
+  // groups of a 32-lane half are 4 LDR apart, which is then 16 banks (with LDR == 16 mod 32 it was 0
+  // banks: a 2-way conflict on every read).
+  static constexpr int LDR = R + ((4 - (R % 32)) + 32) % 32;
   static constexpr int SIZE = KC ? R * LDK : BK * LDR;
   __device__ __forceinline__ static float4 frag(const float* lds, int row, int kc, int lane) {
     const int k = kc + 4 * (lane >> 4);
