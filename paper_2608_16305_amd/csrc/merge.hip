@@ -26,7 +26,7 @@ namespace {
 
 constexpr int XS = 212;   // LDS row stride (floats) of an activation tile: >= 208, XS / 4 odd (conflict-free rows)
 constexpr int MW = 4;     // waves per block; wave w computes the output column tiles w, w + 4, ...
-constexpr int PD = 3;     // weight chunks in flight ahead of the one being multiplied
+constexpr int PD = 3;     // weight chunks in flight ahead of the one being multiplied (6 measured slower)
 
 constexpr int RT1 = 1;   // row tiles per block of the single-layer kernels (query projection, d M', GRU dx);
                           // 2 (half the weight-fragment loads per row) measured slower: half the blocks
