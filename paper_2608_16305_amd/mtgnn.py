@@ -340,7 +340,10 @@ class DeviceEvent:
 
     def __del__(self):
         if getattr(self, "handle", None) and self.handle.value:
-            self._rt.hipEventDestroy(self.handle)
+            try:   # may run at interpreter exit, after the runtime is gone
+                self._rt.hipEventDestroy(self.handle)
+            except Exception:
+                pass
             self.handle = C.c_void_p()
 
 
