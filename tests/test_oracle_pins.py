@@ -509,3 +509,177 @@ def test_restricted_adjacency_equals_full_lists():
     qt = rng.random(40).astype(np.float32) * 50
     for a, b in zip(tgn.sample_recent(part, q, qt, 6), tgn.sample_recent(full, q, qt, 6)):
         assert np.array_equal(a, b)
+
+
+# --------------------------------------------------------------------------- independent torch rendering
+
+def _torch_step_forward(mode, w, mem, x_all, params, mem_batch, q_node, q_t, nbr, nt, neid):
+    """The forward of one step written again in torch (float64 on the CPU), from the raw parameters:
+    torch.nn.GRUCell for the memory update, torch.nn.functional.linear for every layer, masked
+    scaled-dot-product attention per head, ReLU, and the concatenations of the embedding (query input
+    [M || phi(0)], key/value input [M || x || phi(tau - t)], merge input [o || M]).  In "bf16" mode the
+    values that enter a matrix product are cast to bfloat16 with torch (float64 -> float32 -> bfloat16)
+    at exactly the points of the bf16 reading: messages, the query and key/value inputs, the attention
+    output before W_o, o before the merge, relu(m1) before W_2, and the weights; the memory update is
+    stored rounded; the time argument is formed as two float32 operations."""
+    f64 = torch.float64
+    T = lambda a: torch.as_tensor(np.asarray(a, np.float64))   # noqa: E731
+    if mode == "bf16":
+        rnd = lambda v: v.to(torch.float32).to(torch.bfloat16).to(f64)   # noqa: E731
+    else:
+        rnd = lambda v: v                                                 # noqa: E731
+    tw, tb = params["time_w"], params["time_b"]
+
+    def phi(dt):
+        if mode == "bf16":
+            arg = torch.as_tensor(np.asarray(dt, F32))[..., None] * torch.as_tensor(tw) + torch.as_tensor(tb)
+            return torch.cos(arg.to(f64))
+        return torch.cos(T(dt)[..., None] * T(tw) + T(tb))
+
+    Wt = {n: rnd(T(params[n])) for n in ("W_ih", "W_hh", "W_q", "W_k", "W_v", "W_o", "W_1", "W_2")}
+    bt = {n: T(params[n]) for n in ("b_ih", "b_hh", "b_q", "b_k", "b_v", "b_o", "b_1", "b_2")}
+    out = {}
+    # ---- memory phase: the last message of each node (selection taken from the pinned select_last)
+    uniq, winner = tgn.select_last(mem_batch["src"], mem_batch["dst"], mem_batch["t"], mem_batch["eid"])
+    ev, role = winner // 2, winner % 2
+    node = np.where(role == 0, mem_batch["src"][ev], mem_batch["dst"][ev]).astype(np.int64)
+    partner = np.where(role == 0, mem_batch["dst"][ev], mem_batch["src"][ev]).astype(np.int64)
+    tt = np.asarray(mem_batch["t"], F32)[ev]
+    lu0 = np.zeros(w.n_nodes, F32)
+    dtm = (tt - lu0[node]).astype(F32) if mode == "bf16" else tt.astype(np.float64)
+    M0 = T(mem)
+    parts = [M0[node], M0[partner], rnd(phi(dtm))]
+    if w.d_edge:
+        parts.append(rnd(T(x_all[np.asarray(mem_batch["eid"])[ev]])))
+    msg = torch.cat(parts, 1)
+    cell = torch.nn.GRUCell(w.d_msg, w.d_mem, dtype=f64)
+    with torch.no_grad():
+        cell.weight_ih.copy_(Wt["W_ih"])
+        cell.weight_hh.copy_(Wt["W_hh"])
+        cell.bias_ih.copy_(bt["b_ih"])
+        cell.bias_hh.copy_(bt["b_hh"])
+        h_new = cell(msg, M0[uniq])
+    M1 = M0.clone()
+    M1[uniq] = rnd(h_new) if mode == "bf16" else h_new
+    out.update(msg=msg, h_new=h_new, uniq=uniq)
+    # ---- embedding from the updated table
+    Q, k = nbr.shape
+    H, da = w.n_heads, w.d_attn
+    dh = da // H
+    valid = torch.as_tensor(nbr >= 0)
+    hq = M1[q_node]
+    q_in = torch.cat([hq, rnd(phi(np.zeros(Q, F32)))], 1)
+    q = torch.nn.functional.linear(q_in, Wt["W_q"], bt["b_q"])
+    nb = np.where(nbr >= 0, nbr, 0)
+    if mode == "bf16":
+        dts = (np.asarray(q_t, F32)[:, None] - np.asarray(nt, F32)).astype(F32)
+    else:
+        dts = np.asarray(q_t, np.float64)[:, None] - np.asarray(nt, np.float64)
+    kparts = [M1[nb]]
+    if w.d_edge:
+        kparts.append(rnd(T(x_all[np.where(nbr >= 0, neid, 0)])))
+    kparts.append(rnd(phi(dts)))
+    kv_in = torch.cat(kparts, 2)
+    K = torch.nn.functional.linear(kv_in, Wt["W_k"], bt["b_k"])
+    V = torch.nn.functional.linear(kv_in, Wt["W_v"], bt["b_v"])
+    qh = q.reshape(Q, H, 1, dh)
+    Kh = K.reshape(Q, k, H, dh).transpose(1, 2)
+    Vh = V.reshape(Q, k, H, dh).transpose(1, 2)
+    mask = valid[:, None, None, :].expand(Q, H, 1, k)
+    a = torch.nn.functional.scaled_dot_product_attention(qh, Kh, Vh, attn_mask=mask)
+    a = torch.where(valid.any(1)[:, None, None, None], a, torch.zeros_like(a))   # no neighbour: 0
+    attn = rnd(a.reshape(Q, da))
+    o = torch.nn.functional.linear(attn, Wt["W_o"], bt["b_o"])
+    m_in = torch.cat([rnd(o), hq], 1)
+    m1 = torch.nn.functional.linear(m_in, Wt["W_1"], bt["b_1"])
+    a1 = rnd(torch.relu(m1))
+    z = torch.nn.functional.linear(a1, Wt["W_2"], bt["b_2"])
+    out.update(q_in=q_in, q=q, kv_in=kv_in, K=K, V=V, attn=attn, o=o, m_in=m_in, m1=m1, a1=a1, z=z,
+               valid=valid.numpy())
+    return {kk: (v.numpy() if torch.is_tensor(v) else v) for kk, v in out.items()}
+
+
+def _composition_case(seed, H, de, n_valid, mode="f64"):
+    w = tiny_workload(n_nodes=11, n_events=40, d_mem=7, d_time=5, d_edge=de, d_attn=12, n_heads=H, k=4,
+                      batch=10)
+    if mode == "bf16":
+        w = replace(w, dtype="bf16")
+    s = tiny_stream(w, seed=seed, t_scale=20.0, tie_every=4)
+    params = init_params(w, random_bias=True)
+    rng = np.random.default_rng(seed + 100)
+    params["time_w"] = rng.uniform(0.05, 1.2, w.d_time).astype(F32)
+    mem = rng.uniform(-1, 1, (w.n_nodes, w.d_mem))
+    if mode == "bf16":
+        mem = round_bf16(mem.astype(F32)).astype(np.float64)
+    mb = tgn.batch_dict(s, 0, 10)
+    Q = len(n_valid)
+    q_node = rng.integers(0, w.n_nodes, Q)
+    q_t = (rng.random(Q) * 10 + 20).astype(F32)
+    nbr = rng.integers(0, w.n_nodes, (Q, w.k))
+    nt = (rng.random((Q, w.k)) * 20).astype(F32)
+    neid = rng.integers(0, s.n_events, (Q, w.k))
+    for qi, nv in enumerate(n_valid):
+        nbr[qi, nv:], nt[qi, nv:], neid[qi, nv:] = -1, 0, -1
+    return w, s, params, mem, mb, q_node, q_t, nbr, nt, neid
+
+
+@pytest.mark.parametrize("H", [1, 2, 3])
+@pytest.mark.parametrize("de", [0, 3])
+def test_attention_forward_composition_matches_torch_module(H, de):
+    """The whole embedding (projection inputs, W_q/W_k/W_v, per-head softmax, W_o, the merge
+    W_2 relu(W_1 [o || M] + b_1) + b_2) against an independent float64 torch rendering, with queries
+    that have no, one, some and all valid neighbour slots."""
+    n_valid = [0, 1, 2, 4, 4, 3]
+    w, s, params, mem, mb, q_node, q_t, nbr, nt, neid = _composition_case(7 + H + de, H, de, n_valid)
+    p64 = tgn.Prec("f64")
+    mp = tgn.memory_phase(p64, w, mb, mem, np.zeros(w.n_nodes), s.x, params)
+    sv = tgn.attention_fwd(p64, w, mp.mem, s.x, params, q_node, q_t, nbr, nt, neid)
+    ref = _torch_step_forward("f64", w, mem, s.x, params, mb, q_node, q_t, nbr, nt, neid)
+    v = ref["valid"]
+    pairs = [("msg", mp.msg, ref["msg"]), ("h_new", mp.h_new, ref["h_new"]), ("q_in", sv.q_in, ref["q_in"]),
+             ("q", sv.q, ref["q"]), ("kv_in", sv.kv_in[v], ref["kv_in"][v]), ("K", sv.K[v], ref["K"][v]),
+             ("V", sv.V[v], ref["V"][v]), ("attn", sv.attn, ref["attn"]), ("o", sv.o, ref["o"]),
+             ("m_in", sv.m_in, ref["m_in"]), ("m1", sv.m1, ref["m1"]), ("a1", sv.a1, ref["a1"]),
+             ("z", sv.z, ref["z"])]
+    for name, a, b in pairs:
+        assert a.shape == b.shape, name
+        assert np.allclose(a, b, rtol=0, atol=1e-12), (name, np.abs(a - b).max())
+    assert np.all(sv.attn[0] == 0) and np.allclose(sv.o[0], params["b_o"], rtol=0, atol=0)
+
+
+def _bf16_exact(a):
+    a = np.asarray(a, np.float64)
+    return np.array_equal(round_bf16(a.astype(F32)).astype(np.float64), a)
+
+
+def test_bf16_rounding_placement():
+    """bf16 mode rounds exactly the values the bf16 reading names, and nothing else.
+
+    An independent torch rendering applies torch's bfloat16 cast at those points only; every
+    intermediate of the oracle must then agree with it to float64 rounding (a missed or extra rounding
+    moves values by ~4e-3).  The rounded tensors are bf16-representable; the unrounded ones are not."""
+    n_valid = [0, 1, 3, 4, 4, 2, 4, 1]
+    w, s, params, mem, mb, q_node, q_t, nbr, nt, neid = _composition_case(31, 2, 3, n_valid, mode="bf16")
+    p16 = tgn.Prec("bf16")
+    lu0 = np.zeros(w.n_nodes, F32)
+    mp = tgn.memory_phase(p16, w, mb, mem.astype(F32), lu0, s.x, params)
+    sv = tgn.attention_fwd(p16, w, mp.mem, s.x, params, q_node, q_t, nbr, nt, neid)
+    ref = _torch_step_forward("bf16", w, mem, s.x, params, mb, q_node, q_t, nbr, nt, neid)
+    v = ref["valid"]
+    rounded = [("msg", mp.msg, ref["msg"]), ("q_in", sv.q_in, ref["q_in"]), ("kv_in", sv.kv_in[v], ref["kv_in"][v]),
+               ("attn", sv.attn, ref["attn"]), ("m_in", sv.m_in, ref["m_in"]), ("a1", sv.a1, ref["a1"]),
+               ("stored memory rows", mp.mem[mp.uniq], round_bf16(ref["h_new"].astype(F32)))]
+    unrounded = [("h_new", mp.h_new, ref["h_new"]), ("q", sv.q, ref["q"]), ("K", sv.K[v], ref["K"][v]),
+                 ("V", sv.V[v], ref["V"][v]), ("o", sv.o, ref["o"]), ("m1", sv.m1, ref["m1"]), ("z", sv.z, ref["z"])]
+    for name, a, b in rounded:
+        assert _bf16_exact(a), name
+        # equal bit for bit, except where the value before the cast sits within float64 noise of a tie
+        diff = np.asarray(a, np.float64) != np.asarray(b, np.float64)
+        assert diff.mean() < 1e-3, (name, int(diff.sum()))
+    for name, a, b in unrounded:
+        assert not _bf16_exact(a), name
+        scale = max(np.abs(b).max(), 1.0)
+        assert np.allclose(a, b, rtol=0, atol=1e-12 * scale), (name, np.abs(a - b).max())
+    # weights enter the products rounded: a product with unrounded W_2 differs from z by ~1e-3
+    z_unrounded_w = sv.a1 @ np.asarray(params["W_2"], np.float64).T + params["b_2"]
+    assert np.abs(z_unrounded_w - sv.z).max() > 1e-5
