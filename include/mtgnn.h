@@ -122,7 +122,7 @@ size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* dims, int64_t max_rows, i
  * op = MTGNN_OP_GRU_UPDATE or MTGNN_OP_TEMPORAL_ATTN; 0 otherwise. */
 size_t mtgnn_save_bytes(int op, const mtgnn_dims* dims, int64_t max_rows, int64_t max_q);
 
-/* Row a1. Batch intake (Definition 2 and Eq. 12).  Builds the query list of
+/* Batch intake (Definition 2 and Eq. 12).  Builds the query list of
  * the target events (flags & 3 == 0) in batch order as three blocks:
  * sources, then destinations, then negatives, each at its event's time.
  *   neg    -- [b->n] negative destination per event (device);
@@ -132,7 +132,8 @@ size_t mtgnn_save_bytes(int op, const mtgnn_dims* dims, int64_t max_rows, int64_
 mtgnn_status mtgnn_build_queries(const mtgnn_batch* b, const int32_t* neg, int32_t* q_node, float* q_t,
                                  int32_t* n_q, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Row a2. Most-recent message aggregation (Eq. 2 applied once per batch).
+/* Most-recent message aggregation (Eq. 2 applied once per batch; TGN's last-message aggregator,
+ * Section VII-A).
  * Every non-pruned event i sends message 2i to src[i] (role 0) and message
  * 2i+1 to dst[i] (role 1).  For each node that receives a message, the winner
  * is its message with the largest (t, eid, role).  Under the batch order
@@ -148,7 +149,7 @@ mtgnn_status mtgnn_build_queries(const mtgnn_batch* b, const int32_t* neg, int32
 mtgnn_status mtgnn_aggregate_last(const mtgnn_batch* b, int64_t n_nodes, int32_t* uniq, int32_t* winner,
                                   int32_t* n_uniq, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Row a3. Message construction (Eq. 1) for each aggregated row r < n_rows.
+/* Message construction (Eq. 1) for each aggregated row r < n_rows.
  * Let i = winner[r] / 2 be the event, node = uniq[r] and partner its other
  * endpoint.  Then
  *     msg[r] = [ M[node] || M[partner] || cos(time_w * dt + time_b) || x[eid_i] ],
@@ -166,7 +167,7 @@ mtgnn_status mtgnn_build_messages(const mtgnn_batch* b, const int32_t* uniq, con
                                   const float* time_b, const mtgnn_dims* dims, void* msg, float* dt,
                                   hipStream_t stream);
 
-/* Row a4. GRU memory update (Eq. 2), gate order r, z, n:
+/* GRU memory update (Eq. 2; TGN's memory updater, Section VII-A), gate order r, z, n:
  *   r = sig(W_ir x + b_ir + W_hr h + b_hr),  z = sig(W_iz x + b_iz + W_hz h + b_hz),
  *   n = tanh(W_in x + b_in + r * (W_hn h + b_hn)),  h' = (1 - z) n + z h,
  * with x = msg[r] and h = memory[uniq[r]].  Writes memory[uniq[r]] = h'
@@ -180,8 +181,10 @@ mtgnn_status mtgnn_gru_update(const mtgnn_batch* b, const int32_t* uniq, const i
                               void* memory, float* last_update, void* save, void* ws, size_t ws_bytes,
                               hipStream_t stream);
 
-/* Row a5. Most-recent-k temporal neighbour sampling over the temporal
- * adjacency.  The adjacency holds every stream event in both directions.
+/* Most-recent-k temporal neighbour sampling over the temporal adjacency: the
+ * temporal neighbourhood that TGN aggregates (Section VII-A), strictly before the
+ * query time so that an event never sees itself or later events (Section III-A).
+ * The adjacency holds every stream event in both directions.
  * For query (n, tau), take the entries of node n with t < tau (strictly),
  * then the k largest by (t, eid, role), newest first.  Missing slots are
  * padded with nbr = -1, t = 0, eid = -1.
@@ -195,7 +198,8 @@ mtgnn_status mtgnn_sample_recent(const int64_t* csr_off, const int32_t* csr_nbr,
                                  const float* q_t, const int32_t* n_q, int64_t max_q, int32_t k,
                                  int32_t* out_nbr, float* out_t, int32_t* out_eid, hipStream_t stream);
 
-/* Row a6. One-layer multi-head temporal attention embedding for each query q.
+/* One-layer multi-head temporal attention embedding (TGN's temporal neighbourhood
+ * aggregation, Section VII-A), for each query q.
  *   q     = W_q [M[q_node] || phi(0)] + b_q
  *   K_j   = W_k [M[nbr_j] || x[eid_j] || phi(q_t - t_j)] + b_k,  V_j likewise with W_v
  *   per head h (d_attn / n_heads columns), over valid slots j (nbr_j >= 0):
@@ -214,7 +218,7 @@ mtgnn_status mtgnn_temporal_attn(const int32_t* q_node, const float* q_t, const 
                                  const mtgnn_attn_params* params, const mtgnn_dims* dims, float* z, void* save,
                                  void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Row a6 in two calls, for callers that run the first on another stream while
+/* The attention embedding in two calls, for callers that run the first on another stream while
  * the memory table is still being updated (it reads neither the memory nor
  * the queries).  mtgnn_temporal_attn is exactly
  * mtgnn_temporal_attn_prepare followed by mtgnn_temporal_attn_prepared on
@@ -252,7 +256,7 @@ mtgnn_status mtgnn_temporal_attn_prepared(const int32_t* q_node, const float* q_
                                           const float* time_b, const mtgnn_attn_params* params, const mtgnn_dims* d,
                                           float* z, void* save, hipStream_t stream);
 
-/* Row a7. Backward of mtgnn_temporal_attn for the output gradient dz [max_q, d_attn].
+/* Backward of the attention embedding, mtgnn_temporal_attn for the output gradient dz [max_q, d_attn].
  * The caller computes dz from the masked loss (Eq. 13).
  *   grads -- every attention parameter gradient (overwritten);
  *   d_mem -- [max_rows, d_mem] float32 out, row r aligned with uniq[r]: the sum of
@@ -271,7 +275,7 @@ mtgnn_status mtgnn_temporal_attn_bwd(const int32_t* q_node, const float* q_t, co
                                      float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes,
                                      hipStream_t stream);
 
-/* Row a7 with two streams: the same computation, arguments and results as
+/* Attention backward with two streams: the same computation, arguments and results as
  * mtgnn_temporal_attn_bwd, with the d_mem part (grouping every occurrence of
  * an updated node and summing it) enqueued on a second stream so that it runs
  * concurrently with the parameter gradients, which stay on `stream`.
@@ -296,7 +300,7 @@ mtgnn_status mtgnn_temporal_attn_bwd_overlap(const int32_t* q_node, const float*
                                              float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
                                              hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join);
 
-/* Row a7, the d_mem grouping ahead of the gradients: every occurrence of an updated node among the
+/* Attention backward, the d_mem grouping ahead of the gradients: every occurrence of an updated node among the
  * queries and the valid neighbour slots, keyed by its updated row, sorted stably by key, and each
  * row's segment bounds, written into ws (the backward's workspace, mtgnn_workspace_bytes for
  * MTGNN_OP_TEMPORAL_ATTN_BWD).  It reads only q_node / n_q, the sampled neighbours nbr
@@ -311,7 +315,7 @@ mtgnn_status mtgnn_temporal_attn_bwd_group(const int32_t* q_node, const int32_t*
                                            const int32_t* n_rows, int64_t max_rows, const mtgnn_dims* dims,
                                            void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Row a7 with two streams, the grouping done ahead: as mtgnn_temporal_attn_bwd_overlap, except that
+/* Attention backward with two streams, the grouping done ahead: as mtgnn_temporal_attn_bwd_overlap, except that
  * the d_mem grouping is the one mtgnn_temporal_attn_bwd_group left in ws, so there is no fork at
  * entry.  dmem_stream must be ordered after that call (it was enqueued on dmem_stream, or
  * dmem_stream waits for it).  The call records `fork` on `stream` once the gradients the sums need
@@ -330,7 +334,7 @@ mtgnn_status mtgnn_temporal_attn_bwd_grouped(const int32_t* q_node, const float*
                                              float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
                                              hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join);
 
-/* Row a8. Backward of mtgnn_gru_update for d_mem = dL/dh' [max_rows, d_mem].
+/* Backward of the GRU memory update (Eq. 2), mtgnn_gru_update, for d_mem = dL/dh' [max_rows, d_mem].
  * The previous memory h is detached.
  *   save, msg   -- the forward call's (save must not be NULL there);
  *   dW_ih, dW_hh, db_ih, db_hh -- float32, overwritten;
@@ -342,7 +346,7 @@ mtgnn_status mtgnn_gru_update_bwd(const float* d_mem, const void* save, const vo
                                   float* dW_ih, float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time,
                                   void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Row a9. Time-encoder gradient of the messages (Eq. 1), ACCUMULATED into d_time_w/d_time_b:
+/* Time-encoder gradient of the messages (Eq. 1), ACCUMULATED into d_time_w/d_time_b:
  *   d_time_w[j] += sum_r dmsg_time[r, j] * (-sin(arg_rj)) * dt[r]
  *   d_time_b[j] += sum_r dmsg_time[r, j] * (-sin(arg_rj))
  * where arg_rj = time_w[j] * dt[r] + time_b[j], rounded as in mtgnn_build_messages.

@@ -116,7 +116,10 @@ __device__ __forceinline__ void gather_q_body(int64_t q, int lane, const int32_t
     q_in[q * Dq + c] = v;
     m_in[q * (da + dm) + da + c] = v;
   }
-  for (int j = lane; j < dt; j += 64) q_in[q * Dq + dm + j] = pack_val(cosf(time_arg(tw[j], 0.f, tb[j])), bf16);
+  for (int j = lane; j < dt; j += 64) {
+    const float arg = time_arg(tw[j], 0.f, tb[j]);
+    q_in[q * Dq + dm + j] = bf16 ? round_to_bf16(cos_for_bf16(arg)) : cosf(arg);
+  }
 }
 
 // Wave per query: the rows of its valid slots, [M[n_j] || x[e_j] || cos(w (tau - t_j) + b)],
@@ -176,8 +179,10 @@ __device__ __forceinline__ void gather_kv_body(int64_t q, int lane, const int32_
       if (j0 + u >= c) break;
       const float delta = __shfl(my_delta, j0 + u, 64);
       const int64_t row = off + j0 + u;
-      for (int jj = lane; jj < dt; jj += 64)
-        kv_in[row * Dkv + dm + de + jj] = pack_val(cosf(time_arg(tw[jj], delta, tb[jj])), bf16);
+      for (int jj = lane; jj < dt; jj += 64) {
+        const float arg = time_arg(tw[jj], delta, tb[jj]);
+        kv_in[row * Dkv + dm + de + jj] = bf16 ? round_to_bf16(cos_for_bf16(arg)) : cosf(arg);
+      }
     }
   }
 }

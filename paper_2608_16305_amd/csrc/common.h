@@ -92,6 +92,20 @@ __device__ __forceinline__ float time_arg(float w, float dt, float b) {
   return a;
 }
 
+// cos(arg) as it enters a bfloat16 matrix input.  The rounding to bfloat16 (nearest, ties to even)
+// is a quantisation: it must be decided on the correctly rounded float32 cosine, not on a float32
+// routine's approximation of it, or a value that lies near a bfloat16 rounding midpoint can round
+// the other way.  The float32 cosine is within a few units in the last place; when its 16 discarded
+// bits lie within 16 units of the midpoint 0x8000, the cosine is recomputed in double precision and
+// rounded to float32, which is then the correctly rounded value except within 2^-29 relative of a
+// float32 midpoint.
+__device__ __forceinline__ float cos_for_bf16(float arg) {
+  float y = cosf(arg);
+  const int low = (int)(__float_as_uint(y) & 0xFFFFu) - 0x8000;
+  if (low >= -16 && low <= 16) y = (float)cos((double)arg);
+  return y;
+}
+
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
 
 // Wave-level reductions (wave64).

@@ -216,7 +216,10 @@ __global__ __launch_bounds__(256) void k_build_messages(const int32_t* __restric
     out[c] = mn[c];
     out[dm + c] = mp[c];
   }
-  for (int j = lane; j < dt_dim; j += 64) Elem<T>::store(out, 2 * dm + j, cosf(time_arg(tw[j], dt, tb[j])));
+  for (int j = lane; j < dt_dim; j += 64) {
+    const float arg = time_arg(tw[j], dt, tb[j]);
+    Elem<T>::store(out, 2 * dm + j, sizeof(T) == 2 ? cos_for_bf16(arg) : cosf(arg));
+  }
   if (de > 0) {
     const float* xr = x + (int64_t)eid[i] * de;
     for (int c = lane; c < de; c += 64) Elem<T>::store(out, 2 * dm + dt_dim + c, xr[c]);

@@ -78,8 +78,10 @@ def test_workload3_window():
 @pytest.mark.parametrize("cid", [4, 5])
 def test_full_size_sampled(cid):
     """Workloads 4 (10M nodes, 100M events, batch 60,000, k 20, fp32) and 5 (replay / pruned
-    masks, bf16) at full size, mid-stream: the whole memory phase and every gradient, with the
+    masks, bf16) at full size, mid-stream: the adjacency (every offset, and the whole lists of every
+    queried node), the whole memory phase, every query row's neighbours, and every gradient with the
     loss gradient on the queries of 256 sampled target events per step."""
+    from tests._gpu import check_csr_full_size, query_nodes_of
     w = workload(cid)
     log(f"[parity] workload {cid} {w.name}: generating the stream")
     s = make_stream(w)
@@ -89,8 +91,13 @@ def test_full_size_sampled(cid):
     r = _runner(w, s, params, mem, lu)
     del mem, lu
     torch.cuda.synchronize()
-    for b in range(w.window_b0, w.window_b0 + 2):
-        compare_step_sampled(r, w, s, b, TOL[w.dtype], n_sample=256, seed=b)
+    steps = range(w.window_b0, w.window_b0 + 2)
+    nodes = query_nodes_of(s, w, steps)
+    log(f"[parity] oracle adjacency of the {nodes.size} queried nodes")
+    adj = tgn.build_adjacency_for(s.src, s.dst, s.t, w.n_nodes, nodes)
+    check_csr_full_size(r, s, w, adj, nodes)
+    for b in steps:
+        compare_step_sampled(r, w, s, b, TOL[w.dtype], n_sample=256, adj=adj, seed=b)
 
 
 # ----------------------------------------------------------------------------- edge cases
