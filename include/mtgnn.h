@@ -356,6 +356,24 @@ mtgnn_status mtgnn_build_messages_bwd(const float* dmsg_time, const float* dt, c
                                       const mtgnn_dims* dims, float* d_time_w, float* d_time_b, void* ws,
                                       size_t ws_bytes, hipStream_t stream);
 
+/* mtgnn_build_messages_bwd without a workspace, for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  Same arguments, computation,
+ * kernels and bitwise results as mtgnn_build_messages_bwd, minus (ws, ws_bytes): the row-chunk partial
+ * sums live in a device scratch array of MTGNN_NOALLOC_SCRATCH_BYTES (4 MiB) that the library holds on
+ * every GPU it runs on until the process ends.  The call allocates and frees nothing.
+ *   - The request needs 8 * d_time * ceil(max_rows / 32) bytes (rounded up to 256); beyond 4 MiB the
+ *     call returns MTGNN_EWORKSPACE before any launch (d_time = 100 allows max_rows up to 167,744).
+ *   - `stream` must belong to the current device (else MTGNN_EINVAL); its first call on a device looks
+ *     up that device's scratch address (MTGNN_EHIP if that fails).
+ *   - Every call on one GPU shares that GPU's scratch, which keeps the last call's partials (nothing in
+ *     it needs to start at zero).  Calls that overlap on one GPU (other streams, other host threads)
+ *     race on it: order them. */
+#define MTGNN_NOALLOC_SCRATCH_BYTES (4 << 20)
+mtgnn_status mtgnn_build_messages_bwd_noalloc(const float* dmsg_time, const float* dt, const int32_t* n_rows,
+                                              int64_t max_rows, const float* time_w, const float* time_b,
+                                              const mtgnn_dims* dims, float* d_time_w, float* d_time_b,
+                                              hipStream_t stream);
+
 /* Temporal adjacency of a whole stream (built once, offline; outside the step).
  * Event e = (src[e], dst[e], t[e]) with eid e gives two entries: (node src,
  * nbr dst, role 0) and (node dst, nbr src, role 1).  Entries are grouped by

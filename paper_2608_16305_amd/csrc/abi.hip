@@ -1,5 +1,6 @@
 // C ABI of the mtgnn library: argument validation (host only, before any HIP
 // call), workspace sizing, status strings, and dispatch to the step kernels.
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -67,6 +68,41 @@ static mtgnn_status check_rows(int64_t max_rows) {
 
 #define REQ(p, name) \
   if (!(p)) return fail(MTGNN_EINVAL, name " is NULL")
+
+// ------------------------------------------------------------------ allocation-free scratch
+
+// Device-resident scratch of the allocation-free entry point.  Each GPU the library runs on holds its
+// own copy for the life of the process.  In host code `scratch` names a host-side stand-in, never the
+// device address: the address is taken once per device with hipGetSymbolAddress and only that pointer
+// reaches kernels.
+static __device__ __align__(256) unsigned char scratch[MTGNN_NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[MAX_DEVICES] = {};
+
+// The scratch address on the current device (looked up on the first call on that device).
+static mtgnn_status scratch_on_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    set_hip_error(e, "hipGetDevice");
+    return MTGNN_EHIP;
+  }
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(MTGNN_EUNSUPPORTED, "device ordinal beyond 64");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      set_hip_error(e, "hipGetSymbolAddress(scratch)");
+      return MTGNN_EHIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MTGNN_OK;
+}
 
 }  // namespace mtgnn
 
@@ -469,6 +505,39 @@ mtgnn_status mtgnn_build_messages_bwd(const float* dmsg_time, const float* dt, c
   REQ(ws, "ws");
   return build_messages_bwd_impl(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d, d_time_w, d_time_b, ws, ws_bytes,
                                  stream);
+}
+
+mtgnn_status mtgnn_build_messages_bwd_noalloc(const float* dmsg_time, const float* dt, const int32_t* n_rows,
+                                              int64_t max_rows, const float* time_w, const float* time_b,
+                                              const mtgnn_dims* d, float* d_time_w, float* d_time_b,
+                                              hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  if (max_rows == 0 || d->d_time == 0) return MTGNN_OK;
+  REQ(dmsg_time, "dmsg_time");
+  REQ(dt, "dt");
+  REQ(time_w, "time_w");
+  REQ(time_b, "time_b");
+  REQ(d_time_w, "d_time_w");
+  REQ(d_time_b, "d_time_b");
+  const size_t need = build_messages_bwd_ws(d, max_rows);
+  if (need > (size_t)MTGNN_NOALLOC_SCRATCH_BYTES)
+    return fail(MTGNN_EWORKSPACE, "build_messages_bwd_noalloc: 8 * d_time * ceil(max_rows / 32) bytes exceed the "
+                                  "4 MiB device scratch");
+  if (stream) {
+    int cur = -1, sdev = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess) e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) {
+      set_hip_error(e, "stream device");
+      return MTGNN_EHIP;
+    }
+    if (sdev != cur) return fail(MTGNN_EINVAL, "stream is not on the current device");
+  }
+  void* ws = nullptr;
+  MTGNN_TRY(scratch_on_current_device(&ws));
+  return build_messages_bwd_impl(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d, d_time_w, d_time_b, ws,
+                                 (size_t)MTGNN_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 mtgnn_status mtgnn_build_temporal_csr(const int32_t* src, const int32_t* dst, const float* t, int64_t n_events,

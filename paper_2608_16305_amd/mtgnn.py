@@ -25,7 +25,7 @@ ENTRY_POINTS = (
     "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap", "mtgnn_temporal_attn_bwd_group",
     "mtgnn_temporal_attn_bwd_grouped",
     "mtgnn_gru_update_bwd",
-    "mtgnn_build_messages_bwd", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
+    "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
 )
 
@@ -84,6 +84,7 @@ _SIGS = {
                                         _SZ, _P, _P, _P, _P],
     "mtgnn_gru_update_bwd": [_P, _P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_build_messages_bwd": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _SZ, _P],
+    "mtgnn_build_messages_bwd_noalloc": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_workspace_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
     "mtgnn_save_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
@@ -405,6 +406,15 @@ def mtgnn_build_messages_bwd(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d:
                                           C.byref(d), _ptr(d_time_w, torch.float32, "d_time_w"),
                                           _ptr(d_time_b, torch.float32, "d_time_b"), wp, wb, _stream(stream)),
            "mtgnn_build_messages_bwd")
+
+
+def mtgnn_build_messages_bwd_noalloc(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d: Dims, d_time_w, d_time_b,
+                                     stream=None):
+    _check(lib().mtgnn_build_messages_bwd_noalloc(
+        _ptr(dmsg_time, torch.float32, "dmsg_time"), _ptr(dt, torch.float32, "dt"),
+        _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows), _ptr(time_w, torch.float32, "time_w"),
+        _ptr(time_b, torch.float32, "time_b"), C.byref(d), _ptr(d_time_w, torch.float32, "d_time_w"),
+        _ptr(d_time_b, torch.float32, "d_time_b"), _stream(stream)), "mtgnn_build_messages_bwd_noalloc")
 
 
 def mtgnn_build_temporal_csr(src, dst, t, n_nodes, csr_off, csr_nbr, csr_t, csr_eid, ws, stream=None):
