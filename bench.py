@@ -34,10 +34,10 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=0, help="timed steps (0: 50, or 30 for batches of 60,000)")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3)
-    ap.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for the CPU baseline (0: skip)")
+    ap.add_argument("--cpu-steps", type=int, default=3, help="oracle steps timed for the CPU baseline (0: skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="before the warmup, copy a buffer of this many MiB twice (HBM counter calibration)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -48,6 +48,10 @@ def parse():
 
 def main():
     args = parse()
+    if args.steps <= 0:   # 50 (30 for batches of 60,000), within the stream after the window start
+        from synth import workload as _wl
+        wl = _wl(args.workload)
+        args.steps = min(30 if wl.batch >= 60_000 else 50, (wl.n_batches - wl.window_b0 - args.warmup) // 2)
     if args.traffic_from:
         write_traffic(args)
         return
@@ -65,7 +69,7 @@ def main():
     params = init_params(w)
     b0 = w.window_b0
     mem, lu = window_state(w, s, b0)
-    n_steps = args.warmup + args.steps
+    n_steps = args.warmup + 2 * args.steps   # the headline's K steps, then K more for the kernel timer
     if b0 + n_steps > w.n_batches:
         raise SystemExit(f"window [{b0}, {b0 + n_steps}) exceeds the {w.n_batches} batches of the stream")
     runner = TGNStep(w, s, params, mem, lu)
@@ -106,22 +110,34 @@ def main():
             site_ms[site] = max(site_ms.get(site, 0.0), ms)
     torch.cuda.synchronize()
     dominant = max(site_ms, key=site_ms.get) if site_ms else HOT_SITES[0]
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    M.timer_start(dominant, 16 * args.steps)
-    t0 = time.perf_counter()
-    ev0.record()
-    for i in range(args.warmup, n_steps):
-        runner.step(b0 + i, dzs[i])
-    enq = time.perf_counter() - t0   # host time to enqueue the timed steps (launch-bound when close to wall)
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    dom_ms, dom_launches = M.timer_stop()
-    gpu_ms = ev0.elapsed_time(ev1)
+
+    def timed(first, count, site=None):
+        """GPU milliseconds of `count` steps from step index `first` (HIP events on the main stream), and the
+        host's enqueue and wall time; with `site`, the library's launch timer brackets that kernel's launches
+        with HIP events on their own stream."""
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if site:
+            M.timer_start(site, 16 * count)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0.record()
+        for i in range(first, first + count):
+            runner.step(b0 + i, dzs[i])
+        enq = time.perf_counter() - t0
+        ev1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        site_t = M.timer_stop() if site else None
+        return ev0.elapsed_time(ev1), enq, wall, site_t
+
+    # the headline: K steps with nothing but the step in the timed region
+    gpu_ms, enq, wall, _ = timed(args.warmup, args.steps)
+    # the dominant kernel's launch durations: the next K steps, with its launches bracketed
+    gpu_ms2, _, _, (dom_ms, dom_launches) = timed(args.warmup + args.steps, args.steps, dominant)
     ms_per_step = gpu_ms / args.steps
     events = w.batch * args.steps
     value = events / (gpu_ms / 1e3)
-    target_events = sum(n_tar[args.warmup:])
+    target_events = sum(n_tar[args.warmup:args.warmup + args.steps])
 
     out = {
         "metric": "events/sec per batch step (fwd+bwd) on 1 MI355X; % HBM / MFMA roofline",
@@ -144,11 +160,9 @@ def main():
                    "n_heads": w.n_heads, "first_batch": b0, "order": "lag-1"},
     }
 
-    # algorithmic work of the dominant kernel: valid neighbour slots of the timed steps
-    valid_pairs = 0
-    for i in range(args.warmup, n_steps):
-        b = b0 + i
-        valid_pairs += valid_slots(runner, s, w, b)
+    # algorithmic work of the dominant kernel: valid neighbour slots of the steps it was timed on
+    lo2, hi2 = args.warmup + args.steps, n_steps
+    valid_pairs = sum(valid_slots(runner, s, w, b0 + i) for i in range(lo2, hi2))
     launches_per_step = dom_launches / args.steps
     # every launch of a hot site covers all valid slots of its step (K and V share one launch)
     per_launch_pairs = valid_pairs / args.steps / max(launches_per_step, 1.0)
@@ -159,8 +173,10 @@ def main():
     out["roofline"] = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                        "frac": achieved / peak, "traffic": read_traffic(dominant, w), "kernel": dominant,
                        "launches_per_step": launches_per_step, "avg_launch_us": avg_s * 1e6,
-                       "flops_per_launch": flops,
+                       "flops_per_launch": flops, "timed_over": f"steps {lo2}..{hi2 - 1} after the headline's "
+                       f"(their ms/step {gpu_ms2 / args.steps:.4f})",
                        "warmup_site_us": {k: v * 1e3 for k, v in site_ms.items()}}
+    out["step_counts"] = step_counts(runner, s, w, b0, args.warmup, args.steps)
 
     if args.cpu_steps > 0:
         out["cpu_baseline"] = cpu_baseline(w, s, params, mem, lu, b0, args.cpu_steps)
@@ -182,23 +198,23 @@ def SITE_N(site, w):
 
 
 def valid_slots(runner, s, w, b):
-    """Non-padded neighbour slots of step b's queries (recomputed on the host from the
-    device-built adjacency, outside the timed region)."""
-    import torch
+    """Non-padded neighbour slots of step b's queries, counted on the host from the device-built
+    adjacency (outside the timed regions): per query, min(k, entries of its node strictly before
+    its time), by one binary search over the keys (node << 32 | float bits of t), which sort as the
+    adjacency does since times are non-negative."""
+    if not hasattr(runner, "_adj_keys"):
+        off = runner.csr_off.cpu().numpy()
+        ct = runner.csr_t.cpu().numpy()[:off[-1]]
+        node = np.repeat(np.arange(off.size - 1, dtype=np.uint64), np.diff(off))
+        runner._adj_keys = (node << np.uint64(32)) | ct.view(np.uint32).astype(np.uint64)
+        runner._adj_off = off
     elo, ehi = runner.batch_range(b)
     tar = np.ones(ehi - elo, bool) if s.flags is None else (s.flags[elo:ehi] & 3) == 0
-    q_node = np.concatenate([s.src[elo:ehi][tar], s.dst[elo:ehi][tar], s.neg[elo:ehi][tar]]).astype(np.int64)
-    q_t = np.tile(s.t[elo:ehi][tar], 3)
-    off = runner.csr_off.cpu().numpy() if not hasattr(runner, "_off_np") else runner._off_np
-    runner._off_np = off
-    if not hasattr(runner, "_csr_t_np"):
-        runner._csr_t_np = runner.csr_t.cpu().numpy()
-    ct = runner._csr_t_np
-    cnt = 0
-    for n, tau in zip(q_node, q_t):
-        lo, hi = off[n], off[n + 1]
-        cnt += min(w.k, int(np.searchsorted(ct[lo:hi], tau, side="left")))
-    return cnt
+    q_node = np.concatenate([s.src[elo:ehi][tar], s.dst[elo:ehi][tar], s.neg[elo:ehi][tar]]).astype(np.uint64)
+    q_t = np.tile(s.t[elo:ehi][tar], 3).astype(np.float32)
+    qk = (q_node << np.uint64(32)) | q_t.view(np.uint32).astype(np.uint64)
+    before = np.searchsorted(runner._adj_keys, qk, side="left") - runner._adj_off[q_node.astype(np.int64)]
+    return int(np.minimum(before, w.k).sum())
 
 
 # ------------------------------------------------------------------ HBM traffic from counter runs
@@ -288,27 +304,57 @@ def write_traffic(args):
     print(json.dumps(rec))
 
 
+def step_counts(runner, s, w, b0, first, count):
+    """Mean per-step sizes of the timed steps: updated rows (the memory batch's distinct non-pruned
+    endpoints), queries and valid neighbour slots (host-side counts, outside the timed region)."""
+    U = Q = P = 0
+    for i in range(first, first + count):
+        b = b0 + i
+        mlo, mhi = (b - 1) * w.batch, b * w.batch
+        act = np.ones(mhi - mlo, bool) if s.flags is None else (s.flags[mlo:mhi] & 2) == 0
+        U += np.unique(np.concatenate([s.src[mlo:mhi][act], s.dst[mlo:mhi][act]])).size
+        elo, ehi = runner.batch_range(b)
+        Q += 3 * (ehi - elo if s.flags is None else int(((s.flags[elo:ehi] & 3) == 0).sum()))
+        P += valid_slots(runner, s, w, b)
+    return {"updated_rows": U / count, "queries": Q / count, "valid_slots": P / count}
+
+
 def cpu_baseline(w, s, params, mem, lu, b0, n):
-    """The oracle (unchanged) on the host cores, over the first n steps of the same window."""
-    from threadpoolctl import threadpool_info
+    """The oracle (unchanged) on the host cores, over the first n steps of the same window, once with
+    its BLAS pinned to one thread and once with all threads."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import tgn
     from synth import loss_noise
-    adj = tgn.build_adjacency(s.src, s.dst, s.t, w.n_nodes)
-    prec = tgn.Prec("bf16" if w.dtype == "bf16" else "f32")
-    m, l = mem.copy(), lu.copy()
-    t0 = time.perf_counter()
+    # the adjacency lists the sample needs: those of the nodes its steps query (the oracle's own build)
+    q_nodes = []
     for i in range(n):
-        b = b0 + i
-        mb = tgn.batch_dict(s, (b - 1) * w.batch, b * w.batch)
-        eb = tgn.batch_dict(s, b * w.batch, (b + 1) * w.batch)
-        r = tgn.step(prec, w, m, l, params, adj, s.x, mb, eb, loss_noise(w, b, 3 * w.batch))
-        m, l = r.mp.mem, r.mp.lu
-    dt = time.perf_counter() - t0
+        lo, hi = (b0 + i) * w.batch, (b0 + i + 1) * w.batch
+        tar = np.ones(hi - lo, bool) if s.flags is None else (s.flags[lo:hi] & 3) == 0
+        q_nodes += [s.src[lo:hi][tar], s.dst[lo:hi][tar], s.neg[lo:hi][tar]]
+    adj = tgn.build_adjacency_for(s.src, s.dst, s.t, w.n_nodes, np.unique(np.concatenate(q_nodes)))
+    prec = tgn.Prec("bf16" if w.dtype == "bf16" else "f32")
+
+    def run():
+        m, l = mem.copy(), lu.copy()
+        t0 = time.perf_counter()
+        for i in range(n):
+            b = b0 + i
+            mb = tgn.batch_dict(s, (b - 1) * w.batch, b * w.batch)
+            eb = tgn.batch_dict(s, b * w.batch, (b + 1) * w.batch)
+            r = tgn.step(prec, w, m, l, params, adj, s.x, mb, eb, loss_noise(w, b, 3 * w.batch))
+            m, l = r.mp.mem, r.mp.lu
+        return w.batch * n / (time.perf_counter() - t0)
+
+    with threadpool_limits(limits=1):
+        one = run()
+    allv = run()
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": w.batch * n / dt, "unit": "events/s", "cores": threads, "kind": "oracle",
+    return {"value": allv, "unit": "events/s", "cores": threads, "kind": "oracle",
+            "single_thread": {"value": one, "cores": 1},
             "sample": f"{n} consecutive steps from batch {b0} of the same workload ({w.batch * n} events), "
-                      f"float64 NumPy oracle, {os.cpu_count()} host CPUs visible"}
+                      f"float64 NumPy oracle, timed with its BLAS at all {threads} threads and again at 1; "
+                      f"{os.cpu_count()} host CPUs visible"}
 
 
 if __name__ == "__main__":
