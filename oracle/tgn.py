@@ -533,6 +533,72 @@ def message_bwd(prec: Prec, dims, dx, dt, time_w, time_b):
     return (dphi * s * np.asarray(dt, F64)[:, None]).sum(0), (dphi * s).sum(0)
 
 
+# --------------------------------------------------------------------------- link prediction and the masked loss
+
+def _softplus(x):
+    """log(1 + e^x), evaluated without overflow."""
+    return np.maximum(x, 0.0) + np.log1p(np.exp(-np.abs(x)))
+
+
+@dataclass
+class LinkLoss:
+    loss: float              # the masked batch loss (Eq. 13)
+    s_pos: np.ndarray        # [n_tar] score of (src, dst)
+    s_neg: np.ndarray        # [n_tar] score of (src, neg)
+    dz: np.ndarray           # [3 n_tar, d_a] d loss / d z in the query layout
+    grads: dict              # W_d1, b_d1, W_d2, b_d2
+
+
+def link_loss(params, z, n_tar: int) -> LinkLoss:
+    """Masked link-prediction loss of one batch (Eq. 12-13) and its gradient.
+
+    z holds the embeddings of the batch's queries: src of the target events,
+    then their dst, then their negatives (n_tar rows each; replayed and pruned
+    events have none, which is the target mask of Eq. 12).  The edge score is
+    TGN's link predictor: s(a, b) = W_d2 relu(W_d1 [z_a || z_b] + b_d1) + b_d2.
+    The edge prediction loss of a target event is the binary cross-entropy of
+    its true edge (label 1) and of its negative edge (label 0):
+        l = -log sigmoid(s(src, dst)) - log(1 - sigmoid(s(src, neg)))
+          = softplus(-s_pos) + softplus(s_neg),
+    and the batch loss is the mean over target events, 0 without any (Eq. 13).
+    Float64 throughout; the decoder's weights are float32 values.
+    """
+    W1 = np.asarray(params["W_d1"], F64)
+    b1 = np.asarray(params["b_d1"], F64)
+    W2 = np.asarray(params["W_d2"], F64)
+    b2 = np.asarray(params["b_d2"], F64)
+    z = np.asarray(z, F64)
+    n = int(n_tar)
+    da = W1.shape[0]
+    zs, zd, zn = z[:n], z[n:2 * n], z[2 * n:3 * n]
+    x_pos = np.concatenate([zs, zd], axis=1)
+    x_neg = np.concatenate([zs, zn], axis=1)
+    pre_pos = x_pos @ W1.T + b1
+    pre_neg = x_neg @ W1.T + b1
+    h_pos = np.maximum(pre_pos, 0.0)
+    h_neg = np.maximum(pre_neg, 0.0)
+    s_pos = (h_pos @ W2.T + b2)[:, 0]
+    s_neg = (h_neg @ W2.T + b2)[:, 0]
+    if n == 0:
+        g = {"W_d1": np.zeros_like(W1), "b_d1": np.zeros_like(b1), "W_d2": np.zeros_like(W2),
+             "b_d2": np.zeros_like(b2)}
+        return LinkLoss(0.0, s_pos, s_neg, np.zeros((0, da)), g)
+    loss = float(np.mean(_softplus(-s_pos) + _softplus(s_neg)))
+    # d loss / d score: (sigmoid(s) - label) / n
+    ds_pos = (_sigmoid(s_pos) - 1.0) / n
+    ds_neg = _sigmoid(s_neg) / n
+    dh_pos = ds_pos[:, None] * W2[0] * (pre_pos > 0)
+    dh_neg = ds_neg[:, None] * W2[0] * (pre_neg > 0)
+    g = {"W_d2": (ds_pos @ h_pos + ds_neg @ h_neg)[None, :],
+         "b_d2": np.array([ds_pos.sum() + ds_neg.sum()]),
+         "W_d1": dh_pos.T @ x_pos + dh_neg.T @ x_neg,
+         "b_d1": dh_pos.sum(0) + dh_neg.sum(0)}
+    dx_pos = dh_pos @ W1
+    dx_neg = dh_neg @ W1
+    dz = np.concatenate([dx_pos[:, :da] + dx_neg[:, :da], dx_pos[:, da:], dx_neg[:, da:]], axis=0)
+    return LinkLoss(loss, s_pos, s_neg, dz, g)
+
+
 # --------------------------------------------------------------------------- one step
 
 @dataclass
@@ -549,17 +615,22 @@ class StepResult:
     ag: AttnGrads
     d_mem: np.ndarray
     grads: dict = field(default_factory=dict)   # every parameter gradient (float64)
+    link: Optional[LinkLoss] = None
 
 
 def step(prec: Prec, dims, mem, lu, params, adj: Adjacency, x_all, mem_batch: Optional[dict],
-         emb_batch: dict, noise) -> StepResult:
+         emb_batch: dict, noise, loss: str = "noise") -> StepResult:
     """One training step over a mixed batch.
 
     The memory phase runs on ``mem_batch`` (the previous batch under the
     default lag-1 order, or the current one under lag-0), the embedding on the
     target events of ``emb_batch`` with the updated table, then the backward
-    pass with the masked-loss gradient dZ = noise / n_tar (Eq. 13; zero when the
-    batch has no target event).
+    pass.  Its input dZ is the gradient of the masked loss of Eq. 13:
+    ``loss="link"`` takes the link-prediction loss (``link_loss``: the decoder
+    and the binary cross-entropy of each target event's true and negative
+    edge, averaged over target events); ``loss="noise"`` takes a linear
+    stand-in with the same masking, dZ = noise / n_tar (zero when the batch has
+    no target event), which lets a test put the gradient on chosen rows.
     """
     if mem_batch is None:
         mem_batch = {"src": np.zeros(0, np.int64), "dst": np.zeros(0, np.int64),
@@ -568,8 +639,13 @@ def step(prec: Prec, dims, mem, lu, params, adj: Adjacency, x_all, mem_batch: Op
     q_node, q_t, n_tar = queries(emb_batch)
     nbr, nt, neid = sample_recent(adj, q_node, q_t, dims.k)
     sv = attention_fwd(prec, dims, mp.mem, x_all, params, q_node, q_t, nbr, nt, neid)
-    noise = np.asarray(noise, F64)[:q_node.size]
-    dz = noise / n_tar if n_tar > 0 else np.zeros_like(noise)
+    link = None
+    if loss == "link":
+        link = link_loss(params, sv.z, n_tar)
+        dz = link.dz
+    else:
+        noise = np.asarray(noise, F64)[:q_node.size]
+        dz = noise / n_tar if n_tar > 0 else np.zeros_like(noise)
     ag = attention_bwd(prec, dims, params, sv, dz)
     d_mem = memory_grad(mp.uniq, q_node, nbr, ag.dhq, ag.dhn)
     gg, dx = gru_bwd(d_mem, mp.msg, mp.h_old, mp.gates, prec.weight(params["W_ih"]),
@@ -579,7 +655,9 @@ def step(prec: Prec, dims, mem, lu, params, adj: Adjacency, x_all, mem_batch: Op
     grads.update(gg)
     grads["time_w"] = ag.d_time_w + dtw
     grads["time_b"] = ag.d_time_b + dtb
-    return StepResult(mp, q_node, q_t, n_tar, nbr, nt, neid, sv, dz, ag, d_mem, grads)
+    if link is not None:
+        grads.update(link.grads)
+    return StepResult(mp, q_node, q_t, n_tar, nbr, nt, neid, sv, dz, ag, d_mem, grads, link)
 
 
 def batch_dict(stream, lo: int, hi: int) -> dict:

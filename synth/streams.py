@@ -208,6 +208,13 @@ def init_params(w: Workload, base_seed: int = 0, random_bias: bool = False,
     p["time_w"] = (10.0 ** (-9.0 * j / max(dt - 1, 1))).astype(np.float32)
     p["time_b"] = (rb.uniform(-1.0, 1.0, dt).astype(np.float32) if random_bias
                    else np.zeros(dt, np.float32))
+    # link-prediction decoder [z_src || z_other] -> d_attn -> 1, drawn after everything above
+    for name, (fo, fi) in (("W_d1", (da, 2 * da)), ("W_d2", (1, da))):
+        a = np.sqrt(6.0 / (fi + fo))
+        p[name] = rng.uniform(-a, a, size=(fo, fi)).astype(np.float32)
+    for name, n in (("b_d1", da), ("b_d2", 1)):
+        p[name] = (rb.uniform(-bias_scale, bias_scale, n).astype(np.float32) if random_bias
+                   else np.zeros(n, np.float32))
     return p
 
 

@@ -683,3 +683,116 @@ def test_bf16_rounding_placement():
     # weights enter the products rounded: a product with unrounded W_2 differs from z by ~1e-3
     z_unrounded_w = sv.a1 @ np.asarray(params["W_2"], np.float64).T + params["b_2"]
     assert np.abs(z_unrounded_w - sv.z).max() > 1e-5
+
+
+# --------------------------------------------------------------------------- link prediction loss (Eq. 12-13)
+
+def _link_case(seed=0, n=7, da=6):
+    w = tiny_workload(d_attn=da, n_heads=2)
+    p = init_params(w, random_bias=True)
+    rng = np.random.default_rng(seed)
+    z = rng.standard_normal((3 * n, da))
+    return p, z
+
+
+def test_link_loss_matches_torch_bce_with_logits():
+    """The masked loss and every gradient against torch's binary cross-entropy with logits and autograd
+    (float64 on the CPU), with the predictor written from its parameters: W_d2 relu(W_d1 [z_a || z_b] + b_d1) + b_d2."""
+    p, z = _link_case()
+    n = z.shape[0] // 3
+    ref = tgn.link_loss(p, z, n)
+    tz = torch.tensor(z, requires_grad=True)
+    tp = {k: torch.tensor(np.asarray(p[k], np.float64), requires_grad=True) for k in ("W_d1", "b_d1", "W_d2", "b_d2")}
+
+    def score(a, b):
+        h = torch.relu(torch.nn.functional.linear(torch.cat([a, b], 1), tp["W_d1"], tp["b_d1"]))
+        return torch.nn.functional.linear(h, tp["W_d2"], tp["b_d2"])[:, 0]
+
+    pos, neg = score(tz[:n], tz[n:2 * n]), score(tz[:n], tz[2 * n:])
+    bce = torch.nn.functional.binary_cross_entropy_with_logits
+    L = bce(pos, torch.ones(n, dtype=torch.float64)) + bce(neg, torch.zeros(n, dtype=torch.float64))
+    L.backward()
+    assert abs(ref.loss - L.item()) < 1e-13
+    assert np.allclose(ref.s_pos, pos.detach().numpy(), rtol=0, atol=1e-13)
+    assert np.allclose(ref.s_neg, neg.detach().numpy(), rtol=0, atol=1e-13)
+    assert np.allclose(ref.dz, tz.grad.numpy(), rtol=0, atol=1e-14)
+    for k in tp:
+        assert np.allclose(ref.grads[k], tp[k].grad.numpy(), rtol=0, atol=1e-14), k
+
+
+def test_link_loss_per_event_sum_and_special_cases():
+    """Eq. 13 written event by event in plain Python: the mean over target events of
+    -log sigmoid(s_pos) - log(1 - sigmoid(s_neg)); a zero output layer gives 2 log 2; no target, 0."""
+    p, z = _link_case(seed=3, n=5)
+    n = 5
+    ref = tgn.link_loss(p, z, n)
+    W1, b1, W2, b2 = (np.asarray(p[k], np.float64) for k in ("W_d1", "b_d1", "W_d2", "b_d2"))
+
+    def s(a, b):
+        x = list(a) + list(b)
+        h = [max(0.0, sum(W1[j][c] * x[c] for c in range(len(x))) + b1[j]) for j in range(len(b1))]
+        return sum(W2[0][j] * h[j] for j in range(len(h))) + b2[0]
+
+    tot = 0.0
+    for i in range(n):
+        sp, sn = s(z[i], z[n + i]), s(z[i], z[2 * n + i])
+        tot += -math.log(1.0 / (1.0 + math.exp(-sp))) - math.log(1.0 - 1.0 / (1.0 + math.exp(-sn)))
+    assert abs(ref.loss - tot / n) < 1e-12
+    p0 = dict(p, W_d2=np.zeros_like(p["W_d2"]), b_d2=np.zeros_like(p["b_d2"]))
+    assert abs(tgn.link_loss(p0, z, n).loss - 2 * math.log(2.0)) < 1e-15
+    empty = tgn.link_loss(p, z[:0], 0)
+    assert empty.loss == 0.0 and empty.dz.shape == (0, z.shape[1])
+    assert all(np.all(g == 0) for g in empty.grads.values())
+
+
+def test_link_loss_masks_replay_and_pruned_events():
+    """Only target events enter the loss (Eq. 12-13): replayed and pruned events get no query, so the
+    step's loss equals the mean of the per-event losses of the target events alone."""
+    w, s, params, mem0, lu0, adj, prev, cur, noise = _fd_setup(seed=5)
+    params.update({k: np.asarray(v, np.float64) for k, v in init_params(w, random_bias=True).items()
+                   if k.endswith(("d1", "d2"))})
+    p64 = tgn.Prec("f64")
+    flags = np.array([0, 1, 0, 3, 1, 0, 0, 1], np.uint8)
+    r = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, dict(cur, flags=flags), None, loss="link")
+    tar = np.nonzero(flags == 0)[0]
+    assert r.n_tar == tar.size and r.q_node.size == 3 * tar.size
+    full = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, cur, None, loss="link")
+    # the same events' embeddings (each query sees the same neighbours whatever the mask)
+    nf = full.n_tar
+    zt = np.concatenate([full.attn.z[tar], full.attn.z[nf + tar], full.attn.z[2 * nf + tar]])
+    assert np.allclose(zt, r.attn.z, rtol=0, atol=1e-14)
+    per = tgn._softplus(-full.link.s_pos) + tgn._softplus(full.link.s_neg)
+    assert abs(r.link.loss - per[tar].mean()) < 1e-14
+    none = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, dict(cur, flags=np.ones(8, np.uint8)), None,
+                    loss="link")
+    assert none.link.loss == 0.0 and all(np.all(np.asarray(g) == 0) for g in none.grads.values())
+
+
+def test_link_step_backward_matches_central_differences():
+    """The whole step under the link loss (decoder, attention, GRU, time encoder): every parameter's
+    gradient against central differences of the loss in float64."""
+    w, s, params, mem0, lu0, adj, prev, cur, noise = _fd_setup(seed=2)
+    params.update({k: np.asarray(v, np.float64) for k, v in init_params(w, random_bias=True).items()
+                   if k.endswith(("d1", "d2"))})
+    p64 = tgn.Prec("f64")
+    res = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, cur, None, loss="link")
+    assert {"W_d1", "b_d1", "W_d2", "b_d2", "W_ih", "W_k", "time_w"} <= set(res.grads)
+
+    def loss(pp):
+        return tgn.step(p64, w, mem0, lu0, pp, adj, s.x, prev, cur, None, loss="link").link.loss
+
+    h = 1e-6
+    for name, g in res.grads.items():
+        base = params[name]
+        fd = np.zeros(base.size)
+        for i in range(base.size):
+            pp = dict(params)
+            for sgn in (1, -1):
+                arr = base.copy().reshape(-1)
+                arr[i] += sgn * h
+                pp[name] = arr.reshape(base.shape)
+                fd[i] += sgn * loss(pp)
+        fd /= 2 * h
+        scale = max(np.abs(fd).max(), 1e-4)
+        err = np.abs(fd - np.asarray(g).reshape(-1)).max() / scale
+        assert err < 1e-6, (name, err)
