@@ -3,9 +3,11 @@
 One step = the whole hot path over one batch: memory phase on the previous
 batch (most-recent aggregation, message construction, GRU update with
 write-back), embedding of the current batch's target events (queries,
-most-recent-k sampling, temporal attention), and the backward pass (attention,
-GRU, time encoder).  Inputs (event stream, temporal adjacency, memory table,
-parameters, loss gradients) are resident in HBM before the timed region.
+most-recent-k sampling, temporal attention), the masked link-prediction loss
+(decoder, binary cross-entropy of the true and negative edges, mean over the
+target events), and the backward pass (decoder, attention, GRU, time encoder).
+Inputs (event stream, temporal adjacency, memory table, parameters) are
+resident in HBM before the timed region.
 
 Default workload: the skewed stream (1M nodes, 10M events, Zipf(1.2) endpoints,
 batch 4,000, k = 10, memory/time/attention width 100, 2 heads, float32),
@@ -62,7 +64,7 @@ def main():
     import torch
 
     from paper_2608_16305_amd.step import TGNStep
-    from synth import init_params, loss_noise, make_stream, window_state, workload
+    from synth import init_params, make_stream, window_state, workload
 
     w = workload(args.workload)
     s = make_stream(w)
@@ -74,15 +76,11 @@ def main():
         raise SystemExit(f"window [{b0}, {b0 + n_steps}) exceeds the {w.n_batches} batches of the stream")
     runner = TGNStep(w, s, params, mem, lu)
 
-    # per-step loss gradients dZ = G / n_tar (masked loss), resident before timing
-    dzs, n_tar = [], []
+    # target events per step (Eq. 12), for the target-only throughput
+    n_tar = []
     for i in range(n_steps):
-        b = b0 + i
-        lo, hi = b * w.batch, min(w.n_events, (b + 1) * w.batch)
-        nt = (hi - lo) if s.flags is None else int(((s.flags[lo:hi] & 3) == 0).sum())
-        G = loss_noise(w, b, runner.max_q)
-        dzs.append(torch.from_numpy((G / max(nt, 1)).astype(np.float32)).cuda())
-        n_tar.append(nt)
+        lo, hi = (b0 + i) * w.batch, min(w.n_events, (b0 + i + 1) * w.batch)
+        n_tar.append((hi - lo) if s.flags is None else int(((s.flags[lo:hi] & 3) == 0).sum()))
     torch.cuda.synchronize()
 
     from paper_2608_16305_amd import mtgnn as M
@@ -104,7 +102,7 @@ def main():
         site = HOT_SITES[i % len(HOT_SITES)] if i >= 1 else None
         if site:
             M.timer_start(site, 16)
-        runner.step(b0 + i, dzs[i])
+        runner.step(b0 + i)
         if site:
             ms, n = M.timer_stop()
             site_ms[site] = max(site_ms.get(site, 0.0), ms)
@@ -122,7 +120,7 @@ def main():
         t0 = time.perf_counter()
         ev0.record()
         for i in range(first, first + count):
-            runner.step(b0 + i, dzs[i])
+            runner.step(b0 + i)
         enq = time.perf_counter() - t0
         ev1.record()
         torch.cuda.synchronize()
@@ -325,7 +323,6 @@ def cpu_baseline(w, s, params, mem, lu, b0, n):
     from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import tgn
-    from synth import loss_noise
     # the adjacency lists the sample needs: those of the nodes its steps query (the oracle's own build)
     q_nodes = []
     for i in range(n):
@@ -342,7 +339,7 @@ def cpu_baseline(w, s, params, mem, lu, b0, n):
             b = b0 + i
             mb = tgn.batch_dict(s, (b - 1) * w.batch, b * w.batch)
             eb = tgn.batch_dict(s, b * w.batch, (b + 1) * w.batch)
-            r = tgn.step(prec, w, m, l, params, adj, s.x, mb, eb, loss_noise(w, b, 3 * w.batch))
+            r = tgn.step(prec, w, m, l, params, adj, s.x, mb, eb, None, loss="link")
             m, l = r.mp.mem, r.mp.lu
         return w.batch * n / (time.perf_counter() - t0)
 

@@ -93,6 +93,18 @@ typedef struct {
   const float *b_q, *b_k, *b_v, *b_o, *b_1, *b_2;
 } mtgnn_attn_params;
 
+/* Link-prediction decoder parameters (float32 whatever the dims' dtype): the edge score
+ *   s(a, b) = W_d2 relu(W_d1 [z_a || z_b] + b_d1) + b_d2,
+ * W_d1 [d_attn, 2 d_attn], b_d1 [d_attn], W_d2 [1, d_attn], b_d2 [1]. */
+typedef struct {
+  const float *W_d1, *b_d1, *W_d2, *b_d2;
+} mtgnn_link_params;
+
+/* Decoder parameter gradients (float32, same shapes, overwritten). */
+typedef struct {
+  float *W_d1, *b_d1, *W_d2, *b_d2;
+} mtgnn_link_grads;
+
 /* Attention parameter gradients (float32, same shapes, overwritten). */
 typedef struct {
   float *W_q, *W_k, *W_v, *W_o, *W_1, *W_2;
@@ -109,7 +121,8 @@ typedef enum {
   MTGNN_OP_TEMPORAL_ATTN_BWD = 6,
   MTGNN_OP_GRU_UPDATE_BWD = 7,
   MTGNN_OP_BUILD_MESSAGES_BWD = 8,
-  MTGNN_OP_BUILD_CSR = 9
+  MTGNN_OP_BUILD_CSR = 9,
+  MTGNN_OP_LINK_LOSS = 10
 } mtgnn_op;
 
 /* Workspace bytes for `op`.  max_rows is the batch size n for BUILD_QUERIES and
@@ -333,6 +346,27 @@ mtgnn_status mtgnn_temporal_attn_bwd_grouped(const int32_t* q_node, const float*
                                              mtgnn_attn_grads* grads, float* d_mem, float* d_time_w,
                                              float* d_time_b, void* ws, size_t ws_bytes, hipStream_t stream,
                                              hipStream_t dmem_stream, hipEvent_t fork, hipEvent_t join);
+
+/* The masked batch loss of Eq. 13 with the link-prediction edge loss, and its gradient.
+ * z holds the embeddings of the batch's queries as mtgnn_build_queries lists them: the src of
+ * the n_tar target events, then their dst, then their negatives, n_tar = n_q / 3 (replayed
+ * and pruned events have no query: this is the target mask M_p of Eq. 12).  Each target
+ * event's edge loss is the binary cross-entropy of its true edge (label 1) and its negative
+ * edge (label 0) under the decoder score s that mtgnn_link_params defines, TGN's link predictor
+ * (Section VII-A):
+ *   l = softplus(-s(src, dst)) + softplus(s(src, neg)),
+ * and the batch loss is the mean of l over the target events, or 0 when there is none.
+ *   z      -- [max_q, d_attn] float32 (mtgnn_temporal_attn's output); max_q a multiple of 3;
+ *   loss   -- device float32 scalar out;
+ *   scores -- [2, max_q / 3] float32 out, s(src, dst) then s(src, neg) per target event, or NULL;
+ *   dz     -- [max_q, d_attn] float32 out: d loss / d z, rows < n_q (the input of
+ *             mtgnn_temporal_attn_bwd);
+ *   grads  -- the decoder's gradients, overwritten (zero when there is no target event).
+ * Deterministic: every sum runs in a fixed order.  Errors: EINVAL (NULL pointers, max_q not a
+ * multiple of 3), EUNSUPPORTED (d_attn > 128), EWORKSPACE. */
+mtgnn_status mtgnn_link_loss(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* params,
+                             const mtgnn_dims* dims, float* loss, float* scores, float* dz, mtgnn_link_grads* grads,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Backward of the GRU memory update (Eq. 2), mtgnn_gru_update, for d_mem = dL/dh' [max_rows, d_mem].
  * The previous memory h is detached.

@@ -354,9 +354,10 @@ class AttnSave:
     m1: np.ndarray
     a1: np.ndarray
     z: np.ndarray
+    relu1: np.ndarray        # the ReLU decisions of m1 (m1 > 0 unless flipped)
 
 
-def attention_fwd(prec: Prec, dims, mem, x_all, params, q_node, q_t, nbr, nt, neid) -> AttnSave:
+def attention_fwd(prec: Prec, dims, mem, x_all, params, q_node, q_t, nbr, nt, neid, flip_m1=None) -> AttnSave:
     """One layer of multi-head temporal attention over the sampled neighbours.
 
     q   = W_q [M[q] || phi(0)] + b_q
@@ -364,6 +365,9 @@ def attention_fwd(prec: Prec, dims, mem, x_all, params, q_node, q_t, nbr, nt, ne
     per head h (d_a/H columns): p = softmax_j(q_h . K_jh / sqrt(d_a/H)) over valid j,
     attn_h = sum_j p_j V_jh (zero when no neighbour is valid)
     o = W_o attn + b_o;  z = W_2 relu(W_1 [o || M[q]] + b_1) + b_2
+
+    ``flip_m1`` (boolean, the shape of m1) inverts chosen ReLU decisions; a caller uses it only
+    where m1 lies within rounding distance of zero, where either decision is a valid result.
     """
     dm, de, da, H = dims.d_mem, dims.d_edge, dims.d_attn, dims.n_heads
     dh = da // H
@@ -407,11 +411,14 @@ def attention_fwd(prec: Prec, dims, mem, x_all, params, q_node, q_t, nbr, nt, ne
     o = attn_p @ W["W_o"].T + b["b_o"]
     m_in = np.concatenate([prec.pack(o), hq], axis=1)
     m1 = m_in @ W["W_1"].T + b["b_1"]
-    a1 = prec.pack(np.maximum(m1, 0.0))
+    relu1 = m1 > 0
+    if flip_m1 is not None:
+        relu1 = relu1 ^ flip_m1
+    a1 = prec.pack(np.where(relu1, m1, 0.0))
     z = a1 @ W["W_2"].T + b["b_2"]
     return AttnSave(np.asarray(q_node), np.asarray(q_t), np.asarray(nbr), np.asarray(nt),
                     np.asarray(neid), valid, hq, q_in, q, kv_in, dts, K, V, p, attn_p, o,
-                    m_in, m1, a1, z)
+                    m_in, m1, a1, z, relu1)
 
 
 @dataclass
@@ -435,7 +442,7 @@ def attention_bwd(prec: Prec, dims, params, sv: AttnSave, dz) -> AttnGrads:
     # z = a1 W_2^T + b_2
     g["W_2"] = dz.T @ sv.a1
     g["b_2"] = dz.sum(0)
-    dm1 = (dz @ W["W_2"]) * (sv.m1 > 0)
+    dm1 = (dz @ W["W_2"]) * sv.relu1
     # m1 = m_in W_1^T + b_1
     g["W_1"] = dm1.T @ sv.m_in
     g["b_1"] = dm1.sum(0)
@@ -547,9 +554,11 @@ class LinkLoss:
     s_neg: np.ndarray        # [n_tar] score of (src, neg)
     dz: np.ndarray           # [3 n_tar, d_a] d loss / d z in the query layout
     grads: dict              # W_d1, b_d1, W_d2, b_d2
+    pre_pos: np.ndarray      # [n_tar, d_a] hidden pre-activations of the true edges
+    pre_neg: np.ndarray      # [n_tar, d_a] ... and of the negative edges
 
 
-def link_loss(params, z, n_tar: int) -> LinkLoss:
+def link_loss(params, z, n_tar: int, flip_pos=None, flip_neg=None) -> LinkLoss:
     """Masked link-prediction loss of one batch (Eq. 12-13) and its gradient.
 
     z holds the embeddings of the batch's queries: src of the target events,
@@ -561,7 +570,8 @@ def link_loss(params, z, n_tar: int) -> LinkLoss:
         l = -log sigmoid(s(src, dst)) - log(1 - sigmoid(s(src, neg)))
           = softplus(-s_pos) + softplus(s_neg),
     and the batch loss is the mean over target events, 0 without any (Eq. 13).
-    Float64 throughout; the decoder's weights are float32 values.
+    Float64 throughout; the decoder's weights are float32 values.  ``flip_pos`` / ``flip_neg``
+    (boolean, [n_tar, d_a]) invert chosen ReLU decisions, as ``attention_fwd``'s ``flip_m1``.
     """
     W1 = np.asarray(params["W_d1"], F64)
     b1 = np.asarray(params["b_d1"], F64)
@@ -575,20 +585,22 @@ def link_loss(params, z, n_tar: int) -> LinkLoss:
     x_neg = np.concatenate([zs, zn], axis=1)
     pre_pos = x_pos @ W1.T + b1
     pre_neg = x_neg @ W1.T + b1
-    h_pos = np.maximum(pre_pos, 0.0)
-    h_neg = np.maximum(pre_neg, 0.0)
+    on_pos = pre_pos > 0 if flip_pos is None else (pre_pos > 0) ^ flip_pos
+    on_neg = pre_neg > 0 if flip_neg is None else (pre_neg > 0) ^ flip_neg
+    h_pos = np.where(on_pos, pre_pos, 0.0)
+    h_neg = np.where(on_neg, pre_neg, 0.0)
     s_pos = (h_pos @ W2.T + b2)[:, 0]
     s_neg = (h_neg @ W2.T + b2)[:, 0]
     if n == 0:
         g = {"W_d1": np.zeros_like(W1), "b_d1": np.zeros_like(b1), "W_d2": np.zeros_like(W2),
              "b_d2": np.zeros_like(b2)}
-        return LinkLoss(0.0, s_pos, s_neg, np.zeros((0, da)), g)
+        return LinkLoss(0.0, s_pos, s_neg, np.zeros((0, da)), g, pre_pos, pre_neg)
     loss = float(np.mean(_softplus(-s_pos) + _softplus(s_neg)))
     # d loss / d score: (sigmoid(s) - label) / n
     ds_pos = (_sigmoid(s_pos) - 1.0) / n
     ds_neg = _sigmoid(s_neg) / n
-    dh_pos = ds_pos[:, None] * W2[0] * (pre_pos > 0)
-    dh_neg = ds_neg[:, None] * W2[0] * (pre_neg > 0)
+    dh_pos = ds_pos[:, None] * W2[0] * on_pos
+    dh_neg = ds_neg[:, None] * W2[0] * on_neg
     g = {"W_d2": (ds_pos @ h_pos + ds_neg @ h_neg)[None, :],
          "b_d2": np.array([ds_pos.sum() + ds_neg.sum()]),
          "W_d1": dh_pos.T @ x_pos + dh_neg.T @ x_neg,
@@ -596,7 +608,7 @@ def link_loss(params, z, n_tar: int) -> LinkLoss:
     dx_pos = dh_pos @ W1
     dx_neg = dh_neg @ W1
     dz = np.concatenate([dx_pos[:, :da] + dx_neg[:, :da], dx_pos[:, da:], dx_neg[:, da:]], axis=0)
-    return LinkLoss(loss, s_pos, s_neg, dz, g)
+    return LinkLoss(loss, s_pos, s_neg, dz, g, pre_pos, pre_neg)
 
 
 # --------------------------------------------------------------------------- one step
@@ -619,7 +631,7 @@ class StepResult:
 
 
 def step(prec: Prec, dims, mem, lu, params, adj: Adjacency, x_all, mem_batch: Optional[dict],
-         emb_batch: dict, noise, loss: str = "noise") -> StepResult:
+         emb_batch: dict, noise, loss: str = "noise", flips: Optional[dict] = None) -> StepResult:
     """One training step over a mixed batch.
 
     The memory phase runs on ``mem_batch`` (the previous batch under the
@@ -631,17 +643,20 @@ def step(prec: Prec, dims, mem, lu, params, adj: Adjacency, x_all, mem_batch: Op
     edge, averaged over target events); ``loss="noise"`` takes a linear
     stand-in with the same masking, dZ = noise / n_tar (zero when the batch has
     no target event), which lets a test put the gradient on chosen rows.
+    ``flips`` ({"m1": ..., "pos": ..., "neg": ...}, boolean arrays) inverts chosen ReLU decisions of
+    the merge layer and the decoder (see ``attention_fwd``).
     """
+    flips = flips or {}
     if mem_batch is None:
         mem_batch = {"src": np.zeros(0, np.int64), "dst": np.zeros(0, np.int64),
                      "t": np.zeros(0, F32), "eid": np.zeros(0, np.int64)}
     mp = memory_phase(prec, dims, mem_batch, mem, lu, x_all, params)
     q_node, q_t, n_tar = queries(emb_batch)
     nbr, nt, neid = sample_recent(adj, q_node, q_t, dims.k)
-    sv = attention_fwd(prec, dims, mp.mem, x_all, params, q_node, q_t, nbr, nt, neid)
+    sv = attention_fwd(prec, dims, mp.mem, x_all, params, q_node, q_t, nbr, nt, neid, flips.get("m1"))
     link = None
     if loss == "link":
-        link = link_loss(params, sv.z, n_tar)
+        link = link_loss(params, sv.z, n_tar, flips.get("pos"), flips.get("neg"))
         dz = link.dz
     else:
         noise = np.asarray(noise, F64)[:q_node.size]

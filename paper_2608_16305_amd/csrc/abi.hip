@@ -186,6 +186,7 @@ size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int6
     case MTGNN_OP_TEMPORAL_ATTN_BWD: return attn_bwd_ws(d, max_q, max_rows);
     case MTGNN_OP_GRU_UPDATE_BWD: return gru_update_bwd_ws(d, max_rows);
     case MTGNN_OP_BUILD_MESSAGES_BWD: return build_messages_bwd_ws(d, max_rows);
+    case MTGNN_OP_LINK_LOSS: return link_loss_ws(d, max_q);
     default: return 0;
   }
 }
@@ -486,6 +487,33 @@ mtgnn_status mtgnn_gru_update_bwd(const float* d_mem, const void* save, const vo
   REQ(ws, "ws");
   return gru_update_bwd_impl(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d, dW_ih, dW_hh, db_ih, db_hh, dmsg_time,
                              ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_link_loss(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* params,
+                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* grads,
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  if (max_q < 0 || max_q >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (max_q % 3 != 0) return fail(MTGNN_EINVAL, "max_q is not a multiple of 3 (src, dst and negative blocks)");
+  if (d->d_attn > 128) return fail(MTGNN_EUNSUPPORTED, "link_loss: d_attn > 128");
+  REQ(params, "params");
+  REQ(grads, "grads");
+  REQ(params->W_d1, "W_d1");
+  REQ(params->b_d1, "b_d1");
+  REQ(params->W_d2, "W_d2");
+  REQ(params->b_d2, "b_d2");
+  REQ(grads->W_d1, "dW_d1");
+  REQ(grads->b_d1, "db_d1");
+  REQ(grads->W_d2, "dW_d2");
+  REQ(grads->b_d2, "db_d2");
+  REQ(loss, "loss");
+  if (max_q > 0) {
+    REQ(z, "z");
+    REQ(dz, "dz");
+  }
+  if (ws_bytes < link_loss_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "link_loss ws");
+  REQ(ws, "ws");
+  return link_loss_impl(z, n_q, max_q, params, d, loss, scores, dz, grads, ws, ws_bytes, stream);
 }
 
 mtgnn_status mtgnn_build_messages_bwd(const float* dmsg_time, const float* dt, const int32_t* n_rows,

@@ -57,6 +57,12 @@ mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const in
                            const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
                            bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
 
+// link-prediction decoder and the masked batch loss
+size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q);
+mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* p,
+                            const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
+                            size_t ws_bytes, hipStream_t s);
+
 // sampling / adjacency
 mtgnn_status sample_recent_impl(const int64_t* off, const int32_t* nbr, const float* t, const int32_t* eid,
                                 const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q, int k,

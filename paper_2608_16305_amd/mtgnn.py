@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmtgnn.so
 F32, BF16 = 0, 1
 OP_BUILD_QUERIES, OP_AGGREGATE_LAST, OP_BUILD_MESSAGES, OP_GRU_UPDATE, OP_SAMPLE_RECENT = 0, 1, 2, 3, 4
 OP_TEMPORAL_ATTN, OP_TEMPORAL_ATTN_BWD, OP_GRU_UPDATE_BWD, OP_BUILD_MESSAGES_BWD, OP_BUILD_CSR = 5, 6, 7, 8, 9
+OP_LINK_LOSS = 10
 
 ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
@@ -24,7 +25,7 @@ ENTRY_POINTS = (
     "mtgnn_temporal_attn_prepare_slots", "mtgnn_temporal_attn_prepared",
     "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap", "mtgnn_temporal_attn_bwd_group",
     "mtgnn_temporal_attn_bwd_grouped",
-    "mtgnn_gru_update_bwd",
+    "mtgnn_gru_update_bwd", "mtgnn_link_loss",
     "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
 )
@@ -55,6 +56,17 @@ class AttnGrads(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in _ATTN]
 
 
+_LINK = ("W_d1", "b_d1", "W_d2", "b_d2")
+
+
+class LinkParams(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in _LINK]
+
+
+class LinkGrads(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in _LINK]
+
+
 _P = C.c_void_p
 _I64 = C.c_int64
 _I32 = C.c_int32
@@ -83,6 +95,8 @@ _SIGS = {
                                         C.POINTER(AttnParams), C.POINTER(Dims), C.POINTER(AttnGrads), _P, _P, _P, _P,
                                         _SZ, _P, _P, _P, _P],
     "mtgnn_gru_update_bwd": [_P, _P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_link_loss": [_P, _P, _I64, C.POINTER(LinkParams), C.POINTER(Dims), _P, _P, _P, C.POINTER(LinkGrads), _P,
+                        _SZ, _P],
     "mtgnn_build_messages_bwd": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _SZ, _P],
     "mtgnn_build_messages_bwd_noalloc": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
@@ -395,6 +409,22 @@ def mtgnn_gru_update_bwd(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d: Dims
                                       _ptr(db_ih, torch.float32, "db_ih"), _ptr(db_hh, torch.float32, "db_hh"),
                                       _ptr(dmsg_time, torch.float32, "dmsg_time", True), wp, wb, _stream(stream)),
            "mtgnn_gru_update_bwd")
+
+
+def link_params(p: dict) -> LinkParams:
+    return LinkParams(*[_ptr(p[n], torch.float32, n) for n in _LINK])
+
+
+def link_grads(g: dict) -> LinkGrads:
+    return LinkGrads(*[_ptr(g[n], torch.float32, "d" + n) for n in _LINK])
+
+
+def mtgnn_link_loss(z, n_q, max_q, params: LinkParams, d: Dims, loss, scores, dz, grads: LinkGrads, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_link_loss(_ptr(z, torch.float32, "z"), _ptr(n_q, torch.int32, "n_q", True), int(max_q),
+                                 C.byref(params), C.byref(d), _ptr(loss, torch.float32, "loss"),
+                                 _ptr(scores, torch.float32, "scores", True), _ptr(dz, torch.float32, "dz"),
+                                 C.byref(grads), wp, wb, _stream(stream)), "mtgnn_link_loss")
 
 
 def mtgnn_build_messages_bwd(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d: Dims, d_time_w, d_time_b, ws,

@@ -3,6 +3,7 @@
 A step on batch b (default lag-1 order) runs
   memory phase on batch b-1:  aggregate_last -> build_messages -> gru_update
   embedding on batch b:       build_queries  -> sample_recent  -> temporal_attn (prepare, prepared)
+  loss:                       link_loss (decoder and the masked loss of Eq. 13, giving dZ)
   backward:                   temporal_attn_bwd -> gru_update_bwd -> build_messages_bwd
 all enqueued on one HIP stream with no host synchronisation (the only
 data-dependent sizes, updated rows and queries, stay in device memory), except
@@ -23,6 +24,7 @@ from . import mtgnn as M
 
 ATTN_W = ("W_q", "W_k", "W_v", "W_o", "W_1", "W_2")
 ATTN_B = ("b_q", "b_k", "b_v", "b_o", "b_1", "b_2")
+LINK = ("W_d1", "b_d1", "W_d2", "b_d2")   # the decoder: float32 in every storage mode
 
 
 class TGNStep:
@@ -51,7 +53,7 @@ class TGNStep:
         self.params = {}
         for k, v in params.items():
             tv = torch.from_numpy(np.ascontiguousarray(v)).to(dev)
-            self.params[k] = tv.to(self.sdt) if k.startswith("W") else tv.float()
+            self.params[k] = tv.to(self.sdt) if k.startswith("W") and k not in LINK else tv.float()
         self.memory = torch.from_numpy(np.ascontiguousarray(memory)).to(dev).to(self.sdt).contiguous()
         self.last_update = torch.from_numpy(np.ascontiguousarray(last_update, np.float32)).to(dev)
         # temporal adjacency, built once on the device
@@ -96,7 +98,18 @@ class TGNStep:
         self.d_mem = torch.empty(R, w.d_mem, **f32)
         self.dmsg_time = torch.empty(R, max(w.d_time, 1), **f32)
         self.grads = {n: torch.empty(tuple(self.params[n].shape), **f32)
-                      for n in list(ATTN_W) + list(ATTN_B) + ["W_ih", "W_hh", "b_ih", "b_hh", "time_w", "time_b"]}
+                      for n in list(ATTN_W) + list(ATTN_B) + ["W_ih", "W_hh", "b_ih", "b_hh", "time_w", "time_b"]
+                      + [n for n in LINK if n in self.params]}
+        self.has_link = all(n in self.params for n in LINK)
+        if self.has_link:
+            # the masked loss: its value, the edge scores and dZ; its own workspace, because the second
+            # stream's d_mem grouping fills the main workspace during the embedding
+            self.loss = torch.zeros(1, **f32)
+            self.scores = torch.empty(2, B, **f32)
+            self.dz = torch.empty(Q, w.d_attn, **f32)
+            self.ws_link = M.alloc_bytes(M.workspace_bytes(M.OP_LINK_LOSS, d, 0, Q), dev)
+            self.lp = M.link_params(self.params)
+            self.lg = M.link_grads(self.grads)
         ops = [(M.OP_BUILD_QUERIES, B, 0), (M.OP_AGGREGATE_LAST, B, 0), (M.OP_GRU_UPDATE, R, 0),
                (M.OP_TEMPORAL_ATTN, 0, Q), (M.OP_TEMPORAL_ATTN_BWD, R, Q), (M.OP_GRU_UPDATE_BWD, R, 0),
                (M.OP_BUILD_MESSAGES_BWD, R, 0)]
@@ -187,6 +200,12 @@ class TGNStep:
                                        self.memory, self.x, p["time_w"], p["time_b"], self.ap, self.d, self.z,
                                        self.attn_save, stream=s)
 
+    def link_loss(self):
+        """The masked loss of the embedded batch (Eq. 13) and dZ, on the main stream."""
+        M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz, self.lg,
+                          self.ws_link, stream=self.ts)
+        return self.dz
+
     def backward(self, dz):
         self._q_chain = self._q_chain if self._in_step else 0
         p, g, s = self.params, self.grads, self.ts
@@ -222,8 +241,9 @@ class TGNStep:
         lo = b * self.B
         return lo, min(self.n_events, lo + self.B)
 
-    def step(self, b, dz):
-        """One training step on batch b: memory phase (lag order), embedding, backward."""
+    def step(self, b, dz=None):
+        """One training step on batch b: memory phase (lag order), embedding, the masked link-prediction
+        loss, backward.  A given dz [max_q, d_attn] replaces the loss's gradient (the loss is not run)."""
         elo, ehi = self.batch_range(b)
         self._in_step = True
         if self.lag == 1:
@@ -276,6 +296,8 @@ class TGNStep:
         else:
             self.memory_phase(mlo, mhi)
             self.embed(elo, ehi)
+        if dz is None:
+            dz = self.link_loss()
         self.backward(dz)
         self._in_step = False
         self._q_chain = self._q_chain + 1 if self.overlap else 0

@@ -176,7 +176,6 @@ def test_backward_overlap_bitwise():
     the d_mem grouping at the backward's entry (mtgnn_temporal_attn_bwd_overlap) and with it done
     during the embedding (mtgnn_temporal_attn_bwd_group, then _grouped)."""
     from paper_2608_16305_amd.step import TGNStep
-    from tests._gpu import dz_tensor, n_targets
     w = workload(2)
     log("[parity] overlap vs single stream, workload 2")
     s = make_stream(w)
@@ -188,12 +187,12 @@ def test_backward_overlap_bitwise():
         r.group_ahead = ahead
         res = {}
         for b in range(1, 4):
-            dz, _ = dz_tensor(r, w, b, n_targets(s, *r.batch_range(b)))
-            r.step(b, dz)
+            r.step(b)   # with the masked link-prediction loss, as in training
             torch.cuda.synchronize()
             n = int(r.n_uniq.item())
             res[f"d_mem{b}"] = to_np(r.d_mem)[:n].copy()
             res.update({f"{k}{b}": to_np(v).copy() for k, v in r.grads.items()})
+            res[f"loss{b}"] = to_np(r.loss).copy()
         res["memory"] = to_np(r.memory).copy()
         outs.append(res)
         del r

@@ -796,3 +796,27 @@ def test_link_step_backward_matches_central_differences():
         scale = max(np.abs(fd).max(), 1e-4)
         err = np.abs(fd - np.asarray(g).reshape(-1)).max() / scale
         assert err < 1e-6, (name, err)
+
+
+def test_relu_flips_only_change_the_chosen_decisions():
+    """Inverting no ReLU decision changes nothing; inverting one whose pre-activation is zero changes
+    no forward value and makes the backward take the other one-sided derivative."""
+    w, s, params, mem0, lu0, adj, prev, cur, noise = _fd_setup(seed=4)
+    p64 = tgn.Prec("f64")
+    r0 = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, cur, None, loss="link")
+    none = {"m1": np.zeros_like(r0.attn.m1, bool), "pos": np.zeros_like(r0.link.pre_pos, bool),
+            "neg": np.zeros_like(r0.link.pre_neg, bool)}
+    r1 = tgn.step(p64, w, mem0, lu0, params, adj, s.x, prev, cur, None, loss="link", flips=none)
+    for k in r0.grads:
+        assert np.array_equal(r0.grads[k], r1.grads[k]), k
+    # shift b_d1 so that one decoder unit of event 0's true edge sits exactly at zero
+    j = int(np.argmax(np.abs(r0.link.pre_pos[0])))
+    pz = dict(params, b_d1=params["b_d1"].copy())
+    pz["b_d1"][j] -= r0.link.pre_pos[0, j]
+    a = tgn.step(p64, w, mem0, lu0, pz, adj, s.x, prev, cur, None, loss="link")
+    assert a.link.pre_pos[0, j] == 0.0
+    fl = dict(none, pos=none["pos"].copy())
+    fl["pos"][0, j] = True
+    bb = tgn.step(p64, w, mem0, lu0, pz, adj, s.x, prev, cur, None, loss="link", flips=fl)
+    assert a.link.loss == bb.link.loss
+    assert not np.array_equal(a.grads["W_d1"], bb.grads["W_d1"])
