@@ -97,7 +97,7 @@ __global__ void k_link_finish(const float* __restrict__ sums, int da, float* __r
 
 struct LinkWs {
   int32_t* n_tar;
-  float *Y, *DA, *DB, *Hp, *sums, *db_scratch;
+  float *Y, *DA, *DB, *Hp, *sums, *db_scratch, *Wp, *part;
   void* rest;
   size_t rest_bytes;
 };
@@ -124,6 +124,8 @@ LinkWs link_ws_layout(void* ws, int da, int64_t max_q, size_t* total = nullptr) 
   L.Hp = (float*)take(sizeof(float) * (size_t)(max_tar < 1 ? 1 : max_tar) * (da + 2));
   L.sums = (float*)take(sizeof(float) * (size_t)(da + 2));
   L.db_scratch = (float*)take(sizeof(float) * (size_t)da);
+  L.Wp = (float*)take(sizeof(float) * link_fused_weight_floats(da));
+  L.part = (float*)take(sizeof(float) * (size_t)cdiv(max_tar < 1 ? 1 : max_tar, 16) * (da + 2));
   L.rest_bytes = link_rest_bytes(da, max_q);
   L.rest = take(L.rest_bytes);
   if (total) *total = off;
@@ -147,7 +149,14 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
   if (ws_bytes < link_loss_ws(d, max_q)) return MTGNN_EWORKSPACE;
   const int64_t max_tar = max_q / 3;
   LinkWs L = link_ws_layout(ws, da, max_q);
-  // first layer's two halves over every query row
+  if (link_fused_ok(da)) {
+    MTGNN_TRY(link_fused(z, n_q, max_q, da, p->W_d1, p->b_d1, p->W_d2, p->b_d2, L.Wp, L.DA, L.DB, L.part, dz, scores,
+                         g->W_d2, g->b_d2, loss, s));
+    const DwProblem dp[2] = {{L.DA, da, z, da, g->W_d1, 2 * da, da, da, g->b_d1},
+                             {L.DB, da, z, da, g->W_d1 + da, 2 * da, da, da, L.db_scratch}};
+    return linear_dw_batch(dp, 2, max_q, n_q, MTGNN_F32, L.rest, L.rest_bytes, s);
+  }
+  // general widths: the first layer's two halves over every query row
   const FwdProblem fp[2] = {{z, da, p->W_d1, 2 * da, nullptr, L.Y, 2 * da, da, da},
                             {z, da, p->W_d1 + da, 2 * da, nullptr, L.Y + da, 2 * da, da, da}};
   MTGNN_TRY(linear_fwd_batch(fp, 2, max_q, n_q, MTGNN_F32, MTGNN_F32, s));

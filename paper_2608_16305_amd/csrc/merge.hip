@@ -377,6 +377,153 @@ __global__ __launch_bounds__(64 * MW) void k_gru_dx(const float* __restrict__ dg
   });
 }
 
+// ---------------------------------------------------------------- the link-prediction decoder
+
+// One block per 16 target events (their src, dst and negative query rows of z).  Forward:
+//   pre_pos = W_a z_src + W_b z_dst + b_d1,  pre_neg = W_a z_src + W_b z_neg + b_d1,
+//   s = W_d2 relu(pre) + b_d2,  l = softplus(-s_pos) + softplus(s_neg);
+// backward: ds_pos = (sigmoid(s_pos) - 1) / n, ds_neg = sigmoid(s_neg) / n, dh = ds W_d2 [pre > 0],
+//   dz_src = (dh_pos + dh_neg) W_a, dz_dst = dh_pos W_b, dz_neg = dh_neg W_b.
+// W_a, W_b are the column halves of W_d1; Wp holds their zero-padded copies and transposes.  The
+// hidden-row gradients also go to the query-layout buffers DA (src rows: dh_pos + dh_neg, other rows
+// zero) and DB (dst rows dh_pos, neg rows dh_neg, src rows zero), for dW_d1 = [DA^T z | DB^T z];
+// part[block] = the block's sums of ds_pos h_pos + ds_neg h_neg (d_a), ds_pos + ds_neg, and l / n.
+template <int NA>
+__global__ __launch_bounds__(64 * MW) void k_link_fused(const float* __restrict__ z, const int32_t* __restrict__ n_q,
+                                                        int64_t max_tar, int da, const float* __restrict__ Wp,
+                                                        const float* __restrict__ b1, const float* __restrict__ W2,
+                                                        const float* __restrict__ b2, float* __restrict__ DA,
+                                                        float* __restrict__ DB, float* __restrict__ dz,
+                                                        float* __restrict__ scores, float* __restrict__ part) {
+  constexpr int XL = 16 * NA + 4;   // LDS row stride: >= 16 NA, XL / 4 odd
+  constexpr int NU = Tiles<NA>::per_wave;
+  constexpr size_t WSZ = (size_t)16 * MW * NU * 16 * NA;   // floats per padded copy
+  __shared__ __attribute__((aligned(16))) float T[5][16 * XL];   // z_src, z_dst, z_neg (then dh), pre_pos, pre_neg
+  __shared__ float red[MW][2 * 64 + 2];
+  const int64_t n = (n_q ? (int64_t)*n_q : 3 * max_tar) / 3;
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= n) return;   // block-uniform
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, fr = lane & 15, fg = lane >> 4;
+  for (int b = 0; b < 3; ++b) {
+    zero_cols<XL, 1>(T[b], da, 16 * NA);
+    load_rows<XL, 1>(T[b], 0, z + (int64_t)b * n * da, da, da, r0, n);
+  }
+  __syncthreads();
+  {
+    f32x4 as[NU], ad[NU], an[NU];
+    layer<NA, NA, XL, 1>(T[0], Wp, as);
+    layer<NA, NA, XL, 1>(T[1], Wp + WSZ, ad);
+    layer<NA, NA, XL, 1>(T[2], Wp + WSZ, an);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int j = 16 * (wid + MW * u) + fr;
+      if (j >= 16 * NA) continue;
+      const float bj = j < da ? b1[j] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 4 * fg + r;
+        T[3][i * XL + j] = (as[u][r] + ad[u][r]) + bj;
+        T[4][i * XL + j] = (as[u][r] + an[u][r]) + bj;
+      }
+    }
+  }
+  __syncthreads();
+  // scores, loss terms and hidden-row gradients: wave w takes events 4w .. 4w + 3
+  const float inv_n = 1.0f / (float)n;
+  float gsum[2] = {0.f, 0.f}, dsum = 0.f, lsum = 0.f;
+  float w2[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) w2[h] = lane + 64 * h < da ? W2[lane + 64 * h] : 0.f;
+  for (int e = 4 * wid; e < 4 * wid + 4; ++e) {
+    const bool ok = r0 + e < n;
+    float sp = 0.f, sn = 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int j = lane + 64 * h;
+      if (j < da) {
+        sp += w2[h] * fmaxf(T[3][e * XL + j], 0.f);
+        sn += w2[h] * fmaxf(T[4][e * XL + j], 0.f);
+      }
+    }
+    sp = wave_sum(sp) + b2[0];
+    sn = wave_sum(sn) + b2[0];
+    const float dsp = ok ? (1.0f / (1.0f + expf(-sp)) - 1.0f) * inv_n : 0.f;
+    const float dsn = ok ? (1.0f / (1.0f + expf(-sn))) * inv_n : 0.f;
+    const int64_t q = r0 + e;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int j = lane + 64 * h;
+      if (j < 16 * NA) {
+        const float pp = T[3][e * XL + j], pn = T[4][e * XL + j];
+        const float dhp = (j < da && pp > 0.f) ? dsp * w2[h] : 0.f;
+        const float dhn = (j < da && pn > 0.f) ? dsn * w2[h] : 0.f;
+        T[0][e * XL + j] = dhp + dhn;
+        T[1][e * XL + j] = dhp;
+        T[2][e * XL + j] = dhn;
+        if (ok && j < da) {
+          DA[q * da + j] = dhp + dhn;
+          DA[(n + q) * da + j] = 0.f;
+          DA[(2 * n + q) * da + j] = 0.f;
+          DB[q * da + j] = 0.f;
+          DB[(n + q) * da + j] = dhp;
+          DB[(2 * n + q) * da + j] = dhn;
+          gsum[h] += dsp * fmaxf(pp, 0.f) + dsn * fmaxf(pn, 0.f);
+        }
+      }
+    }
+    if (ok) {
+      dsum += dsp + dsn;
+      lsum += (fmaxf(-sp, 0.f) + log1pf(expf(-fabsf(sp)))) * inv_n + (fmaxf(sn, 0.f) + log1pf(expf(-fabsf(sn)))) * inv_n;
+      if (scores && lane == 0) {
+        scores[q] = sp;
+        scores[max_tar + q] = sn;
+      }
+    }
+  }
+  red[wid][lane] = gsum[0];
+  red[wid][64 + lane] = gsum[1];
+  if (lane == 0) {
+    red[wid][128] = dsum;
+    red[wid][129] = lsum;
+  }
+  __syncthreads();
+  // the block's partial sums, the four waves added in a fixed order
+  for (int c = threadIdx.x; c < da + 2; c += 64 * MW) {
+    const int k = c < da ? c : 128 + (c - da);
+    part[(int64_t)blockIdx.x * (da + 2) + c] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
+  }
+  // dz for the three query blocks
+  for (int b = 0; b < 3; ++b) {
+    f32x4 acc[NU];
+    layer<NA, NA, XL, 1>(T[b], Wp + (b == 0 ? 2 : 3) * WSZ, acc);
+    float* out = dz + (int64_t)b * n * da;
+    each_out<NA, 1>(acc, da, r0, n, [&](int i, int j, bool ok, float v) {
+      if (ok) out[(r0 + i) * da + j] = v;
+    });
+  }
+}
+
+// Column sums of the partials of the blocks that hold target events (cdiv(n_tar, 16)), in a fixed order,
+// a wave per column: dW_d2, db_d2 and the loss.
+__global__ __launch_bounds__(256) void k_link_reduce_dev(const float* __restrict__ part,
+                                                         const int32_t* __restrict__ n_q, int64_t max_tar, int da,
+                                                         float* __restrict__ dW2, float* __restrict__ db2,
+                                                         float* __restrict__ loss) {
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (c >= da + 2) return;
+  const int64_t n = (n_q ? (int64_t)*n_q : 3 * max_tar) / 3;
+  const int64_t nblk = cdiv(n, 16);
+  float v = 0.f;
+  for (int64_t b = lane; b < nblk; b += 64) v += part[b * (da + 2) + c];
+  v = wave_sum(v);
+  if (lane == 0) {
+    if (c < da) dW2[c] = v;
+    else if (c == da) db2[0] = v;
+    else loss[0] = v;
+  }
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
 
 }  // namespace
@@ -472,6 +619,57 @@ mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int
   else
     k_qproj_dx<2, 2><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
   MTGNN_CHECK_LAUNCH("qproj_dx");
+  return MTGNN_OK;
+}
+
+bool link_fused_ok(int da) {
+  const int na = (int)cdiv(da, 16);
+  return da % 4 == 0 && (na == 7 || na == 2);
+}
+
+size_t link_fused_weight_floats(int da) {
+  const int na = (int)cdiv(da, 16);
+  return (size_t)4 * 16 * MW * cdiv(na, MW) * 16 * na;
+}
+
+mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
+                        const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
+                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s) {
+  if (!link_fused_ok(da) || !aligned16(z) || !aligned16(Wp) || !aligned16(dz)) return MTGNN_EUNSUPPORTED;
+  const int na = (int)cdiv(da, 16);
+  const int rows = 16 * MW * (int)cdiv(na, MW), cols = 16 * na;
+  const size_t wsz = (size_t)rows * cols;
+  // zero-padded W_a, W_b (the column halves of W_d1) and their transposes
+  PrepArgs a;
+  for (int m = 0; m < 4; ++m) {
+    a.src[m] = W1 + (m % 2 ? da : 0);
+    a.dst[m] = Wp + m * wsz;
+    a.rows[m] = rows;
+    a.cols[m] = cols;
+    a.n[m] = da;
+    a.k[m] = da;
+    a.ld[m] = 2 * da;
+    a.tr[m] = m >= 2 ? 1 : 0;
+    a.ldd[m] = cols;
+  }
+  a.ncopy = 4;
+  k_merge_prepare<<<dim3((unsigned)cdiv(wsz, 256), 4u), 256, 0, s>>>(a);
+  MTGNN_CHECK_LAUNCH("link_prepare");
+  const int64_t max_tar = max_q / 3;
+  const int64_t nblk = cdiv(max_tar < 1 ? 1 : max_tar, 16);
+  if (max_tar > 0) {
+    TimedScope ts("link_fused", s);
+    if (na == 7)
+      k_link_fused<7><<<(unsigned)nblk, 64 * MW, 0, s>>>(z, n_q, max_tar, da, Wp, b1, W2, b2, DA, DB, dz, scores,
+                                                          part);
+    else
+      k_link_fused<2><<<(unsigned)nblk, 64 * MW, 0, s>>>(z, n_q, max_tar, da, Wp, b1, W2, b2, DA, DB, dz, scores,
+                                                          part);
+    MTGNN_CHECK_LAUNCH("link_fused");
+  }
+  // blocks past the device's target count wrote no partial: sum only those below it
+  k_link_reduce_dev<<<(unsigned)cdiv(da + 2, 4), 256, 0, s>>>(part, n_q, max_tar, da, dW2, db2, loss);
+  MTGNN_CHECK_LAUNCH("link_reduce");
   return MTGNN_OK;
 }
 

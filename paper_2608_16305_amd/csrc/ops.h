@@ -58,6 +58,14 @@ mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const in
                            bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
 
 // link-prediction decoder and the masked batch loss
+// The fused form (merge.hip) for d_attn = 100 or 32: one kernel per 16 target events for the forward, the
+// loss terms and dz, and the hidden-row gradients DA / DB for the first layer's weight gradient; then the
+// column sums of the per-block partials into dW_d2, db_d2 and the loss.  Wp: link_fused_weight_floats.
+bool link_fused_ok(int da);
+size_t link_fused_weight_floats(int da);
+mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
+                        const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
+                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s);
 size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q);
 mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* p,
                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
