@@ -17,4 +17,6 @@ steps in the paper's order.  Module map:
 * ``sequential`` -- the literal per-event reading of Eq. 1-2 (one event at a
                     time), used to pin the batched memory phase.
 * ``bf16``       -- round-to-nearest-even conversion to bfloat16.
+* ``depscan``    -- the offline backward dependency scan and mixed-batch
+                    construction of Algorithm 1.
 """

@@ -820,3 +820,85 @@ def test_relu_flips_only_change_the_chosen_decisions():
     bb = tgn.step(p64, w, mem0, lu0, pz, adj, s.x, prev, cur, None, loss="link", flips=fl)
     assert a.link.loss == bb.link.loss
     assert not np.array_equal(a.grads["W_d1"], bb.grads["W_d1"])
+
+
+# --------------------------------------------------------------------------- Algorithm 1 (dependency scan)
+
+def test_dependency_scan_example_chain():
+    """The paper's worked dependency (Example 2, Section III-C) through Algorithm 1: worker p owns
+    node 4, the source of e8 = (4, 3); node 3 and every other node are remote.  With the events in two
+    batches (e1..e4, e5..e8) the auxiliary replay events are exactly the events node 3's state depends
+    on (e7, e6, e3, e1), and the refresh set holds node 3 and their remote endpoints."""
+    from oracle import depscan
+    with open(os.path.join(GOLDEN, "example2_dependency.json")) as f:
+        ex = json.load(f)
+    ev = ex["events"]
+    src = np.array([e[0] for e in ev])
+    dst = np.array([e[1] for e in ev])
+    owner = np.ones(16, np.int64)
+    owner[4] = 0
+    tar, aux, F = depscan.backward_scan(src, dst, owner, 0, [[0, 1, 2, 3], [4, 5, 6, 7]])
+    assert sorted(e + 1 for s in tar for e in s) == [ex["target_event"]]
+    assert sorted(e + 1 for s in aux for e in s) == sorted(ex["must_depend_on"])
+    assert F == {3, 11, 10, 2, 1}
+
+
+def _scan_fixed_point(src, dst, owner, p, batches):
+    """Algorithm 1's result as the least fixed point of its membership rule, by repeated sweeps over
+    all events: an event whose source is remote is auxiliary iff an endpoint is in the frontier before
+    it, i.e. among the remote destinations of the targets of its batch or of later batches, or the
+    remote endpoints of the auxiliary events visited before it (later batches, or later in its batch)."""
+    order = [(s, e) for s in reversed(range(len(batches))) for e in reversed(batches[s])]
+    pos = {e: i for i, (_, e) in enumerate(order)}
+    batch_of = {e: s for s, b in enumerate(batches) for e in b}
+    aux = set()
+    changed = True
+    while changed:
+        changed = False
+        for s, e in order:
+            if owner[src[e]] == p or e in aux:
+                continue
+            front = {int(dst[x]) for b in batches[s:] for x in b if owner[src[x]] == p and owner[dst[x]] != p}
+            for a in aux:
+                if pos[a] < pos[e]:
+                    front |= {int(i) for i in (src[a], dst[a]) if owner[i] != p}
+            if int(src[e]) in front or int(dst[e]) in front:
+                aux.add(e)
+                changed = True
+    return aux, batch_of
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_dependency_scan_equals_fixed_point_of_its_rule(seed):
+    from oracle import depscan
+    rng = np.random.default_rng(seed)
+    N, E, P = 14, 60, 3
+    src = rng.integers(0, N, E)
+    dst = rng.integers(0, N, E)
+    owner = rng.integers(0, P, N)
+    batches = [list(range(b, min(E, b + 12))) for b in range(0, E, 12)]
+    for p in range(P):
+        tar, aux, F = depscan.backward_scan(src, dst, owner, p, batches)
+        fp, _ = _scan_fixed_point(src, dst, owner, p, batches)
+        assert {e for s in aux for e in s} == fp
+        assert all(owner[src[e]] == p for s in tar for e in s)
+        # the refresh set: remote nodes only, and every remote endpoint of an auxiliary event
+        assert all(owner[x] != p for x in F)
+        assert all(x in F for s in aux for e in s for x in (src[e], dst[e]) if owner[x] != p)
+
+
+def test_mixed_batches_sorted_and_masked():
+    from oracle import depscan
+    rng = np.random.default_rng(7)
+    N, E = 20, 200
+    src, dst = rng.integers(0, N, E), rng.integers(0, N, E)
+    t = np.sort(rng.random(E) * 10).astype(np.float32)
+    owner = rng.integers(0, 4, N)
+    role, sync = depscan.scan_stream(src, dst, t, owner, 4, 25, 3)
+    # every event is a target of exactly the worker owning its source
+    assert np.array_equal((role == 1).argmax(0), owner[src]) and np.all((role == 1).sum(0) == 1)
+    for p in range(4):
+        ids = np.nonzero(role[p])[0]
+        mixed, is_aux = depscan.mixed_batch(t, list(ids[role[p, ids] == 1]), list(ids[role[p, ids] == 2]))
+        assert mixed == sorted(ids.tolist())          # the stream order is already sort_t
+        assert is_aux == (role[p, mixed] == 2).tolist()
