@@ -122,7 +122,8 @@ typedef enum {
   MTGNN_OP_GRU_UPDATE_BWD = 7,
   MTGNN_OP_BUILD_MESSAGES_BWD = 8,
   MTGNN_OP_BUILD_CSR = 9,
-  MTGNN_OP_LINK_LOSS = 10
+  MTGNN_OP_LINK_LOSS = 10,
+  MTGNN_OP_MIXED_BATCHES = 11
 } mtgnn_op;
 
 /* Workspace bytes for `op`.  max_rows is the batch size n for BUILD_QUERIES and
@@ -407,6 +408,35 @@ mtgnn_status mtgnn_build_messages_bwd_noalloc(const float* dmsg_time, const floa
                                               int64_t max_rows, const float* time_w, const float* time_b,
                                               const mtgnn_dims* dims, float* d_time_w, float* d_time_b,
                                               hipStream_t stream);
+
+/* Offline backward dependency scan and mixed-batch construction (Algorithm 1, Section IV-B), for
+ * every worker p < n_workers and every synchronization window (Definition 1: `window` consecutive
+ * batches of `batch` events; the last batch and window may be short).  For each (p, window) the
+ * window's batches are scanned latest first: the batch's target events of p (source owned by p,
+ * owner[src] == p) are kept and their remote destinations join the frontier F; then every event of
+ * the batch whose source is remote and that touches F, visited latest first, becomes an auxiliary
+ * replay event of p, and its remote endpoints join F.  Writes
+ *   role      -- [n_workers, n_events] uint8: 0 = not in p's mixed batches, 1 = target of p,
+ *                2 = auxiliary replay event of p;
+ *   sync_bits -- [n_workers, n_windows, ceil(n_nodes / 32)] uint32: F at the end of each scan, the
+ *                candidate boundary refresh set N_sync (bit n % 32 of word n / 32).
+ * src, dst [n_events] int32 and owner [n_nodes] int32 (the node ownership map pi) are device arrays.
+ * The result is the sequential algorithm's, bit for bit (no ordering freedom).  Errors: EINVAL. */
+mtgnn_status mtgnn_dependency_scan(const int32_t* src, const int32_t* dst, int64_t n_events, const int32_t* owner,
+                                   int64_t n_nodes, int32_t n_workers, int64_t batch, int32_t window, uint8_t* role,
+                                   uint32_t* sync_bits, hipStream_t stream);
+
+/* One worker's mixed batches (Eq. 5) from its roles: the events with role != 0 in stream order
+ * (sort_t, as the stream is sorted by time), with the event-type mask.
+ *   role      -- [n_events] uint8 (one worker's row of mtgnn_dependency_scan's output);
+ *   eid_out   -- [n_events] int32 out: the event ids, batch after batch;
+ *   flags_out -- [n_events] uint8 out: bit 0 set for auxiliary replay events (the mtgnn_batch flags);
+ *   batch_off -- [ceil(n_events / batch) + 1] int32 out: batch s of the worker is entries
+ *                batch_off[s] .. batch_off[s + 1] - 1; the last entry is the total.
+ * Workspace: mtgnn_workspace_bytes(MTGNN_OP_MIXED_BATCHES, NULL, n_events, 0). */
+mtgnn_status mtgnn_mixed_batches(const uint8_t* role, int64_t n_events, int64_t batch, int32_t* eid_out,
+                                 uint8_t* flags_out, int32_t* batch_off, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
 
 /* Temporal adjacency of a whole stream (built once, offline; outside the step).
  * Event e = (src[e], dst[e], t[e]) with eid e gives two entries: (node src,

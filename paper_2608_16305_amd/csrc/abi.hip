@@ -176,6 +176,7 @@ size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int6
     case MTGNN_OP_AGGREGATE_LAST: return aggregate_last_ws(max_rows, d ? d->n_nodes : 0);
     case MTGNN_OP_BUILD_MESSAGES: return 0;
     case MTGNN_OP_SAMPLE_RECENT: return 0;
+    case MTGNN_OP_MIXED_BATCHES: return mixed_batches_ws(max_rows);
     case MTGNN_OP_BUILD_CSR: return build_csr_ws(max_rows, d ? d->n_nodes : 0);
     default: break;
   }
@@ -566,6 +567,40 @@ mtgnn_status mtgnn_build_messages_bwd_noalloc(const float* dmsg_time, const floa
   MTGNN_TRY(scratch_on_current_device(&ws));
   return build_messages_bwd_impl(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d, d_time_w, d_time_b, ws,
                                  (size_t)MTGNN_NOALLOC_SCRATCH_BYTES, stream);
+}
+
+mtgnn_status mtgnn_dependency_scan(const int32_t* src, const int32_t* dst, int64_t n_events, const int32_t* owner,
+                                   int64_t n_nodes, int32_t n_workers, int64_t batch, int32_t window, uint8_t* role,
+                                   uint32_t* sync_bits, hipStream_t stream) {
+  if (n_events < 0 || n_events >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "n_events");
+  if (n_nodes <= 0 || n_nodes >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "n_nodes");
+  if (n_workers <= 0 || n_workers > 4096) return fail(MTGNN_EINVAL, "n_workers");
+  if (batch <= 0 || window <= 0) return fail(MTGNN_EINVAL, "batch / window");
+  if (n_events == 0) return MTGNN_OK;
+  if ((int64_t)n_workers * cdiv(cdiv(n_events, batch), window) >= (int64_t(1) << 31))
+    return fail(MTGNN_EINVAL, "too many (worker, window) scans");
+  REQ(src, "src");
+  REQ(dst, "dst");
+  REQ(owner, "owner");
+  REQ(role, "role");
+  REQ(sync_bits, "sync_bits");
+  return dep_scan_impl(src, dst, n_events, owner, n_nodes, n_workers, batch, window, role, sync_bits, stream);
+}
+
+mtgnn_status mtgnn_mixed_batches(const uint8_t* role, int64_t n_events, int64_t batch, int32_t* eid_out,
+                                 uint8_t* flags_out, int32_t* batch_off, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  if (n_events < 0 || n_events >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "n_events");
+  if (batch <= 0) return fail(MTGNN_EINVAL, "batch");
+  REQ(batch_off, "batch_off");
+  if (n_events > 0) {
+    REQ(role, "role");
+    REQ(eid_out, "eid_out");
+    REQ(flags_out, "flags_out");
+    REQ(ws, "ws");
+  }
+  if (ws_bytes < mixed_batches_ws(n_events)) return fail(MTGNN_EWORKSPACE, "mixed_batches ws");
+  return mixed_batches_impl(role, n_events, batch, eid_out, flags_out, batch_off, ws, ws_bytes, stream);
 }
 
 mtgnn_status mtgnn_build_temporal_csr(const int32_t* src, const int32_t* dst, const float* t, int64_t n_events,

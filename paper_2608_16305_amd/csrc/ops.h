@@ -71,6 +71,13 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
                             size_t ws_bytes, hipStream_t s);
 
+// offline dependency scan (Algorithm 1) and the mixed batches of one worker
+mtgnn_status dep_scan_impl(const int32_t* src, const int32_t* dst, int64_t E, const int32_t* owner, int64_t n_nodes,
+                           int n_workers, int64_t batch, int window, uint8_t* role, uint32_t* sync, hipStream_t s);
+size_t mixed_batches_ws(int64_t E);
+mtgnn_status mixed_batches_impl(const uint8_t* role, int64_t E, int64_t batch, int32_t* eid_out, uint8_t* flags_out,
+                                int32_t* batch_off, void* ws, size_t ws_bytes, hipStream_t s);
+
 // sampling / adjacency
 mtgnn_status sample_recent_impl(const int64_t* off, const int32_t* nbr, const float* t, const int32_t* eid,
                                 const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q, int k,

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmtgnn.so
 F32, BF16 = 0, 1
 OP_BUILD_QUERIES, OP_AGGREGATE_LAST, OP_BUILD_MESSAGES, OP_GRU_UPDATE, OP_SAMPLE_RECENT = 0, 1, 2, 3, 4
 OP_TEMPORAL_ATTN, OP_TEMPORAL_ATTN_BWD, OP_GRU_UPDATE_BWD, OP_BUILD_MESSAGES_BWD, OP_BUILD_CSR = 5, 6, 7, 8, 9
-OP_LINK_LOSS = 10
+OP_LINK_LOSS, OP_MIXED_BATCHES = 10, 11
 
 ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
@@ -26,7 +26,8 @@ ENTRY_POINTS = (
     "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap", "mtgnn_temporal_attn_bwd_group",
     "mtgnn_temporal_attn_bwd_grouped",
     "mtgnn_gru_update_bwd", "mtgnn_link_loss",
-    "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
+    "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr",
+    "mtgnn_dependency_scan", "mtgnn_mixed_batches", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
 )
 
@@ -100,6 +101,8 @@ _SIGS = {
     "mtgnn_build_messages_bwd": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _SZ, _P],
     "mtgnn_build_messages_bwd_noalloc": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_dependency_scan": [_P, _P, _I64, _P, _I64, _I32, _I64, _I32, _P, _P, _P],
+    "mtgnn_mixed_batches": [_P, _I64, _I64, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_workspace_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
     "mtgnn_save_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
     "mtgnn_status_string": [C.c_int],
@@ -454,6 +457,22 @@ def mtgnn_build_temporal_csr(src, dst, t, n_nodes, csr_off, csr_nbr, csr_t, csr_
                                           _ptr(csr_off, torch.int64, "csr_off"), _ptr(csr_nbr, torch.int32, "csr_nbr"),
                                           _ptr(csr_t, torch.float32, "csr_t"), _ptr(csr_eid, torch.int32, "csr_eid"),
                                           wp, wb, _stream(stream)), "mtgnn_build_temporal_csr")
+
+
+def mtgnn_dependency_scan(src, dst, owner, n_workers, batch, window, role, sync_bits, stream=None):
+    _check(lib().mtgnn_dependency_scan(_ptr(src, torch.int32, "src"), _ptr(dst, torch.int32, "dst"), int(src.numel()),
+                                       _ptr(owner, torch.int32, "owner"), int(owner.numel()), int(n_workers),
+                                       int(batch), int(window), _ptr(role, torch.uint8, "role"),
+                                       _ptr(sync_bits, torch.int32, "sync_bits"), _stream(stream)),
+           "mtgnn_dependency_scan")
+
+
+def mtgnn_mixed_batches(role, batch, eid_out, flags_out, batch_off, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_mixed_batches(_ptr(role, torch.uint8, "role"), int(role.numel()), int(batch),
+                                     _ptr(eid_out, torch.int32, "eid_out"), _ptr(flags_out, torch.uint8, "flags_out"),
+                                     _ptr(batch_off, torch.int32, "batch_off"), wp, wb, _stream(stream)),
+           "mtgnn_mixed_batches")
 
 
 def timer_start(kernel: str, max_launches: int):

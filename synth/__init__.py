@@ -14,4 +14,5 @@ from .streams import (  # noqa: F401
     window_state,
     loss_noise,
     batch_slice,
+    node_owner,
 )

@@ -17,7 +17,7 @@ from .configs import Workload
 CHUNK = 10_000_000  # events per generation chunk
 
 # seed "parts"
-_SRC, _DST, _T, _X, _NEG, _FLAGS, _PERM, _PARAMS, _M0, _G, _BIAS = range(11)
+_SRC, _DST, _T, _X, _NEG, _FLAGS, _PERM, _PARAMS, _M0, _G, _BIAS, _OWNER = range(12)
 
 FLAG_REPLAY = 1   # bit 0: event replayed from the temporal-event cache (auxiliary)
 FLAG_PRUNED = 2   # bit 1: replay event removed by load-aware pruning
@@ -249,3 +249,8 @@ def last_event_time(src, dst, t, n_nodes: int) -> np.ndarray:
 def loss_noise(w: Workload, step: int, n_rows: int, base_seed: int = 0) -> np.ndarray:
     """Seeded N(0,1) noise G [n_rows, d_attn] (float32) for one step's loss gradient."""
     return _rng(base_seed, w.cid, _G, step).standard_normal((n_rows, w.d_attn), dtype=np.float32)
+
+
+def node_owner(n_nodes: int, n_workers: int, base_seed: int = 0, cid: int = 0) -> np.ndarray:
+    """A node ownership map pi for n_workers workers: each node's owner drawn uniformly (int32 [n_nodes])."""
+    return _rng(base_seed, cid, _OWNER).integers(0, n_workers, n_nodes).astype(np.int32)
