@@ -902,3 +902,57 @@ def test_mixed_batches_sorted_and_masked():
         mixed, is_aux = depscan.mixed_batch(t, list(ids[role[p, ids] == 1]), list(ids[role[p, ids] == 2]))
         assert mixed == sorted(ids.tolist())          # the stream order is already sort_t
         assert is_aux == (role[p, mixed] == 2).tolist()
+
+
+# --------------------------------------------------------------------------- runtime controller (Section V, Alg. 2)
+
+def test_controller_equations_by_hand():
+    from oracle import controller as C
+    # Eq. 6 / 8: the first value initialises the average
+    assert C.ema(0.0, 3.0, 0.2) == 3.0
+    assert abs(C.ema(3.0, 1.0, 0.25) - (0.25 * 1.0 + 0.75 * 3.0)) < 1e-15
+    # Eq. 7: skip only when r > 0, the EMA is positive and the last norm is below tau_g times it
+    assert C.sync_decision(0, 0.1, 1.0, 0.9) == 1
+    assert C.sync_decision(5, 0.1, 0.0, 0.9) == 1
+    assert C.sync_decision(5, 0.8, 1.0, 0.9) == 0
+    assert C.sync_decision(5, 0.9, 1.0, 0.9) == 1      # not strictly below
+    # Eq. 9: heavy when the last time exceeds tau_c times the EMA
+    assert C.heavy_load(0, 9.0, 1.0, 1.5) == 0
+    assert C.heavy_load(3, 1.6, 1.0, 1.5) == 1
+    assert C.heavy_load(3, 1.5, 1.0, 1.5) == 0
+    assert C.heavy_load(3, 1.6, 0.0, 1.5) == 0
+    # a worked sequence: norms 2, 1, 4; alpha 0.5 -> EMAs 2, 1.5, 2.75
+    c = C.Controller(alpha=0.5, beta=0.5, tau_g=0.9, tau_c=1.2, interval=2)
+    seq = []
+    for r, (g, t) in enumerate([(2.0, 10.0), (1.0, 10.0), (4.0, 20.0), (1.0, 10.0)]):
+        seq.append((c.boundary(r), c.sync(r), c.heavy(r)))
+        c.observe(g, t)
+    assert seq == [(True, 1, 0), (False, 1, 0), (True, 0, 0), (False, 1, 1)]
+    assert c.g_bar == 0.5 * 1.0 + 0.5 * 2.75 and c.c_bar == 0.5 * 10 + 0.5 * 15
+
+
+def test_prune_aux_keeps_targets_and_refresh_copies_rows():
+    from oracle import controller as C
+    f = np.array([0, 1, 0, 3, 1, 2], np.uint8)
+    assert C.prune_aux(f, 1).tolist() == [0, 3, 0, 3, 3, 0]
+    assert C.prune_aux(f, 0).tolist() == [0, 1, 0, 1, 1, 0]
+    cm, cl = np.zeros((5, 2)), np.zeros(5)
+    am, al = np.arange(10.0).reshape(5, 2), np.arange(5.0) + 0.5
+    m, l = C.cache_refresh(cm, cl, am, al, {1, 4})
+    assert m.tolist() == [[0, 0], [2, 3], [0, 0], [0, 0], [8, 9]] and l.tolist() == [0, 1.5, 0, 0, 4.5]
+
+
+def test_adam_matches_torch_adam():
+    from oracle import controller as C
+    rng = np.random.default_rng(0)
+    th = rng.standard_normal(7)
+    p = torch.tensor(th.copy(), requires_grad=True)
+    opt = torch.optim.Adam([p], lr=1e-2, betas=(0.9, 0.999), eps=1e-8)
+    m = v = np.zeros(7)
+    for t in range(1, 5):
+        g = rng.standard_normal(7)
+        p.grad = torch.tensor(g)
+        opt.step()
+        th, m, v = C.adam(th, g, m, v, t, 1e-2, 0.9, 0.999, 1e-8)
+        assert np.allclose(th, p.detach().numpy(), rtol=0, atol=1e-14)
+    assert abs(C.grad_norm([np.array([3.0]), np.array([[4.0, 12.0]])]) - 13.0) < 1e-15
