@@ -438,6 +438,72 @@ mtgnn_status mtgnn_mixed_batches(const uint8_t* role, int64_t n_events, int64_t 
                                  uint8_t* flags_out, int32_t* batch_off, void* ws, size_t ws_bytes,
                                  hipStream_t stream);
 
+/* ------------------------------------------------------------------ adaptive runtime controller
+ * The decisions of one worker's runtime controller (Section V, Algorithm 2), kept on the host:
+ *   gradient-norm EMA (Eq. 6):   g_bar = g_r if g_bar was 0, else alpha g_r + (1 - alpha) g_bar;
+ *   boundary decision (Eq. 7):   at a candidate refresh boundary r (r % interval == 0, Definition 1),
+ *                                S_r = 0 (skip the refresh) iff r > 0, g_bar > 0 and g_{r-1} < tau_g g_bar;
+ *   batch-time EMA (Eq. 8):      c_bar = c_r if c_bar was 0, else beta c_r + (1 - beta) c_bar;
+ *   heavy load (Eq. 9):          H_r = 1 iff r > 0, c_bar > 0 and c_{r-1} > tau_c c_bar.
+ * The paper fixes no values for alpha, beta, tau_g, tau_c; the caller chooses them. */
+typedef struct {
+  double alpha, beta;   /* EMA factors of the gradient norm and the batch time, in (0, 1] */
+  double tau_g, tau_c;  /* thresholds, > 0 */
+  int32_t interval;     /* K, the synchronization interval in batches, > 0 */
+} mtgnn_controller_config;
+
+typedef struct mtgnn_controller mtgnn_controller;   /* opaque, host memory */
+
+/* Creates a controller in its initial state (every average and last value 0).  EINVAL on a NULL
+ * argument or a value out of range.  Host-only; no HIP call. */
+mtgnn_status mtgnn_controller_create(const mtgnn_controller_config* cfg, mtgnn_controller** out);
+void mtgnn_controller_destroy(mtgnn_controller* c);
+/* Before batch r: whether r is a candidate refresh boundary, the boundary decision S_r (0 when r is no
+ * boundary) and the heavy-load mode H_r, from the state the previous observe left.  Any of the outputs
+ * may be NULL. */
+mtgnn_status mtgnn_controller_decide(const mtgnn_controller* c, int64_t r, int32_t* boundary, int32_t* sync,
+                                     int32_t* heavy);
+/* After batch r: its gradient norm g_r and batch time c_r (finite, >= 0; EINVAL otherwise) update the
+ * averages and the last values. */
+mtgnn_status mtgnn_controller_observe(mtgnn_controller* c, double grad_norm, double batch_time);
+mtgnn_status mtgnn_controller_state(const mtgnn_controller* c, double* g_bar, double* g_last, double* c_bar,
+                                    double* c_prev);
+
+/* The gradient norm g_r of Eq. 6: sqrt of the sum of squares of every element of the n (<= 32) float32
+ * tensors grads[i] (device pointers, host array) of sizes[i] (host array) elements, summed in double
+ * precision in a fixed order (deterministic).  norm: a device double.  Workspace:
+ * 8 * sum_i ceil(sizes[i] / 4096) bytes, rounded up to 256 (mtgnn_grad_norm_ws_bytes). */
+size_t mtgnn_grad_norm_ws_bytes(const int64_t* sizes, int32_t n);
+mtgnn_status mtgnn_grad_norm(const float* const* grads, const int64_t* sizes, int32_t n, double* norm, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+
+/* PruneAux (Eq. 10-11) of a mixed batch's event-type masks (mtgnn_batch flags, device, n entries): with
+ * heavy != 0, every auxiliary replay event (bit 0: its source is not owned by the worker, the eligible
+ * set of Eq. 10) gets bit 1 (pruned): the step then gives it no message, query or loss, as if removed;
+ * target events are never touched.  With heavy == 0 bit 1 is cleared, restoring the mixed batch. */
+mtgnn_status mtgnn_prune_aux(uint8_t* flags, int64_t n, int32_t heavy, hipStream_t stream);
+
+/* Boundary cache refresh (Eq. 25): for every node n whose bit is set in sync_bits (bit n % 32 of word
+ * n / 32, as mtgnn_dependency_scan writes the refresh set N_sync), memory row n and last_update[n] take
+ * the authoritative table's values.  Other rows are not touched.  Tables: [n_nodes, d_mem] in the dims'
+ * dtype and [n_nodes] float32, device. */
+mtgnn_status mtgnn_cache_refresh(const uint32_t* sync_bits, int64_t n_nodes, const void* auth_memory,
+                                 const float* auth_last_update, const mtgnn_dims* dims, void* memory,
+                                 float* last_update, hipStream_t stream);
+
+/* The parameter update of Algorithm 2: one Adam step (bias-corrected, step count t >= 1) over n (<= 32)
+ * float32 parameter tensors in place, with their float32 moment buffers m, v; shadow (NULL, or per
+ * tensor NULL or a bfloat16 buffer) receives the round-to-nearest-even bf16 copy of the updated
+ * parameter (the storage weights of a bf16 run).  All tensor pointers are device pointers in host
+ * arrays. */
+typedef struct {
+  double lr, beta1, beta2, eps;   /* the update's coefficients are formed in double, then used in float32 */
+  int32_t t;
+} mtgnn_adam_config;
+mtgnn_status mtgnn_adam_step(float* const* params, const float* const* grads, float* const* m, float* const* v,
+                             void* const* shadow, const int64_t* sizes, int32_t n, const mtgnn_adam_config* cfg,
+                             hipStream_t stream);
+
 /* Temporal adjacency of a whole stream (built once, offline; outside the step).
  * Event e = (src[e], dst[e], t[e]) with eid e gives two entries: (node src,
  * nbr dst, role 0) and (node dst, nbr src, role 1).  Entries are grouped by

@@ -603,6 +603,63 @@ mtgnn_status mtgnn_mixed_batches(const uint8_t* role, int64_t n_events, int64_t 
   return mixed_batches_impl(role, n_events, batch, eid_out, flags_out, batch_off, ws, ws_bytes, stream);
 }
 
+static mtgnn_status check_tensor_list(const void* const* ptrs, const int64_t* sizes, int32_t n) {
+  if (!ptrs || !sizes) return fail(MTGNN_EINVAL, "tensor list is NULL");
+  if (n <= 0 || n > RT_MAX_TENSORS) return fail(MTGNN_EINVAL, "tensor count not in 1..32");
+  for (int i = 0; i < n; ++i) {
+    if (!ptrs[i]) return fail(MTGNN_EINVAL, "tensor pointer is NULL");
+    if (sizes[i] <= 0 || sizes[i] >= (int64_t(1) << 40)) return fail(MTGNN_EINVAL, "tensor size");
+  }
+  return MTGNN_OK;
+}
+
+size_t mtgnn_grad_norm_ws_bytes(const int64_t* sizes, int32_t n) {
+  if (!sizes || n <= 0 || n > RT_MAX_TENSORS) return 0;
+  return grad_norm_ws(sizes, n);
+}
+
+mtgnn_status mtgnn_grad_norm(const float* const* grads, const int64_t* sizes, int32_t n, double* norm, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_tensor_list((const void* const*)grads, sizes, n));
+  REQ(norm, "norm");
+  REQ(ws, "ws");
+  if (ws_bytes < grad_norm_ws(sizes, n)) return fail(MTGNN_EWORKSPACE, "grad_norm ws");
+  return grad_norm_impl(grads, sizes, n, norm, ws, stream);
+}
+
+mtgnn_status mtgnn_prune_aux(uint8_t* flags, int64_t n, int32_t heavy, hipStream_t stream) {
+  if (n < 0) return fail(MTGNN_EINVAL, "n");
+  if (n > 0) REQ(flags, "flags");
+  return prune_aux_impl(flags, n, heavy, stream);
+}
+
+mtgnn_status mtgnn_cache_refresh(const uint32_t* sync_bits, int64_t n_nodes, const void* auth_memory,
+                                 const float* auth_last_update, const mtgnn_dims* d, void* memory,
+                                 float* last_update, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  if (n_nodes <= 0 || n_nodes > d->n_nodes) return fail(MTGNN_EINVAL, "n_nodes");
+  REQ(sync_bits, "sync_bits");
+  REQ(auth_memory, "auth_memory");
+  REQ(auth_last_update, "auth_last_update");
+  REQ(memory, "memory");
+  REQ(last_update, "last_update");
+  return cache_refresh_impl(sync_bits, n_nodes, auth_memory, auth_last_update, d, memory, last_update, stream);
+}
+
+mtgnn_status mtgnn_adam_step(float* const* params, const float* const* grads, float* const* m, float* const* v,
+                             void* const* shadow, const int64_t* sizes, int32_t n, const mtgnn_adam_config* cfg,
+                             hipStream_t stream) {
+  MTGNN_TRY(check_tensor_list((const void* const*)params, sizes, n));
+  MTGNN_TRY(check_tensor_list((const void* const*)grads, sizes, n));
+  MTGNN_TRY(check_tensor_list((const void* const*)m, sizes, n));
+  MTGNN_TRY(check_tensor_list((const void* const*)v, sizes, n));
+  REQ(cfg, "cfg");
+  if (cfg->t < 1 || !(cfg->lr >= 0) || !(cfg->beta1 >= 0 && cfg->beta1 < 1) || !(cfg->beta2 >= 0 && cfg->beta2 < 1) ||
+      !(cfg->eps > 0))
+    return fail(MTGNN_EINVAL, "adam config");
+  return adam_impl(params, grads, m, v, shadow, sizes, n, cfg, stream);
+}
+
 mtgnn_status mtgnn_build_temporal_csr(const int32_t* src, const int32_t* dst, const float* t, int64_t n_events,
                                       int64_t n_nodes, int64_t* csr_off, int32_t* csr_nbr, float* csr_t,
                                       int32_t* csr_eid, void* ws, size_t ws_bytes, hipStream_t stream) {

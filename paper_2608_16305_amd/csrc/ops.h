@@ -78,6 +78,17 @@ size_t mixed_batches_ws(int64_t E);
 mtgnn_status mixed_batches_impl(const uint8_t* role, int64_t E, int64_t batch, int32_t* eid_out, uint8_t* flags_out,
                                 int32_t* batch_off, void* ws, size_t ws_bytes, hipStream_t s);
 
+// runtime controller's device work (runtime.hip)
+constexpr int RT_MAX_TENSORS = 32;
+size_t grad_norm_ws(const int64_t* sizes, int n);
+mtgnn_status grad_norm_impl(const float* const* grads, const int64_t* sizes, int n, double* norm, void* ws,
+                            hipStream_t s);
+mtgnn_status prune_aux_impl(uint8_t* flags, int64_t n, int heavy, hipStream_t s);
+mtgnn_status cache_refresh_impl(const uint32_t* bits, int64_t n_nodes, const void* auth_mem, const float* auth_lu,
+                                const mtgnn_dims* d, void* mem, float* lu, hipStream_t s);
+mtgnn_status adam_impl(float* const* params, const float* const* grads, float* const* m, float* const* v,
+                       void* const* shadow, const int64_t* sizes, int n, const mtgnn_adam_config* c, hipStream_t s);
+
 // sampling / adjacency
 mtgnn_status sample_recent_impl(const int64_t* off, const int32_t* nbr, const float* t, const int32_t* eid,
                                 const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q, int k,

@@ -27,7 +27,9 @@ ENTRY_POINTS = (
     "mtgnn_temporal_attn_bwd_grouped",
     "mtgnn_gru_update_bwd", "mtgnn_link_loss",
     "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr",
-    "mtgnn_dependency_scan", "mtgnn_mixed_batches", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
+    "mtgnn_dependency_scan", "mtgnn_mixed_batches", "mtgnn_controller_create", "mtgnn_controller_destroy",
+    "mtgnn_controller_decide", "mtgnn_controller_observe", "mtgnn_controller_state", "mtgnn_grad_norm_ws_bytes",
+    "mtgnn_grad_norm", "mtgnn_prune_aux", "mtgnn_cache_refresh", "mtgnn_adam_step", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
 )
 
@@ -58,6 +60,16 @@ class AttnGrads(C.Structure):
 
 
 _LINK = ("W_d1", "b_d1", "W_d2", "b_d2")
+
+
+class ControllerConfig(C.Structure):
+    _fields_ = [("alpha", C.c_double), ("beta", C.c_double), ("tau_g", C.c_double), ("tau_c", C.c_double),
+                ("interval", C.c_int32)]
+
+
+class AdamConfig(C.Structure):
+    _fields_ = [("lr", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
+                ("t", C.c_int32)]
 
 
 class LinkParams(C.Structure):
@@ -102,6 +114,16 @@ _SIGS = {
     "mtgnn_build_messages_bwd_noalloc": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_dependency_scan": [_P, _P, _I64, _P, _I64, _I32, _I64, _I32, _P, _P, _P],
+    "mtgnn_controller_create": [C.POINTER(ControllerConfig), C.POINTER(C.c_void_p)],
+    "mtgnn_controller_destroy": [_P],
+    "mtgnn_controller_decide": [_P, _I64, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32)],
+    "mtgnn_controller_observe": [_P, C.c_double, C.c_double],
+    "mtgnn_controller_state": [_P] + [C.POINTER(C.c_double)] * 4,
+    "mtgnn_grad_norm_ws_bytes": [C.POINTER(C.c_int64), _I32],
+    "mtgnn_grad_norm": [C.POINTER(C.c_void_p), C.POINTER(C.c_int64), _I32, _P, _P, _SZ, _P],
+    "mtgnn_prune_aux": [_P, _I64, _I32, _P],
+    "mtgnn_cache_refresh": [_P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
+    "mtgnn_adam_step": [C.POINTER(C.c_void_p)] * 5 + [C.POINTER(C.c_int64), _I32, C.POINTER(AdamConfig), _P],
     "mtgnn_mixed_batches": [_P, _I64, _I64, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_workspace_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
     "mtgnn_save_bytes": [C.c_int, C.POINTER(Dims), _I64, _I64],
@@ -111,7 +133,8 @@ _SIGS = {
     "mtgnn_timer_start": [C.c_char_p, C.c_int],
     "mtgnn_timer_stop": [C.POINTER(C.c_double), C.POINTER(C.c_int)],
 }
-_RES = {"mtgnn_workspace_bytes": _SZ, "mtgnn_save_bytes": _SZ, "mtgnn_status_string": C.c_char_p,
+_RES = {"mtgnn_workspace_bytes": _SZ, "mtgnn_save_bytes": _SZ, "mtgnn_grad_norm_ws_bytes": _SZ,
+        "mtgnn_controller_destroy": None, "mtgnn_status_string": C.c_char_p,
         "mtgnn_last_error": C.c_char_p, "mtgnn_version": C.c_int}
 
 _lib = None
@@ -473,6 +496,85 @@ def mtgnn_mixed_batches(role, batch, eid_out, flags_out, batch_off, ws, stream=N
                                      _ptr(eid_out, torch.int32, "eid_out"), _ptr(flags_out, torch.uint8, "flags_out"),
                                      _ptr(batch_off, torch.int32, "batch_off"), wp, wb, _stream(stream)),
            "mtgnn_mixed_batches")
+
+
+class Controller:
+    """The library's host-side runtime controller (Eq. 6-9): decisions before a batch, observations after."""
+
+    def __init__(self, alpha, beta, tau_g, tau_c, interval):
+        h = C.c_void_p()
+        _check(lib().mtgnn_controller_create(C.byref(ControllerConfig(alpha, beta, tau_g, tau_c, int(interval))),
+                                             C.byref(h)), "mtgnn_controller_create")
+        self._h = h
+
+    def decide(self, r):
+        """(boundary, S_r, H_r) before batch r."""
+        b, sy, hv = C.c_int32(), C.c_int32(), C.c_int32()
+        _check(lib().mtgnn_controller_decide(self._h, int(r), C.byref(b), C.byref(sy), C.byref(hv)),
+               "mtgnn_controller_decide")
+        return b.value, sy.value, hv.value
+
+    def observe(self, grad_norm, batch_time):
+        _check(lib().mtgnn_controller_observe(self._h, float(grad_norm), float(batch_time)),
+               "mtgnn_controller_observe")
+
+    def state(self):
+        v = [C.c_double() for _ in range(4)]
+        _check(lib().mtgnn_controller_state(self._h, *[C.byref(x) for x in v]), "mtgnn_controller_state")
+        return tuple(x.value for x in v)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.mtgnn_controller_destroy(h)
+            self._h = None
+
+
+def _ptr_array(ts, dtype, name):
+    arr = (C.c_void_p * len(ts))()
+    for i, t in enumerate(ts):
+        arr[i] = _ptr(t, dtype, name).value
+    return arr
+
+
+def _sizes(ts):
+    return (C.c_int64 * len(ts))(*[int(t.numel()) for t in ts])
+
+
+def grad_norm_ws_bytes(tensors) -> int:
+    return int(lib().mtgnn_grad_norm_ws_bytes(_sizes(tensors), len(tensors)))
+
+
+def mtgnn_grad_norm(grads, norm, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_grad_norm(_ptr_array(grads, torch.float32, "grad"), _sizes(grads), len(grads),
+                                 _ptr(norm, torch.float64, "norm"), wp, wb, _stream(stream)), "mtgnn_grad_norm")
+
+
+def mtgnn_prune_aux(flags, heavy, stream=None):
+    _check(lib().mtgnn_prune_aux(_ptr(flags, torch.uint8, "flags"), int(flags.numel()), int(heavy), _stream(stream)),
+           "mtgnn_prune_aux")
+
+
+def mtgnn_cache_refresh(sync_bits, n_nodes, auth_memory, auth_lu, d: Dims, memory, last_update, stream=None):
+    _check(lib().mtgnn_cache_refresh(_ptr(sync_bits, torch.int32, "sync_bits"), int(n_nodes),
+                                     _ptr(auth_memory, None, "auth_memory"), _ptr(auth_lu, torch.float32, "auth_lu"),
+                                     C.byref(d), _ptr(memory, None, "memory"),
+                                     _ptr(last_update, torch.float32, "last_update"), _stream(stream)),
+           "mtgnn_cache_refresh")
+
+
+def mtgnn_adam_step(params, grads, m, v, shadow, lr, beta1, beta2, eps, t, stream=None):
+    """params, grads, m, v: lists of float32 tensors; shadow: None or a list of (None | bf16 tensor)."""
+    sh = None
+    if shadow is not None:
+        sh = (C.c_void_p * len(shadow))()
+        for i, x in enumerate(shadow):
+            sh[i] = None if x is None else _ptr(x, torch.bfloat16, "shadow").value
+    _check(lib().mtgnn_adam_step(_ptr_array(params, torch.float32, "param"), _ptr_array(grads, torch.float32, "grad"),
+                                 _ptr_array(m, torch.float32, "m"), _ptr_array(v, torch.float32, "v"), sh,
+                                 _sizes(params), len(params), C.byref(AdamConfig(lr, beta1, beta2, eps, int(t))),
+                                 _stream(stream)), "mtgnn_adam_step")
 
 
 def timer_start(kernel: str, max_launches: int):

@@ -29,8 +29,11 @@ LINK = ("W_d1", "b_d1", "W_d2", "b_d2")   # the decoder: float32 in every storag
 
 class TGNStep:
     def __init__(self, w, stream, params: dict, memory: np.ndarray, last_update: np.ndarray, device="cuda",
-                 lag: int = 1, torch_stream=None, overlap: bool = True):
+                 lag: int = 1, torch_stream=None, overlap: bool = True, batch_off=None):
+        """batch_off: optional batch boundaries ([n_batches + 1] event offsets, e.g. a worker's mixed
+        batches); by default the stream is cut into batches of w.batch events."""
         self.w = w
+        self.batch_off = None if batch_off is None else np.asarray(batch_off, np.int64)
         self.lag = lag
         self.overlap = overlap
         self.dev = torch.device(device)
@@ -66,7 +69,7 @@ class TGNStep:
         M.mtgnn_build_temporal_csr(self.src, self.dst, self.t, N, self.csr_off, self.csr_nbr, self.csr_t,
                                    self.csr_eid, ws, stream=self.ts)
         del ws
-        self._alloc(w.batch)
+        self._alloc(w.batch if self.batch_off is None else max(1, int(np.diff(self.batch_off).max(initial=1))))
 
     # ------------------------------------------------------------------ buffers
     def _alloc(self, B):
@@ -237,7 +240,14 @@ class TGNStep:
         M.mtgnn_build_messages_bwd(self.dmsg_time, self.dt, self.n_uniq, self.max_rows, p["time_w"], p["time_b"],
                                    self.d, g["time_w"], g["time_b"], self.ws, stream=s)
 
+    def params_changed(self):
+        """The caller updated the parameters in place: messages built ahead from the old time encoder
+        (during the previous step's embedding) are discarded, and the next step builds its own."""
+        self._pre = None
+
     def batch_range(self, b):
+        if self.batch_off is not None:
+            return int(self.batch_off[b]), int(self.batch_off[b + 1])
         lo = b * self.B
         return lo, min(self.n_events, lo + self.B)
 
