@@ -11,6 +11,7 @@ from .streams import (  # noqa: F401
     Stream,
     make_stream,
     init_params,
+    init_params_jodie,
     window_state,
     loss_noise,
     batch_slice,

@@ -254,3 +254,21 @@ def loss_noise(w: Workload, step: int, n_rows: int, base_seed: int = 0) -> np.nd
 def node_owner(n_nodes: int, n_workers: int, base_seed: int = 0, cid: int = 0) -> np.ndarray:
     """A node ownership map pi for n_workers workers: each node's owner drawn uniformly (int32 [n_nodes])."""
     return _rng(base_seed, cid, _OWNER).integers(0, n_workers, n_nodes).astype(np.int32)
+
+
+def init_params_jodie(w: Workload, base_seed: int = 0, random_bias: bool = False, bias_scale: float = 0.1) -> dict:
+    """JODIE's parameters: the recurrent cell W_ih [d_m, d_msg], W_hh [d_m, d_m] (Xavier-uniform), the time
+    projection W_p [d_m, 1], b_p [d_m], the time encoder and the link decoder (as init_params)."""
+    dm = w.d_mem
+    rng = np.random.default_rng(np.random.SeedSequence([base_seed, w.cid, _PARAMS, 1]))
+    p = {}
+    for name, (fo, fi) in (("W_ih", (dm, w.d_msg)), ("W_hh", (dm, dm)), ("W_p", (dm, 1))):
+        a = np.sqrt(6.0 / (fi + fo))
+        p[name] = rng.uniform(-a, a, size=(fo, fi)).astype(np.float32)
+    for name in ("b_ih", "b_hh", "b_p"):
+        p[name] = (rng.uniform(-bias_scale, bias_scale, dm).astype(np.float32) if random_bias
+                   else np.zeros(dm, np.float32))
+    base = init_params(w, base_seed, random_bias, bias_scale)
+    for k in ("time_w", "time_b", "W_d1", "b_d1", "W_d2", "b_d2"):
+        p[k] = base[k]
+    return p

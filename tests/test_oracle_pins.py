@@ -956,3 +956,82 @@ def test_adam_matches_torch_adam():
         th, m, v = C.adam(th, g, m, v, t, 1e-2, 0.9, 0.999, 1e-8)
         assert np.allclose(th, p.detach().numpy(), rtol=0, atol=1e-14)
     assert abs(C.grad_norm([np.array([3.0]), np.array([[4.0, 12.0]])]) - 13.0) < 1e-15
+
+
+# --------------------------------------------------------------------------- JODIE variant (Section VII-A)
+
+def _jodie_case(seed=0):
+    from synth import init_params_jodie
+    w = tiny_workload(n_nodes=7, n_events=24, batch=8, k=1, d_mem=5, d_time=3, d_edge=2, d_attn=5, n_heads=1)
+    s = tiny_stream(w, seed=seed, t_scale=6.0, tie_every=5)
+    params = {k: v.astype(np.float64) for k, v in init_params_jodie(w, random_bias=True).items()}
+    rng = np.random.default_rng(seed + 20)
+    params["time_w"] = rng.uniform(0.2, 1.5, w.d_time)
+    mem0 = rng.uniform(-1, 1, (w.n_nodes, w.d_mem))
+    lu0 = np.zeros(w.n_nodes)
+    return w, s, params, mem0, lu0, tgn.batch_dict(s, 8, 16), tgn.batch_dict(s, 16, 24)
+
+
+def test_jodie_rnn_matches_torch_rnncell():
+    from oracle import jodie
+    rng = np.random.default_rng(1)
+    x, h = rng.standard_normal((4, 9)), rng.standard_normal((4, 5))
+    cell = torch.nn.RNNCell(9, 5, nonlinearity="tanh", dtype=torch.float64)
+    got = jodie.rnn_cell(x, h, cell.weight_ih.detach().numpy(), cell.weight_hh.detach().numpy(),
+                         cell.bias_ih.detach().numpy(), cell.bias_hh.detach().numpy())
+    ref = cell(torch.from_numpy(x), torch.from_numpy(h)).detach().numpy()
+    assert np.allclose(got, ref, rtol=0, atol=1e-14)
+
+
+def test_jodie_step_matches_torch_autograd():
+    """The whole JODIE step (RNN memory update, time projection, link loss) written again with torch
+    float64 modules from the raw parameters; the loss, z, the updated rows and every gradient agree."""
+    from oracle import jodie
+    w, s, params, mem0, lu0, prev, cur = _jodie_case(3)
+    scale = 0.37
+    r = jodie.step(tgn.Prec("f64"), w, mem0, lu0, params, s.x, prev, cur, scale)
+    T = {k: torch.tensor(np.asarray(v, np.float64), requires_grad=True) for k, v in params.items()}
+    uniq, winner = r.mp.uniq, r.mp.winner
+    ev, role = winner // 2, winner % 2
+    node = np.where(role == 0, prev["src"][ev], prev["dst"][ev])
+    partner = np.where(role == 0, prev["dst"][ev], prev["src"][ev])
+    M0 = torch.from_numpy(mem0)
+    dt = torch.from_numpy(np.asarray(prev["t"], np.float64)[ev] - lu0[node])
+    phi = torch.cos(dt[:, None] * T["time_w"] + T["time_b"])
+    msg = torch.cat([M0[node], M0[partner], phi, torch.from_numpy(s.x[prev["eid"][ev]].astype(np.float64))], 1)
+    cell = torch.nn.RNNCell(w.d_msg, w.d_mem, dtype=torch.float64)
+    h = torch.tanh(torch.nn.functional.linear(msg, T["W_ih"], T["b_ih"])
+                   + torch.nn.functional.linear(M0[uniq], T["W_hh"], T["b_hh"]))
+    del cell
+    M1 = M0.clone()
+    M1[uniq] = h
+    lu1 = lu0.copy()
+    lu1[uniq] = np.asarray(prev["t"], np.float64)[ev]
+    q_node, q_t, n = tgn.queries(cur)
+    delta = torch.from_numpy((np.asarray(q_t, np.float64) - lu1[q_node]) * scale)
+    z = M1[q_node] * (1 + delta[:, None] * T["W_p"][:, 0] + T["b_p"])
+
+    def score(a, b):
+        hh = torch.relu(torch.nn.functional.linear(torch.cat([a, b], 1), T["W_d1"], T["b_d1"]))
+        return torch.nn.functional.linear(hh, T["W_d2"], T["b_d2"])[:, 0]
+
+    bce = torch.nn.functional.binary_cross_entropy_with_logits
+    L = bce(score(z[:n], z[n:2 * n]), torch.ones(n, dtype=torch.float64)) + \
+        bce(score(z[:n], z[2 * n:]), torch.zeros(n, dtype=torch.float64))
+    L.backward()
+    assert abs(r.link.loss - L.item()) < 1e-13
+    assert np.allclose(r.z, z.detach().numpy(), rtol=0, atol=1e-13)
+    assert np.allclose(r.mp.h_new, h.detach().numpy(), rtol=0, atol=1e-14)
+    for k, g in r.grads.items():
+        ref = T[k].grad.numpy()
+        assert np.allclose(g, ref, rtol=0, atol=1e-13), (k, np.abs(g - ref).max())
+
+
+def test_jodie_projection_special_cases():
+    from oracle import jodie
+    rng = np.random.default_rng(2)
+    M = rng.standard_normal((3, 4))
+    Wp, bp = rng.standard_normal((4, 1)), np.zeros(4)
+    assert np.array_equal(jodie.project(M, np.zeros(3, np.float32), Wp, bp), M)       # no elapsed time: z = M
+    d = jodie.projection_delta(tgn.Prec("f32"), np.array([5.0, 7.5], np.float32), np.array([1.0, 7.5], np.float32), 0.5)
+    assert d.tolist() == [2.0, 0.0]
