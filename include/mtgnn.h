@@ -123,7 +123,10 @@ typedef enum {
   MTGNN_OP_BUILD_MESSAGES_BWD = 8,
   MTGNN_OP_BUILD_CSR = 9,
   MTGNN_OP_LINK_LOSS = 10,
-  MTGNN_OP_MIXED_BATCHES = 11
+  MTGNN_OP_MIXED_BATCHES = 11,
+  MTGNN_OP_RNN_UPDATE = 12,
+  MTGNN_OP_RNN_UPDATE_BWD = 13,
+  MTGNN_OP_TIME_PROJECTION_BWD = 14
 } mtgnn_op;
 
 /* Workspace bytes for `op`.  max_rows is the batch size n for BUILD_QUERIES and
@@ -133,7 +136,7 @@ typedef enum {
 size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* dims, int64_t max_rows, int64_t max_q);
 
 /* Bytes of the forward save buffer that the backward call of `op` reads.
- * op = MTGNN_OP_GRU_UPDATE or MTGNN_OP_TEMPORAL_ATTN; 0 otherwise. */
+ * op = MTGNN_OP_GRU_UPDATE, MTGNN_OP_RNN_UPDATE or MTGNN_OP_TEMPORAL_ATTN; 0 otherwise. */
 size_t mtgnn_save_bytes(int op, const mtgnn_dims* dims, int64_t max_rows, int64_t max_q);
 
 /* Batch intake (Definition 2 and Eq. 12).  Builds the query list of
@@ -437,6 +440,52 @@ mtgnn_status mtgnn_dependency_scan(const int32_t* src, const int32_t* dst, int64
 mtgnn_status mtgnn_mixed_batches(const uint8_t* role, int64_t n_events, int64_t batch, int32_t* eid_out,
                                  uint8_t* flags_out, int32_t* batch_off, void* ws, size_t ws_bytes,
                                  hipStream_t stream);
+
+/* ------------------------------------------------------------------ the JODIE variant
+ * Section VII-A's second model.  Its memory phase uses mtgnn_aggregate_last and mtgnn_build_messages
+ * as TGN's does; Update (Eq. 2) is a recurrent cell, and the embedding a projection of the memory in
+ * time instead of the attention (no neighbour sampling).  The masked loss is mtgnn_link_loss with
+ * d_attn = d_mem.  d_mem <= 256. */
+
+/* JODIE's memory update (Eq. 2): for each aggregated row r < n_rows,
+ *   h' = tanh(W_ih x + b_ih + W_hh h + b_hh),  x = msg[r], h = M[uniq[r]] (the first d_mem columns of
+ *   msg[r]); memory[uniq[r]] = h' (rounded to the dtype), last_update[uniq[r]] = t of the winner.
+ *   W_ih [d_mem, d_msg], W_hh [d_mem, d_mem] (dtype); b_ih, b_hh [d_mem] float32;
+ *   save -- mtgnn_save_bytes(MTGNN_OP_RNN_UPDATE) bytes (h', float32) for the backward, or NULL.
+ * Arguments and errors otherwise as mtgnn_gru_update. */
+mtgnn_status mtgnn_rnn_update(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                              const int32_t* n_rows, int64_t max_rows, const void* msg, const void* W_ih,
+                              const void* W_hh, const float* b_ih, const float* b_hh, const mtgnn_dims* dims,
+                              void* memory, float* last_update, void* save, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/* Backward of mtgnn_rnn_update for d_mem = dL/dh' (the previous memory is detached): with
+ * dpre = d_mem (1 - h'^2), dW_ih = dpre^T msg, dW_hh = dpre^T h, db_ih = db_hh = sum of dpre (overwritten),
+ * and dmsg_time = dpre W_ih[:, 2 d_mem : 2 d_mem + d_time] (the message's time slice). */
+mtgnn_status mtgnn_rnn_update_bwd(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,
+                                  int64_t max_rows, const void* W_ih, const void* W_hh, const mtgnn_dims* dims,
+                                  float* dW_ih, float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* JODIE's time-projection embedding of each query q < n_q:
+ *   z[q] = M[n] (1 + W_p Delta + b_p),  Delta = (q_t[q] - last_update[n]) * time_scale  (two float32
+ *   operations), n = q_node[q], with the table after this step's update.
+ *   W_p [d_mem] (the [d_mem, 1] weight), b_p [d_mem] float32; z [max_q, d_mem] float32 out. */
+mtgnn_status mtgnn_time_projection(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                   const void* memory, const float* last_update, const float* W_p, const float* b_p,
+                                   float time_scale, const mtgnn_dims* dims, float* z, hipStream_t stream);
+
+/* Backward of mtgnn_time_projection for dz [max_q, d_mem]:
+ *   dW_p, db_p [d_mem] (overwritten): the column sums over the queries of dz M Delta and dz M;
+ *   d_mem [max_rows, d_mem] out, row r aligned with uniq[r]: the sum over the queries of node uniq[r]
+ *     of dz (1 + W_p Delta + b_p), in query order (rows of uniq that no query names get 0; nodes not
+ *     in uniq get nothing: the table is not differentiated across steps).
+ * Deterministic (fixed-order sums).  Workspace: MTGNN_OP_TIME_PROJECTION_BWD with max_q. */
+mtgnn_status mtgnn_time_projection_bwd(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                       const void* memory, const float* last_update, const float* W_p,
+                                       const float* b_p, float time_scale, const float* dz, const int32_t* uniq,
+                                       const int32_t* n_rows, int64_t max_rows, const mtgnn_dims* dims, float* dW_p,
+                                       float* db_p, float* d_mem, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------ adaptive runtime controller
  * The decisions of one worker's runtime controller (Section V, Algorithm 2), kept on the host:

@@ -73,9 +73,11 @@ def memory_phase(prec, dims, batch, mem, lu, x_all, params):
     return tgn.MemoryPhase(uniq, winner, msg, dt, h_old, (), h_new, mem2, lu2)
 
 
-def step(prec, dims, mem, lu, params, x_all, mem_batch, emb_batch, scale) -> JodieStep:
+def step(prec, dims, mem, lu, params, x_all, mem_batch, emb_batch, scale, flips=None) -> JodieStep:
     """One JODIE training step: memory phase on mem_batch, projection of emb_batch's queries with the
-    updated table, the masked link loss, and the backward pass (memory is detached across steps)."""
+    updated table, the masked link loss, and the backward pass (memory is detached across steps).
+    ``flips`` inverts chosen decoder ReLU decisions, as ``tgn.step``'s."""
+    flips = flips or {}
     if mem_batch is None:
         mem_batch = {"src": np.zeros(0, np.int64), "dst": np.zeros(0, np.int64), "t": np.zeros(0, F32),
                      "eid": np.zeros(0, np.int64)}
@@ -84,7 +86,7 @@ def step(prec, dims, mem, lu, params, x_all, mem_batch, emb_batch, scale) -> Jod
     delta = projection_delta(prec, q_t, mp.lu[q_node], scale)
     Mq = np.asarray(mp.mem[q_node], F64)
     z = project(Mq, delta, params["W_p"], params["b_p"])
-    link = tgn.link_loss(params, z, n_tar)
+    link = tgn.link_loss(params, z, n_tar, flips.get("pos"), flips.get("neg"))
     dz = link.dz
     g = dict(link.grads)
     # z = M (1 + W_p Delta + b_p)

@@ -188,6 +188,9 @@ size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int6
     case MTGNN_OP_GRU_UPDATE_BWD: return gru_update_bwd_ws(d, max_rows);
     case MTGNN_OP_BUILD_MESSAGES_BWD: return build_messages_bwd_ws(d, max_rows);
     case MTGNN_OP_LINK_LOSS: return link_loss_ws(d, max_q);
+    case MTGNN_OP_RNN_UPDATE: return rnn_update_ws(d, max_rows);
+    case MTGNN_OP_RNN_UPDATE_BWD: return rnn_update_bwd_ws(d, max_rows);
+    case MTGNN_OP_TIME_PROJECTION_BWD: return time_projection_bwd_ws(d, max_q);
     default: return 0;
   }
 }
@@ -195,6 +198,7 @@ size_t mtgnn_workspace_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int6
 size_t mtgnn_save_bytes(int op, const mtgnn_dims* d, int64_t max_rows, int64_t max_q) {
   if (check_dims(d) != MTGNN_OK || max_rows < 0 || max_q < 0) return 0;
   if (op == MTGNN_OP_GRU_UPDATE) return gru_save_bytes(d, max_rows);
+  if (op == MTGNN_OP_RNN_UPDATE) return rnn_save_bytes(d, max_rows);
   if (op == MTGNN_OP_TEMPORAL_ATTN) return attn_save_bytes(d, max_q);
   return 0;
 }
@@ -658,6 +662,98 @@ mtgnn_status mtgnn_adam_step(float* const* params, const float* const* grads, fl
       !(cfg->eps > 0))
     return fail(MTGNN_EINVAL, "adam config");
   return adam_impl(params, grads, m, v, shadow, sizes, n, cfg, stream);
+}
+
+mtgnn_status mtgnn_rnn_update(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner,
+                              const int32_t* n_rows, int64_t max_rows, const void* msg, const void* W_ih,
+                              const void* W_hh, const float* b_ih, const float* b_hh, const mtgnn_dims* d,
+                              void* memory, float* last_update, void* save, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_batch(b));
+  MTGNN_TRY(check_rows(max_rows));
+  if (d->d_mem > 256) return fail(MTGNN_EUNSUPPORTED, "rnn_update: d_mem > 256");
+  if (max_rows == 0) return MTGNN_OK;
+  REQ(uniq, "uniq");
+  REQ(winner, "winner");
+  REQ(msg, "msg");
+  REQ(W_ih, "W_ih");
+  REQ(W_hh, "W_hh");
+  REQ(b_ih, "b_ih");
+  REQ(b_hh, "b_hh");
+  REQ(memory, "memory");
+  REQ(last_update, "last_update");
+  if (ws_bytes < rnn_update_ws(d, max_rows)) return fail(MTGNN_EWORKSPACE, "rnn_update ws");
+  REQ(ws, "ws");
+  return rnn_update_impl(b, uniq, winner, n_rows, max_rows, msg, W_ih, W_hh, b_ih, b_hh, d, memory, last_update, save,
+                         ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_rnn_update_bwd(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,
+                                  int64_t max_rows, const void* W_ih, const void* W_hh, const mtgnn_dims* d,
+                                  float* dW_ih, float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time,
+                                  void* ws, size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  REQ(dW_ih, "dW_ih");
+  REQ(dW_hh, "dW_hh");
+  REQ(db_ih, "db_ih");
+  REQ(db_hh, "db_hh");
+  if (max_rows == 0) return fail(MTGNN_EINVAL, "max_rows == 0 (no updated row: every gradient is zero; skip the call)");
+  REQ(d_mem, "d_mem");
+  REQ(save, "save");
+  REQ(msg, "msg");
+  REQ(W_ih, "W_ih");
+  if (ws_bytes < rnn_update_bwd_ws(d, max_rows)) return fail(MTGNN_EWORKSPACE, "rnn_update_bwd ws");
+  REQ(ws, "ws");
+  return rnn_update_bwd_impl(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d, dW_ih, dW_hh, db_ih, db_hh, dmsg_time,
+                             ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_time_projection(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                   const void* memory, const float* last_update, const float* W_p, const float* b_p,
+                                   float time_scale, const mtgnn_dims* d, float* z, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  if (max_q < 0 || max_q >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (max_q == 0) return MTGNN_OK;
+  REQ(q_node, "q_node");
+  REQ(q_t, "q_t");
+  REQ(memory, "memory");
+  REQ(last_update, "last_update");
+  REQ(W_p, "W_p");
+  REQ(b_p, "b_p");
+  REQ(z, "z");
+  return time_projection_impl(q_node, q_t, n_q, max_q, memory, last_update, W_p, b_p, time_scale, d, z, stream);
+}
+
+mtgnn_status mtgnn_time_projection_bwd(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                       const void* memory, const float* last_update, const float* W_p,
+                                       const float* b_p, float time_scale, const float* dz, const int32_t* uniq,
+                                       const int32_t* n_rows, int64_t max_rows, const mtgnn_dims* d, float* dW_p,
+                                       float* db_p, float* d_mem, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_rows(max_rows));
+  if (d->d_mem > 256) return fail(MTGNN_EUNSUPPORTED, "time_projection_bwd: d_mem > 256");
+  if (max_q < 0 || max_q >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  REQ(dW_p, "dW_p");
+  REQ(db_p, "db_p");
+  REQ(W_p, "W_p");
+  REQ(b_p, "b_p");
+  if (max_q > 0) {
+    REQ(q_node, "q_node");
+    REQ(q_t, "q_t");
+    REQ(memory, "memory");
+    REQ(last_update, "last_update");
+    REQ(dz, "dz");
+  }
+  if (max_rows > 0) {
+    REQ(uniq, "uniq");
+    REQ(d_mem, "d_mem");
+  }
+  if (ws_bytes < time_projection_bwd_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "time_projection_bwd ws");
+  REQ(ws, "ws");
+  return time_projection_bwd_impl(q_node, q_t, n_q, max_q, memory, last_update, W_p, b_p, time_scale, dz, uniq, n_rows,
+                                  max_rows, d, dW_p, db_p, d_mem, ws, ws_bytes, stream);
 }
 
 mtgnn_status mtgnn_build_temporal_csr(const int32_t* src, const int32_t* dst, const float* t, int64_t n_events,

@@ -89,6 +89,28 @@ mtgnn_status cache_refresh_impl(const uint32_t* bits, int64_t n_nodes, const voi
 mtgnn_status adam_impl(float* const* params, const float* const* grads, float* const* m, float* const* v,
                        void* const* shadow, const int64_t* sizes, int n, const mtgnn_adam_config* c, hipStream_t s);
 
+// the JODIE variant (jodie.hip)
+size_t rnn_save_bytes(const mtgnn_dims* d, int64_t max_rows);
+size_t rnn_update_ws(const mtgnn_dims* d, int64_t max_rows);
+mtgnn_status rnn_update_impl(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner, const int32_t* n_rows,
+                             int64_t max_rows, const void* msg, const void* W_ih, const void* W_hh, const float* b_ih,
+                             const float* b_hh, const mtgnn_dims* d, void* memory, float* lu, void* save, void* ws,
+                             size_t ws_bytes, hipStream_t s);
+size_t rnn_update_bwd_ws(const mtgnn_dims* d, int64_t max_rows);
+mtgnn_status rnn_update_bwd_impl(const float* d_mem, const void* save, const void* msg, const int32_t* n_rows,
+                                 int64_t max_rows, const void* W_ih, const void* W_hh, const mtgnn_dims* d,
+                                 float* dW_ih, float* dW_hh, float* db_ih, float* db_hh, float* dmsg_time, void* ws,
+                                 size_t ws_bytes, hipStream_t s);
+mtgnn_status time_projection_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                  const void* memory, const float* lu, const float* Wp, const float* bp, float scale,
+                                  const mtgnn_dims* d, float* z, hipStream_t s);
+size_t time_projection_bwd_ws(const mtgnn_dims* d, int64_t max_q);
+mtgnn_status time_projection_bwd_impl(const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q,
+                                      const void* memory, const float* lu, const float* Wp, const float* bp,
+                                      float scale, const float* dz, const int32_t* uniq, const int32_t* n_rows,
+                                      int64_t max_rows, const mtgnn_dims* d, float* dWp, float* dbp, float* d_mem,
+                                      void* ws, size_t ws_bytes, hipStream_t s);
+
 // sampling / adjacency
 mtgnn_status sample_recent_impl(const int64_t* off, const int32_t* nbr, const float* t, const int32_t* eid,
                                 const int32_t* q_node, const float* q_t, const int32_t* n_q, int64_t max_q, int k,

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmtgnn.so
 F32, BF16 = 0, 1
 OP_BUILD_QUERIES, OP_AGGREGATE_LAST, OP_BUILD_MESSAGES, OP_GRU_UPDATE, OP_SAMPLE_RECENT = 0, 1, 2, 3, 4
 OP_TEMPORAL_ATTN, OP_TEMPORAL_ATTN_BWD, OP_GRU_UPDATE_BWD, OP_BUILD_MESSAGES_BWD, OP_BUILD_CSR = 5, 6, 7, 8, 9
-OP_LINK_LOSS, OP_MIXED_BATCHES = 10, 11
+OP_LINK_LOSS, OP_MIXED_BATCHES, OP_RNN_UPDATE, OP_RNN_UPDATE_BWD, OP_TIME_PROJECTION_BWD = 10, 11, 12, 13, 14
 
 ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
@@ -27,7 +27,8 @@ ENTRY_POINTS = (
     "mtgnn_temporal_attn_bwd_grouped",
     "mtgnn_gru_update_bwd", "mtgnn_link_loss",
     "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr",
-    "mtgnn_dependency_scan", "mtgnn_mixed_batches", "mtgnn_controller_create", "mtgnn_controller_destroy",
+    "mtgnn_dependency_scan", "mtgnn_mixed_batches", "mtgnn_rnn_update", "mtgnn_rnn_update_bwd",
+    "mtgnn_time_projection", "mtgnn_time_projection_bwd", "mtgnn_controller_create", "mtgnn_controller_destroy",
     "mtgnn_controller_decide", "mtgnn_controller_observe", "mtgnn_controller_state", "mtgnn_grad_norm_ws_bytes",
     "mtgnn_grad_norm", "mtgnn_prune_aux", "mtgnn_cache_refresh", "mtgnn_adam_step", "mtgnn_workspace_bytes", "mtgnn_save_bytes",
     "mtgnn_status_string", "mtgnn_last_error", "mtgnn_version", "mtgnn_timer_start", "mtgnn_timer_stop",
@@ -114,6 +115,12 @@ _SIGS = {
     "mtgnn_build_messages_bwd_noalloc": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_dependency_scan": [_P, _P, _I64, _P, _I64, _I32, _I64, _I32, _P, _P, _P],
+    "mtgnn_rnn_update": [C.POINTER(Batch), _P, _P, _P, _I64, _P, _P, _P, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _SZ,
+                         _P],
+    "mtgnn_rnn_update_bwd": [_P, _P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _P, _P, _SZ, _P],
+    "mtgnn_time_projection": [_P, _P, _P, _I64, _P, _P, _P, _P, C.c_float, C.POINTER(Dims), _P, _P],
+    "mtgnn_time_projection_bwd": [_P, _P, _P, _I64, _P, _P, _P, _P, C.c_float, _P, _P, _P, _I64, C.POINTER(Dims),
+                                  _P, _P, _P, _P, _SZ, _P],
     "mtgnn_controller_create": [C.POINTER(ControllerConfig), C.POINTER(C.c_void_p)],
     "mtgnn_controller_destroy": [_P],
     "mtgnn_controller_decide": [_P, _I64, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32)],
@@ -496,6 +503,52 @@ def mtgnn_mixed_batches(role, batch, eid_out, flags_out, batch_off, ws, stream=N
                                      _ptr(eid_out, torch.int32, "eid_out"), _ptr(flags_out, torch.uint8, "flags_out"),
                                      _ptr(batch_off, torch.int32, "batch_off"), wp, wb, _stream(stream)),
            "mtgnn_mixed_batches")
+
+
+def mtgnn_rnn_update(b: Batch, uniq, winner, n_rows, max_rows, msg, W_ih, W_hh, b_ih, b_hh, d: Dims, memory,
+                     last_update, save, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_rnn_update(C.byref(b), _ptr(uniq, torch.int32, "uniq"), _ptr(winner, torch.int32, "winner"),
+                                  _ptr(n_rows, torch.int32, "n_rows", True), int(max_rows), _ptr(msg, _DT[d.dtype], "msg"),
+                                  _ptr(W_ih, _DT[d.dtype], "W_ih"), _ptr(W_hh, _DT[d.dtype], "W_hh"),
+                                  _ptr(b_ih, torch.float32, "b_ih"), _ptr(b_hh, torch.float32, "b_hh"), C.byref(d),
+                                  _ptr(memory, _DT[d.dtype], "memory"), _ptr(last_update, torch.float32, "last_update"),
+                                  _ptr(save, torch.uint8, "save", True), wp, wb, _stream(stream)), "mtgnn_rnn_update")
+
+
+def mtgnn_rnn_update_bwd(d_mem, save, msg, n_rows, max_rows, W_ih, W_hh, d: Dims, dW_ih, dW_hh, db_ih, db_hh,
+                         dmsg_time, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_rnn_update_bwd(_ptr(d_mem, torch.float32, "d_mem"), _ptr(save, torch.uint8, "save"),
+                                      _ptr(msg, _DT[d.dtype], "msg"), _ptr(n_rows, torch.int32, "n_rows", True),
+                                      int(max_rows), _ptr(W_ih, _DT[d.dtype], "W_ih"), _ptr(W_hh, _DT[d.dtype], "W_hh"),
+                                      C.byref(d), _ptr(dW_ih, torch.float32, "dW_ih"),
+                                      _ptr(dW_hh, torch.float32, "dW_hh"), _ptr(db_ih, torch.float32, "db_ih"),
+                                      _ptr(db_hh, torch.float32, "db_hh"),
+                                      _ptr(dmsg_time, torch.float32, "dmsg_time", True), wp, wb, _stream(stream)),
+           "mtgnn_rnn_update_bwd")
+
+
+def mtgnn_time_projection(q_node, q_t, n_q, max_q, memory, last_update, W_p, b_p, time_scale, d: Dims, z,
+                          stream=None):
+    _check(lib().mtgnn_time_projection(_ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"),
+                                       _ptr(n_q, torch.int32, "n_q", True), int(max_q),
+                                       _ptr(memory, _DT[d.dtype], "memory"),
+                                       _ptr(last_update, torch.float32, "last_update"), _ptr(W_p, torch.float32, "W_p"),
+                                       _ptr(b_p, torch.float32, "b_p"), float(time_scale), C.byref(d),
+                                       _ptr(z, torch.float32, "z"), _stream(stream)), "mtgnn_time_projection")
+
+
+def mtgnn_time_projection_bwd(q_node, q_t, n_q, max_q, memory, last_update, W_p, b_p, time_scale, dz, uniq, n_rows,
+                              max_rows, d: Dims, dW_p, db_p, d_mem, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_time_projection_bwd(
+        _ptr(q_node, torch.int32, "q_node"), _ptr(q_t, torch.float32, "q_t"), _ptr(n_q, torch.int32, "n_q", True),
+        int(max_q), _ptr(memory, _DT[d.dtype], "memory"), _ptr(last_update, torch.float32, "last_update"),
+        _ptr(W_p, torch.float32, "W_p"), _ptr(b_p, torch.float32, "b_p"), float(time_scale),
+        _ptr(dz, torch.float32, "dz"), _ptr(uniq, torch.int32, "uniq"), _ptr(n_rows, torch.int32, "n_rows", True),
+        int(max_rows), C.byref(d), _ptr(dW_p, torch.float32, "dW_p"), _ptr(db_p, torch.float32, "db_p"),
+        _ptr(d_mem, torch.float32, "d_mem"), wp, wb, _stream(stream)), "mtgnn_time_projection_bwd")
 
 
 class Controller:
