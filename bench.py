@@ -39,9 +39,18 @@ def parse():
     ap.add_argument("--steps", type=int, default=0, help="timed steps (0: 50, or 30 for batches of 60,000)")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--model", choices=("tgn", "jodie", "adaptive"), default="tgn",
+                    help="tgn: the TGN step (default); jodie: the JODIE variant's step; adaptive: Algorithm 2's loop "
+                         "for one worker of --workers over its mixed batches (dependency scan, controller, PruneAux, "
+                         "refresh, Adam)")
+    ap.add_argument("--workers", type=int, default=8, help="workers of the partition (--model adaptive)")
+    ap.add_argument("--window", type=int, default=10, help="synchronization window in batches (--model adaptive)")
     ap.add_argument("--cpu-steps", type=int, default=3, help="oracle steps timed for the CPU baseline (0: skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="before the warmup, copy a buffer of this many MiB twice (HBM counter calibration)")
+    ap.add_argument("--kernel-report", nargs=3, metavar=("TRACE_CSV", "FETCH_CSV", "WRITE_CSV"),
+                    help="turn a rocprofv3 --kernel-trace CSV and two --pmc CSVs (FETCH_SIZE, WRITE_SIZE; runs made "
+                         "with --copy-probe) into per-kernel HBM traffic and achieved GB/s under profiles/, then exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a run made with "
                          "--copy-probe into the traffic record under profiles/, then exit")
@@ -57,10 +66,16 @@ def main():
     if args.traffic_from:
         write_traffic(args)
         return
+    if args.kernel_report:
+        kernel_report(args)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the multi-GPU sharding is described, not built.", file=sys.stderr)
         sys.exit(2)
+    if args.model != "tgn":
+        other_model(args)
+        return
     import torch
 
     from paper_2608_16305_amd.step import TGNStep
@@ -178,6 +193,62 @@ def main():
 
     if args.cpu_steps > 0:
         out["cpu_baseline"] = cpu_baseline(w, s, params, mem, lu, b0, args.cpu_steps)
+    print(json.dumps(out), flush=True)
+
+
+def other_model(args):
+    """The JODIE step, or Algorithm 2's loop for one worker: one JSON line, events/s over K timed steps."""
+    import torch
+
+    from synth import init_params, init_params_jodie, make_stream, node_owner, window_state, workload
+    w = workload(args.workload)
+    s = make_stream(w)
+    b0 = w.window_b0
+    mem, lu = window_state(w, s, b0)
+    out = {"metric": "events/sec per batch step (fwd+bwd) on 1 MI355X; % HBM / MFMA roofline", "unit": "events/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if w.dtype == "bf16" else "f32", "data": "synthetic",
+           "roofline": None}
+    if args.model == "jodie":
+        from paper_2608_16305_amd.jodie_step import JodieStep
+        r = JodieStep(w, s, init_params_jodie(w), mem, lu)
+        for i in range(args.warmup):
+            r.step(b0 + i)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record()
+        for i in range(args.warmup, args.warmup + args.steps):
+            r.step(b0 + i)
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1)
+        out.update(value=w.batch * args.steps / (ms / 1e3), ms_per_step=ms / args.steps,
+                   config={"workload": w.name, "model": "JODIE (recurrent update, time projection, masked link loss)",
+                           "batch": w.batch, "d_mem": w.d_mem, "d_time": w.d_time, "first_batch": b0})
+    else:
+        from paper_2608_16305_amd.runtime import AdaptiveTrainer
+        P = args.workers
+        tr = AdaptiveTrainer(w, s, init_params(w), mem, lu, node_owner(w.n_nodes, P), 0, P, args.window)
+        n = min(tr.n_batches, args.warmup + args.steps)
+        for r in range(args.warmup):
+            tr.batch(r)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for r in range(args.warmup, n):
+            tr.batch(r)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        recs = tr.records[args.warmup:n]
+        ev = sum(x.n_events for x in recs)
+        tar = sum(int(((tr.local.flags[tr.batch_off[x.r]:tr.batch_off[x.r + 1]] & 1) == 0).sum()) for x in recs)
+        out.update(value=ev / wall, ms_per_step=wall * 1e3 / len(recs), target_events_per_s=tar / wall,
+                   decisions={"refresh": sum(x.sync for x in recs), "skipped": sum(x.boundary and not x.sync
+                                                                                   for x in recs),
+                              "heavy": sum(x.heavy for x in recs)},
+                   config={"workload": w.name, "model": "TGN, Algorithm 2 loop of worker 0", "workers": P,
+                           "window": args.window, "batches": len(recs), "replay_share": float(
+                               (tr.local.flags & 1).mean()), "note": "from the stream's start; memory from the "
+                           "window snapshot; wall-clock incl. the per-batch host reads Algorithm 2 needs"})
     print(json.dumps(out), flush=True)
 
 
@@ -315,6 +386,58 @@ def step_counts(runner, s, w, b0, first, count):
         Q += 3 * (ehi - elo if s.flags is None else int(((s.flags[elo:ehi] & 3) == 0).sum()))
         P += valid_slots(runner, s, w, b)
     return {"updated_rows": U / count, "queries": Q / count, "valid_slots": P / count}
+
+
+def _clean_kernel(name):
+    for x in ("mtgnn::", "(anonymous namespace)::", "site::"):
+        name = name.replace(x, "")
+    return name.split("(")[0]
+
+
+def kernel_report(args):
+    """Per kernel of the step: mean duration (kernel trace), calibrated FETCH_SIZE and WRITE_SIZE bytes per
+    dispatch (counter runs), achieved GB/s and its fraction of the 8 TB/s HBM peak."""
+    import csv
+    from synth import workload
+    w = workload(args.workload)
+    probe = args.copy_probe * (1 << 20)
+    if probe <= 0:
+        raise SystemExit("--kernel-report needs --copy-probe MIB (the probe size of the counter runs)")
+    trace_csv, fetch_csv, write_csv = args.kernel_report
+    dur = {}
+    with open(trace_csv) as fh:
+        for r in csv.DictReader(fh):
+            k = _clean_kernel(r["Kernel_Name"])
+            dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+
+    def counter(path, name):
+        rows = _counter_rows(path, name)
+        first = next(i for i, r in enumerate(rows) if "k_agg_reset" in r["Kernel_Name"])
+        probes = [r for r in rows[:first] if "copyBuffer" in r["Kernel_Name"]][-2:]
+        factor = probe / 1024.0 / (sum(float(r["Counter_Value"]) for r in probes) / 2)
+        per = {}
+        for r in rows[first:]:
+            per.setdefault(_clean_kernel(r["Kernel_Name"]), []).append(float(r["Counter_Value"]) * 1024.0 * factor)
+        return {k: sum(v) / len(v) for k, v in per.items()}, factor
+
+    fetch, ff = counter(fetch_csv, "FETCH_SIZE")
+    write, fw = counter(write_csv, "WRITE_SIZE")
+    rows = []
+    for k in fetch:
+        if k not in write or k not in dur or "copyBuffer" in k:
+            continue
+        us = sorted(dur[k])[len(dur[k]) // 2]
+        by = fetch[k] + write[k]
+        rows.append({"kernel": k, "median_us": us, "fetch_MB": fetch[k] / 1e6, "write_MB": write[k] / 1e6,
+                     "GBps": by / (us * 1e-6) / 1e9, "hbm_frac": by / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                     "launches": len(dur[k])})
+    rows.sort(key=lambda r: -r["median_us"])
+    base = os.path.join(ROOT, "profiles", f"kernel-hbm-{w.name}")
+    rec = {"workload": w.name, "fetch_factor": ff, "write_factor": fw, "probe_bytes": probe, "kernels": rows}
+    with open(base + ".json", "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps({"written": base + ".json", "kernels": len(rows)}))
 
 
 def cpu_baseline(w, s, params, mem, lu, b0, n):

@@ -71,7 +71,8 @@ __global__ __launch_bounds__(256) void k_time_proj_bwd_rows(
     const int32_t* __restrict__ q_node, const float* __restrict__ q_t, const int32_t* __restrict__ n_q, int64_t max_q,
     const T* __restrict__ mem, const float* __restrict__ lu, float s, int dm, const float* __restrict__ dz,
     const int32_t* __restrict__ uniq, const int32_t* __restrict__ n_rows, const int32_t* __restrict__ row_of,
-    int64_t max_rows, float* __restrict__ G, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+    int64_t max_rows, const float* __restrict__ Wp, const float* __restrict__ bp, float* __restrict__ G,
+    float* __restrict__ Cq, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
   const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (q >= max_q) return;
@@ -96,6 +97,7 @@ __global__ __launch_bounds__(256) void k_time_proj_bwd_rows(
     const float g = dz[q * dm + j] * Elem<T>::load(mem, n * dm + j);
     G[q * 2 * dm + j] = g * dl;
     G[q * 2 * dm + dm + j] = g;
+    Cq[q * dm + j] = dz[q * dm + j] * (1.0f + dl * Wp[j] + bp[j]);
   }
 }
 
@@ -144,6 +146,46 @@ __global__ __launch_bounds__(256) void k_jodie_dmem(const uint32_t* __restrict__
   for (int u = 0; u < NC; ++u) {
     const int j = lane + 64 * u;
     if (j < dm) d_mem[r * dm + j] = acc[u];
+  }
+}
+
+// The same sums with the occurrences spread over the lanes: lane l adds occurrences l, l + 64, ... of the
+// row's segment (all d_mem columns, 4 per register group), then the 64 lane sums are added by a fixed
+// butterfly per column.  A hub row's thousands of occurrences then take tens of rounds, not thousands.
+template <int NQ>
+__global__ __launch_bounds__(256) void k_jodie_dmem_lanes(const uint32_t* __restrict__ skeys,
+                                                          const uint32_t* __restrict__ svals, int64_t n_occ,
+                                                          const float* __restrict__ Cq,
+                                                          const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
+                                                          float* __restrict__ d_mem) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= eff_count(max_rows, n_rows)) return;
+  const int64_t lo = lower_bound_u32(skeys, n_occ, (uint32_t)r);
+  const int64_t hi = lower_bound_u32(skeys, n_occ, (uint32_t)r + 1);
+  float4 acc[NQ];
+#pragma unroll
+  for (int u = 0; u < NQ; ++u) acc[u] = float4{0.f, 0.f, 0.f, 0.f};
+  const int nq = dm / 4;
+  for (int64_t i = lo + lane; i < hi; i += 64) {
+    const float4* row = reinterpret_cast<const float4*>(Cq + (int64_t)svals[i] * dm);
+#pragma unroll
+    for (int u = 0; u < NQ; ++u) {
+      if (u < nq) {
+        const float4 c = row[u];
+        acc[u].x += c.x;
+        acc[u].y += c.y;
+        acc[u].z += c.z;
+        acc[u].w += c.w;
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < NQ; ++u) {
+    if (u < nq) {
+      const float x = wave_sum(acc[u].x), y = wave_sum(acc[u].y), z = wave_sum(acc[u].z), w = wave_sum(acc[u].w);
+      if (lane == 0) reinterpret_cast<float4*>(d_mem + r * dm)[u] = float4{x, y, z, w};
+    }
   }
 }
 
@@ -235,7 +277,7 @@ mtgnn_status time_projection_impl(const int32_t* q_node, const float* q_t, const
 struct ProjBwdWs {
   int32_t* row_of;
   uint32_t *keys, *vals;
-  float *G, *sums;
+  float *G, *Cq, *sums;
   void* sort_ws;
   size_t sort_bytes;
   void* cs_ws;
@@ -256,6 +298,7 @@ static ProjBwdWs proj_bwd_layout(void* ws, const mtgnn_dims* d, int64_t max_q) {
   L.keys = (uint32_t*)take(sizeof(uint32_t) * (size_t)mq);
   L.vals = (uint32_t*)take(sizeof(uint32_t) * (size_t)mq);
   L.G = (float*)take(sizeof(float) * (size_t)mq * 2 * d->d_mem);
+  L.Cq = (float*)take(sizeof(float) * (size_t)mq * d->d_mem);
   L.sums = (float*)take(sizeof(float) * 2 * (size_t)d->d_mem);
   L.sort_bytes = radix_sort_ws_bytes(mq);
   L.sort_ws = take(L.sort_bytes);
@@ -286,10 +329,11 @@ mtgnn_status time_projection_bwd_impl(const int32_t* q_node, const float* q_t, c
     const unsigned g = (unsigned)cdiv(max_q, 4);
     if (d->dtype == MTGNN_BF16)
       k_time_proj_bwd_rows<uint16_t><<<g, 256, 0, s>>>(q_node, q_t, n_q, max_q, (const uint16_t*)memory, lu, scale, dm,
-                                                       dz, uniq, n_rows, L.row_of, max_rows, L.G, L.keys, L.vals);
+                                                       dz, uniq, n_rows, L.row_of, max_rows, Wp, bp, L.G, L.Cq, L.keys, L.vals);
     else
       k_time_proj_bwd_rows<float><<<g, 256, 0, s>>>(q_node, q_t, n_q, max_q, (const float*)memory, lu, scale, dm, dz,
-                                                    uniq, n_rows, L.row_of, max_rows, L.G, L.keys, L.vals);
+                                                    uniq, n_rows, L.row_of, max_rows, Wp, bp, L.G, L.Cq, L.keys,
+                                                    L.vals);
     MTGNN_CHECK_LAUNCH("time_proj_bwd_rows");
   }
   MTGNN_TRY(colsum(L.G, 2 * dm, max_q, n_q, 2 * dm, L.sums, false, L.cs_ws, L.cs_bytes, s));
@@ -298,12 +342,16 @@ mtgnn_status time_projection_bwd_impl(const int32_t* q_node, const float* q_t, c
   if (max_rows > 0) {
     uint32_t *sk = L.keys, *sv = L.vals;
     if (max_q > 0) MTGNN_TRY(radix_sort_pairs(&sk, &sv, max_q, bits_for(max_rows), L.sort_ws, L.sort_bytes, s));
-    if (d->dtype == MTGNN_BF16)
-      k_jodie_dmem<uint16_t><<<(unsigned)cdiv(max_rows, 4), 256, 0, s>>>(sk, sv, max_q, q_node, q_t, lu, Wp, bp, scale,
-                                                                         dz, n_rows, max_rows, dm, d_mem);
+    const unsigned g = (unsigned)cdiv(max_rows, 4);
+    const bool lanes = dm % 4 == 0 && dm <= 128 && ((uintptr_t)L.Cq | (uintptr_t)d_mem) % 16 == 0;
+    if (lanes)
+      k_jodie_dmem_lanes<32><<<g, 256, 0, s>>>(sk, sv, max_q, L.Cq, n_rows, max_rows, dm, d_mem);
+    else if (d->dtype == MTGNN_BF16)
+      k_jodie_dmem<uint16_t><<<g, 256, 0, s>>>(sk, sv, max_q, q_node, q_t, lu, Wp, bp, scale, dz, n_rows, max_rows, dm,
+                                               d_mem);
     else
-      k_jodie_dmem<float><<<(unsigned)cdiv(max_rows, 4), 256, 0, s>>>(sk, sv, max_q, q_node, q_t, lu, Wp, bp, scale,
-                                                                      dz, n_rows, max_rows, dm, d_mem);
+      k_jodie_dmem<float><<<g, 256, 0, s>>>(sk, sv, max_q, q_node, q_t, lu, Wp, bp, scale, dz, n_rows, max_rows, dm,
+                                            d_mem);
     MTGNN_CHECK_LAUNCH("jodie_dmem");
   }
   return MTGNN_OK;

@@ -221,7 +221,7 @@ __global__ __launch_bounds__(SORT_THREADS) void k_radix_scatter(const uint32_t* 
 
 constexpr int CS_COLS = 64;
 constexpr int CS_ROWGROUPS = 4;
-constexpr int CS_ROWS_PER_CHUNK = 1024;
+constexpr int CS_ROWS_PER_CHUNK = 128;   // 32 rows per thread: short dependent chains, many blocks
 
 __global__ __launch_bounds__(256) void k_colsum_partial(const float* __restrict__ X, int64_t ld, int64_t rows,
                                                         const int32_t* __restrict__ rows_dev, int cols,
@@ -242,13 +242,16 @@ __global__ __launch_bounds__(256) void k_colsum_partial(const float* __restrict_
                                               red[3][threadIdx.x];
 }
 
+// A wave per column: lane l adds chunks l, l + 64, ... in order, then a fixed butterfly.
 __global__ void k_colsum_final(const float* __restrict__ partial, int nchunks, int cols, float* __restrict__ out,
                                int accumulate) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (c >= cols) return;
   float s = 0.f;
-  for (int j = 0; j < nchunks; ++j) s += partial[(int64_t)j * cols + c];
-  out[c] = accumulate ? out[c] + s : s;
+  for (int j = lane; j < nchunks; j += 64) s += partial[(int64_t)j * cols + c];
+  s = wave_sum(s);
+  if (lane == 0) out[c] = accumulate ? out[c] + s : s;
 }
 
 }  // namespace
@@ -368,7 +371,7 @@ mtgnn_status colsum(const float* X, int64_t ld, int64_t rows, const int32_t* row
   dim3 g((unsigned)cdiv(cols, CS_COLS), (unsigned)nch);
   k_colsum_partial<<<g, 256, 0, s>>>(X, ld, rows, rows_dev, cols, partial);
   MTGNN_CHECK_LAUNCH("colsum_partial");
-  k_colsum_final<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(partial, (int)nch, cols, out, accumulate ? 1 : 0);
+  k_colsum_final<<<(unsigned)cdiv(cols, 4), 256, 0, s>>>(partial, (int)nch, cols, out, accumulate ? 1 : 0);
   MTGNN_CHECK_LAUNCH("colsum_final");
   return MTGNN_OK;
 }
