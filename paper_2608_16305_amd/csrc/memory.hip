@@ -614,7 +614,9 @@ size_t gru_save_bytes(const mtgnn_dims* d, int64_t max_rows) {
 }
 
 size_t gru_update_ws(const mtgnn_dims* d, int64_t max_rows) {
-  return a256(sizeof(float) * max_rows * 6 * d->d_mem) + a256(sizeof(float) * max_rows * d->d_mem);
+  const int dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
+  return a256(sizeof(float) * max_rows * 6 * d->d_mem) + a256(sizeof(float) * max_rows * d->d_mem) +
+         a256(sizeof(float) * gru_fused_weight_floats(d->d_mem, dmsg));
 }
 
 mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const int32_t* winner, const int32_t* n_rows,
@@ -635,6 +637,17 @@ mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const in
   }
   const unsigned gel = (unsigned)cdiv(max_rows * dm, 256);
   int64_t ldh = dm;
+  if (gru_fused_ok(d->dtype, dm, dmsg)) {   // both products and the gates in one kernel
+    GruWTArgs wa{};
+    if (save && gru_dx_fused_ok(d->dtype, dm, d->d_time)) {
+      const int kc = (int)cdiv(3 * dm, 16);
+      wa = GruWTArgs{(float*)((char*)save + 5 * plane), (int)(gru_dx_weight_floats(dm, d->d_time) / (16 * kc)),
+                     16 * kc, d->d_time, 3 * dm, dmsg, 2 * dm};
+    }
+    float* Wp = (float*)((char*)ws + a256(sizeof(float) * max_rows * 6 * dm) + a256(sizeof(float) * max_rows * dm));
+    return gru_fused((const float*)msg, (const float*)W_ih, (const float*)W_hh, b_ih, b_hh, uniq, winner, b->t,
+                     n_rows, max_rows, dm, dmsg, Wp, (float*)memory, lu, sr, sz, sn, sghn, wa, s);
+  }
   if (d->dtype == MTGNN_F32) {   // h = msg[:, :dm]; both products in one launch (their inputs share a type)
     h_old = (float*)msg;
     ldh = dmsg;

@@ -377,6 +377,105 @@ __global__ __launch_bounds__(64 * MW) void k_gru_dx(const float* __restrict__ dg
   });
 }
 
+// ---------------------------------------------------------------- the GRU update on the layer machinery
+
+// A block owns 16 updated rows and GRU_UNITS hidden units: the r, z and n columns of both products for
+// those units (6 x 32 = 192 output columns; the padded weight copy of group g holds the r, z, n rows of
+// its units, then 32 zero rows).  The message rows go to LDS once: the input product reads all of them,
+// the hidden product their first d_mem columns (h = M[node], the message's first slice; the padded W_hh
+// is zero past d_mem).  The six pre-activations meet in LDS and the gates are applied there.
+constexpr int GRU_UNITS = 32;
+constexpr int GRU_GROUP_ROWS = 128;   // 6 column tiles of the layer read 8 tiles' rows (16 MW NU)
+
+// The padded per-group weights (float32): Wi [groups][128][16 ki], Wh [groups][128][16 kh]; row 32 gate + u
+// of group g is unit 32 g + u of gate (r, z, n) = (0, 1, 2); rows 96..127, units past d_mem and columns past
+// the true width are zero.  Side job: the backward's padded W_ih time slice (as the unfused gate kernel).
+__global__ void k_gru_prepare(const float* __restrict__ W_ih, const float* __restrict__ W_hh, int dm, int dmsg,
+                              int ki16, int kh16, int groups, float* __restrict__ Wi, float* __restrict__ Wh,
+                              GruWTArgs wt) {
+  const int64_t e0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t ni = (int64_t)groups * GRU_GROUP_ROWS * ki16, nh = (int64_t)groups * GRU_GROUP_ROWS * kh16;
+  for (int64_t x = e0; x < ni + nh; x += stride) {
+    const bool in = x < ni;
+    const int64_t y = in ? x : x - ni;
+    const int kk = in ? ki16 : kh16;
+    const int g = (int)(y / (GRU_GROUP_ROWS * kk));
+    const int row = (int)(y / kk % GRU_GROUP_ROWS), col = (int)(y % kk);
+    const int gate = row / GRU_UNITS, unit = GRU_UNITS * g + row % GRU_UNITS;
+    const int K = in ? dmsg : dm;
+    float v = 0.f;
+    if (gate < 3 && unit < dm && col < K) v = (in ? W_ih : W_hh)[(int64_t)(gate * dm + unit) * K + col];
+    (in ? Wi : Wh)[y] = v;
+  }
+  if (wt.dst)
+    for (int64_t x = e0; x < (int64_t)wt.rows * wt.cols; x += stride) {
+      const int rr = (int)(x / wt.cols), cc = (int)(x % wt.cols);
+      wt.dst[x] = (rr < wt.dt && cc < wt.K) ? W_ih[(int64_t)cc * wt.ld + wt.col0 + rr] : 0.f;
+    }
+}
+
+template <int KI, int KH>
+__global__ __launch_bounds__(64 * MW) void k_gru_fused(const float* __restrict__ msg, int dmsg,
+                                                       const float* __restrict__ Wi, const float* __restrict__ Wh,
+                                                       const float* __restrict__ b_ih, const float* __restrict__ b_hh,
+                                                       const int32_t* __restrict__ uniq,
+                                                       const int32_t* __restrict__ winner, const float* __restrict__ t,
+                                                       const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
+                                                       float* __restrict__ mem, float* __restrict__ lu,
+                                                       float* __restrict__ sr, float* __restrict__ sz,
+                                                       float* __restrict__ sn, float* __restrict__ sghn) {
+  constexpr int XL = 16 * KI + 4;   // LDS row stride, XL / 4 odd
+  constexpr int GL = 6 * GRU_UNITS + 4;
+  __shared__ __attribute__((aligned(16))) float X[16 * XL];
+  __shared__ float G[16 * GL];
+  const int64_t M = eff_count(max_rows, n_rows);
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  if (r0 >= M) return;   // block-uniform
+  const int g = blockIdx.y;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, fr = lane & 15, fg = lane >> 4;
+  zero_cols<XL, 1>(X, dmsg, 16 * KI);
+  load_rows<XL, 1>(X, 0, msg, dmsg, dmsg, r0, M);
+  __syncthreads();
+  {
+    f32x4 ai[Tiles<6>::per_wave], ah[Tiles<6>::per_wave];
+    layer<6, KI, XL, 1>(X, Wi + (size_t)g * GRU_GROUP_ROWS * 16 * KI, ai);
+    layer<6, KH, XL, 1>(X, Wh + (size_t)g * GRU_GROUP_ROWS * 16 * KH, ah);
+#pragma unroll
+    for (int u = 0; u < Tiles<6>::per_wave; ++u) {
+      const int c = 16 * (wid + MW * u) + fr;
+      if (c >= 3 * GRU_UNITS) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        G[(4 * fg + r) * GL + c] = ai[u][r];
+        G[(4 * fg + r) * GL + 3 * GRU_UNITS + c] = ah[u][r];
+      }
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 16 * GRU_UNITS; e += 64 * MW) {
+    const int i = e / GRU_UNITS, jj = e % GRU_UNITS, j = GRU_UNITS * g + jj;
+    if (j >= dm || r0 + i >= M) continue;
+    const float* gi = G + i * GL;
+    const float* gh = gi + 3 * GRU_UNITS;
+    const float rr = sigmoidf_((gi[jj] + b_ih[j]) + (gh[jj] + b_hh[j]));
+    const float zz = sigmoidf_((gi[GRU_UNITS + jj] + b_ih[dm + j]) + (gh[GRU_UNITS + jj] + b_hh[dm + j]));
+    const float ghn = gh[2 * GRU_UNITS + jj] + b_hh[2 * dm + j];
+    const float nn = tanhf((gi[2 * GRU_UNITS + jj] + b_ih[2 * dm + j]) + rr * ghn);
+    const float h = X[i * XL + j];
+    const float hn = (1.f - zz) * nn + zz * h;
+    const int64_t row = r0 + i;
+    const int64_t node = uniq[row];
+    mem[node * dm + j] = hn;
+    if (j == 0) lu[node] = t[winner[row] >> 1];
+    if (sr) {
+      sr[row * dm + j] = rr;
+      sz[row * dm + j] = zz;
+      sn[row * dm + j] = nn;
+      sghn[row * dm + j] = ghn;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- the link-prediction decoder
 
 // One block per 16 target events (their src, dst and negative query rows of z).  Forward:
@@ -619,6 +718,50 @@ mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int
   else
     k_qproj_dx<2, 2><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
   MTGNN_CHECK_LAUNCH("qproj_dx");
+  return MTGNN_OK;
+}
+
+static bool gru_fused_shape(int dm, int dmsg, int& ki, int& kh) {
+  ki = (int)cdiv(dmsg, 16);
+  kh = (int)cdiv(dm, 16);
+  return dm % 4 == 0 && dmsg % 4 == 0 &&
+         ((ki == 19 && kh == 7) || (ki == 20 && kh == 7) || (ki == 30 && kh == 7) || (ki == 7 && kh == 2));
+}
+
+bool gru_fused_ok(int dtype, int dm, int dmsg) {
+  int ki, kh;
+  return dtype == MTGNN_F32 && gru_fused_shape(dm, dmsg, ki, kh);
+}
+
+size_t gru_fused_weight_floats(int dm, int dmsg) {
+  const int64_t groups = cdiv(dm, GRU_UNITS);
+  return (size_t)groups * GRU_GROUP_ROWS * 16 * (cdiv(dmsg, 16) + cdiv(dm, 16));
+}
+
+mtgnn_status gru_fused(const float* msg, const float* W_ih, const float* W_hh, const float* b_ih, const float* b_hh,
+                       const int32_t* uniq, const int32_t* winner, const float* t, const int32_t* n_rows,
+                       int64_t max_rows, int dm, int dmsg, float* Wp, float* mem, float* lu, float* sr, float* sz,
+                       float* sn, float* sghn, GruWTArgs wt, hipStream_t s) {
+  int ki, kh;
+  if (!gru_fused_shape(dm, dmsg, ki, kh) || !aligned16(msg)) return MTGNN_EUNSUPPORTED;
+  const int groups = (int)cdiv(dm, GRU_UNITS);
+  float* Wi = Wp;
+  float* Wh = Wp + (size_t)groups * GRU_GROUP_ROWS * 16 * ki;
+  const int64_t tot = (int64_t)groups * GRU_GROUP_ROWS * 16 * (ki + kh);
+  k_gru_prepare<<<(unsigned)std::min<int64_t>(cdiv(tot, 256), 1024), 256, 0, s>>>(W_ih, W_hh, dm, dmsg, 16 * ki,
+                                                                                   16 * kh, groups, Wi, Wh, wt);
+  MTGNN_CHECK_LAUNCH("gru_prepare");
+  if (max_rows <= 0) return MTGNN_OK;
+  const dim3 grid((unsigned)cdiv(max_rows, 16), (unsigned)groups);
+#define MTGNN_GRU_FUSED(KI_, KH_)                                                                          \
+  k_gru_fused<KI_, KH_><<<grid, 64 * MW, 0, s>>>(msg, dmsg, Wi, Wh, b_ih, b_hh, uniq, winner, t, n_rows, \
+                                                  max_rows, dm, mem, lu, sr, sz, sn, sghn)
+  if (ki == 19) MTGNN_GRU_FUSED(19, 7);
+  else if (ki == 20) MTGNN_GRU_FUSED(20, 7);
+  else if (ki == 30) MTGNN_GRU_FUSED(30, 7);
+  else MTGNN_GRU_FUSED(7, 2);
+#undef MTGNN_GRU_FUSED
+  MTGNN_CHECK_LAUNCH("gru_fused");
   return MTGNN_OK;
 }
 

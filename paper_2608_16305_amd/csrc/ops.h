@@ -57,6 +57,20 @@ mtgnn_status timegrad_rows(const float* dphi, int64_t ld, int64_t rows, const in
                            const float* sin_saved, const float* tw, const float* tb, int dt_dim, float* dw, float* db,
                            bool accumulate, void* ws, size_t ws_bytes, hipStream_t s);
 
+// The GRU update fused on the layer machinery (merge.hip), float32: both products and the gates per block
+// of 16 rows x 32 hidden units, from zero-padded per-group weight copies (Wp: gru_fused_weight_floats) that
+// the same call writes first; wt (optional) is the backward's padded W_ih time slice, written alongside.
+struct GruWTArgs {
+  float* dst;
+  int rows, cols, dt, K, ld, col0;
+};
+bool gru_fused_ok(int dtype, int dm, int dmsg);
+size_t gru_fused_weight_floats(int dm, int dmsg);
+mtgnn_status gru_fused(const float* msg, const float* W_ih, const float* W_hh, const float* b_ih, const float* b_hh,
+                       const int32_t* uniq, const int32_t* winner, const float* t, const int32_t* n_rows,
+                       int64_t max_rows, int dm, int dmsg, float* Wp, float* mem, float* lu, float* sr, float* sz,
+                       float* sn, float* sghn, GruWTArgs wt, hipStream_t s);
+
 // link-prediction decoder and the masked batch loss
 // The fused form (merge.hip) for d_attn = 100 or 32: one kernel per 16 target events for the forward, the
 // loss terms and dz, and the hidden-row gradients DA / DB for the first layer's weight gradient; then the
