@@ -107,6 +107,15 @@ __device__ __forceinline__ float cos_for_bf16(float arg) {
 }
 
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
+// Gate nonlinearities on the hardware base-2 exponential and reciprocal (about 1 ulp each):
+// sigma(x) = 1 / (1 + 2^(-x log2 e)),  tanh(x) = 1 - 2 / (1 + 2^(2 x log2 e)).  Both saturate correctly
+// (2^(+large) = inf, 1 / inf = 0); tanh's absolute error stays near 1e-7 around zero.
+__device__ __forceinline__ float sigmoid_hw(float x) {
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
+}
+__device__ __forceinline__ float tanh_hw(float x) {
+  return 1.f - 2.f * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(2.8853900817779268f * x));
+}
 
 // Wave-level reductions (wave64).
 __device__ __forceinline__ float wave_sum(float v) {

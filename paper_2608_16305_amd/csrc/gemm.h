@@ -34,6 +34,7 @@ struct Generic { static constexpr const char* name = "gemm"; };
 struct KvProj { static constexpr const char* name = "gemm_kv_proj"; };    // K, V = kv_in W^T + b (neighbour slots)
 struct KvDw { static constexpr const char* name = "gemm_kv_dw"; };        // dW_k, dW_v (+ db) over neighbour slots
 struct KvDx { static constexpr const char* name = "gemm_kv_dx"; };        // dphi = dK W_k,t + dV W_v,t
+struct GruDw { static constexpr const char* name = "gemm_gru_dw"; };      // dW_ih, dW_hh (+ biases) over updated rows
 }  // namespace site
 
 struct GemmArgs {
@@ -52,6 +53,8 @@ struct GemmArgs {
   float* C2;
   int64_t ldc2;
   int64_t kchunk;              // split-K chunk (blockIdx.z covers [z*kchunk, (z+1)*kchunk))
+  int ksplit_dev = 0;          // > 0: split z covers the z-th of ksplit_dev equal chunks (multiples of 16) of the
+                               // device count K_dev instead (every split holds rows whatever the count)
   int64_t c_split_stride;      // element offset of split z's output
   const float* gate;           // optional: result *= (gate(i,j) > 0)  (ReLU backward)
   int64_t ldgate;
@@ -381,8 +384,9 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, const TileCoord tc)
   const int64_t row0 = tc.x * BM;
   const int64_t col0 = tc.y * BN;
   if (row0 >= M) return;
-  const int64_t kbeg = tc.z * g.kchunk;
-  const int64_t kend = min(Kall, kbeg + g.kchunk);
+  const int64_t kchunk = g.ksplit_dev > 0 ? cdiv(cdiv(Kall, g.ksplit_dev), 16) * 16 : g.kchunk;
+  const int64_t kbeg = tc.z * kchunk;
+  const int64_t kend = min(Kall, kbeg + kchunk);
 
   const TA* A = (const TA*)g.A;
   const TB* B = (const TB*)g.B;
@@ -540,7 +544,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gemm_batch(GemmBatch b) {
   tc.x = blockIdx.x;
   tc.y = blockIdx.y;
   tc.z = blockIdx.z % (uint32_t)b.zper;
-  if (tc.y * BN >= g.N || tc.z * g.kchunk >= g.K) return;
+  if (tc.y * BN >= g.N || (g.ksplit_dev == 0 && tc.z * g.kchunk >= g.K)) return;
   gemm_body<Site, BN, WM, BK, NBUF, VEC, TA, TB, A_KCONTIG, B_KCONTIG>(g, tc);
 }
 
@@ -576,8 +580,14 @@ struct DwPlan {
   int ksplit;
   int64_t kchunk;
   int bn, bk;
+  int ksplit_dev = 0;   // > 0: the splits cut the device row count (GemmArgs::ksplit_dev)
 };
 DwPlan dw_plan(int64_t R, int64_t N, int64_t K);
+// With a device row count, `tiles` output tiles per split: the splits cut the device count into
+// equal chunks, so every split holds rows, with about DW_DEV_BLOCKS blocks in all and never more
+// splits than the host plan (whose workspace then suffices).
+constexpr int64_t DW_DEV_BLOCKS = 512;
+DwPlan dw_plan_dev(DwPlan host, int64_t tiles);
 
 // A 4-wide load along the contiguous dimension is aligned when the base and the other stride are.
 inline bool vec_ok(const void* p, int64_t other_stride, size_t esz) {
@@ -835,12 +845,14 @@ mtgnn_status linear_dw(const float* dy, int64_t lddy, const void* x, int x_dtype
       return dw_rs_launch(dy, lddy, (int)N, (const float*)x, ldx, (int)K, R, R_dev, dW, lddw, db, ws, ws_bytes, s);
   }
   const int64_t Kc = db ? K + 1 : K;   // extra all-ones column of x gives the bias gradient
-  const DwPlan plan = dw_plan(R, N, Kc);
+  DwPlan plan = dw_plan(R, N, Kc);
+  if (R_dev) plan = dw_plan_dev(plan, cdiv(N, 64 * G_WM) * cdiv(Kc, plan.bn));
   const int ksplit = plan.ksplit;
   const int64_t kchunk = plan.kchunk;
   GemmArgs g{};
   g.tile_bn = plan.bn;
   g.tile_bk = plan.bk;
+  g.ksplit_dev = plan.ksplit_dev;
   g.M = N; g.N = Kc; g.K = R; g.K_dev = R_dev;
   if (db) { g.ones_col = K; g.col_out = db; }
   g.A = dy; g.a_si = 1; g.a_sk = lddy;
@@ -903,8 +915,9 @@ struct DwOsProblem {
   float* part;
   int nx, ny, b_begin, nblk;
 };
+constexpr int DW_OS_MAXP = 16;   // problems (or output tiles) per launch
 struct DwOsBatch {
-  DwOsProblem p[G_MAXBATCH];
+  DwOsProblem p[DW_OS_MAXP];
   int n;
   int64_t R;
   const int32_t* R_dev;
@@ -912,6 +925,31 @@ struct DwOsBatch {
 constexpr int DW_OS_MAX_BLOCKS = 256;
 mtgnn_status dw_os_launch(const DwOsBatch& b, int grid, hipStream_t s);
 int dw_os_cu_count();
+
+// A weight gradient cut into output tiles for the output-stationary kernel: tile t is
+// dW_t[nx, ny] = X_t^T Y_t and, if db, db_t[nx] = column sums of X_t, over the R rows (clamped by R_dev);
+// X_t, Y_t start at the tile's first column (row strides ldx, ldy; 16-byte aligned, strides multiples of
+// 4), nx and ny multiples of 4 with nx <= 112 and ny <= 108.  Rows i < dup_rows of the tile's output are
+// also written to dup (row stride lddup; if not null) and, with db, their sums to dup_db (if not null):
+// a product that another weight shares.
+struct DwTile {
+  const float* X;
+  int64_t ldx;
+  const float* Y;
+  int64_t ldy;
+  int nx, ny;
+  float* dW;
+  int64_t lddw;
+  float* db;
+  float* dup;
+  int64_t lddup;
+  int dup_rows;
+  float* dup_db;
+};
+size_t dw_tiles_ws_bytes(const DwTile* t, int n);
+mtgnn_status dw_tiles(const DwTile* t, int n, int64_t R, const int32_t* R_dev, void* ws, size_t ws_bytes,
+                      hipStream_t s);
+template <class Site = site::Generic>
 mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_t* R_dev, int x_dtype, void* ws,
                              size_t ws_bytes, hipStream_t s);
 

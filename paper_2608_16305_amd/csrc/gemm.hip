@@ -6,31 +6,43 @@ namespace mtgnn {
 namespace {
 
 // 64 outputs per block; the 4 waves sum interleaved split slices, combined in a fixed order.
+// The partials are [nsplit][rows][ldp] (ldp 0: cols); rows i < dup_rows are also written to dup / dup_col.
 __device__ __forceinline__ void splitk_reduce_body(const float* __restrict__ part, int64_t split_stride, int nsplit,
                                                    int64_t rows, int64_t cols, float* __restrict__ out, int64_t ldo,
                                                    int64_t ones_col, float* __restrict__ col_out,
                                                    float* __restrict__ out_hi = nullptr,
-                                                   float* __restrict__ col_out_hi = nullptr, int64_t row_split = 0) {
+                                                   float* __restrict__ col_out_hi = nullptr, int64_t row_split = 0,
+                                                   int64_t ldp = 0, float* __restrict__ dup = nullptr,
+                                                   int64_t lddup = 0, int64_t dup_rows = 0,
+                                                   float* __restrict__ dup_col = nullptr) {
   __shared__ float red[4][64];
   const int64_t e = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
   const int g = threadIdx.x >> 6;
+  int64_t i = e / cols;
+  const int64_t j = e % cols;
+  const int64_t pe = ldp > 0 ? i * ldp + j : e;
   float s = 0.f;
   if (e < rows * cols) {
     int z = g;
     for (; z + 12 < nsplit; z += 16) {   // four loads in flight
-      const float a0 = part[(int64_t)z * split_stride + e], a1 = part[(int64_t)(z + 4) * split_stride + e];
-      const float a2 = part[(int64_t)(z + 8) * split_stride + e], a3 = part[(int64_t)(z + 12) * split_stride + e];
+      const float a0 = part[(int64_t)z * split_stride + pe], a1 = part[(int64_t)(z + 4) * split_stride + pe];
+      const float a2 = part[(int64_t)(z + 8) * split_stride + pe], a3 = part[(int64_t)(z + 12) * split_stride + pe];
       s += ((a0 + a1) + a2) + a3;
     }
-    for (; z < nsplit; z += 4) s += part[(int64_t)z * split_stride + e];
+    for (; z < nsplit; z += 4) s += part[(int64_t)z * split_stride + pe];
   }
   red[g][threadIdx.x & 63] = s;
   __syncthreads();
   if (g != 0 || e >= rows * cols) return;
   const int l = threadIdx.x;
   s = ((red[0][l] + red[1][l]) + red[2][l]) + red[3][l];
-  int64_t i = e / cols;
-  const int64_t j = e % cols;
+  if (i < dup_rows) {
+    if (j == ones_col) {
+      if (dup_col) dup_col[i] = s;
+    } else if (dup) {
+      dup[i * lddup + j] = s;
+    }
+  }
   if (out_hi && i >= row_split) {   // rows from row_split on go to the second output pair
     i -= row_split;
     out = out_hi;
@@ -49,9 +61,13 @@ struct ReduceProblem {
   int64_t ldo;
   int64_t ones_col;
   float* col_out;
+  int64_t ldp = 0;
+  float* dup = nullptr;
+  int64_t lddup = 0, dup_rows = 0;
+  float* dup_col = nullptr;
 };
 struct ReduceBatch {
-  ReduceProblem p[G_MAXBATCH];
+  ReduceProblem p[DW_OS_MAXP];
   int n;
 };
 
@@ -60,7 +76,8 @@ __global__ __launch_bounds__(256) void k_splitk_reduce_batch(ReduceBatch b) {
   if ((int)blockIdx.y >= b.n) return;
   const ReduceProblem& q = b.p[blockIdx.y];
   if ((int64_t)blockIdx.x * 64 >= q.rows * q.cols) return;
-  splitk_reduce_body(q.part, q.split_stride, q.nsplit, q.rows, q.cols, q.out, q.ldo, q.ones_col, q.col_out);
+  splitk_reduce_body(q.part, q.split_stride, q.nsplit, q.rows, q.cols, q.out, q.ldo, q.ones_col, q.col_out, nullptr,
+                     nullptr, 0, q.ldp, q.dup, q.lddup, q.dup_rows, q.dup_col);
 }
 
 }  // namespace
@@ -124,6 +141,14 @@ DwPlan dw_plan(int64_t R, int64_t N, int64_t K) {
   p.ksplit = (int)cdiv(r, p.kchunk);
   if (p.ksplit == 1) p.kchunk = r;
   return p;
+}
+
+DwPlan dw_plan_dev(DwPlan host, int64_t tiles) {
+  if (host.ksplit <= 1) return host;
+  const int64_t want = cdiv(DW_DEV_BLOCKS, tiles < 1 ? 1 : tiles);
+  host.ksplit = (int)(want < 1 ? 1 : want > host.ksplit ? host.ksplit : want);
+  host.ksplit_dev = host.ksplit;
+  return host;
 }
 
 // ---------------------------------------------------------------- batched products
@@ -202,6 +227,7 @@ size_t linear_dw_batch_ws_bytes(int64_t R, const int64_t* N, const int64_t* K, i
   return b;
 }
 
+template <class Site>
 mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_t* R_dev, int x_dtype, void* ws,
                              size_t ws_bytes, hipStream_t s) {
   if (n < 1 || n > G_MAXBATCH) return MTGNN_EINVAL;
@@ -241,7 +267,12 @@ mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_
     MTGNN_CHECK_LAUNCH("splitk_reduce_batch");
     return MTGNN_OK;
   }
-  const DwPlan plan = dw_batch_plan(R, Ns, Ks, n);
+  DwPlan plan = dw_batch_plan(R, Ns, Ks, n);
+  if (R_dev) {
+    int64_t tiles = 0;
+    for (int i = 0; i < n; ++i) tiles += cdiv(Ns[i], 64 * G_WM) * cdiv(ps[i].db ? Ks[i] + 1 : Ks[i], plan.bn);
+    plan = dw_plan_dev(plan, tiles);
+  }
   GemmArgs gs[G_MAXBATCH];
   ReduceBatch rb{};
   rb.n = n;
@@ -256,6 +287,7 @@ mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_
     g.A = q.dy; g.a_si = 1; g.a_sk = q.lddy;
     g.B = q.x; g.b_sk = q.ldx; g.b_sj = 1;
     g.kchunk = plan.kchunk;
+    g.ksplit_dev = plan.ksplit_dev;
     g.tile_bn = plan.bn;
     g.tile_bk = plan.bk;
     if (plan.ksplit == 1) {
@@ -268,13 +300,94 @@ mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_
     }
     gs[i] = g;
   }
-  MTGNN_TRY((gemm_batch_launch<site::Generic, false, false>(gs, n, plan.ksplit, MTGNN_F32, x_dtype, s)));
+  MTGNN_TRY((gemm_batch_launch<Site, false, false>(gs, n, plan.ksplit, MTGNN_F32, x_dtype, s)));
   if (plan.ksplit > 1) {
     k_splitk_reduce_batch<<<dim3((unsigned)cdiv(max_out, 64), (unsigned)n), 256, 0, s>>>(rb);
     MTGNN_CHECK_LAUNCH("splitk_reduce_batch");
   }
   return MTGNN_OK;
 }
+
+// Blocks per tile: the launch's blocks (one per CU, at most DW_OS_MAX_BLOCKS) in proportion to each
+// tile's MFMAs per row chunk (7 x 2 or 7 x 4 tiles a wave), at least one each.
+static int dw_tiles_split(const DwTile* t, int n, int* nblk) {
+  int64_t K[DW_OS_MAXP];
+  for (int i = 0; i < n; ++i) K[i] = t[i].ny;
+  const int total = std::max(std::min(dw_os_cu_count(), DW_OS_MAX_BLOCKS), n);
+  int w[DW_OS_MAXP], sum = 0;
+  for (int i = 0; i < n; ++i) sum += (w[i] = cdiv(K[i] + 1, 16) <= 7 ? 2 : 4);
+  int used = 0;
+  for (int i = 0; i < n; ++i) used += (nblk[i] = std::max(1, (int)((int64_t)total * w[i] / sum)));
+  return used;
+}
+
+static bool dw_tiles_shapes_ok(const DwTile* t, int n) {
+  if (n < 1 || n > DW_OS_MAXP) return false;
+  for (int i = 0; i < n; ++i) {
+    const DwTile& q = t[i];
+    if (q.nx < 4 || q.nx > 112 || q.nx % 4 || q.ny < 4 || q.ny > 108 || q.ny % 4) return false;
+  }
+  return true;
+}
+
+static bool dw_tiles_ok(const DwTile* t, int n) {
+  if (!dw_tiles_shapes_ok(t, n)) return false;
+  for (int i = 0; i < n; ++i) {
+    const DwTile& q = t[i];
+    if (!vec_ok(q.X, q.ldx, 4) || !vec_ok(q.Y, q.ldy, 4) || (q.dup_rows > 0 && !q.dup && !q.dup_db)) return false;
+  }
+  return true;
+}
+
+size_t dw_tiles_ws_bytes(const DwTile* t, int n) {   // depends on the shapes only
+  if (!dw_tiles_shapes_ok(t, n)) return 0;
+  int nblk[DW_OS_MAXP];
+  dw_tiles_split(t, n, nblk);
+  size_t b = 0;
+  for (int i = 0; i < n; ++i) b += (sizeof(float) * (size_t)nblk[i] * t[i].nx * (t[i].ny + 1) + 255) & ~size_t(255);
+  return b;
+}
+
+mtgnn_status dw_tiles(const DwTile* t, int n, int64_t R, const int32_t* R_dev, void* ws, size_t ws_bytes,
+                      hipStream_t s) {
+  if (!dw_tiles_ok(t, n) || dw_os_cu_count() <= 0) return MTGNN_EUNSUPPORTED;
+  if (ws_bytes < dw_tiles_ws_bytes(t, n)) return MTGNN_EWORKSPACE;
+  int nblk[DW_OS_MAXP];
+  dw_tiles_split(t, n, nblk);
+  DwOsBatch b{};
+  ReduceBatch rb{};
+  b.n = rb.n = n;
+  b.R = R < 0 ? 0 : R;
+  b.R_dev = R_dev;
+  char* w = (char*)ws;
+  int64_t max_out = 1;
+  int begin = 0;
+  for (int i = 0; i < n; ++i) {
+    const DwTile& q = t[i];
+    const int64_t per = (int64_t)q.nx * (q.ny + 1);
+    b.p[i] = DwOsProblem{q.X, q.ldx, q.Y, q.ldy, (float*)w, q.nx, q.ny, begin, nblk[i]};
+    ReduceProblem rp{(const float*)w, per, nblk[i], q.nx, q.db ? q.ny + 1 : q.ny, q.dW, q.lddw, q.db ? q.ny : -1,
+                     q.db};
+    rp.ldp = q.ny + 1;
+    rp.dup = q.dup;
+    rp.lddup = q.lddup;
+    rp.dup_rows = q.dup_rows;
+    rp.dup_col = q.dup_db;
+    rb.p[i] = rp;
+    w += (sizeof(float) * (size_t)nblk[i] * per + 255) & ~size_t(255);
+    begin += nblk[i];
+    max_out = std::max(max_out, per);
+  }
+  MTGNN_TRY(dw_os_launch(b, begin, s));
+  k_splitk_reduce_batch<<<dim3((unsigned)cdiv(max_out, 64), (unsigned)n), 256, 0, s>>>(rb);
+  MTGNN_CHECK_LAUNCH("splitk_reduce_batch");
+  return MTGNN_OK;
+}
+
+template mtgnn_status linear_dw_batch<site::Generic>(const DwProblem*, int, int64_t, const int32_t*, int, void*, size_t,
+                                                     hipStream_t);
+template mtgnn_status linear_dw_batch<site::GruDw>(const DwProblem*, int, int64_t, const int32_t*, int, void*, size_t,
+                                                   hipStream_t);
 
 size_t dw_rs_ws_bytes(int nx, int ny);
 

@@ -574,10 +574,11 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_os(DwOsBatch b) {
   constexpr int SLOT_MAX = 16 * (rs::dw_stride(7) + rs::dw_stride(13));
   __shared__ __attribute__((aligned(16))) float lds[DW_OS_SLOTS * SLOT_MAX];
   const int bx = blockIdx.x;
-  const DwOsProblem q = (b.n > 3 && bx >= b.p[3].b_begin)   ? b.p[3]
-                        : (b.n > 2 && bx >= b.p[2].b_begin) ? b.p[2]
-                        : (b.n > 1 && bx >= b.p[1].b_begin) ? b.p[1]
-                                                            : b.p[0];
+  int pi = 0;   // the problems' block ranges ascend
+#pragma unroll
+  for (int k = 1; k < DW_OS_MAXP; ++k)
+    if (k < b.n && bx >= b.p[k].b_begin) pi = k;
+  const DwOsProblem q = b.p[pi];
   const int64_t rows = eff_count(b.R, b.R_dev);
   if (q.ny + 1 <= 16 * 7) dw_os_body<7, 7>(q, rows, bx - q.b_begin, lds);
   else dw_os_body<7, 13>(q, rows, bx - q.b_begin, lds);

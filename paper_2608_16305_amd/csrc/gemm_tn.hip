@@ -17,5 +17,6 @@ template mtgnn_status gemm_launch<site::Generic, false, false>(const GemmArgs&, 
 template mtgnn_status gemm_launch<site::KvDw, false, false>(const GemmArgs&, int, int, int, hipStream_t);
 
 template mtgnn_status gemm_batch_launch<site::Generic, false, false>(const GemmArgs*, int, int, int, int, hipStream_t);
+template mtgnn_status gemm_batch_launch<site::GruDw, false, false>(const GemmArgs*, int, int, int, int, hipStream_t);
 
 }  // namespace mtgnn

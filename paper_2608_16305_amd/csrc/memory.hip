@@ -678,6 +678,58 @@ mtgnn_status gru_update_impl(const mtgnn_batch* b, const int32_t* uniq, const in
   return MTGNN_OK;
 }
 
+// The float32 GRU weight gradients as output tiles (dw_tiles).  The reset and update gates' hidden
+// products equal their input products over the message's first d_mem columns (h is that slice and both
+// products see the same pre-activation gradient), so dW_hh's r, z rows and db_hh's r, z entries are
+// copies of dW_ih's and db_ih's: only the candidate's hidden product is computed apart.
+//   dW_ih = dgi^T [msg | 1]: column tiles of the 3 d_mem gradient columns (<= 112 wide) times column tiles
+//   of the message ([0, d_mem), then <= 108 wide); dW_hh,n = dgh_n^T [h | 1].
+// Returns the tile count, 0 if the shape does not fit.
+static int gru_dw_tiles(const float* dgi, const float* dgh, const float* msg, int dm, int dmsg, float* dW_ih,
+                        float* dW_hh, float* db_ih, float* db_hh, DwTile* t) {
+  if (dm % 4 || dmsg % 4 || dm > 108 || dmsg <= dm) return 0;
+  const int nxt = (int)cdiv(3 * dm, 112), wx = (int)cdiv(cdiv(3 * dm, nxt), 4) * 4;
+  const int nyt = (int)cdiv(dmsg - dm, 108), wy = (int)cdiv(cdiv(dmsg - dm, nyt), 4) * 4;
+  if (nxt * (nyt + 1) + 1 > DW_OS_MAXP) return 0;
+  int n = 0;
+  for (int x0 = 0; x0 < 3 * dm; x0 += wx) {
+    const int nx = std::min(wx, 3 * dm - x0);
+    const int shared = std::max(0, std::min(nx, 2 * dm - x0));   // reset and update rows of this tile
+    for (int y0 = 0; y0 < dmsg; y0 = y0 == 0 ? dm : y0 + wy) {
+      const int ny = y0 == 0 ? dm : std::min(wy, dmsg - y0);
+      const bool last = y0 + ny == dmsg;
+      DwTile q{};
+      q.X = dgi + x0;
+      q.ldx = 3 * dm;
+      q.Y = msg + y0;
+      q.ldy = dmsg;
+      q.nx = nx;
+      q.ny = ny;
+      q.dW = dW_ih + (int64_t)x0 * dmsg + y0;
+      q.lddw = dmsg;
+      q.db = last ? db_ih + x0 : nullptr;
+      if (shared > 0 && (y0 == 0 || last)) {
+        q.dup = y0 == 0 ? dW_hh + (int64_t)x0 * dm : nullptr;
+        q.lddup = dm;
+        q.dup_rows = shared;
+        q.dup_db = last ? db_hh + x0 : nullptr;
+      }
+      t[n++] = q;
+    }
+  }
+  DwTile q{};
+  q.X = dgh + 2 * dm;
+  q.ldx = 3 * dm;
+  q.Y = msg;
+  q.ldy = dmsg;
+  q.nx = q.ny = dm;
+  q.dW = dW_hh + (int64_t)2 * dm * dm;
+  q.lddw = dm;
+  q.db = db_hh + 2 * dm;
+  t[n++] = q;
+  return n;
+}
+
 size_t gru_update_bwd_ws(const mtgnn_dims* d, int64_t max_rows) {
   const int dm = d->d_mem, dmsg = 2 * d->d_mem + d->d_time + d->d_edge;
   size_t dw = linear_dw_ws_bytes(max_rows, 3 * dm, dmsg);
@@ -686,6 +738,11 @@ size_t gru_update_bwd_ws(const mtgnn_dims* d, int64_t max_rows) {
   size_t dwb = linear_dw_batch_ws_bytes(max_rows, Ns, Ks, 2);
   size_t m = dw > dw2 ? dw : dw2;
   m = m > dwb ? m : dwb;
+  DwTile t[DW_OS_MAXP];
+  const float* base = nullptr;   // tile offsets only: the sizes do not depend on the buffers
+  const int nt = d->dtype == MTGNN_F32 ? gru_dw_tiles(base, base, base, dm, dmsg, nullptr, nullptr, nullptr,
+                                                      nullptr, t) : 0;
+  if (nt) m = std::max(m, dw_tiles_ws_bytes(t, nt));
   return 2 * a256(sizeof(float) * max_rows * 3 * dm) + a256(m);
 }
 
@@ -712,11 +769,20 @@ mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const voi
   k_gru_bwd_gates<<<(unsigned)cdiv(max_rows * dm, 256), 256, 0, s>>>(d_mem, h_old, ldh, sr, sz, sn, sghn, n_rows,
                                                                         max_rows, dm, dgi, dgh);
   MTGNN_CHECK_LAUNCH("gru_bwd_gates");
-  if (d->dtype == MTGNN_F32) {   // both weight gradients in one launch
+  DwTile tiles[DW_OS_MAXP];
+  const int nt = d->dtype == MTGNN_F32 ? gru_dw_tiles(dgi, dgh, (const float*)msg, dm, dmsg, dW_ih, dW_hh, db_ih,
+                                                      db_hh, tiles) : 0;
+  mtgnn_status st = MTGNN_EUNSUPPORTED;
+  if (nt) {   // one output-stationary launch and one reduce (unsupported: misaligned operands)
+    TimedScope ts(site::GruDw::name, s);
+    st = dw_tiles(tiles, nt, max_rows, n_rows, w, rest, s);
+    if (st != MTGNN_OK && st != MTGNN_EUNSUPPORTED) return st;
+  }
+  if (st != MTGNN_OK && d->dtype == MTGNN_F32) {   // both weight gradients in one launch
     const DwProblem ps[2] = {{dgi, 3 * dm, msg, dmsg, dW_ih, dmsg, 3 * dm, dmsg, db_ih},
                              {dgh, 3 * dm, h_old, ldh, dW_hh, dm, 3 * dm, dm, db_hh}};
-    MTGNN_TRY(linear_dw_batch(ps, 2, max_rows, n_rows, MTGNN_F32, w, rest, s));
-  } else {
+    MTGNN_TRY(linear_dw_batch<site::GruDw>(ps, 2, max_rows, n_rows, MTGNN_F32, w, rest, s));
+  } else if (st != MTGNN_OK) {
     MTGNN_TRY(linear_dw(dgi, 3 * dm, msg, d->dtype, dmsg, dW_ih, dmsg, max_rows, n_rows, 3 * dm, dmsg, w, rest, s,
                         db_ih));
     MTGNN_TRY(linear_dw(dgh, 3 * dm, h_old, MTGNN_F32, dm, dW_hh, dm, max_rows, n_rows, 3 * dm, dm, w, rest, s,

@@ -73,21 +73,32 @@ __device__ __forceinline__ void layer(const float* X, const float* __restrict__ 
 }
 
 // rows r0 .. r0 + 16 RT - 1 (those < M) of a row-major [M, n] matrix into an LDS tile at column offset col0
-template <int XSS = XS, int RT = 1>
+// (n <= XSS - col0).  Every load of a thread is issued before its first LDS store, so the tile costs one
+// memory latency, not one per 64 MW elements.
+template <int XSS = XS, int RT = 1, int NTH = 64 * MW>
 __device__ __forceinline__ void load_rows(float* X, int col0, const float* __restrict__ src, int64_t ld, int n,
                                           int64_t r0, int64_t M) {
-  const int nq = n / 4;
-  for (int e = threadIdx.x; e < 16 * RT * nq; e += 64 * MW) {
+  constexpr int PER = (16 * RT * (XSS / 4) + NTH - 1) / NTH;
+  const int nq = n / 4, tot = 16 * RT * nq;
+  if (nq <= 0) return;
+  float4 v[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = threadIdx.x + NTH * k;
     const int r = e / nq, q = e % nq;
-    const float4 v = r0 + r < M ? *reinterpret_cast<const float4*>(src + (r0 + r) * ld + 4 * q)
-                                : float4{0.f, 0.f, 0.f, 0.f};
-    *reinterpret_cast<float4*>(X + r * XSS + col0 + 4 * q) = v;
+    v[k] = e < tot && r0 + r < M ? *reinterpret_cast<const float4*>(src + (r0 + r) * ld + 4 * q)
+                                 : float4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = threadIdx.x + NTH * k;
+    if (e < tot) *reinterpret_cast<float4*>(X + (e / nq) * XSS + col0 + 4 * (e % nq)) = v[k];
   }
 }
 
-template <int XSS = XS, int RT = 1>
+template <int XSS = XS, int RT = 1, int NTH = 64 * MW>
 __device__ __forceinline__ void zero_cols(float* X, int c0, int c1) {
-  for (int e = threadIdx.x; e < 16 * RT * (c1 - c0); e += 64 * MW)
+  for (int e = threadIdx.x; e < 16 * RT * (c1 - c0); e += NTH)
     X[(e / (c1 - c0)) * XSS + c0 + e % (c1 - c0)] = 0.f;
 }
 
@@ -379,33 +390,106 @@ __global__ __launch_bounds__(64 * MW) void k_gru_dx(const float* __restrict__ dg
 
 // ---------------------------------------------------------------- the GRU update on the layer machinery
 
-// A block owns 16 updated rows and GRU_UNITS hidden units: the r, z and n columns of both products for
-// those units (6 x 32 = 192 output columns; the padded weight copy of group g holds the r, z, n rows of
-// its units, then 32 zero rows).  The message rows go to LDS once: the input product reads all of them,
-// the hidden product their first d_mem columns (h = M[node], the message's first slice; the padded W_hh
-// is zero past d_mem).  The six pre-activations meet in LDS and the gates are applied there.
-constexpr int GRU_UNITS = 32;
-constexpr int GRU_GROUP_ROWS = 128;   // 6 column tiles of the layer read 8 tiles' rows (16 MW NU)
+// h is the message's first d_mem columns (h = M[node], the first slice of the message), so the reset and
+// update gates' two products fold into one: W_ih,g x + W_hh,g h = (W_ih,g + [W_hh,g | 0]) x for g = r, z.
+// Only the candidate gate keeps its hidden product apart (the reset gate multiplies it).
+//
+// A block owns 16 RT updated rows and U hidden units (unit group blockIdx.y).  Its output columns, packed
+// in 16-wide tiles: TI tiles of the input product (the folded r columns, the folded z columns, the
+// candidate's input columns: 3 U, zero-padded) over the KI message chunks, then TH tiles of the candidate's
+// hidden product (U columns) over the KH chunks of h.  Job j (tile j of the TI + TH) goes to a wave in snake
+// order (round j / NW left to right, the next round right to left), which balances the long input tiles
+// against the short hidden ones; round q of a wave accumulates in acc[q].  The pre-activations meet in LDS
+// and the gates are applied there.
+constexpr int GRU_NW = 4;   // waves per block (eight measured no faster)
+template <int NW>
+struct GruJobs {
+  static constexpr int job(int round, int wave) { return round * NW + ((round & 1) ? NW - 1 - wave : wave); }
+};
 
-// The padded per-group weights (float32): Wi [groups][128][16 ki], Wh [groups][128][16 kh]; row 32 gate + u
-// of group g is unit 32 g + u of gate (r, z, n) = (0, 1, 2); rows 96..127, units past d_mem and columns past
-// the true width are zero.  Side job: the backward's padded W_ih time slice (as the unfused gate kernel).
+// acc[q][r] += X (row tile r) B^T over the KC chunks, for the rounds q whose job lies in [JB, JE); the
+// job's tile is tile (job - JB) of B, stored fragment-major: [JE - JB][KC][64 lanes][4] (fragment-major
+// copy of a zero-padded [16 (JE - JB)][16 KC] matrix: lane l of chunk c holds row 16 t + l % 16, columns
+// 16 c + 4 (l / 16) .. + 3).  The wave W is a template
+// argument, so the rounds a wave skips cost no branch in the chunk loop (a branch there would make every
+// chunk wait for all loads in flight, the prefetched ones included).
+// `pre` runs once the first chunks' weight loads are in flight (the block's tile load, so that the two
+// latencies overlap).
+template <int NW, int NR, int KC, int XSS, int RT, int W, int JB, int JE, class Pre>
+__device__ __forceinline__ void gru_jobs(const float* X, const float* __restrict__ B, f32x4 (&acc)[NR][RT], Pre pre) {
+  const int lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  const float* Bl[NR];
+#pragma unroll
+  for (int q = 0; q < NR; ++q) {
+    const int j = GruJobs<NW>::job(q, W);
+    Bl[q] = B + (size_t)(j >= JB && j < JE ? j - JB : 0) * KC * 256 + 4 * lane;
+  }
+  float4 bf[KC][NR];
+  auto load_b = [&](int c) {   // one contiguous 1 KB fragment per wave and tile
+#pragma unroll
+    for (int q = 0; q < NR; ++q)
+      if (GruJobs<NW>::job(q, W) >= JB && GruJobs<NW>::job(q, W) < JE)
+        bf[c][q] = *reinterpret_cast<const float4*>(Bl[q] + 256 * c);
+  };
+#pragma unroll
+  for (int c = 0; c < PD && c < KC; ++c) load_b(c);
+  pre();
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    if (c + PD < KC) load_b(c + PD);
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const float4 a = *reinterpret_cast<const float4*>(X + (16 * r + fr) * XSS + 16 * c + 4 * fg);
+#pragma unroll
+      for (int q = 0; q < NR; ++q) {
+        if (!(GruJobs<NW>::job(q, W) >= JB && GruJobs<NW>::job(q, W) < JE)) continue;
+        f32x4& d = acc[q][r];
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, bf[c][q].x, d, 0, 0, 0);
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, bf[c][q].y, d, 0, 0, 0);
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, bf[c][q].z, d, 0, 0, 0);
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, bf[c][q].w, d, 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// The padded per-group weights (float32, fragment-major as gru_jobs reads them): Wi [S][16 TI][16 KI],
+// Wh [S][16 TH][16 KH].  Row t of group g's
+// Wi: t < U the folded reset row of unit g U + t, then U folded update rows, then U candidate input rows;
+// row t < U of Wh: the candidate hidden row of unit g U + t.  Rows past those, units past d_mem and columns
+// past the true width are zero.  Side job: the backward's padded W_ih time slice.
+struct GruShape {
+  int S, U, ti, th;
+};
 __global__ void k_gru_prepare(const float* __restrict__ W_ih, const float* __restrict__ W_hh, int dm, int dmsg,
-                              int ki16, int kh16, int groups, float* __restrict__ Wi, float* __restrict__ Wh,
+                              int ki16, int kh16, GruShape sh, float* __restrict__ Wi, float* __restrict__ Wh,
                               GruWTArgs wt) {
   const int64_t e0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t ni = (int64_t)groups * GRU_GROUP_ROWS * ki16, nh = (int64_t)groups * GRU_GROUP_ROWS * kh16;
+  const int64_t ni = (int64_t)sh.S * 16 * sh.ti * ki16, nh = (int64_t)sh.S * 16 * sh.th * kh16;
   for (int64_t x = e0; x < ni + nh; x += stride) {
-    const bool in = x < ni;
-    const int64_t y = in ? x : x - ni;
-    const int kk = in ? ki16 : kh16;
-    const int g = (int)(y / (GRU_GROUP_ROWS * kk));
-    const int row = (int)(y / kk % GRU_GROUP_ROWS), col = (int)(y % kk);
-    const int gate = row / GRU_UNITS, unit = GRU_UNITS * g + row % GRU_UNITS;
-    const int K = in ? dmsg : dm;
     float v = 0.f;
-    if (gate < 3 && unit < dm && col < K) v = (in ? W_ih : W_hh)[(int64_t)(gate * dm + unit) * K + col];
-    (in ? Wi : Wh)[y] = v;
+    if (x < ni) {   // x = ((g ti + tile) KI + chunk) 256 + 4 lane + e
+      const int rows = 16 * sh.ti;
+      const int g = (int)(x / ((int64_t)rows * ki16)), w = (int)(x % ((int64_t)rows * ki16));
+      const int tile = w / (16 * ki16), c = w / 256 % (ki16 / 16), l = w / 4 % 64, e = w % 4;
+      const int t = 16 * tile + l % 16, col = 16 * c + 4 * (l / 16) + e;
+      const int gate = t / sh.U, unit = sh.U * g + t % sh.U;
+      if (gate < 3 && unit < dm && col < dmsg) {
+        v = W_ih[(int64_t)(gate * dm + unit) * dmsg + col];
+        if (gate < 2 && col < dm) v += W_hh[(int64_t)(gate * dm + unit) * dm + col];
+      }
+      Wi[x] = v;
+    } else {
+      const int64_t y = x - ni;
+      const int rows = 16 * sh.th;
+      const int g = (int)(y / ((int64_t)rows * kh16)), w = (int)(y % ((int64_t)rows * kh16));
+      const int tile = w / (16 * kh16), c = w / 256 % (kh16 / 16), l = w / 4 % 64, e = w % 4;
+      const int t = 16 * tile + l % 16, col = 16 * c + 4 * (l / 16) + e;
+      const int unit = sh.U * g + t;
+      if (t < sh.U && unit < dm && col < dm) v = W_hh[(int64_t)(2 * dm + unit) * dm + col];
+      Wh[y] = v;
+    }
   }
   if (wt.dst)
     for (int64_t x = e0; x < (int64_t)wt.rows * wt.cols; x += stride) {
@@ -414,8 +498,8 @@ __global__ void k_gru_prepare(const float* __restrict__ W_ih, const float* __res
     }
 }
 
-template <int KI, int KH>
-__global__ __launch_bounds__(64 * MW) void k_gru_fused(const float* __restrict__ msg, int dmsg,
+template <int KI, int KH, int TI, int TH, int U, int RT, int NW>
+__global__ __launch_bounds__(64 * NW) void k_gru_fused(const float* __restrict__ msg, int dmsg,
                                                        const float* __restrict__ Wi, const float* __restrict__ Wh,
                                                        const float* __restrict__ b_ih, const float* __restrict__ b_hh,
                                                        const int32_t* __restrict__ uniq,
@@ -424,49 +508,114 @@ __global__ __launch_bounds__(64 * MW) void k_gru_fused(const float* __restrict__
                                                        float* __restrict__ mem, float* __restrict__ lu,
                                                        float* __restrict__ sr, float* __restrict__ sz,
                                                        float* __restrict__ sn, float* __restrict__ sghn) {
-  constexpr int XL = 16 * KI + 4;   // LDS row stride, XL / 4 odd
-  constexpr int GL = 6 * GRU_UNITS + 4;
-  __shared__ __attribute__((aligned(16))) float X[16 * XL];
-  __shared__ float G[16 * GL];
+  constexpr int XL = 16 * KI + 4;          // LDS row strides, / 4 odd
+  constexpr int GL = 16 * (TI + TH) + 4;
+  constexpr int NR = (TI + TH + NW - 1) / NW;
+  constexpr int NTH = 64 * NW;
+  constexpr int ROWS = 16 * RT;
+  constexpr int NB = 6 * U + 2 * ROWS;     // biases of the group's units (b_ih r, z, n, b_hh r, z, n), row ids
+  constexpr int PB = (NB + NTH - 1) / NTH;
+  __shared__ __attribute__((aligned(16))) float X[ROWS * XL];
+  __shared__ float G[ROWS * GL];
+  __shared__ float BS[6 * U];
+  __shared__ int RI[2 * ROWS];             // node id, then the winning event, of each row
   const int64_t M = eff_count(max_rows, n_rows);
-  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  const int64_t r0 = (int64_t)blockIdx.x * ROWS;
   if (r0 >= M) return;   // block-uniform
   const int g = blockIdx.y;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, fr = lane & 15, fg = lane >> 4;
-  zero_cols<XL, 1>(X, dmsg, 16 * KI);
-  load_rows<XL, 1>(X, 0, msg, dmsg, dmsg, r0, M);
-  __syncthreads();
-  {
-    f32x4 ai[Tiles<6>::per_wave], ah[Tiles<6>::per_wave];
-    layer<6, KI, XL, 1>(X, Wi + (size_t)g * GRU_GROUP_ROWS * 16 * KI, ai);
-    layer<6, KH, XL, 1>(X, Wh + (size_t)g * GRU_GROUP_ROWS * 16 * KH, ah);
+  const int lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // the block's inputs: message rows, biases and row ids, all loads issued before the first LDS store
+  auto prologue = [&]() {
+    float bv[PB];
 #pragma unroll
-    for (int u = 0; u < Tiles<6>::per_wave; ++u) {
-      const int c = 16 * (wid + MW * u) + fr;
-      if (c >= 3 * GRU_UNITS) continue;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        G[(4 * fg + r) * GL + c] = ai[u][r];
-        G[(4 * fg + r) * GL + 3 * GRU_UNITS + c] = ah[u][r];
+    for (int k = 0; k < PB; ++k) {
+      const int e = threadIdx.x + NTH * k;
+      bv[k] = 0.f;
+      if (e < 6 * U) {
+        const int unit = U * g + e % U, gate = e / U;
+        if (unit < dm) bv[k] = (gate < 3 ? b_ih : b_hh)[(gate % 3) * dm + unit];
+      } else if (e < NB) {
+        const int i = (e - 6 * U) % ROWS;
+        const int32_t* src = e - 6 * U < ROWS ? uniq : winner;
+        bv[k] = __int_as_float(r0 + i < M ? src[r0 + i] : 0);
       }
     }
+    zero_cols<XL, RT, NTH>(X, dmsg, 16 * KI);
+    load_rows<XL, RT, NTH>(X, 0, msg, dmsg, dmsg, r0, M);
+#pragma unroll
+    for (int k = 0; k < PB; ++k) {
+      const int e = threadIdx.x + NTH * k;
+      if (e < 6 * U) BS[e] = bv[k];
+      else if (e < NB) RI[e - 6 * U] = __float_as_int(bv[k]);
+    }
+    __syncthreads();
+  };
+  auto products = [&](auto wave) {
+    constexpr int W = decltype(wave)::value;
+    f32x4 acc[NR][RT];
+#pragma unroll
+    for (int q = 0; q < NR; ++q)
+#pragma unroll
+      for (int r = 0; r < RT; ++r) acc[q][r] = f32x4{0.f, 0.f, 0.f, 0.f};
+    gru_jobs<NW, NR, KI, XL, RT, W, 0, TI>(X, Wi + (size_t)g * 16 * TI * 16 * KI, acc, prologue);
+    gru_jobs<NW, NR, KH, XL, RT, W, TI, TI + TH>(X, Wh + (size_t)g * 16 * TH * 16 * KH, acc, [] {});
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+      const int j = GruJobs<NW>::job(q, W);
+      if (j >= TI + TH) continue;
+#pragma unroll
+      for (int r = 0; r < RT; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) G[(16 * r + 4 * fg + e) * GL + 16 * j + fr] = acc[q][r][e];
+    }
+  };
+  // every wave runs the prologue (and its barrier) inside its own product body; the branch is wave-uniform
+  static_assert(NW == 4 || NW == 8, "one product body per wave");
+  switch (wid) {
+    case 0: products(std::integral_constant<int, 0>{}); break;
+    case 1: products(std::integral_constant<int, 1>{}); break;
+    case 2: products(std::integral_constant<int, 2>{}); break;
+    case 3: products(std::integral_constant<int, 3>{}); break;
+    case 4: if constexpr (NW > 4) products(std::integral_constant<int, 4 % NW>{}); break;
+    case 5: if constexpr (NW > 5) products(std::integral_constant<int, 5 % NW>{}); break;
+    case 6: if constexpr (NW > 6) products(std::integral_constant<int, 6 % NW>{}); break;
+    default: if constexpr (NW > 7) products(std::integral_constant<int, 7 % NW>{}); break;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 16 * GRU_UNITS; e += 64 * MW) {
-    const int i = e / GRU_UNITS, jj = e % GRU_UNITS, j = GRU_UNITS * g + jj;
-    if (j >= dm || r0 + i >= M) continue;
+  if (g == 0 && threadIdx.x < ROWS && r0 + threadIdx.x < M)   // last_update of the row's node
+    lu[RI[threadIdx.x]] = t[RI[ROWS + threadIdx.x] >> 1];
+  // gates: thread (row group rg, unit jj) takes rows rg, rg + RG, ...; its unit's biases stay in registers
+  // and every LDS read of its rows is issued before the math
+  constexpr int RG = NTH / U, PR = (ROWS + RG - 1) / RG;
+  const int jj = threadIdx.x % U, rg = threadIdx.x / U, j = U * g + jj;
+  if (rg >= RG || j >= dm) return;
+  const float br = BS[jj] , bz = BS[U + jj], bn = BS[2 * U + jj];
+  const float cr = BS[3 * U + jj], cz = BS[4 * U + jj], cn = BS[5 * U + jj];
+  float pr[PR], pz[PR], pn[PR], ph[PR], hv[PR];
+  int node[PR];
+#pragma unroll
+  for (int k = 0; k < PR; ++k) {
+    const int i = rg + RG * k < ROWS ? rg + RG * k : ROWS - 1;
     const float* gi = G + i * GL;
-    const float* gh = gi + 3 * GRU_UNITS;
-    const float rr = sigmoidf_((gi[jj] + b_ih[j]) + (gh[jj] + b_hh[j]));
-    const float zz = sigmoidf_((gi[GRU_UNITS + jj] + b_ih[dm + j]) + (gh[GRU_UNITS + jj] + b_hh[dm + j]));
-    const float ghn = gh[2 * GRU_UNITS + jj] + b_hh[2 * dm + j];
-    const float nn = tanhf((gi[2 * GRU_UNITS + jj] + b_ih[2 * dm + j]) + rr * ghn);
-    const float h = X[i * XL + j];
-    const float hn = (1.f - zz) * nn + zz * h;
+    pr[k] = gi[jj];
+    pz[k] = gi[U + jj];
+    pn[k] = gi[2 * U + jj];
+    ph[k] = gi[16 * TI + jj];
+    hv[k] = X[i * XL + j];
+    node[k] = RI[i];
+  }
+#pragma unroll
+  for (int k = 0; k < PR; ++k) {
+    const int i = rg + RG * k;
+    if (i >= ROWS || r0 + i >= M) break;
+    const float rr = sigmoid_hw((pr[k] + br) + cr);
+    const float zz = sigmoid_hw((pz[k] + bz) + cz);
+    const float ghn = ph[k] + cn;
+    const float nn = tanh_hw((pn[k] + bn) + rr * ghn);
+    const float hn = (1.f - zz) * nn + zz * hv[k];
     const int64_t row = r0 + i;
-    const int64_t node = uniq[row];
-    mem[node * dm + j] = hn;
-    if (j == 0) lu[node] = t[winner[row] >> 1];
+    mem[(int64_t)node[k] * dm + j] = hn;
     if (sr) {
       sr[row * dm + j] = rr;
       sz[row * dm + j] = zz;
@@ -721,21 +870,31 @@ mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int
   return MTGNN_OK;
 }
 
-static bool gru_fused_shape(int dm, int dmsg, int& ki, int& kh) {
+// Unit groups: two for d_mem above 64 (more blocks at a few thousand rows), else one.  Rows per block:
+// 32 from 16 Ki rows on (each weight fragment then serves two row tiles), else 16.
+static bool gru_fused_shape(int dm, int dmsg, int& ki, int& kh, GruShape& sh) {
   ki = (int)cdiv(dmsg, 16);
   kh = (int)cdiv(dm, 16);
-  return dm % 4 == 0 && dmsg % 4 == 0 &&
-         ((ki == 19 && kh == 7) || (ki == 20 && kh == 7) || (ki == 30 && kh == 7) || (ki == 7 && kh == 2));
+  sh.S = dm > 64 ? 2 : 1;
+  sh.U = (int)cdiv(dm, sh.S);
+  sh.ti = (int)cdiv(3 * sh.U, 16);
+  sh.th = (int)cdiv(sh.U, 16);
+  const bool wide = kh == 7 && sh.U == 50 && (ki == 19 || ki == 20 || ki == 30);   // ti 10, th 4
+  const bool narrow = ki == 7 && kh == 2 && sh.U == 32;                               // ti 6, th 2
+  return dm % 4 == 0 && dmsg % 4 == 0 && (wide || narrow);
 }
 
 bool gru_fused_ok(int dtype, int dm, int dmsg) {
   int ki, kh;
-  return dtype == MTGNN_F32 && gru_fused_shape(dm, dmsg, ki, kh);
+  GruShape sh;
+  return dtype == MTGNN_F32 && gru_fused_shape(dm, dmsg, ki, kh, sh);
 }
 
 size_t gru_fused_weight_floats(int dm, int dmsg) {
-  const int64_t groups = cdiv(dm, GRU_UNITS);
-  return (size_t)groups * GRU_GROUP_ROWS * 16 * (cdiv(dmsg, 16) + cdiv(dm, 16));
+  int ki, kh;
+  GruShape sh;
+  gru_fused_shape(dm, dmsg, ki, kh, sh);
+  return (size_t)sh.S * 256 * ((size_t)sh.ti * ki + (size_t)sh.th * kh);
 }
 
 mtgnn_status gru_fused(const float* msg, const float* W_ih, const float* W_hh, const float* b_ih, const float* b_hh,
@@ -743,24 +902,35 @@ mtgnn_status gru_fused(const float* msg, const float* W_ih, const float* W_hh, c
                        int64_t max_rows, int dm, int dmsg, float* Wp, float* mem, float* lu, float* sr, float* sz,
                        float* sn, float* sghn, GruWTArgs wt, hipStream_t s) {
   int ki, kh;
-  if (!gru_fused_shape(dm, dmsg, ki, kh) || !aligned16(msg)) return MTGNN_EUNSUPPORTED;
-  const int groups = (int)cdiv(dm, GRU_UNITS);
+  GruShape sh;
+  if (!gru_fused_shape(dm, dmsg, ki, kh, sh) || !aligned16(msg)) return MTGNN_EUNSUPPORTED;
   float* Wi = Wp;
-  float* Wh = Wp + (size_t)groups * GRU_GROUP_ROWS * 16 * ki;
-  const int64_t tot = (int64_t)groups * GRU_GROUP_ROWS * 16 * (ki + kh);
+  float* Wh = Wp + (size_t)sh.S * 256 * sh.ti * ki;
+  const int64_t tot = (int64_t)gru_fused_weight_floats(dm, dmsg);
   k_gru_prepare<<<(unsigned)std::min<int64_t>(cdiv(tot, 256), 1024), 256, 0, s>>>(W_ih, W_hh, dm, dmsg, 16 * ki,
-                                                                                   16 * kh, groups, Wi, Wh, wt);
+                                                                                   16 * kh, sh, Wi, Wh, wt);
   MTGNN_CHECK_LAUNCH("gru_prepare");
   if (max_rows <= 0) return MTGNN_OK;
-  const dim3 grid((unsigned)cdiv(max_rows, 16), (unsigned)groups);
-#define MTGNN_GRU_FUSED(KI_, KH_)                                                                          \
-  k_gru_fused<KI_, KH_><<<grid, 64 * MW, 0, s>>>(msg, dmsg, Wi, Wh, b_ih, b_hh, uniq, winner, t, n_rows, \
-                                                  max_rows, dm, mem, lu, sr, sz, sn, sghn)
-  if (ki == 19) MTGNN_GRU_FUSED(19, 7);
-  else if (ki == 20) MTGNN_GRU_FUSED(20, 7);
-  else if (ki == 30) MTGNN_GRU_FUSED(30, 7);
-  else MTGNN_GRU_FUSED(7, 2);
-#undef MTGNN_GRU_FUSED
+  const int rt = max_rows >= 16384 ? 2 : 1;
+  const dim3 grid((unsigned)cdiv(max_rows, 16 * rt), (unsigned)sh.S);
+  TimedScope ts("gru_fused", s);
+  auto launch = [&](auto kern) {
+    kern<<<grid, 64 * GRU_NW, 0, s>>>(msg, dmsg, Wi, Wh, b_ih, b_hh, uniq, winner, t, n_rows, max_rows, dm, mem,
+                                         lu, sr, sz, sn, sghn);
+  };
+  if (ki == 19) {
+    if (rt == 2) launch(k_gru_fused<19, 7, 10, 4, 50, 2, GRU_NW>);
+    else launch(k_gru_fused<19, 7, 10, 4, 50, 1, GRU_NW>);
+  } else if (ki == 20) {
+    if (rt == 2) launch(k_gru_fused<20, 7, 10, 4, 50, 2, GRU_NW>);
+    else launch(k_gru_fused<20, 7, 10, 4, 50, 1, GRU_NW>);
+  } else if (ki == 30) {
+    if (rt == 2) launch(k_gru_fused<30, 7, 10, 4, 50, 2, GRU_NW>);
+    else launch(k_gru_fused<30, 7, 10, 4, 50, 1, GRU_NW>);
+  } else {
+    if (rt == 2) launch(k_gru_fused<7, 2, 6, 2, 32, 2, GRU_NW>);
+    else launch(k_gru_fused<7, 2, 6, 2, 32, 1, GRU_NW>);
+  }
   MTGNN_CHECK_LAUNCH("gru_fused");
   return MTGNN_OK;
 }
