@@ -27,6 +27,34 @@
 namespace mtgnn {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Four float32 values as the bfloat16 operand of an MFMA (k = 4 (l / 16) .. + 3 of lane l, in order).
+// Weights stored as bfloat16 are exact in float32: their high halves are taken as they are.
+__device__ __forceinline__ s16x4 bf16x4_exact(float4 v) {
+  const uint32_t lo = (__float_as_uint(v.x) >> 16) | (__float_as_uint(v.y) & 0xffff0000u);
+  const uint32_t hi = (__float_as_uint(v.z) >> 16) | (__float_as_uint(v.w) & 0xffff0000u);
+  s16x4 r;
+  r.x = (short)(lo & 0xffffu);
+  r.y = (short)(lo >> 16);
+  r.z = (short)(hi & 0xffffu);
+  r.w = (short)(hi >> 16);
+  return r;
+}
+// Activations are rounded to bfloat16 (nearest, ties to even) as they enter a bfloat16 product; values
+// already rounded by their producer pass through unchanged.
+__device__ __forceinline__ s16x4 bf16x4_round(float4 v) {
+  auto rn = [](float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (short)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+  };
+  s16x4 r;
+  r.x = rn(v.x);
+  r.y = rn(v.y);
+  r.z = rn(v.z);
+  r.w = rn(v.w);
+  return r;
+}
 
 // Call-site tags: the hot sites get their own kernel symbol (and timer name).
 namespace site {
@@ -415,6 +443,11 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, const TileCoord tc)
     }
   };
 
+  // Forward products with bfloat16 weights (x W^T, both operands contiguous along k) run on the bfloat16
+  // MFMA: the activations enter rounded to bfloat16 (they already are: every forward input of the
+  // bfloat16 mode is stored or produced rounded), products are exact and accumulate in float32.
+  constexpr bool MMA_BF16 = std::is_same<TB, uint16_t>::value && A_KCONTIG && B_KCONTIG && !TGE;
+
   // MFMA work on one LDS tile pair
   auto compute = [&](const float* as, const float* bs) {
 #pragma unroll
@@ -425,6 +458,18 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& g, const TileCoord tc)
       float4 b4[NT];
 #pragma unroll
       for (int j = 0; j < NT; ++j) b4[j] = LB::frag(bs, j * 16 + (lane & 15), kc, lane);
+      if constexpr (MMA_BF16) {   // one 16 x 16 x 16 bfloat16 MFMA per tile pair and chunk
+        s16x4 ab[WM], bb[NT];
+#pragma unroll
+        for (int i = 0; i < WM; ++i) ab[i] = bf16x4_round(a4[i]);
+#pragma unroll
+        for (int j = 0; j < NT; ++j) bb[j] = bf16x4_exact(b4[j]);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ab[i], bb[j], acc[i][j], 0, 0, 0);
+        continue;
+      }
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
