@@ -794,14 +794,8 @@ mtgnn_status gemm_batch_launch_t(const GemmArgs* gs, int n, int zper, hipStream_
   return MTGNN_OK;
 }
 
-// Instantiated once per (site, layout) in gemm_nt.hip / gemm_nn.hip / gemm_tn.hip.
 template <class Site, bool AK, bool BK>
-mtgnn_status gemm_launch(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s);
-template <class Site, bool AK, bool BK>
-mtgnn_status gemm_batch_launch(const GemmArgs* gs, int n, int zper, int dtype_a, int dtype_b, hipStream_t s);
-
-template <class Site, bool AK, bool BK>
-mtgnn_status gemm_batch_launch_impl(const GemmArgs* gs, int n, int zper, int dtype_a, int dtype_b, hipStream_t s) {
+mtgnn_status gemm_batch_launch(const GemmArgs* gs, int n, int zper, int dtype_a, int dtype_b, hipStream_t s) {
   if (dtype_a == MTGNN_F32 && dtype_b == MTGNN_F32) return gemm_batch_launch_t<Site, float, float, AK, BK>(gs, n, zper, s);
   if (dtype_a == MTGNN_F32) return gemm_batch_launch_t<Site, float, uint16_t, AK, BK>(gs, n, zper, s);
   if (dtype_b == MTGNN_F32) return MTGNN_EUNSUPPORTED;
@@ -809,13 +803,35 @@ mtgnn_status gemm_batch_launch_impl(const GemmArgs* gs, int n, int zper, int dty
 }
 
 template <class Site, bool AK, bool BK>
-mtgnn_status gemm_launch_impl(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s) {
+mtgnn_status gemm_launch(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return MTGNN_OK;
   if (dtype_a == MTGNN_F32 && dtype_b == MTGNN_F32) return gemm_launch_t<Site, float, float, AK, BK>(g, ksplit, s);
   if (dtype_a == MTGNN_F32) return gemm_launch_t<Site, float, uint16_t, AK, BK>(g, ksplit, s);
   if (dtype_b == MTGNN_F32) return MTGNN_EUNSUPPORTED;   // bf16 activations always meet bf16 weights
   return gemm_launch_t<Site, uint16_t, uint16_t, AK, BK>(g, ksplit, s);
 }
+
+// The instances the library uses, each compiled in one place: gemm_nt.hip (x W^T, both operands
+// contiguous along k), gemm_nn.hip (dy W) and gemm_tn.hip (dy^T x).  One translation unit per operand
+// layout: each takes one to two minutes to compile, and the build runs them in parallel.
+#define MTGNN_GEMM_INSTANCES(EXTERN)                                                                                 \
+  EXTERN template mtgnn_status gemm_launch<site::Generic, true, true>(const GemmArgs&, int, int, int, hipStream_t);  \
+  EXTERN template mtgnn_status gemm_launch<site::KvProj, true, true>(const GemmArgs&, int, int, int, hipStream_t);   \
+  EXTERN template mtgnn_status gemm_batch_launch<site::Generic, true, true>(const GemmArgs*, int, int, int, int,      \
+                                                                            hipStream_t);
+#define MTGNN_GEMM_INSTANCES_NN(EXTERN)                                                                              \
+  EXTERN template mtgnn_status gemm_launch<site::Generic, true, false>(const GemmArgs&, int, int, int, hipStream_t); \
+  EXTERN template mtgnn_status gemm_launch<site::KvDx, true, false>(const GemmArgs&, int, int, int, hipStream_t);
+#define MTGNN_GEMM_INSTANCES_TN(EXTERN)                                                                              \
+  EXTERN template mtgnn_status gemm_launch<site::Generic, false, false>(const GemmArgs&, int, int, int, hipStream_t); \
+  EXTERN template mtgnn_status gemm_launch<site::KvDw, false, false>(const GemmArgs&, int, int, int, hipStream_t);   \
+  EXTERN template mtgnn_status gemm_batch_launch<site::Generic, false, false>(const GemmArgs*, int, int, int, int,    \
+                                                                              hipStream_t);                          \
+  EXTERN template mtgnn_status gemm_batch_launch<site::GruDw, false, false>(const GemmArgs*, int, int, int, int,      \
+                                                                            hipStream_t);
+MTGNN_GEMM_INSTANCES(extern)
+MTGNN_GEMM_INSTANCES_NN(extern)
+MTGNN_GEMM_INSTANCES_TN(extern)
 
 // y[M,N] (+)= x[M,K] W[N,K]^T + bias.
 // pre_relu: store the pre-activation there and relu(y) in y.  round_bf16: round y to bfloat16.

@@ -1,14 +1,8 @@
-// Data-gradient products dx = dy W (A contiguous along k, B along the output columns).
+// Data-gradient products dx = dy W (A contiguous along k, B along the output columns): this layout's instances of the strip GEMM.
 #include "gemm.h"
 
 namespace mtgnn {
 
-template <class Site, bool AK, bool BK>
-mtgnn_status gemm_launch(const GemmArgs& g, int dtype_a, int dtype_b, int ksplit, hipStream_t s) {
-  return gemm_launch_impl<Site, AK, BK>(g, dtype_a, dtype_b, ksplit, s);
-}
-
-template mtgnn_status gemm_launch<site::Generic, true, false>(const GemmArgs&, int, int, int, hipStream_t);
-template mtgnn_status gemm_launch<site::KvDx, true, false>(const GemmArgs&, int, int, int, hipStream_t);
+MTGNN_GEMM_INSTANCES_NN()
 
 }  // namespace mtgnn
