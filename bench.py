@@ -51,6 +51,12 @@ def parse():
     ap.add_argument("--kernel-report", nargs=3, metavar=("TRACE_CSV", "FETCH_CSV", "WRITE_CSV"),
                     help="turn a rocprofv3 --kernel-trace CSV and two --pmc CSVs (FETCH_SIZE, WRITE_SIZE; runs made "
                          "with --copy-probe) into per-kernel HBM traffic and achieved GB/s under profiles/, then exit")
+    ap.add_argument("--mfma-report", nargs=2, metavar=("TRACE_CSV", "SQ_CSV"),
+                    help="turn a rocprofv3 --kernel-trace CSV and a --pmc CSV of SQ_VALU_MFMA_BUSY_CYCLES into each "
+                         "matrix kernel's MFMA-busy fraction under profiles/, then exit")
+    ap.add_argument("--step-report", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
+                    help="turn a rocprofv3 --kernel-trace --stats output directory of this bench and the bench's "
+                         "JSON line into the per-step kernel table under profiles/, then exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a run made with "
                          "--copy-probe into the traffic record under profiles/, then exit")
@@ -68,6 +74,12 @@ def main():
         return
     if args.kernel_report:
         kernel_report(args)
+        return
+    if args.mfma_report:
+        mfma_report(args)
+        return
+    if args.step_report:
+        step_report(args)
         return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -370,6 +382,26 @@ def write_traffic(args):
     with open(traffic_path(w), "w") as fh:
         json.dump(rec, fh, indent=1)
         fh.write("\n")
+    n, mib = args.workload, args.copy_probe
+    lines = [f"# HBM traffic of the neighbour-slot products on {w.name} (fp32)", "",
+             "Two counter passes, each its own run (repository root, MI355X), then the record:", "", "```",
+             f"timeout -s KILL 400 rocprofv3 --pmc FETCH_SIZE -f csv -d gpurun_out/pmcF_w{n} -o run -- python -u bench.py "
+             f"--workload {n} --steps 2 --warmup 1 --cpu-steps 0 --copy-probe {mib}",
+             f"timeout -s KILL 400 rocprofv3 --pmc WRITE_SIZE -f csv -d gpurun_out/pmcW_w{n} -o run -- python -u bench.py "
+             f"--workload {n} --steps 2 --warmup 1 --cpu-steps 0 --copy-probe {mib}",
+             f"python bench.py --workload {n} --copy-probe {mib} --traffic-from "
+             f"gpurun_out/pmcF_w{n}/run_counter_collection.csv gpurun_out/pmcW_w{n}/run_counter_collection.csv", "```", "",
+             f"Calibration: `--copy-probe {mib}` copies a {mib} MiB buffer twice just before the first step; the copy "
+             f"reads FETCH_SIZE = {fkib:.0f} KiB and WRITE_SIZE = {wkib:.0f} KiB for {probe // 1024} KiB moved each way, "
+             f"so FETCH_SIZE is scaled by {ff:.4f} and WRITE_SIZE by {fw:.4f}.", "",
+             f"Per launch (mean over the run's dispatches), from `{os.path.basename(traffic_path(w))}`, which bench.py "
+             "reads for its `traffic` field while the hash of the kernel sources (`fingerprint`) matches:", "",
+             "| site | fetch MB | write MB | total MB | dispatches |", "|---|---|---|---|---|"]
+    for k, v in sites.items():
+        lines.append(f"| {k} | {v['fetch_bytes_per_launch'] / 1e6:.1f} | {v['write_bytes_per_launch'] / 1e6:.1f} | "
+                     f"{v['bytes_per_launch'] / 1e6:.1f} | {v['dispatches']} |")
+    with open(os.path.join(ROOT, "profiles", f"hbm-traffic-hot-sites-{w.name}.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
     print(json.dumps(rec))
 
 
@@ -437,7 +469,136 @@ def kernel_report(args):
     with open(base + ".json", "w") as fh:
         json.dump(rec, fh, indent=1)
         fh.write("\n")
+    n = args.workload
+    lines = [f"# HBM traffic and achieved bandwidth per kernel, {w.name} (MI355X)", "",
+             "Three runs of the same step (repository root), then the report:", "", "```",
+             f"rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/kt_w{n} -o run -- python -u bench.py --workload {n} "
+             f"--steps 10 --warmup 3 --cpu-steps 0",
+             f"timeout -s KILL 400 rocprofv3 --pmc FETCH_SIZE -f csv -d gpurun_out/pmcF_w{n} -o run -- python -u bench.py "
+             f"--workload {n} --steps 2 --warmup 1 --cpu-steps 0 --copy-probe {args.copy_probe}",
+             f"timeout -s KILL 400 rocprofv3 --pmc WRITE_SIZE -f csv -d gpurun_out/pmcW_w{n} -o run -- python -u bench.py "
+             f"--workload {n} --steps 2 --warmup 1 --cpu-steps 0 --copy-probe {args.copy_probe}",
+             f"python bench.py --workload {n} --copy-probe {args.copy_probe} --kernel-report "
+             f"gpurun_out/kt_w{n}/run_kernel_trace.csv gpurun_out/pmcF_w{n}/run_counter_collection.csv "
+             f"gpurun_out/pmcW_w{n}/run_counter_collection.csv", "```", "",
+             f"Calibration: the {args.copy_probe} MiB probe copy reads FETCH_SIZE x {ff:.4f} and WRITE_SIZE x {fw:.4f} "
+             "of the bytes it moves; both counters are scaled by those factors.  Bytes are per dispatch (mean over the "
+             "counter runs), durations the median of the kernel-trace run, GB/s = (fetch + write) / duration, and the "
+             "fraction is of the 8 TB/s HBM3E peak.  Matrix-product kernels are listed for completeness: their bound "
+             "is the MFMA rate, not HBM.", "",
+             "| median us | fetch MB | write MB | GB/s | % of HBM peak | launches | kernel |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['median_us']:.1f} | {r['fetch_MB']:.1f} | {r['write_MB']:.1f} | {r['GBps']:.0f} | "
+                     f"{100 * r['hbm_frac']:.1f} | {r['launches']} | `{r['kernel'][:100]}` |")
+    with open(base + ".md", "w") as fh:
+        fh.write("\n".join(lines) + "\n")
     print(json.dumps({"written": base + ".json", "kernels": len(rows)}))
+
+
+MFMA_SIMDS = 256 * 4      # MI355X: 256 compute units, 4 SIMDs each
+MFMA_CLOCK_GHZ = 2.4      # peak engine clock
+
+
+def mfma_report(args):
+    """Per matrix kernel of the step: median duration (kernel trace) and the mean MFMA-busy cycles per dispatch
+    (SQ_VALU_MFMA_BUSY_CYCLES, summed over the SIMDs), as a fraction of all SIMDs' cycles over the duration at
+    the peak engine clock (a lower bound when the clock runs below its peak)."""
+    import csv
+    from synth import workload
+    w = workload(args.workload)
+    trace_csv, sq_csv = args.mfma_report
+    dur = {}
+    with open(trace_csv) as fh:
+        for r in csv.DictReader(fh):
+            dur.setdefault(_clean_kernel(r["Kernel_Name"]), []).append(
+                (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    rows_c = _counter_rows(sq_csv, "SQ_VALU_MFMA_BUSY_CYCLES")
+    first = next(i for i, r in enumerate(rows_c) if "k_agg_reset" in r["Kernel_Name"])
+    busy = {}
+    for r in rows_c[first:]:
+        busy.setdefault(_clean_kernel(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+    rows = []
+    for k, v in busy.items():
+        cyc = sum(v) / len(v)
+        if cyc <= 0 or k not in dur:
+            continue
+        us = sorted(dur[k])[len(dur[k]) // 2]
+        rows.append({"kernel": k, "median_us": us, "mfma_busy_cycles": cyc, "launches": len(dur[k]),
+                     "mfma_busy_frac": cyc / (MFMA_SIMDS * us * 1e3 * MFMA_CLOCK_GHZ)})
+    rows.sort(key=lambda r: -r["median_us"])
+    base = os.path.join(ROOT, "profiles", f"mfma-busy-{w.name}")
+    with open(base + ".json", "w") as fh:
+        json.dump({"workload": w.name, "simds": MFMA_SIMDS, "clock_ghz": MFMA_CLOCK_GHZ, "kernels": rows}, fh, indent=1)
+        fh.write("\n")
+    n = args.workload
+    lines = [f"# MFMA-busy fraction per matrix kernel, {w.name} (MI355X)", "",
+             "Two runs of the same step (repository root), then the report:", "", "```",
+             f"rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/kt_w{n} -o run -- python -u bench.py --workload {n} "
+             f"--steps 10 --warmup 3 --cpu-steps 0",
+             f"timeout -s KILL 400 rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES -f csv -d gpurun_out/pmcQ_w{n} "
+             f"-o run -- python -u bench.py --workload {n} --steps 2 --warmup 1 --cpu-steps 0",
+             f"python bench.py --workload {n} --mfma-report gpurun_out/kt_w{n}/run_kernel_trace.csv "
+             f"gpurun_out/pmcQ_w{n}/run_counter_collection.csv", "```", "",
+             "SQ_VALU_MFMA_BUSY_CYCLES counts the cycles the matrix cores are busy, summed over the SIMDs (each "
+             "v_mfma_f32_16x16x4_f32 adds 32: a kernel's count matches its instruction count times 32).  The "
+             "fraction divides the mean per dispatch "
+             f"by {MFMA_SIMDS} SIMDs x the median duration x {MFMA_CLOCK_GHZ} GHz; in the step the two streams share "
+             "the chip, so a kernel that ran beside another shows less than it would alone.", "",
+             "| median us | MFMA-busy cycles (M) | MFMA busy % | launches | kernel |", "|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['median_us']:.1f} | {r['mfma_busy_cycles'] / 1e6:.2f} | {100 * r['mfma_busy_frac']:.1f} | "
+                     f"{r['launches']} | `{r['kernel'][:100]}` |")
+    with open(base + ".md", "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(json.dumps({"written": base + ".json", "kernels": len(rows)}))
+
+
+def step_report(args):
+    """Kernel time per step of a profiled bench run: the totals of rocprofv3's kernel statistics over the step
+    intervals between consecutive aggregation launches (the first warmup steps skipped)."""
+    import csv
+    from synth import workload
+    w = workload(args.workload)
+    d, bench_json = args.step_report
+    with open(os.path.join(d, "run_kernel_trace.csv")) as fh:
+        trace = sorted(csv.DictReader(fh), key=lambda r: int(r["Start_Timestamp"]))
+    idx = [i for i, r in enumerate(trace) if "k_agg_reset" in r["Kernel_Name"]]
+    spans = list(zip(idx[3:-1], idx[4:]))
+    if not spans:
+        raise SystemExit(f"{d}: too few steps in the trace")
+    per = {}
+    total = 0.0
+    for a, b in spans:
+        for r in trace[a:b]:
+            us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            k = _clean_kernel(r["Kernel_Name"])
+            t, c = per.get(k, (0.0, 0))
+            per[k] = (t + us, c + 1)
+            total += us
+    ns = len(spans)
+    with open(bench_json) as fh:
+        bench = json.loads(fh.read().strip().splitlines()[-1])
+    rl = bench["roofline"]
+    n = args.workload
+    lines = [f"# Kernel time of one batch step on {w.name} (MI355X)", "", "Command (repository root):", "", "```",
+             f"rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/kt_w{n} -o run -- python -u bench.py --workload {n} "
+             f"--steps 10 --warmup 3 --cpu-steps 0",
+             f"python bench.py --workload {n} --step-report gpurun_out/kt_w{n} BENCH_LINE.json", "```", "",
+             f"Per-step figures average the {ns} step intervals between the 4th and the last aggregation launch (the "
+             f"warmup's first steps are skipped).  Kernel time per step: {total / ns:.1f} us in "
+             f"{sum(c for _, c in per.values()) / ns:.0f} launches (two streams overlap, so the step takes less).", "",
+             f"bench.py headline (separate run, `python -u bench.py --workload {n} --cpu-steps 0`): "
+             f"{bench['value'] / 1e6:.3f} M events/s, {bench['ms_per_step'] * 1e3:.1f} us per step; step sizes "
+             f"{json.dumps(bench.get('step_counts', {}))}; dominant product `{rl['kernel']}` "
+             f"{rl['avg_launch_us']:.1f} us per launch, {rl['achieved']:.1f} TFLOP/s = {100 * rl['frac']:.2f}% of "
+             f"{rl['peak']} TFLOP/s.", "",
+             "| % of kernel time | us/step | launches/step | us/launch | kernel |", "|---|---|---|---|---|"]
+    for k, (t, c) in sorted(per.items(), key=lambda kv: -kv[1][0])[:45]:
+        lines.append(f"| {100 * t / total:.2f} | {t / ns:.2f} | {c / ns:.2f} | {t / c:.2f} | `{k[:110]}` |")
+    path = os.path.join(ROOT, "profiles", f"step-kernels-{w.name}.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(json.dumps({"written": path, "kernels": len(per)}))
 
 
 def cpu_baseline(w, s, params, mem, lu, b0, n):

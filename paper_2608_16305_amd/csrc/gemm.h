@@ -984,6 +984,7 @@ struct DwOsBatch {
   const int32_t* R_dev;
 };
 constexpr int DW_OS_MAX_BLOCKS = 256;
+template <class Site = site::Generic>
 mtgnn_status dw_os_launch(const DwOsBatch& b, int grid, hipStream_t s);
 int dw_os_cu_count();
 
@@ -1008,6 +1009,7 @@ struct DwTile {
   float* dup_db;
 };
 size_t dw_tiles_ws_bytes(const DwTile* t, int n);
+template <class Site = site::Generic>
 mtgnn_status dw_tiles(const DwTile* t, int n, int64_t R, const int32_t* R_dev, void* ws, size_t ws_bytes,
                       hipStream_t s);
 template <class Site = site::Generic>

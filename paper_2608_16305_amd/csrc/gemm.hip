@@ -348,6 +348,7 @@ size_t dw_tiles_ws_bytes(const DwTile* t, int n) {   // depends on the shapes on
   return b;
 }
 
+template <class Site>
 mtgnn_status dw_tiles(const DwTile* t, int n, int64_t R, const int32_t* R_dev, void* ws, size_t ws_bytes,
                       hipStream_t s) {
   if (!dw_tiles_ok(t, n) || dw_os_cu_count() <= 0) return MTGNN_EUNSUPPORTED;
@@ -378,11 +379,14 @@ mtgnn_status dw_tiles(const DwTile* t, int n, int64_t R, const int32_t* R_dev, v
     begin += nblk[i];
     max_out = std::max(max_out, per);
   }
-  MTGNN_TRY(dw_os_launch(b, begin, s));
+  MTGNN_TRY(dw_os_launch<Site>(b, begin, s));
   k_splitk_reduce_batch<<<dim3((unsigned)cdiv(max_out, 64), (unsigned)n), 256, 0, s>>>(rb);
   MTGNN_CHECK_LAUNCH("splitk_reduce_batch");
   return MTGNN_OK;
 }
+
+template mtgnn_status dw_tiles<site::Generic>(const DwTile*, int, int64_t, const int32_t*, void*, size_t, hipStream_t);
+template mtgnn_status dw_tiles<site::GruDw>(const DwTile*, int, int64_t, const int32_t*, void*, size_t, hipStream_t);
 
 template mtgnn_status linear_dw_batch<site::Generic>(const DwProblem*, int, int64_t, const int32_t*, int, void*, size_t,
                                                      hipStream_t);

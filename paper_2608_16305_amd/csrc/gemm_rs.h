@@ -570,6 +570,7 @@ __device__ __forceinline__ void dw_os_body(const DwOsProblem& q, int64_t rows, i
 }
 
 // One launch for the whole batch: block b works for the problem whose block range holds b.
+template <class Site>   // the call site names the kernel symbol only
 __global__ __launch_bounds__(G_THREADS, 1) void k_dw_os(DwOsBatch b) {
   constexpr int SLOT_MAX = 16 * (rs::dw_stride(7) + rs::dw_stride(13));
   __shared__ __attribute__((aligned(16))) float lds[DW_OS_SLOTS * SLOT_MAX];

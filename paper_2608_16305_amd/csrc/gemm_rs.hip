@@ -87,13 +87,17 @@ mtgnn_status dw_rs_launch_rows2(const float* X, int64_t ldx, int nx, const float
 
 int dw_os_cu_count() { return cu_count(); }
 
+template <class Site>
 mtgnn_status dw_os_launch(const DwOsBatch& b, int grid, hipStream_t s) {
   {
     TimedScope ts("dw_os", s);
-    k_dw_os<<<(unsigned)grid, G_THREADS, 0, s>>>(b);
+    k_dw_os<Site><<<(unsigned)grid, G_THREADS, 0, s>>>(b);
   }
   MTGNN_CHECK_LAUNCH("dw_os");
   return MTGNN_OK;
 }
+
+template mtgnn_status dw_os_launch<site::Generic>(const DwOsBatch&, int, hipStream_t);
+template mtgnn_status dw_os_launch<site::GruDw>(const DwOsBatch&, int, hipStream_t);
 
 }  // namespace mtgnn

@@ -775,7 +775,7 @@ mtgnn_status gru_update_bwd_impl(const float* d_mem, const void* save, const voi
   mtgnn_status st = MTGNN_EUNSUPPORTED;
   if (nt) {   // one output-stationary launch and one reduce (unsupported: misaligned operands)
     TimedScope ts(site::GruDw::name, s);
-    st = dw_tiles(tiles, nt, max_rows, n_rows, w, rest, s);
+    st = dw_tiles<site::GruDw>(tiles, nt, max_rows, n_rows, w, rest, s);
     if (st != MTGNN_OK && st != MTGNN_EUNSUPPORTED) return st;
   }
   if (st != MTGNN_OK && d->dtype == MTGNN_F32) {   // both weight gradients in one launch
