@@ -207,19 +207,19 @@ __global__ __launch_bounds__(256) void k_attn_gather(GatherArgs a, const T* __re
                     a.dt, a.bf16, a.kv_in, a.pair_nbr, a.pair_delta);
 }
 
-// Float32 fast path (no edge features, widths divisible by 4): the values of k_attn_gather<float>,
-// computed the same way, with a query's rows cut into 4-float groups laid out flat across the
-// wave, so that each lane moves 16 bytes per load or store: the query row in one pass, then the
-// memory groups of all its valid slots (loads issued GV_UNROLL passes at a time before any store),
-// then the time-encoding groups (four cosines per lane).
+// Float32 fast path (widths divisible by 4): the values of k_attn_gather<float>, computed the same
+// way, with a query's rows cut into 4-float groups laid out flat across the wave, so that each lane
+// moves 16 bytes per load or store: the query row in one pass, then the memory groups of all its
+// valid slots (loads issued GV_UNROLL passes at a time before any store), their edge-feature groups
+// the same way, then the time-encoding groups (four cosines per lane).
 constexpr int GV_UNROLL = 4;
 
 __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const float* __restrict__ mem) {
   const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (q >= eff_count(a.max_q, a.n_q)) return;
-  const int dm = a.dm, dt = a.dt, da = a.da, gm = dm >> 2, gt = dt >> 2;
-  const int D = dm + dt;   // row width of both q_in and kv_in
+  const int dm = a.dm, dt = a.dt, da = a.da, de = a.de, gm = dm >> 2, gt = dt >> 2, ge = de >> 2;
+  const int Dq = dm + dt, D = dm + de + dt;   // row widths of q_in and kv_in
   // every per-query scalar first, so that their loads overlap the query row's
   const int64_t node = a.q_node[q];
   const int c = a.cnt[q];
@@ -228,13 +228,15 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
   // loaded on lane < k (in bounds of the [max_q, k] arrays), so they need not wait for c
   const int32_t nb_raw = lane < a.k ? a.nbr[q * a.k + lane] : 0;
   const float t_raw = lane < a.k ? a.nt[q * a.k + lane] : 0.f;
+  const int32_t e_raw = lane < a.k && de > 0 ? a.neid[q * a.k + lane] : 0;
   const int32_t my_nb = lane < c ? nb_raw : 0;
+  const int32_t my_e = lane < c ? e_raw : 0;
   const float my_t = lane < c ? t_raw : 0.f;
   {
     for (int g = lane; g < gm + gt; g += 64) {
       if (g < gm) {
         const float4 v = *(const float4*)(mem + node * dm + 4 * g);
-        *(float4*)(a.q_in + q * D + 4 * g) = v;
+        *(float4*)(a.q_in + q * Dq + 4 * g) = v;
         *(float4*)(a.m_in + q * (da + dm) + da + 4 * g) = v;
       } else {
         const int j = 4 * (g - gm);
@@ -243,7 +245,7 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
         o.y = cosf(time_arg(a.tw[j + 1], 0.f, a.tb[j + 1]));
         o.z = cosf(time_arg(a.tw[j + 2], 0.f, a.tb[j + 2]));
         o.w = cosf(time_arg(a.tw[j + 3], 0.f, a.tb[j + 3]));
-        *(float4*)(a.q_in + q * D + dm + j) = o;
+        *(float4*)(a.q_in + q * Dq + dm + j) = o;
       }
     }
   }
@@ -269,6 +271,23 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
     for (int u = 0; u < GV_UNROLL; ++u)
       if (e0 + 64 * u + lane < nm) *(float4*)(a.kv_in + dst[u]) = v[u];
   }
+  const int nx = c * ge;
+  for (int e0 = 0; e0 < nx; e0 += 64 * GV_UNROLL) {   // edge features [dm, dm + de)
+    float4 v[GV_UNROLL];
+    int64_t dst[GV_UNROLL];
+#pragma unroll
+    for (int u = 0; u < GV_UNROLL; ++u) {
+      const int e = e0 + 64 * u + lane;
+      const int ec = e < nx ? e : nx - 1;
+      const int sl = ec / ge, g = ec - sl * ge;
+      const int64_t eid = __shfl(my_e, sl, 64);
+      v[u] = *(const float4*)(a.x + eid * de + 4 * g);
+      dst[u] = (off + sl) * D + dm + 4 * g;
+    }
+#pragma unroll
+    for (int u = 0; u < GV_UNROLL; ++u)
+      if (e0 + 64 * u + lane < nx) *(float4*)(a.kv_in + dst[u]) = v[u];
+  }
   const int ntg = c * gt;
   for (int e0 = 0; e0 < ntg; e0 += 64) {
     const int e = e0 + lane;
@@ -282,7 +301,7 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
       o.y = cosf(time_arg(a.tw[j + 1], delta, a.tb[j + 1]));
       o.z = cosf(time_arg(a.tw[j + 2], delta, a.tb[j + 2]));
       o.w = cosf(time_arg(a.tw[j + 3], delta, a.tb[j + 3]));
-      *(float4*)(a.kv_in + (off + sl) * D + dm + j) = o;
+      *(float4*)(a.kv_in + (off + sl) * D + dm + de + j) = o;
     }
   }
 }
@@ -1143,8 +1162,8 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
   const unsigned gq = (unsigned)cdiv(sh.Q, 4);
   const GatherArgs ga{q_node, nbr, neid, n_q, sv.cnt, sv.pair_off, nt, q_t, edge_feat, tw, tb, max_q, sh.k, sh.dm,
                       sh.de, sh.dt, sh.da, bf, sv.q_in, sv.m_in, sv.kv_in, sv.pair_delta, sv.pair_nbr};
-  const bool v4 = !bf && sh.de == 0 && sh.dm % 4 == 0 && sh.dt % 4 == 0 && sh.da % 4 == 0 &&
-                  ((uintptr_t)memory & 15) == 0;
+  const bool v4 = !bf && sh.de % 4 == 0 && sh.dm % 4 == 0 && sh.dt % 4 == 0 && sh.da % 4 == 0 &&
+                  ((uintptr_t)memory & 15) == 0 && (sh.de == 0 || ((uintptr_t)edge_feat & 15) == 0);
   if (v4)
     k_attn_gather_v4<<<gq, 256, 0, s>>>(ga, (const float*)memory);
   else if (!bf)
