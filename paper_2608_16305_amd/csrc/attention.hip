@@ -214,7 +214,24 @@ __global__ __launch_bounds__(256) void k_attn_gather(GatherArgs a, const T* __re
 // the same way, then the time-encoding groups (four cosines per lane).
 constexpr int GV_UNROLL = 4;
 
-__global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const float* __restrict__ mem) {
+// Four consecutive values of a memory row (float32, or bfloat16 widened exactly).
+__device__ __forceinline__ float4 load4(const float* p) { return *(const float4*)p; }
+__device__ __forceinline__ float4 load4(const uint16_t* p) {
+  const uint2 u = *(const uint2*)p;
+  return make_float4(bf16_to_f32((uint16_t)(u.x & 0xffffu)), bf16_to_f32((uint16_t)(u.x >> 16)),
+                     bf16_to_f32((uint16_t)(u.y & 0xffffu)), bf16_to_f32((uint16_t)(u.y >> 16)));
+}
+// A time-encoding value as it enters the product (bfloat16 mode: rounded, decided on the correctly
+// rounded cosine).
+__device__ __forceinline__ float enc_val(float arg, int bf16) {
+  return bf16 ? round_to_bf16(cos_for_bf16(arg)) : cosf(arg);
+}
+__device__ __forceinline__ float4 pack4(float4 v, int bf16) {
+  return bf16 ? make_float4(round_to_bf16(v.x), round_to_bf16(v.y), round_to_bf16(v.z), round_to_bf16(v.w)) : v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const T* __restrict__ mem) {
   const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (q >= eff_count(a.max_q, a.n_q)) return;
@@ -235,16 +252,16 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
   {
     for (int g = lane; g < gm + gt; g += 64) {
       if (g < gm) {
-        const float4 v = *(const float4*)(mem + node * dm + 4 * g);
+        const float4 v = load4(mem + node * dm + 4 * g);
         *(float4*)(a.q_in + q * Dq + 4 * g) = v;
         *(float4*)(a.m_in + q * (da + dm) + da + 4 * g) = v;
       } else {
         const int j = 4 * (g - gm);
         float4 o;
-        o.x = cosf(time_arg(a.tw[j], 0.f, a.tb[j]));
-        o.y = cosf(time_arg(a.tw[j + 1], 0.f, a.tb[j + 1]));
-        o.z = cosf(time_arg(a.tw[j + 2], 0.f, a.tb[j + 2]));
-        o.w = cosf(time_arg(a.tw[j + 3], 0.f, a.tb[j + 3]));
+        o.x = enc_val(time_arg(a.tw[j], 0.f, a.tb[j]), a.bf16);
+        o.y = enc_val(time_arg(a.tw[j + 1], 0.f, a.tb[j + 1]), a.bf16);
+        o.z = enc_val(time_arg(a.tw[j + 2], 0.f, a.tb[j + 2]), a.bf16);
+        o.w = enc_val(time_arg(a.tw[j + 3], 0.f, a.tb[j + 3]), a.bf16);
         *(float4*)(a.q_in + q * Dq + dm + j) = o;
       }
     }
@@ -264,7 +281,7 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
       const int ec = e < nm ? e : nm - 1;   // a valid group, stored only when e < nm
       const int sl = ec / gm, g = ec - sl * gm;
       const int64_t nb = __shfl(my_nb, sl, 64);
-      v[u] = *(const float4*)(mem + nb * dm + 4 * g);
+      v[u] = load4(mem + nb * dm + 4 * g);
       dst[u] = (off + sl) * D + 4 * g;
     }
 #pragma unroll
@@ -281,7 +298,7 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
       const int ec = e < nx ? e : nx - 1;
       const int sl = ec / ge, g = ec - sl * ge;
       const int64_t eid = __shfl(my_e, sl, 64);
-      v[u] = *(const float4*)(a.x + eid * de + 4 * g);
+      v[u] = pack4(*(const float4*)(a.x + eid * de + 4 * g), a.bf16);
       dst[u] = (off + sl) * D + dm + 4 * g;
     }
 #pragma unroll
@@ -297,10 +314,10 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const floa
     if (e < ntg) {
       const int j = 4 * g;
       float4 o;
-      o.x = cosf(time_arg(a.tw[j], delta, a.tb[j]));
-      o.y = cosf(time_arg(a.tw[j + 1], delta, a.tb[j + 1]));
-      o.z = cosf(time_arg(a.tw[j + 2], delta, a.tb[j + 2]));
-      o.w = cosf(time_arg(a.tw[j + 3], delta, a.tb[j + 3]));
+      o.x = enc_val(time_arg(a.tw[j], delta, a.tb[j]), a.bf16);
+      o.y = enc_val(time_arg(a.tw[j + 1], delta, a.tb[j + 1]), a.bf16);
+      o.z = enc_val(time_arg(a.tw[j + 2], delta, a.tb[j + 2]), a.bf16);
+      o.w = enc_val(time_arg(a.tw[j + 3], delta, a.tb[j + 3]), a.bf16);
       *(float4*)(a.kv_in + (off + sl) * D + dm + de + j) = o;
     }
   }
@@ -1162,10 +1179,12 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
   const unsigned gq = (unsigned)cdiv(sh.Q, 4);
   const GatherArgs ga{q_node, nbr, neid, n_q, sv.cnt, sv.pair_off, nt, q_t, edge_feat, tw, tb, max_q, sh.k, sh.dm,
                       sh.de, sh.dt, sh.da, bf, sv.q_in, sv.m_in, sv.kv_in, sv.pair_delta, sv.pair_nbr};
-  const bool v4 = !bf && sh.de % 4 == 0 && sh.dm % 4 == 0 && sh.dt % 4 == 0 && sh.da % 4 == 0 &&
-                  ((uintptr_t)memory & 15) == 0 && (sh.de == 0 || ((uintptr_t)edge_feat & 15) == 0);
-  if (v4)
-    k_attn_gather_v4<<<gq, 256, 0, s>>>(ga, (const float*)memory);
+  const bool v4 = sh.de % 4 == 0 && sh.dm % 4 == 0 && sh.dt % 4 == 0 && sh.da % 4 == 0 &&
+                  ((uintptr_t)memory & (bf ? 7 : 15)) == 0 && (sh.de == 0 || ((uintptr_t)edge_feat & 15) == 0);
+  if (v4 && !bf)
+    k_attn_gather_v4<float><<<gq, 256, 0, s>>>(ga, (const float*)memory);
+  else if (v4)
+    k_attn_gather_v4<uint16_t><<<gq, 256, 0, s>>>(ga, (const uint16_t*)memory);
   else if (!bf)
     k_attn_gather<float><<<gq, 256, 0, s>>>(ga, (const float*)memory);
   else
