@@ -760,7 +760,8 @@ __global__ void k_seg_bounds(const uint32_t* __restrict__ keys, int64_t n, uint3
   if (p == n - 1 || keys[p + 1] != k) seg_hi[k] = (int32_t)(p + 1);
 }
 
-constexpr int SEG_TILE = 64;     // sorted occurrences per wave
+constexpr int SEG_TILE = 64;     // sorted occurrences per wave (the attention's d M')
+constexpr int SEG_TILE_ROWS = 16;   // the same for segsum_rows (few occurrences: more, shorter waves)
 constexpr int SEG_MAXC = 8;      // columns per lane: width <= 512
 
 struct SegCtx {
@@ -779,6 +780,7 @@ struct SegCtx {
   float* tail;        // [ntiles, W]
   const int32_t* seg_lo;   // [rows] first sorted position of the row
   const int32_t* seg_hi;   // [rows] one past its last
+  int tile;                // sorted positions per wave (at most 64)
 };
 
 // A complete row of sums: columns < dm to D, the rest to S.
@@ -814,7 +816,7 @@ __device__ __forceinline__ void seg_row_nc(const SegCtx& c, uint32_t o, float* r
   }
 }
 
-// Wave per tile of SEG_TILE (= 64) sorted positions; lane i holds position
+// Wave per tile of c.tile (at most 64) sorted positions; lane i holds position
 // p0 + i.  The wave walks the positions in order with one running sum,
 // loading the rows of SEG_PREFETCH positions at a time (whatever segments
 // they belong to); when the key changes, the finished segment is stored.  A
@@ -828,9 +830,9 @@ template <int NC>
 __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int64_t p0 = tile * SEG_TILE;
+  const int64_t p0 = tile * c.tile;
   if (p0 >= c.n_occ) return;
-  const int cnt = (int)min((int64_t)SEG_TILE, c.n_occ - p0);
+  const int cnt = (int)min((int64_t)c.tile, c.n_occ - p0);
   const int W = c.dm + c.w2;
   const uint32_t my_key = lane < cnt ? c.keys[p0 + lane] : c.sentinel;
   const uint32_t my_val = lane < cnt ? c.vals[p0 + lane] : 0u;
@@ -920,9 +922,9 @@ __device__ __forceinline__ void seg_flush_v4(const SegCtx& c, int64_t tile, uint
 __global__ __launch_bounds__(256) void k_segsum_tiles_v4(SegCtx c) {
   const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int64_t p0 = tile * SEG_TILE;
+  const int64_t p0 = tile * c.tile;
   if (p0 >= c.n_occ) return;
-  const int cnt = (int)min((int64_t)SEG_TILE, c.n_occ - p0);
+  const int cnt = (int)min((int64_t)c.tile, c.n_occ - p0);
   const int W = c.dm + c.w2, W4 = W >> 2, dm4 = c.dm >> 2;
   const int qa = lane, qb = lane + 64;   // this lane's column groups
   const uint32_t my_key = lane < cnt ? c.keys[p0 + lane] : c.sentinel;
@@ -1002,12 +1004,12 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
   }
   // the rest depends on the block only (uniform branches around the barrier)
   if (blk >= ntiles) return;
-  const int64_t p_last = min((blk + 1) * SEG_TILE, c.n_occ) - 1;
+  const int64_t p_last = min((blk + 1) * c.tile, c.n_occ) - 1;
   if (p_last + 1 >= c.n_occ) return;
   const uint32_t key = c.keys[p_last];
   if (key == c.sentinel || c.keys[p_last + 1] != key) return;
-  if (c.seg_lo[key] < blk * SEG_TILE) return;   // started in an earlier tile, whose block sums it
-  const int64_t t1 = (c.seg_hi[key] - 1) / SEG_TILE;
+  if (c.seg_lo[key] < blk * c.tile) return;   // started in an earlier tile, whose block sums it
+  const int64_t t1 = (c.seg_hi[key] - 1) / c.tile;
   float acc[SEG_MAXC];
 #pragma unroll
   for (int i = 0; i < SEG_MAXC; ++i) acc[i] = 0.f;
@@ -1104,7 +1106,66 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   return v;
 }
 
+__global__ void k_seg_clear(int32_t* __restrict__ seg_lo, int32_t* __restrict__ seg_hi, int64_t n) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < n) seg_lo[r] = seg_hi[r] = 0;
+}
+
 }  // namespace
+
+size_t segsum_rows_ws_bytes(int64_t n_occ, int64_t max_rows, int dm) {
+  const int64_t nt = cdiv(n_occ < 1 ? 1 : n_occ, SEG_TILE_ROWS), mr = max_rows < 1 ? 1 : max_rows;
+  return 2 * a256(sizeof(int32_t) * mr) + 2 * a256(sizeof(float) * nt * dm);
+}
+
+mtgnn_status segsum_rows(const uint32_t* skeys, const uint32_t* svals, int64_t n_occ, const float* src, int64_t ld,
+                         int dm, const int32_t* n_rows, int64_t max_rows, float* D, void* ws, size_t ws_bytes,
+                         hipStream_t s) {
+  if (dm < 1 || dm > 512) return MTGNN_EUNSUPPORTED;
+  if (ws_bytes < segsum_rows_ws_bytes(n_occ, max_rows, dm)) return MTGNN_EWORKSPACE;
+  if (max_rows <= 0) return MTGNN_OK;
+  const int64_t ntiles = cdiv(n_occ < 1 ? 1 : n_occ, SEG_TILE_ROWS);
+  char* w = (char*)ws;
+  SegCtx c{};
+  c.tile = SEG_TILE_ROWS;
+  c.seg_lo = (int32_t*)w;
+  w += a256(sizeof(int32_t) * max_rows);
+  c.seg_hi = (int32_t*)w;
+  w += a256(sizeof(int32_t) * max_rows);
+  c.head = (float*)w;
+  w += a256(sizeof(float) * ntiles * dm);
+  c.tail = (float*)w;
+  // every occurrence reads its row from src (all of them are "query" rows; no slot part)
+  c.keys = skeys; c.vals = svals; c.n_occ = n_occ; c.sentinel = (uint32_t)max_rows; c.max_q = n_occ;
+  c.dhq = src; c.ldq = ld; c.dkv = nullptr; c.dm = dm; c.w2 = 0; c.S = nullptr; c.D = D;
+  k_seg_clear<<<(unsigned)cdiv(max_rows, 256), 256, 0, s>>>((int32_t*)c.seg_lo, (int32_t*)c.seg_hi, max_rows);
+  MTGNN_CHECK_LAUNCH("seg_clear");
+  if (n_occ > 0) {
+    k_seg_bounds<<<(unsigned)cdiv(n_occ, 256), 256, 0, s>>>(skeys, n_occ, c.sentinel, (int32_t*)c.seg_lo,
+                                                             (int32_t*)c.seg_hi);
+    MTGNN_CHECK_LAUNCH("seg_bounds");
+    const unsigned gt = (unsigned)cdiv(ntiles, 4);
+    if (dm % 4 == 0 && ld % 4 == 0 && ((uintptr_t)src | (uintptr_t)D) % 16 == 0) {
+      k_segsum_tiles_v4<<<gt, 256, 0, s>>>(c);
+    } else {
+      switch (cdiv(dm, 64)) {
+        case 1: k_segsum_tiles<1><<<gt, 256, 0, s>>>(c); break;
+        case 2: k_segsum_tiles<2><<<gt, 256, 0, s>>>(c); break;
+        case 3: k_segsum_tiles<3><<<gt, 256, 0, s>>>(c); break;
+        case 4: k_segsum_tiles<4><<<gt, 256, 0, s>>>(c); break;
+        case 5: k_segsum_tiles<5><<<gt, 256, 0, s>>>(c); break;
+        case 6: k_segsum_tiles<6><<<gt, 256, 0, s>>>(c); break;
+        case 7: k_segsum_tiles<7><<<gt, 256, 0, s>>>(c); break;
+        default: k_segsum_tiles<8><<<gt, 256, 0, s>>>(c); break;
+      }
+    }
+    MTGNN_CHECK_LAUNCH("segsum_tiles");
+  }
+  const int64_t nfix = ntiles > cdiv(max_rows, FIX_WAVES) ? ntiles : cdiv(max_rows, FIX_WAVES);
+  k_segsum_fixup<<<(unsigned)nfix, 64 * FIX_WAVES, 0, s>>>(c, n_rows, max_rows, n_occ > 0 ? ntiles : 0);
+  MTGNN_CHECK_LAUNCH("segsum_fixup");
+  return MTGNN_OK;
+}
 
 size_t attn_save_bytes(const mtgnn_dims* d, int64_t max_q) { return carve_save(nullptr, AttnShape(d, max_q)).total; }
 
@@ -1281,7 +1342,7 @@ mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSav
     c.keys = (uint32_t*)skeys; c.vals = (uint32_t*)svals; c.n_occ = n_occ; c.sentinel = sentinel; c.max_q = max_q;
     c.seg_lo = b.seg_lo; c.seg_hi = b.seg_hi;
     c.dhq = b.dm_in + da; c.ldq = ldm; c.dkv = b.dKV; c.dm = dm; c.w2 = 2 * da;
-    c.S = b.S; c.D = d_mem; c.head = b.head; c.tail = b.tail;
+    c.S = b.S; c.D = d_mem; c.head = b.head; c.tail = b.tail; c.tile = SEG_TILE;
     const int64_t ntiles = cdiv(n_occ, SEG_TILE);
     const unsigned gt = (unsigned)cdiv(ntiles, 4);
     if (dm % 4 == 0 && da % 4 == 0 && dm + 2 * da <= 512) {   // 16-byte aligned rows and groups

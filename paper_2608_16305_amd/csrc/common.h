@@ -153,4 +153,13 @@ mtgnn_status colsum(const float* X, int64_t ld, int64_t rows, const int32_t* row
 
 int bits_for(int64_t max_value);   // bits needed to hold values 0..max_value
 
+// Deterministic per-row sums over occurrences sorted by row (attention.hip): D[r] (row stride dm) = the sum,
+// over the sorted positions p with skeys[p] == r and in that order, of src[svals[p]] (row stride ld, dm
+// columns); rows r below the device row count with no occurrence get zeros.  Keys past the rows are
+// `max_rows` (they sort last).  dm <= 512.
+size_t segsum_rows_ws_bytes(int64_t n_occ, int64_t max_rows, int dm);
+mtgnn_status segsum_rows(const uint32_t* skeys, const uint32_t* svals, int64_t n_occ, const float* src, int64_t ld,
+                         int dm, const int32_t* n_rows, int64_t max_rows, float* D, void* ws, size_t ws_bytes,
+                         hipStream_t s);
+
 }  // namespace mtgnn

@@ -282,6 +282,8 @@ struct ProjBwdWs {
   size_t sort_bytes;
   void* cs_ws;
   size_t cs_bytes;
+  void* seg_ws;      // the per-row sums of d M', for up to max_q updated rows
+  size_t seg_bytes;
   size_t total;
 };
 
@@ -304,6 +306,8 @@ static ProjBwdWs proj_bwd_layout(void* ws, const mtgnn_dims* d, int64_t max_q) {
   L.sort_ws = take(L.sort_bytes);
   L.cs_bytes = colsum_ws_bytes(mq, 2 * d->d_mem);
   L.cs_ws = take(L.cs_bytes);
+  L.seg_bytes = segsum_rows_ws_bytes(mq, mq, d->d_mem);
+  L.seg_ws = take(L.seg_bytes);
   L.total = off;
   return L;
 }
@@ -344,7 +348,9 @@ mtgnn_status time_projection_bwd_impl(const int32_t* q_node, const float* q_t, c
     if (max_q > 0) MTGNN_TRY(radix_sort_pairs(&sk, &sv, max_q, bits_for(max_rows), L.sort_ws, L.sort_bytes, s));
     const unsigned g = (unsigned)cdiv(max_rows, 4);
     const bool lanes = dm % 4 == 0 && dm <= 128 && ((uintptr_t)L.Cq | (uintptr_t)d_mem) % 16 == 0;
-    if (lanes)
+    if (max_rows <= (max_q < 1 ? 1 : max_q) && dm <= 512)   // tiles of sorted occurrences, then the rows that span tiles
+      MTGNN_TRY(segsum_rows(sk, sv, max_q, L.Cq, dm, dm, n_rows, max_rows, d_mem, L.seg_ws, L.seg_bytes, s));
+    else if (lanes)
       k_jodie_dmem_lanes<32><<<g, 256, 0, s>>>(sk, sv, max_q, L.Cq, n_rows, max_rows, dm, d_mem);
     else if (d->dtype == MTGNN_BF16)
       k_jodie_dmem<uint16_t><<<g, 256, 0, s>>>(sk, sv, max_q, q_node, q_t, lu, Wp, bp, scale, dz, n_rows, max_rows, dm,
