@@ -152,8 +152,9 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
   if (link_fused_ok(da)) {
     MTGNN_TRY(link_fused(z, n_q, max_q, da, p->W_d1, p->b_d1, p->W_d2, p->b_d2, L.Wp, L.DA, L.DB, L.part, dz, scores,
                          g->W_d2, g->b_d2, loss, s));
-    const DwProblem dp[2] = {{L.DA, da, z, da, g->W_d1, 2 * da, da, da, g->b_d1},
-                             {L.DB, da, z, da, g->W_d1 + da, 2 * da, da, da, L.db_scratch}};
+    // DA is zero past the src block (the first third of the query rows), DB on it
+    const DwProblem dp[2] = {{L.DA, da, z, da, g->W_d1, 2 * da, da, da, g->b_d1, 0, 1, 3},
+                             {L.DB, da, z, da, g->W_d1 + da, 2 * da, da, da, L.db_scratch, 1, 3, 3}};
     return linear_dw_batch(dp, 2, max_q, n_q, MTGNN_F32, L.rest, L.rest_bytes, s);
   }
   // general widths: the first layer's two halves over every query row

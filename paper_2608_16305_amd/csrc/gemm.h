@@ -962,6 +962,9 @@ struct DwProblem {
   int64_t lddw;
   int64_t N, K;
   float* db;
+  // Optional (row_den > 0): dy is zero outside rows [R row_lo / row_den, R row_hi / row_den) of the R rows (the
+  // device count), so the output-stationary kernel skips the rest (the strip kernel sums them all).
+  int row_lo = 0, row_hi = 0, row_den = 0;
 };
 size_t linear_dw_batch_ws_bytes(int64_t R, const int64_t* N, const int64_t* K, int n);   // sizes only
 
@@ -975,6 +978,7 @@ struct DwOsProblem {
   int64_t ldy;
   float* part;
   int nx, ny, b_begin, nblk;
+  int row_lo = 0, row_hi = 0, row_den = 0;   // row_den > 0: only rows [R lo / den, R hi / den) of the R can be nonzero
 };
 constexpr int DW_OS_MAXP = 16;   // problems (or output tiles) per launch
 struct DwOsBatch {

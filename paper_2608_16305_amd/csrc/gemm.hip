@@ -194,10 +194,16 @@ bool dw_os_shapes_ok(const int64_t* N, const int64_t* K, int n) {
   return true;
 }
 
-// Blocks per problem out of `total`, in proportion to the MFMAs per chunk (7 x 2 or 7 x 4 tiles a wave).
-void dw_os_split(const int64_t* K, int n, int total, int* nblk) {
+// Blocks per problem out of `total`, in proportion to the MFMAs per chunk (7 x 2 or 7 x 4 tiles a wave) times
+// the share of the rows the problem reads (row_den > 0: (row_hi - row_lo) / row_den, else all).
+void dw_os_split(const int64_t* K, int n, int total, int* nblk, const DwProblem* ps = nullptr) {
   int w[G_MAXBATCH], sum = 0;
-  for (int i = 0; i < n; ++i) sum += (w[i] = cdiv(K[i] + 1, 16) <= 7 ? 2 : 4);
+  for (int i = 0; i < n; ++i) {
+    w[i] = (cdiv(K[i] + 1, 16) <= 7 ? 2 : 4) * 12;
+    if (ps && ps[i].row_den > 0) w[i] = w[i] * (ps[i].row_hi - ps[i].row_lo) / ps[i].row_den;
+    if (w[i] < 1) w[i] = 1;
+    sum += w[i];
+  }
   int used = 0;
   for (int i = 0; i < n; ++i) {
     nblk[i] = (int)((int64_t)total * w[i] / sum);
@@ -208,12 +214,10 @@ void dw_os_split(const int64_t* K, int n, int total, int* nblk) {
     while (nblk[i] > 1 && used > total) --nblk[i], --used;
 }
 
-size_t dw_os_ws(const int64_t* N, const int64_t* K, int n, int total) {
-  int nblk[G_MAXBATCH];
-  dw_os_split(K, n, total, nblk);
-  size_t b = 0;
-  for (int i = 0; i < n; ++i) b += (sizeof(float) * (size_t)nblk[i] * N[i] * (K[i] + 1) + 255) & ~size_t(255);
-  return b;
+size_t dw_os_ws(const int64_t* N, const int64_t* K, int n, int total) {   // any split of `total` blocks fits
+  size_t per = 0;
+  for (int i = 0; i < n; ++i) per = std::max(per, sizeof(float) * (size_t)N[i] * (K[i] + 1));
+  return per * (size_t)total + 256 * (size_t)n;
 }
 
 }  // namespace
@@ -244,7 +248,7 @@ mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_
   if (os) {   // one block per CU, blocks split over the problems; fixed-order reduce of the partials
     const int total = std::min(dw_os_cu_count(), DW_OS_MAX_BLOCKS);
     int nblk[G_MAXBATCH];
-    dw_os_split(Ks, n, total, nblk);
+    dw_os_split(Ks, n, total, nblk, ps);
     DwOsBatch b{};
     ReduceBatch rb{};
     b.n = rb.n = n;
@@ -256,7 +260,7 @@ mtgnn_status linear_dw_batch(const DwProblem* ps, int n, int64_t R, const int32_
       const DwProblem& q = ps[i];
       const int64_t per = q.N * (q.K + 1);
       b.p[i] = DwOsProblem{q.dy, q.lddy, (const float*)q.x, q.ldx, (float*)w, (int)q.N, (int)q.K, (int)begin,
-                           nblk[i]};
+                           nblk[i], q.row_lo, q.row_hi, q.row_den};
       rb.p[i] = ReduceProblem{(const float*)w, per, nblk[i], q.N, q.K + 1, q.dW, q.lddw, q.K, q.db};
       w += (sizeof(float) * (size_t)nblk[i] * per + 255) & ~size_t(255);
       begin += nblk[i];

@@ -579,8 +579,14 @@ __global__ __launch_bounds__(G_THREADS, 1) void k_dw_os(DwOsBatch b) {
 #pragma unroll
   for (int k = 1; k < DW_OS_MAXP; ++k)
     if (k < b.n && bx >= b.p[k].b_begin) pi = k;
-  const DwOsProblem q = b.p[pi];
-  const int64_t rows = eff_count(b.R, b.R_dev);
+  DwOsProblem q = b.p[pi];
+  int64_t rows = eff_count(b.R, b.R_dev);
+  if (q.row_den > 0) {   // only this row range can be nonzero: the rows are taken from its start
+    const int64_t lo = rows * q.row_lo / q.row_den, hi = rows * q.row_hi / q.row_den;
+    q.X += lo * q.ldx;
+    q.Y += lo * q.ldy;
+    rows = hi > lo ? hi - lo : 0;
+  }
   if (q.ny + 1 <= 16 * 7) dw_os_body<7, 7>(q, rows, bx - q.b_begin, lds);
   else dw_os_body<7, 13>(q, rows, bx - q.b_begin, lds);
 }
