@@ -387,12 +387,12 @@ class DeviceEvent:
         _hip_check(self._rt.hipStreamWaitEvent(_stream(stream), self.handle, C.c_uint(0)), "hipStreamWaitEvent")
 
     def __del__(self):
-        if getattr(self, "handle", None) and self.handle.value:
-            try:   # may run at interpreter exit, after the runtime is gone
+        try:   # may run at interpreter exit, after the runtime (or this module's globals) are gone
+            if getattr(self, "handle", None) and self.handle.value:
                 self._rt.hipEventDestroy(self.handle)
-            except Exception:
-                pass
-            self.handle = C.c_void_p()
+                self.handle = None
+        except Exception:
+            pass
 
 
 def _event(e, name):
