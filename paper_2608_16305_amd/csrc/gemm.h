@@ -704,16 +704,16 @@ void gemm_set_vec_flags(GemmArgs& g) {   // general loader: 4-wide only when ali
 }
 
 bool gemm_rs_applicable(const GemmArgs& g);
-mtgnn_status gemm_rs_launch(const GemmArgs& g, hipStream_t s);
+mtgnn_status gemm_rs_launch(const GemmArgs& g, hipStream_t s, bool bf16_weights = false);
 
 template <class Site, typename TA, typename TB, bool AK, bool BK>
 mtgnn_status gemm_launch_t(const GemmArgs& g0, int ksplit, hipStream_t s) {
-  if constexpr (std::is_same<Site, site::KvProj>::value && std::is_same<TA, float>::value &&
-                std::is_same<TB, float>::value && AK && BK) {
-    // key/value projection over the neighbour slots: weight-stationary kernel (gemm_rs.h)
+  if constexpr (std::is_same<Site, site::KvProj>::value && std::is_same<TA, float>::value && AK && BK) {
+    // key/value projection over the neighbour slots: weight-stationary kernel (gemm_rs.h), with float32 or
+    // bfloat16 weights (the slot rows are float32 holding bfloat16 values in that mode)
     if (ksplit <= 1 && gemm_rs_applicable(g0)) {
       TimedScope ts(Site::name, s);
-      return gemm_rs_launch(g0, s);
+      return gemm_rs_launch(g0, s, std::is_same<TB, uint16_t>::value);
     }
   }
   GemmArgs g = g0;

@@ -41,8 +41,13 @@ constexpr int stride_for(int kc) {   // smallest stride >= 16 kc floats with str
 // Grid: blocks of 256 threads; block b handles row tiles b, b + gridDim.x, ...
 // Requirements (checked by gemm_rs_ok on the host): A 16-byte aligned, a_sk = 1,
 // a_si % 4 == 0, K % 4 == 0, 16 (KC - 1) < K <= 16 KC <= 256, N <= 16 NCT.
-template <class Site, int NCT, int KC, int OCC>
+//
+// TB = uint16_t (bfloat16 weights): the products run on v_mfma_f32_16x16x16_bf16, one per tile and chunk,
+// with the register share of B packed to bfloat16 pairs.  A's rows are the bfloat16 mode's neighbour-slot
+// inputs, which their producer stores already rounded to bfloat16, so their high halves are exact.
+template <class Site, int NCT, int KC, int OCC, typename TB = float>
 __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
+  constexpr bool BF = std::is_same<TB, uint16_t>::value;
   constexpr int NTW = NCT / 4, NR = NCT % 4;
   constexpr int KQ = (KC + 3) / 4;                 // remainder chunks per wave, at most
   constexpr int KS = rs::stride_for(KC);           // A row stride in LDS (floats)
@@ -61,7 +66,7 @@ __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int fr = lane & 15, fg = lane >> 4;
   const float* A = (const float*)g.A;
-  const float* B = (const float*)g.B;
+  const TB* B = (const TB*)g.B;
   const uint32_t base = (uint32_t)(uintptr_t)(lds_void_ptr)lds;
   const uint32_t red_base = base + 2u * SLOT * 4u;
 
@@ -87,10 +92,16 @@ __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
   issue(b0, 0);
 
   // B in registers (zero past K and N), then the bias of the register tiles
-  float bw[NTW][KC][4];
-  float br[NR > 0 ? NR : 1][KQ][4];
+  // float32 weights as floats; bfloat16 weights packed four to a register pair (the MFMA operand)
+  float bw[BF ? 1 : NTW][BF ? 1 : KC][4];
+  float br[BF || NR == 0 ? 1 : NR][BF ? 1 : KQ][4];
+  s16x4 bwp[BF ? NTW : 1][BF ? KC : 1];
+  s16x4 brp[BF && NR > 0 ? NR : 1][BF ? KQ : 1];
   auto bval = [&](int64_t k, int64_t j) -> float {
-    return (k < K && j < N) ? B[k * g.b_sk + j * g.b_sj] : 0.f;
+    return (k < K && j < N) ? Elem<TB>::load(B, k * g.b_sk + j * g.b_sj) : 0.f;
+  };
+  auto braw = [&](int64_t k, int64_t j) -> short {   // bfloat16 bits (zero outside B)
+    return (k < K && j < N) ? (short)reinterpret_cast<const uint16_t*>(B)[k * g.b_sk + j * g.b_sj] : (short)0;
   };
 #pragma unroll
   for (int t = 0; t < NTW; ++t) {
@@ -98,7 +109,9 @@ __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
       const int64_t k = 16 * c + 4 * fg;
-      if (g.b_vec && k + 3 < K && j < N) {   // b_vec: B contiguous along k and 16-byte aligned
+      if constexpr (BF) {
+        bwp[t][c] = s16x4{braw(k, j), braw(k + 1, j), braw(k + 2, j), braw(k + 3, j)};
+      } else if (g.b_vec && k + 3 < K && j < N) {   // b_vec: B contiguous along k and 16-byte aligned
         const float4 v = *reinterpret_cast<const float4*>(B + j * g.b_sj + k);
         bw[t][c][0] = v.x; bw[t][c][1] = v.y; bw[t][c][2] = v.z; bw[t][c][3] = v.w;
       } else {
@@ -113,8 +126,13 @@ __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
 #pragma unroll
     for (int cc = 0; cc < KQ; ++cc) {
       const int c = 4 * cc + wid;
+      const int64_t k = 16 * c + 4 * fg;
+      if constexpr (BF) {
+        brp[q][cc] = c < KC ? s16x4{braw(k, j), braw(k + 1, j), braw(k + 2, j), braw(k + 3, j)} : s16x4{0, 0, 0, 0};
+      } else {
 #pragma unroll
-      for (int s = 0; s < 4; ++s) br[q][cc][s] = c < KC ? bval(16 * c + 4 * fg + s, j) : 0.f;
+        for (int s = 0; s < 4; ++s) br[q][cc][s] = c < KC ? bval(k + s, j) : 0.f;
+      }
     }
   }
   float bias_w[NTW], bias_r[NR > 0 ? NR : 1];
@@ -189,23 +207,40 @@ __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
       // chunk's read: its MFMAs cannot be hoisted above that read, so the read's latency
       // hides behind them (and the two fragments never share registers)
       dma::tie(af[c]);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
+      if constexpr (BF) {
+        const s16x4 ap = bf16x4_exact(float4{af[c][0], af[c][1], af[c][2], af[c][3]});
 #pragma unroll
         for (int t = 0; t < NTW; ++t)
-          cu_w[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[c][s], bw[t][c][s], cu_w[t], 0, 0, 0);
-        if (s == 1 && prev) {   // previous tile, register results: two rows of a tile per chunk, early in
-                                // the tile so they complete before the next tile's vmcnt(0)
+          cu_w[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ap, bwp[t][c], cu_w[t], 0, 0, 0);
+        if (prev) {   // previous tile, register results: two rows of a tile per chunk
 #pragma unroll
           for (int k = 2 * c; k < 4 * NTW && k < 2 * c + 2; ++k) store_reg(prow0, k / 4, k % 4, st_w[k / 4][k % 4]);
         }
-      }
-      if (NR > 0 && (c & 3) == wid) {
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
+        if (NR > 0 && (c & 3) == wid) {
 #pragma unroll
           for (int q = 0; q < NR; ++q)
-            cu_r[q] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[c][s], br[q][c / 4][s], cu_r[q], 0, 0, 0);
+            cu_r[q] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ap, brp[q][c / 4], cu_r[q], 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+#pragma unroll
+          for (int t = 0; t < NTW; ++t)
+            cu_w[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[c][s], bw[t][c][s], cu_w[t], 0, 0, 0);
+          if (s == 1 && prev) {   // previous tile, register results: two rows of a tile per chunk, early in
+                                  // the tile so they complete before the next tile's vmcnt(0)
+#pragma unroll
+            for (int k = 2 * c; k < 4 * NTW && k < 2 * c + 2; ++k)
+              store_reg(prow0, k / 4, k % 4, st_w[k / 4][k % 4]);
+          }
+        }
+        if (NR > 0 && (c & 3) == wid) {
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int q = 0; q < NR; ++q)
+              cu_r[q] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[c][s], br[q][c / 4][s], cu_r[q], 0, 0, 0);
+        }
       }
       if (reducer) {   // previous tile, remainder q: partials read at chunk 2q, summed and stored at 2q + 1
 #pragma unroll
@@ -259,7 +294,7 @@ __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
 // heads) and the fp32 operands meet the kernel's requirements.  gemm_rs_launch
 // launches it with one block per CU (at most one per 16-row tile).
 bool gemm_rs_applicable(const GemmArgs& g);
-mtgnn_status gemm_rs_launch(const GemmArgs& g, hipStream_t s);
+mtgnn_status gemm_rs_launch(const GemmArgs& g, hipStream_t s, bool bf16_weights);
 
 }  // namespace mtgnn
 

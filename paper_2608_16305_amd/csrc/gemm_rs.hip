@@ -26,13 +26,19 @@ bool gemm_rs_applicable(const GemmArgs& g) {
          !g.accumulate && !g.relu && g.gate == nullptr && !g.round_bf16 && g.tg_part == nullptr && cu_count() > 0;
 }
 
-mtgnn_status gemm_rs_launch(const GemmArgs& g0, hipStream_t s) {
+mtgnn_status gemm_rs_launch(const GemmArgs& g0, hipStream_t s, bool bf16_weights) {
   GemmArgs g = g0;
-  g.b_vec = (g.b_sk == 1 && vec_ok(g.B, g.b_sj, sizeof(float))) ? 1 : 0;
+  g.b_vec = (!bf16_weights && g.b_sk == 1 && vec_ok(g.B, g.b_sj, sizeof(float))) ? 1 : 0;
   const int64_t tiles = cdiv(g.M, 16);
   const unsigned grid = (unsigned)(tiles < cu_count() ? tiles : cu_count());
-  if (cdiv(g.K, 16) == 13) k_gemm_rs<site::KvProj, 13, 13, 1><<<grid, G_THREADS, 0, s>>>(g);
-  else k_gemm_rs<site::KvProj, 13, 14, 1><<<grid, G_THREADS, 0, s>>>(g);
+  if (bf16_weights) {
+    if (cdiv(g.K, 16) == 13) k_gemm_rs<site::KvProj, 13, 13, 1, uint16_t><<<grid, G_THREADS, 0, s>>>(g);
+    else k_gemm_rs<site::KvProj, 13, 14, 1, uint16_t><<<grid, G_THREADS, 0, s>>>(g);
+  } else if (cdiv(g.K, 16) == 13) {
+    k_gemm_rs<site::KvProj, 13, 13, 1><<<grid, G_THREADS, 0, s>>>(g);
+  } else {
+    k_gemm_rs<site::KvProj, 13, 14, 1><<<grid, G_THREADS, 0, s>>>(g);
+  }
   MTGNN_CHECK_LAUNCH("gemm_rs");
   return MTGNN_OK;
 }
