@@ -28,8 +28,15 @@ constexpr int XS = 212;   // LDS row stride (floats) of an activation tile: >= 2
 constexpr int MW = 4;     // waves per block; wave w computes the output column tiles w, w + 4, ...
 constexpr int PD = 3;     // weight chunks in flight ahead of the one being multiplied (6 measured slower)
 
-constexpr int RT1 = 1;   // row tiles per block of the single-layer kernels (query projection, d M', GRU dx);
-                          // 2 (half the weight-fragment loads per row) measured slower: half the blocks
+// Row tiles per block of the single-layer kernels (query projection, d M', GRU dx): one at a few thousand
+// rows (two, half the weight-fragment loads per row, measured slower there: half the blocks), two from
+// RT2_ROWS rows on, where the blocks far outnumber the CUs and the weight reads dominate.
+constexpr int RT2_ROWS = 16384;
+template <class F>
+void with_row_tiles(int64_t rows, F f) {
+  if (rows >= RT2_ROWS) f(std::integral_constant<int, 2>{});
+  else f(std::integral_constant<int, 1>{});
+}
 
 template <int NCT> struct Tiles { static constexpr int per_wave = (NCT + MW - 1) / MW; };
 
@@ -73,21 +80,26 @@ __device__ __forceinline__ void layer(const float* X, const float* __restrict__ 
 }
 
 // rows r0 .. r0 + 16 RT - 1 (those < M) of a row-major [M, n] matrix into an LDS tile at column offset col0
-// (n <= XSS - col0).  Every load of a thread is issued before its first LDS store, so the tile costs one
-// memory latency, not one per 64 MW elements.
+// (n <= XSS - col0; r0 < M).  Every load of a thread is issued before its first LDS store, so the tile costs
+// one memory latency, not one per 64 MW elements: the loads are unconditional (a slot past the tile or past
+// row M - 1 reads an element of the tile's last valid row and keeps zero), since a load under a per-lane
+// condition is compiled into a branch of its own that waits for it.
 template <int XSS = XS, int RT = 1, int NTH = 64 * MW>
 __device__ __forceinline__ void load_rows(float* X, int col0, const float* __restrict__ src, int64_t ld, int n,
                                           int64_t r0, int64_t M) {
   constexpr int PER = (16 * RT * (XSS / 4) + NTH - 1) / NTH;
   const int nq = n / 4, tot = 16 * RT * nq;
   if (nq <= 0) return;
+  const int64_t last = M - 1 - r0;   // >= 0: the tile's last valid row
   float4 v[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int e = threadIdx.x + NTH * k;
-    const int r = e / nq, q = e % nq;
-    v[k] = e < tot && r0 + r < M ? *reinterpret_cast<const float4*>(src + (r0 + r) * ld + 4 * q)
-                                 : float4{0.f, 0.f, 0.f, 0.f};
+    const int ec = e < tot ? e : tot - 1;
+    const int r = ec / nq, q = ec % nq;
+    const bool ok = e < tot && r <= last;
+    const float4 x = *reinterpret_cast<const float4*>(src + (r0 + (r <= last ? r : last)) * ld + 4 * q);
+    v[k] = ok ? x : float4{0.f, 0.f, 0.f, 0.f};
   }
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -307,61 +319,61 @@ struct QLayout {
 // the same for every query, so qv = W_q[:, :dm] M[q] + c with c = b_q + W_q[:, dm:] phi(0) (formed
 // once by the weight preparation): the product runs over the dm memory columns of q_in (row stride
 // D_q).  Wp: W_q[:, :dm] padded.
-template <int NA, int KM>
+template <int NA, int KM, int RT>
 __global__ __launch_bounds__(64 * MW) void k_qproj_fwd(const float* __restrict__ q_in, const float* __restrict__ Wp,
                                                        const float* __restrict__ cq, float* __restrict__ qv,
                                                        const int32_t* __restrict__ n_q, int64_t max_q, int da, int dm,
                                                        int Dq) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT * XS];
   const int64_t M = eff_count(max_q, n_q);
-  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT;
   if (r0 >= M) return;   // block-uniform
-  zero_cols<XS, RT1>(X0, dm, 16 * KM);
-  load_rows<XS, RT1>(X0, 0, q_in, Dq, dm, r0, M);
+  zero_cols<XS, RT>(X0, dm, 16 * KM);
+  load_rows<XS, RT>(X0, 0, q_in, Dq, dm, r0, M);
   __syncthreads();
-  f32x4 acc[RT1 * Tiles<NA>::per_wave];
-  layer<NA, KM, XS, RT1>(X0, Wp, acc);
-  each_out<NA, RT1>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT * Tiles<NA>::per_wave];
+  layer<NA, KM, XS, RT>(X0, Wp, acc);
+  each_out<NA, RT>(acc, da, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) qv[(r0 + i) * da + j] = v + cq[j];
   });
 }
 
 // dm_in[:, da:] += dqv W_q[:, :dm] (the memory part of the query input), WqT = W_q[:, :dm]^T padded.
-template <int NM, int NA>
+template <int NM, int NA, int RT>
 __global__ __launch_bounds__(64 * MW) void k_qproj_dx(const float* __restrict__ dqv, const float* __restrict__ WqT,
                                                       float* __restrict__ dm_in, int64_t ldm,
                                                       const int32_t* __restrict__ n_q, int64_t max_q, int da, int dm) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT * XS];
   const int64_t M = eff_count(max_q, n_q);
-  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT;
   if (r0 >= M) return;   // block-uniform
-  zero_cols<XS, RT1>(X0, da, 16 * NA);
-  load_rows<XS, RT1>(X0, 0, dqv, da, da, r0, M);
+  zero_cols<XS, RT>(X0, da, 16 * NA);
+  load_rows<XS, RT>(X0, 0, dqv, da, da, r0, M);
   __syncthreads();
-  f32x4 acc[RT1 * Tiles<NM>::per_wave];
-  layer<NM, NA, XS, RT1>(X0, WqT, acc);
-  each_out<NM, RT1>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT * Tiles<NM>::per_wave];
+  layer<NM, NA, XS, RT>(X0, WqT, acc);
+  each_out<NM, RT>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) dm_in[(r0 + i) * ldm + da + j] += v;
   });
 }
 
 // d_mem[:, :dm] += S[:, dm : dm + 2 da] W_kv[:, :dm] over 16-row tiles (S: the per-row sums of
 // [dh_q | dK | dV], row stride ldS; WkT = W_kv[:, :dm]^T padded).
-template <int NM, int KK>
+template <int NM, int KK, int RT>
 __global__ __launch_bounds__(64 * MW) void k_dmem_dx(const float* __restrict__ S, int64_t ldS,
                                                      const float* __restrict__ WkT, float* __restrict__ d_mem,
                                                      const int32_t* __restrict__ n_rows, int64_t max_rows, int dm,
                                                      int w2) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT * XS];
   const int64_t M = eff_count(max_rows, n_rows);
-  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT;
   if (r0 >= M) return;   // block-uniform
-  zero_cols<XS, RT1>(X0, w2, 16 * KK);
-  load_rows<XS, RT1>(X0, 0, S + dm, ldS, w2, r0, M);
+  zero_cols<XS, RT>(X0, w2, 16 * KK);
+  load_rows<XS, RT>(X0, 0, S + dm, ldS, w2, r0, M);
   __syncthreads();
-  f32x4 acc[RT1 * Tiles<NM>::per_wave];
-  layer<NM, KK, XS, RT1>(X0, WkT, acc);
-  each_out<NM, RT1>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT * Tiles<NM>::per_wave];
+  layer<NM, KK, XS, RT>(X0, WkT, acc);
+  each_out<NM, RT>(acc, dm, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) d_mem[(r0 + i) * dm + j] += v;
   });
 }
@@ -370,20 +382,20 @@ __global__ __launch_bounds__(64 * MW) void k_dmem_dx(const float* __restrict__ S
 // (3 dm wide); WT = W_ih[:, c0 : c0 + dt]^T zero-padded (gru_dx_weight_copy).
 constexpr int XS_GRU = 308;   // >= 304 (19 chunks of 16), XS_GRU / 4 odd
 
-template <int NT, int KC>
+template <int NT, int KC, int RT>
 __global__ __launch_bounds__(64 * MW) void k_gru_dx(const float* __restrict__ dgi, int64_t ldg,
                                                     const float* __restrict__ WT, float* __restrict__ out, int dt,
                                                     const int32_t* __restrict__ n_rows, int64_t max_rows, int K) {
-  __shared__ __attribute__((aligned(16))) float X0[16 * RT1 * XS_GRU];
+  __shared__ __attribute__((aligned(16))) float X0[16 * RT * XS_GRU];
   const int64_t M = eff_count(max_rows, n_rows);
-  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT1;
+  const int64_t r0 = (int64_t)blockIdx.x * 16 * RT;
   if (r0 >= M) return;   // block-uniform
-  zero_cols<XS_GRU, RT1>(X0, K, 16 * KC);
-  load_rows<XS_GRU, RT1>(X0, 0, dgi, ldg, K, r0, M);
+  zero_cols<XS_GRU, RT>(X0, K, 16 * KC);
+  load_rows<XS_GRU, RT>(X0, 0, dgi, ldg, K, r0, M);
   __syncthreads();
-  f32x4 acc[RT1 * Tiles<NT>::per_wave];
-  layer<NT, KC, XS_GRU, RT1>(X0, WT, acc);
-  each_out<NT, RT1>(acc, dt, r0, M, [&](int i, int j, bool ok, float v) {
+  f32x4 acc[RT * Tiles<NT>::per_wave];
+  layer<NT, KC, XS_GRU, RT>(X0, WT, acc);
+  each_out<NT, RT>(acc, dt, r0, M, [&](int i, int j, bool ok, float v) {
     if (ok) out[(r0 + i) * dt + j] = v;
   });
 }
@@ -790,11 +802,14 @@ mtgnn_status gru_dx_fused(const float* dgi, const float* WT, float* dmsg_time, c
                           int64_t max_rows, int dm, int dt, hipStream_t s) {
   if (max_rows <= 0) return MTGNN_OK;
   if (!aligned16(dgi) || !aligned16(WT)) return MTGNN_EUNSUPPORTED;
-  const unsigned grid = (unsigned)cdiv(max_rows, 16 * RT1);
-  if (cdiv(3 * dm, 16) == 19)
-    k_gru_dx<7, 19><<<grid, 64 * MW, 0, s>>>(dgi, 3 * dm, WT, dmsg_time, dt, n_rows, max_rows, 3 * dm);
-  else
-    k_gru_dx<2, 6><<<grid, 64 * MW, 0, s>>>(dgi, 3 * dm, WT, dmsg_time, dt, n_rows, max_rows, 3 * dm);
+  with_row_tiles(max_rows, [&](auto rt) {
+    constexpr int RT = decltype(rt)::value;
+    const unsigned grid = (unsigned)cdiv(max_rows, 16 * RT);
+    if (cdiv(3 * dm, 16) == 19)
+      k_gru_dx<7, 19, RT><<<grid, 64 * MW, 0, s>>>(dgi, 3 * dm, WT, dmsg_time, dt, n_rows, max_rows, 3 * dm);
+    else
+      k_gru_dx<2, 6, RT><<<grid, 64 * MW, 0, s>>>(dgi, 3 * dm, WT, dmsg_time, dt, n_rows, max_rows, 3 * dm);
+  });
   MTGNN_CHECK_LAUNCH("gru_dx");
   return MTGNN_OK;
 }
@@ -833,11 +848,14 @@ mtgnn_status dmem_dx_fused(const float* S, int64_t ldS, const float* Wp, float* 
   if (max_rows <= 0) return MTGNN_OK;
   if (!aligned16(S) || !aligned16(Wp) || (dm * sizeof(float)) % 16 != 0 || ldS % 4 != 0) return MTGNN_EUNSUPPORTED;
   const QLayout L(da, dm, dt);
-  const unsigned grid = (unsigned)cdiv(max_rows, 16 * RT1);
-  if (L.nm == 7)
-    k_dmem_dx<7, 13><<<grid, 64 * MW, 0, s>>>(S, ldS, Wp + L.off[2], d_mem, n_rows, max_rows, dm, 2 * da);
-  else
-    k_dmem_dx<2, 4><<<grid, 64 * MW, 0, s>>>(S, ldS, Wp + L.off[2], d_mem, n_rows, max_rows, dm, 2 * da);
+  with_row_tiles(max_rows, [&](auto rt) {
+    constexpr int RT = decltype(rt)::value;
+    const unsigned grid = (unsigned)cdiv(max_rows, 16 * RT);
+    if (L.nm == 7)
+      k_dmem_dx<7, 13, RT><<<grid, 64 * MW, 0, s>>>(S, ldS, Wp + L.off[2], d_mem, n_rows, max_rows, dm, 2 * da);
+    else
+      k_dmem_dx<2, 4, RT><<<grid, 64 * MW, 0, s>>>(S, ldS, Wp + L.off[2], d_mem, n_rows, max_rows, dm, 2 * da);
+  });
   MTGNN_CHECK_LAUNCH("dmem_dx");
   return MTGNN_OK;
 }
@@ -847,11 +865,14 @@ mtgnn_status qproj_fwd_fused(const float* q_in, const float* Wp, const float* cq
   if (max_q <= 0) return MTGNN_OK;
   if (!aligned16(q_in) || !aligned16(Wp) || (dm + dt) % 4 != 0) return MTGNN_EUNSUPPORTED;
   const QLayout L(da, dm, dt);
-  const unsigned grid = (unsigned)cdiv(max_q, 16 * RT1);
-  if (L.na == 7)
-    k_qproj_fwd<7, 7><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], cq, qv, n_q, max_q, da, dm, dm + dt);
-  else
-    k_qproj_fwd<2, 2><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], cq, qv, n_q, max_q, da, dm, dm + dt);
+  with_row_tiles(max_q, [&](auto rt) {
+    constexpr int RT = decltype(rt)::value;
+    const unsigned grid = (unsigned)cdiv(max_q, 16 * RT);
+    if (L.na == 7)
+      k_qproj_fwd<7, 7, RT><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], cq, qv, n_q, max_q, da, dm, dm + dt);
+    else
+      k_qproj_fwd<2, 2, RT><<<grid, 64 * MW, 0, s>>>(q_in, Wp + L.off[0], cq, qv, n_q, max_q, da, dm, dm + dt);
+  });
   MTGNN_CHECK_LAUNCH("qproj_fwd");
   return MTGNN_OK;
 }
@@ -861,11 +882,14 @@ mtgnn_status qproj_dx_fused(const float* dqv, const float* Wp, float* dm_in, int
   if (max_q <= 0) return MTGNN_OK;
   if (!aligned16(dqv) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
   const QLayout L(da, dm, dt);
-  const unsigned grid = (unsigned)cdiv(max_q, 16 * RT1);
-  if (L.na == 7)
-    k_qproj_dx<7, 7><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
-  else
-    k_qproj_dx<2, 2><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
+  with_row_tiles(max_q, [&](auto rt) {
+    constexpr int RT = decltype(rt)::value;
+    const unsigned grid = (unsigned)cdiv(max_q, 16 * RT);
+    if (L.na == 7)
+      k_qproj_dx<7, 7, RT><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
+    else
+      k_qproj_dx<2, 2, RT><<<grid, 64 * MW, 0, s>>>(dqv, Wp + L.off[1], dm_in, ldm, n_q, max_q, da, dm);
+  });
   MTGNN_CHECK_LAUNCH("qproj_dx");
   return MTGNN_OK;
 }
