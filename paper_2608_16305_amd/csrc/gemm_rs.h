@@ -91,60 +91,111 @@ __global__ __launch_bounds__(G_THREADS, OCC) void k_gemm_rs(GemmArgs g) {
   }
   issue(b0, 0);
 
-  // B in registers (zero past K and N), then the bias of the register tiles
-  // float32 weights as floats; bfloat16 weights packed four to a register pair (the MFMA operand)
+  // B in registers (zero past K and N), then the bias of the register tiles; float32 weights as floats,
+  // bfloat16 weights packed four to a register pair (the MFMA operand).  No load sits under a per-lane
+  // condition: such a load is compiled into a branch of its own that waits for it, one memory round trip
+  // per load.  The host admits only 16 (KC - 1) < K <= 16 KC and 16 (NCT - 1) < N <= 16 NCT, so only chunk
+  // KC - 1 reaches past K, and with NR > 0 every register tile lies left of column 16 (NCT - 1) < N: those
+  // loads need no test at all.  The others read a clamped index, and their value is replaced by zero after
+  // the group's loads have been issued (the empty asm keeps each such load unconditional).
   float bw[BF ? 1 : NTW][BF ? 1 : KC][4];
   float br[BF || NR == 0 ? 1 : NR][BF ? 1 : KQ][4];
   s16x4 bwp[BF ? NTW : 1][BF ? KC : 1];
   s16x4 brp[BF && NR > 0 ? NR : 1][BF ? KQ : 1];
-  auto bval = [&](int64_t k, int64_t j) -> float {
-    return (k < K && j < N) ? Elem<TB>::load(B, k * g.b_sk + j * g.b_sj) : 0.f;
+  constexpr bool REG_J_IN = NR > 0;
+  auto raw_at = [&](int64_t k, int64_t j) -> uint32_t {   // bits of B(k, j), indices clamped into B
+    const int64_t i = (k < K ? k : K - 1) * g.b_sk + (j < N ? j : N - 1) * g.b_sj;
+    if constexpr (BF) return reinterpret_cast<const uint16_t*>(B)[i];
+    else return __float_as_uint(reinterpret_cast<const float*>(B)[i]);
   };
-  auto braw = [&](int64_t k, int64_t j) -> short {   // bfloat16 bits (zero outside B)
-    return (k < K && j < N) ? (short)reinterpret_cast<const uint16_t*>(B)[k * g.b_sk + j * g.b_sj] : (short)0;
-  };
+  auto live = [](uint32_t& v) { asm volatile("" : "+v"(v)); };
+  if (!BF && g.b_vec) {   // B contiguous along k and 16-byte aligned; K % 4 == 0, so k < K holds the whole quad
 #pragma unroll
-  for (int t = 0; t < NTW; ++t) {
-    const int64_t j = (int64_t)(wid * NTW + t) * 16 + fr;
+    for (int t = 0; t < NTW; ++t) {
+      const int64_t j = (int64_t)(wid * NTW + t) * 16 + fr;
+      const float* col = (const float*)B + (REG_J_IN || j < N ? j : N - 1) * g.b_sj;
+      f32x4 v[KC];
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int64_t k = 16 * c + 4 * fg;
-      if constexpr (BF) {
-        bwp[t][c] = s16x4{braw(k, j), braw(k + 1, j), braw(k + 2, j), braw(k + 3, j)};
-      } else if (g.b_vec && k + 3 < K && j < N) {   // b_vec: B contiguous along k and 16-byte aligned
-        const float4 v = *reinterpret_cast<const float4*>(B + j * g.b_sj + k);
-        bw[t][c][0] = v.x; bw[t][c][1] = v.y; bw[t][c][2] = v.z; bw[t][c][3] = v.w;
-      } else {
+      for (int c = 0; c < KC; ++c) {
+        const int64_t k = 16 * c + 4 * fg;
+        v[c] = *reinterpret_cast<const f32x4*>(col + (c < KC - 1 || k < K ? k : K - 4));
+      }
 #pragma unroll
-        for (int s = 0; s < 4; ++s) bw[t][c][s] = bval(k + s, j);
+      for (int c = 0; c < KC; ++c)
+        if (c == KC - 1 || !REG_J_IN) dma::tie(v[c]);
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        const bool ok = (c < KC - 1 || 16 * c + 4 * fg < K) && (REG_J_IN || j < N);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) bw[t][c][s] = ok ? v[c][s] : 0.f;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < NTW; ++t) {
+      const int64_t j = (int64_t)(wid * NTW + t) * 16 + fr;
+      uint32_t raw[KC][4];
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) raw[c][s] = raw_at(16 * c + 4 * fg + s, j);
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          if (c == KC - 1 || !REG_J_IN) live(raw[c][s]);
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        uint32_t v[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          v[s] = (c < KC - 1 || 16 * c + 4 * fg + s < K) && (REG_J_IN || j < N) ? raw[c][s] : 0u;
+        if constexpr (BF) bwp[t][c] = s16x4{(short)v[0], (short)v[1], (short)v[2], (short)v[3]};
+        else
+#pragma unroll
+          for (int s = 0; s < 4; ++s) bw[t][c][s] = __uint_as_float(v[s]);
       }
     }
   }
 #pragma unroll
-  for (int q = 0; q < NR; ++q) {
+  for (int q = 0; q < NR; ++q) {   // remainder tiles: this wave's chunks c = 4 cc + wid (a chunk past KC reads as zero)
     const int64_t j = (int64_t)(4 * NTW + q) * 16 + fr;
+    uint32_t raw[KQ][4];
+#pragma unroll
+    for (int cc = 0; cc < KQ; ++cc)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) raw[cc][s] = raw_at(16 * (4 * cc + wid) + 4 * fg + s, j);
+#pragma unroll
+    for (int cc = 0; cc < KQ; ++cc)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) live(raw[cc][s]);
 #pragma unroll
     for (int cc = 0; cc < KQ; ++cc) {
       const int c = 4 * cc + wid;
-      const int64_t k = 16 * c + 4 * fg;
-      if constexpr (BF) {
-        brp[q][cc] = c < KC ? s16x4{braw(k, j), braw(k + 1, j), braw(k + 2, j), braw(k + 3, j)} : s16x4{0, 0, 0, 0};
-      } else {
+      uint32_t v[4];
 #pragma unroll
-        for (int s = 0; s < 4; ++s) br[q][cc][s] = c < KC ? bval(k + s, j) : 0.f;
-      }
+      for (int s = 0; s < 4; ++s) v[s] = c < KC && 16 * c + 4 * fg + s < K && j < N ? raw[cc][s] : 0u;
+      if constexpr (BF) brp[q][cc] = s16x4{(short)v[0], (short)v[1], (short)v[2], (short)v[3]};
+      else
+#pragma unroll
+        for (int s = 0; s < 4; ++s) br[q][cc][s] = __uint_as_float(v[s]);
     }
   }
   float bias_w[NTW], bias_r[NR > 0 ? NR : 1];
+  {
+    float v[NTW + NR];
 #pragma unroll
-  for (int t = 0; t < NTW; ++t) {
-    const int64_t j = (int64_t)(wid * NTW + t) * 16 + fr;
-    bias_w[t] = (g.bias && j < N) ? g.bias[j] : 0.f;
-  }
+    for (int t = 0; t < NTW + NR; ++t) {   // tile t: register tile t, then remainder tile t - NTW
+      const int64_t j = (int64_t)(t < NTW ? wid * NTW + t : 4 * NTW + t - NTW) * 16 + fr;
+      v[t] = g.bias ? g.bias[j < N ? j : N - 1] : 0.f;
+    }
 #pragma unroll
-  for (int q = 0; q < NR; ++q) {
-    const int64_t j = (int64_t)(4 * NTW + q) * 16 + fr;
-    bias_r[q] = (g.bias && j < N) ? g.bias[j] : 0.f;
+    for (int t = 0; t < NTW + NR; ++t) asm volatile("" : "+v"(v[t]));
+#pragma unroll
+    for (int t = 0; t < NTW + NR; ++t) {
+      const int64_t j = (int64_t)(t < NTW ? wid * NTW + t : 4 * NTW + t - NTW) * 16 + fr;
+      (t < NTW ? bias_w[t] : bias_r[t - NTW]) = j < N ? v[t] : 0.f;
+    }
   }
 
   // output columns of this lane: register tiles, then remainder tiles
