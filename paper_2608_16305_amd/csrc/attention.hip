@@ -211,8 +211,11 @@ __global__ __launch_bounds__(256) void k_attn_gather(GatherArgs a, const T* __re
 // way, with a query's rows cut into 4-float groups laid out flat across the wave, so that each lane
 // moves 16 bytes per load or store: the query row in one pass, then the memory groups of all its
 // valid slots (loads issued GV_UNROLL passes at a time before any store), their edge-feature groups
-// the same way, then the time-encoding groups (four cosines per lane).
+// the same way, then the time-encoding groups (four cosines per lane).  The time encoder's weights
+// and phases are staged in LDS once per block: read from global memory next to each cosine, every
+// group waited for its own loads (the cosine's branches keep the next loads from being hoisted).
 constexpr int GV_UNROLL = 4;
+constexpr int GV_MAX_DT = 256;   // time-encoder width of the fast path (its LDS stage)
 
 // Four consecutive values of a memory row (float32, or bfloat16 widened exactly).
 __device__ __forceinline__ float4 load4(const float* p) { return *(const float4*)p; }
@@ -232,10 +235,22 @@ __device__ __forceinline__ float4 pack4(float4 v, int bf16) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const T* __restrict__ mem) {
+  __shared__ float enc_wb[2 * GV_MAX_DT];   // the time encoder's w, then b
   const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (q >= eff_count(a.max_q, a.n_q)) return;
   const int dm = a.dm, dt = a.dt, da = a.da, de = a.de, gm = dm >> 2, gt = dt >> 2, ge = de >> 2;
+  if (dt > 0) {   // every thread stores (slots past 2 dt hold copies that are never read)
+    for (int i0 = 0; i0 < 2 * dt; i0 += 256) {
+      const int i = i0 + (int)threadIdx.x;
+      const int iw = i < dt ? i : dt - 1, ib = i < dt ? 0 : (i - dt < dt ? i - dt : dt - 1);
+      const float w = a.tw[iw], b = a.tb[ib];
+      enc_wb[i < 2 * GV_MAX_DT ? i : 2 * GV_MAX_DT - 1] = i < dt ? w : b;
+    }
+  }
+  __syncthreads();
+  if (q >= eff_count(a.max_q, a.n_q)) return;
+  const float* tw = enc_wb;
+  const float* tb = enc_wb + dt;
   const int Dq = dm + dt, D = dm + de + dt;   // row widths of q_in and kv_in
   // every per-query scalar first, so that their loads overlap the query row's
   const int64_t node = a.q_node[q];
@@ -258,10 +273,10 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const T* _
       } else {
         const int j = 4 * (g - gm);
         float4 o;
-        o.x = enc_val(time_arg(a.tw[j], 0.f, a.tb[j]), a.bf16);
-        o.y = enc_val(time_arg(a.tw[j + 1], 0.f, a.tb[j + 1]), a.bf16);
-        o.z = enc_val(time_arg(a.tw[j + 2], 0.f, a.tb[j + 2]), a.bf16);
-        o.w = enc_val(time_arg(a.tw[j + 3], 0.f, a.tb[j + 3]), a.bf16);
+        o.x = enc_val(time_arg(tw[j], 0.f, tb[j]), a.bf16);
+        o.y = enc_val(time_arg(tw[j + 1], 0.f, tb[j + 1]), a.bf16);
+        o.z = enc_val(time_arg(tw[j + 2], 0.f, tb[j + 2]), a.bf16);
+        o.w = enc_val(time_arg(tw[j + 3], 0.f, tb[j + 3]), a.bf16);
         *(float4*)(a.q_in + q * Dq + dm + j) = o;
       }
     }
@@ -314,10 +329,10 @@ __global__ __launch_bounds__(256) void k_attn_gather_v4(GatherArgs a, const T* _
     if (e < ntg) {
       const int j = 4 * g;
       float4 o;
-      o.x = enc_val(time_arg(a.tw[j], delta, a.tb[j]), a.bf16);
-      o.y = enc_val(time_arg(a.tw[j + 1], delta, a.tb[j + 1]), a.bf16);
-      o.z = enc_val(time_arg(a.tw[j + 2], delta, a.tb[j + 2]), a.bf16);
-      o.w = enc_val(time_arg(a.tw[j + 3], delta, a.tb[j + 3]), a.bf16);
+      o.x = enc_val(time_arg(tw[j], delta, tb[j]), a.bf16);
+      o.y = enc_val(time_arg(tw[j + 1], delta, tb[j + 1]), a.bf16);
+      o.z = enc_val(time_arg(tw[j + 2], delta, tb[j + 2]), a.bf16);
+      o.w = enc_val(time_arg(tw[j + 3], delta, tb[j + 3]), a.bf16);
       *(float4*)(a.kv_in + (off + sl) * D + dm + de + j) = o;
     }
   }
@@ -762,7 +777,6 @@ __global__ void k_seg_bounds(const uint32_t* __restrict__ keys, int64_t n, uint3
 
 constexpr int SEG_TILE = 64;     // sorted occurrences per wave (the attention's d M')
 constexpr int SEG_TILE_ROWS = 16;   // the same for segsum_rows (few occurrences: more, shorter waves)
-constexpr int SEG_MAXC = 8;      // columns per lane: width <= 512
 
 struct SegCtx {
   const uint32_t* keys;
@@ -981,26 +995,122 @@ __global__ __launch_bounds__(256) void k_segsum_tiles_v4(SegCtx c) {
   seg_flush_v4(c, tile, cur, start == 0 && key_before == cur, key_after == cur, qa, qb, acc_a, acc_b);
 }
 
-// Block b (FIX_WAVES waves): wave w first zeroes row FIX_WAVES b + w if that
-// row has no occurrence.  Then, if the row at the end of tile b starts in
-// tile b and continues past it (rows inside one tile were written whole), the
-// block sums that row: tail[b] + head[b+1] + ... + head[t1].  The waves take
-// interleaved heads with four loads in flight; their partial sums are added
-// in wave order.
+// The rows no tile could finish.  Every wave first zeroes, grid-stride, the rows with no occurrence.
+// Then block b checks tiles tpb b .. tpb b + tpb - 1 (one lane each, tpb <= 64, about 1024 blocks over
+// all tiles, so that a skewed stream's many hub rows spread over many blocks): a tile whose last row starts in it and
+// continues past it (rows inside one tile were written whole) has that row summed by the whole block:
+// tail[tile] + head[tile + 1] + ... + head[t1].  The waves take interleaved heads, four at a time with
+// all their loads in flight (no per-lane test: a chunk past the row's W columns re-reads column W - 1
+// and is never stored), and their partial sums are added in wave order.  NC = ceil(W / 64) <= 5.
 constexpr int FIX_WAVES = 16;
+constexpr int FIX_BLOCKS = 1024;   // blocks the tile checks aim for
 
+template <int NC>
 __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const int32_t* __restrict__ n_rows,
-                                                                 int64_t max_rows, int64_t ntiles) {
-  __shared__ float part[FIX_WAVES][SEG_MAXC * 64];
+                                                                 int64_t max_rows, int64_t ntiles, int tpb) {
+  __shared__ float part[FIX_WAVES][NC * 64];
+  const int64_t blk = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int W = c.dm + c.w2;
+  const int64_t rows = eff_count(max_rows, n_rows);
+  for (int64_t zr = blk * FIX_WAVES + wid; zr < rows; zr += (int64_t)gridDim.x * FIX_WAVES) {
+    if (c.seg_lo[zr] == c.seg_hi[zr]) {   // no occurrence: zero gradient
+      float z[NC];
+#pragma unroll
+      for (int i = 0; i < NC; ++i) z[i] = 0.f;
+      seg_store_row<NC>(c, zr, z, lane);
+    }
+  }
+  // the rest depends on the block only (uniform branches around the barriers)
+  const int64_t tile0 = blk * tpb;
+  if (tile0 >= ntiles) return;
+  uint64_t todo;   // lane l: does tile tile0 + l end inside a row that starts in it and continues past it?
+  {
+    const int64_t tile = tile0 + lane < ntiles ? tile0 + lane : ntiles - 1;
+    const int64_t p_last = min((tile + 1) * c.tile, c.n_occ) - 1;
+    const int64_t p_next = p_last + 1 < c.n_occ ? p_last + 1 : p_last;
+    const uint32_t key = c.keys[p_last], next = c.keys[p_next];
+    const bool cont = lane < tpb && tile0 + lane < ntiles && p_last + 1 < c.n_occ && key != c.sentinel && next == key;
+    const bool starts = cont && c.seg_lo[key] >= tile * c.tile;
+    todo = __ballot(starts);
+  }
+  int cc[NC];
+#pragma unroll
+  for (int i = 0; i < NC; ++i) cc[i] = lane + 64 * i < W ? lane + 64 * i : W - 1;
+  while (todo) {
+    const int l = __builtin_ctzll(todo);
+    todo &= todo - 1;
+    const int64_t tile = tile0 + l;
+    const int64_t p_last = min((tile + 1) * c.tile, c.n_occ) - 1;
+    const uint32_t key = c.keys[p_last];
+    const int64_t t1 = (c.seg_hi[key] - 1) / c.tile;
+    float acc[NC];
+#pragma unroll
+    for (int i = 0; i < NC; ++i) acc[i] = 0.f;
+    int64_t t = tile + 1 + wid;
+    constexpr int64_t S4 = 4 * FIX_WAVES;
+    for (; t + 3 * FIX_WAVES <= t1; t += S4) {
+      const float* h0 = c.head + t * W;
+      const float* h1 = h0 + FIX_WAVES * (int64_t)W;
+      const float* h2 = h0 + 2 * FIX_WAVES * (int64_t)W;
+      const float* h3 = h0 + 3 * FIX_WAVES * (int64_t)W;
+      float v[4][NC];
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        v[0][i] = h0[cc[i]];
+        v[1][i] = h1[cc[i]];
+        v[2][i] = h2[cc[i]];
+        v[3][i] = h3[cc[i]];
+      }
+#pragma unroll
+      for (int i = 0; i < NC; ++i) acc[i] += ((v[0][i] + v[1][i]) + v[2][i]) + v[3][i];
+    }
+    for (; t <= t1; t += FIX_WAVES) {
+      const float* h = c.head + t * W;
+      float v[NC];
+#pragma unroll
+      for (int i = 0; i < NC; ++i) v[i] = h[cc[i]];
+#pragma unroll
+      for (int i = 0; i < NC; ++i) acc[i] += v[i];
+    }
+#pragma unroll
+    for (int i = 0; i < NC; ++i) part[wid][i * 64 + lane] = acc[i];
+    __syncthreads();
+    if (wid == 0) {
+      const float* tl = c.tail + tile * W;
+      float tv[NC];
+#pragma unroll
+      for (int i = 0; i < NC; ++i) tv[i] = tl[cc[i]];
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        const int o = i * 64 + lane;
+        float sum = 0.f;
+        for (int w = 0; w < FIX_WAVES; ++w) sum += part[w][o];
+        acc[i] = tv[i] + sum;
+      }
+      seg_store_row<NC>(c, (int64_t)key, acc, lane);
+    }
+    __syncthreads();   // part is free for the next row
+  }
+}
+
+// Rows of 321 to 512 columns: the same sums with a per-chunk test around each load (the batched
+// form above would need more than the 128 registers a thread of a 1024-thread block has).
+constexpr int FIX_WIDE_C = 8;
+
+__global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup_wide(SegCtx c, const int32_t* __restrict__ n_rows,
+                                                                      int64_t max_rows, int64_t ntiles) {
+  __shared__ float part[FIX_WAVES][FIX_WIDE_C * 64];
   const int64_t blk = blockIdx.x;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int W = c.dm + c.w2;
   const int64_t zr = blk * FIX_WAVES + wid;
   if (zr < eff_count(max_rows, n_rows) && c.seg_lo[zr] == c.seg_hi[zr]) {   // no occurrence: zero gradient
-    float z[SEG_MAXC];
+    float z[FIX_WIDE_C];
 #pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) z[i] = 0.f;
-    seg_store_row<SEG_MAXC>(c, zr, z, lane);
+    for (int i = 0; i < FIX_WIDE_C; ++i) z[i] = 0.f;
+    seg_store_row<FIX_WIDE_C>(c, zr, z, lane);
   }
   // the rest depends on the block only (uniform branches around the barrier)
   if (blk >= ntiles) return;
@@ -1010,9 +1120,9 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
   if (key == c.sentinel || c.keys[p_last + 1] != key) return;
   if (c.seg_lo[key] < blk * c.tile) return;   // started in an earlier tile, whose block sums it
   const int64_t t1 = (c.seg_hi[key] - 1) / c.tile;
-  float acc[SEG_MAXC];
+  float acc[FIX_WIDE_C];
 #pragma unroll
-  for (int i = 0; i < SEG_MAXC; ++i) acc[i] = 0.f;
+  for (int i = 0; i < FIX_WIDE_C; ++i) acc[i] = 0.f;
   int64_t t = blk + 1 + wid;
   constexpr int64_t S4 = 4 * FIX_WAVES;
   for (; t + 3 * FIX_WAVES <= t1; t += S4) {
@@ -1021,7 +1131,7 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
     const float* h2 = h0 + 2 * FIX_WAVES * (int64_t)W;
     const float* h3 = h0 + 3 * FIX_WAVES * (int64_t)W;
 #pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) {
+    for (int i = 0; i < FIX_WIDE_C; ++i) {
       const int col = lane + 64 * i;
       if (col < W) acc[i] += ((h0[col] + h1[col]) + h2[col]) + h3[col];
     }
@@ -1029,18 +1139,18 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
   for (; t <= t1; t += FIX_WAVES) {
     const float* h = c.head + t * W;
 #pragma unroll
-    for (int i = 0; i < SEG_MAXC; ++i) {
+    for (int i = 0; i < FIX_WIDE_C; ++i) {
       const int col = lane + 64 * i;
       if (col < W) acc[i] += h[col];
     }
   }
 #pragma unroll
-  for (int i = 0; i < SEG_MAXC; ++i) part[wid][i * 64 + lane] = acc[i];
+  for (int i = 0; i < FIX_WIDE_C; ++i) part[wid][i * 64 + lane] = acc[i];
   __syncthreads();
   if (wid != 0) return;
   const float* tl = c.tail + blk * W;
 #pragma unroll
-  for (int i = 0; i < SEG_MAXC; ++i) {
+  for (int i = 0; i < FIX_WIDE_C; ++i) {
     const int col = lane + 64 * i;
     const int o = i * 64 + lane;
     if (col < W) {
@@ -1049,7 +1159,31 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
       acc[i] = tl[col] + sum;
     }
   }
-  seg_store_row<SEG_MAXC>(c, (int64_t)key, acc, lane);
+  seg_store_row<FIX_WIDE_C>(c, (int64_t)key, acc, lane);
+}
+
+// The fixup over max_rows rows and ntiles tiles (its grid covers both), with ceil(W / 64) column chunks.
+void launch_segsum_fixup(const SegCtx& c, const int32_t* n_rows, int64_t max_rows, int64_t ntiles, hipStream_t s) {
+  const unsigned b = 64 * FIX_WAVES;
+  if (cdiv(c.dm + c.w2, 64) > 5) {   // one block per tile (and per FIX_WAVES rows)
+    const int64_t nfix = ntiles > cdiv(max_rows, FIX_WAVES) ? ntiles : cdiv(max_rows, FIX_WAVES);
+    k_segsum_fixup_wide<<<(unsigned)nfix, b, 0, s>>>(c, n_rows, max_rows, ntiles);
+    return;
+  }
+  // tpb tiles per block (about FIX_BLOCKS blocks), and at least enough blocks for the row zeroing to take a
+  // few rows per wave
+  const int64_t tpb64 = cdiv(ntiles, FIX_BLOCKS);
+  const int tpb = (int)(tpb64 < 1 ? 1 : (tpb64 > 64 ? 64 : tpb64));
+  const int64_t zb = cdiv(max_rows, FIX_WAVES) < FIX_BLOCKS ? cdiv(max_rows, FIX_WAVES) : FIX_BLOCKS;
+  const int64_t tb = cdiv(ntiles, tpb);
+  const unsigned g = (unsigned)(tb > zb ? tb : (zb > 0 ? zb : 1));
+  switch (cdiv(c.dm + c.w2, 64)) {
+    case 1: k_segsum_fixup<1><<<g, b, 0, s>>>(c, n_rows, max_rows, ntiles, tpb); break;
+    case 2: k_segsum_fixup<2><<<g, b, 0, s>>>(c, n_rows, max_rows, ntiles, tpb); break;
+    case 3: k_segsum_fixup<3><<<g, b, 0, s>>>(c, n_rows, max_rows, ntiles, tpb); break;
+    case 4: k_segsum_fixup<4><<<g, b, 0, s>>>(c, n_rows, max_rows, ntiles, tpb); break;
+    default: k_segsum_fixup<5><<<g, b, 0, s>>>(c, n_rows, max_rows, ntiles, tpb); break;
+  }
 }
 
 struct BwdWs {
@@ -1161,8 +1295,7 @@ mtgnn_status segsum_rows(const uint32_t* skeys, const uint32_t* svals, int64_t n
     }
     MTGNN_CHECK_LAUNCH("segsum_tiles");
   }
-  const int64_t nfix = ntiles > cdiv(max_rows, FIX_WAVES) ? ntiles : cdiv(max_rows, FIX_WAVES);
-  k_segsum_fixup<<<(unsigned)nfix, 64 * FIX_WAVES, 0, s>>>(c, n_rows, max_rows, n_occ > 0 ? ntiles : 0);
+  launch_segsum_fixup(c, n_rows, max_rows, n_occ > 0 ? ntiles : 0, s);
   MTGNN_CHECK_LAUNCH("segsum_fixup");
   return MTGNN_OK;
 }
@@ -1240,7 +1373,7 @@ mtgnn_status attn_fwd_prepared_impl(const int32_t* q_node, const float* q_t, con
   const unsigned gq = (unsigned)cdiv(sh.Q, 4);
   const GatherArgs ga{q_node, nbr, neid, n_q, sv.cnt, sv.pair_off, nt, q_t, edge_feat, tw, tb, max_q, sh.k, sh.dm,
                       sh.de, sh.dt, sh.da, bf, sv.q_in, sv.m_in, sv.kv_in, sv.pair_delta, sv.pair_nbr};
-  const bool v4 = sh.de % 4 == 0 && sh.dm % 4 == 0 && sh.dt % 4 == 0 && sh.da % 4 == 0 &&
+  const bool v4 = sh.de % 4 == 0 && sh.dm % 4 == 0 && sh.dt % 4 == 0 && sh.da % 4 == 0 && sh.dt <= GV_MAX_DT &&
                   ((uintptr_t)memory & (bf ? 7 : 15)) == 0 && (sh.de == 0 || ((uintptr_t)edge_feat & 15) == 0);
   if (v4 && !bf)
     k_attn_gather_v4<float><<<gq, 256, 0, s>>>(ga, (const float*)memory);
@@ -1360,8 +1493,7 @@ mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSav
       }
     }
     MTGNN_CHECK_LAUNCH("segsum_tiles");
-    const int64_t nfix = ntiles > cdiv(max_rows, FIX_WAVES) ? ntiles : cdiv(max_rows, FIX_WAVES);
-    k_segsum_fixup<<<(unsigned)nfix, 64 * FIX_WAVES, 0, s>>>(c, n_rows, max_rows, ntiles);
+    launch_segsum_fixup(c, n_rows, max_rows, ntiles, s);
     MTGNN_CHECK_LAUNCH("segsum_fixup");
     const int W = dm + 2 * da;
     if (qproj_fused_ok(wt, da, dm, sh.dt))

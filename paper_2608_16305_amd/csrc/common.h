@@ -106,6 +106,15 @@ __device__ __forceinline__ float cos_for_bf16(float arg) {
   return y;
 }
 
+// Keeps a loaded 32-bit value in its register whatever the lanes do next.  A load whose result is used
+// only under a per-lane condition may be moved into that condition's branch, where it is waited for on
+// the spot; issuing a batch of loads, then this on each, keeps them all in flight together.
+template <class T>
+__device__ __forceinline__ void keep_live(T& v) {
+  static_assert(sizeof(T) == 4, "one 32-bit register");
+  asm volatile("" : "+v"(v));
+}
+
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
 // Gate nonlinearities on the hardware base-2 exponential and reciprocal (about 1 ulp each):
 // sigma(x) = 1 / (1 + 2^(-x log2 e)),  tanh(x) = 1 - 2 / (1 + 2^(2 x log2 e)).  Both saturate correctly

@@ -51,10 +51,17 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_scan_reduce(const int32_t* __r
                                                               int32_t* __restrict__ block_sums) {
   __shared__ int lds[8];
   const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
-  int s = 0;
+  int v[SCAN_ITEMS];   // every item loaded up front (an index past n reads element n - 1 and counts 0)
+#pragma unroll
   for (int i = 0; i < SCAN_ITEMS; ++i) {
-    int64_t idx = base + (int64_t)i * SCAN_THREADS + threadIdx.x;
-    if (idx < n) s += in[idx];
+    const int64_t idx = base + (int64_t)i * SCAN_THREADS + threadIdx.x;
+    v[i] = in[idx < n ? idx : n - 1];
+  }
+  int s = 0;
+#pragma unroll
+  for (int i = 0; i < SCAN_ITEMS; ++i) {
+    keep_live(v[i]);
+    s += base + (int64_t)i * SCAN_THREADS + threadIdx.x < n ? v[i] : 0;
   }
   int excl;
   int tot = block_exclusive_scan(s, &excl, lds);
@@ -103,10 +110,20 @@ __global__ __launch_bounds__(SCAN1_THREADS) void k_scan_one_block(const int32_t*
   __shared__ int buf[CAP + CAP / 32];
   __shared__ int wsum[SCAN1_THREADS / 64];
   const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
+  {
+    const int last = (int)n - 1;   // n <= SCAN1_MAX: 32-bit offsets from the uniform base
+    int x[ITEMS];   // every item loaded up front (an index past n reads element n - 1 and stores 0)
 #pragma unroll
-  for (int j = 0; j < ITEMS; ++j) {
-    const int i = j * SCAN1_THREADS + t;
-    buf[scan1_pad(i)] = i < n ? in[i] : 0;
+    for (int j = 0; j < ITEMS; ++j) {
+      const int i = j * SCAN1_THREADS + t;
+      x[j] = in[i < last ? i : last];
+    }
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j) {
+      const int i = j * SCAN1_THREADS + t;
+      keep_live(x[j]);
+      buf[scan1_pad(i)] = i < n ? x[j] : 0;
+    }
   }
   __syncthreads();
   int v[ITEMS];
@@ -154,9 +171,17 @@ __global__ __launch_bounds__(SORT_THREADS) void k_radix_hist(const uint32_t* __r
   for (int i = threadIdx.x; i < 4 * RADIX; i += SORT_THREADS) (&hist[0][0])[i] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * SORT_TILE;
+  uint32_t kk[SORT_ITEMS];   // the tile's keys loaded up front (an index past n reads key n - 1, not counted)
+#pragma unroll
   for (int i = 0; i < SORT_ITEMS; ++i) {
-    int64_t idx = base + (int64_t)i * SORT_THREADS + threadIdx.x;
-    if (idx < n) atomicAdd(&hist[wid][(keys[idx] >> shift) & dmask], 1);
+    const int64_t idx = base + (int64_t)i * SORT_THREADS + threadIdx.x;
+    kk[i] = keys[idx < n ? idx : n - 1];
+  }
+#pragma unroll
+  for (int i = 0; i < SORT_ITEMS; ++i) {
+    const int64_t idx = base + (int64_t)i * SORT_THREADS + threadIdx.x;
+    keep_live(kk[i]);
+    if (idx < n) atomicAdd(&hist[wid][(kk[i] >> shift) & dmask], 1);
   }
   __syncthreads();
   for (int d = threadIdx.x; d < (1 << digit_bits); d += SORT_THREADS)
