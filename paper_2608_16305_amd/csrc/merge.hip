@@ -43,8 +43,10 @@ template <int NCT> struct Tiles { static constexpr int per_wave = (NCT + MW - 1)
 // acc[r NU + u] (16 x 16 output tile t = wave + 4 u of row tile r) += X[16 rows of tile r, 16 KC]
 // B[16 t.., 16 KC]^T.  X: the block's LDS tile of 16 RT rows (row stride XSS, zero beyond the true width).
 // B: a zero-padded weight copy, 16 MW NU rows by 16 KC columns, so every fragment load is in bounds and
-// unconditional; each fragment serves the RT row tiles.
-template <int NCT, int KC, int XSS = XS, int RT = 1>
+// unconditional; each fragment serves the RT row tiles.  PDT weight chunks are in flight ahead of the
+// one being multiplied (PDT = KC: the whole share is requested at once, for launches too small to hide
+// the latency with other blocks).
+template <int NCT, int KC, int XSS = XS, int RT = 1, int PDT = PD>
 __device__ __forceinline__ void layer(const float* X, const float* __restrict__ B,
                                       f32x4 (&acc)[RT * Tiles<NCT>::per_wave]) {
   constexpr int NU = Tiles<NCT>::per_wave;
@@ -59,10 +61,10 @@ __device__ __forceinline__ void layer(const float* X, const float* __restrict__ 
     for (int u = 0; u < NU; ++u) bf[c][u] = *reinterpret_cast<const float4*>(Bl + 16 * MW * u * LDB + 16 * c);
   };
 #pragma unroll
-  for (int c = 0; c < PD && c < KC; ++c) load_b(c);
+  for (int c = 0; c < PDT && c < KC; ++c) load_b(c);
 #pragma unroll
   for (int c = 0; c < KC; ++c) {
-    if (c + PD < KC) load_b(c + PD);   // in flight while this chunk's MFMAs run
+    if (c + PDT < KC) load_b(c + PDT);   // in flight while this chunk's MFMAs run
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
       const float4 a = *reinterpret_cast<const float4*>(X + (16 * r + fr) * XSS + 16 * c + 4 * fg);
@@ -670,10 +672,11 @@ __global__ __launch_bounds__(64 * MW) void k_link_fused(const float* __restrict_
   }
   __syncthreads();
   {
-    f32x4 as[NU], ad[NU], an[NU];
-    layer<NA, NA, XL, 1>(T[0], Wp, as);
-    layer<NA, NA, XL, 1>(T[1], Wp + WSZ, ad);
-    layer<NA, NA, XL, 1>(T[2], Wp + WSZ, an);
+    // z_src W_a, then z_dst and z_neg (adjacent LDS tiles) as two row tiles of one pass over W_b; every
+    // weight chunk requested at once (a block per 16 targets: too few blocks to hide the latency)
+    f32x4 as[NU], adn[2 * NU];
+    layer<NA, NA, XL, 1, NA>(T[0], Wp, as);
+    layer<NA, NA, XL, 2, NA>(T[1], Wp + WSZ, adn);
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
       const int j = 16 * (wid + MW * u) + fr;
@@ -682,8 +685,8 @@ __global__ __launch_bounds__(64 * MW) void k_link_fused(const float* __restrict_
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = 4 * fg + r;
-        T[3][i * XL + j] = (as[u][r] + ad[u][r]) + bj;
-        T[4][i * XL + j] = (as[u][r] + an[u][r]) + bj;
+        T[3][i * XL + j] = (as[u][r] + adn[u][r]) + bj;
+        T[4][i * XL + j] = (as[u][r] + adn[NU + u][r]) + bj;
       }
     }
   }
@@ -752,14 +755,32 @@ __global__ __launch_bounds__(64 * MW) void k_link_fused(const float* __restrict_
     const int k = c < da ? c : 128 + (c - da);
     part[(int64_t)blockIdx.x * (da + 2) + c] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
   }
-  // dz for the three query blocks
-  for (int b = 0; b < 3; ++b) {
+  // dz for the three query blocks: the sources through W_a^T, then destinations and negatives (adjacent
+  // LDS tiles) as two row tiles of one pass over W_b^T
+  {
     f32x4 acc[NU];
-    layer<NA, NA, XL, 1>(T[b], Wp + (b == 0 ? 2 : 3) * WSZ, acc);
-    float* out = dz + (int64_t)b * n * da;
+    layer<NA, NA, XL, 1, NA>(T[0], Wp + 2 * WSZ, acc);
     each_out<NA, 1>(acc, da, r0, n, [&](int i, int j, bool ok, float v) {
-      if (ok) out[(r0 + i) * da + j] = v;
+      if (ok) dz[(r0 + i) * da + j] = v;
     });
+  }
+  {
+    f32x4 acc[2 * NU];
+    layer<NA, NA, XL, 2, NA>(T[1], Wp + 3 * WSZ, acc);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {   // row tile b: query block 1 + b
+      float* out = dz + (int64_t)(1 + b) * n * da;
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const int j = 16 * (wid + MW * u) + fr;
+        if (j >= da) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t row = r0 + 4 * fg + r;
+          if (row < n) out[row * da + j] = acc[b * NU + u][r];
+        }
+      }
+    }
   }
 }
 
