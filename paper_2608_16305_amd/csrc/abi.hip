@@ -494,9 +494,9 @@ mtgnn_status mtgnn_gru_update_bwd(const float* d_mem, const void* save, const vo
                              ws, ws_bytes, stream);
 }
 
-mtgnn_status mtgnn_link_loss(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* params,
-                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* grads,
-                             void* ws, size_t ws_bytes, hipStream_t stream) {
+static mtgnn_status check_link_loss(const float* z, int64_t max_q, const mtgnn_link_params* params,
+                                    const mtgnn_dims* d, float* loss, float* dz, mtgnn_link_grads* grads, void* ws,
+                                    size_t ws_bytes) {
   MTGNN_TRY(check_dims(d));
   if (max_q < 0 || max_q >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
   if (max_q % 3 != 0) return fail(MTGNN_EINVAL, "max_q is not a multiple of 3 (src, dst and negative blocks)");
@@ -518,7 +518,24 @@ mtgnn_status mtgnn_link_loss(const float* z, const int32_t* n_q, int64_t max_q, 
   }
   if (ws_bytes < link_loss_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "link_loss ws");
   REQ(ws, "ws");
+  return MTGNN_OK;
+}
+
+mtgnn_status mtgnn_link_loss(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* params,
+                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* grads,
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_link_loss(z, max_q, params, d, loss, dz, grads, ws, ws_bytes));
   return link_loss_impl(z, n_q, max_q, params, d, loss, scores, dz, grads, ws, ws_bytes, stream);
+}
+
+mtgnn_status mtgnn_link_loss_overlap(const float* z, const int32_t* n_q, int64_t max_q,
+                                     const mtgnn_link_params* params, const mtgnn_dims* d, float* loss, float* scores,
+                                     float* dz, mtgnn_link_grads* grads, void* ws, size_t ws_bytes,
+                                     hipStream_t stream, hipStream_t dw_stream, hipEvent_t fork) {
+  MTGNN_TRY(check_link_loss(z, max_q, params, d, loss, dz, grads, ws, ws_bytes));
+  REQ(dw_stream, "dw_stream");
+  REQ(fork, "fork");
+  return link_loss_impl(z, n_q, max_q, params, d, loss, scores, dz, grads, ws, ws_bytes, stream, dw_stream, fork);
 }
 
 mtgnn_status mtgnn_build_messages_bwd(const float* dmsg_time, const float* dt, const int32_t* n_rows,

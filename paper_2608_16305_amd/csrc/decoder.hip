@@ -143,7 +143,7 @@ size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q) {
 
 mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* p,
                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
-                            size_t ws_bytes, hipStream_t s) {
+                            size_t ws_bytes, hipStream_t s, hipStream_t s_dw, hipEvent_t fork) {
   const int da = d->d_attn;
   if (da > 64 * LINK_MAX_COLS) return MTGNN_EUNSUPPORTED;
   if (ws_bytes < link_loss_ws(d, max_q)) return MTGNN_EWORKSPACE;
@@ -152,10 +152,19 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
   if (link_fused_ok(da)) {
     MTGNN_TRY(link_fused(z, n_q, max_q, da, p->W_d1, p->b_d1, p->W_d2, p->b_d2, L.Wp, L.DA, L.DB, L.part, dz, scores,
                          g->W_d2, g->b_d2, loss, s));
+    // W_d1's gradient needs only DA, DB and z: on the second stream if there is one
+    if (s_dw) {
+      hipError_t e = hipEventRecord(fork, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s_dw, fork, 0);
+      if (e != hipSuccess) {
+        set_hip_error(e, "link_loss fork");
+        return MTGNN_EHIP;
+      }
+    }
     // DA is zero past the src block (the first third of the query rows), DB on it
     const DwProblem dp[2] = {{L.DA, da, z, da, g->W_d1, 2 * da, da, da, g->b_d1, 0, 1, 3},
                              {L.DB, da, z, da, g->W_d1 + da, 2 * da, da, da, L.db_scratch, 1, 3, 3}};
-    return linear_dw_batch(dp, 2, max_q, n_q, MTGNN_F32, L.rest, L.rest_bytes, s);
+    return linear_dw_batch(dp, 2, max_q, n_q, MTGNN_F32, L.rest, L.rest_bytes, s_dw ? s_dw : s);
   }
   // general widths: the first layer's two halves over every query row
   const FwdProblem fp[2] = {{z, da, p->W_d1, 2 * da, nullptr, L.Y, 2 * da, da, da},

@@ -81,9 +81,11 @@ mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int d
                         const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
                         float* scores, float* dW2, float* db2, float* loss, hipStream_t s);
 size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q);
+// s_dw, fork: a second stream and an event (or NULL, NULL): W_d1's gradient is then enqueued on s_dw after
+// fork, recorded on s once dz and the decoder's row gradients are written (fused widths only).
 mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* p,
                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
-                            size_t ws_bytes, hipStream_t s);
+                            size_t ws_bytes, hipStream_t s, hipStream_t s_dw = nullptr, hipEvent_t fork = nullptr);
 
 // offline dependency scan (Algorithm 1) and the mixed batches of one worker
 mtgnn_status dep_scan_impl(const int32_t* src, const int32_t* dst, int64_t E, const int32_t* owner, int64_t n_nodes,

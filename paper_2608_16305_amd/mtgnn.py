@@ -25,7 +25,7 @@ ENTRY_POINTS = (
     "mtgnn_temporal_attn_prepare_slots", "mtgnn_temporal_attn_prepared",
     "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap", "mtgnn_temporal_attn_bwd_group",
     "mtgnn_temporal_attn_bwd_grouped",
-    "mtgnn_gru_update_bwd", "mtgnn_link_loss",
+    "mtgnn_gru_update_bwd", "mtgnn_link_loss", "mtgnn_link_loss_overlap",
     "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr",
     "mtgnn_dependency_scan", "mtgnn_mixed_batches", "mtgnn_rnn_update", "mtgnn_rnn_update_bwd",
     "mtgnn_time_projection", "mtgnn_time_projection_bwd", "mtgnn_controller_create", "mtgnn_controller_destroy",
@@ -111,6 +111,8 @@ _SIGS = {
     "mtgnn_gru_update_bwd": [_P, _P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _P, _P, _P, _SZ, _P],
     "mtgnn_link_loss": [_P, _P, _I64, C.POINTER(LinkParams), C.POINTER(Dims), _P, _P, _P, C.POINTER(LinkGrads), _P,
                         _SZ, _P],
+    "mtgnn_link_loss_overlap": [_P, _P, _I64, C.POINTER(LinkParams), C.POINTER(Dims), _P, _P, _P,
+                                C.POINTER(LinkGrads), _P, _SZ, _P, _P, _P],
     "mtgnn_build_messages_bwd": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _SZ, _P],
     "mtgnn_build_messages_bwd_noalloc": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
@@ -452,12 +454,18 @@ def link_grads(g: dict) -> LinkGrads:
     return LinkGrads(*[_ptr(g[n], torch.float32, "d" + n) for n in _LINK])
 
 
-def mtgnn_link_loss(z, n_q, max_q, params: LinkParams, d: Dims, loss, scores, dz, grads: LinkGrads, ws, stream=None):
+def mtgnn_link_loss(z, n_q, max_q, params: LinkParams, d: Dims, loss, scores, dz, grads: LinkGrads, ws, stream=None,
+                    dw_stream=None, fork=None):
+    """dw_stream and fork given: mtgnn_link_loss_overlap (W_d1's gradient on dw_stream after fork)."""
     wp, wb = _ws(ws)
-    _check(lib().mtgnn_link_loss(_ptr(z, torch.float32, "z"), _ptr(n_q, torch.int32, "n_q", True), int(max_q),
-                                 C.byref(params), C.byref(d), _ptr(loss, torch.float32, "loss"),
-                                 _ptr(scores, torch.float32, "scores", True), _ptr(dz, torch.float32, "dz"),
-                                 C.byref(grads), wp, wb, _stream(stream)), "mtgnn_link_loss")
+    args = (_ptr(z, torch.float32, "z"), _ptr(n_q, torch.int32, "n_q", True), int(max_q), C.byref(params), C.byref(d),
+            _ptr(loss, torch.float32, "loss"), _ptr(scores, torch.float32, "scores", True), _ptr(dz, torch.float32, "dz"),
+            C.byref(grads), wp, wb, _stream(stream))
+    if dw_stream is None:
+        _check(lib().mtgnn_link_loss(*args), "mtgnn_link_loss")
+    else:
+        _check(lib().mtgnn_link_loss_overlap(*args, _stream(dw_stream), _event(fork, "fork")),
+               "mtgnn_link_loss_overlap")
 
 
 def mtgnn_build_messages_bwd(dmsg_time, dt, n_rows, max_rows, time_w, time_b, d: Dims, d_time_w, d_time_b, ws,

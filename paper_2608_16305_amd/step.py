@@ -132,6 +132,7 @@ class TGNStep:
         self.fork, self.join = M.DeviceEvent(), M.DeviceEvent()
         self.q_fork, self.q_join = M.DeviceEvent(), M.DeviceEvent()
         self.g_join = M.DeviceEvent()
+        self.l_fork = M.DeviceEvent()   # the link loss's fork (decoder weight gradient on the second stream)
         self.m_done, self.pre_join = M.DeviceEvent(), M.DeviceEvent()
         self.group_ahead = True   # step(): the backward's d_mem grouping during the embedding (second stream)
         self._grouped = False     # ... and it has been enqueued
@@ -204,9 +205,15 @@ class TGNStep:
                                        self.attn_save, stream=s)
 
     def link_loss(self):
-        """The masked loss of the embedded batch (Eq. 13) and dZ, on the main stream."""
-        M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz, self.lg,
-                          self.ws_link, stream=self.ts)
+        """The masked loss of the embedded batch (Eq. 13) and dZ, on the main stream; with overlap, the
+        decoder's first-layer weight gradient runs on the second stream (idle between the embedding and
+        the backward's d_mem sums), ahead of the d_mem work there, so the backward's join covers it."""
+        if self.overlap:
+            M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz,
+                              self.lg, self.ws_link, stream=self.ts, dw_stream=self.side_stream, fork=self.l_fork)
+        else:
+            M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz,
+                              self.lg, self.ws_link, stream=self.ts)
         return self.dz
 
     def backward(self, dz):

@@ -68,3 +68,34 @@ def test_link_loss_ragged_width():
     errs = {"loss": abs(loss - ref.loss) / abs(ref.loss), "dz": rel_err(dz, ref.dz)}
     errs.update({k: rel_err(g[k], ref.grads[k]) for k in ref.grads})
     assert max(errs.values()) <= 1e-4, errs
+
+
+@pytest.mark.parametrize("cid,max_tar,n_tar", [(3, 4_000, 3_517), (1, 200, 137)])
+def test_link_loss_overlap_bitwise(cid, max_tar, n_tar):
+    """mtgnn_link_loss_overlap (W_d1's gradient on a second stream after a fork) against mtgnn_link_loss:
+    every output bit for bit."""
+    w = workload(cid)
+    log(f"[link] overlap entry, workload {cid}: {n_tar} of {max_tar} target events")
+    params = init_params(w, random_bias=True)
+    rng = np.random.default_rng(cid + n_tar)
+    z = torch.from_numpy((rng.standard_normal((3 * max_tar, w.d_attn)) * 0.7).astype(np.float32)).cuda()
+    d = M.dims(w.n_nodes, w.d_mem, w.d_time, w.d_edge, w.d_attn, w.n_heads, w.k, M.F32)
+    p = {k: torch.from_numpy(params[k]).cuda() for k in ("W_d1", "b_d1", "W_d2", "b_d2")}
+    n_q = torch.tensor([3 * n_tar], dtype=torch.int32, device="cuda")
+    side, fork = torch.cuda.Stream(), M.DeviceEvent()
+    outs = []
+    for overlap in (False, True):
+        g = {k: torch.full_like(v, np.nan) for k, v in p.items()}
+        loss = torch.full((1,), np.nan, device="cuda")
+        scores = torch.full((2, max_tar), np.nan, device="cuda")
+        dz = torch.full((3 * max_tar, w.d_attn), np.nan, device="cuda")
+        ws = M.alloc_bytes(M.workspace_bytes(M.OP_LINK_LOSS, d, 0, 3 * max_tar))
+        if overlap:
+            M.mtgnn_link_loss(z, n_q, 3 * max_tar, M.link_params(p), d, loss, scores, dz, M.link_grads(g), ws,
+                              dw_stream=side, fork=fork)
+        else:
+            M.mtgnn_link_loss(z, n_q, 3 * max_tar, M.link_params(p), d, loss, scores, dz, M.link_grads(g), ws)
+        torch.cuda.synchronize()
+        outs.append([loss, scores, dz] + [g[k] for k in sorted(g)])
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
