@@ -1188,6 +1188,8 @@ void launch_segsum_fixup(const SegCtx& c, const int32_t* n_rows, int64_t max_row
 
 struct BwdWs {
   float *dm1, *dm_in, *dattn, *dqv, *dKV, *tg_part, *tg_part2, *S, *head, *tail, *dWkv, *dbkv;
+  char* scratch_merge;    // split-K partials of the output and merge layers' weight gradients (their own:
+  size_t scratch_merge_bytes;   // with a second stream they run there, beside the other products)
   uint32_t *keys, *vals;
   int32_t *seg_lo, *seg_hi, *row_of;
   char* scratch;          // split-K partials of the parameter-gradient products
@@ -1196,6 +1198,13 @@ struct BwdWs {
   size_t sort_scratch_bytes;
   size_t total;
 };
+
+// The output and merge layers' weight gradients apart from the query layer's, on the second stream when
+// there is one, from this many query rows on (at a few thousand rows that batch, beside the score
+// backward and the query projection's data gradient, slowed them more than it saved: 7.98 -> 7.80 M
+// events/s on the skewed stream, 12,000 queries; 6.35 -> 6.73 M at 180,000).
+constexpr int64_t MERGE_DW_APART_ROWS = 65536;
+bool merge_dw_apart(int64_t Q) { return Q >= MERGE_DW_APART_ROWS; }
 
 BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   char* w = (char*)base;
@@ -1225,11 +1234,19 @@ BwdWs carve_bwd(void* base, const AttnShape& s, int64_t max_rows) {
   size_t sc = 0;
   auto mx = [&](size_t x) { if (x > sc) sc = x; };
   {
-    // the query weight's problem spans d_m columns when its time columns are closed-form, else D_q
+    // the query weight's problem spans d_m columns when its time columns are closed-form, else D_q;
+    // with the query layer on its own (merge_dw_apart) the other three have a region of their own
     const int64_t Ns[4] = {s.da, s.da, s.da, s.da}, Ks[4] = {s.da, s.da + s.dm, s.da, s.Dq};
     const int64_t Ks2[4] = {s.da, s.da + s.dm, s.da, s.dm};
     mx(linear_dw_batch_ws_bytes(s.Q, Ns, Ks, 4));
     mx(linear_dw_batch_ws_bytes(s.Q, Ns, Ks2, 4));
+    v.scratch_merge_bytes = 256;
+    if (merge_dw_apart(s.Q)) {
+      mx(linear_dw_batch_ws_bytes(s.Q, Ns + 3, Ks + 3, 1));
+      mx(linear_dw_batch_ws_bytes(s.Q, Ns + 3, Ks2 + 3, 1));
+      v.scratch_merge_bytes = a256(linear_dw_batch_ws_bytes(s.Q, Ns, Ks, 3));
+    }
+    v.scratch_merge = take(v.scratch_merge_bytes);
   }
   mx(linear_dw_ws_bytes(s.P, 2 * s.da, s.Dkv));
   v.scratch = take(sc > 0 ? sc : 1);
@@ -1504,12 +1521,25 @@ mtgnn_status attn_bwd_dmem_sum(int64_t max_q, const AttnShape& sh, const AttnSav
   return MTGNN_OK;
 }
 
-// The parameter gradients that follow the fork point (weight gradients of the
-// query/output/merge layers and of [W_k; W_v], the time-encoder gradients).
+// Weight gradients of the merge MLP and the output projection, one batch over the query rows: they need
+// only dz and the merge backward's dm1 and do (dm_in's first d_a columns), so with a second stream they
+// run there while the score backward and the query projection's data gradient run on `stream`.
+mtgnn_status attn_bwd_merge_dw(const int32_t* n_q, const AttnShape& sh, const AttnSave& sv, const BwdWs& b,
+                               const float* dz, mtgnn_attn_grads* g, hipStream_t s) {
+  const int64_t ldm = sh.da + sh.dm;
+  const int da = sh.da;
+  const DwProblem ps[3] = {{dz, da, sv.a1, da, g->W_2, da, da, da, g->b_2},
+                           {b.dm1, da, sv.m_in, ldm, g->W_1, ldm, da, ldm, g->b_1},
+                           {b.dm_in, ldm, sv.attn, da, g->W_o, da, da, da, g->b_o}};
+  return linear_dw_batch(ps, 3, sh.Q, n_q, MTGNN_F32, b.scratch_merge, b.scratch_merge_bytes, s);
+}
+
+// The parameter gradients that follow the fork point (weight gradient of the
+// query layer and of [W_k; W_v], the time-encoder gradients).
 mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const AttnSave& sv, const BwdWs& b,
                              const float* dz, const float* tw, const float* tb, const mtgnn_attn_params* p,
                              int wt, mtgnn_attn_grads* g, float* d_time_w, float* d_time_b, hipStream_t s) {
-  const int64_t Q = sh.Q, P = sh.P, ldm = sh.da + sh.dm;
+  const int64_t Q = sh.Q, P = sh.P;
   const int da = sh.da, dm = sh.dm, dt = sh.dt;
   char* sc = b.scratch;
   const size_t scb = b.scratch_bytes;
@@ -1533,13 +1563,16 @@ mtgnn_status attn_bwd_params(const int32_t* n_q, const AttnShape& sh, const Attn
       MTGNN_TRY(timegrad_reduce_blocks2(b.tg_part, Q, n_q, b.tg_part2, P, sv.n_valid, G_TG_ROWS, dt, d_time_w,
                                         d_time_b, s));
   }
-  // weight gradients of the query, output and merge layers, one batch over the query rows
+  // weight gradients of the query, output and merge layers, one batch over the query rows (the query
+  // layer's alone when the others run apart: attn_bwd_merge_dw)
   {
+    const int64_t ldm = sh.da + sh.dm;
     const DwProblem ps[4] = {{dz, da, sv.a1, da, g->W_2, da, da, da, g->b_2},
                              {b.dm1, da, sv.m_in, ldm, g->W_1, ldm, da, ldm, g->b_1},
                              {b.dm_in, ldm, sv.attn, da, g->W_o, da, da, da, g->b_o},
                              {b.dqv, da, sv.q_in, sh.Dq, g->W_q, sh.Dq, da, q_closed && dt > 0 ? dm : sh.Dq, g->b_q}};
-    MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
+    if (merge_dw_apart(Q)) MTGNN_TRY(linear_dw_batch(ps + 3, 1, Q, n_q, MTGNN_F32, sc, scb, s));
+    else MTGNN_TRY(linear_dw_batch(ps, 4, Q, n_q, MTGNN_F32, sc, scb, s));
   }
   if (dt > 0 && q_closed)
     MTGNN_TRY(timegrad_reduce_slots_q(b.tg_part2, P, sv.n_valid, G_TG_ROWS, dt, g->b_q, (const float*)p->W_q, sh.Dq,
@@ -1621,6 +1654,19 @@ mtgnn_status attn_bwd_impl(const int32_t* q_node, const float* q_t, const int32_
       MTGNN_TRY(linear_dx(dz, da, p->W_2, wt, da, b.dm1, da, Q, n_q, da, da, false, s, sv.m1, da));
       MTGNN_TRY(linear_dx(b.dm1, da, p->W_1, wt, ldm, b.dm_in, ldm, Q, n_q, da, ldm, false, s));
       MTGNN_TRY(linear_dx(b.dm_in, ldm, p->W_o, wt, da, b.dattn, da, Q, n_q, da, da, false, s));
+    }
+    // their weight gradients (many query rows): on the second stream (after a fork) while the rest of the
+    // chain runs here (the query projection's data gradient writes dm_in's other columns only)
+    if (merge_dw_apart(Q) && overlap) {
+      hipError_t e = hipEventRecord(fork, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s_dmem, fork, 0);
+      if (e != hipSuccess) {
+        set_hip_error(e, "attn_bwd fork");
+        return MTGNN_EHIP;
+      }
+      MTGNN_TRY(attn_bwd_merge_dw(n_q, sh, sv, b, dz, g, s_dmem));
+    } else if (merge_dw_apart(Q)) {
+      MTGNN_TRY(attn_bwd_merge_dw(n_q, sh, sv, b, dz, g, s));
     }
     // softmax-weighted sum and scores
     {

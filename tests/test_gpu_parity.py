@@ -170,15 +170,22 @@ def test_edge_large_batch_multiblock_paths():
     _tiny_run(w, s, mem, lu, range(1, 3))
 
 
-def test_backward_overlap_bitwise():
+@pytest.mark.parametrize("case", ["bipartite", "large_batch"])
+def test_backward_overlap_bitwise(case):
     """The two-stream attention backward (d_mem part on a second stream) gives bitwise the
     results of the single-stream call, from the same state (bipartite stream, 3 steps), both with
     the d_mem grouping at the backward's entry (mtgnn_temporal_attn_bwd_overlap) and with it done
-    during the embedding (mtgnn_temporal_attn_bwd_group, then _grouped)."""
+    during the embedding (mtgnn_temporal_attn_bwd_group, then _grouped).  large_batch: 22,000 events
+    per batch (66,000 query rows), where the output and merge layers' weight gradients also run on
+    the second stream."""
     from paper_2608_16305_amd.step import TGNStep
-    w = workload(2)
-    log("[parity] overlap vs single stream, workload 2")
-    s = make_stream(w)
+    if case == "bipartite":
+        w = workload(2)
+    else:
+        w = tiny_workload(n_nodes=30000, n_events=88000, batch=22000, k=3, d_mem=8, d_time=4, d_edge=2, d_attn=8,
+                          n_heads=2)
+    log(f"[parity] overlap vs single stream, {case}")
+    s = make_stream(w) if case == "bipartite" else tiny_stream(w, seed=3)
     params = init_params(w, random_bias=True)
     mem, lu = random_state(w, seed=11)
     outs = []
