@@ -24,6 +24,13 @@ __device__ __forceinline__ void splitk_reduce_body(const float* __restrict__ par
   float s = 0.f;
   if (e < rows * cols) {
     int z = g;
+    for (; z + 60 < nsplit; z += 64) {   // sixteen loads in flight, added as four passes of the loop below
+      float a[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) a[u] = part[(int64_t)(z + 4 * u) * split_stride + pe];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s += ((a[4 * q] + a[4 * q + 1]) + a[4 * q + 2]) + a[4 * q + 3];
+    }
     for (; z + 12 < nsplit; z += 16) {   // four loads in flight
       const float a0 = part[(int64_t)z * split_stride + pe], a1 = part[(int64_t)(z + 4) * split_stride + pe];
       const float a2 = part[(int64_t)(z + 8) * split_stride + pe], a3 = part[(int64_t)(z + 12) * split_stride + pe];
