@@ -12,9 +12,11 @@ and joined with events: the queries, their sampling and the attention's
 preparation, during the memory phase; the next step's aggregation and
 messages (lag-1 order: its memory batch is this step's batch, read from the
 memory this step's update leaves), and the attention backward's d_mem
-grouping (a key sort), during the embedding; and the backward's d_mem sums
-followed by the GRU backward, during the attention parameter gradients.
-Results are bitwise those of overlap=False.
+grouping (a key sort), during the embedding; the decoder's first-layer weight
+gradient, during the backward's data gradients; the output and merge layers'
+weight gradients at batches of 65,536 queries or more, beside the score
+backward; and the backward's d_mem sums followed by the GRU backward, during
+the attention parameter gradients.  Results are bitwise those of overlap=False.
 """
 
 import numpy as np
