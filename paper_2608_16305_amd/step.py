@@ -7,7 +7,7 @@ A step on batch b (default lag-1 order) runs
   backward:                   temporal_attn_bwd -> gru_update_bwd -> build_messages_bwd
 all enqueued on one HIP stream with no host synchronisation (the only
 data-dependent sizes, updated rows and queries, stay in device memory), except
-that with overlap=True (the default) two pieces run on a second stream, forked
+that with overlap=True (the default) several pieces run on a second stream, forked
 and joined with events: the queries, their sampling and the attention's
 preparation, during the memory phase; the next step's aggregation and
 messages (lag-1 order: its memory batch is this step's batch, read from the
