@@ -906,35 +906,38 @@ __global__ __launch_bounds__(256) void k_segsum_tiles(SegCtx c) {
   flush(cnt);
 }
 
-// k_segsum_tiles with 16-byte groups (d_mem and d_attn divisible by 4, W <= 512): lane l holds
-// the row's 4-column groups l and l + 64, so a neighbour slot's row is two loads per lane and a
-// query's one.  Every column's sum runs over the positions in the same order as k_segsum_tiles,
-// so the results are bitwise the same.
-__device__ __forceinline__ float4 f4add(float4 a, float4 b) {
-  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-}
-
 // A finished segment's sums (groups qa and qb of this lane): a whole segment to D / S, a piece that
 // began before the tile to head[tile], one that continues past it to tail[tile].
 __device__ __forceinline__ void seg_flush_v4(const SegCtx& c, int64_t tile, uint32_t cur, bool before, bool after,
-                                             int qa, int qb, float4 acc_a, float4 acc_b) {
+                                             int qa, int qb, f32x4 acc_a, f32x4 acc_b) {
   const int W = c.dm + c.w2, W4 = W >> 2, dm4 = c.dm >> 2;
   if (!before && !after) {
     float* row_d = c.D + (int64_t)cur * c.dm;
     float* row_s = c.S + (int64_t)cur * W;
-    if (qa < dm4) *(float4*)(row_d + 4 * qa) = acc_a;
-    else if (qa < W4) *(float4*)(row_s + 4 * qa) = acc_a;
-    if (qb < dm4) *(float4*)(row_d + 4 * qb) = acc_b;
-    else if (qb < W4) *(float4*)(row_s + 4 * qb) = acc_b;
+    if (qa < dm4) *(f32x4*)(row_d + 4 * qa) = acc_a;
+    else if (qa < W4) *(f32x4*)(row_s + 4 * qa) = acc_a;
+    if (qb < dm4) *(f32x4*)(row_d + 4 * qb) = acc_b;
+    else if (qb < W4) *(f32x4*)(row_s + 4 * qb) = acc_b;
     return;
   }
   float* dst = before ? c.head + tile * W : c.tail + tile * W;
-  if (qa < W4) *(float4*)(dst + 4 * qa) = acc_a;
-  if (qb < W4) *(float4*)(dst + 4 * qb) = acc_b;
+  if (qa < W4) *(f32x4*)(dst + 4 * qa) = acc_a;
+  if (qb < W4) *(f32x4*)(dst + 4 * qb) = acc_b;
 }
 
+// A loaded 16-byte group kept in its registers (see keep_live).
+__device__ __forceinline__ void keep_live4(f32x4& v) { asm volatile("" : "+v"(v)); }
+
+// k_segsum_tiles with 16-byte groups (d_mem and d_attn divisible by 4, W <= 512): lane l holds
+// the row's 4-column groups l and l + 64.  Every column's sum runs over the positions in the same
+// order as k_segsum_tiles, so the results are bitwise the same.  The tile's positions are read with
+// wave-uniform lane indices, so the keys and row choices are scalar; each prefetched position loads
+// one clamped 16-byte group per lane group, unconditionally (a position past the tile's end or past
+// its last key re-reads position 0's row), and the groups outside the row are zeroed afterwards.
+// With no load under a per-lane test, all of a batch's loads are in flight together.
 __global__ __launch_bounds__(256) void k_segsum_tiles_v4(SegCtx c) {
-  const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t tile = (int64_t)blockIdx.x * 4 + wid;
   const int lane = threadIdx.x & 63;
   const int64_t p0 = tile * c.tile;
   if (p0 >= c.n_occ) return;
@@ -945,40 +948,38 @@ __global__ __launch_bounds__(256) void k_segsum_tiles_v4(SegCtx c) {
   const uint32_t my_val = lane < cnt ? c.vals[p0 + lane] : 0u;
   const uint32_t key_before = p0 > 0 ? c.keys[p0 - 1] : c.sentinel;
   const uint32_t key_after = p0 + cnt < c.n_occ ? c.keys[p0 + cnt] : c.sentinel;
-  uint32_t cur = __shfl(my_key, 0, 64);
+  uint32_t cur = (uint32_t)__builtin_amdgcn_readfirstlane((int)my_key);
   if (cur == c.sentinel) return;   // sentinels sort last: nothing in this tile
-  const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
-  // groups this lane loads from a query row (columns < dm) and from a slot row (columns >= dm)
-  const bool qa_q = qa < dm4, qb_q = qb < dm4;
-  const bool qa_s = qa >= dm4 && qa < W4, qb_s = qb >= dm4 && qb < W4;
+  const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
   int start = 0;
-  float4 acc_a = z4, acc_b = z4;
+  f32x4 acc_a = z4, acc_b = z4;
   for (int q0 = 0; q0 < cnt; q0 += SEG_PREFETCH) {
-    float4 ra[SEG_PREFETCH], rb[SEG_PREFETCH];
+    f32x4 ra[SEG_PREFETCH], rb[SEG_PREFETCH];
+    bool va[SEG_PREFETCH], vb[SEG_PREFETCH];
 #pragma unroll
     for (int u = 0; u < SEG_PREFETCH; ++u) {
       const int p = q0 + u;
-      const uint32_t k = __shfl(my_key, p, 64);
-      const uint32_t o = __shfl(my_val, p, 64);
-      ra[u] = z4;
-      rb[u] = z4;
-      if (p < cnt && k != c.sentinel) {
-        if ((int64_t)o < c.max_q) {
-          const float* src = c.dhq + (int64_t)o * c.ldq;
-          if (qa_q) ra[u] = *(const float4*)(src + 4 * qa);
-          if (qb_q) rb[u] = *(const float4*)(src + 4 * qb);
-        } else {
-          const float* src = c.dkv + ((int64_t)o - c.max_q) * c.w2 - c.dm;   // column col at src[col]
-          if (qa_s) ra[u] = *(const float4*)(src + 4 * qa);
-          if (qb_s) rb[u] = *(const float4*)(src + 4 * qb);
-        }
-      }
+      const uint32_t k = (uint32_t)__builtin_amdgcn_readlane((int)my_key, p < cnt ? p : 0);
+      const bool live = p < cnt && k != c.sentinel;
+      const uint32_t o = (uint32_t)__builtin_amdgcn_readlane((int)my_val, live ? p : 0);
+      const bool isq = (int64_t)o < c.max_q;
+      const float* src = isq ? c.dhq + (int64_t)o * c.ldq : c.dkv + ((int64_t)o - c.max_q) * c.w2 - c.dm;
+      const int lo = isq ? 0 : dm4, hi = isq ? dm4 : W4;   // the row's groups: [lo, hi), never empty
+      ra[u] = *(const f32x4*)(src + 4 * min(max(qa, lo), hi - 1));
+      rb[u] = *(const f32x4*)(src + 4 * min(max(qb, lo), hi - 1));
+      va[u] = live && qa >= lo && qa < hi;
+      vb[u] = live && qb >= lo && qb < hi;
+    }
+#pragma unroll
+    for (int u = 0; u < SEG_PREFETCH; ++u) {
+      keep_live4(ra[u]);
+      keep_live4(rb[u]);
     }
 #pragma unroll
     for (int u = 0; u < SEG_PREFETCH; ++u) {
       const int p = q0 + u;
       if (p < cnt) {
-        const uint32_t k = __shfl(my_key, p, 64);
+        const uint32_t k = (uint32_t)__builtin_amdgcn_readlane((int)my_key, p);
         if (k != cur) {
           seg_flush_v4(c, tile, cur, start == 0 && key_before == cur, false, qa, qb, acc_a, acc_b);
           if (k == c.sentinel) return;
@@ -987,8 +988,8 @@ __global__ __launch_bounds__(256) void k_segsum_tiles_v4(SegCtx c) {
           acc_a = z4;
           acc_b = z4;
         }
-        acc_a = f4add(acc_a, ra[u]);
-        acc_b = f4add(acc_b, rb[u]);
+        acc_a += va[u] ? ra[u] : z4;
+        acc_b += vb[u] ? rb[u] : z4;
       }
     }
   }
@@ -998,10 +999,11 @@ __global__ __launch_bounds__(256) void k_segsum_tiles_v4(SegCtx c) {
 // The rows no tile could finish.  Every wave first zeroes, grid-stride, the rows with no occurrence.
 // Then block b checks tiles tpb b .. tpb b + tpb - 1 (one lane each, tpb <= 64, about 1024 blocks over
 // all tiles, so that a skewed stream's many hub rows spread over many blocks): a tile whose last row starts in it and
-// continues past it (rows inside one tile were written whole) has that row summed by the whole block:
-// tail[tile] + head[tile + 1] + ... + head[t1].  The waves take interleaved heads, four at a time with
-// all their loads in flight (no per-lane test: a chunk past the row's W columns re-reads column W - 1
-// and is never stored), and their partial sums are added in wave order.  NC = ceil(W / 64) <= 5.
+// continues past it (rows inside one tile were written whole) has that row summed:
+// tail[tile] + head[tile + 1] + ... + head[t1].  A row of more than FIX_WAVES heads is summed by the
+// whole block: the waves take interleaved heads, four at a time with all their loads in flight (no
+// per-lane test: a chunk past the row's W columns re-reads column W - 1 and is never stored), and their
+// partial sums are added in wave order.  A shorter row is summed by one wave.  NC = ceil(W / 64) <= 5.
 constexpr int FIX_WAVES = 16;
 constexpr int FIX_BLOCKS = 1024;   // blocks the tile checks aim for
 
@@ -1025,7 +1027,9 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
   // the rest depends on the block only (uniform branches around the barriers)
   const int64_t tile0 = blk * tpb;
   if (tile0 >= ntiles) return;
-  uint64_t todo;   // lane l: does tile tile0 + l end inside a row that starts in it and continues past it?
+  // lane l: does tile tile0 + l end inside a row that starts in it and continues past it (todo: for more
+  // than FIX_WAVES further tiles, shorter: for fewer)?
+  uint64_t todo, shorter;
   {
     const int64_t tile = tile0 + lane < ntiles ? tile0 + lane : ntiles - 1;
     const int64_t p_last = min((tile + 1) * c.tile, c.n_occ) - 1;
@@ -1033,11 +1037,54 @@ __global__ __launch_bounds__(64 * FIX_WAVES) void k_segsum_fixup(SegCtx c, const
     const uint32_t key = c.keys[p_last], next = c.keys[p_next];
     const bool cont = lane < tpb && tile0 + lane < ntiles && p_last + 1 < c.n_occ && key != c.sentinel && next == key;
     const bool starts = cont && c.seg_lo[key] >= tile * c.tile;
-    todo = __ballot(starts);
+    const bool longer = starts && (int64_t)(c.seg_hi[key] - 1) / c.tile - tile > FIX_WAVES;
+    todo = __ballot(starts && longer);
+    shorter = __ballot(starts && !longer);
   }
   int cc[NC];
 #pragma unroll
   for (int i = 0; i < NC; ++i) cc[i] = lane + 64 * i < W ? lane + 64 * i : W - 1;
+  // Rows with at most FIX_WAVES heads: one wave each (every FIX_WAVES-th such row to this wave).  On
+  // the block path each wave would hold at most one head and the parts be added in wave order, so
+  // tail + (((0 + head 1) + head 2) + ...) here is the same sum, bit for bit.
+  for (int idx = 0; shorter; ++idx) {
+    const int l = __builtin_ctzll(shorter);
+    shorter &= shorter - 1;
+    if (idx % FIX_WAVES != wid) continue;
+    const int64_t tile = tile0 + l;
+    const int64_t p_last = min((tile + 1) * c.tile, c.n_occ) - 1;
+    const uint32_t key = c.keys[p_last];
+    const int64_t t1 = (c.seg_hi[key] - 1) / c.tile;
+    const float* tl = c.tail + tile * W;
+    float acc[NC], tv[NC];
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      tv[i] = tl[cc[i]];
+      acc[i] = 0.f;
+    }
+    for (int64_t t = tile + 1; t <= t1; t += 4) {   // four heads' loads in flight, added in order
+      float v[4][NC];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float* h = c.head + (t + u <= t1 ? t + u : t1) * W;
+#pragma unroll
+        for (int i = 0; i < NC; ++i) v[u][i] = h[cc[i]];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int i = 0; i < NC; ++i) keep_live(v[u][i]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (t + u <= t1) {
+#pragma unroll
+          for (int i = 0; i < NC; ++i) acc[i] += v[u][i];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < NC; ++i) acc[i] = tv[i] + acc[i];
+    seg_store_row<NC>(c, (int64_t)key, acc, lane);
+  }
   while (todo) {
     const int l = __builtin_ctzll(todo);
     todo &= todo - 1;
