@@ -391,6 +391,27 @@ mtgnn_status mtgnn_link_loss_overlap(const float* z, const int32_t* n_q, int64_t
                                      float* scores, float* dz, mtgnn_link_grads* grads, void* ws, size_t ws_bytes,
                                      hipStream_t stream, hipStream_t dw_stream, hipEvent_t fork);
 
+/* The decoder's weight copies of mtgnn_link_loss (Eq. 13's scoring layer), made ahead on any stream so
+ * that the loss itself need not make them: the zero-padded column halves of params->W_d1 and their
+ * transposes, written into ws (the workspace a later mtgnn_link_loss_prepared call with the same
+ * d_attn and max_q gets; nothing else in ws is touched).  At widths the fused decoder kernel does not
+ * take (d_attn a multiple of 4 in 17..32 or 97..112) nothing is written.  The copies stay valid until
+ * W_d1 or ws is written again.
+ * Errors: as mtgnn_link_loss for max_q, dims, params->W_d1 and ws. */
+mtgnn_status mtgnn_link_prepare_weights(const mtgnn_link_params* params, const mtgnn_dims* dims, int64_t max_q,
+                                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* mtgnn_link_loss (dw_stream and fork NULL) or mtgnn_link_loss_overlap (both given) with the decoder's
+ * weight copies already in ws: a mtgnn_link_prepare_weights call with the same params->W_d1, dims,
+ * max_q and ws, ordered before this call on `stream` (same stream, or an event the caller records
+ * after it and `stream` waits for), and W_d1 not written since.  Same computation and bitwise results
+ * as those calls.  Errors: as mtgnn_link_loss_overlap; EINVAL if only one of dw_stream and fork is
+ * NULL. */
+mtgnn_status mtgnn_link_loss_prepared(const float* z, const int32_t* n_q, int64_t max_q,
+                                      const mtgnn_link_params* params, const mtgnn_dims* dims, float* loss,
+                                      float* scores, float* dz, mtgnn_link_grads* grads, void* ws, size_t ws_bytes,
+                                      hipStream_t stream, hipStream_t dw_stream, hipEvent_t fork);
+
 /* Backward of the GRU memory update (Eq. 2), mtgnn_gru_update, for d_mem = dL/dh' [max_rows, d_mem].
  * The previous memory h is detached.
  *   save, msg   -- the forward call's (save must not be NULL there);

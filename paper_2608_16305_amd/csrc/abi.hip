@@ -538,6 +538,29 @@ mtgnn_status mtgnn_link_loss_overlap(const float* z, const int32_t* n_q, int64_t
   return link_loss_impl(z, n_q, max_q, params, d, loss, scores, dz, grads, ws, ws_bytes, stream, dw_stream, fork);
 }
 
+mtgnn_status mtgnn_link_prepare_weights(const mtgnn_link_params* params, const mtgnn_dims* d, int64_t max_q, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  if (max_q < 0 || max_q >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (max_q % 3 != 0) return fail(MTGNN_EINVAL, "max_q is not a multiple of 3 (src, dst and negative blocks)");
+  if (d->d_attn > 128) return fail(MTGNN_EUNSUPPORTED, "link_prepare_weights: d_attn > 128");
+  REQ(params, "params");
+  REQ(params->W_d1, "W_d1");
+  if (ws_bytes < link_loss_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "link_prepare_weights ws");
+  REQ(ws, "ws");
+  return link_prepare_impl(params, d, max_q, ws, stream);
+}
+
+mtgnn_status mtgnn_link_loss_prepared(const float* z, const int32_t* n_q, int64_t max_q,
+                                      const mtgnn_link_params* params, const mtgnn_dims* d, float* loss,
+                                      float* scores, float* dz, mtgnn_link_grads* grads, void* ws, size_t ws_bytes,
+                                      hipStream_t stream, hipStream_t dw_stream, hipEvent_t fork) {
+  MTGNN_TRY(check_link_loss(z, max_q, params, d, loss, dz, grads, ws, ws_bytes));
+  if ((dw_stream == nullptr) != (fork == nullptr)) return fail(MTGNN_EINVAL, "dw_stream and fork: both or neither");
+  return link_loss_impl(z, n_q, max_q, params, d, loss, scores, dz, grads, ws, ws_bytes, stream, dw_stream, fork,
+                        true);
+}
+
 mtgnn_status mtgnn_build_messages_bwd(const float* dmsg_time, const float* dt, const int32_t* n_rows,
                                       int64_t max_rows, const float* time_w, const float* time_b, const mtgnn_dims* d,
                                       float* d_time_w, float* d_time_b, void* ws, size_t ws_bytes,

@@ -141,9 +141,17 @@ size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q) {
   return total;
 }
 
+mtgnn_status link_prepare_impl(const mtgnn_link_params* p, const mtgnn_dims* d, int64_t max_q, void* ws,
+                               hipStream_t s) {
+  const int da = d->d_attn;
+  if (!link_fused_ok(da)) return MTGNN_OK;   // the general widths read W_d1 directly
+  const LinkWs L = link_ws_layout(ws, da, max_q);
+  return link_prepare_weights(p->W_d1, da, L.Wp, s);
+}
+
 mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* p,
                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
-                            size_t ws_bytes, hipStream_t s, hipStream_t s_dw, hipEvent_t fork) {
+                            size_t ws_bytes, hipStream_t s, hipStream_t s_dw, hipEvent_t fork, bool prepared) {
   const int da = d->d_attn;
   if (da > 64 * LINK_MAX_COLS) return MTGNN_EUNSUPPORTED;
   if (ws_bytes < link_loss_ws(d, max_q)) return MTGNN_EWORKSPACE;
@@ -151,7 +159,7 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
   LinkWs L = link_ws_layout(ws, da, max_q);
   if (link_fused_ok(da)) {
     MTGNN_TRY(link_fused(z, n_q, max_q, da, p->W_d1, p->b_d1, p->W_d2, p->b_d2, L.Wp, L.DA, L.DB, L.part, dz, scores,
-                         g->W_d2, g->b_d2, loss, s));
+                         g->W_d2, g->b_d2, loss, s, prepared));
     // W_d1's gradient needs only DA, DB and z: on the second stream if there is one
     if (s_dw) {
       hipError_t e = hipEventRecord(fork, s);

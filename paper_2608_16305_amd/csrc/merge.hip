@@ -990,10 +990,8 @@ size_t link_fused_weight_floats(int da) {
   return (size_t)4 * 16 * MW * cdiv(na, MW) * 16 * na;
 }
 
-mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
-                        const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
-                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s) {
-  if (!link_fused_ok(da) || !aligned16(z) || !aligned16(Wp) || !aligned16(dz)) return MTGNN_EUNSUPPORTED;
+mtgnn_status link_prepare_weights(const float* W1, int da, float* Wp, hipStream_t s) {
+  if (!link_fused_ok(da) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
   const int na = (int)cdiv(da, 16);
   const int rows = 16 * MW * (int)cdiv(na, MW), cols = 16 * na;
   const size_t wsz = (size_t)rows * cols;
@@ -1013,6 +1011,15 @@ mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int d
   a.ncopy = 4;
   k_merge_prepare<<<dim3((unsigned)cdiv(wsz, 256), 4u), 256, 0, s>>>(a);
   MTGNN_CHECK_LAUNCH("link_prepare");
+  return MTGNN_OK;
+}
+
+mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
+                        const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
+                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s, bool prepared) {
+  if (!link_fused_ok(da) || !aligned16(z) || !aligned16(Wp) || !aligned16(dz)) return MTGNN_EUNSUPPORTED;
+  if (!prepared) MTGNN_TRY(link_prepare_weights(W1, da, Wp, s));
+  const int na = (int)cdiv(da, 16);
   const int64_t max_tar = max_q / 3;
   const int64_t nblk = cdiv(max_tar < 1 ? 1 : max_tar, 16);
   if (max_tar > 0) {

@@ -77,15 +77,23 @@ mtgnn_status gru_fused(const float* msg, const float* W_ih, const float* W_hh, c
 // column sums of the per-block partials into dW_d2, db_d2 and the loss.  Wp: link_fused_weight_floats.
 bool link_fused_ok(int da);
 size_t link_fused_weight_floats(int da);
+// prepared: Wp already holds link_prepare_weights' copies of this W1 (else they are made first).
 mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
                         const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
-                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s);
+                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s, bool prepared = false);
+// The zero-padded copies of W_d1's two column halves and their transposes that link_fused reads from Wp.
+mtgnn_status link_prepare_weights(const float* W1, int da, float* Wp, hipStream_t s);
 size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q);
 // s_dw, fork: a second stream and an event (or NULL, NULL): W_d1's gradient is then enqueued on s_dw after
 // fork, recorded on s once dz and the decoder's row gradients are written (fused widths only).
+// prepared: link_prepare_impl has filled ws's weight copies from p (same max_q), ordered before this call.
 mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* p,
                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
-                            size_t ws_bytes, hipStream_t s, hipStream_t s_dw = nullptr, hipEvent_t fork = nullptr);
+                            size_t ws_bytes, hipStream_t s, hipStream_t s_dw = nullptr, hipEvent_t fork = nullptr,
+                            bool prepared = false);
+// The fused decoder's weight copies in the link workspace (nothing at the general widths).
+mtgnn_status link_prepare_impl(const mtgnn_link_params* p, const mtgnn_dims* d, int64_t max_q, void* ws,
+                               hipStream_t s);
 
 // offline dependency scan (Algorithm 1) and the mixed batches of one worker
 mtgnn_status dep_scan_impl(const int32_t* src, const int32_t* dst, int64_t E, const int32_t* owner, int64_t n_nodes,

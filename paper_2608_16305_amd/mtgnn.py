@@ -25,7 +25,8 @@ ENTRY_POINTS = (
     "mtgnn_temporal_attn_prepare_slots", "mtgnn_temporal_attn_prepared",
     "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap", "mtgnn_temporal_attn_bwd_group",
     "mtgnn_temporal_attn_bwd_grouped",
-    "mtgnn_gru_update_bwd", "mtgnn_link_loss", "mtgnn_link_loss_overlap",
+    "mtgnn_gru_update_bwd", "mtgnn_link_loss", "mtgnn_link_loss_overlap", "mtgnn_link_prepare_weights",
+    "mtgnn_link_loss_prepared",
     "mtgnn_build_messages_bwd", "mtgnn_build_messages_bwd_noalloc", "mtgnn_build_temporal_csr",
     "mtgnn_dependency_scan", "mtgnn_mixed_batches", "mtgnn_rnn_update", "mtgnn_rnn_update_bwd",
     "mtgnn_time_projection", "mtgnn_time_projection_bwd", "mtgnn_controller_create", "mtgnn_controller_destroy",
@@ -113,6 +114,9 @@ _SIGS = {
                         _SZ, _P],
     "mtgnn_link_loss_overlap": [_P, _P, _I64, C.POINTER(LinkParams), C.POINTER(Dims), _P, _P, _P,
                                 C.POINTER(LinkGrads), _P, _SZ, _P, _P, _P],
+    "mtgnn_link_prepare_weights": [C.POINTER(LinkParams), C.POINTER(Dims), _I64, _P, _SZ, _P],
+    "mtgnn_link_loss_prepared": [_P, _P, _I64, C.POINTER(LinkParams), C.POINTER(Dims), _P, _P, _P,
+                                 C.POINTER(LinkGrads), _P, _SZ, _P, _P, _P],
     "mtgnn_build_messages_bwd": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P, _SZ, _P],
     "mtgnn_build_messages_bwd_noalloc": [_P, _P, _P, _I64, _P, _P, C.POINTER(Dims), _P, _P, _P],
     "mtgnn_build_temporal_csr": [_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _SZ, _P],
@@ -454,14 +458,25 @@ def link_grads(g: dict) -> LinkGrads:
     return LinkGrads(*[_ptr(g[n], torch.float32, "d" + n) for n in _LINK])
 
 
+def mtgnn_link_prepare_weights(params: LinkParams, d: Dims, max_q, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(lib().mtgnn_link_prepare_weights(C.byref(params), C.byref(d), int(max_q), wp, wb, _stream(stream)),
+           "mtgnn_link_prepare_weights")
+
+
 def mtgnn_link_loss(z, n_q, max_q, params: LinkParams, d: Dims, loss, scores, dz, grads: LinkGrads, ws, stream=None,
-                    dw_stream=None, fork=None):
-    """dw_stream and fork given: mtgnn_link_loss_overlap (W_d1's gradient on dw_stream after fork)."""
+                    dw_stream=None, fork=None, prepared=False):
+    """dw_stream and fork given: mtgnn_link_loss_overlap (W_d1's gradient on dw_stream after fork).
+    prepared: mtgnn_link_loss_prepared (ws holds mtgnn_link_prepare_weights' copies of params' W_d1)."""
     wp, wb = _ws(ws)
     args = (_ptr(z, torch.float32, "z"), _ptr(n_q, torch.int32, "n_q", True), int(max_q), C.byref(params), C.byref(d),
             _ptr(loss, torch.float32, "loss"), _ptr(scores, torch.float32, "scores", True), _ptr(dz, torch.float32, "dz"),
             C.byref(grads), wp, wb, _stream(stream))
-    if dw_stream is None:
+    if prepared:
+        ov = dw_stream is not None
+        _check(lib().mtgnn_link_loss_prepared(*args, _stream(dw_stream) if ov else None,
+                                              _event(fork, "fork") if ov else None), "mtgnn_link_loss_prepared")
+    elif dw_stream is None:
         _check(lib().mtgnn_link_loss(*args), "mtgnn_link_loss")
     else:
         _check(lib().mtgnn_link_loss_overlap(*args, _stream(dw_stream), _event(fork, "fork")),

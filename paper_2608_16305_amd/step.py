@@ -138,6 +138,7 @@ class TGNStep:
         self.m_done, self.pre_join = M.DeviceEvent(), M.DeviceEvent()
         self.group_ahead = True   # step(): the backward's d_mem grouping during the embedding (second stream)
         self._grouped = False     # ... and it has been enqueued
+        self._link_ready = False  # step(): the decoder's weight copies made on the second stream for its loss
 
     def _batch(self, lo, hi):
         if hi <= lo:
@@ -211,8 +212,12 @@ class TGNStep:
         decoder's first-layer weight gradient runs on the second stream (idle between the embedding and
         the backward's d_mem sums), ahead of the d_mem work there, so the backward's join covers it."""
         if self.overlap:
+            # prepared: the step made the decoder's weight copies on the second stream before the join
+            # that precedes the embedding
             M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz,
-                              self.lg, self.ws_link, stream=self.ts, dw_stream=self.side_stream, fork=self.l_fork)
+                              self.lg, self.ws_link, stream=self.ts, dw_stream=self.side_stream, fork=self.l_fork,
+                              prepared=self._link_ready)
+            self._link_ready = False
         else:
             M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz,
                               self.lg, self.ws_link, stream=self.ts)
@@ -282,6 +287,11 @@ class TGNStep:
                 self.q_fork.record(main)
                 self.q_fork.wait(side)
             self.queries(elo, ehi, side)
+            if dz is None and self.has_link:
+                # the decoder's weight copies, here rather than at the loss on the main stream: this stream
+                # is done with its queries well before the main stream waits for them
+                M.mtgnn_link_prepare_weights(self.lp, self.d, self.max_q, self.ws_link, stream=side)
+                self._link_ready = True
             self.q_join.record(side)
             self.prepare_weights(main)   # one launch here, so the second stream's chain is shorter
             if self.lag == 1 and self._pre == (mlo, mhi):

@@ -99,6 +99,17 @@ def test_null_and_size_checks_return_before_hip():
     # CSR build: bad sizes
     assert L.mtgnn_build_temporal_csr(p, p, p, -1, 10, p, p, p, p, p, 0, None) == -1
     assert L.mtgnn_build_temporal_csr(p, p, p, 10, 0, p, p, p, p, p, 0, None) == -1
+    # decoder weight copies: NULL params, a max_q that is not a multiple of 3, too small a workspace
+    lp = M.LinkParams(p, p, p, p)
+    assert L.mtgnn_link_prepare_weights(None, C.byref(d), 6, p, 1 << 30, None) == -1
+    assert L.mtgnn_link_prepare_weights(C.byref(lp), C.byref(d), 5, p, 1 << 30, None) == -1
+    assert L.mtgnn_link_prepare_weights(C.byref(lp), C.byref(d), 6, p, 16, None) == -3
+    # prepared loss: the second stream without its fork event (or the reverse) is rejected
+    lg = M.LinkGrads(p, p, p, p)
+    assert L.mtgnn_link_loss_prepared(p, p, 6, C.byref(lp), C.byref(d), p, p, p, C.byref(lg), p, 1 << 30, None, p,
+                                      None) == -1
+    assert L.mtgnn_link_loss_prepared(p, p, 6, C.byref(lp), C.byref(d), p, p, p, C.byref(lg), p, 1 << 30, None, None,
+                                      p) == -1
 
 
 def test_binding_refuses_host_tensors():

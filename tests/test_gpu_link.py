@@ -99,3 +99,47 @@ def test_link_loss_overlap_bitwise(cid, max_tar, n_tar):
         outs.append([loss, scores, dz] + [g[k] for k in sorted(g)])
     for a, b in zip(*outs):
         assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+@pytest.mark.parametrize("cid,max_tar,n_tar", [(3, 4_000, 3_517), (1, 200, 137)])
+def test_link_loss_prepared_bitwise(cid, max_tar, n_tar):
+    """mtgnn_link_loss_prepared after mtgnn_link_prepare_weights (on the same stream, and on another stream
+    ordered by an event, with the decoder's gradient on that stream too) against mtgnn_link_loss: every
+    output bit for bit.  The workspace is filled with NaN bytes first, so a copy the prepare call did not
+    make would show."""
+    w = workload(cid)
+    log(f"[link] prepared entry, workload {cid}: {n_tar} of {max_tar} target events")
+    params = init_params(w, random_bias=True)
+    rng = np.random.default_rng(cid + 7 * n_tar)
+    z = torch.from_numpy((rng.standard_normal((3 * max_tar, w.d_attn)) * 0.7).astype(np.float32)).cuda()
+    d = M.dims(w.n_nodes, w.d_mem, w.d_time, w.d_edge, w.d_attn, w.n_heads, w.k, M.F32)
+    p = {k: torch.from_numpy(params[k]).cuda() for k in ("W_d1", "b_d1", "W_d2", "b_d2")}
+    n_q = torch.tensor([3 * n_tar], dtype=torch.int32, device="cuda")
+    side, fork, filled, ready = torch.cuda.Stream(), M.DeviceEvent(), M.DeviceEvent(), M.DeviceEvent()
+    outs = []
+    for mode in ("plain", "prepared", "prepared_side"):
+        g = {k: torch.full_like(v, np.nan) for k, v in p.items()}
+        loss = torch.full((1,), np.nan, device="cuda")
+        scores = torch.full((2, max_tar), np.nan, device="cuda")
+        dz = torch.full((3 * max_tar, w.d_attn), np.nan, device="cuda")
+        ws = M.alloc_bytes(M.workspace_bytes(M.OP_LINK_LOSS, d, 0, 3 * max_tar))
+        ws.fill_(255)
+        lp, lg = M.link_params(p), M.link_grads(g)
+        if mode == "plain":
+            M.mtgnn_link_loss(z, n_q, 3 * max_tar, lp, d, loss, scores, dz, lg, ws)
+        elif mode == "prepared":
+            M.mtgnn_link_prepare_weights(lp, d, 3 * max_tar, ws)
+            M.mtgnn_link_loss(z, n_q, 3 * max_tar, lp, d, loss, scores, dz, lg, ws, prepared=True)
+        else:
+            filled.record()
+            filled.wait(side)
+            M.mtgnn_link_prepare_weights(lp, d, 3 * max_tar, ws, stream=side)
+            ready.record(side)
+            ready.wait()
+            M.mtgnn_link_loss(z, n_q, 3 * max_tar, lp, d, loss, scores, dz, lg, ws, dw_stream=side, fork=fork,
+                              prepared=True)
+        torch.cuda.synchronize()
+        outs.append([loss, scores, dz] + [g[k] for k in sorted(g)])
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert torch.equal(a.view(torch.int32), b.view(torch.int32))
