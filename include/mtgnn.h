@@ -401,6 +401,14 @@ mtgnn_status mtgnn_link_loss_overlap(const float* z, const int32_t* n_q, int64_t
 mtgnn_status mtgnn_link_prepare_weights(const mtgnn_link_params* params, const mtgnn_dims* dims, int64_t max_q,
                                         void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* mtgnn_temporal_attn_prepare_weights and mtgnn_link_prepare_weights (link, max_q, link_ws) in one
+ * call: for float32 weights of the fused merge and decoder widths, every copy of both is made by a
+ * single launch.  Arguments, results and errors as those two calls. */
+mtgnn_status mtgnn_temporal_attn_prepare_weights_link(const mtgnn_attn_params* params, const float* time_w,
+                                                      const float* time_b, const mtgnn_dims* dims, void* save,
+                                                      const mtgnn_link_params* link, int64_t max_q, void* link_ws,
+                                                      size_t link_ws_bytes, hipStream_t stream);
+
 /* mtgnn_link_loss (dw_stream and fork NULL) or mtgnn_link_loss_overlap (both given) with the decoder's
  * weight copies already in ws: a mtgnn_link_prepare_weights call with the same params->W_d1, dims,
  * max_q and ws, ordered before this call on `stream` (same stream, or an event the caller records

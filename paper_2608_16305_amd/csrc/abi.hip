@@ -551,6 +551,26 @@ mtgnn_status mtgnn_link_prepare_weights(const mtgnn_link_params* params, const m
   return link_prepare_impl(params, d, max_q, ws, stream);
 }
 
+mtgnn_status mtgnn_temporal_attn_prepare_weights_link(const mtgnn_attn_params* params, const float* time_w,
+                                                      const float* time_b, const mtgnn_dims* d, void* save,
+                                                      const mtgnn_link_params* link, int64_t max_q, void* link_ws,
+                                                      size_t link_ws_bytes, hipStream_t stream) {
+  MTGNN_TRY(check_dims(d));
+  MTGNN_TRY(check_attn_params(params));
+  REQ(save, "save");
+  if (d->d_time > 0 && (!time_w || !time_b)) return fail(MTGNN_EINVAL, "time arrays");
+  if (max_q < 0 || max_q >= (int64_t(1) << 31) - 1) return fail(MTGNN_EINVAL, "max_q");
+  if (max_q % 3 != 0) return fail(MTGNN_EINVAL, "max_q is not a multiple of 3 (src, dst and negative blocks)");
+  if (d->d_attn > 128) return fail(MTGNN_EUNSUPPORTED, "link weights: d_attn > 128");
+  REQ(link, "link");
+  REQ(link->W_d1, "W_d1");
+  if (link_ws_bytes < link_loss_ws(d, max_q)) return fail(MTGNN_EWORKSPACE, "link ws");
+  REQ(link_ws, "link_ws");
+  PadCopy c[4];
+  const int n = link_copies_impl(link, d, max_q, link_ws, c);
+  return attn_prepare_weights_impl(params, time_w, time_b, d, save, stream, c, n);
+}
+
 mtgnn_status mtgnn_link_loss_prepared(const float* z, const int32_t* n_q, int64_t max_q,
                                       const mtgnn_link_params* params, const mtgnn_dims* d, float* loss,
                                       float* scores, float* dz, mtgnn_link_grads* grads, void* ws, size_t ws_bytes,

@@ -1369,11 +1369,13 @@ size_t attn_save_bytes(const mtgnn_dims* d, int64_t max_q) { return carve_save(n
 size_t attn_fwd_ws(const mtgnn_dims*, int64_t max_q) { return scan_ws_bytes(max_q); }
 
 mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const float* tw, const float* tb,
-                                       const mtgnn_dims* d, void* save, hipStream_t s) {
+                                       const mtgnn_dims* d, void* save, hipStream_t s, const PadCopy* more,
+                                       int n_more) {
+  if (n_more < 0 || n_more > 4) return MTGNN_EINVAL;
   const AttnShape sh(d, 0);
   const AttnSave sv = carve_save(save, sh);
   if (merge_fused_ok(d->dtype, sh.da, sh.dm)) {   // float32: one launch for every copy
-    PadCopy ex[8] = {plain_copy((const float*)p->W_k, (float*)sv.W_kv, sh.da, (int)sh.Dkv),
+    PadCopy ex[12] = {plain_copy((const float*)p->W_k, (float*)sv.W_kv, sh.da, (int)sh.Dkv),
                      plain_copy((const float*)p->W_v, (float*)sv.W_kv + (size_t)sh.da * sh.Dkv, sh.da, (int)sh.Dkv),
                      plain_copy(p->b_k, sv.b_kv, 1, sh.da), plain_copy(p->b_v, sv.b_kv + sh.da, 1, sh.da)};
     int n_ex = 4;
@@ -1385,6 +1387,7 @@ mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const float* 
         ex[n_ex++] = dmem_copy((const float*)p->W_k, (const float*)p->W_v, sh.da, sh.dm, sh.dt, (int)sh.Dkv,
                                sv.merge_w, which);
     }
+    for (int i = 0; i < n_more; ++i) ex[n_ex++] = more[i];
     const QConst qc{(const float*)p->W_q, p->b_q, tw, tb, sv.qc, sh.da, sh.dm, sh.dt};
     return merge_prepare((const float*)p->W_o, (const float*)p->W_1, (const float*)p->W_2, sh.da, sh.dm, sv.merge_w,
                          s, ex, n_ex, qf ? &qc : nullptr);
@@ -1398,7 +1401,7 @@ mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const float* 
                                                                   p->b_k, p->b_v, sh.da, sh.Dkv,
                                                                   (uint16_t*)sv.W_kv, sv.b_kv);
   MTGNN_CHECK_LAUNCH("stack_kv");
-  return MTGNN_OK;
+  return pad_copies(more, n_more, s);
 }
 
 mtgnn_status attn_prepare_slots_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_dims* d,

@@ -141,12 +141,18 @@ size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q) {
   return total;
 }
 
+int link_copies_impl(const mtgnn_link_params* p, const mtgnn_dims* d, int64_t max_q, void* ws, PadCopy* out) {
+  const int da = d->d_attn;
+  if (!link_fused_ok(da)) return 0;   // the general widths read W_d1 directly
+  const LinkWs L = link_ws_layout(ws, da, max_q);
+  return link_pad_copies(p->W_d1, da, L.Wp, out);
+}
+
 mtgnn_status link_prepare_impl(const mtgnn_link_params* p, const mtgnn_dims* d, int64_t max_q, void* ws,
                                hipStream_t s) {
-  const int da = d->d_attn;
-  if (!link_fused_ok(da)) return MTGNN_OK;   // the general widths read W_d1 directly
-  const LinkWs L = link_ws_layout(ws, da, max_q);
-  return link_prepare_weights(p->W_d1, da, L.Wp, s);
+  PadCopy c[4];
+  const int n = link_copies_impl(p, d, max_q, ws, c);
+  return pad_copies(c, n, s);
 }
 
 mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, const mtgnn_link_params* p,

@@ -244,7 +244,7 @@ __global__ __launch_bounds__(64 * MW) void k_merge_bwd(const float* __restrict__
 
 // Zero-padded copies of the merge weights: dst[r][c] = W[r][c] (or W[c][r] for a transposed copy) for r < n,
 // c < k, else 0.  blockIdx.y selects the copy.
-constexpr int PREP_MAX = 14;   // the six merge copies and up to eight extra copies
+constexpr int PREP_MAX = 18;   // the six merge copies and up to twelve extra copies
 struct PrepArgs {
   const float* src[PREP_MAX];
   float* dst[PREP_MAX];
@@ -990,28 +990,44 @@ size_t link_fused_weight_floats(int da) {
   return (size_t)4 * 16 * MW * cdiv(na, MW) * 16 * na;
 }
 
-mtgnn_status link_prepare_weights(const float* W1, int da, float* Wp, hipStream_t s) {
-  if (!link_fused_ok(da) || !aligned16(Wp)) return MTGNN_EUNSUPPORTED;
+int link_pad_copies(const float* W1, int da, float* Wp, PadCopy* out) {
+  if (!link_fused_ok(da) || !aligned16(Wp)) return 0;
   const int na = (int)cdiv(da, 16);
   const int rows = 16 * MW * (int)cdiv(na, MW), cols = 16 * na;
   const size_t wsz = (size_t)rows * cols;
   // zero-padded W_a, W_b (the column halves of W_d1) and their transposes
+  for (int m = 0; m < 4; ++m)
+    out[m] = PadCopy{W1 + (m % 2 ? da : 0), Wp + m * wsz, rows, cols, da, da, 2 * da, m >= 2 ? 1 : 0, cols};
+  return 4;
+}
+
+mtgnn_status pad_copies(const PadCopy* c, int n, hipStream_t s) {
+  if (n < 0 || n > PREP_MAX) return MTGNN_EINVAL;
+  if (n == 0) return MTGNN_OK;
   PrepArgs a;
-  for (int m = 0; m < 4; ++m) {
-    a.src[m] = W1 + (m % 2 ? da : 0);
-    a.dst[m] = Wp + m * wsz;
-    a.rows[m] = rows;
-    a.cols[m] = cols;
-    a.n[m] = da;
-    a.k[m] = da;
-    a.ld[m] = 2 * da;
-    a.tr[m] = m >= 2 ? 1 : 0;
-    a.ldd[m] = cols;
+  int64_t most = 0;
+  for (int m = 0; m < n; ++m) {
+    a.src[m] = c[m].src;
+    a.dst[m] = c[m].dst;
+    a.rows[m] = c[m].rows;
+    a.cols[m] = c[m].cols;
+    a.n[m] = c[m].n;
+    a.k[m] = c[m].k;
+    a.ld[m] = c[m].ld;
+    a.tr[m] = c[m].tr;
+    a.ldd[m] = c[m].ldd > 0 ? c[m].ldd : c[m].cols;
+    most = std::max<int64_t>(most, (int64_t)c[m].rows * c[m].cols);
   }
-  a.ncopy = 4;
-  k_merge_prepare<<<dim3((unsigned)cdiv(wsz, 256), 4u), 256, 0, s>>>(a);
-  MTGNN_CHECK_LAUNCH("link_prepare");
+  a.ncopy = n;
+  k_merge_prepare<<<dim3((unsigned)cdiv(most, 256), (unsigned)n), 256, 0, s>>>(a);
+  MTGNN_CHECK_LAUNCH("pad_copies");
   return MTGNN_OK;
+}
+
+mtgnn_status link_prepare_weights(const float* W1, int da, float* Wp, hipStream_t s) {
+  PadCopy c[4];
+  if (link_pad_copies(W1, da, Wp, c) != 4) return MTGNN_EUNSUPPORTED;
+  return pad_copies(c, 4, s);
 }
 
 mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,

@@ -81,8 +81,7 @@ size_t link_fused_weight_floats(int da);
 mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
                         const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
                         float* scores, float* dW2, float* db2, float* loss, hipStream_t s, bool prepared = false);
-// The zero-padded copies of W_d1's two column halves and their transposes that link_fused reads from Wp.
-mtgnn_status link_prepare_weights(const float* W1, int da, float* Wp, hipStream_t s);
+
 size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q);
 // s_dw, fork: a second stream and an event (or NULL, NULL): W_d1's gradient is then enqueued on s_dw after
 // fork, recorded on s once dz and the decoder's row gradients are written (fused widths only).
@@ -91,9 +90,7 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
                             const mtgnn_dims* d, float* loss, float* scores, float* dz, mtgnn_link_grads* g, void* ws,
                             size_t ws_bytes, hipStream_t s, hipStream_t s_dw = nullptr, hipEvent_t fork = nullptr,
                             bool prepared = false);
-// The fused decoder's weight copies in the link workspace (nothing at the general widths).
-mtgnn_status link_prepare_impl(const mtgnn_link_params* p, const mtgnn_dims* d, int64_t max_q, void* ws,
-                               hipStream_t s);
+
 
 // offline dependency scan (Algorithm 1) and the mixed batches of one worker
 mtgnn_status dep_scan_impl(const int32_t* src, const int32_t* dst, int64_t E, const int32_t* owner, int64_t n_nodes,
@@ -158,6 +155,18 @@ struct PadCopy {
 inline PadCopy plain_copy(const float* src, float* dst, int rows, int cols) {
   return PadCopy{src, dst, rows, cols, rows, cols, cols, 0, 0};
 }
+// The four copies of link_prepare_weights as descriptors (4 written to out), or 0 at widths the fused
+// decoder does not take.
+int link_pad_copies(const float* W1, int da, float* Wp, PadCopy* out);
+// Zero-padded copies in one launch (n <= 18).
+mtgnn_status pad_copies(const PadCopy* c, int n, hipStream_t s);
+// The fused decoder's weight copies in the link workspace (nothing at the general widths): as
+// descriptors (returns how many, 0 or 4), or made on s.
+int link_copies_impl(const mtgnn_link_params* p, const mtgnn_dims* d, int64_t max_q, void* ws, PadCopy* out);
+mtgnn_status link_prepare_impl(const mtgnn_link_params* p, const mtgnn_dims* d, int64_t max_q, void* ws,
+                               hipStream_t s);
+// The zero-padded copies of W_d1's two column halves and their transposes that link_fused reads from Wp.
+mtgnn_status link_prepare_weights(const float* W1, int da, float* Wp, hipStream_t s);
 // The query projection's constant: out[j] = bq[j] + sum_t Wq[j][dm + t] cos(w_t 0 + b_t) (a query's
 // time input is phi(0)); Wq row stride dm + dt.
 struct QConst {
@@ -205,8 +214,10 @@ mtgnn_status attn_fwd_impl(const int32_t* q_node, const float* q_t, const int32_
                            const mtgnn_dims* d, float* z, void* save, void* ws, size_t ws_bytes, hipStream_t s);
 // The forward's inputs that need only the sampled neighbours and the weights (stacked key/value
 // weights, padded merge weights, per-query valid-slot counts and offsets), then the rest.
+// more, n_more: up to 4 further zero-padded copies, made in the same launch on the float32 fused path.
 mtgnn_status attn_prepare_weights_impl(const mtgnn_attn_params* p, const float* tw, const float* tb,
-                                       const mtgnn_dims* d, void* save, hipStream_t s);
+                                       const mtgnn_dims* d, void* save, hipStream_t s,
+                                       const PadCopy* more = nullptr, int n_more = 0);
 mtgnn_status attn_prepare_slots_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_dims* d,
                                      void* save, void* ws, size_t ws_bytes, hipStream_t s);
 mtgnn_status attn_prepare_impl(const int32_t* nbr, const int32_t* n_q, int64_t max_q, const mtgnn_attn_params* p,

@@ -22,6 +22,7 @@ OP_LINK_LOSS, OP_MIXED_BATCHES, OP_RNN_UPDATE, OP_RNN_UPDATE_BWD, OP_TIME_PROJEC
 ENTRY_POINTS = (
     "mtgnn_build_queries", "mtgnn_aggregate_last", "mtgnn_build_messages", "mtgnn_gru_update",
     "mtgnn_sample_recent", "mtgnn_temporal_attn", "mtgnn_temporal_attn_prepare", "mtgnn_temporal_attn_prepare_weights",
+    "mtgnn_temporal_attn_prepare_weights_link",
     "mtgnn_temporal_attn_prepare_slots", "mtgnn_temporal_attn_prepared",
     "mtgnn_temporal_attn_bwd", "mtgnn_temporal_attn_bwd_overlap", "mtgnn_temporal_attn_bwd_group",
     "mtgnn_temporal_attn_bwd_grouped",
@@ -97,6 +98,8 @@ _SIGS = {
                             _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_prepare": [_P, _P, _I64, C.POINTER(AttnParams), _P, _P, C.POINTER(Dims), _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_prepare_weights": [C.POINTER(AttnParams), _P, _P, C.POINTER(Dims), _P, _P],
+    "mtgnn_temporal_attn_prepare_weights_link": [C.POINTER(AttnParams), _P, _P, C.POINTER(Dims), _P,
+                                                 C.POINTER(LinkParams), _I64, _P, _SZ, _P],
     "mtgnn_temporal_attn_prepare_slots": [_P, _P, _I64, C.POINTER(Dims), _P, _P, _SZ, _P],
     "mtgnn_temporal_attn_prepared": [_P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _P, C.POINTER(AttnParams),
                                      C.POINTER(Dims), _P, _P, _P],
@@ -313,6 +316,16 @@ def mtgnn_temporal_attn_prepare_weights(params: AttnParams, time_w, time_b, d: D
                                                      _ptr(time_b, torch.float32, "time_b"), C.byref(d),
                                                      _ptr(save, torch.uint8, "save"), _stream(stream)),
            "mtgnn_temporal_attn_prepare_weights")
+
+
+def mtgnn_temporal_attn_prepare_weights_link(params: AttnParams, time_w, time_b, d: Dims, save, link: LinkParams,
+                                             max_q, link_ws, stream=None):
+    wp, wb = _ws(link_ws)
+    _check(lib().mtgnn_temporal_attn_prepare_weights_link(C.byref(params), _ptr(time_w, torch.float32, "time_w"),
+                                                          _ptr(time_b, torch.float32, "time_b"), C.byref(d),
+                                                          _ptr(save, torch.uint8, "save"), C.byref(link), int(max_q),
+                                                          wp, wb, _stream(stream)),
+           "mtgnn_temporal_attn_prepare_weights_link")
 
 
 def mtgnn_temporal_attn_prepare_slots(nbr, n_q, max_q, d: Dims, save, ws=None, stream=None):

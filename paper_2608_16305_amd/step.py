@@ -138,7 +138,7 @@ class TGNStep:
         self.m_done, self.pre_join = M.DeviceEvent(), M.DeviceEvent()
         self.group_ahead = True   # step(): the backward's d_mem grouping during the embedding (second stream)
         self._grouped = False     # ... and it has been enqueued
-        self._link_ready = False  # step(): the decoder's weight copies made on the second stream for its loss
+        self._link_ready = False  # step(): the decoder's weight copies made for its loss
 
     def _batch(self, lo, hi):
         if hi <= lo:
@@ -191,11 +191,18 @@ class TGNStep:
         M.mtgnn_temporal_attn_prepare_slots(self.nbr, self.n_q, self.max_q, self.d, self.attn_save, self.ws_q,
                                             stream=stream)
 
-    def prepare_weights(self, stream):
-        """The attention's weight copies (stacked K|V, padded merge layers): they read only the weights."""
+    def prepare_weights(self, stream, link=False):
+        """The attention's weight copies (stacked K|V, padded merge layers): they read only the weights.
+        link: with the decoder's (same launch), for this step's link loss."""
         self._q_chain = self._q_chain if self._in_step else 0
         p = self.params
-        M.mtgnn_temporal_attn_prepare_weights(self.ap, p["time_w"], p["time_b"], self.d, self.attn_save, stream=stream)
+        if link:
+            M.mtgnn_temporal_attn_prepare_weights_link(self.ap, p["time_w"], p["time_b"], self.d, self.attn_save,
+                                                       self.lp, self.max_q, self.ws_link, stream=stream)
+            self._link_ready = True
+        else:
+            M.mtgnn_temporal_attn_prepare_weights(self.ap, p["time_w"], p["time_b"], self.d, self.attn_save,
+                                                  stream=stream)
 
     def embed(self, lo, hi, queries_done=False):
         self._q_chain = self._q_chain if self._in_step else 0
@@ -212,8 +219,7 @@ class TGNStep:
         decoder's first-layer weight gradient runs on the second stream (idle between the embedding and
         the backward's d_mem sums), ahead of the d_mem work there, so the backward's join covers it."""
         if self.overlap:
-            # prepared: the step made the decoder's weight copies on the second stream before the join
-            # that precedes the embedding
+            # prepared: the step made the decoder's weight copies with the attention's, on this stream
             M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz,
                               self.lg, self.ws_link, stream=self.ts, dw_stream=self.side_stream, fork=self.l_fork,
                               prepared=self._link_ready)
@@ -287,13 +293,10 @@ class TGNStep:
                 self.q_fork.record(main)
                 self.q_fork.wait(side)
             self.queries(elo, ehi, side)
-            if dz is None and self.has_link:
-                # the decoder's weight copies, here rather than at the loss on the main stream: this stream
-                # is done with its queries well before the main stream waits for them
-                M.mtgnn_link_prepare_weights(self.lp, self.d, self.max_q, self.ws_link, stream=side)
-                self._link_ready = True
             self.q_join.record(side)
-            self.prepare_weights(main)   # one launch here, so the second stream's chain is shorter
+            # one launch here, so the second stream's chain is shorter; after any parameter update the
+            # caller made on this stream, and with the decoder's weight copies when the loss runs
+            self.prepare_weights(main, link=dz is None and self.has_link)
             if self.lag == 1 and self._pre == (mlo, mhi):
                 # this memory batch's aggregation and messages were built during the previous step's
                 # embedding, from the memory as it is now: only the GRU update is left

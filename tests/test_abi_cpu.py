@@ -104,6 +104,11 @@ def test_null_and_size_checks_return_before_hip():
     assert L.mtgnn_link_prepare_weights(None, C.byref(d), 6, p, 1 << 30, None) == -1
     assert L.mtgnn_link_prepare_weights(C.byref(lp), C.byref(d), 5, p, 1 << 30, None) == -1
     assert L.mtgnn_link_prepare_weights(C.byref(lp), C.byref(d), 6, p, 16, None) == -3
+    # the attention's and the decoder's copies in one call: NULL decoder parameters, a bad max_q
+    assert L.mtgnn_temporal_attn_prepare_weights_link(C.byref(ap), p, p, C.byref(d), p, None, 6, p, 1 << 30,
+                                                      None) == -1
+    assert L.mtgnn_temporal_attn_prepare_weights_link(C.byref(ap), p, p, C.byref(d), p, C.byref(lp), 7, p, 1 << 30,
+                                                      None) == -1
     # prepared loss: the second stream without its fork event (or the reverse) is rejected
     lg = M.LinkGrads(p, p, p, p)
     assert L.mtgnn_link_loss_prepared(p, p, 6, C.byref(lp), C.byref(d), p, p, p, C.byref(lg), p, 1 << 30, None, p,
