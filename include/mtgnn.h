@@ -372,16 +372,16 @@ mtgnn_status mtgnn_link_loss(const float* z, const int32_t* n_q, int64_t max_q, 
                              const mtgnn_dims* dims, float* loss, float* scores, float* dz, mtgnn_link_grads* grads,
                              void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* The masked batch loss with the decoder's first-layer weight gradient on a second stream: the same
- * computation, arguments and results as mtgnn_link_loss (bitwise), except that once loss, scores, dz
- * and the second layer's gradients are enqueued on `stream`, the call records `fork` on `stream`, makes
- * dw_stream wait for it and enqueues grads->W_d1 and grads->b_d1 on dw_stream (for the widths the fused
- * decoder kernel takes: d_attn a multiple of 4 in 17..32 or 97..112; at other widths everything runs on
- * `stream` and nothing is recorded).  Work enqueued on
- * `stream` afterwards (the attention backward, which needs only dz) overlaps it.  The first-layer
- * gradients are complete when the work this call enqueued on dw_stream is; until then the caller
- * writes neither z nor ws and reads neither grads->W_d1 nor grads->b_d1 (an event recorded on dw_stream
- * after this call, or later work on dw_stream, orders that).
+/* The masked batch loss with its last reductions and the decoder's first-layer weight gradient on a
+ * second stream: the same computation, arguments and results as mtgnn_link_loss (bitwise), except that
+ * once scores, dz and the per-block partial sums are enqueued on `stream`, the call records `fork` on
+ * `stream`, makes dw_stream wait for it and enqueues the loss, grads->W_d2, grads->b_d2, grads->W_d1 and
+ * grads->b_d1 on dw_stream (for the widths the fused decoder kernel takes: d_attn a multiple of 4 in
+ * 17..32 or 97..112; at other widths everything runs on `stream` and nothing is recorded).  Work
+ * enqueued on `stream` afterwards (the attention backward, which needs only dz) overlaps it.  The loss
+ * and the decoder's gradients are complete when the work this call enqueued on dw_stream is; until
+ * then the caller writes neither z nor ws and reads neither the loss nor those gradients (an event
+ * recorded on dw_stream after this call, or later work on dw_stream, orders that).
  *   dw_stream -- a second stream of the caller, at the default priority;
  *   fork      -- an event of the caller (timing may be disabled).
  * Errors: as mtgnn_link_loss; EINVAL if dw_stream or fork is NULL; EHIP if the fork cannot be recorded

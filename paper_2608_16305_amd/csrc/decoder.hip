@@ -165,8 +165,9 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
   LinkWs L = link_ws_layout(ws, da, max_q);
   if (link_fused_ok(da)) {
     MTGNN_TRY(link_fused(z, n_q, max_q, da, p->W_d1, p->b_d1, p->W_d2, p->b_d2, L.Wp, L.DA, L.DB, L.part, dz, scores,
-                         g->W_d2, g->b_d2, loss, s, prepared));
-    // W_d1's gradient needs only DA, DB and z: on the second stream if there is one
+                         g->W_d2, g->b_d2, loss, s, prepared, s_dw != nullptr));
+    // the partials' sums (loss, W_d2's gradient) and W_d1's gradient need only the fused kernel's outputs and
+    // z: on the second stream if there is one
     if (s_dw) {
       hipError_t e = hipEventRecord(fork, s);
       if (e == hipSuccess) e = hipStreamWaitEvent(s_dw, fork, 0);
@@ -174,6 +175,7 @@ mtgnn_status link_loss_impl(const float* z, const int32_t* n_q, int64_t max_q, c
         set_hip_error(e, "link_loss fork");
         return MTGNN_EHIP;
       }
+      MTGNN_TRY(link_reduce(L.part, n_q, max_q, da, g->W_d2, g->b_d2, loss, s_dw));
     }
     // DA is zero past the src block (the first third of the query rows), DB on it
     const DwProblem dp[2] = {{L.DA, da, z, da, g->W_d1, 2 * da, da, da, g->b_d1, 0, 1, 3},

@@ -1032,7 +1032,8 @@ mtgnn_status link_prepare_weights(const float* W1, int da, float* Wp, hipStream_
 
 mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
                         const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
-                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s, bool prepared) {
+                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s, bool prepared,
+                        bool s_reduce) {
   if (!link_fused_ok(da) || !aligned16(z) || !aligned16(Wp) || !aligned16(dz)) return MTGNN_EUNSUPPORTED;
   if (!prepared) MTGNN_TRY(link_prepare_weights(W1, da, Wp, s));
   const int na = (int)cdiv(da, 16);
@@ -1048,8 +1049,13 @@ mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int d
                                                           part);
     MTGNN_CHECK_LAUNCH("link_fused");
   }
+  return s_reduce ? MTGNN_OK : link_reduce(part, n_q, max_q, da, dW2, db2, loss, s);
+}
+
+mtgnn_status link_reduce(const float* part, const int32_t* n_q, int64_t max_q, int da, float* dW2, float* db2,
+                         float* loss, hipStream_t s) {
   // blocks past the device's target count wrote no partial: sum only those below it
-  k_link_reduce_dev<<<(unsigned)cdiv(da + 2, 4), 256, 0, s>>>(part, n_q, max_tar, da, dW2, db2, loss);
+  k_link_reduce_dev<<<(unsigned)cdiv(da + 2, 4), 256, 0, s>>>(part, n_q, max_q / 3, da, dW2, db2, loss);
   MTGNN_CHECK_LAUNCH("link_reduce");
   return MTGNN_OK;
 }

@@ -78,9 +78,14 @@ mtgnn_status gru_fused(const float* msg, const float* W_ih, const float* W_hh, c
 bool link_fused_ok(int da);
 size_t link_fused_weight_floats(int da);
 // prepared: Wp already holds link_prepare_weights' copies of this W1 (else they are made first).
+// s_reduce: the caller launches link_reduce itself (on another stream ordered after this call's work).
 mtgnn_status link_fused(const float* z, const int32_t* n_q, int64_t max_q, int da, const float* W1, const float* b1,
                         const float* W2, const float* b2, float* Wp, float* DA, float* DB, float* part, float* dz,
-                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s, bool prepared = false);
+                        float* scores, float* dW2, float* db2, float* loss, hipStream_t s, bool prepared = false,
+                        bool s_reduce = false);
+// The fixed-order sums of link_fused's per-block partials into dW_d2, db_d2 and the loss.
+mtgnn_status link_reduce(const float* part, const int32_t* n_q, int64_t max_q, int da, float* dW2, float* db2,
+                         float* loss, hipStream_t s);
 
 size_t link_loss_ws(const mtgnn_dims* d, int64_t max_q);
 // s_dw, fork: a second stream and an event (or NULL, NULL): W_d1's gradient is then enqueued on s_dw after
