@@ -211,6 +211,46 @@ def test_backward_overlap_bitwise(case):
             assert a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
 
 
+def test_param_update_between_steps_bitwise():
+    """Parameters updated in place on the caller's stream between steps (as an optimizer does): the
+    two-stream step gives bitwise the results of the single-stream step, so nothing the second stream
+    runs reads a parameter before the update.  The caller's stream sleeps before each update, so that
+    the second stream, which goes on to the next step's queries meanwhile, would read the old values
+    if it read any (bipartite stream, 3 steps)."""
+    from paper_2608_16305_amd.step import TGNStep
+    w = workload(2)
+    log("[parity] parameter update between steps, overlap vs single stream")
+    s = make_stream(w)
+    params = init_params(w, random_bias=True)
+    mem, lu = random_state(w, seed=5)
+    outs = []
+    for overlap in (False, True):
+        r = TGNStep(w, s, params, mem, lu, overlap=overlap)
+        snaps = {}
+        for b in range(1, 4):
+            r.step(b)
+            # copies on the caller's stream (ordered after the step's join); no host wait until the end,
+            # so the next step is enqueued while this stream still sleeps
+            snaps[f"loss{b}"] = r.loss.clone()
+            snaps[f"z{b}"] = r.z.clone()
+            snaps.update({f"{k}{b}": v.clone() for k, v in r.grads.items()})
+            torch.cuda._sleep(20_000_000)   # the update below waits behind it
+            for v in r.params.values():
+                if v.dtype == torch.float32:
+                    v.mul_(1.0 + 1.0 / 64)
+            r.params_changed()
+        torch.cuda.synchronize()
+        res = {k: to_np(v).copy() for k, v in snaps.items()}
+        res["memory"] = to_np(r.memory).copy()
+        outs.append(res)
+        del r
+        torch.cuda.empty_cache()
+    assert outs[0].keys() == outs[1].keys()
+    for k in outs[0]:
+        a, b = outs[0][k], outs[1][k]
+        assert a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
+
+
 def test_forward_single_call_matches_prepare_prepared():
     """mtgnn_temporal_attn in one call gives bitwise the z and the save buffer of
     mtgnn_temporal_attn_prepare followed by mtgnn_temporal_attn_prepared, and of the preparation's
