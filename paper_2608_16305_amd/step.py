@@ -216,8 +216,9 @@ class TGNStep:
 
     def link_loss(self):
         """The masked loss of the embedded batch (Eq. 13) and dZ, on the main stream; with overlap, the
-        decoder's first-layer weight gradient runs on the second stream (idle between the embedding and
-        the backward's d_mem sums), ahead of the d_mem work there, so the backward's join covers it."""
+        loss value, the second layer's gradient sums and the first layer's weight gradient run on the second
+        stream (idle between the embedding and the backward's d_mem sums), ahead of the d_mem work there,
+        so the backward's join covers them."""
         if self.overlap:
             # prepared: the step made the decoder's weight copies with the attention's, on this stream
             M.mtgnn_link_loss(self.z, self.n_q, self.max_q, self.lp, self.d, self.loss, self.scores, self.dz,
